@@ -1,0 +1,156 @@
+"""Gaussian-process surrogate, fp64 (test infrastructure, not the product path).
+
+Paper: "Overall MOBO workflow" step (i) fits one GP per objective
+(``SingleTaskGP`` models combined by ``ModelListGP``, implementation section),
+with an ARD Matern kernel of smoothness 5/2 wrapped in a scale kernel, in
+double precision. Hyperparameters are given here, not learned.
+
+Readings of points the paper does not state:
+
+* Matern-5/2 is the standard form k(rho) = s (1 + sqrt5 rho + 5/3 rho^2)
+  exp(-sqrt5 rho) with rho the lengthscale-scaled Euclidean distance
+  (Rasmussen & Williams 2006, Section 4.2), s the output scale.
+* Observation noise is homoscedastic Gaussian with variance eta added to the
+  diagonal of the training covariance.
+* The posterior is that of the latent function (no noise added to the
+  predictive variance); variance is clamped at 0.
+* The q x q batch covariance is factorised without jitter; a Schur pivot
+  <= 1e-10 * s zeroes that column of the factor.
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass, field
+from typing import List
+
+import numpy as np
+from scipy.linalg import solve_triangular
+
+SQRT5 = math.sqrt(5.0)
+PIVOT_RTOL = 1e-10
+
+
+class NotPositiveDefinite(ValueError):
+    """The training covariance matrix of some objective is not PD."""
+
+
+def scaled_distance(U: np.ndarray, V: np.ndarray, ls: np.ndarray) -> np.ndarray:
+    """rho[i, j] = sqrt(sum_t ((U[i,t] - V[j,t]) / ls[t])^2), direct differences."""
+    U = np.asarray(U, dtype=np.float64)
+    V = np.asarray(V, dtype=np.float64)
+    ls = np.asarray(ls, dtype=np.float64)
+    D = (U[:, None, :] - V[None, :, :]) / ls
+    return np.sqrt(np.einsum("ijt,ijt->ij", D, D))
+
+
+def matern52(rho: np.ndarray, s: float) -> np.ndarray:
+    """Matern nu=5/2 covariance of scaled distance ``rho`` with output scale s."""
+    rho = np.asarray(rho, dtype=np.float64)
+    return float(s) * (1.0 + SQRT5 * rho + (5.0 / 3.0) * rho * rho) * np.exp(-SQRT5 * rho)
+
+
+@dataclass
+class GPModel:
+    X: np.ndarray            # [n, d]
+    Y: np.ndarray            # [n, m]
+    ls: np.ndarray           # [m, d]
+    s: np.ndarray            # [m]
+    eta: np.ndarray          # [m]
+    L: List[np.ndarray] = field(default_factory=list)      # m x [n, n] lower
+    alpha: List[np.ndarray] = field(default_factory=list)  # m x [n]
+
+    @property
+    def n(self) -> int:
+        return self.X.shape[0]
+
+    @property
+    def m(self) -> int:
+        return self.Y.shape[1]
+
+
+def fit(X, Y, ls, s, eta) -> GPModel:
+    """Condition one GP per objective on (X, Y[:, k]).
+
+    K_k = [k_k(x_i, x_j)] + eta_k I;  L_k = chol(K_k) (lower);
+    alpha_k = L_k^T \\ (L_k \\ y_k).
+    Raises NotPositiveDefinite when a factorisation fails.
+    """
+    X = np.asarray(X, dtype=np.float64)
+    Y = np.asarray(Y, dtype=np.float64)
+    ls = np.asarray(ls, dtype=np.float64).reshape(Y.shape[1], X.shape[1])
+    s = np.asarray(s, dtype=np.float64).reshape(-1)
+    eta = np.asarray(eta, dtype=np.float64).reshape(-1)
+    model = GPModel(X=X, Y=Y, ls=ls, s=s, eta=eta)
+    n = X.shape[0]
+    for k in range(Y.shape[1]):
+        K = matern52(scaled_distance(X, X, ls[k]), s[k]) + eta[k] * np.eye(n)
+        try:
+            L = np.linalg.cholesky(K)
+        except np.linalg.LinAlgError as e:  # pragma: no cover - message path
+            raise NotPositiveDefinite(f"objective {k}: {e}") from e
+        if not np.all(np.isfinite(L)):
+            raise NotPositiveDefinite(f"objective {k}: non-finite factor")
+        w = solve_triangular(L, Y[:, k], lower=True)
+        alpha = solve_triangular(L.T, w, lower=False)
+        model.L.append(L)
+        model.alpha.append(alpha)
+    return model
+
+
+def posterior(model: GPModel, cand: np.ndarray, chunk: int = 512):
+    """Posterior of every objective at a set of q-batches.
+
+    cand: [B, q, d]. Returns (mu [B, q, m], cov [B, m, q, q]).
+    For each point x*: k* = k(x*, X), mu = k*^T alpha, v = L \\ k* (forward
+    substitution), and for a batch Sigma[a, b] = k(x*_a, x*_b) - v_a^T v_b.
+    The diagonal is clamped at 0 (variance of the latent function).
+    """
+    cand = np.asarray(cand, dtype=np.float64)
+    B, q, d = cand.shape
+    m = model.m
+    mu = np.zeros((B, q, m))
+    cov = np.zeros((B, m, q, q))
+    for b0 in range(0, B, chunk):
+        b1 = min(B, b0 + chunk)
+        P = cand[b0:b1].reshape(-1, d)
+        nb = b1 - b0
+        for k in range(m):
+            Ks = matern52(scaled_distance(P, model.X, model.ls[k]), model.s[k])
+            mu[b0:b1, :, k] = (Ks @ model.alpha[k]).reshape(nb, q)
+            V = solve_triangular(model.L[k], Ks.T, lower=True)   # [n, nb*q]
+            Vb = V.T.reshape(nb, q, -1)
+            Pb = cand[b0:b1]
+            prior = np.empty((nb, q, q))
+            for a in range(q):
+                for c in range(q):
+                    diff = (Pb[:, a, :] - Pb[:, c, :]) / model.ls[k]
+                    rho = np.sqrt(np.sum(diff * diff, axis=1))
+                    prior[:, a, c] = matern52(rho, model.s[k])
+            S = prior - Vb @ np.transpose(Vb, (0, 2, 1))
+            idx = np.arange(q)
+            S[:, idx, idx] = np.maximum(S[:, idx, idx], 0.0)
+            cov[b0:b1, k] = S
+    return mu, cov
+
+
+def chol_psd(Sig: np.ndarray, s) -> np.ndarray:
+    """Lower Cholesky factor of a batch of PSD q x q matrices, no jitter.
+
+    Sig: [..., q, q]; s: output scale (broadcast over the leading axes).
+    Column j is computed from the Schur pivot p = Sig[j,j] - sum_{t<j} C[j,t]^2;
+    if p <= 1e-10 * s the whole column j of C is zero, otherwise
+    C[j,j] = sqrt(p) and C[i,j] = (Sig[i,j] - sum_{t<j} C[i,t] C[j,t]) / C[j,j].
+    """
+    Sig = np.asarray(Sig, dtype=np.float64)
+    q = Sig.shape[-1]
+    s = np.broadcast_to(np.asarray(s, dtype=np.float64), Sig.shape[:-2])
+    C = np.zeros_like(Sig)
+    for j in range(q):
+        p = Sig[..., j, j] - np.sum(C[..., j, :j] ** 2, axis=-1)
+        ok = p > PIVOT_RTOL * s
+        cjj = np.where(ok, np.sqrt(np.where(ok, p, 1.0)), 0.0)
+        C[..., j, j] = cjj
+        for i in range(j + 1, q):
+            num = Sig[..., i, j] - np.sum(C[..., i, :j] * C[..., j, :j], axis=-1)
+            C[..., i, j] = np.where(ok, num / np.where(ok, cjj, 1.0), 0.0)
+    return C
