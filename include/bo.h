@@ -1,0 +1,219 @@
+/*
+ * bo.h — C ABI of the batch acquisition scorer (MI355X / gfx950).
+ *
+ * Scores a large batch of encoded candidate configurations for one iteration
+ * of multi-objective Bayesian optimisation, as in the online phase of BOute
+ * (Jiang, Fu, Yoneki — "BOute: Cost-Efficient LLM Serving with Heterogeneous
+ * LLMs and GPUs via Multi-Objective Bayesian Optimization"):
+ *
+ *   bo_fit    — condition one GP per objective on the observations
+ *               (workflow step (i), "Surrogate model fitting"; ARD
+ *               Matern-5/2 kernel with an output scale, implementation
+ *               section "MOBO optimization kernels").
+ *   bo_score  — GP posterior of every candidate plus Monte-Carlo expected
+ *               hypervolume improvement against the Pareto front
+ *               (workflow step (ii) and the "Constrained qNEHVI" paragraph:
+ *               expectation of HVI over samples of the joint posterior).
+ *   bo_argmax — index of the best candidate ("selecting the next candidate
+ *               configuration theta*").
+ *
+ * Conventions shared by every entry point:
+ *   - All floating-point arrays are fp32, row-major, contiguous.
+ *   - "device" pointers are HIP device memory on the current device; "host"
+ *     pointers are ordinary host memory read before the call returns.
+ *   - The caller owns every buffer it passes; the library never frees them.
+ *     Asynchronous calls read/write caller buffers when the stream reaches
+ *     the work, so the caller keeps them alive until then.
+ *   - stream is a hipStream_t passed as void*; NULL means the null stream.
+ *   - Every function returns a status; nothing throws or aborts across the
+ *     ABI. Arguments are validated before any device work is enqueued.
+ *     bo_last_error_message() gives a thread-local detail string.
+ *   - Objectives are maximised and live in standardised units (the caller
+ *     standardises Y; the reference point and EHVI are in the same units).
+ *   - Kernel faults of an asynchronous call surface at the next synchronous
+ *     call; setting BO_SYNC_DEBUG=1 synchronises and checks after each launch.
+ *
+ * Thread safety: distinct models may be used from distinct threads. Calls
+ * that share a model must be ordered by the caller (same stream, or
+ * synchronised), because a model keeps one scoring workspace.
+ */
+#ifndef BO_H_
+#define BO_H_
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct bo_model_s* bo_model;   /* opaque, owned by the library */
+
+typedef enum {
+  BO_OK = 0,
+  BO_ERR_INVALID_ARGUMENT = 1,      /* bad size, null pointer, bad hyperparameter */
+  BO_ERR_NOT_POSITIVE_DEFINITE = 2, /* Cholesky pivot <= 0 or non-finite      */
+  BO_ERR_CAPACITY = 3,              /* n, d, S or box count beyond compiled limits */
+  BO_ERR_DEVICE = 4,                /* a HIP runtime call failed               */
+  BO_ERR_OUT_OF_MEMORY = 5,         /* device or host allocation failed        */
+  BO_ERR_NONFINITE_INPUT = 6        /* NaN/Inf in a host-side input            */
+} bo_status;
+
+/* Compiled limits (BO_ERR_CAPACITY beyond them). */
+#define BO_MAX_N 2048        /* observations                                 */
+#define BO_MAX_D 32          /* encoded dimensions                           */
+#define BO_MAX_S 4096        /* Monte-Carlo samples                          */
+#define BO_MAX_BOXES 4096    /* boxes of the non-dominated region            */
+
+/*
+ * bo_fit — exact GP conditioning, one independent GP per objective.
+ *
+ * Paper: workflow step (i) and the implementation section (one
+ * SingleTaskGP per objective combined as a model list; ARD Matern-5/2 in a
+ * scale kernel). Hyperparameters are given, not learned.
+ *
+ * For each objective k (s = outputscale[k], eta = noise[k],
+ * l = lengthscale[k*d .. k*d+d-1]):
+ *   k(u,v) = s (1 + sqrt5 r + 5/3 r^2) exp(-sqrt5 r),
+ *            r = sqrt(sum_t ((u_t - v_t)/l_t)^2)
+ *   K = [k(x_i,x_j)] + eta I;  L = chol(K);  alpha = K^{-1} y_k.
+ * The factorisation runs in fp64 on the device; the model keeps L^{-1}
+ * (fp32, lower blocks only), alpha (fp32) and the lengthscale-scaled X.
+ * It also extracts the non-dominated set of Y on the host.
+ *
+ * X      device [n][d]   encoded observations
+ * Y      device [n][m]   standardised objective values (maximise)
+ * n      1..BO_MAX_N;  d 1..BO_MAX_D;  m in {2, 3}
+ * lengthscale host [m][d] > 0;  outputscale host [m] > 0;  noise host [m] >= 0
+ * stream hipStream_t or NULL
+ * out    receives a new model on BO_OK (untouched otherwise)
+ *
+ * Synchronous: returns after the device work has finished and the positive
+ * definiteness check has been read back. Errors: INVALID_ARGUMENT,
+ * NONFINITE_INPUT (hyperparameters or Y not finite), CAPACITY,
+ * NOT_POSITIVE_DEFINITE, OUT_OF_MEMORY, DEVICE.
+ */
+bo_status bo_fit(const float* X, const float* Y, int64_t n, int32_t d, int32_t m,
+                 const float* lengthscale, const float* outputscale,
+                 const float* noise, void* stream, bo_model* out);
+
+/*
+ * bo_score — posterior plus Monte-Carlo (q)EHVI for M candidates.
+ *
+ * Paper: "Constrained qNEHVI" paragraph (expected HVI over samples of the
+ * joint posterior, Monte-Carlo integration) without the feasibility factor,
+ * against the fixed front of the observations.
+ *
+ * Per candidate batch b (q points x_1..x_q) and objective k:
+ *   mu_a = k(x_a, X) alpha_k;  v_a = L_k^{-1} k(X, x_a);
+ *   Sigma[a,b] = k(x_a, x_b) - v_a^T v_b;  C_k = chol_psd(Sigma) (q > 1)
+ *   y_s[a,k] = mu_a + sigma_a z_s[0,k]               (q = 1)
+ *   y_s[a,k] = mu_a + sum_c C_k[a,c] z_s[c,k]        (q > 1)
+ *   ehvi[b] = 1/S sum_s qHVI({y_s[a,:]}) , the hypervolume improvement of
+ *   the batch over the front F = non-dominated observations strictly above
+ *   ref_point, computed over a disjoint box decomposition of the region F
+ *   does not dominate (inclusion-exclusion over the 2^q - 1 member subsets).
+ * chol_psd: no jitter; a Schur pivot <= 1e-10 * outputscale zeroes that
+ * column. sigma = sqrt(max(Sigma[a,a], 0)).
+ *
+ * model        from bo_fit (same device must be current)
+ * cand         device [M][q][d]
+ * M            >= 0 (0 is a no-op);  q in {1, 2, 4}
+ * ref_point    host [m], finite
+ * base_samples device [S][q][m], standard normal draws shared by all M
+ * S            1..BO_MAX_S
+ * ehvi         device [M] out
+ * mu, sigma    device [M][q][m] out, or NULL to skip writing them
+ * stream       hipStream_t or NULL
+ *
+ * Asynchronous: enqueues kernels and returns. The box decomposition is built
+ * on the host when ref_point (or the model) changes and copied with the
+ * stream. Errors: INVALID_ARGUMENT, NONFINITE_INPUT (ref_point), CAPACITY
+ * (box count, S), OUT_OF_MEMORY (workspace growth), DEVICE.
+ */
+bo_status bo_score(bo_model model, const float* cand, int64_t M, int32_t q,
+                   const float* ref_point, const float* base_samples, int32_t S,
+                   float* ehvi, float* mu, float* sigma, void* stream);
+
+/*
+ * bo_argmax — first index of the maximum of values[0..M).
+ *
+ * Paper: workflow step (ii), choosing theta* as the maximiser of the
+ * acquisition over the candidates.
+ *
+ * values device [M];  M in [0, 2^31)
+ * index  device int64 out: lowest index among equal maxima; NaN never wins;
+ *        -1 when M == 0 or every value is NaN
+ * value  device float out: values[index], or NaN when index == -1
+ * Asynchronous. Uses *index as its own reduction cell (no workspace).
+ * Errors: INVALID_ARGUMENT.
+ */
+bo_status bo_argmax(const float* values, int64_t M, int64_t* index, float* value,
+                    void* stream);
+
+/* Number of non-dominated observations kept by bo_fit (before the
+ * reference-point filter), or -1 for a NULL model. */
+int32_t bo_model_front_size(bo_model model);
+
+/* Copies min(cap, front size) indices (into Y rows) of the non-dominated
+ * observations, sorted by objective 0 ascending then index, to host memory.
+ * Errors: INVALID_ARGUMENT. */
+bo_status bo_model_front_indices(bo_model model, int32_t* idx_host, int32_t cap);
+
+/*
+ * bo_cholesky_test — the blocked right-looking Cholesky used by bo_fit,
+ * exposed so its failure path can be tested.
+ * A device [n][n] symmetric (lower triangle read), L device [n][n] out
+ * (lower factor, zeros above the diagonal). 1 <= n <= BO_MAX_N.
+ * Synchronous. Errors: INVALID_ARGUMENT, NOT_POSITIVE_DEFINITE (a pivot
+ * <= 0 or non-finite), OUT_OF_MEMORY, DEVICE.
+ */
+bo_status bo_cholesky_test(const float* A, int64_t n, float* L, void* stream);
+
+/*
+ * Host-only geometry (no device work; callable without a GPU).
+ *
+ * bo_pareto_front: non-dominated rows of Y (maximise; duplicates keep the
+ * lowest index) that are strictly above ref in every objective, sorted by
+ * objective 0 ascending then index. Y host [n][m], ref host [m] or NULL
+ * (no reference filter). Writes min(cap, count) indices; *count gets the
+ * full count.
+ *
+ * bo_box_decomposition: disjoint boxes [lo, hi) covering
+ * {z > ref : no f in F with f >= z} for a front F host [P][m] (m in {2,3},
+ * every row strictly above ref). hi may be +inf. lo/hi host [cap][m];
+ * *count gets the number of boxes (BO_ERR_CAPACITY when it exceeds cap).
+ */
+bo_status bo_pareto_front(const float* Y, int64_t n, int32_t m, const float* ref,
+                          int32_t* idx, int32_t cap, int32_t* count);
+bo_status bo_box_decomposition(const float* F, int32_t P, int32_t m,
+                               const float* ref, float* lo, float* hi,
+                               int32_t cap, int32_t* count);
+
+/*
+ * Phase timing for benchmarks. While enabled, every bo_score call records
+ * HIP events on its stream before its posterior launches, between them and
+ * the (q)EHVI launch, and after it. bo_profile_read waits for the recorded
+ * events, returns the summed milliseconds of each phase, the number of
+ * bo_score calls and the number of posterior launches (one per objective per
+ * call) since the last read, and clears them. Enabling resets the counters.
+ * Up to 4096 calls are kept; later calls are not timed (see *calls).
+ * Errors: INVALID_ARGUMENT (NULL output), DEVICE.
+ */
+bo_status bo_profile_enable(int32_t on);
+bo_status bo_profile_read(double* posterior_ms, double* ehvi_ms, int64_t* calls,
+                          int64_t* posterior_launches);
+
+/* Releases a model (waits for its last stream first). NULL is a no-op. */
+void bo_free(bo_model model);
+
+/* Static description of a status code. */
+const char* bo_status_string(bo_status status);
+
+/* Detail of the last error on the calling thread ("" if none). */
+const char* bo_last_error_message(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BO_H_ */

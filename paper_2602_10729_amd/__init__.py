@@ -1,0 +1,266 @@
+"""Python binding of libbo, the MI355X batch acquisition scorer.
+
+Argument marshalling only: every step of fitting, scoring and the argmax runs
+in the HIP kernels of ``libbo.so``; torch tensors supply device memory and the
+current stream. There is no CPU fallback: if the library is missing or a
+tensor is not on the GPU, the call raises.
+
+Functions mirror the C ABI in ``include/bo.h``:
+``fit``, ``score``, ``argmax``, ``cholesky_test`` (device) and
+``pareto_front``, ``box_decomposition`` (host geometry, no GPU needed).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+
+__all__ = ["BoError", "Model", "lib", "lib_path", "fit", "score", "argmax",
+           "cholesky_test", "profile_enable", "profile_read", "pareto_front", "box_decomposition", "STATUS",
+           "MAX_N", "MAX_D", "MAX_S", "MAX_BOXES"]
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "libbo.so")
+_lib = None
+
+STATUS = {
+    0: "BO_OK", 1: "BO_ERR_INVALID_ARGUMENT", 2: "BO_ERR_NOT_POSITIVE_DEFINITE",
+    3: "BO_ERR_CAPACITY", 4: "BO_ERR_DEVICE", 5: "BO_ERR_OUT_OF_MEMORY",
+    6: "BO_ERR_NONFINITE_INPUT",
+}
+MAX_N, MAX_D, MAX_S, MAX_BOXES = 2048, 32, 4096, 4096
+
+
+class BoError(RuntimeError):
+    def __init__(self, status: int, where: str, detail: str):
+        self.status = status
+        self.name = STATUS.get(status, str(status))
+        super().__init__(f"{where}: {self.name}: {detail}")
+
+
+def lib_path() -> str:
+    return _LIB_PATH
+
+
+def lib() -> ctypes.CDLL:
+    """Load libbo.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        raise RuntimeError(
+            f"{_LIB_PATH} is missing: build it with `python -m paper_2602_10729_amd.build`")
+    L = ctypes.CDLL(_LIB_PATH)
+    vp, i64, i32, fp = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p
+    L.bo_fit.argtypes = [vp, vp, i64, i32, i32, fp, fp, fp, vp, ctypes.POINTER(vp)]
+    L.bo_fit.restype = ctypes.c_int
+    L.bo_score.argtypes = [vp, vp, i64, i32, fp, vp, i32, vp, vp, vp, vp]
+    L.bo_score.restype = ctypes.c_int
+    L.bo_argmax.argtypes = [vp, i64, vp, vp, vp]
+    L.bo_argmax.restype = ctypes.c_int
+    L.bo_model_front_size.argtypes = [vp]
+    L.bo_model_front_size.restype = i32
+    L.bo_model_front_indices.argtypes = [vp, vp, i32]
+    L.bo_model_front_indices.restype = ctypes.c_int
+    L.bo_cholesky_test.argtypes = [vp, i64, vp, vp]
+    L.bo_cholesky_test.restype = ctypes.c_int
+    L.bo_pareto_front.argtypes = [vp, i64, i32, vp, vp, i32, ctypes.POINTER(i32)]
+    L.bo_pareto_front.restype = ctypes.c_int
+    L.bo_box_decomposition.argtypes = [vp, i32, i32, vp, vp, vp, i32, ctypes.POINTER(i32)]
+    L.bo_box_decomposition.restype = ctypes.c_int
+    L.bo_profile_enable.argtypes = [i32]
+    L.bo_profile_enable.restype = ctypes.c_int
+    L.bo_profile_read.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double),
+                                  ctypes.POINTER(i64), ctypes.POINTER(i64)]
+    L.bo_profile_read.restype = ctypes.c_int
+    L.bo_free.argtypes = [vp]
+    L.bo_free.restype = None
+    L.bo_status_string.argtypes = [ctypes.c_int]
+    L.bo_status_string.restype = ctypes.c_char_p
+    L.bo_last_error_message.argtypes = []
+    L.bo_last_error_message.restype = ctypes.c_char_p
+    _lib = L
+    return L
+
+
+def _check(status: int, where: str):
+    if status != 0:
+        detail = lib().bo_last_error_message().decode(errors="replace")
+        raise BoError(status, where, detail)
+
+
+def _stream(stream):
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(int(stream.cuda_stream))
+
+
+def _dev(t, name, dtype=None):
+    import torch
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch tensor on the GPU")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must live on a GPU (got {t.device})")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype} (got {t.dtype})")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _host_f32(a, shape, name):
+    a = np.ascontiguousarray(np.asarray(a, dtype=np.float32))
+    if a.size != int(np.prod(shape)):
+        raise ValueError(f"{name} must have {int(np.prod(shape))} elements")
+    return a
+
+
+class Model:
+    """A fitted model (opaque handle owned by the library)."""
+
+    def __init__(self, handle: int, n: int, d: int, m: int):
+        self._h = ctypes.c_void_p(handle)
+        self.n, self.d, self.m = n, d, m
+
+    @property
+    def handle(self):
+        return self._h
+
+    def front_indices(self) -> np.ndarray:
+        L = lib()
+        P = L.bo_model_front_size(self._h)
+        out = np.zeros(max(P, 0), dtype=np.int32)
+        _check(L.bo_model_front_indices(self._h, out.ctypes.data_as(ctypes.c_void_p), P),
+               "bo_model_front_indices")
+        return out
+
+    def close(self):
+        if self._h is not None and self._h.value:
+            lib().bo_free(self._h)
+        self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def fit(X, Y, lengthscale, outputscale, noise, stream=None) -> Model:
+    """bo_fit: X [n, d], Y [n, m] fp32 GPU tensors; hyperparameters on host."""
+    import torch
+    n, d = X.shape
+    m = Y.shape[1]
+    ls = _host_f32(lengthscale, (m, d), "lengthscale")
+    os_ = _host_f32(outputscale, (m,), "outputscale")
+    nz = _host_f32(noise, (m,), "noise")
+    h = ctypes.c_void_p()
+    st = lib().bo_fit(_dev(X, "X", torch.float32), _dev(Y, "Y", torch.float32), n, d, m,
+                      ls.ctypes.data_as(ctypes.c_void_p), os_.ctypes.data_as(ctypes.c_void_p),
+                      nz.ctypes.data_as(ctypes.c_void_p), _stream(stream), ctypes.byref(h))
+    _check(st, "bo_fit")
+    return Model(h.value, n, d, m)
+
+
+def score(model: Model, cand, ref, Z, ehvi=None, mu=None, sigma=None, stream=None):
+    """bo_score: cand [M, q, d], Z [S, q, m] fp32 GPU tensors; ref host [m].
+
+    Returns the ehvi tensor [M] (allocated if not given). mu/sigma
+    [M, q, m] are written only when passed.
+    """
+    import torch
+    M, q, d = cand.shape
+    S = Z.shape[0]
+    r = _host_f32(ref, (model.m,), "ref")
+    if ehvi is None:
+        ehvi = torch.empty(M, dtype=torch.float32, device=cand.device)
+    mu_p = _dev(mu, "mu", torch.float32) if mu is not None else ctypes.c_void_p(0)
+    sg_p = _dev(sigma, "sigma", torch.float32) if sigma is not None else ctypes.c_void_p(0)
+    st = lib().bo_score(model.handle, _dev(cand, "cand", torch.float32), M, q,
+                        r.ctypes.data_as(ctypes.c_void_p), _dev(Z, "Z", torch.float32), S,
+                        _dev(ehvi, "ehvi", torch.float32), mu_p, sg_p, _stream(stream))
+    _check(st, "bo_score")
+    return ehvi
+
+
+def argmax(values, index=None, value=None, stream=None):
+    """bo_argmax into device scalars (int64 index, float32 value)."""
+    import torch
+    dev = values.device
+    if index is None:
+        index = torch.empty(1, dtype=torch.int64, device=dev)
+    if value is None:
+        value = torch.empty(1, dtype=torch.float32, device=dev)
+    st = lib().bo_argmax(_dev(values, "values", torch.float32), values.numel(),
+                         _dev(index, "index", torch.int64), _dev(value, "value", torch.float32),
+                         _stream(stream))
+    _check(st, "bo_argmax")
+    return index, value
+
+
+def profile_enable(on: bool = True):
+    """Start (or stop) per-phase event timing of bo_score calls."""
+    _check(lib().bo_profile_enable(1 if on else 0), "bo_profile_enable")
+
+
+def profile_read():
+    """(posterior_ms, ehvi_ms, calls, posterior_launches) since the last read."""
+    a, b = ctypes.c_double(), ctypes.c_double()
+    c, n = ctypes.c_int64(), ctypes.c_int64()
+    _check(lib().bo_profile_read(ctypes.byref(a), ctypes.byref(b), ctypes.byref(c),
+                                 ctypes.byref(n)), "bo_profile_read")
+    return a.value, b.value, c.value, n.value
+
+
+def cholesky_test(A, L=None, stream=None):
+    """bo_cholesky_test: lower factor of a symmetric fp32 GPU matrix."""
+    import torch
+    n = A.shape[0]
+    if L is None:
+        L = torch.empty_like(A)
+    st = lib().bo_cholesky_test(_dev(A, "A", torch.float32), n, _dev(L, "L", torch.float32),
+                                _stream(stream))
+    _check(st, "bo_cholesky_test")
+    return L
+
+
+def pareto_front(Y, ref: Optional[np.ndarray] = None) -> np.ndarray:
+    """Host: front indices (sorted by objective 0) of Y [n, m] (fp32)."""
+    Y = np.ascontiguousarray(np.asarray(Y, dtype=np.float32))
+    n, m = Y.shape
+    rp = ctypes.c_void_p(0)
+    if ref is not None:
+        ref = _host_f32(ref, (m,), "ref")
+        rp = ref.ctypes.data_as(ctypes.c_void_p)
+    idx = np.zeros(max(n, 1), dtype=np.int32)
+    cnt = ctypes.c_int32(0)
+    _check(lib().bo_pareto_front(Y.ctypes.data_as(ctypes.c_void_p), n, m, rp,
+                                 idx.ctypes.data_as(ctypes.c_void_p), n, ctypes.byref(cnt)),
+           "bo_pareto_front")
+    return idx[:cnt.value].copy()
+
+
+def box_decomposition(F, ref):
+    """Host: disjoint boxes (lo, hi) [B, m] of the region F does not dominate."""
+    F = np.ascontiguousarray(np.asarray(F, dtype=np.float32))
+    m = np.asarray(ref).shape[0]
+    F = F.reshape(-1, m)
+    r = _host_f32(ref, (m,), "ref")
+    cnt = ctypes.c_int32(0)
+    L = lib()
+    cap = 4 * F.shape[0] + 8
+    while True:
+        lo = np.zeros((cap, m), dtype=np.float32)
+        hi = np.zeros((cap, m), dtype=np.float32)
+        st = L.bo_box_decomposition(F.ctypes.data_as(ctypes.c_void_p), F.shape[0], m,
+                                    r.ctypes.data_as(ctypes.c_void_p),
+                                    lo.ctypes.data_as(ctypes.c_void_p),
+                                    hi.ctypes.data_as(ctypes.c_void_p), cap, ctypes.byref(cnt))
+        if st == 3 and cnt.value > cap:
+            cap = cnt.value
+            continue
+        _check(st, "bo_box_decomposition")
+        return lo[:cnt.value].copy(), hi[:cnt.value].copy()

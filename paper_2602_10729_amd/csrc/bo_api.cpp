@@ -1,0 +1,585 @@
+// C ABI entry points: validation, model lifecycle and launch sequencing.
+//
+// bo_fit      — Gram (fp64) -> blocked Cholesky -> L^{-1} -> alpha -> pack,
+//               all on the caller's stream, then one synchronisation to read
+//               the positive-definiteness flag back.
+// bo_score    — per objective one posterior launch, then one (q)EHVI launch;
+//               asynchronous. The box decomposition is rebuilt on the host
+//               only when the reference point changes.
+// bo_argmax   — three tiny launches using the caller's index cell.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdlib>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "bo_internal.h"
+
+namespace bo {
+
+size_t posterior_lds_bytes(int nb, int q);
+size_t ehvi_lds_bytes(int S, int q, int m, int nbox);
+
+namespace {
+thread_local std::string g_err;
+
+bool sync_debug() {
+  static int v = [] {
+    const char* e = std::getenv("BO_SYNC_DEBUG");
+    return (e && e[0] == '1') ? 1 : 0;
+  }();
+  return v != 0;
+}
+
+constexpr size_t kLdsLimit = 160 * 1024;
+
+// Device pointer check: the whole [p, p + bytes) must lie in one device
+// allocation of the current device.
+bo_status check_dev(const void* p, size_t bytes, const char* name) {
+  if (!p) return fail(BO_ERR_INVALID_ARGUMENT, std::string(name) + " is NULL");
+  hipPointerAttribute_t attr;
+  hipError_t e = hipPointerGetAttributes(&attr, p);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(BO_ERR_INVALID_ARGUMENT, std::string(name) + " is not a device pointer");
+  }
+  if (attr.type != hipMemoryTypeDevice && attr.type != hipMemoryTypeManaged) {
+    return fail(BO_ERR_INVALID_ARGUMENT, std::string(name) + " is not device memory");
+  }
+  int dev = -1;
+  (void)hipGetDevice(&dev);
+  if (attr.device != dev) {
+    return fail(BO_ERR_INVALID_ARGUMENT, std::string(name) + " lives on another device");
+  }
+  if (bytes > 0) {
+    hipDeviceptr_t base = nullptr;
+    size_t size = 0;
+    e = hipMemGetAddressRange(&base, &size, const_cast<void*>(p));
+    if (e != hipSuccess) {
+      (void)hipGetLastError();
+      return fail(BO_ERR_INVALID_ARGUMENT, std::string(name) + ": no allocation range");
+    }
+    const char* b = static_cast<const char*>(base);
+    const char* q = static_cast<const char*>(p);
+    if (q < b || static_cast<size_t>(q - b) + bytes > size) {
+      return fail(BO_ERR_INVALID_ARGUMENT,
+                  std::string(name) + " is smaller than the sizes passed require");
+    }
+  }
+  return BO_OK;
+}
+
+bo_status after_launch(hipError_t e, hipStream_t st, const char* what) {
+  if (e != hipSuccess) return hip_fail(e, what);
+  if (sync_debug()) {
+    e = hipStreamSynchronize(st);
+    if (e != hipSuccess) return hip_fail(e, what);
+  }
+  return BO_OK;
+}
+
+bool all_finite(const float* v, size_t n) {
+  for (size_t i = 0; i < n; ++i)
+    if (!std::isfinite(v[i])) return false;
+  return true;
+}
+
+template <typename T>
+bo_status dmalloc(T** p, size_t count, const char* what) {
+  *p = nullptr;
+  if (count == 0) return BO_OK;
+  hipError_t e = hipMalloc(reinterpret_cast<void**>(p), sizeof(T) * count);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    *p = nullptr;
+    return fail(BO_ERR_OUT_OF_MEMORY, std::string("hipMalloc failed for ") + what);
+  }
+  return BO_OK;
+}
+
+struct DeviceGuard {
+  int prev = -1;
+  bool ok = true;
+  explicit DeviceGuard(int dev) {
+    (void)hipGetDevice(&prev);
+    if (prev != dev) ok = hipSetDevice(dev) == hipSuccess;
+  }
+  ~DeviceGuard() {
+    int cur = -1;
+    (void)hipGetDevice(&cur);
+    if (prev >= 0 && cur != prev) (void)hipSetDevice(prev);
+  }
+};
+
+// Temporary device buffers of the fit, released on every exit path.
+struct FitScratch {
+  double* A = nullptr;
+  double* W = nullptr;
+  double* Dinv = nullptr;
+  double* hyp = nullptr;
+  double* tmp = nullptr;
+  int* flag = nullptr;
+  ~FitScratch() {
+    (void)hipFree(A); (void)hipFree(W); (void)hipFree(Dinv);
+    (void)hipFree(hyp); (void)hipFree(tmp); (void)hipFree(flag);
+  }
+};
+
+// Frees the device/pinned buffers of a model (not the host object).
+void release_buffers(Model* M) {
+  (void)hipDeviceSynchronize();   // earlier launches may still read them
+  (void)hipFree(M->Xs);
+  (void)hipFree(M->invls);
+  (void)hipFree(M->alpha);
+  (void)hipFree(M->Lp);
+  (void)hipFree(M->ws);
+  (void)hipFree(M->d_boxes);
+  if (M->h_boxes) (void)hipHostFree(M->h_boxes);
+  if (M->box_evt) (void)hipEventDestroy(M->box_evt);
+  M->Xs = M->invls = M->alpha = M->Lp = M->ws = M->d_boxes = M->h_boxes = nullptr;
+  M->box_evt = nullptr;
+}
+
+// Phase timing (bo_profile_enable / bo_profile_read).
+struct Profile {
+  std::mutex mu;
+  bool on = false;
+  struct Rec { hipEvent_t e[3]; int launches; };
+  std::vector<Rec> pool;
+  size_t used = 0;
+};
+Profile& profile() {
+  static Profile p;
+  return p;
+}
+constexpr size_t kProfileCap = 4096;
+
+}  // namespace
+
+bo_status fail(bo_status st, const std::string& msg) {
+  g_err = msg;
+  return st;
+}
+
+bo_status hip_fail(hipError_t e, const char* what) {
+  g_err = std::string(what) + ": " + hipGetErrorString(e);
+  (void)hipGetLastError();
+  return (e == hipErrorOutOfMemory) ? BO_ERR_OUT_OF_MEMORY : BO_ERR_DEVICE;
+}
+
+}  // namespace bo
+
+struct bo_model_s {
+  bo::Model m;
+};
+
+using namespace bo;
+
+extern "C" {
+
+const char* bo_status_string(bo_status s) {
+  switch (s) {
+    case BO_OK: return "ok";
+    case BO_ERR_INVALID_ARGUMENT: return "invalid argument";
+    case BO_ERR_NOT_POSITIVE_DEFINITE: return "matrix not positive definite";
+    case BO_ERR_CAPACITY: return "size beyond compiled capacity";
+    case BO_ERR_DEVICE: return "HIP runtime error";
+    case BO_ERR_OUT_OF_MEMORY: return "out of memory";
+    case BO_ERR_NONFINITE_INPUT: return "non-finite input";
+  }
+  return "unknown status";
+}
+
+const char* bo_last_error_message(void) { return g_err.c_str(); }
+
+bo_status bo_pareto_front(const float* Y, int64_t n, int32_t m, const float* ref,
+                          int32_t* idx, int32_t cap, int32_t* count) {
+  if (!Y || !count || (cap > 0 && !idx) || n < 0 || cap < 0)
+    return fail(BO_ERR_INVALID_ARGUMENT, "bo_pareto_front: bad pointer or size");
+  if (m < 1 || m > 8) return fail(BO_ERR_INVALID_ARGUMENT, "bo_pareto_front: m out of range");
+  std::vector<int32_t> out;
+  host_front(Y, n, m, ref, out);
+  *count = static_cast<int32_t>(out.size());
+  const int32_t k = std::min<int32_t>(cap, *count);
+  for (int32_t i = 0; i < k; ++i) idx[i] = out[i];
+  return BO_OK;
+}
+
+bo_status bo_box_decomposition(const float* F, int32_t P, int32_t m, const float* ref,
+                               float* lo, float* hi, int32_t cap, int32_t* count) {
+  if ((P > 0 && !F) || !ref || !count || P < 0 || cap < 0 || (cap > 0 && (!lo || !hi)))
+    return fail(BO_ERR_INVALID_ARGUMENT, "bo_box_decomposition: bad pointer or size");
+  if (m != 2 && m != 3) return fail(BO_ERR_INVALID_ARGUMENT, "bo_box_decomposition: m must be 2 or 3");
+  if (!all_finite(ref, m) || !all_finite(F, static_cast<size_t>(P) * m))
+    return fail(BO_ERR_NONFINITE_INPUT, "bo_box_decomposition: non-finite input");
+  for (int32_t i = 0; i < P; ++i)
+    for (int k = 0; k < m; ++k)
+      if (!(F[i * m + k] > ref[k]))
+        return fail(BO_ERR_INVALID_ARGUMENT, "bo_box_decomposition: front row not above ref");
+  std::vector<float> Fs;
+  const float* Fp = F;
+  if (m == 2) {
+    // the staircase needs the 2-D non-dominated points sorted by objective 0
+    std::vector<int32_t> nd;
+    host_front(F, P, 2, nullptr, nd);
+    for (int32_t i : nd) { Fs.push_back(F[2 * i]); Fs.push_back(F[2 * i + 1]); }
+    Fp = Fs.data();
+    P = static_cast<int32_t>(nd.size());
+  }
+  std::vector<float> l, h;
+  host_boxes(Fp, P, m, ref, l, h);
+  const int32_t nbx = static_cast<int32_t>(l.size() / m);
+  *count = nbx;
+  if (nbx > cap) return fail(BO_ERR_CAPACITY, "bo_box_decomposition: cap too small");
+  std::memcpy(lo, l.data(), sizeof(float) * l.size());
+  std::memcpy(hi, h.data(), sizeof(float) * h.size());
+  return BO_OK;
+}
+
+int32_t bo_model_front_size(bo_model model) {
+  if (!model) return -1;
+  return static_cast<int32_t>(model->m.nd.size());
+}
+
+bo_status bo_model_front_indices(bo_model model, int32_t* idx_host, int32_t cap) {
+  if (!model || (cap > 0 && !idx_host) || cap < 0)
+    return fail(BO_ERR_INVALID_ARGUMENT, "bo_model_front_indices: bad argument");
+  const int32_t k = std::min<int32_t>(cap, static_cast<int32_t>(model->m.nd.size()));
+  for (int32_t i = 0; i < k; ++i) idx_host[i] = model->m.nd[i];
+  return BO_OK;
+}
+
+bo_status bo_fit(const float* X, const float* Y, int64_t n, int32_t d, int32_t m,
+                 const float* lengthscale, const float* outputscale, const float* noise,
+                 void* stream, bo_model* out) {
+  if (!out) return fail(BO_ERR_INVALID_ARGUMENT, "bo_fit: out is NULL");
+  if (!lengthscale || !outputscale || !noise)
+    return fail(BO_ERR_INVALID_ARGUMENT, "bo_fit: NULL hyperparameter pointer");
+  if (n < 1 || d < 1 || (m != 2 && m != 3))
+    return fail(BO_ERR_INVALID_ARGUMENT, "bo_fit: need n >= 1, d >= 1, m in {2,3}");
+  if (n > BO_MAX_N || d > BO_MAX_D)
+    return fail(BO_ERR_CAPACITY, "bo_fit: n or d beyond compiled limits");
+  if (!all_finite(lengthscale, (size_t)m * d) || !all_finite(outputscale, m) ||
+      !all_finite(noise, m))
+    return fail(BO_ERR_NONFINITE_INPUT, "bo_fit: non-finite hyperparameter");
+  for (int i = 0; i < m * d; ++i)
+    if (!(lengthscale[i] > 0.f)) return fail(BO_ERR_INVALID_ARGUMENT, "bo_fit: lengthscale <= 0");
+  for (int k = 0; k < m; ++k) {
+    if (!(outputscale[k] > 0.f)) return fail(BO_ERR_INVALID_ARGUMENT, "bo_fit: outputscale <= 0");
+    if (!(noise[k] >= 0.f)) return fail(BO_ERR_INVALID_ARGUMENT, "bo_fit: noise < 0");
+  }
+  bo_status s;
+  if ((s = check_dev(X, sizeof(float) * n * d, "X")) != BO_OK) return s;
+  if ((s = check_dev(Y, sizeof(float) * n * m, "Y")) != BO_OK) return s;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+
+  bo_model_s* h = new (std::nothrow) bo_model_s();
+  if (!h) return fail(BO_ERR_OUT_OF_MEMORY, "bo_fit: host allocation");
+  Model* M = &h->m;
+  (void)hipGetDevice(&M->device);
+  M->n = n; M->d = d; M->m = m;
+  M->n_pad = static_cast<int>((n + kBlk - 1) / kBlk) * kBlk;
+  M->nb = M->n_pad / kBlk;
+  M->dx = (d + 3) / 4 * 4;
+  M->ls.assign(lengthscale, lengthscale + (size_t)m * d);
+  M->os.assign(outputscale, outputscale + m);
+  M->noise.assign(noise, noise + m);
+
+  auto bail = [&](bo_status st_) {
+    release_buffers(M);
+    delete h;
+    return st_;
+  };
+
+  // Y to the host for the front (and to check finiteness)
+  M->Yh.resize((size_t)n * m);
+  hipError_t e = hipMemcpyAsync(M->Yh.data(), Y, sizeof(float) * n * m, hipMemcpyDeviceToHost, st);
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  if (e != hipSuccess) return bail(hip_fail(e, "bo_fit: copy Y"));
+  if (!all_finite(M->Yh.data(), M->Yh.size())) return bail(fail(BO_ERR_NONFINITE_INPUT, "bo_fit: Y not finite"));
+  host_front(M->Yh.data(), n, m, nullptr, M->nd);
+
+  const int nf = static_cast<int>((n + kFitBlk - 1) / kFitBlk) * kFitBlk;
+  const size_t nblk = (size_t)M->nb * (M->nb + 1) / 2;
+  M->lp_per_obj = nblk * 64 * 4;
+  FitScratch fs;
+  if ((s = dmalloc(&fs.A, (size_t)m * nf * nf, "fit matrix")) != BO_OK) return bail(s);
+  if ((s = dmalloc(&fs.W, (size_t)m * nf * nf, "fit inverse")) != BO_OK) return bail(s);
+  if ((s = dmalloc(&fs.Dinv, (size_t)m * nf * kFitBlk, "fit block inverses")) != BO_OK) return bail(s);
+  if ((s = dmalloc(&fs.hyp, (size_t)m * d + 2 * m, "hyperparameters")) != BO_OK) return bail(s);
+  if ((s = dmalloc(&fs.tmp, (size_t)m * nf, "fit vector")) != BO_OK) return bail(s);
+  if ((s = dmalloc(&fs.flag, 1, "flag")) != BO_OK) return bail(s);
+  if ((s = dmalloc(&M->Xs, (size_t)m * M->n_pad * M->dx, "scaled X")) != BO_OK) return bail(s);
+  if ((s = dmalloc(&M->invls, (size_t)m * M->dx, "inverse lengthscales")) != BO_OK) return bail(s);
+  if ((s = dmalloc(&M->alpha, (size_t)m * M->n_pad, "alpha")) != BO_OK) return bail(s);
+  if ((s = dmalloc(&M->Lp, (size_t)m * M->lp_per_obj, "packed inverse")) != BO_OK) return bail(s);
+
+  std::vector<double> hyp((size_t)m * d + 2 * m);
+  for (int i = 0; i < m * d; ++i) hyp[i] = lengthscale[i];
+  for (int k = 0; k < m; ++k) {
+    hyp[(size_t)m * d + k] = outputscale[k];
+    hyp[(size_t)m * d + m + k] = noise[k];
+  }
+  std::vector<float> invls((size_t)m * M->dx, 0.f);
+  for (int k = 0; k < m; ++k)
+    for (int t = 0; t < d; ++t) invls[(size_t)k * M->dx + t] = 1.0f / lengthscale[k * d + t];
+
+  e = hipMemcpyAsync(fs.hyp, hyp.data(), sizeof(double) * hyp.size(), hipMemcpyHostToDevice, st);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(M->invls, invls.data(), sizeof(float) * invls.size(), hipMemcpyHostToDevice, st);
+  if (e == hipSuccess) e = hipMemsetAsync(fs.flag, 0, sizeof(int), st);
+  if (e != hipSuccess) return bail(hip_fail(e, "bo_fit: upload"));
+
+  const double* d_ls = fs.hyp;
+  const double* d_os = fs.hyp + (size_t)m * d;
+  const double* d_noise = d_os + m;
+  if ((s = after_launch(launch_gram(X, n, d, m, nf, d_ls, d_os, d_noise, fs.A, st), st, "gram")) != BO_OK) return bail(s);
+  if ((s = after_launch(launch_cholesky(fs.A, fs.Dinv, nf, m, fs.flag, st), st, "cholesky")) != BO_OK) return bail(s);
+  if ((s = after_launch(launch_trtri(fs.A, fs.Dinv, fs.W, nf, m, st), st, "trtri")) != BO_OK) return bail(s);
+  if ((s = after_launch(launch_alpha(fs.W, Y, n, m, nf, M->n_pad, fs.tmp, M->alpha, st), st, "alpha")) != BO_OK) return bail(s);
+  if ((s = after_launch(launch_pack(fs.W, n, m, nf, M->nb, M->Lp, X, d, M->dx, M->invls, M->Xs, st), st, "pack")) != BO_OK) return bail(s);
+
+  int flag = 0;
+  e = hipMemcpyAsync(&flag, fs.flag, sizeof(int), hipMemcpyDeviceToHost, st);
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  if (e != hipSuccess) return bail(hip_fail(e, "bo_fit: sync"));
+  if (flag) return bail(fail(BO_ERR_NOT_POSITIVE_DEFINITE, "bo_fit: non-positive Cholesky pivot"));
+
+  e = hipEventCreateWithFlags(&M->box_evt, hipEventDisableTiming);
+  if (e != hipSuccess) return bail(hip_fail(e, "bo_fit: event"));
+  M->last_stream = st;
+  *out = h;
+  return BO_OK;
+}
+
+void bo_free(bo_model model) {
+  if (!model) return;
+  DeviceGuard g(model->m.device);
+  release_buffers(&model->m);
+  delete model;
+}
+
+bo_status bo_score(bo_model model, const float* cand, int64_t M_, int32_t q,
+                   const float* ref_point, const float* base_samples, int32_t S,
+                   float* ehvi, float* mu, float* sigma, void* stream) {
+  if (!model) return fail(BO_ERR_INVALID_ARGUMENT, "bo_score: model is NULL");
+  Model& M = model->m;
+  if (M_ < 0) return fail(BO_ERR_INVALID_ARGUMENT, "bo_score: M < 0");
+  if (q != 1 && q != 2 && q != 4) return fail(BO_ERR_INVALID_ARGUMENT, "bo_score: q must be 1, 2 or 4");
+  if (S < 1) return fail(BO_ERR_INVALID_ARGUMENT, "bo_score: S < 1");
+  if (S > BO_MAX_S) return fail(BO_ERR_CAPACITY, "bo_score: S beyond compiled limit");
+  if (!ref_point) return fail(BO_ERR_INVALID_ARGUMENT, "bo_score: ref_point is NULL");
+  if (!all_finite(ref_point, M.m)) return fail(BO_ERR_NONFINITE_INPUT, "bo_score: ref_point not finite");
+  if (M_ > (int64_t)1 << 40) return fail(BO_ERR_CAPACITY, "bo_score: M too large");
+  DeviceGuard g(M.device);
+  if (!g.ok) return fail(BO_ERR_DEVICE, "bo_score: cannot select the model's device");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int m = M.m;
+  const int64_t npts = M_ * q;
+  bo_status s;
+  if (M_ == 0) return BO_OK;
+  if ((s = check_dev(cand, sizeof(float) * npts * M.d, "cand")) != BO_OK) return s;
+  if ((s = check_dev(base_samples, sizeof(float) * (size_t)S * q * m, "base_samples")) != BO_OK) return s;
+  if ((s = check_dev(ehvi, sizeof(float) * M_, "ehvi")) != BO_OK) return s;
+  if (mu && (s = check_dev(mu, sizeof(float) * npts * m, "mu")) != BO_OK) return s;
+  if (sigma && (s = check_dev(sigma, sizeof(float) * npts * m, "sigma")) != BO_OK) return s;
+  if (posterior_lds_bytes(M.nb, q) > kLdsLimit)
+    return fail(BO_ERR_CAPACITY, "bo_score: posterior tile exceeds LDS");
+
+  // ---- boxes (host, cached per reference point) ------------------------
+  const bool same_ref = M.nbox >= 0 && M.box_ref.size() == (size_t)m &&
+                        std::memcmp(M.box_ref.data(), ref_point, sizeof(float) * m) == 0;
+  if (!same_ref) {
+    std::vector<float> F;
+    for (int32_t i : M.nd) {
+      const float* y = &M.Yh[(size_t)i * m];
+      bool above = true;
+      for (int k = 0; k < m; ++k) above = above && (y[k] > ref_point[k]);
+      if (above) F.insert(F.end(), y, y + m);
+    }
+    std::vector<float> lo, hi;
+    host_boxes(F.data(), static_cast<int>(F.size() / m), m, ref_point, lo, hi);
+    const int nbox = static_cast<int>(lo.size() / m);
+    if (nbox > BO_MAX_BOXES) return fail(BO_ERR_CAPACITY, "bo_score: too many boxes");
+    if (ehvi_lds_bytes(S, q, m, nbox) > kLdsLimit)
+      return fail(BO_ERR_CAPACITY, "bo_score: samples and boxes exceed LDS");
+    hipError_t e;
+    if (nbox > M.box_cap) {
+      // buffers may still be read by earlier launches: wait before replacing
+      e = hipDeviceSynchronize();
+      if (e != hipSuccess) return hip_fail(e, "bo_score: sync before box realloc");
+      (void)hipFree(M.d_boxes);
+      M.d_boxes = nullptr;
+      if (M.h_boxes) (void)hipHostFree(M.h_boxes);
+      M.h_boxes = nullptr;
+      M.box_cap = 0;
+      const int cap = std::max(64, nbox);
+      if ((s = dmalloc(&M.d_boxes, (size_t)cap * 2 * m, "boxes")) != BO_OK) return s;
+      e = hipHostMalloc(reinterpret_cast<void**>(&M.h_boxes), sizeof(float) * cap * 2 * m, hipHostMallocDefault);
+      if (e != hipSuccess) return hip_fail(e, "bo_score: pinned boxes");
+      M.box_cap = cap;
+    } else {
+      e = hipEventSynchronize(M.box_evt);       // previous staging copy done
+      if (e != hipSuccess) return hip_fail(e, "bo_score: box event");
+    }
+    for (int c = 0; c < nbox; ++c)
+      for (int k = 0; k < m; ++k) {
+        const float l = lo[(size_t)c * m + k], h = hi[(size_t)c * m + k];
+        M.h_boxes[(size_t)c * 2 * m + k] = l;
+        M.h_boxes[(size_t)c * 2 * m + m + k] = h - l;     // inf stays inf
+      }
+    e = hipMemcpyAsync(M.d_boxes, M.h_boxes, sizeof(float) * nbox * 2 * m, hipMemcpyHostToDevice, st);
+    if (e == hipSuccess) e = hipEventRecord(M.box_evt, st);
+    if (e != hipSuccess) return hip_fail(e, "bo_score: box upload");
+    M.nbox = nbox;
+    M.box_ref.assign(ref_point, ref_point + m);
+  } else if (ehvi_lds_bytes(S, q, m, M.nbox) > kLdsLimit) {
+    return fail(BO_ERR_CAPACITY, "bo_score: samples and boxes exceed LDS");
+  }
+
+  // ---- workspace ----------------------------------------------------------
+  const int T = q * (q + 1) / 2;
+  const size_t need = (mu ? 0 : (size_t)npts * m) + (sigma ? 0 : (size_t)npts * m) +
+                      (q > 1 ? (size_t)M_ * m * T : 0);
+  if (need > M.ws_floats) {
+    hipError_t e = hipDeviceSynchronize();
+    if (e != hipSuccess) return hip_fail(e, "bo_score: sync before workspace growth");
+    (void)hipFree(M.ws);
+    M.ws = nullptr;
+    M.ws_floats = 0;
+    if ((s = dmalloc(&M.ws, need, "score workspace")) != BO_OK) return s;
+    M.ws_floats = need;
+  }
+  float* w = M.ws;
+  float* mu_buf = mu ? mu : w;
+  if (!mu) w += (size_t)npts * m;
+  float* sd_buf = sigma ? sigma : w;
+  if (!sigma) w += (size_t)npts * m;
+  float* chol_buf = (q > 1) ? w : nullptr;
+
+  // ---- launches -------------------------------------------------------------
+  Profile::Rec* rec = nullptr;
+  {
+    Profile& P = profile();
+    std::lock_guard<std::mutex> lk(P.mu);
+    if (P.on && P.used < P.pool.size()) rec = &P.pool[P.used++];
+  }
+  if (rec) {
+    rec->launches = m;
+    hipError_t e = hipEventRecord(rec->e[0], st);
+    if (e != hipSuccess) return hip_fail(e, "bo_score: profile event");
+  }
+  for (int k = 0; k < m; ++k) {
+    PosteriorArgs pa;
+    pa.cand = cand; pa.npts = npts; pa.d = M.d; pa.dx = M.dx; pa.q = q;
+    pa.Xs = M.Xs + (size_t)k * M.n_pad * M.dx;
+    pa.invls = M.invls + (size_t)k * M.dx;
+    pa.alpha = M.alpha + (size_t)k * M.n_pad;
+    pa.Lp = M.Lp + (size_t)k * M.lp_per_obj;
+    pa.n = static_cast<int>(M.n); pa.nb = M.nb;
+    pa.s = M.os[k];
+    pa.m = m; pa.k = k;
+    pa.mu = mu_buf; pa.sd = sd_buf; pa.chol = chol_buf;
+    if ((s = after_launch(launch_posterior(pa, st), st, "posterior")) != BO_OK) return s;
+  }
+  if (rec) {
+    hipError_t e = hipEventRecord(rec->e[1], st);
+    if (e != hipSuccess) return hip_fail(e, "bo_score: profile event");
+  }
+  EhviArgs ea;
+  ea.mu = mu_buf; ea.sd = sd_buf; ea.chol = chol_buf;
+  ea.Z = base_samples; ea.boxes = M.d_boxes;
+  ea.nbat = M_; ea.q = q; ea.m = m; ea.S = S; ea.nbox = M.nbox;
+  ea.ehvi = ehvi;
+  if ((s = after_launch(launch_ehvi(ea, st), st, "ehvi")) != BO_OK) return s;
+  if (rec) {
+    hipError_t e = hipEventRecord(rec->e[2], st);
+    if (e != hipSuccess) return hip_fail(e, "bo_score: profile event");
+  }
+  M.last_stream = st;
+  return BO_OK;
+}
+
+bo_status bo_profile_enable(int32_t on) {
+  Profile& P = profile();
+  std::lock_guard<std::mutex> lk(P.mu);
+  if (on && P.pool.empty()) {
+    P.pool.resize(kProfileCap);
+    for (auto& r : P.pool)
+      for (auto& e : r.e) {
+        hipError_t err = hipEventCreate(&e);
+        if (err != hipSuccess) return hip_fail(err, "bo_profile_enable");
+      }
+  }
+  P.on = on != 0;
+  P.used = 0;
+  return BO_OK;
+}
+
+bo_status bo_profile_read(double* posterior_ms, double* ehvi_ms, int64_t* calls,
+                          int64_t* posterior_launches) {
+  if (!posterior_ms || !ehvi_ms || !calls || !posterior_launches)
+    return fail(BO_ERR_INVALID_ARGUMENT, "bo_profile_read: NULL output");
+  Profile& P = profile();
+  std::lock_guard<std::mutex> lk(P.mu);
+  double a = 0.0, b = 0.0;
+  int64_t launches = 0;
+  for (size_t i = 0; i < P.used; ++i) {
+    Profile::Rec& r = P.pool[i];
+    hipError_t e = hipEventSynchronize(r.e[2]);
+    float t01 = 0.f, t12 = 0.f;
+    if (e == hipSuccess) e = hipEventElapsedTime(&t01, r.e[0], r.e[1]);
+    if (e == hipSuccess) e = hipEventElapsedTime(&t12, r.e[1], r.e[2]);
+    if (e != hipSuccess) return hip_fail(e, "bo_profile_read");
+    a += t01;
+    b += t12;
+    launches += r.launches;
+  }
+  *posterior_ms = a;
+  *ehvi_ms = b;
+  *calls = static_cast<int64_t>(P.used);
+  *posterior_launches = launches;
+  P.used = 0;
+  return BO_OK;
+}
+
+bo_status bo_argmax(const float* values, int64_t M, int64_t* index, float* value, void* stream) {
+  if (M < 0 || M >= ((int64_t)1 << 31)) return fail(BO_ERR_INVALID_ARGUMENT, "bo_argmax: M out of range");
+  bo_status s;
+  if ((s = check_dev(index, sizeof(int64_t), "index")) != BO_OK) return s;
+  if ((s = check_dev(value, sizeof(float), "value")) != BO_OK) return s;
+  if (M > 0 && (s = check_dev(values, sizeof(float) * M, "values")) != BO_OK) return s;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  return after_launch(launch_argmax(values, M, index, value, st), st, "argmax");
+}
+
+bo_status bo_cholesky_test(const float* A, int64_t n, float* L, void* stream) {
+  if (n < 1) return fail(BO_ERR_INVALID_ARGUMENT, "bo_cholesky_test: n < 1");
+  if (n > BO_MAX_N) return fail(BO_ERR_CAPACITY, "bo_cholesky_test: n beyond limit");
+  bo_status s;
+  if ((s = check_dev(A, sizeof(float) * n * n, "A")) != BO_OK) return s;
+  if ((s = check_dev(L, sizeof(float) * n * n, "L")) != BO_OK) return s;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int nf = static_cast<int>((n + kFitBlk - 1) / kFitBlk) * kFitBlk;
+  FitScratch fs;
+  if ((s = dmalloc(&fs.A, (size_t)nf * nf, "matrix")) != BO_OK) return s;
+  if ((s = dmalloc(&fs.Dinv, (size_t)nf * kFitBlk, "block inverses")) != BO_OK) return s;
+  if ((s = dmalloc(&fs.flag, 1, "flag")) != BO_OK) return s;
+  hipError_t e = hipMemsetAsync(fs.flag, 0, sizeof(int), st);
+  if (e != hipSuccess) return hip_fail(e, "bo_cholesky_test: memset");
+  if ((s = after_launch(launch_f32_to_padded(A, n, nf, fs.A, st), st, "pad")) != BO_OK) return s;
+  if ((s = after_launch(launch_cholesky(fs.A, fs.Dinv, nf, 1, fs.flag, st), st, "cholesky")) != BO_OK) return s;
+  if ((s = after_launch(launch_lower_to_f32(fs.A, n, nf, L, st), st, "convert")) != BO_OK) return s;
+  int flag = 0;
+  e = hipMemcpyAsync(&flag, fs.flag, sizeof(int), hipMemcpyDeviceToHost, st);
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  if (e != hipSuccess) return hip_fail(e, "bo_cholesky_test: sync");
+  if (flag) return fail(BO_ERR_NOT_POSITIVE_DEFINITE, "bo_cholesky_test: non-positive pivot");
+  return BO_OK;
+}
+
+}  // extern "C"

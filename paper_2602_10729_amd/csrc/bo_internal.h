@@ -1,0 +1,131 @@
+// Internal declarations shared by the host API and the kernel launchers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "../../include/bo.h"
+
+namespace bo {
+
+// Tile geometry of the scoring path.
+constexpr int kBlk = 16;        // MFMA 16x16x4 fp32 block edge
+constexpr int kFitBlk = 64;     // Cholesky / inverse block edge (fp64)
+
+// Thread-local error detail; returns the status for chaining.
+bo_status fail(bo_status st, const std::string& msg);
+bo_status hip_fail(hipError_t e, const char* what);
+
+// Host geometry (host_geom.cpp) -------------------------------------------
+// Non-dominated rows of Y (maximise, duplicates keep the lowest index),
+// optionally only rows strictly above ref, sorted by objective 0 then index.
+void host_front(const float* Y, int64_t n, int m, const float* ref,
+                std::vector<int32_t>& out);
+// Disjoint boxes of the region the front does not dominate; lo/hi row-major
+// [count][m]; hi may be +inf.
+void host_boxes(const float* F, int P, int m, const float* ref,
+                std::vector<float>& lo, std::vector<float>& hi);
+
+// Device layout of a fitted model ----------------------------------------
+struct Model {
+  int device = 0;
+  int64_t n = 0;
+  int d = 0, m = 0;
+  int n_pad = 0;                 // n rounded up to kBlk
+  int nb = 0;                    // n_pad / kBlk
+  int dx = 0;                    // padded coordinate stride (multiple of 4)
+  std::vector<float> ls, os, noise;
+  std::vector<float> Yh;         // host copy of Y [n][m]
+  std::vector<int32_t> nd;       // non-dominated rows (no reference filter)
+
+  float* Xs = nullptr;           // [m][n_pad][dx] X / lengthscale (fp32)
+  float* invls = nullptr;        // [m][dx] 1 / lengthscale (fp32, 0-padded)
+  float* alpha = nullptr;        // [m][n_pad]
+  float* Lp = nullptr;           // [m][nb(nb+1)/2][64][4] packed L^{-1}
+  size_t lp_per_obj = 0;         // floats per objective in Lp
+
+  // scoring workspace (grown on demand)
+  float* ws = nullptr;
+  size_t ws_floats = 0;
+  // box cache (rebuilt when the reference point changes)
+  float* d_boxes = nullptr;      // [nbox][2m]: lo then width
+  int box_cap = 0;
+  int nbox = -1;
+  std::vector<float> box_ref;
+  float* h_boxes = nullptr;      // pinned staging
+  hipEvent_t box_evt = nullptr;
+  hipStream_t last_stream = nullptr;
+};
+
+// Kernel launchers (fit.hip / posterior.hip / ehvi.hip / argmax.hip) -------
+// All return hipSuccess or the launch error.
+
+// Gram matrices K_k + eta_k I in fp64 for all objectives, padded to
+// n_fit x n_fit with an identity tail. A: [m][n_fit][n_fit].
+hipError_t launch_gram(const float* X, int64_t n, int d, int m, int n_fit,
+                       const double* ls, const double* os, const double* noise,
+                       double* A, hipStream_t st);
+// Blocked right-looking Cholesky of m matrices [m][nf][nf] (lower, in place)
+// with diagonal-block inverses Dinv [m][nf/kFitBlk][kFitBlk][kFitBlk];
+// *flag is set non-zero on a non-positive or non-finite pivot.
+hipError_t launch_cholesky(double* A, double* Dinv, int nf, int m, int* flag,
+                           hipStream_t st);
+// W = L^{-1} (lower, [m][nf][nf]) from the factor and its block inverses.
+hipError_t launch_trtri(const double* A, const double* Dinv, double* W, int nf,
+                        int m, hipStream_t st);
+// alpha_k = W_k^T (W_k y_k), y from Y [n][m] (fp32), written fp32 [m][n_pad].
+hipError_t launch_alpha(const double* W, const float* Y, int64_t n, int m,
+                        int nf, int n_pad, double* tmp, float* alpha,
+                        hipStream_t st);
+// Pack W into MFMA A-fragment order (fp32, lower blocks, zeros beyond n) and
+// write the lengthscale-scaled X.
+hipError_t launch_pack(const double* W, int64_t n, int m, int nf, int nb,
+                       float* Lp, const float* X, int d, int dx,
+                       const float* invls, float* Xs, hipStream_t st);
+// Convert a fp64 [n][n] lower factor (leading dimension nf) to fp32 [n][n].
+hipError_t launch_lower_to_f32(const double* A, int64_t n, int nf, float* L,
+                               hipStream_t st);
+// Copy a fp32 [n][n] matrix into a fp64 padded [nf][nf] with identity tail.
+hipError_t launch_f32_to_padded(const float* A, int64_t n, int nf, double* P,
+                                hipStream_t st);
+
+// Posterior of one objective for npts points (q consecutive points form a
+// batch). Writes mu/var (q = 1) or mu + packed chol factor (q > 1) into the
+// workspace arrays described in posterior.hip.
+struct PosteriorArgs {
+  const float* cand;   // [npts][d]
+  int64_t npts;
+  int d, dx, q;
+  const float* Xs;     // [n_pad][dx]
+  const float* invls;  // [dx]
+  const float* alpha;  // [n_pad]
+  const float* Lp;     // packed fragments of this objective
+  int n, nb;
+  float s;             // output scale
+  int m, k;            // objective count / index (output strides)
+  float* mu;           // [npts][m]   (mu of objective k at [p*m+k])
+  float* sd;           // [npts][m]   marginal posterior std
+  float* chol;         // q > 1: [npts/q][m][q(q+1)/2] lower factor, row-major
+};
+hipError_t launch_posterior(const PosteriorArgs& a, hipStream_t st);
+
+// Monte-Carlo EHVI over boxes for nbat batches.
+struct EhviArgs {
+  const float* mu;     // [nbat*q][m]
+  const float* sd;     // [nbat*q][m]  (q = 1)
+  const float* chol;   // [nbat][m][q(q+1)/2] (q > 1)
+  const float* Z;      // [S][q][m]
+  const float* boxes;  // [nbox][2m] lo then width
+  int64_t nbat;
+  int q, m, S, nbox;
+  float* ehvi;         // [nbat]
+};
+hipError_t launch_ehvi(const EhviArgs& a, hipStream_t st);
+
+hipError_t launch_argmax(const float* v, int64_t M, int64_t* index,
+                         float* value, hipStream_t st);
+
+}  // namespace bo

@@ -1,0 +1,152 @@
+// Host-side Pareto front and box decomposition of the non-dominated region.
+//
+// The acquisition (paper, "Constrained qNEHVI" paragraph) measures the
+// hypervolume a candidate adds to the front of the observations. Both the
+// front and the region it does not dominate are small (P up to a few
+// hundred) and change once per model / reference point, so they are built
+// here on the host and shipped to the device as a flat box list.
+//
+// Front: maximisation; y_j dominates y_i when y_j >= y_i everywhere and
+// y_j != y_i; exact duplicates keep the lowest index; sorted by objective 0
+// ascending, ties by index.
+//
+// Boxes: disjoint [lo, hi) with hi possibly +inf, covering
+// {z > ref : no f in F with f >= z}.
+//   m = 2: staircase under the sorted front, P + 1 boxes.
+//   m = 3: sweep over objective 2 from the top. The active points (those at
+//   or above the current level) cast a 2-D staircase kept in an ordered map
+//   (x ascending, y descending). Inserting a point closes the boxes of the
+//   staircase steps it removes and of its right neighbour, and opens its own
+//   step and the neighbour's narrowed step; boxes that survive an insertion
+//   keep growing downwards. Every box therefore spans the z-range during
+//   which its (x, y) footprint was unchanged, and the count stays O(P).
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <limits>
+#include <map>
+#include <numeric>
+#include <vector>
+
+#include "bo_internal.h"
+
+namespace bo {
+
+void host_front(const float* Y, int64_t n, int m, const float* ref,
+                std::vector<int32_t>& out) {
+  out.clear();
+  for (int64_t i = 0; i < n; ++i) {
+    const float* yi = Y + i * m;
+    if (ref) {
+      bool above = true;
+      for (int k = 0; k < m; ++k) above = above && (yi[k] > ref[k]);
+      if (!above) continue;
+    }
+    bool keep = true;
+    for (int64_t j = 0; j < n && keep; ++j) {
+      if (j == i) continue;
+      const float* yj = Y + j * m;
+      bool ge = true, gt = false;
+      for (int k = 0; k < m; ++k) {
+        ge = ge && (yj[k] >= yi[k]);
+        gt = gt || (yj[k] > yi[k]);
+      }
+      if (ge && gt) keep = false;            // strictly dominated
+      else if (ge && !gt && j < i) keep = false;  // duplicate, keep lowest
+    }
+    if (keep) out.push_back(static_cast<int32_t>(i));
+  }
+  std::stable_sort(out.begin(), out.end(), [&](int32_t a, int32_t b) {
+    return Y[static_cast<int64_t>(a) * m] < Y[static_cast<int64_t>(b) * m];
+  });
+}
+
+namespace {
+
+constexpr float kInf = std::numeric_limits<float>::infinity();
+
+void push_box(std::vector<float>& lo, std::vector<float>& hi,
+              float l0, float l1, float l2, float h0, float h1, float h2, int m) {
+  lo.push_back(l0); lo.push_back(l1);
+  hi.push_back(h0); hi.push_back(h1);
+  if (m == 3) { lo.push_back(l2); hi.push_back(h2); }
+}
+
+}  // namespace
+
+void host_boxes(const float* F, int P, int m, const float* ref,
+                std::vector<float>& lo, std::vector<float>& hi) {
+  lo.clear();
+  hi.clear();
+  if (m == 2) {
+    // F sorted by objective 0 ascending: box i covers objective 0 in
+    // [x_{i-1}, x_i) (x_0 = ref_0) and objective 1 above y_i; the last box
+    // covers [x_P, inf) above ref_1.
+    float xlo = ref[0];
+    for (int i = 0; i < P; ++i) {
+      push_box(lo, hi, xlo, F[2 * i + 1], 0.f, F[2 * i], kInf, 0.f, 2);
+      xlo = F[2 * i];
+    }
+    push_box(lo, hi, xlo, ref[1], 0.f, kInf, kInf, 0.f, 2);
+    return;
+  }
+  // m == 3
+  std::vector<int> order(P);
+  std::iota(order.begin(), order.end(), 0);
+  std::stable_sort(order.begin(), order.end(),
+                   [&](int a, int b) { return F[3 * a + 2] > F[3 * b + 2]; });
+  struct Step { float y; float ztop; };          // box (prev.x, x) x [y, inf)
+  std::map<float, Step> stair;                    // keyed by x ascending
+  float tail_ztop = kInf;                         // box [last.x, inf) x [ref1, inf)
+  auto close = [&](float xl, float xh, float yl, float zl, float zt) {
+    if (zt > zl) push_box(lo, hi, xl, yl, zl, xh, kInf, zt, 3);
+  };
+  for (int idx : order) {
+    const float px = F[3 * idx], py = F[3 * idx + 1], zb = F[3 * idx + 2];
+    // dominated in 2-D by an active point (x >= px and y >= py)?
+    auto it = stair.lower_bound(px);              // first x >= px
+    if (it != stair.end() && it->second.y >= py) continue;
+    // predecessor chain: active points with x <= px and y <= py are removed
+    // (only those with x < px can remain here, since it->x >= px has y < py
+    // when it exists; an equal-x point with lower y is removed too)
+    auto first_rm = it;
+    if (it != stair.end() && it->first == px) {
+      // equal x, lower y: removed below together with the predecessor run
+      ++first_rm;
+    }
+    // walk left over predecessors with y <= py
+    auto left = it;
+    while (left != stair.begin()) {
+      auto prev = std::prev(left);
+      if (prev->second.y <= py) left = prev; else break;
+    }
+    // range [left, first_rm) is removed; compute the x just before it
+    float pred_x = (left == stair.begin()) ? ref[0] : std::prev(left)->first;
+    // close removed steps
+    float xl = pred_x;
+    for (auto r = left; r != first_rm; ++r) {
+      close(xl, r->first, r->second.y, zb, r->second.ztop);
+      xl = r->first;
+    }
+    // right neighbour (or the tail box) narrows from xl to px
+    if (first_rm != stair.end()) {
+      Step& s = first_rm->second;
+      close(xl, first_rm->first, s.y, zb, s.ztop);
+      s.ztop = zb;
+    } else {
+      close(xl, kInf, ref[1], zb, tail_ztop);
+      tail_ztop = zb;
+    }
+    stair.erase(left, first_rm);
+    stair[px] = Step{py, zb};
+  }
+  // close everything at ref_2
+  float xl = ref[0];
+  for (auto& kv : stair) {
+    close(xl, kv.first, kv.second.y, ref[2], kv.second.ztop);
+    xl = kv.first;
+  }
+  close(xl, kInf, ref[1], ref[2], tail_ztop);
+}
+
+}  // namespace bo

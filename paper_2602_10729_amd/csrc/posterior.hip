@@ -1,0 +1,325 @@
+// GP posterior of a batch of candidate points, one objective per launch.
+//
+// Paper: workflow step (ii) evaluates the acquisition on samples of the
+// joint posterior of the GP surrogates; the posterior of an exact GP at x*
+// is mu = k*^T alpha and Sigma = k(x*,x*) - v^T v with v = L^{-1} k*.
+//
+// One workgroup (4 waves) owns a tile of NT points:
+//   phase 1 (VALU): the cross-covariance tile K*^T [n_pad x NT] of the
+//     ARD Matern-5/2 kernel, computed from lengthscale-scaled coordinates by
+//     direct differences (no |a|^2 + |b|^2 - 2ab cancellation), written to
+//     LDS in the MFMA B-fragment order; mu = K* alpha is reduced on the fly.
+//   phase 2 (MFMA): V = L^{-1} K*^T over the lower 16x16 blocks only,
+//     row block by row block. Waves take row blocks in a snake order so the
+//     triangle is split evenly; each row block's V rows live only in the
+//     MFMA accumulators and are squared into per-column sums at once
+//     (q = 1 needs only |v|^2; q > 1 also needs the cross products of batch
+//     members, which sit in the same 4-lane group of the accumulator and
+//     are exchanged with DPP quad permutes).
+//   L^{-1} is pre-packed by the fit so each lane fetches its four A operands
+//   of a 16x16 block with one 16-byte load (1 KiB per block per wave).
+// MFMA: v_mfma_f32_16x16x4f32, A[i][k] from lane i + 16k, B[k][j] from lane
+// j + 16k, D[i][j] in lane j + 16(i/4), element i%4.
+#include <hip/hip_runtime.h>
+
+#include "bo_internal.h"
+
+namespace bo {
+namespace {
+
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+constexpr int kThreads = 256;
+constexpr int kWaves = 4;
+
+__device__ inline float matern52_f(float r2, float s) {
+  const float r = __builtin_amdgcn_sqrtf(r2);
+  // exp(-sqrt5 r) = 2^(-sqrt5 log2(e) r)
+  constexpr float kNegSqrt5Log2e = static_cast<float>(-2.23606797749978969641 * 1.44269504088896340736);
+  const float e = __builtin_amdgcn_exp2f(kNegSqrt5Log2e * r);
+  const float poly = fmaf(r, 2.23606798f, fmaf(r2, 1.66666667f, 1.0f));
+  return s * poly * e;
+}
+
+// Row block handled by a wave in round `it` (snake over the 4 waves).
+__device__ inline int snake_block(int it, int wave) {
+  return it * kWaves + ((it & 1) ? (kWaves - 1 - wave) : wave);
+}
+
+template <int Q>
+__device__ inline float quad_xor(float v, int x) {
+  // DPP quad_perm: lane i of each group of 4 reads lane i ^ x.
+  int iv = __float_as_int(v);
+  int r;
+  if (x == 1) r = __builtin_amdgcn_mov_dpp(iv, 0xB1, 0xF, 0xF, false);      // [1,0,3,2]
+  else if (x == 2) r = __builtin_amdgcn_mov_dpp(iv, 0x4E, 0xF, 0xF, false); // [2,3,0,1]
+  else r = __builtin_amdgcn_mov_dpp(iv, 0x1B, 0xF, 0xF, false);             // [3,2,1,0]
+  return __int_as_float(r);
+}
+
+template <int NT, int DX4, int Q>
+__global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
+  extern __shared__ float smem[];
+  constexpr int NCB = NT / 16;          // 16-column blocks per tile
+  constexpr int NX = (Q > 1) ? Q : 1;   // per-point partial slots (diag + xors)
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int n_pad = a.nb * kBlk;
+  float* Kt = smem;                                  // n_pad * NT
+  float* red = smem + (size_t)n_pad * NT;            // kWaves * NT * NX
+  float* mured = red + kWaves * NT * NX;             // kThreads
+  float* kpp = mured + kThreads;                     // NT * 4 (prior cross-cov)
+  const int64_t p0 = (int64_t)blockIdx.x * NT;
+
+  // ---- phase 1: K*^T tile into LDS, mu partials -------------------------
+  const int col = tid % NT;
+  const int64_t p = p0 + col;
+  const bool valid = p < a.npts;
+  float c[DX4 * 4];
+#pragma unroll
+  for (int t = 0; t < DX4 * 4; ++t) c[t] = 0.f;
+  if (valid) {
+    const float* cp = a.cand + p * a.d;
+#pragma unroll
+    for (int t = 0; t < DX4 * 4; ++t)
+      if (t < a.d) c[t] = cp[t] * a.invls[t];
+  }
+  float mu_part = 0.f;
+  const int cb = col >> 4;
+  for (int row = tid / NT; row < n_pad; row += kThreads / NT) {
+    const float4* xr = reinterpret_cast<const float4*>(a.Xs + (size_t)row * a.dx);
+    float r2 = 0.f;
+#pragma unroll
+    for (int t4 = 0; t4 < DX4; ++t4) {
+      const float4 x = xr[t4];
+      const float d0 = c[4 * t4 + 0] - x.x;
+      const float d1 = c[4 * t4 + 1] - x.y;
+      const float d2 = c[4 * t4 + 2] - x.z;
+      const float d3 = c[4 * t4 + 3] - x.w;
+      r2 = fmaf(d0, d0, r2);
+      r2 = fmaf(d1, d1, r2);
+      r2 = fmaf(d2, d2, r2);
+      r2 = fmaf(d3, d3, r2);
+    }
+    float kv = 0.f;
+    if (valid && row < a.n) kv = matern52_f(r2, a.s);
+    mu_part = fmaf(a.alpha[row], kv, mu_part);
+    const int J = row >> 4, r16 = row & 15;
+    const int ln = (r16 & 3) * 16 + (col & 15);
+    Kt[(((J * NCB + cb) * 64 + ln) << 2) + (r16 >> 2)] = kv;
+  }
+  mured[tid] = mu_part;
+  if (Q > 1 && tid < NT) {
+    // prior covariance of this point with its batch mates (point ^ x)
+    for (int x = 1; x < Q; ++x) {
+      const int64_t pm = p ^ x;
+      float r2 = 0.f;
+      if (valid && pm < a.npts) {
+        const float* cp = a.cand + pm * a.d;
+#pragma unroll
+        for (int t = 0; t < DX4 * 4; ++t)
+          if (t < a.d) {
+            const float dd = c[t] - cp[t] * a.invls[t];
+            r2 = fmaf(dd, dd, r2);
+          }
+      }
+      kpp[tid * 4 + x] = matern52_f(r2, a.s);
+    }
+  }
+  __syncthreads();
+
+  // ---- phase 2: V = L^{-1} K*^T on MFMA, squared on the fly ---------------
+  float ss[NCB];
+  float gx[NCB][NX];
+#pragma unroll
+  for (int b = 0; b < NCB; ++b) {
+    ss[b] = 0.f;
+#pragma unroll
+    for (int x = 0; x < NX; ++x) gx[b][x] = 0.f;
+  }
+  const float4* Lp4 = reinterpret_cast<const float4*>(a.Lp);
+  const float4* Kt4 = reinterpret_cast<const float4*>(Kt);
+  for (int it = 0;; ++it) {
+    const int I = snake_block(it, wave);
+    if (I >= a.nb) break;
+    floatx4 acc[NCB];
+#pragma unroll
+    for (int b = 0; b < NCB; ++b) acc[b] = floatx4{0.f, 0.f, 0.f, 0.f};
+    const float4* Ablk = Lp4 + (size_t)I * (I + 1) / 2 * 64 + lane;
+    float4 av = Ablk[0];
+    for (int J = 0; J <= I; ++J) {
+      const float4 cur = av;
+      if (J < I) av = Ablk[(size_t)(J + 1) * 64];
+#pragma unroll
+      for (int b = 0; b < NCB; ++b) {
+        const float4 bv = Kt4[(J * NCB + b) * 64 + lane];
+        acc[b] = __builtin_amdgcn_mfma_f32_16x16x4f32(cur.x, bv.x, acc[b], 0, 0, 0);
+        acc[b] = __builtin_amdgcn_mfma_f32_16x16x4f32(cur.y, bv.y, acc[b], 0, 0, 0);
+        acc[b] = __builtin_amdgcn_mfma_f32_16x16x4f32(cur.z, bv.z, acc[b], 0, 0, 0);
+        acc[b] = __builtin_amdgcn_mfma_f32_16x16x4f32(cur.w, bv.w, acc[b], 0, 0, 0);
+      }
+    }
+#pragma unroll
+    for (int b = 0; b < NCB; ++b) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float v = acc[b][r];
+        ss[b] = fmaf(v, v, ss[b]);
+        if (Q > 1) {
+#pragma unroll
+          for (int x = 1; x < NX; ++x) gx[b][x] = fmaf(v, quad_xor<Q>(v, x), gx[b][x]);
+        }
+      }
+    }
+  }
+  // reduce over the four 16-lane row groups, then over waves in LDS
+#pragma unroll
+  for (int b = 0; b < NCB; ++b) {
+    ss[b] += __shfl_xor(ss[b], 16);
+    ss[b] += __shfl_xor(ss[b], 32);
+#pragma unroll
+    for (int x = 1; x < NX; ++x) {
+      gx[b][x] += __shfl_xor(gx[b][x], 16);
+      gx[b][x] += __shfl_xor(gx[b][x], 32);
+    }
+    if (lane < 16) {
+      const int cc = b * 16 + lane;
+      red[(wave * NT + cc) * NX + 0] = ss[b];
+#pragma unroll
+      for (int x = 1; x < NX; ++x) red[(wave * NT + cc) * NX + x] = gx[b][x];
+    }
+  }
+  __syncthreads();
+
+  // ---- epilogue -------------------------------------------------------------
+  if (tid < NT) {
+    float tot[NX];
+#pragma unroll
+    for (int x = 0; x < NX; ++x) tot[x] = 0.f;
+    for (int w = 0; w < kWaves; ++w)
+#pragma unroll
+      for (int x = 0; x < NX; ++x) tot[x] += red[(w * NT + tid) * NX + x];
+    float mu = 0.f;
+    for (int i = tid; i < kThreads; i += NT) mu += mured[i];
+    const float var = a.s - tot[0];
+    if (valid) {
+      a.mu[p * a.m + a.k] = mu;
+      a.sd[p * a.m + a.k] = __builtin_amdgcn_sqrtf(fmaxf(var, 0.f));
+    }
+    if (Q > 1) {
+      // covariance row of this point (diagonal, then partner p ^ x) for the
+      // batch owner; each thread rewrites only its own kpp slots
+      kpp[tid * 4 + 0] = var;
+#pragma unroll
+      for (int x = 1; x < NX; ++x) kpp[tid * 4 + x] -= tot[x];
+    }
+  }
+  if (Q > 1) {
+    __syncthreads();
+    constexpr int NB = NT / Q;
+    if (tid < NB) {
+      const int64_t bat = (int64_t)blockIdx.x * NB + tid;
+      if (bat * Q < a.npts) {
+        float S[Q][Q];
+#pragma unroll
+        for (int i = 0; i < Q; ++i)
+#pragma unroll
+          for (int j = 0; j < Q; ++j)
+            S[i][j] = (i == j) ? kpp[(tid * Q + i) * 4 + 0] : kpp[(tid * Q + i) * 4 + (i ^ j)];
+        float C[Q][Q];
+#pragma unroll
+        for (int i = 0; i < Q; ++i)
+#pragma unroll
+          for (int j = 0; j < Q; ++j) C[i][j] = 0.f;
+        const float tol = 1e-10f * a.s;
+#pragma unroll
+        for (int j = 0; j < Q; ++j) {
+          float pv = S[j][j];
+#pragma unroll
+          for (int t = 0; t < j; ++t) pv = fmaf(-C[j][t], C[j][t], pv);
+          if (pv > tol) {
+            const float cjj = __builtin_amdgcn_sqrtf(pv);
+            C[j][j] = cjj;
+            const float inv = 1.0f / cjj;
+#pragma unroll
+            for (int i = j + 1; i < Q; ++i) {
+              float num = S[i][j];
+#pragma unroll
+              for (int t = 0; t < j; ++t) num = fmaf(-C[i][t], C[j][t], num);
+              C[i][j] = num * inv;
+            }
+          }
+        }
+        constexpr int T = Q * (Q + 1) / 2;
+        float* dst = a.chol + (bat * a.m + a.k) * T;
+#pragma unroll
+        for (int i = 0; i < Q; ++i)
+#pragma unroll
+          for (int j = 0; j <= i; ++j) dst[i * (i + 1) / 2 + j] = C[i][j];
+      }
+    }
+  }
+}
+
+template <int NT, int DX4, int Q>
+hipError_t launch_t(const PosteriorArgs& a, hipStream_t st) {
+  const int n_pad = a.nb * kBlk;
+  const size_t lds = sizeof(float) * ((size_t)n_pad * NT + kWaves * NT * ((Q > 1) ? Q : 1) +
+                                      kThreads + NT * 4);
+  static bool attr_set = false;
+  if (!attr_set) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_posterior<NT, DX4, Q>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       static_cast<int>(160 * 1024));
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  const unsigned grid = static_cast<unsigned>((a.npts + NT - 1) / NT);
+  hipLaunchKernelGGL((k_posterior<NT, DX4, Q>), dim3(grid), dim3(kThreads), lds, st, a);
+  return hipGetLastError();
+}
+
+template <int NT, int Q>
+hipError_t launch_dx(const PosteriorArgs& a, hipStream_t st) {
+  switch (a.dx / 4) {
+    case 1: return launch_t<NT, 1, Q>(a, st);
+    case 2: return launch_t<NT, 2, Q>(a, st);
+    case 3: return launch_t<NT, 3, Q>(a, st);
+    case 4: return launch_t<NT, 4, Q>(a, st);
+    case 5: return launch_t<NT, 5, Q>(a, st);
+    case 6: return launch_t<NT, 6, Q>(a, st);
+    case 7: return launch_t<NT, 7, Q>(a, st);
+    case 8: return launch_t<NT, 8, Q>(a, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+template <int NT>
+hipError_t launch_q(const PosteriorArgs& a, hipStream_t st) {
+  switch (a.q) {
+    case 1: return launch_dx<NT, 1>(a, st);
+    case 2: return launch_dx<NT, 2>(a, st);
+    case 4: return launch_dx<NT, 4>(a, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace
+
+// Tile width: 32 points when K*^T fits LDS with room to spare, else 16.
+int posterior_tile(int nb) { return (nb * kBlk <= 1024) ? 32 : 16; }
+
+size_t posterior_lds_bytes(int nb, int q) {
+  const int NT = posterior_tile(nb);
+  return sizeof(float) * ((size_t)nb * kBlk * NT + kWaves * NT * ((q > 1) ? q : 1) +
+                          kThreads + NT * 4);
+}
+
+hipError_t launch_posterior(const PosteriorArgs& a, hipStream_t st) {
+  if (a.npts <= 0) return hipSuccess;
+  if (posterior_tile(a.nb) == 32) return launch_q<32>(a, st);
+  return launch_q<16>(a, st);
+}
+
+}  // namespace bo

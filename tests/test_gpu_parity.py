@@ -1,0 +1,225 @@
+"""GPU parity: the HIP path through the C ABI against the fp64 oracle.
+
+Every case prints its name, seed and shape before touching the GPU so a
+failing run identifies itself.
+"""
+import numpy as np
+import pytest
+
+import bo_inputs as bi
+import oracle as O
+from gpu_util import (TOL_MU, TOL_SIGMA, TOL_EHVI, gpu_run, oracle_fit,
+                      oracle_score, assert_close, check_argmax, to_dev)
+
+pytestmark = pytest.mark.gpu
+
+
+def _announce(*a):
+    print("[case]", *a, flush=True)
+
+
+def _full_parity(wl, g, o):
+    assert np.array_equal(g["front"], O.nondominated(wl.Y.astype(np.float64))[
+        np.argsort(wl.Y.astype(np.float64)[O.nondominated(wl.Y.astype(np.float64)), 0], kind="stable")])
+    assert_close(g["mu"], o["mu"], TOL_MU, "mu")
+    assert_close(g["sigma"], o["sigma"], TOL_SIGMA, "sigma")
+    assert_close(g["ehvi"], o["ehvi"], TOL_EHVI, "ehvi")
+    check_argmax(g["idx"], o["ehvi"])
+    assert g["val"] == g["ehvi"][g["idx"]]
+
+
+# configs at sizes the oracle finishes in seconds; M chosen ragged against
+# the 16/32-point tiles and the 256-candidate EHVI blocks
+SMALL = [(0, 4096), (1, 3001), (2, 2003), (4, 61)]
+
+
+@pytest.mark.parametrize("cfg,M", SMALL)
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_small_config_parity(cfg, M, seed):
+    if cfg == 4 and seed == 2:
+        pytest.skip("config 4 checked on seeds 0 and 1 (oracle cost)")
+    _announce("small", cfg, seed, M)
+    wl = bi.make_config(cfg, seed=seed, M=M)
+    g = gpu_run(wl)
+    o = oracle_score(oracle_fit(wl), wl)
+    _full_parity(wl, g, o)
+
+
+def test_config1_full_size_elementwise():
+    _announce("config1 full", 0)
+    wl = bi.make_config(1, seed=0)
+    g = gpu_run(wl)
+    o = oracle_score(oracle_fit(wl), wl)
+    _full_parity(wl, g, o)
+
+
+def _sampled_full_size(cfg, nsample, seed=0):
+    wl = bi.make_config(cfg, seed=seed)
+    g = gpu_run(wl)
+    M = wl.M
+    tile = 32 if wl.n <= 1024 else 16
+    pts_per_tile = tile // wl.q
+    r = np.random.default_rng(99)
+    edges = [0, 1, M - 1, M - 2, pts_per_tile - 1, pts_per_tile, 255, 256, M // 2]
+    idx = np.unique(np.concatenate([edges, r.integers(0, M, nsample)]))
+    model = oracle_fit(wl)
+    o = oracle_score(model, wl, cand=wl.cand[idx])
+    assert_close(g["mu"][idx], o["mu"], TOL_MU, "mu (sampled)")
+    assert_close(g["sigma"][idx], o["sigma"], TOL_SIGMA, "sigma (sampled)")
+    assert_close(g["ehvi"][idx], o["ehvi"], TOL_EHVI, "ehvi (sampled)")
+    # argmax: any candidate the oracle could rank first has a GPU value
+    # within the EHVI tolerance of the GPU maximum; score that pool exactly
+    e = g["ehvi"].astype(np.float64)
+    top = e.max()
+    pool = np.nonzero(e >= top - 2 * (TOL_EHVI[0] * abs(top) + TOL_EHVI[1]) - 1e-3 * abs(top))[0]
+    assert pool.size < 4096, pool.size
+    op = oracle_score(model, wl, cand=wl.cand[pool])
+    assert_close(e[pool], op["ehvi"], TOL_EHVI, "ehvi (top pool)")
+    check_argmax(g["idx"], op["ehvi"], idx_pool=pool)
+    assert g["idx"] == int(np.argmax(g["ehvi"]))
+    return wl, g
+
+
+def test_config2_full_size_sampled():
+    _announce("config2 full sampled", 0)
+    _sampled_full_size(2, 400)
+
+
+def test_config3_full_size_sampled():
+    _announce("config3 full sampled", 0)
+    _sampled_full_size(3, 400)
+
+
+def test_config4_full_size_sampled():
+    _announce("config4 full sampled", 0)
+    _sampled_full_size(4, 12)
+
+
+def test_near_data_candidates():
+    """Candidates at distance ~0.01 from observations: large k*, the solve
+    does real work and sigma approaches the noise level. sigma is compared
+    through the variance with an absolute bound derived from fp32 rounding
+    of |v|^2 ~ 1 (see DESIGN)."""
+    for cfg in (0, 2):
+        _announce("near-data", cfg)
+        wl = bi.make_config(cfg, seed=0, M=8)
+        cand = bi.near_data_candidates(wl, 512, scale=0.01)
+        g = gpu_run(wl, cand=cand)
+        o = oracle_score(oracle_fit(wl), wl, cand=cand)
+        assert_close(g["mu"], o["mu"], TOL_MU, "mu near data")
+        var_tol = (1e-4, 4e-6 * (wl.n ** 0.5) / 32.0 * 8)
+        assert_close(g["sigma"] ** 2, o["sigma"] ** 2, var_tol, "variance near data")
+        # EHVI is a smooth function of (mu, sigma): same relative bar
+        assert_close(g["ehvi"], o["ehvi"], (2e-3, 1e-5), "ehvi near data")
+
+
+def test_small_models_and_odd_shapes():
+    r = np.random.default_rng(5)
+    for n, d in [(1, 3), (2, 1), (37, 5), (130, 7), (17, 32)]:
+        _announce("odd shape", n, d)
+        wl = bi.make_config(0, seed=1, M=50)
+        X = r.random((n, d)).astype(np.float32)
+        Y = r.standard_normal((n, 2)).astype(np.float32)
+        wl.X, wl.Y, wl.d, wl.n = X, Y, d, n
+        wl.lengthscale = r.uniform(0.2, 0.8, size=(2, d)).astype(np.float32)
+        wl.cand = r.random((77, 1, d)).astype(np.float32)
+        wl.ref = (Y.astype(np.float64).min(0) - 0.1).astype(np.float32)
+        g = gpu_run(wl)
+        o = oracle_score(oracle_fit(wl), wl)
+        assert_close(g["mu"], o["mu"], TOL_MU, f"mu n={n} d={d}")
+        assert_close(g["sigma"], o["sigma"], TOL_SIGMA, f"sigma n={n} d={d}")
+        assert_close(g["ehvi"], o["ehvi"], TOL_EHVI, f"ehvi n={n} d={d}")
+
+
+def test_q2_path_and_three_objectives_q1():
+    """q = 2 (pairs) with m = 2, and m = 3 with q = 1, built from config 4's
+    observations."""
+    base = bi.make_config(4, seed=0, M=16)
+    r = np.random.default_rng(3)
+    for q, m in [(2, 2), (1, 3), (2, 3), (4, 2)]:
+        _announce("q/m variant", q, m)
+        wl = bi.make_config(4, seed=0, M=16)
+        wl.Y = base.Y[:, :m].copy()
+        wl.m = m
+        wl.lengthscale = base.lengthscale[:m].copy()
+        wl.outputscale = base.outputscale[:m].copy()
+        wl.noise = base.noise[:m].copy()
+        wl.ref = (wl.Y.astype(np.float64).min(0) - 0.1).astype(np.float32)
+        wl.q = q
+        wl.cand = r.random((40, q, wl.d)).astype(np.float32)
+        wl.Z = r.standard_normal((256, q, m)).astype(np.float32)
+        g = gpu_run(wl)
+        o = oracle_score(oracle_fit(wl), wl)
+        assert_close(g["mu"], o["mu"], TOL_MU, "mu")
+        assert_close(g["sigma"], o["sigma"], TOL_SIGMA, "sigma")
+        assert_close(g["ehvi"], o["ehvi"], TOL_EHVI, "ehvi")
+
+
+def test_q4_marginals_match_q1_path():
+    _announce("q4 vs q1 marginals")
+    wl = bi.make_config(4, seed=1, M=40)
+    g4 = gpu_run(wl)
+    flat = wl.cand.reshape(-1, 1, wl.d)
+    Z1 = wl.Z[:, :1, :].copy()
+    g1 = gpu_run(wl, cand=flat, Z=Z1)
+    np.testing.assert_allclose(g4["mu"].reshape(-1, wl.m), g1["mu"][:, 0, :], rtol=0, atol=0)
+    np.testing.assert_allclose(g4["sigma"].reshape(-1, wl.m), g1["sigma"][:, 0, :], rtol=1e-5, atol=1e-6)
+
+
+def test_empty_front_and_extreme_reference():
+    _announce("empty front")
+    wl = bi.make_config(0, seed=0, M=300)
+    ref = (wl.Y.astype(np.float64).max(0) + 0.5).astype(np.float32)   # above every point
+    g = gpu_run(wl, ref=ref)
+    o = oracle_score(oracle_fit(wl), wl, ref=ref)
+    assert o["lo"].shape[0] == 1
+    assert_close(g["ehvi"], o["ehvi"], TOL_EHVI, "ehvi with empty front")
+
+
+def test_single_sample_and_single_candidate():
+    _announce("S=1, M=1")
+    wl = bi.make_config(1, seed=2, M=1)
+    Z = wl.Z[:1].copy()
+    g = gpu_run(wl, Z=Z)
+    o = oracle_score(oracle_fit(wl), wl, Z=Z)
+    assert_close(g["ehvi"], o["ehvi"], TOL_EHVI, "ehvi S=1")
+    assert g["idx"] == 0
+
+
+def test_zero_candidates_is_noop():
+    import torch
+    import paper_2602_10729_amd as bo
+    _announce("M=0")
+    wl = bi.make_config(0, seed=0, M=4)
+    model = bo.fit(to_dev(wl.X), to_dev(wl.Y), wl.lengthscale, wl.outputscale, wl.noise)
+    cand = torch.empty((0, 1, wl.d), dtype=torch.float32, device="cuda")
+    e = bo.score(model, cand, wl.ref, to_dev(wl.Z))
+    idx, val = bo.argmax(e)
+    torch.cuda.synchronize()
+    assert e.numel() == 0 and int(idx.item()) == -1 and np.isnan(float(val.item()))
+
+
+def test_deterministic_repeat():
+    _announce("determinism cfg2")
+    wl = bi.make_config(2, seed=0, M=5000)
+    a = gpu_run(wl)
+    b = gpu_run(wl)
+    for k in ("mu", "sigma", "ehvi"):
+        assert np.array_equal(a[k], b[k]), k
+    assert a["idx"] == b["idx"]
+
+
+def test_score_reuses_model_with_new_reference_point():
+    import torch
+    import paper_2602_10729_amd as bo
+    _announce("ref change")
+    wl = bi.make_config(0, seed=0, M=500)
+    model = bo.fit(to_dev(wl.X), to_dev(wl.Y), wl.lengthscale, wl.outputscale, wl.noise)
+    om = oracle_fit(wl)
+    c, z = to_dev(wl.cand), to_dev(wl.Z)
+    for shift in (0.0, 0.3, -0.2, 0.0):
+        ref = (wl.ref + shift).astype(np.float32)
+        e = bo.score(model, c, ref, z)
+        torch.cuda.synchronize()
+        o = oracle_score(om, wl, ref=ref)
+        assert_close(e.cpu().numpy(), o["ehvi"], TOL_EHVI, f"ehvi ref shift {shift}")
