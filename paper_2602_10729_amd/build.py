@@ -27,8 +27,7 @@ COMMON = [
     "-Wall", "-Wno-unused-result",
     "-I", os.path.join(ROOT, "include"),
 ]
-DEVICE_ONLY = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-               "-munsafe-fp-atomics"]
+DEVICE_ONLY = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 
 
 def hipcc() -> str:
@@ -46,9 +45,9 @@ def sources():
     return out
 
 
-def _compile(src: str, verbose: bool) -> str:
-    obj = os.path.join(BUILD, os.path.basename(src) + ".o")
-    cmd = [hipcc()] + COMMON
+def _compile(src: str, verbose: bool, extra=(), bdir=BUILD) -> str:
+    obj = os.path.join(bdir, os.path.basename(src) + ".o")
+    cmd = [hipcc()] + COMMON + list(extra)
     if src.endswith(".hip"):
         cmd += DEVICE_ONLY + ["-x", "hip"]
     cmd += ["-c", src, "-o", obj]
@@ -65,28 +64,35 @@ def _compile(src: str, verbose: bool) -> str:
     return obj
 
 
-def build(jobs: int = 8, verbose: bool = False) -> str:
-    os.makedirs(BUILD, exist_ok=True)
+def build(jobs: int = 8, verbose: bool = False, extra_flags=(), out: str = LIB,
+          build_dir: str = BUILD) -> str:
+    """Compile every source and link ``out``. ``extra_flags`` (e.g. -D tuning
+    macros) are added to every compile line."""
+    os.makedirs(build_dir, exist_ok=True)
     srcs = sources()
     with cf.ThreadPoolExecutor(max_workers=max(1, jobs)) as ex:
-        objs = list(ex.map(lambda s: _compile(s, verbose), srcs))
-    tmp = LIB + ".tmp"
+        objs = list(ex.map(lambda s: _compile(s, verbose, extra_flags, build_dir), srcs))
+    tmp = out + ".tmp"
     cmd = [hipcc(), "-shared", "-fPIC", f"--offload-arch={ARCH}", "-o", tmp] + objs
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed\n{r.stdout}\n{r.stderr}")
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, out)
+    return out
 
 
 def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--jobs", type=int, default=min(8, os.cpu_count() or 1))
     ap.add_argument("--verbose", action="store_true")
+    ap.add_argument("-D", dest="defines", action="append", default=[],
+                    help="extra preprocessor definition, e.g. -D BO_POST_WAVES=4")
+    ap.add_argument("--out", default=LIB)
+    ap.add_argument("--build-dir", default=BUILD)
     a = ap.parse_args(argv)
-    print(build(a.jobs, a.verbose))
+    print(build(a.jobs, a.verbose, ["-D" + d for d in a.defines], a.out, a.build_dir))
 
 
 if __name__ == "__main__":

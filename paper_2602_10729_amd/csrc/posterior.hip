@@ -29,8 +29,20 @@ namespace {
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
-constexpr int kThreads = 256;
-constexpr int kWaves = 4;
+// Compile-time tuning of the posterior kernel (set with -D at build time).
+#ifndef BO_POST_WAVES
+#define BO_POST_WAVES 8      // waves per workgroup (2 per SIMD)
+#endif
+#ifndef BO_POST_PF
+#define BO_POST_PF 4         // L^{-1} fragments in flight per wave
+#endif
+#ifndef BO_POST_NT_SMALL_N
+#define BO_POST_NT_SMALL_N 32  // points per tile when n_pad <= 1024
+#endif
+constexpr int kWaves = BO_POST_WAVES;
+constexpr int kThreads = 64 * kWaves;
+constexpr int kPF = BO_POST_PF;
+constexpr int kCpt = 4;              // tile columns per thread in phase 1
 
 __device__ inline float matern52_f(float r2, float s) {
   const float r = __builtin_amdgcn_sqrtf(r2);
@@ -41,12 +53,12 @@ __device__ inline float matern52_f(float r2, float s) {
   return s * poly * e;
 }
 
-// Row block handled by a wave in round `it` (snake over the 4 waves).
+// Row block handled by a wave in round `it` (snake over the waves, so every
+// wave's share of the lower triangle is the same up to one block).
 __device__ inline int snake_block(int it, int wave) {
   return it * kWaves + ((it & 1) ? (kWaves - 1 - wave) : wave);
 }
 
-template <int Q>
 __device__ inline float quad_xor(float v, int x) {
   // DPP quad_perm: lane i of each group of 4 reads lane i ^ x.
   int iv = __float_as_int(v);
@@ -57,74 +69,115 @@ __device__ inline float quad_xor(float v, int x) {
   return __int_as_float(r);
 }
 
+template <int NCB>
+__device__ inline void mfma_block(const float4 av, const float4* __restrict__ bptr,
+                                  floatx4 (&acc)[NCB]) {
+#pragma unroll
+  for (int b = 0; b < NCB; ++b) {
+    const float4 bv = bptr[b * 64];
+    acc[b] = __builtin_amdgcn_mfma_f32_16x16x4f32(av.x, bv.x, acc[b], 0, 0, 0);
+    acc[b] = __builtin_amdgcn_mfma_f32_16x16x4f32(av.y, bv.y, acc[b], 0, 0, 0);
+    acc[b] = __builtin_amdgcn_mfma_f32_16x16x4f32(av.z, bv.z, acc[b], 0, 0, 0);
+    acc[b] = __builtin_amdgcn_mfma_f32_16x16x4f32(av.w, bv.w, acc[b], 0, 0, 0);
+  }
+}
+
 template <int NT, int DX4, int Q>
 __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
   extern __shared__ float smem[];
   constexpr int NCB = NT / 16;          // 16-column blocks per tile
   constexpr int NX = (Q > 1) ? Q : 1;   // per-point partial slots (diag + xors)
+  constexpr int NCG = NT / kCpt;        // column groups in phase 1
+  constexpr int RL = kThreads / NCG;    // row lanes in phase 1
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int n_pad = a.nb * kBlk;
   float* Kt = smem;                                  // n_pad * NT
   float* red = smem + (size_t)n_pad * NT;            // kWaves * NT * NX
-  float* mured = red + kWaves * NT * NX;             // kThreads
-  float* kpp = mured + kThreads;                     // NT * 4 (prior cross-cov)
+  float* mured = red + kWaves * NT * NX;             // kThreads * kCpt
+  float* kpp = mured + kThreads * kCpt;              // NT * 4 (prior cross-cov)
   const int64_t p0 = (int64_t)blockIdx.x * NT;
 
   // ---- phase 1: K*^T tile into LDS, mu partials -------------------------
-  const int col = tid % NT;
-  const int64_t p = p0 + col;
-  const bool valid = p < a.npts;
-  float c[DX4 * 4];
+  // thread = (row lane rl, column group cg): kCpt candidates held in
+  // registers, one training point fetched per row and reused kCpt times.
+  {
+    const int cg = tid % NCG;
+    const int rl = tid / NCG;
+    float c[kCpt][DX4 * 4];
+    bool valid[kCpt];
 #pragma unroll
-  for (int t = 0; t < DX4 * 4; ++t) c[t] = 0.f;
-  if (valid) {
-    const float* cp = a.cand + p * a.d;
+    for (int u = 0; u < kCpt; ++u) {
+      const int64_t p = p0 + cg * kCpt + u;
+      valid[u] = p < a.npts;
 #pragma unroll
-    for (int t = 0; t < DX4 * 4; ++t)
-      if (t < a.d) c[t] = cp[t] * a.invls[t];
-  }
-  float mu_part = 0.f;
-  const int cb = col >> 4;
-  for (int row = tid / NT; row < n_pad; row += kThreads / NT) {
-    const float4* xr = reinterpret_cast<const float4*>(a.Xs + (size_t)row * a.dx);
-    float r2 = 0.f;
-#pragma unroll
-    for (int t4 = 0; t4 < DX4; ++t4) {
-      const float4 x = xr[t4];
-      const float d0 = c[4 * t4 + 0] - x.x;
-      const float d1 = c[4 * t4 + 1] - x.y;
-      const float d2 = c[4 * t4 + 2] - x.z;
-      const float d3 = c[4 * t4 + 3] - x.w;
-      r2 = fmaf(d0, d0, r2);
-      r2 = fmaf(d1, d1, r2);
-      r2 = fmaf(d2, d2, r2);
-      r2 = fmaf(d3, d3, r2);
-    }
-    float kv = 0.f;
-    if (valid && row < a.n) kv = matern52_f(r2, a.s);
-    mu_part = fmaf(a.alpha[row], kv, mu_part);
-    const int J = row >> 4, r16 = row & 15;
-    const int ln = (r16 & 3) * 16 + (col & 15);
-    Kt[(((J * NCB + cb) * 64 + ln) << 2) + (r16 >> 2)] = kv;
-  }
-  mured[tid] = mu_part;
-  if (Q > 1 && tid < NT) {
-    // prior covariance of this point with its batch mates (point ^ x)
-    for (int x = 1; x < Q; ++x) {
-      const int64_t pm = p ^ x;
-      float r2 = 0.f;
-      if (valid && pm < a.npts) {
-        const float* cp = a.cand + pm * a.d;
+      for (int t = 0; t < DX4 * 4; ++t) c[u][t] = 0.f;
+      if (valid[u]) {
+        const float* cp = a.cand + p * a.d;
 #pragma unroll
         for (int t = 0; t < DX4 * 4; ++t)
-          if (t < a.d) {
-            const float dd = c[t] - cp[t] * a.invls[t];
-            r2 = fmaf(dd, dd, r2);
-          }
+          if (t < a.d) c[u][t] = cp[t] * a.invls[t];
       }
-      kpp[tid * 4 + x] = matern52_f(r2, a.s);
+    }
+    float mu_part[kCpt];
+#pragma unroll
+    for (int u = 0; u < kCpt; ++u) mu_part[u] = 0.f;
+    const int col0 = cg * kCpt;
+    const int cb = col0 >> 4;
+    for (int row = rl; row < n_pad; row += RL) {
+      const float4* xr = reinterpret_cast<const float4*>(a.Xs + (size_t)row * a.dx);
+      float4 x[DX4];
+#pragma unroll
+      for (int t4 = 0; t4 < DX4; ++t4) x[t4] = xr[t4];
+      const float al = a.alpha[row];
+      const bool live = row < a.n;
+      const int J = row >> 4, r16 = row & 15;
+      float* dst = Kt + ((((J * NCB + cb) * 64 + (r16 & 3) * 16 + (col0 & 15)) << 2) + (r16 >> 2));
+#pragma unroll
+      for (int u = 0; u < kCpt; ++u) {
+        float r2 = 0.f;
+#pragma unroll
+        for (int t4 = 0; t4 < DX4; ++t4) {
+          const float d0 = c[u][4 * t4 + 0] - x[t4].x;
+          const float d1 = c[u][4 * t4 + 1] - x[t4].y;
+          const float d2 = c[u][4 * t4 + 2] - x[t4].z;
+          const float d3 = c[u][4 * t4 + 3] - x[t4].w;
+          r2 = fmaf(d0, d0, r2);
+          r2 = fmaf(d1, d1, r2);
+          r2 = fmaf(d2, d2, r2);
+          r2 = fmaf(d3, d3, r2);
+        }
+        const float kv = (valid[u] && live) ? matern52_f(r2, a.s) : 0.f;
+        mu_part[u] = fmaf(al, kv, mu_part[u]);
+        dst[u * 4] = kv;          // next column: next lane slot (4 floats on)
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kCpt; ++u) mured[(rl * NCG + cg) * kCpt + u] = mu_part[u];
+    if (Q > 1) {
+      // prior covariance of each point with its batch mates (point ^ x)
+#pragma unroll
+      for (int u = 0; u < kCpt; ++u) {
+        const int colu = col0 + u;
+        if (rl == 0) {
+          const int64_t p = p0 + colu;
+          for (int x = 1; x < Q; ++x) {
+            const int64_t pm = p ^ x;
+            float r2 = 0.f;
+            if (valid[u] && pm < a.npts) {
+              const float* cp = a.cand + pm * a.d;
+#pragma unroll
+              for (int t = 0; t < DX4 * 4; ++t)
+                if (t < a.d) {
+                  const float dd = c[u][t] - cp[t] * a.invls[t];
+                  r2 = fmaf(dd, dd, r2);
+                }
+            }
+            kpp[colu * 4 + x] = matern52_f(r2, a.s);
+          }
+        }
+      }
     }
   }
   __syncthreads();
@@ -139,27 +192,31 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
     for (int x = 0; x < NX; ++x) gx[b][x] = 0.f;
   }
   const float4* Lp4 = reinterpret_cast<const float4*>(a.Lp);
-  const float4* Kt4 = reinterpret_cast<const float4*>(Kt);
+  const float4* Kt4 = reinterpret_cast<const float4*>(Kt) + lane;
   for (int it = 0;; ++it) {
     const int I = snake_block(it, wave);
     if (I >= a.nb) break;
     floatx4 acc[NCB];
 #pragma unroll
     for (int b = 0; b < NCB; ++b) acc[b] = floatx4{0.f, 0.f, 0.f, 0.f};
+    // row block I of L^{-1}: blocks (I, 0..I), 1 KiB each, consecutive
     const float4* Ablk = Lp4 + (size_t)I * (I + 1) / 2 * 64 + lane;
-    float4 av = Ablk[0];
-    for (int J = 0; J <= I; ++J) {
-      const float4 cur = av;
-      if (J < I) av = Ablk[(size_t)(J + 1) * 64];
+    const int nJ = I + 1;
+    float4 ring[kPF];
 #pragma unroll
-      for (int b = 0; b < NCB; ++b) {
-        const float4 bv = Kt4[(J * NCB + b) * 64 + lane];
-        acc[b] = __builtin_amdgcn_mfma_f32_16x16x4f32(cur.x, bv.x, acc[b], 0, 0, 0);
-        acc[b] = __builtin_amdgcn_mfma_f32_16x16x4f32(cur.y, bv.y, acc[b], 0, 0, 0);
-        acc[b] = __builtin_amdgcn_mfma_f32_16x16x4f32(cur.z, bv.z, acc[b], 0, 0, 0);
-        acc[b] = __builtin_amdgcn_mfma_f32_16x16x4f32(cur.w, bv.w, acc[b], 0, 0, 0);
+    for (int u = 0; u < kPF; ++u) ring[u] = (u < nJ) ? Ablk[u * 64] : float4{0.f, 0.f, 0.f, 0.f};
+    int J = 0;
+    for (; J + kPF <= nJ; J += kPF) {
+#pragma unroll
+      for (int u = 0; u < kPF; ++u) {
+        const float4 cur = ring[u];
+        if (J + u + kPF < nJ) ring[u] = Ablk[(size_t)(J + u + kPF) * 64];
+        mfma_block<NCB>(cur, Kt4 + (J + u) * NCB * 64, acc);
       }
     }
+#pragma unroll
+    for (int u = 0; u < kPF; ++u)
+      if (J + u < nJ) mfma_block<NCB>(ring[u], Kt4 + (J + u) * NCB * 64, acc);
 #pragma unroll
     for (int b = 0; b < NCB; ++b) {
 #pragma unroll
@@ -168,7 +225,7 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
         ss[b] = fmaf(v, v, ss[b]);
         if (Q > 1) {
 #pragma unroll
-          for (int x = 1; x < NX; ++x) gx[b][x] = fmaf(v, quad_xor<Q>(v, x), gx[b][x]);
+          for (int x = 1; x < NX; ++x) gx[b][x] = fmaf(v, quad_xor(v, x), gx[b][x]);
         }
       }
     }
@@ -194,14 +251,17 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
 
   // ---- epilogue -------------------------------------------------------------
   if (tid < NT) {
+    const int64_t p = p0 + tid;
+    const bool valid = p < a.npts;
     float tot[NX];
 #pragma unroll
     for (int x = 0; x < NX; ++x) tot[x] = 0.f;
     for (int w = 0; w < kWaves; ++w)
 #pragma unroll
       for (int x = 0; x < NX; ++x) tot[x] += red[(w * NT + tid) * NX + x];
+    // mu: partials of column tid live at (rl, cg = tid / kCpt, u = tid % kCpt)
     float mu = 0.f;
-    for (int i = tid; i < kThreads; i += NT) mu += mured[i];
+    for (int rl = 0; rl < RL; ++rl) mu += mured[(rl * NCG + tid / kCpt) * kCpt + tid % kCpt];
     const float var = a.s - tot[0];
     if (valid) {
       a.mu[p * a.m + a.k] = mu;
@@ -266,7 +326,7 @@ template <int NT, int DX4, int Q>
 hipError_t launch_t(const PosteriorArgs& a, hipStream_t st) {
   const int n_pad = a.nb * kBlk;
   const size_t lds = sizeof(float) * ((size_t)n_pad * NT + kWaves * NT * ((Q > 1) ? Q : 1) +
-                                      kThreads + NT * 4);
+                                      kThreads * kCpt + NT * 4);
   static bool attr_set = false;
   if (!attr_set) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_posterior<NT, DX4, Q>),
@@ -308,18 +368,19 @@ hipError_t launch_q(const PosteriorArgs& a, hipStream_t st) {
 }  // namespace
 
 // Tile width: 32 points when K*^T fits LDS with room to spare, else 16.
-int posterior_tile(int nb) { return (nb * kBlk <= 1024) ? 32 : 16; }
+int posterior_tile(int nb) { return (nb * kBlk <= 1024) ? BO_POST_NT_SMALL_N : 16; }
 
 size_t posterior_lds_bytes(int nb, int q) {
   const int NT = posterior_tile(nb);
   return sizeof(float) * ((size_t)nb * kBlk * NT + kWaves * NT * ((q > 1) ? q : 1) +
-                          kThreads + NT * 4);
+                          kThreads * kCpt + NT * 4);
 }
 
 hipError_t launch_posterior(const PosteriorArgs& a, hipStream_t st) {
   if (a.npts <= 0) return hipSuccess;
   if (posterior_tile(a.nb) == 32) return launch_q<32>(a, st);
   return launch_q<16>(a, st);
+  static_assert(BO_POST_NT_SMALL_N == 16 || BO_POST_NT_SMALL_N == 32, "tile width");
 }
 
 }  // namespace bo
