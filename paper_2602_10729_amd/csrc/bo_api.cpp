@@ -88,17 +88,67 @@ bool all_finite(const float* v, size_t n) {
   return true;
 }
 
+// Per-device library state: a stream-ordered memory pool (allocations made
+// and released inside the hot path come back from it without a device-wide
+// synchronisation) and one pinned staging buffer for box uploads.
+struct DeviceState {
+  std::mutex mu;
+  hipMemPool_t pool = nullptr;
+  float* stage = nullptr;
+  size_t stage_floats = 0;
+  hipEvent_t stage_evt = nullptr;
+};
+constexpr int kMaxDevices = 64;
+
+DeviceState* device_state(int dev) {
+  static DeviceState states[kMaxDevices];
+  if (dev < 0 || dev >= kMaxDevices) return nullptr;
+  return &states[dev];
+}
+
+bo_status get_pool(int dev, hipMemPool_t* out) {
+  DeviceState* S = device_state(dev);
+  if (!S) return fail(BO_ERR_DEVICE, "device index out of range");
+  std::lock_guard<std::mutex> lk(S->mu);
+  if (!S->pool) {
+    hipMemPoolProps props = {};
+    props.allocType = hipMemAllocationTypePinned;
+    props.location.type = hipMemLocationTypeDevice;
+    props.location.id = dev;
+    hipError_t e = hipMemPoolCreate(&S->pool, &props);
+    if (e != hipSuccess) { S->pool = nullptr; return hip_fail(e, "hipMemPoolCreate"); }
+    uint64_t keep = UINT64_MAX;      // never trim: reuse across calls
+    e = hipMemPoolSetAttribute(S->pool, hipMemPoolAttrReleaseThreshold, &keep);
+    if (e != hipSuccess) return hip_fail(e, "hipMemPoolSetAttribute");
+  }
+  *out = S->pool;
+  return BO_OK;
+}
+
+// Stream-ordered allocation of `count` elements on the current device.
 template <typename T>
-bo_status dmalloc(T** p, size_t count, const char* what) {
+bo_status palloc(T** p, size_t count, hipStream_t st, const char* what) {
   *p = nullptr;
   if (count == 0) return BO_OK;
-  hipError_t e = hipMalloc(reinterpret_cast<void**>(p), sizeof(T) * count);
+  int dev = 0;
+  (void)hipGetDevice(&dev);
+  hipMemPool_t pool;
+  bo_status s = get_pool(dev, &pool);
+  if (s != BO_OK) return s;
+  void* q = nullptr;
+  hipError_t e = hipMallocFromPoolAsync(&q, sizeof(T) * count, pool, st);
   if (e != hipSuccess) {
     (void)hipGetLastError();
-    *p = nullptr;
-    return fail(BO_ERR_OUT_OF_MEMORY, std::string("hipMalloc failed for ") + what);
+    return fail(BO_ERR_OUT_OF_MEMORY, std::string("device allocation failed for ") + what);
   }
+  *p = static_cast<T*>(q);
   return BO_OK;
+}
+
+template <typename T>
+void pfree(T*& p, hipStream_t st) {
+  if (p) (void)hipFreeAsync(p, st);
+  p = nullptr;
 }
 
 struct DeviceGuard {
@@ -115,33 +165,32 @@ struct DeviceGuard {
   }
 };
 
-// Temporary device buffers of the fit, released on every exit path.
+// Temporary device buffers of the fit, returned to the pool on every exit
+// path (ordered after the fit's work on its stream).
 struct FitScratch {
+  hipStream_t st = nullptr;
   double* A = nullptr;
   double* W = nullptr;
-  double* Dinv = nullptr;
   double* hyp = nullptr;
   double* tmp = nullptr;
   int* flag = nullptr;
   ~FitScratch() {
-    (void)hipFree(A); (void)hipFree(W); (void)hipFree(Dinv);
-    (void)hipFree(hyp); (void)hipFree(tmp); (void)hipFree(flag);
+    pfree(A, st); pfree(W, st); pfree(hyp, st); pfree(tmp, st); pfree(flag, st);
   }
 };
 
-// Frees the device/pinned buffers of a model (not the host object).
+// Releases the device buffers of a model after all device work (not the host
+// object). The caller may have used the model on several streams, so wait
+// for the whole device before handing memory back to the pool.
 void release_buffers(Model* M) {
-  (void)hipDeviceSynchronize();   // earlier launches may still read them
-  (void)hipFree(M->Xs);
-  (void)hipFree(M->invls);
-  (void)hipFree(M->alpha);
-  (void)hipFree(M->Lp);
-  (void)hipFree(M->ws);
-  (void)hipFree(M->d_boxes);
-  if (M->h_boxes) (void)hipHostFree(M->h_boxes);
-  if (M->box_evt) (void)hipEventDestroy(M->box_evt);
-  M->Xs = M->invls = M->alpha = M->Lp = M->ws = M->d_boxes = M->h_boxes = nullptr;
-  M->box_evt = nullptr;
+  if (M->Xs || M->invls || M->alpha || M->Lp || M->ws || M->d_boxes)
+    (void)hipDeviceSynchronize();
+  pfree(M->Xs, nullptr);
+  pfree(M->invls, nullptr);
+  pfree(M->alpha, nullptr);
+  pfree(M->Lp, nullptr);
+  pfree(M->ws, nullptr);
+  pfree(M->d_boxes, nullptr);
 }
 
 // Phase timing (bo_profile_enable / bo_profile_read).
@@ -307,16 +356,16 @@ bo_status bo_fit(const float* X, const float* Y, int64_t n, int32_t d, int32_t m
   const size_t nblk = (size_t)M->nb * (M->nb + 1) / 2;
   M->lp_per_obj = nblk * 64 * 4;
   FitScratch fs;
-  if ((s = dmalloc(&fs.A, (size_t)m * nf * nf, "fit matrix")) != BO_OK) return bail(s);
-  if ((s = dmalloc(&fs.W, (size_t)m * nf * nf, "fit inverse")) != BO_OK) return bail(s);
-  if ((s = dmalloc(&fs.Dinv, (size_t)m * nf * kFitBlk, "fit block inverses")) != BO_OK) return bail(s);
-  if ((s = dmalloc(&fs.hyp, (size_t)m * d + 2 * m, "hyperparameters")) != BO_OK) return bail(s);
-  if ((s = dmalloc(&fs.tmp, (size_t)m * nf, "fit vector")) != BO_OK) return bail(s);
-  if ((s = dmalloc(&fs.flag, 1, "flag")) != BO_OK) return bail(s);
-  if ((s = dmalloc(&M->Xs, (size_t)m * M->n_pad * M->dx, "scaled X")) != BO_OK) return bail(s);
-  if ((s = dmalloc(&M->invls, (size_t)m * M->dx, "inverse lengthscales")) != BO_OK) return bail(s);
-  if ((s = dmalloc(&M->alpha, (size_t)m * M->n_pad, "alpha")) != BO_OK) return bail(s);
-  if ((s = dmalloc(&M->Lp, (size_t)m * M->lp_per_obj, "packed inverse")) != BO_OK) return bail(s);
+  fs.st = st;
+  if ((s = palloc(&fs.A, (size_t)m * nf * nf, st, "fit matrix")) != BO_OK) return bail(s);
+  if ((s = palloc(&fs.W, (size_t)m * nf * nf, st, "fit inverse")) != BO_OK) return bail(s);
+  if ((s = palloc(&fs.hyp, (size_t)m * d + 2 * m, st, "hyperparameters")) != BO_OK) return bail(s);
+  if ((s = palloc(&fs.tmp, (size_t)m * nf, st, "fit vector")) != BO_OK) return bail(s);
+  if ((s = palloc(&fs.flag, 1, st, "flag")) != BO_OK) return bail(s);
+  if ((s = palloc(&M->Xs, (size_t)m * M->n_pad * M->dx, st, "scaled X")) != BO_OK) return bail(s);
+  if ((s = palloc(&M->invls, (size_t)m * M->dx, st, "inverse lengthscales")) != BO_OK) return bail(s);
+  if ((s = palloc(&M->alpha, (size_t)m * M->n_pad, st, "alpha")) != BO_OK) return bail(s);
+  if ((s = palloc(&M->Lp, (size_t)m * M->lp_per_obj, st, "packed inverse")) != BO_OK) return bail(s);
 
   std::vector<double> hyp((size_t)m * d + 2 * m);
   for (int i = 0; i < m * d; ++i) hyp[i] = lengthscale[i];
@@ -338,8 +387,7 @@ bo_status bo_fit(const float* X, const float* Y, int64_t n, int32_t d, int32_t m
   const double* d_os = fs.hyp + (size_t)m * d;
   const double* d_noise = d_os + m;
   if ((s = after_launch(launch_gram(X, n, d, m, nf, d_ls, d_os, d_noise, fs.A, st), st, "gram")) != BO_OK) return bail(s);
-  if ((s = after_launch(launch_cholesky(fs.A, fs.Dinv, nf, m, fs.flag, st), st, "cholesky")) != BO_OK) return bail(s);
-  if ((s = after_launch(launch_trtri(fs.A, fs.Dinv, fs.W, nf, m, st), st, "trtri")) != BO_OK) return bail(s);
+  if ((s = after_launch(launch_cholesky(fs.A, fs.W, nf, m, fs.flag, st), st, "cholesky")) != BO_OK) return bail(s);
   if ((s = after_launch(launch_alpha(fs.W, Y, n, m, nf, M->n_pad, fs.tmp, M->alpha, st), st, "alpha")) != BO_OK) return bail(s);
   if ((s = after_launch(launch_pack(fs.W, n, m, nf, M->nb, M->Lp, X, d, M->dx, M->invls, M->Xs, st), st, "pack")) != BO_OK) return bail(s);
 
@@ -349,8 +397,6 @@ bo_status bo_fit(const float* X, const float* Y, int64_t n, int32_t d, int32_t m
   if (e != hipSuccess) return bail(hip_fail(e, "bo_fit: sync"));
   if (flag) return bail(fail(BO_ERR_NOT_POSITIVE_DEFINITE, "bo_fit: non-positive Cholesky pivot"));
 
-  e = hipEventCreateWithFlags(&M->box_evt, hipEventDisableTiming);
-  if (e != hipSuccess) return bail(hip_fail(e, "bo_fit: event"));
   M->last_stream = st;
   *out = h;
   return BO_OK;
@@ -407,34 +453,46 @@ bo_status bo_score(bo_model model, const float* cand, int64_t M_, int32_t q,
     if (nbox > BO_MAX_BOXES) return fail(BO_ERR_CAPACITY, "bo_score: too many boxes");
     if (ehvi_lds_bytes(S, q, m, nbox) > kLdsLimit)
       return fail(BO_ERR_CAPACITY, "bo_score: samples and boxes exceed LDS");
-    hipError_t e;
     if (nbox > M.box_cap) {
-      // buffers may still be read by earlier launches: wait before replacing
-      e = hipDeviceSynchronize();
-      if (e != hipSuccess) return hip_fail(e, "bo_score: sync before box realloc");
-      (void)hipFree(M.d_boxes);
-      M.d_boxes = nullptr;
-      if (M.h_boxes) (void)hipHostFree(M.h_boxes);
-      M.h_boxes = nullptr;
+      if (M.d_boxes) {
+        hipError_t e = hipDeviceSynchronize();   // earlier launches may read it
+        if (e != hipSuccess) return hip_fail(e, "bo_score: sync before box growth");
+        pfree(M.d_boxes, st);
+      }
       M.box_cap = 0;
       const int cap = std::max(64, nbox);
-      if ((s = dmalloc(&M.d_boxes, (size_t)cap * 2 * m, "boxes")) != BO_OK) return s;
-      e = hipHostMalloc(reinterpret_cast<void**>(&M.h_boxes), sizeof(float) * cap * 2 * m, hipHostMallocDefault);
-      if (e != hipSuccess) return hip_fail(e, "bo_score: pinned boxes");
+      if ((s = palloc(&M.d_boxes, (size_t)cap * 2 * m, st, "boxes")) != BO_OK) return s;
       M.box_cap = cap;
-    } else {
-      e = hipEventSynchronize(M.box_evt);       // previous staging copy done
-      if (e != hipSuccess) return hip_fail(e, "bo_score: box event");
     }
-    for (int c = 0; c < nbox; ++c)
-      for (int k = 0; k < m; ++k) {
-        const float l = lo[(size_t)c * m + k], h = hi[(size_t)c * m + k];
-        M.h_boxes[(size_t)c * 2 * m + k] = l;
-        M.h_boxes[(size_t)c * 2 * m + m + k] = h - l;     // inf stays inf
+    {
+      // stage in the device's pinned buffer; the previous upload from it must
+      // have completed before it is rewritten
+      DeviceState* DS = device_state(M.device);
+      std::lock_guard<std::mutex> lk(DS->mu);
+      hipError_t e = hipSuccess;
+      if (!DS->stage_evt) e = hipEventCreateWithFlags(&DS->stage_evt, hipEventDisableTiming);
+      else e = hipEventSynchronize(DS->stage_evt);
+      if (e != hipSuccess) return hip_fail(e, "bo_score: staging event");
+      const size_t need_f = (size_t)nbox * 2 * m;
+      if (need_f > DS->stage_floats) {
+        if (DS->stage) (void)hipHostFree(DS->stage);
+        DS->stage = nullptr;
+        DS->stage_floats = 0;
+        const size_t cap = std::max<size_t>(need_f, (size_t)BO_MAX_BOXES * 6);
+        e = hipHostMalloc(reinterpret_cast<void**>(&DS->stage), sizeof(float) * cap, hipHostMallocDefault);
+        if (e != hipSuccess) return hip_fail(e, "bo_score: pinned staging");
+        DS->stage_floats = cap;
       }
-    e = hipMemcpyAsync(M.d_boxes, M.h_boxes, sizeof(float) * nbox * 2 * m, hipMemcpyHostToDevice, st);
-    if (e == hipSuccess) e = hipEventRecord(M.box_evt, st);
-    if (e != hipSuccess) return hip_fail(e, "bo_score: box upload");
+      for (int c = 0; c < nbox; ++c)
+        for (int k = 0; k < m; ++k) {
+          const float l = lo[(size_t)c * m + k], h = hi[(size_t)c * m + k];
+          DS->stage[(size_t)c * 2 * m + k] = l;
+          DS->stage[(size_t)c * 2 * m + m + k] = h - l;     // inf stays inf
+        }
+      e = hipMemcpyAsync(M.d_boxes, DS->stage, sizeof(float) * need_f, hipMemcpyHostToDevice, st);
+      if (e == hipSuccess) e = hipEventRecord(DS->stage_evt, st);
+      if (e != hipSuccess) return hip_fail(e, "bo_score: box upload");
+    }
     M.nbox = nbox;
     M.box_ref.assign(ref_point, ref_point + m);
   } else if (ehvi_lds_bytes(S, q, m, M.nbox) > kLdsLimit) {
@@ -446,12 +504,13 @@ bo_status bo_score(bo_model model, const float* cand, int64_t M_, int32_t q,
   const size_t need = (mu ? 0 : (size_t)npts * m) + (sigma ? 0 : (size_t)npts * m) +
                       (q > 1 ? (size_t)M_ * m * T : 0);
   if (need > M.ws_floats) {
-    hipError_t e = hipDeviceSynchronize();
-    if (e != hipSuccess) return hip_fail(e, "bo_score: sync before workspace growth");
-    (void)hipFree(M.ws);
-    M.ws = nullptr;
+    if (M.ws) {
+      hipError_t e = hipDeviceSynchronize();      // earlier launches may use it
+      if (e != hipSuccess) return hip_fail(e, "bo_score: sync before workspace growth");
+      pfree(M.ws, st);
+    }
     M.ws_floats = 0;
-    if ((s = dmalloc(&M.ws, need, "score workspace")) != BO_OK) return s;
+    if ((s = palloc(&M.ws, need, st, "score workspace")) != BO_OK) return s;
     M.ws_floats = need;
   }
   float* w = M.ws;
@@ -566,13 +625,13 @@ bo_status bo_cholesky_test(const float* A, int64_t n, float* L, void* stream) {
   hipStream_t st = static_cast<hipStream_t>(stream);
   const int nf = static_cast<int>((n + kFitBlk - 1) / kFitBlk) * kFitBlk;
   FitScratch fs;
-  if ((s = dmalloc(&fs.A, (size_t)nf * nf, "matrix")) != BO_OK) return s;
-  if ((s = dmalloc(&fs.Dinv, (size_t)nf * kFitBlk, "block inverses")) != BO_OK) return s;
-  if ((s = dmalloc(&fs.flag, 1, "flag")) != BO_OK) return s;
+  fs.st = st;
+  if ((s = palloc(&fs.A, (size_t)nf * nf, st, "matrix")) != BO_OK) return s;
+  if ((s = palloc(&fs.flag, 1, st, "flag")) != BO_OK) return s;
   hipError_t e = hipMemsetAsync(fs.flag, 0, sizeof(int), st);
   if (e != hipSuccess) return hip_fail(e, "bo_cholesky_test: memset");
   if ((s = after_launch(launch_f32_to_padded(A, n, nf, fs.A, st), st, "pad")) != BO_OK) return s;
-  if ((s = after_launch(launch_cholesky(fs.A, fs.Dinv, nf, 1, fs.flag, st), st, "cholesky")) != BO_OK) return s;
+  if ((s = after_launch(launch_cholesky(fs.A, nullptr, nf, 1, fs.flag, st), st, "cholesky")) != BO_OK) return s;
   if ((s = after_launch(launch_lower_to_f32(fs.A, n, nf, L, st), st, "convert")) != BO_OK) return s;
   int flag = 0;
   e = hipMemcpyAsync(&flag, fs.flag, sizeof(int), hipMemcpyDeviceToHost, st);

@@ -55,8 +55,6 @@ struct Model {
   int box_cap = 0;
   int nbox = -1;
   std::vector<float> box_ref;
-  float* h_boxes = nullptr;      // pinned staging
-  hipEvent_t box_evt = nullptr;
   hipStream_t last_stream = nullptr;
 };
 
@@ -68,14 +66,11 @@ struct Model {
 hipError_t launch_gram(const float* X, int64_t n, int d, int m, int n_fit,
                        const double* ls, const double* os, const double* noise,
                        double* A, hipStream_t st);
-// Blocked right-looking Cholesky of m matrices [m][nf][nf] (lower, in place)
-// with diagonal-block inverses Dinv [m][nf/kFitBlk][kFitBlk][kFitBlk];
+// Blocked right-looking Cholesky of m matrices [m][nf][nf] (lower, in place).
+// With W != nullptr it also leaves W = L^{-1} (lower, [m][nf][nf]).
 // *flag is set non-zero on a non-positive or non-finite pivot.
-hipError_t launch_cholesky(double* A, double* Dinv, int nf, int m, int* flag,
+hipError_t launch_cholesky(double* A, double* W, int nf, int m, int* flag,
                            hipStream_t st);
-// W = L^{-1} (lower, [m][nf][nf]) from the factor and its block inverses.
-hipError_t launch_trtri(const double* A, const double* Dinv, double* W, int nf,
-                        int m, hipStream_t st);
 // alpha_k = W_k^T (W_k y_k), y from Y [n][m] (fp32), written fp32 [m][n_pad].
 hipError_t launch_alpha(const double* W, const float* Y, int64_t n, int m,
                         int nf, int n_pad, double* tmp, float* alpha,

@@ -11,14 +11,18 @@
 // runs in fp64 here: the fp32 scoring path then inherits factors rounded
 // once, and its whole error budget goes to the scoring arithmetic.
 //
-// Blocked right-looking Cholesky with 64x64 blocks, three launches per block
-// column:
-//   potrf: factor the diagonal block in LDS and invert it (one workgroup per
-//          objective);
-//   trsm:  panel blocks below the diagonal times the inverse's transpose;
-//   syrk:  trailing update of every lower block (ib >= jb' > jb).
-// The inverse W = L^{-1} is built column block by column block: one
-// workgroup per block column walks down it, W_ij = -D_i^{-1} sum_t L_it W_tj.
+// Blocked right-looking Cholesky with 64x64 blocks that carries the inverse
+// along. W starts as the identity; after step kb its block rows <= kb hold
+// L^{-1} and the rows below hold R_i = delta_i - sum_{k<=kb} L_ik W_k. Step kb:
+//   panel:  rows below the diagonal solve x L_kk^T = a (forward substitution,
+//           one thread per row), and W's block row kb solves L_kk w = r
+//           (one thread per column);
+//   update: trailing A_ic -= L_ik L_ck^T (kb < c <= i) and R_ij -= L_ik W_kj
+//           (i > kb, j <= kb), 64x64x64 tiles; the workgroup that updates
+//           the next diagonal tile factors it at once (one wave, row per
+//           lane), so no separate factor launch is needed after the first.
+// Two launches per block column; the serial chain is one 64-step
+// factorisation plus two substitutions per block column.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -60,66 +64,133 @@ __global__ void k_gram(const float* __restrict__ X, int64_t n, int d, int nf,
   A[((int64_t)k * nf + i) * nf + j] = v;
 }
 
-// Factor the diagonal block jb of every objective in LDS, write L_jj (lower,
-// zeros above) back and its inverse to Dinv.
-__global__ __launch_bounds__(256) void k_potrf(double* __restrict__ A,
-                                               double* __restrict__ Dinv, int nf,
-                                               int jb, int* __restrict__ flag) {
-  __shared__ double a[B][LDP];
-  __shared__ double x[B][LDP];
-  __shared__ int bad;
-  const int k = blockIdx.x;
-  const int tid = threadIdx.x;
-  double* Ak = A + (int64_t)k * nf * nf;
-  const int o = jb * B;
-  for (int e = tid; e < B * B; e += 256) {
-    const int i = e / B, c = e % B;
-    a[i][c] = Ak[(int64_t)(o + i) * nf + o + c];
-  }
-  if (tid == 0) bad = 0;
-  __syncthreads();
-  for (int j = 0; j < B; ++j) {
-    if (tid == 0) {
-      const double p = a[j][j];
-      if (!(p > 0.0) || !isfinite(p)) {
-        bad = 1;
-        a[j][j] = 1.0;
-      } else {
-        a[j][j] = sqrt(p);
-      }
-    }
-    __syncthreads();
-    const double djj = a[j][j];
-    for (int i = j + 1 + tid; i < B; i += 256) a[i][j] /= djj;
-    __syncthreads();
-    const int w = B - j - 1;
-    for (int e = tid; e < w * w; e += 256) {
-      const int i = j + 1 + e / w, c = j + 1 + e % w;
-      if (c <= i) a[i][c] -= a[i][j] * a[c][j];
-    }
-    __syncthreads();
-  }
-  // inverse of the lower block: column c solves L x = e_c by substitution
-  if (tid < B) {
-    const int c = tid;
-    for (int i = 0; i < B; ++i) {
-      if (i < c) { x[i][c] = 0.0; continue; }
-      double acc = (i == c) ? 1.0 : 0.0;
-      for (int t = c; t < i; ++t) acc -= a[i][t] * x[t][c];
-      x[i][c] = acc / a[i][i];
-    }
-  }
-  __syncthreads();
-  double* Dk = Dinv + ((int64_t)k * (nf / B) + jb) * B * B;
-  for (int e = tid; e < B * B; e += 256) {
-    const int i = e / B, c = e % B;
-    Ak[(int64_t)(o + i) * nf + o + c] = (c <= i) ? a[i][c] : 0.0;
-    Dk[e] = x[i][c];
-  }
-  if (tid == 0 && bad) atomicOr(flag, 1);
+// Factor the symmetric 64x64 block in LDS (lower triangle read) in place:
+// wave 0 holds row `lane` in registers; pivots and the scaled column are
+// read across lanes with readlane (j and c are compile-time after unrolling).
+// Zeros are written above the diagonal. A non-positive or non-finite pivot
+// sets *bad and is replaced by 1 so the rest stays finite.
+__device__ inline double readlane_d(double v, int l) {
+  const long long b = __double_as_longlong(v);
+  const int lo = __builtin_amdgcn_readlane(static_cast<int>(b & 0xffffffffll), l);
+  const int hi = __builtin_amdgcn_readlane(static_cast<int>(b >> 32), l);
+  return __longlong_as_double((static_cast<long long>(hi) << 32) |
+                              (static_cast<unsigned int>(lo)));
 }
 
-// 64x64x64 product helper: out[i][c] (4x4 per thread) = sum_t P[i][t] * Q[c][t].
+__device__ __forceinline__ void potrf64_wave0(double (*a)[LDP], int* bad_flag) {
+  const int tid = threadIdx.x;
+  if (tid >= 64) return;
+  const int i = tid;
+  double r[B];
+#pragma unroll
+  for (int c = 0; c < B; ++c) r[c] = a[i][c];
+  bool bad = false;
+#pragma unroll
+  for (int j = 0; j < B; ++j) {
+    double piv = readlane_d(r[j], j);
+    if (!(piv > 0.0) || !isfinite(piv)) {
+      bad = true;
+      piv = 1.0;
+    }
+    const double djj = sqrt(piv);
+    const double inv = 1.0 / djj;
+    r[j] = (i == j) ? djj : r[j] * inv;      // rows above j keep their value
+#pragma unroll
+    for (int c = j + 1; c < B; ++c) {
+      const double lcj = readlane_d(r[j], c);  // L[c][j] (scaled on lane c)
+      r[c] = fma(-r[j], lcj, r[c]);            // meaningful for c <= i only
+    }
+  }
+#pragma unroll
+  for (int c = 0; c < B; ++c) a[i][c] = (c <= i) ? r[c] : 0.0;
+  if (bad && i == 0) atomicOr(bad_flag, 1);
+  // lanes see the same `bad` (pivots are wave-uniform), so lane 0 reports
+}
+
+__device__ inline void load_block(double (*dst)[LDP], const double* src, int ld) {
+  for (int e = threadIdx.x; e < B * B; e += blockDim.x) {
+    const int i = e >> 6, c = e & 63;
+    dst[i][c] = src[(int64_t)i * ld + c];
+  }
+}
+
+__device__ inline void store_block(double* dst, int ld, const double (*srcb)[LDP]) {
+  for (int e = threadIdx.x; e < B * B; e += blockDim.x) {
+    const int i = e >> 6, c = e & 63;
+    dst[(int64_t)i * ld + c] = srcb[i][c];
+  }
+}
+
+// First diagonal block (kb = 0) of every objective.
+__global__ __launch_bounds__(64) void k_potrf_first(double* __restrict__ A, int nf,
+                                                    int* __restrict__ flag) {
+  __shared__ double a[B][LDP];
+  double* Ak = A + (int64_t)blockIdx.x * nf * nf;
+  load_block(a, Ak, nf);
+  __syncthreads();
+  potrf64_wave0(a, flag);
+  __syncthreads();
+  store_block(Ak, nf, a);
+}
+
+// Panel of step kb: blocks [0, nrow_blk) solve rows of A below the diagonal,
+// blocks [nrow_blk, ...) solve columns of W's block row kb (if W != null).
+__global__ __launch_bounds__(256) void k_panel(double* __restrict__ A, double* __restrict__ W,
+                                               int nf, int kb, int nrow_blk) {
+  __shared__ double l[B][LDP];
+  __shared__ double dinv[B];
+  const int k = blockIdx.y;
+  double* Ak = A + (int64_t)k * nf * nf;
+  const int o = kb * B;
+  load_block(l, Ak + (int64_t)o * nf + o, nf);
+  __syncthreads();
+  if (threadIdx.x < B) dinv[threadIdx.x] = 1.0 / l[threadIdx.x][threadIdx.x];
+  __syncthreads();
+  if ((int)blockIdx.x < nrow_blk) {
+    // row i of the panel: x L^T = a  =>  x_j = (a_j - sum_{t<j} x_t L[j][t]) / L[j][j]
+    const int i = o + B + blockIdx.x * 256 + threadIdx.x;
+    if (i >= nf) return;
+    double* row = Ak + (int64_t)i * nf + o;
+    double x[B];
+#pragma unroll
+    for (int j = 0; j < B; ++j) x[j] = row[j];
+#pragma unroll
+    for (int j = 0; j < B; ++j) {
+      double s0 = x[j], s1 = 0.0;
+#pragma unroll
+      for (int t = 0; t < j; t += 2) {
+        s0 = fma(-x[t], l[j][t], s0);
+        if (t + 1 < j) s1 = fma(-x[t + 1], l[j][t + 1], s1);
+      }
+      x[j] = (s0 + s1) * dinv[j];
+    }
+#pragma unroll
+    for (int j = 0; j < B; ++j) row[j] = x[j];
+  } else {
+    if (W == nullptr) return;
+    // column c of W's block row kb: L_kk w = r  =>  w_j = (r_j - sum_{t<j} L[j][t] w_t) / L[j][j]
+    const int c = (blockIdx.x - nrow_blk) * 256 + threadIdx.x;
+    if (c >= o + B) return;
+    double* Wk = W + (int64_t)k * nf * nf;
+    double w[B];
+#pragma unroll
+    for (int j = 0; j < B; ++j) w[j] = Wk[(int64_t)(o + j) * nf + c];
+#pragma unroll
+    for (int j = 0; j < B; ++j) {
+      double s0 = w[j], s1 = 0.0;
+#pragma unroll
+      for (int t = 0; t < j; t += 2) {
+        s0 = fma(-l[j][t], w[t], s0);
+        if (t + 1 < j) s1 = fma(-l[j][t + 1], w[t + 1], s1);
+      }
+      w[j] = (s0 + s1) * dinv[j];
+    }
+#pragma unroll
+    for (int j = 0; j < B; ++j) Wk[(int64_t)(o + j) * nf + c] = w[j];
+  }
+}
+
+// 64x64x64 product helper: acc[r][c] (4x4 per thread) += sum_t P[ty*4+r][t] * Q[tx*4+c][t].
 __device__ inline void gemm_nt_64(const double (*P)[LDP], const double (*Q)[LDP],
                                   double acc[4][4], int ty, int tx) {
   for (int t = 0; t < B; ++t) {
@@ -135,50 +206,45 @@ __device__ inline void gemm_nt_64(const double (*P)[LDP], const double (*Q)[LDP]
   }
 }
 
-// Panel: A[ib][jb] <- A[ib][jb] * Dinv_jb^T for ib > jb.
-__global__ __launch_bounds__(256) void k_trsm(double* __restrict__ A,
-                                              const double* __restrict__ Dinv,
-                                              int nf, int jb) {
+// Update of step kb. Tile t < T(T+1)/2: trailing A tile; the rest: R tiles of
+// W (if W != null). Tile 0 is the next diagonal block, factored right after
+// its update.
+__global__ __launch_bounds__(256) void k_update(double* __restrict__ A, double* __restrict__ W,
+                                                int nf, int kb, int* __restrict__ flag) {
   __shared__ double p[B][LDP];
   __shared__ double q[B][LDP];
   const int k = blockIdx.y;
-  const int ib = jb + 1 + blockIdx.x;
-  const int tid = threadIdx.x, tx = tid % 16, ty = tid / 16;
-  double* Ak = A + (int64_t)k * nf * nf;
-  const double* Dk = Dinv + ((int64_t)k * (nf / B) + jb) * B * B;
-  for (int e = tid; e < B * B; e += 256) {
-    const int i = e / B, c = e % B;
-    p[i][c] = Ak[(int64_t)(ib * B + i) * nf + jb * B + c];
-    q[i][c] = Dk[e];
-  }
-  __syncthreads();
-  double acc[4][4] = {};
-  gemm_nt_64(p, q, acc, ty, tx);
-#pragma unroll
-  for (int r = 0; r < 4; ++r)
-#pragma unroll
-    for (int c = 0; c < 4; ++c)
-      Ak[(int64_t)(ib * B + ty * 4 + r) * nf + jb * B + tx * 4 + c] = acc[r][c];
-}
-
-// Trailing update: A[ib][cb] -= L[ib][jb] * L[cb][jb]^T for jb < cb <= ib.
-__global__ __launch_bounds__(256) void k_syrk(double* __restrict__ A, int nf, int jb) {
-  __shared__ double p[B][LDP];
-  __shared__ double q[B][LDP];
-  const int k = blockIdx.y;
-  // triangular tile index -> (ib, cb) with cb <= ib, both offset by jb + 1
+  const int nbk = nf / B;
+  const int T = nbk - kb - 1;
+  const int nsyrk = T * (T + 1) / 2;
   const int t = blockIdx.x;
-  int r = static_cast<int>((sqrt(8.0 * t + 1.0) - 1.0) * 0.5);
-  while ((r + 1) * (r + 2) / 2 <= t) ++r;
-  while (r * (r + 1) / 2 > t) --r;
-  const int ib = jb + 1 + r;
-  const int cb = jb + 1 + (t - r * (r + 1) / 2);
   const int tid = threadIdx.x, tx = tid % 16, ty = tid / 16;
   double* Ak = A + (int64_t)k * nf * nf;
-  for (int e = tid; e < B * B; e += 256) {
-    const int i = e / B, c = e % B;
-    p[i][c] = Ak[(int64_t)(ib * B + i) * nf + jb * B + c];
-    q[i][c] = Ak[(int64_t)(cb * B + i) * nf + jb * B + c];
+  double* Wk = (W != nullptr) ? W + (int64_t)k * nf * nf : nullptr;
+  const int o = kb * B;
+  double* dst;
+  if (t < nsyrk) {
+    // (ib, cb) with kb < cb <= ib: tile index t -> row r, column within row
+    int r = static_cast<int>((sqrt(8.0 * t + 1.0) - 1.0) * 0.5);
+    while ((r + 1) * (r + 2) / 2 <= t) ++r;
+    while (r * (r + 1) / 2 > t) --r;
+    const int ib = kb + 1 + r;
+    const int cb = kb + 1 + (t - r * (r + 1) / 2);
+    load_block(p, Ak + (int64_t)ib * B * nf + o, nf);       // L[ib][kb]
+    load_block(q, Ak + (int64_t)cb * B * nf + o, nf);       // L[cb][kb]
+    dst = Ak + (int64_t)ib * B * nf + cb * B;
+  } else {
+    // R tile (ib, jb): ib > kb, jb <= kb:  W[ib][jb] -= L[ib][kb] W[kb][jb]
+    const int u = t - nsyrk;
+    const int ib = kb + 1 + u / (kb + 1);
+    const int jb = u % (kb + 1);
+    load_block(p, Ak + (int64_t)ib * B * nf + o, nf);       // L[ib][kb]
+    // q = W[kb][jb]^T so that gemm_nt forms P * W[kb][jb]
+    for (int e = tid; e < B * B; e += 256) {
+      const int i = e >> 6, c = e & 63;
+      q[c][i] = Wk[(int64_t)(o + i) * nf + jb * B + c];
+    }
+    dst = Wk + (int64_t)ib * B * nf + jb * B;
   }
   __syncthreads();
   double acc[4][4] = {};
@@ -187,64 +253,30 @@ __global__ __launch_bounds__(256) void k_syrk(double* __restrict__ A, int nf, in
   for (int rr = 0; rr < 4; ++rr)
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
-      double* dst = Ak + (int64_t)(ib * B + ty * 4 + rr) * nf + cb * B + tx * 4 + c;
-      *dst -= acc[rr][c];
+      double* d = dst + (int64_t)(ty * 4 + rr) * nf + tx * 4 + c;
+      acc[rr][c] = *d - acc[rr][c];
+      *d = acc[rr][c];
     }
+  if (t == 0) {
+    // next diagonal block: stage the updated tile and factor it
+    __syncthreads();
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr)
+#pragma unroll
+      for (int c = 0; c < 4; ++c) p[ty * 4 + rr][tx * 4 + c] = acc[rr][c];
+    __syncthreads();
+    potrf64_wave0(p, flag);
+    __syncthreads();
+    store_block(dst, nf, p);
+  }
 }
 
-// Inverse of the factor, one workgroup per (block column j, objective).
-__global__ __launch_bounds__(256) void k_trtri(const double* __restrict__ A,
-                                               const double* __restrict__ Dinv,
-                                               double* __restrict__ W, int nf) {
-  __shared__ double p[B][LDP];
-  __shared__ double q[B][LDP];
+// W = identity (the starting R of the carried inverse)
+__global__ void k_identity(double* __restrict__ W, int nf) {
+  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
   const int k = blockIdx.y;
-  const int j = blockIdx.x;
-  const int nbk = nf / B;
-  const int tid = threadIdx.x, tx = tid % 16, ty = tid / 16;
-  const double* Ak = A + (int64_t)k * nf * nf;
-  const double* Dk = Dinv + (int64_t)k * nbk * B * B;
-  double* Wk = W + (int64_t)k * nf * nf;
-  // W_jj = D_j^{-1}
-  for (int e = tid; e < B * B; e += 256) {
-    const int i = e / B, c = e % B;
-    Wk[(int64_t)(j * B + i) * nf + j * B + c] = Dk[(int64_t)j * B * B + e];
-  }
-  __threadfence();
-  __syncthreads();
-  for (int i = j + 1; i < nbk; ++i) {
-    // acc = sum_{t=j}^{i-1} L_it W_tj   (computed as P * Q^T with Q = W_tj^T)
-    double acc[4][4] = {};
-    for (int tb = j; tb < i; ++tb) {
-      for (int e = tid; e < B * B; e += 256) {
-        const int r = e / B, c = e % B;
-        p[r][c] = Ak[(int64_t)(i * B + r) * nf + tb * B + c];
-        q[c][r] = Wk[(int64_t)(tb * B + r) * nf + j * B + c];   // q = W_tj^T
-      }
-      __syncthreads();
-      gemm_nt_64(p, q, acc, ty, tx);
-      __syncthreads();
-    }
-    // W_ij = -D_i^{-1} acc: stage acc^T in q, D_i in p
-#pragma unroll
-    for (int r = 0; r < 4; ++r)
-#pragma unroll
-      for (int c = 0; c < 4; ++c) q[tx * 4 + c][ty * 4 + r] = acc[r][c];
-    for (int e = tid; e < B * B; e += 256) {
-      const int r = e / B, c = e % B;
-      p[r][c] = Dk[(int64_t)i * B * B + e];
-    }
-    __syncthreads();
-    double out[4][4] = {};
-    gemm_nt_64(p, q, out, ty, tx);
-#pragma unroll
-    for (int r = 0; r < 4; ++r)
-#pragma unroll
-      for (int c = 0; c < 4; ++c)
-        Wk[(int64_t)(i * B + ty * 4 + r) * nf + j * B + tx * 4 + c] = -out[r][c];
-    __threadfence();
-    __syncthreads();
-  }
+  if (e >= (int64_t)nf * nf) return;
+  W[(int64_t)k * nf * nf + e] = ((e / nf) == (e % nf)) ? 1.0 : 0.0;
 }
 
 // tmp_k = W_k y_k  (one wave per row, lanes over columns)
@@ -263,20 +295,28 @@ __global__ __launch_bounds__(256) void k_wy(const double* __restrict__ W,
   if (lane == 0) tmp[(int64_t)k * nf + row] = (row < n) ? acc : 0.0;
 }
 
-// alpha_k[j] = sum_{i >= j} W_k[i][j] tmp_k[i]  (thread per column)
+// alpha_k[j] = sum_{i >= j} W_k[i][j] tmp_k[i]: 64 columns per block, four
+// row phases per column (coalesced row reads), combined in LDS.
 __global__ __launch_bounds__(256) void k_wty(const double* __restrict__ W,
                                              const double* __restrict__ tmp,
                                              int64_t n, int nf, int n_pad,
                                              float* __restrict__ alpha) {
+  __shared__ double part[4][64];
   const int k = blockIdx.y;
-  const int j = blockIdx.x * 256 + threadIdx.x;
-  if (j >= n_pad) return;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  const int j = blockIdx.x * 64 + tx;
   double acc = 0.0;
   if (j < n) {
     const double* Wk = W + (int64_t)k * nf * nf;
-    for (int64_t i = j; i < n; ++i) acc += Wk[i * nf + j] * tmp[(int64_t)k * nf + i];
+    const double* tk = tmp + (int64_t)k * nf;
+    for (int64_t i = j + ty; i < n; i += 4) acc = fma(Wk[i * nf + j], tk[i], acc);
   }
-  alpha[(int64_t)k * n_pad + j] = static_cast<float>(acc);
+  part[ty][tx] = acc;
+  __syncthreads();
+  if (ty == 0 && j < n_pad) {
+    const double v = (part[0][tx] + part[1][tx]) + (part[2][tx] + part[3][tx]);
+    alpha[(int64_t)k * n_pad + j] = (j < n) ? static_cast<float>(v) : 0.f;
+  }
 }
 
 // Pack lower 16x16 blocks of W into MFMA A-fragment order:
@@ -349,34 +389,35 @@ hipError_t launch_gram(const float* X, int64_t n, int d, int m, int n_fit,
   return hipGetLastError();
 }
 
-hipError_t launch_cholesky(double* A, double* Dinv, int nf, int m, int* flag,
+hipError_t launch_cholesky(double* A, double* W, int nf, int m, int* flag,
                            hipStream_t st) {
   const int nbk = nf / B;
-  for (int jb = 0; jb < nbk; ++jb) {
-    hipLaunchKernelGGL(k_potrf, dim3(m), dim3(256), 0, st, A, Dinv, nf, jb, flag);
-    const int T = nbk - jb - 1;
-    if (T > 0) {
-      hipLaunchKernelGGL(k_trsm, dim3(T, m), dim3(256), 0, st, A, Dinv, nf, jb);
-      hipLaunchKernelGGL(k_syrk, dim3(T * (T + 1) / 2, m), dim3(256), 0, st, A, nf, jb);
-    }
+  if (W != nullptr) {
+    const unsigned g = static_cast<unsigned>(((int64_t)nf * nf + 255) / 256);
+    hipLaunchKernelGGL(k_identity, dim3(g, m), dim3(256), 0, st, W, nf);
+  }
+  hipLaunchKernelGGL(k_potrf_first, dim3(m), dim3(64), 0, st, A, nf, flag);
+  for (int kb = 0; kb < nbk; ++kb) {
+    const int rows_below = nf - (kb + 1) * B;
+    const int nrow_blk = (rows_below + 255) / 256;
+    const int ncol_blk = (W != nullptr) ? ((kb + 1) * B + 255) / 256 : 0;
+    if (nrow_blk + ncol_blk > 0)
+      hipLaunchKernelGGL(k_panel, dim3(nrow_blk + ncol_blk, m), dim3(256), 0, st, A, W, nf,
+                         kb, nrow_blk);
+    const int T = nbk - kb - 1;
+    const int ntile = T * (T + 1) / 2 + ((W != nullptr) ? T * (kb + 1) : 0);
+    if (T > 0)
+      hipLaunchKernelGGL(k_update, dim3(ntile, m), dim3(256), 0, st, A, W, nf, kb, flag);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
 }
 
-hipError_t launch_trtri(const double* A, const double* Dinv, double* W, int nf, int m,
-                        hipStream_t st) {
-  hipError_t e = hipMemsetAsync(W, 0, sizeof(double) * (size_t)m * nf * nf, st);
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_trtri, dim3(nf / B, m), dim3(256), 0, st, A, Dinv, W, nf);
-  return hipGetLastError();
-}
-
 hipError_t launch_alpha(const double* W, const float* Y, int64_t n, int m, int nf,
                         int n_pad, double* tmp, float* alpha, hipStream_t st) {
   hipLaunchKernelGGL(k_wy, dim3((nf + 3) / 4, m), dim3(256), 0, st, W, Y, n, m, nf, tmp);
-  hipLaunchKernelGGL(k_wty, dim3((n_pad + 255) / 256, m), dim3(256), 0, st, W, tmp, n,
+  hipLaunchKernelGGL(k_wty, dim3((n_pad + 63) / 64, m), dim3(256), 0, st, W, tmp, n,
                      nf, n_pad, alpha);
   return hipGetLastError();
 }
