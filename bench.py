@@ -78,6 +78,8 @@ def main(argv=None):
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-sample", type=int, default=4096)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calib-copy-mb", type=int, default=0,
+                    help="also run one plain device copy of this many MiB (counter calibration)")
     a = ap.parse_args(argv)
 
     if a.gpus != 1:
@@ -116,6 +118,15 @@ def main(argv=None):
     m0 = bo.fit(X, Y, wl.lengthscale, wl.outputscale, wl.noise, stream=stream)
     fit_ms = (time.perf_counter() - t0) * 1e3
     del m0
+
+    if a.calib_copy_mb > 0:
+        nbytes = a.calib_copy_mb << 20
+        src = torch.ones(nbytes // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     bo.profile_enable(True)
     torch.cuda.synchronize()

@@ -319,8 +319,9 @@ __global__ __launch_bounds__(256) void k_wty(const double* __restrict__ W,
   }
 }
 
-// Pack lower 16x16 blocks of W into MFMA A-fragment order:
-// Lp[k][blk(I,J)][lane][kk] = W[I*16 + lane%16][J*16 + 4*kk + lane/16].
+// Pack lower 16x16 blocks of W into MFMA A-fragment order (inner index of a
+// block split as 4 * lane-group + step):
+// Lp[k][blk(I,J)][lane][kk] = W[I*16 + lane%16][J*16 + 4*(lane/16) + kk].
 __global__ __launch_bounds__(256) void k_pack(const double* __restrict__ W, int64_t n,
                                               int nf, int nb, float* __restrict__ Lp) {
   const int k = blockIdx.y;
@@ -339,7 +340,7 @@ __global__ __launch_bounds__(256) void k_pack(const double* __restrict__ W, int6
   float* vp = reinterpret_cast<float*>(&v);
 #pragma unroll
   for (int kk = 0; kk < 4; ++kk) {
-    const int col = J * kBlk + 4 * kk + lane / 16;
+    const int col = J * kBlk + 4 * (lane / 16) + kk;
     vp[kk] = (row < n && col < n) ? static_cast<float>(Wk[(int64_t)row * nf + col]) : 0.f;
   }
   reinterpret_cast<float4*>(Lp)[(int64_t)k * nblk * 64 + g] = v;

@@ -4,11 +4,15 @@
 // joint posterior of the GP surrogates; the posterior of an exact GP at x*
 // is mu = k*^T alpha and Sigma = k(x*,x*) - v^T v with v = L^{-1} k*.
 //
-// One workgroup (4 waves) owns a tile of NT points:
+// One workgroup (8 waves, two per SIMD) owns a tile of NT points:
 //   phase 1 (VALU): the cross-covariance tile K*^T [n_pad x NT] of the
 //     ARD Matern-5/2 kernel, computed from lengthscale-scaled coordinates by
-//     direct differences (no |a|^2 + |b|^2 - 2ab cancellation), written to
-//     LDS in the MFMA B-fragment order; mu = K* alpha is reduced on the fly.
+//     direct differences (no |a|^2 + |b|^2 - 2ab cancellation). Each wave
+//     owns NT/8 candidates (coordinates in registers) and walks the training
+//     points one per lane, prefetching the next point, so every LDS store is
+//     a contiguous 256-byte run; mu = K* alpha is reduced with shuffles.
+//     K*^T is stored column-major with a column stride of n_pad + 4 floats
+//     (mod 32 banks: 4), which keeps the phase-2 16-byte reads conflict-free.
 //   phase 2 (MFMA): V = L^{-1} K*^T over the lower 16x16 blocks only,
 //     row block by row block. Waves take row blocks in a snake order so the
 //     triangle is split evenly; each row block's V rows live only in the
@@ -16,8 +20,11 @@
 //     (q = 1 needs only |v|^2; q > 1 also needs the cross products of batch
 //     members, which sit in the same 4-lane group of the accumulator and
 //     are exchanged with DPP quad permutes).
-//   L^{-1} is pre-packed by the fit so each lane fetches its four A operands
-//   of a 16x16 block with one 16-byte load (1 KiB per block per wave).
+//   The 16 inner indices of a block are split as k = 4g + kk between the
+//     four 16-lane groups g and the four MFMA steps kk, so each lane's four
+//     A operands are four consecutive columns of L^{-1} (pre-packed by the
+//     fit: one 16-byte load, 1 KiB per block per wave) and its four B
+//     operands are four consecutive rows of K*^T (one 16-byte LDS read).
 // MFMA: v_mfma_f32_16x16x4f32, A[i][k] from lane i + 16k, B[k][j] from lane
 // j + 16k, D[i][j] in lane j + 16(i/4), element i%4.
 #include <hip/hip_runtime.h>
@@ -42,7 +49,6 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 constexpr int kWaves = BO_POST_WAVES;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kPF = BO_POST_PF;
-constexpr int kCpt = 4;              // tile columns per thread in phase 1
 
 __device__ inline float matern52_f(float r2, float s) {
   const float r = __builtin_amdgcn_sqrtf(r2);
@@ -69,17 +75,27 @@ __device__ inline float quad_xor(float v, int x) {
   return __int_as_float(r);
 }
 
+// Column stride of the K*^T tile in LDS: n_pad rounded to 32 floats plus 4,
+// so the sixteen columns read by one 16-lane group start 4 banks apart.
+__host__ __device__ inline int kt_stride(int n_pad) { return (n_pad + 31) / 32 * 32 + 4; }
+
+// One 16x16 block pair: A fragment av, B fragments at bptr (+ b * 16 columns);
+// MFMAs alternate between the column blocks so consecutive ones are
+// independent.
 template <int NCB>
-__device__ inline void mfma_block(const float4 av, const float4* __restrict__ bptr,
+__device__ inline void mfma_block(const float4 av, const float* __restrict__ bptr, int bstride,
                                   floatx4 (&acc)[NCB]) {
+  float4 bv[NCB];
 #pragma unroll
-  for (int b = 0; b < NCB; ++b) {
-    const float4 bv = bptr[b * 64];
-    acc[b] = __builtin_amdgcn_mfma_f32_16x16x4f32(av.x, bv.x, acc[b], 0, 0, 0);
-    acc[b] = __builtin_amdgcn_mfma_f32_16x16x4f32(av.y, bv.y, acc[b], 0, 0, 0);
-    acc[b] = __builtin_amdgcn_mfma_f32_16x16x4f32(av.z, bv.z, acc[b], 0, 0, 0);
-    acc[b] = __builtin_amdgcn_mfma_f32_16x16x4f32(av.w, bv.w, acc[b], 0, 0, 0);
-  }
+  for (int b = 0; b < NCB; ++b) bv[b] = *reinterpret_cast<const float4*>(bptr + b * bstride);
+#pragma unroll
+  for (int b = 0; b < NCB; ++b) acc[b] = __builtin_amdgcn_mfma_f32_16x16x4f32(av.x, bv[b].x, acc[b], 0, 0, 0);
+#pragma unroll
+  for (int b = 0; b < NCB; ++b) acc[b] = __builtin_amdgcn_mfma_f32_16x16x4f32(av.y, bv[b].y, acc[b], 0, 0, 0);
+#pragma unroll
+  for (int b = 0; b < NCB; ++b) acc[b] = __builtin_amdgcn_mfma_f32_16x16x4f32(av.z, bv[b].z, acc[b], 0, 0, 0);
+#pragma unroll
+  for (int b = 0; b < NCB; ++b) acc[b] = __builtin_amdgcn_mfma_f32_16x16x4f32(av.w, bv[b].w, acc[b], 0, 0, 0);
 }
 
 template <int NT, int DX4, int Q>
@@ -87,29 +103,26 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
   extern __shared__ float smem[];
   constexpr int NCB = NT / 16;          // 16-column blocks per tile
   constexpr int NX = (Q > 1) ? Q : 1;   // per-point partial slots (diag + xors)
-  constexpr int NCG = NT / kCpt;        // column groups in phase 1
-  constexpr int RL = kThreads / NCG;    // row lanes in phase 1
+  constexpr int CPW = NT / kWaves;      // candidates per wave in phase 1
+  static_assert(CPW >= 1 && NT % kWaves == 0, "tile width vs waves");
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int n_pad = a.nb * kBlk;
-  float* Kt = smem;                                  // n_pad * NT
-  float* red = smem + (size_t)n_pad * NT;            // kWaves * NT * NX
-  float* mured = red + kWaves * NT * NX;             // kThreads * kCpt
-  float* kpp = mured + kThreads * kCpt;              // NT * 4 (prior cross-cov)
+  const int ks = kt_stride(n_pad);
+  float* Kt = smem;                                  // NT * ks, column-major
+  float* red = smem + (size_t)NT * ks;               // kWaves * NT * NX
+  float* mush = red + kWaves * NT * NX;              // NT
+  float* kpp = mush + NT;                            // NT * 4 (prior cross-cov)
   const int64_t p0 = (int64_t)blockIdx.x * NT;
 
-  // ---- phase 1: K*^T tile into LDS, mu partials -------------------------
-  // thread = (row lane rl, column group cg): kCpt candidates held in
-  // registers, one training point fetched per row and reused kCpt times.
+  // ---- phase 1: K*^T tile into LDS, mu -------------------------------------
   {
-    const int cg = tid % NCG;
-    const int rl = tid / NCG;
-    float c[kCpt][DX4 * 4];
-    bool valid[kCpt];
+    float c[CPW][DX4 * 4];
+    bool valid[CPW];
 #pragma unroll
-    for (int u = 0; u < kCpt; ++u) {
-      const int64_t p = p0 + cg * kCpt + u;
+    for (int u = 0; u < CPW; ++u) {
+      const int64_t p = p0 + wave * CPW + u;
       valid[u] = p < a.npts;
 #pragma unroll
       for (int t = 0; t < DX4 * 4; ++t) c[u][t] = 0.f;
@@ -120,62 +133,81 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
           if (t < a.d) c[u][t] = cp[t] * a.invls[t];
       }
     }
-    float mu_part[kCpt];
+    float mu_part[CPW];
 #pragma unroll
-    for (int u = 0; u < kCpt; ++u) mu_part[u] = 0.f;
-    const int col0 = cg * kCpt;
-    const int cb = col0 >> 4;
-    for (int row = rl; row < n_pad; row += RL) {
-      const float4* xr = reinterpret_cast<const float4*>(a.Xs + (size_t)row * a.dx);
+    for (int u = 0; u < CPW; ++u) mu_part[u] = 0.f;
+    // training point `row` per lane; the next one is fetched ahead
+    float4 xn[DX4];
+    float aln = 0.f;
+    if (lane < n_pad) {
+      const float4* xr = reinterpret_cast<const float4*>(a.Xs + (size_t)lane * a.dx);
+#pragma unroll
+      for (int t4 = 0; t4 < DX4; ++t4) xn[t4] = xr[t4];
+      aln = a.alpha[lane];
+    }
+    float* kcol = Kt + (size_t)(wave * CPW) * ks;
+    for (int row0 = 0; row0 < n_pad; row0 += 64) {
+      const int row = row0 + lane;
       float4 x[DX4];
 #pragma unroll
-      for (int t4 = 0; t4 < DX4; ++t4) x[t4] = xr[t4];
-      const float al = a.alpha[row];
-      const bool live = row < a.n;
-      const int J = row >> 4, r16 = row & 15;
-      float* dst = Kt + ((((J * NCB + cb) * 64 + (r16 & 3) * 16 + (col0 & 15)) << 2) + (r16 >> 2));
+      for (int t4 = 0; t4 < DX4; ++t4) x[t4] = xn[t4];
+      const float al = aln;
+      const int nrow = row + 64;
+      if (nrow < n_pad) {
+        const float4* xr = reinterpret_cast<const float4*>(a.Xs + (size_t)nrow * a.dx);
 #pragma unroll
-      for (int u = 0; u < kCpt; ++u) {
-        float r2 = 0.f;
+        for (int t4 = 0; t4 < DX4; ++t4) xn[t4] = xr[t4];
+        aln = a.alpha[nrow];
+      }
+      if (row < n_pad) {
+        const bool live = row < a.n;
 #pragma unroll
-        for (int t4 = 0; t4 < DX4; ++t4) {
-          const float d0 = c[u][4 * t4 + 0] - x[t4].x;
-          const float d1 = c[u][4 * t4 + 1] - x[t4].y;
-          const float d2 = c[u][4 * t4 + 2] - x[t4].z;
-          const float d3 = c[u][4 * t4 + 3] - x[t4].w;
-          r2 = fmaf(d0, d0, r2);
-          r2 = fmaf(d1, d1, r2);
-          r2 = fmaf(d2, d2, r2);
-          r2 = fmaf(d3, d3, r2);
+        for (int u = 0; u < CPW; ++u) {
+          float r2 = 0.f;
+#pragma unroll
+          for (int t4 = 0; t4 < DX4; ++t4) {
+            const float d0 = c[u][4 * t4 + 0] - x[t4].x;
+            const float d1 = c[u][4 * t4 + 1] - x[t4].y;
+            const float d2 = c[u][4 * t4 + 2] - x[t4].z;
+            const float d3 = c[u][4 * t4 + 3] - x[t4].w;
+            r2 = fmaf(d0, d0, r2);
+            r2 = fmaf(d1, d1, r2);
+            r2 = fmaf(d2, d2, r2);
+            r2 = fmaf(d3, d3, r2);
+          }
+          const float kv = (valid[u] && live) ? matern52_f(r2, a.s) : 0.f;
+          mu_part[u] = fmaf(al, kv, mu_part[u]);
+          kcol[(size_t)u * ks + row] = kv;
         }
-        const float kv = (valid[u] && live) ? matern52_f(r2, a.s) : 0.f;
-        mu_part[u] = fmaf(al, kv, mu_part[u]);
-        dst[u * 4] = kv;          // next column: next lane slot (4 floats on)
       }
     }
 #pragma unroll
-    for (int u = 0; u < kCpt; ++u) mured[(rl * NCG + cg) * kCpt + u] = mu_part[u];
+    for (int u = 0; u < CPW; ++u) {
+      float v = mu_part[u];
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+      if (lane == 0) mush[wave * CPW + u] = v;
+    }
     if (Q > 1) {
-      // prior covariance of each point with its batch mates (point ^ x)
+      // prior covariance of each point with its batch mates (point ^ x),
+      // one partner per lane
 #pragma unroll
-      for (int u = 0; u < kCpt; ++u) {
-        const int colu = col0 + u;
-        if (rl == 0) {
-          const int64_t p = p0 + colu;
-          for (int x = 1; x < Q; ++x) {
-            const int64_t pm = p ^ x;
-            float r2 = 0.f;
-            if (valid[u] && pm < a.npts) {
-              const float* cp = a.cand + pm * a.d;
+      for (int u = 0; u < CPW; ++u) {
+        const int colu = wave * CPW + u;
+        const int x = lane;
+        if (x >= 1 && x < Q) {
+          const int64_t pm = (p0 + colu) ^ x;
+          float r2 = 0.f;
+          if (valid[u] && pm < a.npts) {
+            const float* cp = a.cand + pm * a.d;
 #pragma unroll
-              for (int t = 0; t < DX4 * 4; ++t)
-                if (t < a.d) {
-                  const float dd = c[u][t] - cp[t] * a.invls[t];
-                  r2 = fmaf(dd, dd, r2);
-                }
-            }
-            kpp[colu * 4 + x] = matern52_f(r2, a.s);
+            for (int t = 0; t < DX4 * 4; ++t)
+              if (t < a.d) {
+                const float dd = c[u][t] - cp[t] * a.invls[t];
+                r2 = fmaf(dd, dd, r2);
+              }
           }
+          kpp[colu * 4 + x] = matern52_f(r2, a.s);
         }
       }
     }
@@ -192,7 +224,9 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
     for (int x = 0; x < NX; ++x) gx[b][x] = 0.f;
   }
   const float4* Lp4 = reinterpret_cast<const float4*>(a.Lp);
-  const float4* Kt4 = reinterpret_cast<const float4*>(Kt) + lane;
+  // B fragments: column (b*16 + lane%16), rows J*16 + 4*(lane/16) .. +3
+  const float* Kb = Kt + (size_t)(lane & 15) * ks + 4 * (lane >> 4);
+  const int bstride = 16 * ks;
   for (int it = 0;; ++it) {
     const int I = snake_block(it, wave);
     if (I >= a.nb) break;
@@ -211,12 +245,12 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
       for (int u = 0; u < kPF; ++u) {
         const float4 cur = ring[u];
         if (J + u + kPF < nJ) ring[u] = Ablk[(size_t)(J + u + kPF) * 64];
-        mfma_block<NCB>(cur, Kt4 + (J + u) * NCB * 64, acc);
+        mfma_block<NCB>(cur, Kb + (J + u) * 16, bstride, acc);
       }
     }
 #pragma unroll
     for (int u = 0; u < kPF; ++u)
-      if (J + u < nJ) mfma_block<NCB>(ring[u], Kt4 + (J + u) * NCB * 64, acc);
+      if (J + u < nJ) mfma_block<NCB>(ring[u], Kb + (J + u) * 16, bstride, acc);
 #pragma unroll
     for (int b = 0; b < NCB; ++b) {
 #pragma unroll
@@ -259,9 +293,7 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
     for (int w = 0; w < kWaves; ++w)
 #pragma unroll
       for (int x = 0; x < NX; ++x) tot[x] += red[(w * NT + tid) * NX + x];
-    // mu: partials of column tid live at (rl, cg = tid / kCpt, u = tid % kCpt)
-    float mu = 0.f;
-    for (int rl = 0; rl < RL; ++rl) mu += mured[(rl * NCG + tid / kCpt) * kCpt + tid % kCpt];
+    const float mu = mush[tid];
     const float var = a.s - tot[0];
     if (valid) {
       a.mu[p * a.m + a.k] = mu;
@@ -325,8 +357,8 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
 template <int NT, int DX4, int Q>
 hipError_t launch_t(const PosteriorArgs& a, hipStream_t st) {
   const int n_pad = a.nb * kBlk;
-  const size_t lds = sizeof(float) * ((size_t)n_pad * NT + kWaves * NT * ((Q > 1) ? Q : 1) +
-                                      kThreads * kCpt + NT * 4);
+  const size_t lds = sizeof(float) * ((size_t)NT * kt_stride(n_pad) +
+                                      kWaves * NT * ((Q > 1) ? Q : 1) + NT + NT * 4);
   static bool attr_set = false;
   if (!attr_set) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_posterior<NT, DX4, Q>),
@@ -372,8 +404,8 @@ int posterior_tile(int nb) { return (nb * kBlk <= 1024) ? BO_POST_NT_SMALL_N : 1
 
 size_t posterior_lds_bytes(int nb, int q) {
   const int NT = posterior_tile(nb);
-  return sizeof(float) * ((size_t)nb * kBlk * NT + kWaves * NT * ((q > 1) ? q : 1) +
-                          kThreads * kCpt + NT * 4);
+  return sizeof(float) * ((size_t)NT * kt_stride(nb * kBlk) + kWaves * NT * ((q > 1) ? q : 1) +
+                          NT + NT * 4);
 }
 
 hipError_t launch_posterior(const PosteriorArgs& a, hipStream_t st) {
