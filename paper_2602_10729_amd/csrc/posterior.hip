@@ -79,15 +79,11 @@ __device__ inline float quad_xor(float v, int x) {
 // so the sixteen columns read by one 16-lane group start 4 banks apart.
 __host__ __device__ inline int kt_stride(int n_pad) { return (n_pad + 31) / 32 * 32 + 4; }
 
-// One 16x16 block pair: A fragment av, B fragments at bptr (+ b * 16 columns);
-// MFMAs alternate between the column blocks so consecutive ones are
+// One 16x16 block pair: A fragment av, B fragments bv (one per 16-column
+// block); MFMAs alternate between the column blocks so consecutive ones are
 // independent.
 template <int NCB>
-__device__ inline void mfma_block(const float4 av, const float* __restrict__ bptr, int bstride,
-                                  floatx4 (&acc)[NCB]) {
-  float4 bv[NCB];
-#pragma unroll
-  for (int b = 0; b < NCB; ++b) bv[b] = *reinterpret_cast<const float4*>(bptr + b * bstride);
+__device__ inline void mfma_step(const float4 av, const float4 (&bv)[NCB], floatx4 (&acc)[NCB]) {
 #pragma unroll
   for (int b = 0; b < NCB; ++b) acc[b] = __builtin_amdgcn_mfma_f32_16x16x4f32(av.x, bv[b].x, acc[b], 0, 0, 0);
 #pragma unroll
@@ -107,7 +103,8 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
   static_assert(CPW >= 1 && NT % kWaves == 0, "tile width vs waves");
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  // wave index as a scalar: row-block control flow below stays uniform
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n_pad = a.nb * kBlk;
   const int ks = kt_stride(n_pad);
   float* Kt = smem;                                  // NT * ks, column-major
@@ -233,24 +230,53 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
     floatx4 acc[NCB];
 #pragma unroll
     for (int b = 0; b < NCB; ++b) acc[b] = floatx4{0.f, 0.f, 0.f, 0.f};
-    // row block I of L^{-1}: blocks (I, 0..I), 1 KiB each, consecutive
+    // row block I of L^{-1}: blocks (I, 0..I), 1 KiB each, consecutive.
+    // A fragments run kPF blocks ahead, B fragments one block ahead; loads
+    // past block I are clamped to I (in bounds, never consumed).
     const float4* Ablk = Lp4 + (size_t)I * (I + 1) / 2 * 64 + lane;
     const int nJ = I + 1;
     float4 ring[kPF];
 #pragma unroll
-    for (int u = 0; u < kPF; ++u) ring[u] = (u < nJ) ? Ablk[u * 64] : float4{0.f, 0.f, 0.f, 0.f};
+    for (int u = 0; u < kPF; ++u) ring[u] = Ablk[(size_t)min(u, I) * 64];
+    float4 bv[NCB];
+#pragma unroll
+    for (int b = 0; b < NCB; ++b) bv[b] = *reinterpret_cast<const float4*>(Kb + b * bstride);
     int J = 0;
+    // Each step issues the loads for later steps first, then its eight
+    // MFMAs; scheduling barriers keep the compiler from sinking the loads
+    // next to their consumers (which would expose their latency).
     for (; J + kPF <= nJ; J += kPF) {
 #pragma unroll
       for (int u = 0; u < kPF; ++u) {
         const float4 cur = ring[u];
-        if (J + u + kPF < nJ) ring[u] = Ablk[(size_t)(J + u + kPF) * 64];
-        mfma_block<NCB>(cur, Kb + (J + u) * 16, bstride, acc);
+        ring[u] = Ablk[(size_t)min(J + u + kPF, I) * 64];
+        const int Jn = min(J + u + 1, I);
+        float4 bn[NCB];
+#pragma unroll
+        for (int b = 0; b < NCB; ++b)
+          bn[b] = *reinterpret_cast<const float4*>(Kb + b * bstride + Jn * 16);
+        __builtin_amdgcn_sched_barrier(0);
+        mfma_step<NCB>(cur, bv, acc);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int b = 0; b < NCB; ++b) bv[b] = bn[b];
       }
     }
 #pragma unroll
-    for (int u = 0; u < kPF; ++u)
-      if (J + u < nJ) mfma_block<NCB>(ring[u], Kb + (J + u) * 16, bstride, acc);
+    for (int u = 0; u < kPF; ++u) {
+      if (J + u < nJ) {
+        const int Jn = min(J + u + 1, I);
+        float4 bn[NCB];
+#pragma unroll
+        for (int b = 0; b < NCB; ++b)
+          bn[b] = *reinterpret_cast<const float4*>(Kb + b * bstride + Jn * 16);
+        __builtin_amdgcn_sched_barrier(0);
+        mfma_step<NCB>(ring[u], bv, acc);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int b = 0; b < NCB; ++b) bv[b] = bn[b];
+      }
+    }
 #pragma unroll
     for (int b = 0; b < NCB; ++b) {
 #pragma unroll
