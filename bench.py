@@ -45,6 +45,24 @@ def posterior_flops_per_point(n: int, d: int, q: int) -> float:
     return n * n + 2.0 * n * d + 2.0 * n + 2.0 * n * (q + 1) / 2.0
 
 
+def recorded_traffic(n_launch_flops_workload: str):
+    """HBM bytes per posterior launch from the committed counter summary
+    (FETCH_SIZE + WRITE_SIZE, copy-calibrated), or None when the kernel source
+    has changed since those counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "posterior_counters.json")
+    try:
+        rec = json.load(open(path))
+        src = open(os.path.join(ROOT, rec["source"]), "rb").read()
+    except (OSError, ValueError, KeyError):
+        return None
+    if hashlib.sha256(src).hexdigest() != rec.get("source_sha256"):
+        return None
+    if rec.get("workload", "").split(" ")[0] != n_launch_flops_workload:
+        return None
+    return rec["traffic_bytes_per_launch"]
+
+
 def cpu_baseline(wl, sample: int):
     import oracle as O
     try:
@@ -175,7 +193,7 @@ def main(argv=None):
             "peak": PEAK_FP32_MFMA_TFLOPS,
             "unit": "TFLOP/s",
             "frac": achieved / PEAK_FP32_MFMA_TFLOPS,
-            "traffic": None,
+            "traffic": recorded_traffic("headline") if a.config == 3 else None,
             "launch_ms": launch_ms,
             "flops_per_launch": flops_launch,
         },

@@ -368,7 +368,7 @@ bo_status bo_fit(const float* X, const float* Y, int64_t n, int32_t d, int32_t m
   if ((s = palloc(&M->Lp, (size_t)m * M->lp_per_obj, st, "packed inverse")) != BO_OK) return bail(s);
 
   std::vector<double> hyp((size_t)m * d + 2 * m);
-  for (int i = 0; i < m * d; ++i) hyp[i] = lengthscale[i];
+  for (int i = 0; i < m * d; ++i) hyp[i] = 1.0 / static_cast<double>(lengthscale[i]);
   for (int k = 0; k < m; ++k) {
     hyp[(size_t)m * d + k] = outputscale[k];
     hyp[(size_t)m * d + m + k] = noise[k];
@@ -383,10 +383,10 @@ bo_status bo_fit(const float* X, const float* Y, int64_t n, int32_t d, int32_t m
   if (e == hipSuccess) e = hipMemsetAsync(fs.flag, 0, sizeof(int), st);
   if (e != hipSuccess) return bail(hip_fail(e, "bo_fit: upload"));
 
-  const double* d_ls = fs.hyp;
+  const double* d_ils = fs.hyp;
   const double* d_os = fs.hyp + (size_t)m * d;
   const double* d_noise = d_os + m;
-  if ((s = after_launch(launch_gram(X, n, d, m, nf, d_ls, d_os, d_noise, fs.A, st), st, "gram")) != BO_OK) return bail(s);
+  if ((s = after_launch(launch_gram(X, n, d, m, nf, d_ils, d_os, d_noise, fs.A, st), st, "gram")) != BO_OK) return bail(s);
   if ((s = after_launch(launch_cholesky(fs.A, fs.W, nf, m, fs.flag, st), st, "cholesky")) != BO_OK) return bail(s);
   if ((s = after_launch(launch_alpha(fs.W, Y, n, m, nf, M->n_pad, fs.tmp, M->alpha, st), st, "alpha")) != BO_OK) return bail(s);
   if ((s = after_launch(launch_pack(fs.W, n, m, nf, M->nb, M->Lp, X, d, M->dx, M->invls, M->Xs, st), st, "pack")) != BO_OK) return bail(s);
@@ -627,11 +627,12 @@ bo_status bo_cholesky_test(const float* A, int64_t n, float* L, void* stream) {
   FitScratch fs;
   fs.st = st;
   if ((s = palloc(&fs.A, (size_t)nf * nf, st, "matrix")) != BO_OK) return s;
+  if ((s = palloc(&fs.W, (size_t)nf * nf, st, "inverse")) != BO_OK) return s;
   if ((s = palloc(&fs.flag, 1, st, "flag")) != BO_OK) return s;
   hipError_t e = hipMemsetAsync(fs.flag, 0, sizeof(int), st);
   if (e != hipSuccess) return hip_fail(e, "bo_cholesky_test: memset");
   if ((s = after_launch(launch_f32_to_padded(A, n, nf, fs.A, st), st, "pad")) != BO_OK) return s;
-  if ((s = after_launch(launch_cholesky(fs.A, nullptr, nf, 1, fs.flag, st), st, "cholesky")) != BO_OK) return s;
+  if ((s = after_launch(launch_cholesky(fs.A, fs.W, nf, 1, fs.flag, st), st, "cholesky")) != BO_OK) return s;
   if ((s = after_launch(launch_lower_to_f32(fs.A, n, nf, L, st), st, "convert")) != BO_OK) return s;
   int flag = 0;
   e = hipMemcpyAsync(&flag, fs.flag, sizeof(int), hipMemcpyDeviceToHost, st);

@@ -62,12 +62,13 @@ struct Model {
 // All return hipSuccess or the launch error.
 
 // Gram matrices K_k + eta_k I in fp64 for all objectives, padded to
-// n_fit x n_fit with an identity tail. A: [m][n_fit][n_fit].
+// n_fit x n_fit with an identity tail; only the lower block triangle (64x64
+// blocks) is written. ils: 1 / lengthscale [m][d]. A: [m][n_fit][n_fit].
 hipError_t launch_gram(const float* X, int64_t n, int d, int m, int n_fit,
-                       const double* ls, const double* os, const double* noise,
+                       const double* ils, const double* os, const double* noise,
                        double* A, hipStream_t st);
-// Blocked right-looking Cholesky of m matrices [m][nf][nf] (lower, in place).
-// With W != nullptr it also leaves W = L^{-1} (lower, [m][nf][nf]).
+// Blocked right-looking Cholesky of m matrices [m][nf][nf] (lower, in place);
+// also leaves W = L^{-1} (lower, [m][nf][nf]).
 // *flag is set non-zero on a non-positive or non-finite pivot.
 hipError_t launch_cholesky(double* A, double* W, int nf, int m, int* flag,
                            hipStream_t st);

@@ -13,16 +13,17 @@
 //
 // Blocked right-looking Cholesky with 64x64 blocks that carries the inverse
 // along. W starts as the identity; after step kb its block rows <= kb hold
-// L^{-1} and the rows below hold R_i = delta_i - sum_{k<=kb} L_ik W_k. Step kb:
-//   panel:  rows below the diagonal solve x L_kk^T = a (forward substitution,
-//           one thread per row), and W's block row kb solves L_kk w = r
-//           (one thread per column);
+// L^{-1} and the rows below hold R_i = delta_i - sum_{k<=kb} L_ik W_k.
+// Every diagonal block is factored and inverted in one workgroup
+// (D_kk = L_kk^{-1} lands in W's diagonal block). Step kb:
+//   panel:  L_ik = A_ik D_kk^T for the rows below, W_kj = D_kk R_kj for the
+//           columns left of the diagonal (64x64x64 tiles);
 //   update: trailing A_ic -= L_ik L_ck^T (kb < c <= i) and R_ij -= L_ik W_kj
 //           (i > kb, j <= kb), 64x64x64 tiles; the workgroup that updates
-//           the next diagonal tile factors it at once (one wave, row per
-//           lane), so no separate factor launch is needed after the first.
-// Two launches per block column; the serial chain is one 64-step
-// factorisation plus two substitutions per block column.
+//           the next diagonal tile factors and inverts it at once, so no
+//           separate factor launch is needed after the first.
+// Two launches per block column; the serial chain is one 64-step factor and
+// one 64-step inverse per block column.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -41,20 +42,26 @@ __device__ inline double matern52_d(double r2, double s) {
   return s * (1.0 + c * r + (5.0 / 3.0) * r2) * exp(-c * r);
 }
 
-__global__ void k_gram(const float* __restrict__ X, int64_t n, int d, int nf,
-                       const double* __restrict__ ls, const double* __restrict__ os,
-                       const double* __restrict__ noise, double* __restrict__ A) {
+// Gram matrix in fp64, lower block triangle only (tiles above the diagonal
+// blocks are never read by the factorisation). ils: 1 / lengthscale.
+__global__ __launch_bounds__(256) void k_gram(const float* __restrict__ X, int64_t n, int d,
+                                              int nf, const double* __restrict__ ils,
+                                              const double* __restrict__ os,
+                                              const double* __restrict__ noise,
+                                              double* __restrict__ A) {
   const int k = blockIdx.z;
-  const int i = blockIdx.y * 16 + threadIdx.y;
-  const int j = blockIdx.x * 16 + threadIdx.x;
+  const int bi = blockIdx.y, bj = blockIdx.x;      // 16x16 tiles
+  if ((bj >> 2) > (bi >> 2)) return;                // strictly above the 64-block diagonal
+  const int i = bi * 16 + threadIdx.y;
+  const int j = bj * 16 + threadIdx.x;
   if (i >= nf || j >= nf) return;
   double v;
   if (i < n && j < n) {
     double r2 = 0.0;
     for (int t = 0; t < d; ++t) {
       const double diff = (static_cast<double>(X[(int64_t)i * d + t]) -
-                           static_cast<double>(X[(int64_t)j * d + t])) / ls[k * d + t];
-      r2 += diff * diff;
+                           static_cast<double>(X[(int64_t)j * d + t])) * ils[k * d + t];
+      r2 = fma(diff, diff, r2);
     }
     v = matern52_d(r2, os[k]);
     if (i == j) v += noise[k];
@@ -64,47 +71,87 @@ __global__ void k_gram(const float* __restrict__ X, int64_t n, int d, int nf,
   A[((int64_t)k * nf + i) * nf + j] = v;
 }
 
-// Factor the symmetric 64x64 block in LDS (lower triangle read) in place:
-// wave 0 holds row `lane` in registers; pivots and the scaled column are
-// read across lanes with readlane (j and c are compile-time after unrolling).
-// Zeros are written above the diagonal. A non-positive or non-finite pivot
-// sets *bad and is replaced by 1 so the rest stays finite.
-__device__ inline double readlane_d(double v, int l) {
-  const long long b = __double_as_longlong(v);
-  const int lo = __builtin_amdgcn_readlane(static_cast<int>(b & 0xffffffffll), l);
-  const int hi = __builtin_amdgcn_readlane(static_cast<int>(b >> 32), l);
-  return __longlong_as_double((static_cast<long long>(hi) << 32) |
-                              (static_cast<unsigned int>(lo)));
-}
-
-__device__ __forceinline__ void potrf64_wave0(double (*a)[LDP], int* bad_flag) {
+// Factor the symmetric 64x64 block held in LDS `a` (lower triangle read) and
+// invert the factor: on return a = L (zeros above the diagonal) and
+// x = L^{-1}. All 256 threads take part; thread (c = tid % 64, g = tid / 64)
+// keeps rows 16g..16g+15 of column c in registers, indexed only by unrolled
+// constants; g is scalar. The structural masks (row >= column) are 0/1
+// multipliers fixed per thread, so the per-step update has no branches.
+// Factor step j: column j (published by its owners at the end of step j-1,
+// double-buffered) gives the pivot and the scaled column; the owners write
+// column j of L; every column c > j updates its rows; the owners of column
+// j+1 publish it. Inverse step j: row j of X (published the step before) is
+// scaled by 1/L_jj, written to x and applied to the rows below.
+// A non-positive or non-finite pivot sets *flag and is replaced by 1.
+// Scratch: colj [2*64], rowb [2*64], invd [64].
+__device__ __forceinline__ void chol_inv64(double (*__restrict__ a)[LDP],
+                                           double (*__restrict__ x)[LDP],
+                                           double* __restrict__ colj,
+                                           double* __restrict__ rowb,
+                                           double* __restrict__ invd, int* flag) {
   const int tid = threadIdx.x;
-  if (tid >= 64) return;
-  const int i = tid;
-  double r[B];
+  const int c = tid & 63;
+  const int g = __builtin_amdgcn_readfirstlane(tid >> 6);
+  double r[16], mge[16];
 #pragma unroll
-  for (int c = 0; c < B; ++c) r[c] = a[i][c];
-  bool bad = false;
+  for (int k = 0; k < 16; ++k) {
+    r[k] = a[16 * g + k][c];
+    mge[k] = (16 * g + k >= c) ? 1.0 : 0.0;
+  }
+  if (c == 0) {
 #pragma unroll
+    for (int k = 0; k < 16; ++k) colj[16 * g + k] = r[k];
+  }
   for (int j = 0; j < B; ++j) {
-    double piv = readlane_d(r[j], j);
-    if (!(piv > 0.0) || !isfinite(piv)) {
-      bad = true;
-      piv = 1.0;
-    }
-    const double djj = sqrt(piv);
-    const double inv = 1.0 / djj;
-    r[j] = (i == j) ? djj : r[j] * inv;      // rows above j keep their value
+    __syncthreads();
+    const double* cj = colj + (j & 1) * B;
+    double piv = cj[j];
+    const bool bad = !(piv > 0.0) || !isfinite(piv);
+    if (bad) piv = 1.0;
+    const double d = sqrt(piv);
+    const double inv = 1.0 / d;
+    if (c == j) {
 #pragma unroll
-    for (int c = j + 1; c < B; ++c) {
-      const double lcj = readlane_d(r[j], c);  // L[c][j] (scaled on lane c)
-      r[c] = fma(-r[j], lcj, r[c]);            // meaningful for c <= i only
+      for (int k = 0; k < 16; ++k) {
+        const int i = 16 * g + k;
+        a[i][j] = (i > j) ? r[k] * inv : ((i == j) ? d : 0.0);
+      }
+      if (g == 0) {
+        invd[j] = inv;
+        if (bad) atomicOr(flag, 1);
+      }
+    }
+    double cv[16];
+#pragma unroll
+    for (int k = 0; k < 16; ++k) cv[k] = cj[16 * g + k];
+    const double lcj = (c > j) ? cj[c] * inv * inv : 0.0;   // l_cj / d folded in
+#pragma unroll
+    for (int k = 0; k < 16; ++k) r[k] = fma(-cv[k] * mge[k], lcj, r[k]);
+    if (c == j + 1) {
+      double* cn = colj + ((j + 1) & 1) * B;
+#pragma unroll
+      for (int k = 0; k < 16; ++k) cn[16 * g + k] = r[k];
     }
   }
+  // inverse: X = I; step j: X_j <- X_j / L_jj (final), X_i -= L_ij X_j (i > j)
 #pragma unroll
-  for (int c = 0; c < B; ++c) a[i][c] = (c <= i) ? r[c] : 0.0;
-  if (bad && i == 0) atomicOr(bad_flag, 1);
-  // lanes see the same `bad` (pivots are wave-uniform), so lane 0 reports
+  for (int k = 0; k < 16; ++k) r[k] = (16 * g + k == c) ? 1.0 : 0.0;
+  if (g == 0) rowb[c] = r[0];               // row 0 of X before scaling
+  for (int j = 0; j < B; ++j) {
+    __syncthreads();
+    const double xj = rowb[(j & 1) * B + c] * invd[j];
+    if (g == (j >> 4)) x[j][c] = xj;
+    double av[16];
+#pragma unroll
+    for (int k = 0; k < 16; ++k) av[k] = a[16 * g + k][j];
+#pragma unroll
+    for (int k = 0; k < 16; ++k)
+      if (16 * g + k > j) r[k] = fma(-av[k], xj, r[k]);
+#pragma unroll
+    for (int k = 0; k < 16; ++k)
+      if (16 * g + k == j + 1) rowb[((j + 1) & 1) * B + c] = r[k];
+  }
+  __syncthreads();
 }
 
 __device__ inline void load_block(double (*dst)[LDP], const double* src, int ld) {
@@ -121,73 +168,20 @@ __device__ inline void store_block(double* dst, int ld, const double (*srcb)[LDP
   }
 }
 
-// First diagonal block (kb = 0) of every objective.
-__global__ __launch_bounds__(64) void k_potrf_first(double* __restrict__ A, int nf,
-                                                    int* __restrict__ flag) {
+// First diagonal block (kb = 0) of every objective: L into A, L^{-1} into W.
+__global__ __launch_bounds__(256) void k_factor_first(double* __restrict__ A,
+                                                      double* __restrict__ W, int nf,
+                                                      int* __restrict__ flag) {
   __shared__ double a[B][LDP];
+  __shared__ double x[B][LDP];
+  __shared__ double colj[2 * B], rowb[2 * B], invd[B];
   double* Ak = A + (int64_t)blockIdx.x * nf * nf;
+  double* Wk = W + (int64_t)blockIdx.x * nf * nf;
   load_block(a, Ak, nf);
   __syncthreads();
-  potrf64_wave0(a, flag);
-  __syncthreads();
+  chol_inv64(a, x, colj, rowb, invd, flag);
   store_block(Ak, nf, a);
-}
-
-// Panel of step kb: blocks [0, nrow_blk) solve rows of A below the diagonal,
-// blocks [nrow_blk, ...) solve columns of W's block row kb (if W != null).
-__global__ __launch_bounds__(256) void k_panel(double* __restrict__ A, double* __restrict__ W,
-                                               int nf, int kb, int nrow_blk) {
-  __shared__ double l[B][LDP];
-  __shared__ double dinv[B];
-  const int k = blockIdx.y;
-  double* Ak = A + (int64_t)k * nf * nf;
-  const int o = kb * B;
-  load_block(l, Ak + (int64_t)o * nf + o, nf);
-  __syncthreads();
-  if (threadIdx.x < B) dinv[threadIdx.x] = 1.0 / l[threadIdx.x][threadIdx.x];
-  __syncthreads();
-  if ((int)blockIdx.x < nrow_blk) {
-    // row i of the panel: x L^T = a  =>  x_j = (a_j - sum_{t<j} x_t L[j][t]) / L[j][j]
-    const int i = o + B + blockIdx.x * 256 + threadIdx.x;
-    if (i >= nf) return;
-    double* row = Ak + (int64_t)i * nf + o;
-    double x[B];
-#pragma unroll
-    for (int j = 0; j < B; ++j) x[j] = row[j];
-#pragma unroll
-    for (int j = 0; j < B; ++j) {
-      double s0 = x[j], s1 = 0.0;
-#pragma unroll
-      for (int t = 0; t < j; t += 2) {
-        s0 = fma(-x[t], l[j][t], s0);
-        if (t + 1 < j) s1 = fma(-x[t + 1], l[j][t + 1], s1);
-      }
-      x[j] = (s0 + s1) * dinv[j];
-    }
-#pragma unroll
-    for (int j = 0; j < B; ++j) row[j] = x[j];
-  } else {
-    if (W == nullptr) return;
-    // column c of W's block row kb: L_kk w = r  =>  w_j = (r_j - sum_{t<j} L[j][t] w_t) / L[j][j]
-    const int c = (blockIdx.x - nrow_blk) * 256 + threadIdx.x;
-    if (c >= o + B) return;
-    double* Wk = W + (int64_t)k * nf * nf;
-    double w[B];
-#pragma unroll
-    for (int j = 0; j < B; ++j) w[j] = Wk[(int64_t)(o + j) * nf + c];
-#pragma unroll
-    for (int j = 0; j < B; ++j) {
-      double s0 = w[j], s1 = 0.0;
-#pragma unroll
-      for (int t = 0; t < j; t += 2) {
-        s0 = fma(-l[j][t], w[t], s0);
-        if (t + 1 < j) s1 = fma(-l[j][t + 1], w[t + 1], s1);
-      }
-      w[j] = (s0 + s1) * dinv[j];
-    }
-#pragma unroll
-    for (int j = 0; j < B; ++j) Wk[(int64_t)(o + j) * nf + c] = w[j];
-  }
+  store_block(Wk, nf, x);
 }
 
 // 64x64x64 product helper: acc[r][c] (4x4 per thread) += sum_t P[ty*4+r][t] * Q[tx*4+c][t].
@@ -206,13 +200,54 @@ __device__ inline void gemm_nt_64(const double (*P)[LDP], const double (*Q)[LDP]
   }
 }
 
-// Update of step kb. Tile t < T(T+1)/2: trailing A tile; the rest: R tiles of
-// W (if W != null). Tile 0 is the next diagonal block, factored right after
-// its update.
+// Panel of step kb, with D = L_kk^{-1} (held in W's diagonal block kb):
+// tiles t < T: A[kb+1+t][kb] <- A[kb+1+t][kb] D^T (rows below the diagonal);
+// tiles T <= t < T + kb: W[kb][jb] <- D R[kb][jb] for jb = t - T (< kb).
+__global__ __launch_bounds__(256) void k_panel(double* __restrict__ A, double* __restrict__ W,
+                                               int nf, int kb) {
+  __shared__ double p[B][LDP];
+  __shared__ double q[B][LDP];
+  const int k = blockIdx.y;
+  const int nbk = nf / B;
+  const int T = nbk - kb - 1;
+  const int t = blockIdx.x;
+  const int tid = threadIdx.x, tx = tid % 16, ty = tid / 16;
+  double* Ak = A + (int64_t)k * nf * nf;
+  double* Wk = W + (int64_t)k * nf * nf;
+  const int o = kb * B;
+  const double* D = Wk + (int64_t)o * nf + o;
+  double* dst;
+  if (t < T) {
+    const int ib = kb + 1 + t;
+    dst = Ak + (int64_t)ib * B * nf + o;
+    load_block(p, dst, nf);                 // P = A[ib][kb]
+    load_block(q, D, nf);                   // Q[c][s] = D[c][s]  ->  P D^T
+  } else {
+    const int jb = t - T;
+    dst = Wk + (int64_t)o * nf + jb * B;
+    load_block(p, D, nf);                   // P = D
+    for (int e = tid; e < B * B; e += 256) {  // Q = R^T  ->  D R
+      const int i = e >> 6, c = e & 63;
+      q[c][i] = dst[(int64_t)i * nf + c];
+    }
+  }
+  __syncthreads();
+  double acc[4][4] = {};
+  gemm_nt_64(p, q, acc, ty, tx);
+#pragma unroll
+  for (int r = 0; r < 4; ++r)
+#pragma unroll
+    for (int c = 0; c < 4; ++c) dst[(int64_t)(ty * 4 + r) * nf + tx * 4 + c] = acc[r][c];
+}
+
+// Update of step kb. Tile t < T(T+1)/2: trailing A tile; the rest: R tiles
+// of W. Tile 0 is the next diagonal block, factored and inverted right after
+// its update (L into A, L^{-1} into W's diagonal block kb+1).
 __global__ __launch_bounds__(256) void k_update(double* __restrict__ A, double* __restrict__ W,
                                                 int nf, int kb, int* __restrict__ flag) {
   __shared__ double p[B][LDP];
   __shared__ double q[B][LDP];
+  __shared__ double colj[2 * B], rowb[2 * B], invd[B];
   const int k = blockIdx.y;
   const int nbk = nf / B;
   const int T = nbk - kb - 1;
@@ -220,7 +255,7 @@ __global__ __launch_bounds__(256) void k_update(double* __restrict__ A, double* 
   const int t = blockIdx.x;
   const int tid = threadIdx.x, tx = tid % 16, ty = tid / 16;
   double* Ak = A + (int64_t)k * nf * nf;
-  double* Wk = (W != nullptr) ? W + (int64_t)k * nf * nf : nullptr;
+  double* Wk = W + (int64_t)k * nf * nf;
   const int o = kb * B;
   double* dst;
   if (t < nsyrk) {
@@ -239,8 +274,7 @@ __global__ __launch_bounds__(256) void k_update(double* __restrict__ A, double* 
     const int ib = kb + 1 + u / (kb + 1);
     const int jb = u % (kb + 1);
     load_block(p, Ak + (int64_t)ib * B * nf + o, nf);       // L[ib][kb]
-    // q = W[kb][jb]^T so that gemm_nt forms P * W[kb][jb]
-    for (int e = tid; e < B * B; e += 256) {
+    for (int e = tid; e < B * B; e += 256) {                 // q = W[kb][jb]^T
       const int i = e >> 6, c = e & 63;
       q[c][i] = Wk[(int64_t)(o + i) * nf + jb * B + c];
     }
@@ -258,16 +292,17 @@ __global__ __launch_bounds__(256) void k_update(double* __restrict__ A, double* 
       *d = acc[rr][c];
     }
   if (t == 0) {
-    // next diagonal block: stage the updated tile and factor it
+    // next diagonal block: stage the updated tile, factor and invert it
     __syncthreads();
 #pragma unroll
     for (int rr = 0; rr < 4; ++rr)
 #pragma unroll
       for (int c = 0; c < 4; ++c) p[ty * 4 + rr][tx * 4 + c] = acc[rr][c];
     __syncthreads();
-    potrf64_wave0(p, flag);
-    __syncthreads();
+    chol_inv64(p, q, colj, rowb, invd, flag);
+    const int o1 = o + B;
     store_block(dst, nf, p);
+    store_block(Wk + (int64_t)o1 * nf + o1, nf, q);
   }
 }
 
@@ -295,26 +330,34 @@ __global__ __launch_bounds__(256) void k_wy(const double* __restrict__ W,
   if (lane == 0) tmp[(int64_t)k * nf + row] = (row < n) ? acc : 0.0;
 }
 
-// alpha_k[j] = sum_{i >= j} W_k[i][j] tmp_k[i]: 64 columns per block, four
-// row phases per column (coalesced row reads), combined in LDS.
+// alpha_k[j] = sum_{i >= j} W_k[i][j] tmp_k[i]: 16 columns per block, 16 row
+// phases per column with two accumulators each (several loads in flight),
+// combined in LDS.
 __global__ __launch_bounds__(256) void k_wty(const double* __restrict__ W,
                                              const double* __restrict__ tmp,
                                              int64_t n, int nf, int n_pad,
                                              float* __restrict__ alpha) {
-  __shared__ double part[4][64];
+  __shared__ double part[16][17];
   const int k = blockIdx.y;
-  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-  const int j = blockIdx.x * 64 + tx;
-  double acc = 0.0;
+  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+  const int j = blockIdx.x * 16 + tx;
+  double a0 = 0.0, a1 = 0.0;
   if (j < n) {
     const double* Wk = W + (int64_t)k * nf * nf;
     const double* tk = tmp + (int64_t)k * nf;
-    for (int64_t i = j + ty; i < n; i += 4) acc = fma(Wk[i * nf + j], tk[i], acc);
+    int64_t i = j + ty;
+    for (; i + 16 < n; i += 32) {
+      a0 = fma(Wk[i * nf + j], tk[i], a0);
+      a1 = fma(Wk[(i + 16) * nf + j], tk[i + 16], a1);
+    }
+    if (i < n) a0 = fma(Wk[i * nf + j], tk[i], a0);
   }
-  part[ty][tx] = acc;
+  part[ty][tx] = a0 + a1;
   __syncthreads();
   if (ty == 0 && j < n_pad) {
-    const double v = (part[0][tx] + part[1][tx]) + (part[2][tx] + part[3][tx]);
+    double v = 0.0;
+#pragma unroll
+    for (int t = 0; t < 16; ++t) v += part[t][tx];
     alpha[(int64_t)k * n_pad + j] = (j < n) ? static_cast<float>(v) : 0.f;
   }
 }
@@ -383,32 +426,26 @@ __global__ void k_f32_to_padded(const float* __restrict__ Asrc, int64_t n, int n
 }  // namespace
 
 hipError_t launch_gram(const float* X, int64_t n, int d, int m, int n_fit,
-                       const double* ls, const double* os, const double* noise,
+                       const double* ils, const double* os, const double* noise,
                        double* A, hipStream_t st) {
   dim3 grid((n_fit + 15) / 16, (n_fit + 15) / 16, m), block(16, 16);
-  hipLaunchKernelGGL(k_gram, grid, block, 0, st, X, n, d, n_fit, ls, os, noise, A);
+  hipLaunchKernelGGL(k_gram, grid, block, 0, st, X, n, d, n_fit, ils, os, noise, A);
   return hipGetLastError();
 }
 
 hipError_t launch_cholesky(double* A, double* W, int nf, int m, int* flag,
                            hipStream_t st) {
   const int nbk = nf / B;
-  if (W != nullptr) {
-    const unsigned g = static_cast<unsigned>(((int64_t)nf * nf + 255) / 256);
-    hipLaunchKernelGGL(k_identity, dim3(g, m), dim3(256), 0, st, W, nf);
-  }
-  hipLaunchKernelGGL(k_potrf_first, dim3(m), dim3(64), 0, st, A, nf, flag);
+  const unsigned g = static_cast<unsigned>(((int64_t)nf * nf + 255) / 256);
+  hipLaunchKernelGGL(k_identity, dim3(g, m), dim3(256), 0, st, W, nf);
+  hipLaunchKernelGGL(k_factor_first, dim3(m), dim3(256), 0, st, A, W, nf, flag);
   for (int kb = 0; kb < nbk; ++kb) {
-    const int rows_below = nf - (kb + 1) * B;
-    const int nrow_blk = (rows_below + 255) / 256;
-    const int ncol_blk = (W != nullptr) ? ((kb + 1) * B + 255) / 256 : 0;
-    if (nrow_blk + ncol_blk > 0)
-      hipLaunchKernelGGL(k_panel, dim3(nrow_blk + ncol_blk, m), dim3(256), 0, st, A, W, nf,
-                         kb, nrow_blk);
     const int T = nbk - kb - 1;
-    const int ntile = T * (T + 1) / 2 + ((W != nullptr) ? T * (kb + 1) : 0);
+    if (T + kb > 0)
+      hipLaunchKernelGGL(k_panel, dim3(T + kb, m), dim3(256), 0, st, A, W, nf, kb);
     if (T > 0)
-      hipLaunchKernelGGL(k_update, dim3(ntile, m), dim3(256), 0, st, A, W, nf, kb, flag);
+      hipLaunchKernelGGL(k_update, dim3(T * (T + 1) / 2 + T * (kb + 1), m), dim3(256), 0, st,
+                         A, W, nf, kb, flag);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -418,7 +455,7 @@ hipError_t launch_cholesky(double* A, double* W, int nf, int m, int* flag,
 hipError_t launch_alpha(const double* W, const float* Y, int64_t n, int m, int nf,
                         int n_pad, double* tmp, float* alpha, hipStream_t st) {
   hipLaunchKernelGGL(k_wy, dim3((nf + 3) / 4, m), dim3(256), 0, st, W, Y, n, m, nf, tmp);
-  hipLaunchKernelGGL(k_wty, dim3((n_pad + 63) / 64, m), dim3(256), 0, st, W, tmp, n,
+  hipLaunchKernelGGL(k_wty, dim3((n_pad + 15) / 16, m), dim3(256), 0, st, W, tmp, n,
                      nf, n_pad, alpha);
   return hipGetLastError();
 }
