@@ -34,6 +34,10 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 PEAK_FP32_MFMA_TFLOPS = 157.3
+# VALU issue peak derived from the unit counts: 256 CUs x 128 fp32 lanes per
+# clock (the 157.3 TFLOP/s vector figure counted as 2 flops per FMA lane-op)
+# x 2.4 GHz.
+PEAK_VALU_LANE_OPS = 256 * 128 * 2.4e9
 METRIC = "candidates scored/sec (GP posterior + MC-EHVI), n=1024 d=16 S=512, 1 GPU"
 
 
@@ -43,6 +47,19 @@ def posterior_flops_per_point(n: int, d: int, q: int) -> float:
     counted as n^2), 2nd for the scaled distances, 2n for mu = k*^T alpha and
     2n for |v|^2 (q = 1) or 2n(q+1)/2 per point for the batch V^T V."""
     return n * n + 2.0 * n * d + 2.0 * n + 2.0 * n * (q + 1) / 2.0
+
+
+def ehvi_lane_ops(M: int, q: int, m: int, S: int, nbox: int) -> float:
+    """Algorithmic VALU work of the MC-EHVI in lane-operations, counting a
+    multiply-add as one: per (candidate, sample, box) a subtraction and a clamp
+    per objective and member, for q > 1 the running minima of the 2^q - 1
+    member subsets, and m - 1 multiplies per subset (the last one fused with
+    the accumulation); per (candidate, sample) the reparameterised draw
+    (m FMAs for q = 1, m q(q+1)/2 for the lower-factor product)."""
+    subsets = 2 ** q - 1
+    per_box = 2 * q * m + (subsets - q) * m + subsets * (m - 1)
+    draw = m if q == 1 else m * q * (q + 1) // 2
+    return float(M) * S * (nbox * per_box + draw)
 
 
 def recorded_traffic(n_launch_flops_workload: str):
@@ -96,6 +113,7 @@ def main(argv=None):
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-sample", type=int, default=4096)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-peaks", action="store_true", help="skip the achieved-peak probes")
     ap.add_argument("--calib-copy-mb", type=int, default=0,
                     help="also run one plain device copy of this many MiB (counter calibration)")
     a = ap.parse_args(argv)
@@ -202,6 +220,23 @@ def main(argv=None):
         "score_only_candidates_per_s": wl.M / (score_ms / 1e3) if score_ms > 0 else None,
         "argmax_index": best,
     }
+    nbox = len(bo.box_decomposition(wl.Y[bo.pareto_front(wl.Y, wl.ref)], wl.ref)[0])
+    ehvi_ops = ehvi_lane_ops(wl.M, wl.q, wl.m, wl.S, nbox)
+    ehvi_launch_ms = ehvi_ms / max(calls, 1)
+    ehvi_rate = ehvi_ops / (ehvi_launch_ms / 1e3)
+    rec["ehvi_roofline"] = {
+        "bound": "alu", "kernel": "k_ehvi (one launch per call)", "boxes": nbox,
+        "achieved": ehvi_rate / 1e12, "peak": PEAK_VALU_LANE_OPS / 1e12,
+        "unit": "T lane-ops/s", "frac": ehvi_rate / PEAK_VALU_LANE_OPS,
+        "launch_ms": ehvi_launch_ms, "lane_ops_per_launch": ehvi_ops,
+    }
+    if not a.no_peaks:
+        rec["measured_peaks"] = {
+            "valu_fma_lane_ops_per_s": bo.measure_peak(bo.PEAK_VALU_FMA, 65536),
+            "valu_clamp_lane_ops_per_s": bo.measure_peak(bo.PEAK_VALU_CLAMP, 32768),
+            "mfma_f32_flop_per_s": bo.measure_peak(bo.PEAK_MFMA_F32, 16384),
+            "hbm_copy_bytes_per_s": bo.measure_peak(bo.PEAK_HBM_COPY, 1),
+        }
     if not a.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(wl, a.cpu_sample)
     print(json.dumps(rec), flush=True)

@@ -203,6 +203,23 @@ bo_status bo_profile_enable(int32_t on);
 bo_status bo_profile_read(double* posterior_ms, double* ehvi_ms, int64_t* calls,
                           int64_t* posterior_launches);
 
+/*
+ * Device characterisation for roofline fractions: runs a fixed synthetic
+ * workload over the whole chip on `stream`, synchronously, and returns the
+ * achieved rate in *rate:
+ *   BO_PEAK_VALU_FMA   lane-ops/s of independent fp32 FMA chains (no packed math)
+ *   BO_PEAK_VALU_CLAMP lane-ops/s of the (sub, med3, fma) pattern of the EHVI loop
+ *   BO_PEAK_MFMA_F32   flop/s of independent v_mfma_f32_16x16x4f32 chains
+ *   BO_PEAK_HBM_COPY   bytes/s (read + write) of a 1 GiB streaming copy
+ * iters: inner iterations for the compute probes (ignored by the copy).
+ * Allocates its own buffers. Errors: INVALID_ARGUMENT, DEVICE, OUT_OF_MEMORY.
+ */
+#define BO_PEAK_VALU_FMA 0
+#define BO_PEAK_VALU_CLAMP 1
+#define BO_PEAK_MFMA_F32 2
+#define BO_PEAK_HBM_COPY 3
+bo_status bo_measure_peak(int32_t what, int64_t iters, double* rate, void* stream);
+
 /* Releases a model (waits for its last stream first). NULL is a no-op. */
 void bo_free(bo_model model);
 

@@ -18,7 +18,7 @@ from typing import Optional
 import numpy as np
 
 __all__ = ["BoError", "Model", "lib", "lib_path", "fit", "score", "argmax",
-           "cholesky_test", "profile_enable", "profile_read", "pareto_front", "box_decomposition", "STATUS",
+           "cholesky_test", "profile_enable", "profile_read", "measure_peak", "pareto_front", "box_decomposition", "STATUS",
            "MAX_N", "MAX_D", "MAX_S", "MAX_BOXES"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -75,6 +75,8 @@ def lib() -> ctypes.CDLL:
     L.bo_profile_read.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double),
                                   ctypes.POINTER(i64), ctypes.POINTER(i64)]
     L.bo_profile_read.restype = ctypes.c_int
+    L.bo_measure_peak.argtypes = [i32, i64, ctypes.POINTER(ctypes.c_double), vp]
+    L.bo_measure_peak.restype = ctypes.c_int
     L.bo_free.argtypes = [vp]
     L.bo_free.restype = None
     L.bo_status_string.argtypes = [ctypes.c_int]
@@ -213,6 +215,16 @@ def profile_read():
     _check(lib().bo_profile_read(ctypes.byref(a), ctypes.byref(b), ctypes.byref(c),
                                  ctypes.byref(n)), "bo_profile_read")
     return a.value, b.value, c.value, n.value
+
+
+PEAK_VALU_FMA, PEAK_VALU_CLAMP, PEAK_MFMA_F32, PEAK_HBM_COPY = 0, 1, 2, 3
+
+
+def measure_peak(what: int, iters: int = 4096, stream=None) -> float:
+    """Achieved rate of a synthetic probe (see bo_measure_peak in bo.h)."""
+    r = ctypes.c_double()
+    _check(lib().bo_measure_peak(what, iters, ctypes.byref(r), _stream(stream)), "bo_measure_peak")
+    return r.value
 
 
 def cholesky_test(A, L=None, stream=None):

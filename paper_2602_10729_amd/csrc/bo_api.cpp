@@ -616,6 +616,14 @@ bo_status bo_argmax(const float* values, int64_t M, int64_t* index, float* value
   return after_launch(launch_argmax(values, M, index, value, st), st, "argmax");
 }
 
+bo_status bo_measure_peak(int32_t what, int64_t iters, double* rate, void* stream) {
+  if (!rate || what < BO_PEAK_VALU_FMA || what > BO_PEAK_HBM_COPY || iters < 1 || iters > (1 << 24))
+    return fail(BO_ERR_INVALID_ARGUMENT, "bo_measure_peak: bad argument");
+  hipError_t e = measure_peak(what, iters, rate, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "bo_measure_peak");
+  return BO_OK;
+}
+
 bo_status bo_cholesky_test(const float* A, int64_t n, float* L, void* stream) {
   if (n < 1) return fail(BO_ERR_INVALID_ARGUMENT, "bo_cholesky_test: n < 1");
   if (n > BO_MAX_N) return fail(BO_ERR_CAPACITY, "bo_cholesky_test: n beyond limit");

@@ -124,4 +124,7 @@ hipError_t launch_ehvi(const EhviArgs& a, hipStream_t st);
 hipError_t launch_argmax(const float* v, int64_t M, int64_t* index,
                          float* value, hipStream_t st);
 
+// Achieved-peak probes (peaks.hip); synchronous.
+hipError_t measure_peak(int what, int64_t iters, double* rate, hipStream_t st);
+
 }  // namespace bo
