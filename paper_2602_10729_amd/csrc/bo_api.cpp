@@ -353,7 +353,7 @@ bo_status bo_fit(const float* X, const float* Y, int64_t n, int32_t d, int32_t m
   host_front(M->Yh.data(), n, m, nullptr, M->nd);
 
   const int nf = static_cast<int>((n + kFitBlk - 1) / kFitBlk) * kFitBlk;
-  const size_t nblk = (size_t)M->nb * (M->nb + 1) / 2;
+  const size_t nblk = (size_t)M->nb * (M->nb + 1) / 2 + 1;   // lower blocks + a zero block
   M->lp_per_obj = nblk * 64 * 4;
   FitScratch fs;
   fs.st = st;

@@ -44,7 +44,7 @@ struct Model {
   float* Xs = nullptr;           // [m][n_pad][dx] X / lengthscale (fp32)
   float* invls = nullptr;        // [m][dx] 1 / lengthscale (fp32, 0-padded)
   float* alpha = nullptr;        // [m][n_pad]
-  float* Lp = nullptr;           // [m][nb(nb+1)/2][64][4] packed L^{-1}
+  float* Lp = nullptr;           // [m][nb(nb+1)/2 + 1][64][4] packed L^{-1} + zero block
   size_t lp_per_obj = 0;         // floats per objective in Lp
 
   // scoring workspace (grown on demand)
@@ -76,8 +76,8 @@ hipError_t launch_cholesky(double* A, double* W, int nf, int m, int* flag,
 hipError_t launch_alpha(const double* W, const float* Y, int64_t n, int m,
                         int nf, int n_pad, double* tmp, float* alpha,
                         hipStream_t st);
-// Pack W into MFMA A-fragment order (fp32, lower blocks, zeros beyond n) and
-// write the lengthscale-scaled X.
+// Pack W into MFMA A-fragment order (fp32, lower blocks, zeros beyond n, then
+// one all-zero block) and write the lengthscale-scaled X.
 hipError_t launch_pack(const double* W, int64_t n, int m, int nf, int nb,
                        float* Lp, const float* X, int d, int dx,
                        const float* invls, float* Xs, hipStream_t st);

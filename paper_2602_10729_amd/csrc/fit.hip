@@ -364,11 +364,12 @@ __global__ __launch_bounds__(256) void k_wty(const double* __restrict__ W,
 
 // Pack lower 16x16 blocks of W into MFMA A-fragment order (inner index of a
 // block split as 4 * lane-group + step):
-// Lp[k][blk(I,J)][lane][kk] = W[I*16 + lane%16][J*16 + 4*(lane/16) + kk].
+// Lp[k][blk(I,J)][lane][kk] = W[I*16 + lane%16][J*16 + 4*(lane/16) + kk],
+// followed by one zero block (blk = nb(nb+1)/2, which maps to rows >= n).
 __global__ __launch_bounds__(256) void k_pack(const double* __restrict__ W, int64_t n,
                                               int nf, int nb, float* __restrict__ Lp) {
   const int k = blockIdx.y;
-  const int64_t nblk = (int64_t)nb * (nb + 1) / 2;
+  const int64_t nblk = (int64_t)nb * (nb + 1) / 2 + 1;
   const int64_t g = (int64_t)blockIdx.x * 256 + threadIdx.x;   // (blk, lane)
   if (g >= nblk * 64) return;
   const int64_t blk = g / 64;
@@ -463,7 +464,7 @@ hipError_t launch_alpha(const double* W, const float* Y, int64_t n, int m, int n
 hipError_t launch_pack(const double* W, int64_t n, int m, int nf, int nb, float* Lp,
                        const float* X, int d, int dx, const float* invls, float* Xs,
                        hipStream_t st) {
-  const int64_t nblk = (int64_t)nb * (nb + 1) / 2;
+  const int64_t nblk = (int64_t)nb * (nb + 1) / 2 + 1;   // + the zero block
   const unsigned gx = static_cast<unsigned>((nblk * 64 + 255) / 256);
   hipLaunchKernelGGL(k_pack, dim3(gx, m), dim3(256), 0, st, W, n, nf, nb, Lp);
   const int n_pad = nb * kBlk;
