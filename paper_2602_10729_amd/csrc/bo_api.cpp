@@ -353,8 +353,7 @@ bo_status bo_fit(const float* X, const float* Y, int64_t n, int32_t d, int32_t m
   host_front(M->Yh.data(), n, m, nullptr, M->nd);
 
   const int nf = static_cast<int>((n + kFitBlk - 1) / kFitBlk) * kFitBlk;
-  const size_t nblk = (size_t)M->nb * (M->nb + 1) / 2 + 1;   // lower blocks + a zero block
-  M->lp_per_obj = nblk * 64 * 4;
+  M->lp_per_obj = (size_t)posterior_frag_blocks(M->nb) * 512;   // 2 KiB per block
   FitScratch fs;
   fs.st = st;
   if ((s = palloc(&fs.A, (size_t)m * nf * nf, st, "fit matrix")) != BO_OK) return bail(s);

@@ -44,7 +44,7 @@ struct Model {
   float* Xs = nullptr;           // [m][n_pad][dx] X / lengthscale (fp32)
   float* invls = nullptr;        // [m][dx] 1 / lengthscale (fp32, 0-padded)
   float* alpha = nullptr;        // [m][n_pad]
-  float* Lp = nullptr;           // [m][nb(nb+1)/2 + 1][64][4] packed L^{-1} + zero block
+  float* Lp = nullptr;           // [m][frag blocks][2 KiB] packed fp16 hi/lo L^{-1} + zero block
   size_t lp_per_obj = 0;         // floats per objective in Lp
 
   // scoring workspace (grown on demand)
@@ -76,8 +76,10 @@ hipError_t launch_cholesky(double* A, double* W, int nf, int m, int* flag,
 hipError_t launch_alpha(const double* W, const float* Y, int64_t n, int m,
                         int nf, int n_pad, double* tmp, float* alpha,
                         hipStream_t st);
-// Pack W into MFMA A-fragment order (fp32, lower blocks, zeros beyond n, then
-// one all-zero block) and write the lengthscale-scaled X.
+// Pack W into the posterior's A-fragment format (fp16 hi/lo planes of 16x32
+// lower blocks, zeros beyond n, then one all-zero block; 2 KiB per block,
+// posterior_frag_blocks(nb) blocks per objective) and write the
+// lengthscale-scaled X.
 hipError_t launch_pack(const double* W, int64_t n, int m, int nf, int nb,
                        float* Lp, const float* X, int d, int dx,
                        const float* invls, float* Xs, hipStream_t st);
@@ -107,6 +109,8 @@ struct PosteriorArgs {
   float* chol;         // q > 1: [npts/q][m][q(q+1)/2] lower factor, row-major
 };
 hipError_t launch_posterior(const PosteriorArgs& a, hipStream_t st);
+// Packed L^{-1} blocks per objective (lower 16x32 blocks + the zero block).
+int64_t posterior_frag_blocks(int nb);
 
 // Monte-Carlo EHVI over boxes for nbat batches.
 struct EhviArgs {

@@ -362,32 +362,50 @@ __global__ __launch_bounds__(256) void k_wty(const double* __restrict__ W,
   }
 }
 
-// Pack lower 16x16 blocks of W into MFMA A-fragment order (inner index of a
-// block split as 4 * lane-group + step):
-// Lp[k][blk(I,J)][lane][kk] = W[I*16 + lane%16][J*16 + 4*(lane/16) + kk],
-// followed by one zero block (blk = nb(nb+1)/2, which maps to rows >= n).
+// Pack the lower triangle of W = L^{-1} as fp16 hi/lo MFMA A fragments of
+// 16-row x 32-column blocks (the scoring path's operand format):
+// row block I holds the blocks J = 0 .. I/2, block (I, J) at index
+// start(I) + J with start(2t) = t(t+1), start(2t+1) = (t+1)^2, followed by one
+// zero block (index start(nb), which maps to rows >= n). Each block is 2 KiB:
+// the hi plane, then the lo plane, 16 bytes per lane, lane l element e being
+// W[16I + l%16][32J + 8(l/16) + e] (zero above the diagonal and past n),
+// split as hi = fp16(w), lo = fp16(w - hi).
 __global__ __launch_bounds__(256) void k_pack(const double* __restrict__ W, int64_t n,
-                                              int nf, int nb, float* __restrict__ Lp) {
+                                              int nf, int64_t nblk, _Float16* __restrict__ Lp) {
   const int k = blockIdx.y;
-  const int64_t nblk = (int64_t)nb * (nb + 1) / 2 + 1;
   const int64_t g = (int64_t)blockIdx.x * 256 + threadIdx.x;   // (blk, lane)
   if (g >= nblk * 64) return;
   const int64_t blk = g / 64;
   const int lane = static_cast<int>(g % 64);
-  int I = static_cast<int>((sqrt(8.0 * blk + 1.0) - 1.0) * 0.5);
-  while ((int64_t)(I + 1) * (I + 2) / 2 <= blk) ++I;
-  while ((int64_t)I * (I + 1) / 2 > blk) --I;
-  const int J = static_cast<int>(blk - (int64_t)I * (I + 1) / 2);
-  const int row = I * kBlk + lane % 16;
-  const double* Wk = W + (int64_t)k * nf * nf;
-  float4 v;
-  float* vp = reinterpret_cast<float*>(&v);
-#pragma unroll
-  for (int kk = 0; kk < 4; ++kk) {
-    const int col = J * kBlk + 4 * (lane / 16) + kk;
-    vp[kk] = (row < n && col < n) ? static_cast<float>(Wk[(int64_t)row * nf + col]) : 0.f;
+  // row block I of blk: start(I) <= blk < start(I + 1)
+  int64_t t = static_cast<int64_t>((sqrt(4.0 * blk + 1.0) - 1.0) * 0.5);
+  while ((t + 1) * (t + 2) <= blk) ++t;
+  while (t * (t + 1) > blk) --t;
+  int I, J;
+  if (blk >= (t + 1) * (t + 1)) {
+    I = static_cast<int>(2 * t + 1);
+    J = static_cast<int>(blk - (t + 1) * (t + 1));
+  } else {
+    I = static_cast<int>(2 * t);
+    J = static_cast<int>(blk - t * (t + 1));
   }
-  reinterpret_cast<float4*>(Lp)[(int64_t)k * nblk * 64 + g] = v;
+  const int64_t row = (int64_t)I * kBlk + lane % 16;
+  const double* Wk = W + (int64_t)k * nf * nf;
+  _Float16 hi[8], lo[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int64_t col = (int64_t)J * 32 + 8 * (lane / 16) + e;
+    const double w = (row < n && col < n && col <= row) ? Wk[row * nf + col] : 0.0;
+    const _Float16 h = static_cast<_Float16>(static_cast<float>(w));
+    hi[e] = h;
+    lo[e] = static_cast<_Float16>(static_cast<float>(w - static_cast<double>(h)));
+  }
+  _Float16* dst = Lp + ((int64_t)k * nblk + blk) * 1024 + lane * 8;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    dst[e] = hi[e];
+    dst[512 + e] = lo[e];
+  }
 }
 
 // Xs[k][i][t] = X[i][t] * invls[k][t] (zero padding beyond n and d)
@@ -464,9 +482,10 @@ hipError_t launch_alpha(const double* W, const float* Y, int64_t n, int m, int n
 hipError_t launch_pack(const double* W, int64_t n, int m, int nf, int nb, float* Lp,
                        const float* X, int d, int dx, const float* invls, float* Xs,
                        hipStream_t st) {
-  const int64_t nblk = (int64_t)nb * (nb + 1) / 2 + 1;   // + the zero block
+  const int64_t nblk = posterior_frag_blocks(nb);   // with the zero block
   const unsigned gx = static_cast<unsigned>((nblk * 64 + 255) / 256);
-  hipLaunchKernelGGL(k_pack, dim3(gx, m), dim3(256), 0, st, W, n, nf, nb, Lp);
+  hipLaunchKernelGGL(k_pack, dim3(gx, m), dim3(256), 0, st, W, n, nf, nblk,
+                     reinterpret_cast<_Float16*>(Lp));
   const int n_pad = nb * kBlk;
   const unsigned gx2 = static_cast<unsigned>(((int64_t)n_pad * dx + 255) / 256);
   hipLaunchKernelGGL(k_scale_x, dim3(gx2, m), dim3(256), 0, st, X, n, d, dx, n_pad,

@@ -4,37 +4,49 @@
 // joint posterior of the GP surrogates; the posterior of an exact GP at x*
 // is mu = k*^T alpha and Sigma = k(x*,x*) - v^T v with v = L^{-1} k*.
 //
-// One workgroup (8 waves, two per SIMD) owns a tile of NT points and forms
-// V = L^{-1} K*^T left-looking: the outer loop runs over the 16-row blocks J
-// of K*^T, and every wave adds L^{-1}[I][J] K*^T[J] into the accumulators of
-// the row blocks I >= J that it owns. Row block I of V therefore never
-// leaves the MFMA accumulators until it is complete, and then only its
-// squared column sums (q = 1: |v|^2; q > 1 also the cross products of batch
-// members, which sit in the same 4-lane group and are exchanged with DPP
-// quad permutes) are kept.
+// Arithmetic. V = L^{-1} K*^T runs on the fp16 matrix cores with each
+// operand split into two fp16 halves, x = x_hi + x_lo (x_hi = fp16(x),
+// x_lo = fp16(x - x_hi)), and three products per pair,
+//   a b ~ a_hi b_hi + a_hi b_lo + a_lo b_hi,
+// accumulated in fp32 by the MFMA. The operands carry ~22 significant bits
+// and the dropped a_lo b_lo term is 2^-22 relative, so the result is within
+// a small factor of an fp32 product. On gfx950 this is the fast path: the
+// dense fp16 MFMA runs at 16x the fp32 MFMA rate, and (unlike fp32 MFMA) it
+// executes alongside VALU work, which hides the kernel evaluations below.
+// L^{-1} is split and packed once by the fit; K*^T is split as it is made.
 //
-// K*^T is never resident as a whole: it is produced on the fly, one block
-// ahead of its use, into a two-chunk LDS ring (a chunk is 64 rows). While
-// the matrix core works on block J, the same waves evaluate the ARD
-// Matern-5/2 values of block J + 4 on the vector ALUs (direct differences
-// of lengthscale-scaled coordinates, no |a|^2 + |b|^2 - 2ab cancellation)
-// and accumulate mu = K* alpha. One barrier per chunk publishes it.
+// One workgroup (8 waves, two per SIMD) owns a tile of NT points and forms V
+// left-looking: the outer loop runs over 32-row blocks J of K*^T (the MFMA
+// k), and every wave adds L^{-1}[I][J] K*^T[J] into the accumulators of the
+// 16-row blocks I >= 2J that it owns. Row block I of V stays in the MFMA
+// accumulators until it is complete; then only its squared column sums
+// (q = 1: |v|^2; q > 1 also the cross products of batch members, which sit
+// in the same 4-lane group and are exchanged with DPP quad permutes) are
+// kept.
+//
+// K*^T is never resident as a whole: it is produced one 64-row chunk ahead
+// of its use into a two-chunk LDS ring of fp16 hi/lo planes, from training
+// rows staged through LDS two chunks ahead. While the matrix cores work on
+// block J, the waves evaluate the ARD Matern-5/2 values of block J + 2 on
+// the vector ALUs (direct differences of lengthscale-scaled coordinates, no
+// |a|^2 + |b|^2 - 2ab cancellation) and accumulate mu = K* alpha in fp32.
+// The kernel evaluations and the MFMAs of a step are independent and are
+// interleaved, so each SIMD's matrix core and vector ALU stay busy together.
+// One barrier per chunk publishes the produced block and the staged rows.
 //
 // Each wave owns RB row-block slots, slot r holding row block
 // base + 8r + (r even ? wave : 7 - wave); this snake keeps the per-SIMD
-// share of the lower triangle even at every step of J. Row blocks beyond
-// the matrix (and finished slots) read a zero block appended to the packed
-// L^{-1}, so every load is unconditional and in bounds. For n_pad > 128 RB
-// rows the rows are handled in passes of 8 RB blocks, K*^T being produced
-// again for each pass.
+// share of the lower triangle even at every step of J. Row blocks past the
+// matrix (and finished slots) read a zero block appended to the packed
+// L^{-1}, so every load is unconditional and in bounds. Rows beyond 128 RB
+// are handled in further passes, K*^T being produced again for each pass
+// (RB = 4: two passes for n = 1024; the accumulators of more rows would not
+// fit the register file next to the operands).
 //
-// The 16 inner indices of a block are split as k = 4g + kk between the four
-// 16-lane groups g and the four MFMA steps kk, so each lane's four A
-// operands are four consecutive columns of L^{-1} (pre-packed by the fit: one
-// 16-byte load, 1 KiB per block per wave) and its four B operands are four
-// consecutive rows of K*^T (one 16-byte LDS read).
-// MFMA: v_mfma_f32_16x16x4f32, A[i][k] from lane i + 16k, B[k][j] from lane
-// j + 16k, D[i][j] in lane j + 16(i/4), element i%4.
+// Fragments of v_mfma_f32_16x16x32_f16: A[i][k] from lane i + 16(k/8),
+// element k%8; B[k][j] from lane j + 16(k/8), element k%8; D[i][j] in lane
+// j + 16(i/4), element i%4. Only the pairing of A's and B's k matters, and
+// both sides use this one.
 #include <hip/hip_runtime.h>
 
 #include "bo_internal.h"
@@ -43,16 +55,21 @@ namespace bo {
 namespace {
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef _Float16 halfx8 __attribute__((ext_vector_type(8)));
 
 #ifndef BO_POST_NT
-#define BO_POST_NT 32        // points per tile
+#define BO_POST_NT 64        // points per tile
+#endif
+#ifndef BO_POST_RB
+#define BO_POST_RB 4         // row-block slots per wave (rows per pass / 128)
 #endif
 constexpr int kWaves = 8;
 constexpr int kThreads = 64 * kWaves;
-constexpr int kChunkRows = 64;              // rows of K*^T per ring chunk
-constexpr int kCS = kChunkRows + 4;         // column stride in the ring (mod 32 banks: 4)
+constexpr int kJ = 32;                      // rows of K*^T per step (MFMA k)
+constexpr int kChunk = 2 * kJ;              // rows per ring chunk (one barrier each)
+constexpr int kCSH = kChunk + 8;            // ring column stride in halves (36 dwords)
 
-__device__ inline float matern52_f(float r2, float s) {
+__device__ __forceinline__ float matern52_f(float r2, float s) {
   const float r = __builtin_amdgcn_sqrtf(r2);
   // exp(-sqrt5 r) = 2^(-sqrt5 log2(e) r)
   constexpr float kNegSqrt5Log2e = static_cast<float>(-2.23606797749978969641 * 1.44269504088896340736);
@@ -61,7 +78,7 @@ __device__ inline float matern52_f(float r2, float s) {
   return s * poly * e;
 }
 
-__device__ inline float quad_xor(float v, int x) {
+__device__ __forceinline__ float quad_xor(float v, int x) {
   // DPP quad_perm: lane i of each group of 4 reads lane i ^ x.
   int iv = __float_as_int(v);
   int r;
@@ -72,24 +89,10 @@ __device__ inline float quad_xor(float v, int x) {
 }
 
 // LDS-only barrier: waits for this wave's LDS traffic, not for its global
-// loads in flight (the A-fragment prefetches), then joins the workgroup.
-__device__ inline void lds_barrier() {
+// loads in flight (the fragment prefetches), then joins the workgroup.
+__device__ __forceinline__ void lds_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
-
-// Per-lane state of the K*^T producer: this lane evaluates row (lane & 15)
-// of each block for CPL columns of the tile.
-template <int NT, int DX4>
-struct Producer {
-  static constexpr int CPL = NT / 32;
-  float c[CPL][DX4 * 4];    // scaled candidate coordinates
-  bool valid[CPL];
-  float mu[CPL];
-  float4 xn[DX4];           // training row of the next block
-  float aln;                // alpha of that row
-  int col0;                 // first tile column of this lane
-  __amdgpu_buffer_rsrc_t xs_rs, al_rs;   // scaled X, alpha
-};
 
 // Raw buffer resource over `bytes` bytes at p: loads take a 32-bit lane
 // offset plus a uniform offset, and read zero past the end.
@@ -101,53 +104,114 @@ __device__ __forceinline__ float4 load4(__amdgpu_buffer_rsrc_t rs, int voff, int
   return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rs, voff, soff, 0));
 }
 
-template <int NT, int DX4>
-__device__ __forceinline__ void producer_fetch(Producer<NT, DX4>& P, const PosteriorArgs& a,
-                                               int n_pad, int jb, int rr) {
-  const int row = min(jb * kBlk + rr, n_pad - 1);
-#pragma unroll
-  for (int t4 = 0; t4 < DX4; ++t4) P.xn[t4] = load4(P.xs_rs, (row * a.dx + 4 * t4) * 4, 0);
-  P.aln = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(P.al_rs, row * 4, 0, 0));
+// Index of packed block (I, 0): row block I holds I/2 + 1 blocks of 32
+// columns, so rows 0..I-1 hold t(t+1) (I = 2t) or (t+1)^2 (I = 2t+1).
+__host__ __device__ __forceinline__ int frag_row_start(int I) {
+  const int t = I >> 1;
+  return (I & 1) ? (t + 1) * (t + 1) : t * (t + 1);
 }
 
-// Evaluate block jb of K*^T (the one fetched last) into the ring, then fetch
-// block jb + 1. Blocks past the matrix produce zeros that are never read.
+// Per-lane state of the K*^T producer. A wave makes NT/8 columns of each
+// 32-row block; lane l takes column l % CPW and RPL = CPW/2 consecutive rows.
 template <int NT, int DX4>
-__device__ __forceinline__ void produce(Producer<NT, DX4>& P, const PosteriorArgs& a, int n_pad,
-                                        int jb, int rr, float* ring) {
-  constexpr int CPL = NT / 32;
-  const int row = jb * kBlk + rr;
-  const bool live = row < a.n;
-  float* dst = ring + ((jb >> 2) & 1) * (NT * kCS) + (jb & 3) * kBlk + rr;
+struct Producer {
+  static constexpr int CPW = NT / kWaves;
+  static constexpr int RPL = kJ * CPW / 64;
+  float c[DX4 * 4];         // scaled candidate coordinates
+  bool valid;
+  float mu;
+  int col;                  // tile column of this lane
+  int row0;                 // first row of this lane inside a block
+};
+
+// Training rows of one chunk staged in LDS: [kChunk][dx + 4] floats, the
+// last float4 of a row holding (alpha, 0, 0, 0). Two slots; the stager loads
+// chunk c + 2 into slot c % 2 while chunk c + 1 is produced from the other.
+template <int DX4>
+struct Stager {
+  static constexpr int RS = DX4 * 4 + 4;                 // row stride (floats)
+  static constexpr int kF4 = kChunk * (DX4 + 1);         // float4s per chunk
+  static constexpr int kPer = (kF4 + kThreads - 1) / kThreads;
+  float4 v[kPer];
+  __amdgpu_buffer_rsrc_t xs_rs, al_rs;
+};
+
+template <int DX4>
+__device__ __forceinline__ void stage_load(Stager<DX4>& S, const PosteriorArgs& a, int n_pad,
+                                           int chunk, int tid) {
 #pragma unroll
-  for (int u = 0; u < CPL; ++u) {
+  for (int i = 0; i < Stager<DX4>::kPer; ++i) {
+    const int f = tid + i * kThreads;
+    const int r = f / (DX4 + 1), t4 = f % (DX4 + 1);
+    const int row = min(chunk * kChunk + r, n_pad - 1);
+    if (t4 < DX4) {
+      S.v[i] = load4(S.xs_rs, (row * a.dx + 4 * t4) * 4, 0);
+    } else {
+      const float al =
+          __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(S.al_rs, row * 4, 0, 0));
+      S.v[i] = float4{al, 0.f, 0.f, 0.f};
+    }
+  }
+}
+
+template <int DX4>
+__device__ __forceinline__ void stage_store(const Stager<DX4>& S, float* xst, int chunk, int tid) {
+  float* dst = xst + (chunk & 1) * kChunk * Stager<DX4>::RS;
+#pragma unroll
+  for (int i = 0; i < Stager<DX4>::kPer; ++i) {
+    const int f = tid + i * kThreads;
+    if (f < Stager<DX4>::kF4) {
+      const int r = f / (DX4 + 1), t4 = f % (DX4 + 1);
+      *reinterpret_cast<float4*>(dst + r * Stager<DX4>::RS + 4 * t4) = S.v[i];
+    }
+  }
+}
+
+// Evaluate this lane's rows of block jb into the ring as fp16 hi/lo planes,
+// reading the training rows from the staging slot of jb's chunk. Rows past
+// the matrix produce zeros (never read as B, no weight in mu).
+template <int NT, int DX4>
+__device__ __forceinline__ void produce(Producer<NT, DX4>& P, const PosteriorArgs& a, int jb,
+                                        const float* xst, _Float16* ring) {
+  constexpr int RPL = Producer<NT, DX4>::RPL;
+  constexpr int RS = Stager<DX4>::RS;
+  typedef _Float16 halfr __attribute__((ext_vector_type(RPL)));
+  halfr hi, lo;
+  const float* xr = xst + ((jb >> 1) & 1) * kChunk * RS + ((jb & 1) * kJ + P.row0) * RS;
+#pragma unroll
+  for (int u = 0; u < RPL; ++u) {
+    const int row = jb * kJ + P.row0 + u;
     float r2 = 0.f;
 #pragma unroll
     for (int t4 = 0; t4 < DX4; ++t4) {
-      const float d0 = P.c[u][4 * t4 + 0] - P.xn[t4].x;
-      const float d1 = P.c[u][4 * t4 + 1] - P.xn[t4].y;
-      const float d2 = P.c[u][4 * t4 + 2] - P.xn[t4].z;
-      const float d3 = P.c[u][4 * t4 + 3] - P.xn[t4].w;
+      const float4 x = *reinterpret_cast<const float4*>(xr + u * RS + 4 * t4);
+      const float d0 = P.c[4 * t4 + 0] - x.x;
+      const float d1 = P.c[4 * t4 + 1] - x.y;
+      const float d2 = P.c[4 * t4 + 2] - x.z;
+      const float d3 = P.c[4 * t4 + 3] - x.w;
       r2 = fmaf(d0, d0, r2);
       r2 = fmaf(d1, d1, r2);
       r2 = fmaf(d2, d2, r2);
       r2 = fmaf(d3, d3, r2);
     }
-    const float kv = (P.valid[u] && live) ? matern52_f(r2, a.s) : 0.f;
-    P.mu[u] = fmaf(P.aln, kv, P.mu[u]);
-    dst[(P.col0 + u) * kCS] = kv;
+    const float kv = (P.valid && row < a.n) ? matern52_f(r2, a.s) : 0.f;
+    P.mu = fmaf(xr[u * RS + 4 * DX4], kv, P.mu);
+    const _Float16 h = static_cast<_Float16>(kv);
+    hi[u] = h;
+    lo[u] = static_cast<_Float16>(kv - static_cast<float>(h));
   }
-  producer_fetch(P, a, n_pad, jb + 1, rr);
+  _Float16* dst = ring + (((jb >> 1) & 1) * 2 * NT + P.col) * kCSH + (jb & 1) * kJ + P.row0;
+  *reinterpret_cast<halfr*>(dst) = hi;
+  *reinterpret_cast<halfr*>(dst + NT * kCSH) = lo;
 }
 
 // Row block of slot r in the pass starting at row block `base`.
-__device__ inline int slot_block(int base, int r, int wave) {
+__device__ __forceinline__ int slot_block(int base, int r, int wave) {
   return base + 8 * r + ((r & 1) ? (kWaves - 1 - wave) : wave);
 }
 
-// Row-block slots of a wave in one pass: fragment index of block (I, 0) and
-// I itself, or (zero block, -1) for a slot past the matrix. Block (I, J) of
-// a slot is first + J while J <= I, the zero block afterwards.
+// Row-block slots of a wave in one pass: packed index of block (I, 0) and the
+// last live J (I / 2), or (zero block, -1) for a slot past the matrix.
 template <int RB>
 struct Slots {
   int first[RB];
@@ -158,73 +222,110 @@ __device__ __forceinline__ int frag_block(int first, int last, int J, int zero_b
   return (J <= last) ? first + J : zero_blk;
 }
 
-// MFMAs of one K*^T block for the slots [LO, RB), taken two slots at a time
-// (four independent accumulators per inner step); each pair's fragments for
-// the next block are requested as soon as its MFMAs are issued, so they
-// have a whole step to arrive.
+// A fragments of one slot: hi and lo planes (1 KiB each per block).
+struct AFrag {
+  halfx8 hi, lo;
+};
+
+__device__ __forceinline__ AFrag load_a(__amdgpu_buffer_rsrc_t rs, int voff, int blk) {
+  AFrag f;
+  f.hi = __builtin_bit_cast(halfx8, load4(rs, voff, blk * 2048));
+  f.lo = __builtin_bit_cast(halfx8, load4(rs, voff, blk * 2048 + 1024));
+  return f;
+}
+
+// MFMAs of one K*^T block for the slots [LO, RB), two slots at a time (the
+// three products of a pair of slots and all column blocks are independent);
+// each pair's fragments for the next block are requested as soon as its MFMAs
+// are issued, so they have a whole step to arrive.
 template <int LO, int RB, int NCB>
-__device__ __forceinline__ void mfma_slots(float4 (&av)[RB], const float4 (&bv)[NCB],
-                                           floatx4 (&acc)[RB][NCB], __amdgpu_buffer_rsrc_t lp_rs,
-                                           const Slots<RB>& sl, int Jn, int zero_blk, int voff) {
+__device__ __forceinline__ void mfma_slots(AFrag (&av)[RB], const halfx8 (&bh)[NCB],
+                                           const halfx8 (&bl)[NCB], floatx4 (&acc)[RB][NCB],
+                                           __amdgpu_buffer_rsrc_t lp_rs, const Slots<RB>& sl,
+                                           int Jn, int zero_blk, int voff) {
 #pragma unroll
   for (int r0 = LO; r0 < RB; r0 += 2) {
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk)
+    for (int r = r0; r < r0 + 2 && r < RB; ++r)
 #pragma unroll
-      for (int r = r0; r < r0 + 2 && r < RB; ++r)
-#pragma unroll
-        for (int b = 0; b < NCB; ++b) {
-          const float A = kk == 0 ? av[r].x : kk == 1 ? av[r].y : kk == 2 ? av[r].z : av[r].w;
-          const float B = kk == 0 ? bv[b].x : kk == 1 ? bv[b].y : kk == 2 ? bv[b].z : bv[b].w;
-          acc[r][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(A, B, acc[r][b], 0, 0, 0);
-        }
+      for (int b = 0; b < NCB; ++b)
+        acc[r][b] = __builtin_amdgcn_mfma_f32_16x16x32_f16(av[r].hi, bh[b], acc[r][b], 0, 0, 0);
 #pragma unroll
     for (int r = r0; r < r0 + 2 && r < RB; ++r)
-      av[r] = load4(lp_rs, voff, frag_block(sl.first[r], sl.last[r], Jn, zero_blk) * 1024);
+#pragma unroll
+      for (int b = 0; b < NCB; ++b)
+        acc[r][b] = __builtin_amdgcn_mfma_f32_16x16x32_f16(av[r].hi, bl[b], acc[r][b], 0, 0, 0);
+#pragma unroll
+    for (int r = r0; r < r0 + 2 && r < RB; ++r)
+#pragma unroll
+      for (int b = 0; b < NCB; ++b)
+        acc[r][b] = __builtin_amdgcn_mfma_f32_16x16x32_f16(av[r].lo, bh[b], acc[r][b], 0, 0, 0);
+#pragma unroll
+    for (int r = r0; r < r0 + 2 && r < RB; ++r)
+      av[r] = load_a(lp_rs, voff, frag_block(sl.first[r], sl.last[r], Jn, zero_blk));
   }
 }
 
 // Workgroup-uniform context of the streaming loop.
 struct Ctx {
   __amdgpu_buffer_rsrc_t lp_rs;   // packed fragments of this objective
-  int nb, zero_blk, n_pad, wave, rr;
-  int voff;            // this lane's byte offset inside a fragment block
-  const float* Kb;     // this lane's B-fragment base inside the ring
+  int nb, nbj, zero_blk, n_pad, wave, tid;
+  int voff;                 // this lane's byte offset inside a fragment plane
+  const _Float16* Kb;       // this lane's B-fragment base inside the ring
+  float* xst;               // training-row staging (2 chunks)
 };
 
-// One step J for slots [LO, RB): B fragments of block J, the producer's
-// block J + 4, the MFMAs with the slots' fragments for J + 1, and the chunk
-// barrier after the last block of a chunk.
-template <int LO, int RB, int NT, int DX4>
-__device__ __forceinline__ void step(const Ctx& C, const PosteriorArgs& a, Producer<NT, DX4>& P,
-                                     float* ring, const Slots<RB>& sl, int J, float4 (&av)[RB],
-                                     floatx4 (&acc)[RB][NT / 16]) {
-  constexpr int NCB = NT / 16;
-  float4 bv[NCB];
-  const float* kb = C.Kb + ((J >> 2) & 1) * (NT * kCS) + (J & 3) * kBlk;
+// B fragments of block J: column (b*16 + lane%16), rows 8*(lane/16) .. +7.
+template <int NCB>
+__device__ __forceinline__ void load_b(const Ctx& C, int J, halfx8 (&bh)[NCB], halfx8 (&bl)[NCB]) {
+  constexpr int NT = NCB * 16;
+  const _Float16* kb = C.Kb + ((J >> 1) & 1) * 2 * NT * kCSH + (J & 1) * kJ;
 #pragma unroll
-  for (int b = 0; b < NCB; ++b) bv[b] = *reinterpret_cast<const float4*>(kb + b * 16 * kCS);
-  produce(P, a, C.n_pad, J + 4, C.rr, ring);
-  mfma_slots<LO, RB, NCB>(av, bv, acc, C.lp_rs, sl, J + 1, C.zero_blk, C.voff);
-  if ((J & 3) == 3) lds_barrier();
+  for (int b = 0; b < NCB; ++b) {
+    bh[b] = *reinterpret_cast<const halfx8*>(kb + b * 16 * kCSH);
+    bl[b] = *reinterpret_cast<const halfx8*>(kb + (NT + b * 16) * kCSH);
+  }
 }
 
-// Rounds R.. of the triangular part of a pass: in round R (blocks
-// J in [base + 8R, base + 8R + 8)) slot R is live while J <= its row block,
-// slots above R throughout.
+// One step J for slots [LO, RB): the B fragments of block J are read first
+// (ahead of the producer's LDS stores, so the MFMAs do not wait behind them),
+// then the producer's block J + 2 and the MFMAs of block J (fragments for
+// J + 1 requested on the way) are left to the scheduler to interleave: the
+// two are independent, and the fp16 MFMAs overlap the VALU work. At a chunk's
+// first step the rows of chunk J/2 + 2 are fetched, at its last they are
+// staged and the chunk barrier is taken.
+template <int LO, int RB, int NT, int DX4>
+__device__ __forceinline__ void step(const Ctx& C, const PosteriorArgs& a, Producer<NT, DX4>& P,
+                                     Stager<DX4>& S, _Float16* ring, const Slots<RB>& sl, int J,
+                                     AFrag (&av)[RB], floatx4 (&acc)[RB][NT / 16]) {
+  if ((J & 1) == 0) stage_load(S, a, C.n_pad, (J >> 1) + 2, C.tid);
+  constexpr int NCB = NT / 16;
+  halfx8 bh[NCB], bl[NCB];
+  load_b<NCB>(C, J, bh, bl);
+  produce(P, a, J + 2, C.xst, ring);
+  mfma_slots<LO, RB, NCB>(av, bh, bl, acc, C.lp_rs, sl, J + 1, C.zero_blk, C.voff);
+  if (J & 1) {
+    stage_store(S, C.xst, (J >> 1) + 2, C.tid);
+    lds_barrier();
+  }
+}
+
+// Rounds R.. of the triangular part of a pass: round R covers the row blocks
+// base + 8R .. base + 8R + 7, i.e. J in [base/2 + 4R, base/2 + 4R + 4); slot R
+// is live while J <= its row block / 2, slots above R throughout.
 template <int R, int RB, int NT, int DX4>
 __device__ __forceinline__ void rounds(const Ctx& C, const PosteriorArgs& a, Producer<NT, DX4>& P,
-                                       float* ring, const Slots<RB>& sl, int base,
-                                       float4 (&av)[RB], floatx4 (&acc)[RB][NT / 16]) {
+                                       Stager<DX4>& S, _Float16* ring, const Slots<RB>& sl,
+                                       int base, AFrag (&av)[RB], floatx4 (&acc)[RB][NT / 16]) {
   if constexpr (R < RB) {
-    const int j0 = base + 8 * R;
-    if (j0 >= C.nb) return;
-    const int jend = min(j0 + 8, C.nb);
-    const int jlive = min(slot_block(base, R, C.wave) + 1, jend);
+    const int j0 = base / 2 + 4 * R;
+    if (j0 >= C.nbj) return;
+    const int jend = min(j0 + 4, C.nbj);
+    const int jlive = min(slot_block(base, R, C.wave) / 2 + 1, jend);
     int J = j0;
-    for (; J < jlive; ++J) step<R, RB, NT, DX4>(C, a, P, ring, sl, J, av, acc);
-    for (; J < jend; ++J) step<R + 1, RB, NT, DX4>(C, a, P, ring, sl, J, av, acc);
-    rounds<R + 1, RB, NT, DX4>(C, a, P, ring, sl, base, av, acc);
+    for (; J < jlive; ++J) step<R, RB, NT, DX4>(C, a, P, S, ring, sl, J, av, acc);
+    for (; J < jend; ++J) step<R + 1, RB, NT, DX4>(C, a, P, S, ring, sl, J, av, acc);
+    rounds<R + 1, RB, NT, DX4>(C, a, P, S, ring, sl, base, av, acc);
   }
 }
 
@@ -233,71 +334,71 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
   extern __shared__ float smem[];
   constexpr int NCB = NT / 16;          // 16-column blocks per tile
   constexpr int NX = (Q > 1) ? Q : 1;   // per-point partial slots (diag + xors)
-  constexpr int CPL = NT / 32;
-  static_assert(NT == 32 || NT == 64, "tile width");
+  using Prod = Producer<NT, DX4>;
+  static_assert(Prod::RPL >= 2 && Prod::RPL <= 8 && 64 % Prod::CPW == 0, "tile width");
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   // wave index as a scalar: the loop control below stays uniform
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n_pad = a.nb * kBlk;
-  float* ring = smem;                                // 2 chunks x NT x kCS
-  float* red = ring + 2 * NT * kCS;                  // kWaves * NT * NX
-  float* mush = red + kWaves * NT * NX;              // NT
-  float* kpp = mush + NT;                            // NT * 4 (prior cross-cov)
+  _Float16* ring = reinterpret_cast<_Float16*>(smem);       // 2 chunks x 2 planes x NT x kCSH
+  float* xst = smem + 2 * NT * kCSH;                        // 2 x kChunk x RS (staged rows)
+  float* red = xst + 2 * kChunk * Stager<DX4>::RS;          // kWaves * NT * NX
+  float* mush = red + kWaves * NT * NX;                     // NT
+  float* kpp = mush + NT;                                   // NT * 4 (prior cross-cov)
   const int64_t p0 = (int64_t)blockIdx.x * NT;
-  const int rr = lane & 15;
 
-  Producer<NT, DX4> P;
-  P.col0 = wave * (NT / 8) + (lane >> 4) * CPL;
+  Prod P;
+  P.col = wave * Prod::CPW + lane % Prod::CPW;
+  P.row0 = (lane / Prod::CPW) * Prod::RPL;
+  {
+    const int64_t p = p0 + P.col;
+    P.valid = p < a.npts;
 #pragma unroll
-  for (int u = 0; u < CPL; ++u) {
-    const int64_t p = p0 + P.col0 + u;
-    P.valid[u] = p < a.npts;
-#pragma unroll
-    for (int t = 0; t < DX4 * 4; ++t) P.c[u][t] = 0.f;
-    if (P.valid[u]) {
+    for (int t = 0; t < DX4 * 4; ++t) P.c[t] = 0.f;
+    if (P.valid) {
       const float* cp = a.cand + p * a.d;
 #pragma unroll
       for (int t = 0; t < DX4 * 4; ++t)
-        if (t < a.d) P.c[u][t] = cp[t] * a.invls[t];
+        if (t < a.d) P.c[t] = cp[t] * a.invls[t];
     }
   }
 
   if (Q > 1) {
-    // prior covariance of each point with its batch mates (point ^ x),
-    // partner x on lane rr = x of the column's 16-lane group
+    // prior covariance of each point with its batch mates (point ^ x), partner
+    // x on the lane of the column's group whose row group is x
+    const int x = lane / Prod::CPW;
+    if (x >= 1 && x < Q) {
+      const int64_t pm = (p0 + P.col) ^ x;
+      float r2 = 0.f;
+      if (P.valid && pm < a.npts) {
+        const float* cp = a.cand + pm * a.d;
 #pragma unroll
-    for (int u = 0; u < CPL; ++u) {
-      const int colu = P.col0 + u;
-      if (rr >= 1 && rr < Q) {
-        const int64_t pm = (p0 + colu) ^ rr;
-        float r2 = 0.f;
-        if (P.valid[u] && pm < a.npts) {
-          const float* cp = a.cand + pm * a.d;
-#pragma unroll
-          for (int t = 0; t < DX4 * 4; ++t)
-            if (t < a.d) {
-              const float dd = P.c[u][t] - cp[t] * a.invls[t];
-              r2 = fmaf(dd, dd, r2);
-            }
-        }
-        kpp[colu * 4 + rr] = matern52_f(r2, a.s);
+        for (int t = 0; t < DX4 * 4; ++t)
+          if (t < a.d) {
+            const float dd = P.c[t] - cp[t] * a.invls[t];
+            r2 = fmaf(dd, dd, r2);
+          }
       }
+      kpp[P.col * 4 + x] = matern52_f(r2, a.s);
     }
   }
 
   Ctx C;
   C.nb = a.nb;
-  C.zero_blk = a.nb * (a.nb + 1) / 2;
-  C.lp_rs = make_rsrc(a.Lp, (C.zero_blk + 1) * 1024);
-  P.xs_rs = make_rsrc(a.Xs, n_pad * a.dx * 4);
-  P.al_rs = make_rsrc(a.alpha, n_pad * 4);
+  C.nbj = (a.nb + 1) / 2;
+  C.zero_blk = frag_row_start(a.nb);
+  C.lp_rs = make_rsrc(a.Lp, (C.zero_blk + 1) * 2048);
+  Stager<DX4> S;
+  S.xs_rs = make_rsrc(a.Xs, n_pad * a.dx * 4);
+  S.al_rs = make_rsrc(a.alpha, n_pad * 4);
   C.n_pad = n_pad;
   C.wave = wave;
-  C.rr = rr;
+  C.tid = tid;
+  C.xst = xst;
   C.voff = lane * 16;
-  // B fragments: column (b*16 + lane%16), rows 4*(lane/16) .. +3 of a block
-  C.Kb = ring + (size_t)(lane & 15) * kCS + 4 * (lane >> 4);
+  // B fragments: column (b*16 + lane%16), rows 8*(lane/16) .. +7 of a block
+  C.Kb = ring + (lane & 15) * kCSH + 8 * (lane >> 4);
 
   float ss[NCB];
   float gx[NCB][NX];
@@ -314,26 +415,29 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
     for (int r = 0; r < RB; ++r)
 #pragma unroll
       for (int b = 0; b < NCB; ++b) acc[r][b] = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int u = 0; u < CPL; ++u) P.mu[u] = 0.f;
+    P.mu = 0.f;
     Slots<RB> sl;
-    float4 av[RB];
+    AFrag av[RB];
 #pragma unroll
     for (int r = 0; r < RB; ++r) {
       const int I = slot_block(base, r, wave);
-      sl.first[r] = I < a.nb ? I * (I + 1) / 2 : C.zero_blk;
-      sl.last[r] = I < a.nb ? I : -1;
-      av[r] = load4(C.lp_rs, C.voff, frag_block(sl.first[r], sl.last[r], 0, C.zero_blk) * 1024);
+      sl.first[r] = I < a.nb ? frag_row_start(I) : C.zero_blk;
+      sl.last[r] = I < a.nb ? I / 2 : -1;
+      av[r] = load_a(C.lp_rs, C.voff, frag_block(sl.first[r], sl.last[r], 0, C.zero_blk));
     }
-    // the previous pass may still read chunk 0 of the ring
+    // the previous pass may still read chunk 0 of the ring and the staging
     lds_barrier();
-    producer_fetch(P, a, n_pad, 0, rr);
-#pragma unroll
-    for (int jb = 0; jb < 4; ++jb) produce(P, a, n_pad, jb, rr, ring);
+    stage_load(S, a, n_pad, 0, tid);
+    stage_store(S, xst, 0, tid);
+    stage_load(S, a, n_pad, 1, tid);
+    stage_store(S, xst, 1, tid);
+    lds_barrier();
+    produce(P, a, 0, xst, ring);
+    produce(P, a, 1, xst, ring);
     lds_barrier();
     // blocks left of this pass's triangle: every slot is live
-    for (int J = 0; J < base; ++J) step<0, RB, NT, DX4>(C, a, P, ring, sl, J, av, acc);
-    rounds<0, RB, NT, DX4>(C, a, P, ring, sl, base, av, acc);
+    for (int J = 0; J < base / 2; ++J) step<0, RB, NT, DX4>(C, a, P, S, ring, sl, J, av, acc);
+    rounds<0, RB, NT, DX4>(C, a, P, S, ring, sl, base, av, acc);
 
 #pragma unroll
     for (int r = 0; r < RB; ++r)
@@ -350,14 +454,12 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
         }
   }
 
-  // mu: the last pass produced every block; reduce over the 16 lanes of a
-  // column
+  // mu: the last pass produced every block; reduce over the lanes of a column
+  {
+    float v = P.mu;
 #pragma unroll
-  for (int u = 0; u < CPL; ++u) {
-    float v = P.mu[u];
-#pragma unroll
-    for (int off = 8; off > 0; off >>= 1) v += __shfl_xor(v, off);
-    if (rr == 0) mush[P.col0 + u] = v;
+    for (int off = Prod::CPW; off < 64; off <<= 1) v += __shfl_xor(v, off);
+    if (lane < Prod::CPW) mush[P.col] = v;
   }
   // |v|^2 (and cross terms): over the four 16-lane row groups, then over
   // waves in LDS
@@ -450,13 +552,15 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
   }
 }
 
-constexpr size_t lds_floats(int NT, int q) {
-  return (size_t)2 * NT * kCS + (size_t)kWaves * NT * ((q > 1) ? q : 1) + NT + (size_t)NT * 4;
+constexpr size_t lds_floats(int NT, int DX4, int q) {
+  // ring: 2 chunks x 2 planes x NT columns x kCSH halves; staging: 2 chunks
+  return (size_t)NT * kCSH * 2 + (size_t)2 * kChunk * (DX4 * 4 + 4) +
+         (size_t)kWaves * NT * ((q > 1) ? q : 1) + NT + (size_t)NT * 4;
 }
 
 template <int NT, int DX4, int Q, int RB>
 hipError_t launch_t(const PosteriorArgs& a, hipStream_t st) {
-  const size_t lds = sizeof(float) * lds_floats(NT, Q);
+  const size_t lds = sizeof(float) * lds_floats(NT, DX4, Q);
   const unsigned grid = static_cast<unsigned>((a.npts + NT - 1) / NT);
   hipLaunchKernelGGL((k_posterior<NT, DX4, Q, RB>), dim3(grid), dim3(kThreads), lds, st, a);
   return hipGetLastError();
@@ -491,15 +595,17 @@ hipError_t launch_q(const PosteriorArgs& a, hipStream_t st) {
 
 size_t posterior_lds_bytes(int nb, int q) {
   (void)nb;
-  return sizeof(float) * lds_floats(BO_POST_NT, q);
+  return sizeof(float) * lds_floats(BO_POST_NT, 8, q);   // widest coordinate stride
 }
+
+int64_t posterior_frag_blocks(int nb) { return frag_row_start(nb) + 1; }
 
 hipError_t launch_posterior(const PosteriorArgs& a, hipStream_t st) {
   if (a.npts <= 0) return hipSuccess;
-  // row-block slots per wave: the smallest of 2, 4, 8 covering nb / 8
+  // row-block slots per wave: 2 for up to 256 rows, else the configured count
+  // (further rows in passes)
   if (a.nb <= 16) return launch_q<BO_POST_NT, 2>(a, st);
-  if (a.nb <= 32) return launch_q<BO_POST_NT, 4>(a, st);
-  return launch_q<BO_POST_NT, 8>(a, st);
+  return launch_q<BO_POST_NT, BO_POST_RB>(a, st);
 }
 
 }  // namespace bo
