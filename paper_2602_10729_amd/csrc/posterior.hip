@@ -24,12 +24,14 @@
 // in the same 4-lane group and are exchanged with DPP quad permutes) are
 // kept.
 //
-// K*^T is never resident as a whole: it is produced one 64-row chunk ahead
-// of its use into a two-chunk LDS ring of fp16 hi/lo planes, from training
-// rows staged through LDS two chunks ahead. While the matrix cores work on
-// block J, the waves evaluate the ARD Matern-5/2 values of block J + 2 on
-// the vector ALUs (direct differences of lengthscale-scaled coordinates, no
+// K*^T is produced two blocks ahead of its use into an LDS ring of 16
+// blocks (512 rows) of fp16 hi/lo planes, from training rows staged through
+// LDS two 64-row chunks ahead. While the matrix cores work on block J, the
+// waves evaluate the ARD Matern-5/2 values of block J + 2 on the vector ALUs
+// (direct differences of lengthscale-scaled coordinates, no
 // |a|^2 + |b|^2 - 2ab cancellation) and accumulate mu = K* alpha in fp32.
+// A pass that starts while the ring still holds blocks 0.. reuses them, so
+// for n <= 1024 every kernel value is evaluated once.
 // The kernel evaluations and the MFMAs of a step are independent and are
 // interleaved, so each SIMD's matrix core and vector ALU stay busy together.
 // One barrier per chunk publishes the produced block and the staged rows.
@@ -66,8 +68,9 @@ typedef _Float16 halfx8 __attribute__((ext_vector_type(8)));
 constexpr int kWaves = 8;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kJ = 32;                      // rows of K*^T per step (MFMA k)
-constexpr int kChunk = 2 * kJ;              // rows per ring chunk (one barrier each)
-constexpr int kCSH = kChunk + 8;            // ring column stride in halves (36 dwords)
+constexpr int kChunk = 2 * kJ;              // rows per staging chunk (one barrier each)
+constexpr int kRing = 16;                   // K*^T blocks held in LDS
+constexpr int kCSH = kRing * kJ + 8;        // ring column stride in halves (260 dwords)
 
 __device__ __forceinline__ float matern52_f(float r2, float s) {
   const float r = __builtin_amdgcn_sqrtf(r2);
@@ -137,13 +140,15 @@ struct Stager {
 };
 
 template <int DX4>
-__device__ __forceinline__ void stage_load(Stager<DX4>& S, const PosteriorArgs& a, int n_pad,
+__device__ __forceinline__ void stage_load(Stager<DX4>& S, const PosteriorArgs& a, int /*n_pad*/,
                                            int chunk, int tid) {
 #pragma unroll
   for (int i = 0; i < Stager<DX4>::kPer; ++i) {
     const int f = tid + i * kThreads;
     const int r = f / (DX4 + 1), t4 = f % (DX4 + 1);
-    const int row = min(chunk * kChunk + r, n_pad - 1);
+    // rows past n_pad read zeros (buffer range check): zero alpha, so the
+    // blocks past the matrix that the producer may evaluate add nothing to mu
+    const int row = chunk * kChunk + r;
     if (t4 < DX4) {
       S.v[i] = load4(S.xs_rs, (row * a.dx + 4 * t4) * 4, 0);
     } else {
@@ -168,8 +173,7 @@ __device__ __forceinline__ void stage_store(const Stager<DX4>& S, float* xst, in
 }
 
 // Evaluate this lane's rows of block jb into the ring as fp16 hi/lo planes,
-// reading the training rows from the staging slot of jb's chunk. Rows past
-// the matrix produce zeros (never read as B, no weight in mu).
+// reading the training rows from the staging slot of jb's chunk.
 template <int NT, int DX4>
 __device__ __forceinline__ void produce(Producer<NT, DX4>& P, const PosteriorArgs& a, int jb,
                                         const float* xst, _Float16* ring) {
@@ -194,13 +198,15 @@ __device__ __forceinline__ void produce(Producer<NT, DX4>& P, const PosteriorArg
       r2 = fmaf(d2, d2, r2);
       r2 = fmaf(d3, d3, r2);
     }
-    const float kv = (P.valid && row < a.n) ? matern52_f(r2, a.s) : 0.f;
+    // no mask: rows past n (zero coordinates) meet zero columns of L^{-1}
+    // and zero alpha; columns past the batch are never written
+    const float kv = matern52_f(r2, a.s);
     P.mu = fmaf(xr[u * RS + 4 * DX4], kv, P.mu);
     const _Float16 h = static_cast<_Float16>(kv);
     hi[u] = h;
     lo[u] = static_cast<_Float16>(kv - static_cast<float>(h));
   }
-  _Float16* dst = ring + (((jb >> 1) & 1) * 2 * NT + P.col) * kCSH + (jb & 1) * kJ + P.row0;
+  _Float16* dst = ring + P.col * kCSH + (jb % kRing) * kJ + P.row0;
   *reinterpret_cast<halfr*>(dst) = hi;
   *reinterpret_cast<halfr*>(dst + NT * kCSH) = lo;
 }
@@ -279,7 +285,7 @@ struct Ctx {
 template <int NCB>
 __device__ __forceinline__ void load_b(const Ctx& C, int J, halfx8 (&bh)[NCB], halfx8 (&bl)[NCB]) {
   constexpr int NT = NCB * 16;
-  const _Float16* kb = C.Kb + ((J >> 1) & 1) * 2 * NT * kCSH + (J & 1) * kJ;
+  const _Float16* kb = C.Kb + (J % kRing) * kJ;
 #pragma unroll
   for (int b = 0; b < NCB; ++b) {
     bh[b] = *reinterpret_cast<const halfx8*>(kb + b * 16 * kCSH);
@@ -289,12 +295,12 @@ __device__ __forceinline__ void load_b(const Ctx& C, int J, halfx8 (&bh)[NCB], h
 
 // One step J for slots [LO, RB): the B fragments of block J are read first
 // (ahead of the producer's LDS stores, so the MFMAs do not wait behind them),
-// then the producer's block J + 2 and the MFMAs of block J (fragments for
-// J + 1 requested on the way) are left to the scheduler to interleave: the
-// two are independent, and the fp16 MFMAs overlap the VALU work. At a chunk's
-// first step the rows of chunk J/2 + 2 are fetched, at its last they are
-// staged and the chunk barrier is taken.
-template <int LO, int RB, int NT, int DX4>
+// then the producer's block J + 2 (when PROD) and the MFMAs of block J
+// (fragments for J + 1 requested on the way) are left to the scheduler to
+// interleave: the two are independent, and the fp16 MFMAs overlap the VALU
+// work. At a chunk's first step the rows of chunk J/2 + 2 are fetched, at its
+// last they are staged and the chunk barrier is taken.
+template <int LO, int RB, int NT, int DX4, bool PROD>
 __device__ __forceinline__ void step(const Ctx& C, const PosteriorArgs& a, Producer<NT, DX4>& P,
                                      Stager<DX4>& S, _Float16* ring, const Slots<RB>& sl, int J,
                                      AFrag (&av)[RB], floatx4 (&acc)[RB][NT / 16]) {
@@ -302,12 +308,26 @@ __device__ __forceinline__ void step(const Ctx& C, const PosteriorArgs& a, Produ
   constexpr int NCB = NT / 16;
   halfx8 bh[NCB], bl[NCB];
   load_b<NCB>(C, J, bh, bl);
-  produce(P, a, J + 2, C.xst, ring);
+  if constexpr (PROD) produce(P, a, J + 2, C.xst, ring);
   mfma_slots<LO, RB, NCB>(av, bh, bl, acc, C.lp_rs, sl, J + 1, C.zero_blk, C.voff);
   if (J & 1) {
     stage_store(S, C.xst, (J >> 1) + 2, C.tid);
     lds_barrier();
   }
+}
+
+// Steps [j0, j1) for slots [LO, RB); the producer runs at the steps whose
+// block J + 2 lies in the pass's production window [pw0, pw1).
+template <int LO, int RB, int NT, int DX4>
+__device__ __forceinline__ void span(const Ctx& C, const PosteriorArgs& a, Producer<NT, DX4>& P,
+                                     Stager<DX4>& S, _Float16* ring, const Slots<RB>& sl, int j0,
+                                     int j1, int pw0, int pw1, AFrag (&av)[RB],
+                                     floatx4 (&acc)[RB][NT / 16]) {
+  const int p0 = min(max(pw0 - 2, j0), j1), p1 = min(max(pw1 - 2, p0), j1);
+  int J = j0;
+  for (; J < p0; ++J) step<LO, RB, NT, DX4, false>(C, a, P, S, ring, sl, J, av, acc);
+  for (; J < p1; ++J) step<LO, RB, NT, DX4, true>(C, a, P, S, ring, sl, J, av, acc);
+  for (; J < j1; ++J) step<LO, RB, NT, DX4, false>(C, a, P, S, ring, sl, J, av, acc);
 }
 
 // Rounds R.. of the triangular part of a pass: round R covers the row blocks
@@ -316,16 +336,16 @@ __device__ __forceinline__ void step(const Ctx& C, const PosteriorArgs& a, Produ
 template <int R, int RB, int NT, int DX4>
 __device__ __forceinline__ void rounds(const Ctx& C, const PosteriorArgs& a, Producer<NT, DX4>& P,
                                        Stager<DX4>& S, _Float16* ring, const Slots<RB>& sl,
-                                       int base, AFrag (&av)[RB], floatx4 (&acc)[RB][NT / 16]) {
+                                       int base, int pw0, int pw1, AFrag (&av)[RB],
+                                       floatx4 (&acc)[RB][NT / 16]) {
   if constexpr (R < RB) {
     const int j0 = base / 2 + 4 * R;
     if (j0 >= C.nbj) return;
     const int jend = min(j0 + 4, C.nbj);
     const int jlive = min(slot_block(base, R, C.wave) / 2 + 1, jend);
-    int J = j0;
-    for (; J < jlive; ++J) step<R, RB, NT, DX4>(C, a, P, S, ring, sl, J, av, acc);
-    for (; J < jend; ++J) step<R + 1, RB, NT, DX4>(C, a, P, S, ring, sl, J, av, acc);
-    rounds<R + 1, RB, NT, DX4>(C, a, P, S, ring, sl, base, av, acc);
+    span<R, RB, NT, DX4>(C, a, P, S, ring, sl, j0, jlive, pw0, pw1, av, acc);
+    span<R + 1, RB, NT, DX4>(C, a, P, S, ring, sl, jlive, jend, pw0, pw1, av, acc);
+    rounds<R + 1, RB, NT, DX4>(C, a, P, S, ring, sl, base, pw0, pw1, av, acc);
   }
 }
 
@@ -341,10 +361,10 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
   // wave index as a scalar: the loop control below stays uniform
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n_pad = a.nb * kBlk;
-  _Float16* ring = reinterpret_cast<_Float16*>(smem);       // 2 chunks x 2 planes x NT x kCSH
-  float* xst = smem + 2 * NT * kCSH;                        // 2 x kChunk x RS (staged rows)
-  float* red = xst + 2 * kChunk * Stager<DX4>::RS;          // kWaves * NT * NX
-  float* mush = red + kWaves * NT * NX;                     // NT
+  _Float16* ring = reinterpret_cast<_Float16*>(smem);       // 2 planes x NT x kCSH halves
+  float* xst = smem + NT * kCSH;                            // 2 x kChunk x RS (staged rows)
+  float* red = smem;                                        // kWaves * NT * NX, after the loop
+  float* mush = xst + 2 * kChunk * Stager<DX4>::RS;         // NT
   float* kpp = mush + NT;                                   // NT * 4 (prior cross-cov)
   const int64_t p0 = (int64_t)blockIdx.x * NT;
 
@@ -409,13 +429,15 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
     for (int x = 0; x < NX; ++x) gx[b][x] = 0.f;
   }
 
+  // blocks 0 .. have-1 of K*^T are in the ring (have = 0: start over)
+  int have = 0;
   for (int base = 0; base < a.nb; base += 8 * RB) {
+    const int jpass = min(C.nbj, base / 2 + 4 * RB);   // J range of this pass
     floatx4 acc[RB][NCB];
 #pragma unroll
     for (int r = 0; r < RB; ++r)
 #pragma unroll
       for (int b = 0; b < NCB; ++b) acc[r][b] = floatx4{0.f, 0.f, 0.f, 0.f};
-    P.mu = 0.f;
     Slots<RB> sl;
     AFrag av[RB];
 #pragma unroll
@@ -425,19 +447,26 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
       sl.last[r] = I < a.nb ? I / 2 : -1;
       av[r] = load_a(C.lp_rs, C.voff, frag_block(sl.first[r], sl.last[r], 0, C.zero_blk));
     }
-    // the previous pass may still read chunk 0 of the ring and the staging
+    // the previous pass may still read the staging slots
     lds_barrier();
     stage_load(S, a, n_pad, 0, tid);
     stage_store(S, xst, 0, tid);
     stage_load(S, a, n_pad, 1, tid);
     stage_store(S, xst, 1, tid);
     lds_barrier();
-    produce(P, a, 0, xst, ring);
-    produce(P, a, 1, xst, ring);
-    lds_barrier();
+    if (have == 0) {
+      // start over: blocks 0 and 1, and mu from scratch
+      P.mu = 0.f;
+      produce(P, a, 0, xst, ring);
+      produce(P, a, 1, xst, ring);
+      have = 2;
+      lds_barrier();
+    }
+    const int pw0 = have, pw1 = jpass;   // blocks this pass produces
     // blocks left of this pass's triangle: every slot is live
-    for (int J = 0; J < base / 2; ++J) step<0, RB, NT, DX4>(C, a, P, S, ring, sl, J, av, acc);
-    rounds<0, RB, NT, DX4>(C, a, P, S, ring, sl, base, av, acc);
+    span<0, RB, NT, DX4>(C, a, P, S, ring, sl, 0, base / 2, pw0, pw1, av, acc);
+    rounds<0, RB, NT, DX4>(C, a, P, S, ring, sl, base, pw0, pw1, av, acc);
+    have = (jpass <= kRing) ? max(have, jpass) : 0;
 
 #pragma unroll
     for (int r = 0; r < RB; ++r)
@@ -462,7 +491,8 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
     if (lane < Prod::CPW) mush[P.col] = v;
   }
   // |v|^2 (and cross terms): over the four 16-lane row groups, then over
-  // waves in LDS
+  // waves in LDS (red overlays the ring: wait until every wave is done)
+  __syncthreads();
 #pragma unroll
   for (int b = 0; b < NCB; ++b) {
     ss[b] += __shfl_xor(ss[b], 16);
@@ -553,14 +583,21 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
 }
 
 constexpr size_t lds_floats(int NT, int DX4, int q) {
-  // ring: 2 chunks x 2 planes x NT columns x kCSH halves; staging: 2 chunks
-  return (size_t)NT * kCSH * 2 + (size_t)2 * kChunk * (DX4 * 4 + 4) +
-         (size_t)kWaves * NT * ((q > 1) ? q : 1) + NT + (size_t)NT * 4;
+  // ring: 2 planes x NT columns x kCSH halves (the reduction overlays it);
+  // staging: 2 chunks; mu and the prior cross-covariances
+  return (size_t)NT * kCSH + (size_t)2 * kChunk * (DX4 * 4 + 4) + NT + (size_t)NT * 4;
 }
+static_assert((size_t)kWaves * 64 * 4 <= (size_t)64 * kCSH, "reduction fits the ring");
 
 template <int NT, int DX4, int Q, int RB>
 hipError_t launch_t(const PosteriorArgs& a, hipStream_t st) {
   const size_t lds = sizeof(float) * lds_floats(NT, DX4, Q);
+  // more than 64 KiB of dynamic LDS: opt in (cheap; set on every launch so
+  // that it holds on whichever device is current)
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_posterior<NT, DX4, Q, RB>),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize,
+                                     static_cast<int>(lds));
+  if (e != hipSuccess) return e;
   const unsigned grid = static_cast<unsigned>((a.npts + NT - 1) / NT);
   hipLaunchKernelGGL((k_posterior<NT, DX4, Q, RB>), dim3(grid), dim3(kThreads), lds, st, a);
   return hipGetLastError();
