@@ -26,7 +26,7 @@
 //
 // K*^T is produced two blocks ahead of its use into an LDS ring of 16
 // blocks (512 rows) of fp16 hi/lo planes, from training rows staged through
-// LDS two 64-row chunks ahead. While the matrix cores work on block J, the
+// LDS two blocks ahead of that. While the matrix cores work on block J, the
 // waves evaluate the ARD Matern-5/2 values of block J + 2 on the vector ALUs
 // (direct differences of lengthscale-scaled coordinates, no
 // |a|^2 + |b|^2 - 2ab cancellation) and accumulate mu = K* alpha in fp32.
@@ -34,7 +34,7 @@
 // for n <= 1024 every kernel value is evaluated once.
 // The kernel evaluations and the MFMAs of a step are independent and are
 // interleaved, so each SIMD's matrix core and vector ALU stay busy together.
-// One barrier per chunk publishes the produced block and the staged rows.
+// One barrier per step publishes the produced block and the staged rows.
 //
 // Each wave owns RB row-block slots, slot r holding row block
 // base + 8r + (r even ? wave : 7 - wave); this snake keeps the per-SIMD
@@ -68,7 +68,6 @@ typedef _Float16 halfx8 __attribute__((ext_vector_type(8)));
 constexpr int kWaves = 8;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kJ = 32;                      // rows of K*^T per step (MFMA k)
-constexpr int kChunk = 2 * kJ;              // rows per staging chunk (one barrier each)
 constexpr int kRing = 16;                   // K*^T blocks held in LDS
 constexpr int kCSH = kRing * kJ + 8;        // ring column stride in halves (260 dwords)
 
@@ -127,53 +126,44 @@ struct Producer {
   int row0;                 // first row of this lane inside a block
 };
 
-// Training rows of one chunk staged in LDS: [kChunk][dx + 4] floats, the
-// last float4 of a row holding (alpha, 0, 0, 0). Two slots; the stager loads
-// chunk c + 2 into slot c % 2 while chunk c + 1 is produced from the other.
+// Training rows staged in LDS, one 32-row block per slot, four slots: row
+// r of block b at slot b % 4, [kJ][dx + 4] floats per slot, the last float4
+// of a row holding (alpha, 0, 0, 0). Step J loads the rows of block J + 4
+// first and stores them last, while the producer reads block J + 2. Every
+// thread issues the same loads (a spare thread's store goes to a scratch
+// float4), so no branch makes the compiler drain the loads in flight.
 template <int DX4>
 struct Stager {
   static constexpr int RS = DX4 * 4 + 4;                 // row stride (floats)
-  static constexpr int kF4 = kChunk * (DX4 + 1);         // float4s per chunk
-  static constexpr int kPer = (kF4 + kThreads - 1) / kThreads;
-  float4 v[kPer];
+  static constexpr int kF4 = kJ * (DX4 + 1);             // float4s per block
+  static constexpr int kSlot = kJ * RS;                  // floats per slot
+  static_assert(kF4 <= kThreads, "one float4 per thread");
+  float4 x;                 // the loads in flight (selected at the store,
+  float al;                 // so the loads are not waited for early)
+  int soff;                 // this thread's float offset inside a slot (or the scratch)
+  int row, t4;
   __amdgpu_buffer_rsrc_t xs_rs, al_rs;
 };
 
+// Rows past n_pad read zeros (buffer range check), so blocks past the matrix
+// that the producer may evaluate carry zero alpha and add nothing to mu.
 template <int DX4>
-__device__ __forceinline__ void stage_load(Stager<DX4>& S, const PosteriorArgs& a, int /*n_pad*/,
-                                           int chunk, int tid) {
-#pragma unroll
-  for (int i = 0; i < Stager<DX4>::kPer; ++i) {
-    const int f = tid + i * kThreads;
-    const int r = f / (DX4 + 1), t4 = f % (DX4 + 1);
-    // rows past n_pad read zeros (buffer range check): zero alpha, so the
-    // blocks past the matrix that the producer may evaluate add nothing to mu
-    const int row = chunk * kChunk + r;
-    if (t4 < DX4) {
-      S.v[i] = load4(S.xs_rs, (row * a.dx + 4 * t4) * 4, 0);
-    } else {
-      const float al =
-          __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(S.al_rs, row * 4, 0, 0));
-      S.v[i] = float4{al, 0.f, 0.f, 0.f};
-    }
-  }
+__device__ __forceinline__ void stage_load(Stager<DX4>& S, const PosteriorArgs& a, int jb) {
+  const int row = jb * kJ + S.row;
+  S.x = load4(S.xs_rs, (row * a.dx + 4 * min(S.t4, DX4 - 1)) * 4, 0);
+  S.al = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(S.al_rs, row * 4, 0, 0));
 }
 
 template <int DX4>
-__device__ __forceinline__ void stage_store(const Stager<DX4>& S, float* xst, int chunk, int tid) {
-  float* dst = xst + (chunk & 1) * kChunk * Stager<DX4>::RS;
-#pragma unroll
-  for (int i = 0; i < Stager<DX4>::kPer; ++i) {
-    const int f = tid + i * kThreads;
-    if (f < Stager<DX4>::kF4) {
-      const int r = f / (DX4 + 1), t4 = f % (DX4 + 1);
-      *reinterpret_cast<float4*>(dst + r * Stager<DX4>::RS + 4 * t4) = S.v[i];
-    }
-  }
+__device__ __forceinline__ void stage_store(const Stager<DX4>& S, float* xst, int jb) {
+  const bool is_al = S.t4 == DX4;
+  const float4 v{is_al ? S.al : S.x.x, is_al ? 0.f : S.x.y, is_al ? 0.f : S.x.z,
+                 is_al ? 0.f : S.x.w};
+  *reinterpret_cast<float4*>(xst + (jb & 3) * Stager<DX4>::kSlot + S.soff) = v;
 }
 
 // Evaluate this lane's rows of block jb into the ring as fp16 hi/lo planes,
-// reading the training rows from the staging slot of jb's chunk.
+// reading the training rows from jb's staging slot.
 template <int NT, int DX4>
 __device__ __forceinline__ void produce(Producer<NT, DX4>& P, const PosteriorArgs& a, int jb,
                                         const float* xst, _Float16* ring) {
@@ -181,7 +171,7 @@ __device__ __forceinline__ void produce(Producer<NT, DX4>& P, const PosteriorArg
   constexpr int RS = Stager<DX4>::RS;
   typedef _Float16 halfr __attribute__((ext_vector_type(RPL)));
   halfr hi, lo;
-  const float* xr = xst + ((jb >> 1) & 1) * kChunk * RS + ((jb & 1) * kJ + P.row0) * RS;
+  const float* xr = xst + (jb & 3) * Stager<DX4>::kSlot + P.row0 * RS;
 #pragma unroll
   for (int u = 0; u < RPL; ++u) {
     const int row = jb * kJ + P.row0 + u;
@@ -240,36 +230,35 @@ __device__ __forceinline__ AFrag load_a(__amdgpu_buffer_rsrc_t rs, int voff, int
   return f;
 }
 
-// MFMAs of one K*^T block for the slots [LO, RB), two slots at a time (the
-// three products of a pair of slots and all column blocks are independent);
-// each pair's fragments for the next block are requested as soon as its MFMAs
-// are issued, so they have a whole step to arrive.
-template <int LO, int RB, int NCB>
-__device__ __forceinline__ void mfma_slots(AFrag (&av)[RB], const halfx8 (&bh)[NCB],
-                                           const halfx8 (&bl)[NCB], floatx4 (&acc)[RB][NCB],
-                                           __amdgpu_buffer_rsrc_t lp_rs, const Slots<RB>& sl,
-                                           int Jn, int zero_blk, int voff) {
+// B fragments of one half of a block (column blocks 2h and 2h + 1), hi and lo
+// planes.
+struct BHalf {
+  halfx8 hi[2], lo[2];
+};
+
+// MFMAs of slots r0, r0 + 1 (those below RB) against one half of a block's
+// columns: the three products of the pair's (up to) four accumulators.
+template <int RB, int NCB, int H>
+__device__ __forceinline__ void mfma_pair_half(int r0, const AFrag (&av)[RB], const BHalf& B,
+                                               floatx4 (&acc)[RB][NCB]) {
 #pragma unroll
-  for (int r0 = LO; r0 < RB; r0 += 2) {
+  for (int r = r0; r < r0 + 2 && r < RB; ++r)
 #pragma unroll
-    for (int r = r0; r < r0 + 2 && r < RB; ++r)
+    for (int b = 0; b < 2; ++b)
+      acc[r][2 * H + b] =
+          __builtin_amdgcn_mfma_f32_16x16x32_f16(av[r].hi, B.hi[b], acc[r][2 * H + b], 0, 0, 0);
 #pragma unroll
-      for (int b = 0; b < NCB; ++b)
-        acc[r][b] = __builtin_amdgcn_mfma_f32_16x16x32_f16(av[r].hi, bh[b], acc[r][b], 0, 0, 0);
+  for (int r = r0; r < r0 + 2 && r < RB; ++r)
 #pragma unroll
-    for (int r = r0; r < r0 + 2 && r < RB; ++r)
+    for (int b = 0; b < 2; ++b)
+      acc[r][2 * H + b] =
+          __builtin_amdgcn_mfma_f32_16x16x32_f16(av[r].hi, B.lo[b], acc[r][2 * H + b], 0, 0, 0);
 #pragma unroll
-      for (int b = 0; b < NCB; ++b)
-        acc[r][b] = __builtin_amdgcn_mfma_f32_16x16x32_f16(av[r].hi, bl[b], acc[r][b], 0, 0, 0);
+  for (int r = r0; r < r0 + 2 && r < RB; ++r)
 #pragma unroll
-    for (int r = r0; r < r0 + 2 && r < RB; ++r)
-#pragma unroll
-      for (int b = 0; b < NCB; ++b)
-        acc[r][b] = __builtin_amdgcn_mfma_f32_16x16x32_f16(av[r].lo, bh[b], acc[r][b], 0, 0, 0);
-#pragma unroll
-    for (int r = r0; r < r0 + 2 && r < RB; ++r)
-      av[r] = load_a(lp_rs, voff, frag_block(sl.first[r], sl.last[r], Jn, zero_blk));
-  }
+    for (int b = 0; b < 2; ++b)
+      acc[r][2 * H + b] =
+          __builtin_amdgcn_mfma_f32_16x16x32_f16(av[r].lo, B.hi[b], acc[r][2 * H + b], 0, 0, 0);
 }
 
 // Workgroup-uniform context of the streaming loop.
@@ -278,42 +267,58 @@ struct Ctx {
   int nb, nbj, zero_blk, n_pad, wave, tid;
   int voff;                 // this lane's byte offset inside a fragment plane
   const _Float16* Kb;       // this lane's B-fragment base inside the ring
-  float* xst;               // training-row staging (2 chunks)
+  float* xst;               // training-row staging (4 blocks)
 };
 
-// B fragments of block J: column (b*16 + lane%16), rows 8*(lane/16) .. +7.
-template <int NCB>
-__device__ __forceinline__ void load_b(const Ctx& C, int J, halfx8 (&bh)[NCB], halfx8 (&bl)[NCB]) {
-  constexpr int NT = NCB * 16;
+// B fragments of half h of block J: columns (2h + b)*16 + lane%16, rows
+// 8*(lane/16) .. +7.
+template <int NT>
+__device__ __forceinline__ void load_b(const Ctx& C, int J, int h, BHalf& B) {
   const _Float16* kb = C.Kb + (J % kRing) * kJ;
 #pragma unroll
-  for (int b = 0; b < NCB; ++b) {
-    bh[b] = *reinterpret_cast<const halfx8*>(kb + b * 16 * kCSH);
-    bl[b] = *reinterpret_cast<const halfx8*>(kb + (NT + b * 16) * kCSH);
+  for (int b = 0; b < 2; ++b) {
+    B.hi[b] = *reinterpret_cast<const halfx8*>(kb + (2 * h + b) * 16 * kCSH);
+    B.lo[b] = *reinterpret_cast<const halfx8*>(kb + (NT + (2 * h + b) * 16) * kCSH);
   }
 }
 
-// One step J for slots [LO, RB): the B fragments of block J are read first
-// (ahead of the producer's LDS stores, so the MFMAs do not wait behind them),
-// then the producer's block J + 2 (when PROD) and the MFMAs of block J
-// (fragments for J + 1 requested on the way) are left to the scheduler to
-// interleave: the two are independent, and the fp16 MFMAs overlap the VALU
-// work. At a chunk's first step the rows of chunk J/2 + 2 are fetched, at its
-// last they are staged and the chunk barrier is taken.
+// One step J for slots [LO, RB). B0 holds the first half of block J's B
+// fragments on entry (read during the previous step) and the first half of
+// block J + 1's on exit; the second half is read at the start. The MFMAs of
+// block J (fragments for J + 1 requested on the way) and the producer's block
+// J + 2 (when PROD) are independent and are left to the scheduler to
+// interleave: the fp16 MFMAs overlap the VALU work. The step's barrier
+// publishes the produced block and the staged rows; block J + 1 was
+// published by the previous step's, so its B fragments can be read early.
 template <int LO, int RB, int NT, int DX4, bool PROD>
 __device__ __forceinline__ void step(const Ctx& C, const PosteriorArgs& a, Producer<NT, DX4>& P,
                                      Stager<DX4>& S, _Float16* ring, const Slots<RB>& sl, int J,
-                                     AFrag (&av)[RB], floatx4 (&acc)[RB][NT / 16]) {
-  if ((J & 1) == 0) stage_load(S, a, C.n_pad, (J >> 1) + 2, C.tid);
+                                     BHalf& B0, AFrag (&av)[RB], floatx4 (&acc)[RB][NT / 16]) {
   constexpr int NCB = NT / 16;
-  halfx8 bh[NCB], bl[NCB];
-  load_b<NCB>(C, J, bh, bl);
+  static_assert(NCB == 4, "two halves of two column blocks");
+  // the staging load goes first among the step's loads and its store last,
+  // so the store waits for it alone, a whole step after it was issued
+  stage_load(S, a, J + 4);
+  __builtin_amdgcn_sched_barrier(0);
+  BHalf B1;
+  load_b<NT>(C, J, 1, B1);
   if constexpr (PROD) produce(P, a, J + 2, C.xst, ring);
-  mfma_slots<LO, RB, NCB>(av, bh, bl, acc, C.lp_rs, sl, J + 1, C.zero_blk, C.voff);
-  if (J & 1) {
-    stage_store(S, C.xst, (J >> 1) + 2, C.tid);
-    lds_barrier();
+  // slot pairs in turn, each pair's fragments for J + 1 requested as soon as
+  // its MFMAs are issued (about half a step before the next step needs them);
+  // the next block's first B half is read once the last pair is done with it
+#pragma unroll
+  for (int r0 = LO; r0 < RB; r0 += 2) {
+    mfma_pair_half<RB, NCB, 0>(r0, av, B0, acc);
+    if (r0 + 2 >= RB) load_b<NT>(C, J + 1, 0, B0);
+    mfma_pair_half<RB, NCB, 1>(r0, av, B1, acc);
+#pragma unroll
+    for (int r = r0; r < r0 + 2 && r < RB; ++r)
+      av[r] = load_a(C.lp_rs, C.voff, frag_block(sl.first[r], sl.last[r], J + 1, C.zero_blk));
   }
+  if constexpr (LO >= RB) load_b<NT>(C, J + 1, 0, B0);
+  __builtin_amdgcn_sched_barrier(0);
+  stage_store(S, C.xst, J + 4);
+  lds_barrier();
 }
 
 // Steps [j0, j1) for slots [LO, RB); the producer runs at the steps whose
@@ -321,13 +326,13 @@ __device__ __forceinline__ void step(const Ctx& C, const PosteriorArgs& a, Produ
 template <int LO, int RB, int NT, int DX4>
 __device__ __forceinline__ void span(const Ctx& C, const PosteriorArgs& a, Producer<NT, DX4>& P,
                                      Stager<DX4>& S, _Float16* ring, const Slots<RB>& sl, int j0,
-                                     int j1, int pw0, int pw1, AFrag (&av)[RB],
+                                     int j1, int pw0, int pw1, BHalf& B0, AFrag (&av)[RB],
                                      floatx4 (&acc)[RB][NT / 16]) {
   const int p0 = min(max(pw0 - 2, j0), j1), p1 = min(max(pw1 - 2, p0), j1);
   int J = j0;
-  for (; J < p0; ++J) step<LO, RB, NT, DX4, false>(C, a, P, S, ring, sl, J, av, acc);
-  for (; J < p1; ++J) step<LO, RB, NT, DX4, true>(C, a, P, S, ring, sl, J, av, acc);
-  for (; J < j1; ++J) step<LO, RB, NT, DX4, false>(C, a, P, S, ring, sl, J, av, acc);
+  for (; J < p0; ++J) step<LO, RB, NT, DX4, false>(C, a, P, S, ring, sl, J, B0, av, acc);
+  for (; J < p1; ++J) step<LO, RB, NT, DX4, true>(C, a, P, S, ring, sl, J, B0, av, acc);
+  for (; J < j1; ++J) step<LO, RB, NT, DX4, false>(C, a, P, S, ring, sl, J, B0, av, acc);
 }
 
 // Rounds R.. of the triangular part of a pass: round R covers the row blocks
@@ -336,16 +341,16 @@ __device__ __forceinline__ void span(const Ctx& C, const PosteriorArgs& a, Produ
 template <int R, int RB, int NT, int DX4>
 __device__ __forceinline__ void rounds(const Ctx& C, const PosteriorArgs& a, Producer<NT, DX4>& P,
                                        Stager<DX4>& S, _Float16* ring, const Slots<RB>& sl,
-                                       int base, int pw0, int pw1, AFrag (&av)[RB],
+                                       int base, int pw0, int pw1, BHalf& B0, AFrag (&av)[RB],
                                        floatx4 (&acc)[RB][NT / 16]) {
   if constexpr (R < RB) {
     const int j0 = base / 2 + 4 * R;
     if (j0 >= C.nbj) return;
     const int jend = min(j0 + 4, C.nbj);
     const int jlive = min(slot_block(base, R, C.wave) / 2 + 1, jend);
-    span<R, RB, NT, DX4>(C, a, P, S, ring, sl, j0, jlive, pw0, pw1, av, acc);
-    span<R + 1, RB, NT, DX4>(C, a, P, S, ring, sl, jlive, jend, pw0, pw1, av, acc);
-    rounds<R + 1, RB, NT, DX4>(C, a, P, S, ring, sl, base, pw0, pw1, av, acc);
+    span<R, RB, NT, DX4>(C, a, P, S, ring, sl, j0, jlive, pw0, pw1, B0, av, acc);
+    span<R + 1, RB, NT, DX4>(C, a, P, S, ring, sl, jlive, jend, pw0, pw1, B0, av, acc);
+    rounds<R + 1, RB, NT, DX4>(C, a, P, S, ring, sl, base, pw0, pw1, B0, av, acc);
   }
 }
 
@@ -362,9 +367,9 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n_pad = a.nb * kBlk;
   _Float16* ring = reinterpret_cast<_Float16*>(smem);       // 2 planes x NT x kCSH halves
-  float* xst = smem + NT * kCSH;                            // 2 x kChunk x RS (staged rows)
+  float* xst = smem + NT * kCSH;                            // 4 slots + a scratch float4
   float* red = smem;                                        // kWaves * NT * NX, after the loop
-  float* mush = xst + 2 * kChunk * Stager<DX4>::RS;         // NT
+  float* mush = xst + 4 * Stager<DX4>::kSlot + 4;           // NT
   float* kpp = mush + NT;                                   // NT * 4 (prior cross-cov)
   const int64_t p0 = (int64_t)blockIdx.x * NT;
 
@@ -412,6 +417,9 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
   Stager<DX4> S;
   S.xs_rs = make_rsrc(a.Xs, n_pad * a.dx * 4);
   S.al_rs = make_rsrc(a.alpha, n_pad * 4);
+  S.row = min(tid / (DX4 + 1), kJ - 1);
+  S.t4 = tid % (DX4 + 1);
+  S.soff = (tid < Stager<DX4>::kF4) ? S.row * Stager<DX4>::RS + 4 * S.t4 : 4 * Stager<DX4>::kSlot;
   C.n_pad = n_pad;
   C.wave = wave;
   C.tid = tid;
@@ -449,10 +457,17 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
     }
     // the previous pass may still read the staging slots
     lds_barrier();
-    stage_load(S, a, n_pad, 0, tid);
-    stage_store(S, xst, 0, tid);
-    stage_load(S, a, n_pad, 1, tid);
-    stage_store(S, xst, 1, tid);
+    {
+      // blocks 0..3 at once: one load latency, not four
+      Stager<DX4> S4[4];
+#pragma unroll
+      for (int jb = 0; jb < 4; ++jb) {
+        S4[jb] = S;
+        stage_load(S4[jb], a, jb);
+      }
+#pragma unroll
+      for (int jb = 0; jb < 4; ++jb) stage_store(S4[jb], xst, jb);
+    }
     lds_barrier();
     if (have == 0) {
       // start over: blocks 0 and 1, and mu from scratch
@@ -463,9 +478,11 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
       lds_barrier();
     }
     const int pw0 = have, pw1 = jpass;   // blocks this pass produces
+    BHalf B0;
+    load_b<NT>(C, 0, 0, B0);
     // blocks left of this pass's triangle: every slot is live
-    span<0, RB, NT, DX4>(C, a, P, S, ring, sl, 0, base / 2, pw0, pw1, av, acc);
-    rounds<0, RB, NT, DX4>(C, a, P, S, ring, sl, base, pw0, pw1, av, acc);
+    span<0, RB, NT, DX4>(C, a, P, S, ring, sl, 0, base / 2, pw0, pw1, B0, av, acc);
+    rounds<0, RB, NT, DX4>(C, a, P, S, ring, sl, base, pw0, pw1, B0, av, acc);
     have = (jpass <= kRing) ? max(have, jpass) : 0;
 
 #pragma unroll
@@ -584,8 +601,8 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
 
 constexpr size_t lds_floats(int NT, int DX4, int q) {
   // ring: 2 planes x NT columns x kCSH halves (the reduction overlays it);
-  // staging: 2 chunks; mu and the prior cross-covariances
-  return (size_t)NT * kCSH + (size_t)2 * kChunk * (DX4 * 4 + 4) + NT + (size_t)NT * 4;
+  // staging: 4 slots + a scratch float4; mu and the prior cross-covariances
+  return (size_t)NT * kCSH + (size_t)4 * kJ * (DX4 * 4 + 4) + 4 + NT + (size_t)NT * 4;
 }
 static_assert((size_t)kWaves * 64 * 4 <= (size_t)64 * kCSH, "reduction fits the ring");
 
