@@ -316,6 +316,20 @@ __device__ __forceinline__ void step(const Ctx& C, const PosteriorArgs& a, Produ
       av[r] = load_a(C.lp_rs, C.voff, frag_block(sl.first[r], sl.last[r], J + 1, C.zero_blk));
   }
   if constexpr (LO >= RB) load_b<NT>(C, J + 1, 0, B0);
+  if constexpr (PROD) {
+    // interleave: the scheduler otherwise runs the producer's VALU work and
+    // the MFMAs as two separate stretches, and the two waves of a SIMD
+    // (kept in step by the barriers) then contend for the same unit
+    constexpr int nM = 3 * NCB * (RB - LO);
+    constexpr int nV = Producer<NT, DX4>::RPL * (2 * 4 * DX4 + 14);
+    if constexpr (nM > 0) {
+#pragma unroll
+      for (int i = 0; i < nM; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                  // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x002, (nV + nM - 1) / nM, 0);  // VALU
+      }
+    }
+  }
   __builtin_amdgcn_sched_barrier(0);
   stage_store(S, C.xst, J + 4);
   lds_barrier();
