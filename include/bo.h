@@ -211,6 +211,7 @@ bo_status bo_profile_read(double* posterior_ms, double* ehvi_ms, int64_t* calls,
  *   BO_PEAK_VALU_CLAMP lane-ops/s of the (sub, med3, fma) pattern of the EHVI loop
  *   BO_PEAK_MFMA_F32   flop/s of independent v_mfma_f32_16x16x4f32 chains
  *   BO_PEAK_HBM_COPY   bytes/s (read + write) of a 1 GiB streaming copy
+ *   BO_PEAK_MFMA_F16   flop/s of independent v_mfma_f32_16x16x32_f16 chains
  * iters: inner iterations for the compute probes (ignored by the copy).
  * Allocates its own buffers. Errors: INVALID_ARGUMENT, DEVICE, OUT_OF_MEMORY.
  */
@@ -218,6 +219,7 @@ bo_status bo_profile_read(double* posterior_ms, double* ehvi_ms, int64_t* calls,
 #define BO_PEAK_VALU_CLAMP 1
 #define BO_PEAK_MFMA_F32 2
 #define BO_PEAK_HBM_COPY 3
+#define BO_PEAK_MFMA_F16 4
 bo_status bo_measure_peak(int32_t what, int64_t iters, double* rate, void* stream);
 
 /* Releases a model (waits for its last stream first). NULL is a no-op. */

@@ -217,7 +217,7 @@ def profile_read():
     return a.value, b.value, c.value, n.value
 
 
-PEAK_VALU_FMA, PEAK_VALU_CLAMP, PEAK_MFMA_F32, PEAK_HBM_COPY = 0, 1, 2, 3
+PEAK_VALU_FMA, PEAK_VALU_CLAMP, PEAK_MFMA_F32, PEAK_HBM_COPY, PEAK_MFMA_F16 = 0, 1, 2, 3, 4
 
 
 def measure_peak(what: int, iters: int = 4096, stream=None) -> float:

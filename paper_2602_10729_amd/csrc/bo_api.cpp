@@ -616,7 +616,7 @@ bo_status bo_argmax(const float* values, int64_t M, int64_t* index, float* value
 }
 
 bo_status bo_measure_peak(int32_t what, int64_t iters, double* rate, void* stream) {
-  if (!rate || what < BO_PEAK_VALU_FMA || what > BO_PEAK_HBM_COPY || iters < 1 || iters > (1 << 24))
+  if (!rate || what < BO_PEAK_VALU_FMA || what > BO_PEAK_MFMA_F16 || iters < 1 || iters > (1 << 24))
     return fail(BO_ERR_INVALID_ARGUMENT, "bo_measure_peak: bad argument");
   hipError_t e = measure_peak(what, iters, rate, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "bo_measure_peak");

@@ -8,6 +8,7 @@
 //   BO_PEAK_MFMA_F32   — independent v_mfma_f32_16x16x4f32 chains (flop/s)
 //   BO_PEAK_HBM_COPY   — float4 streaming copy of a large buffer (bytes/s,
 //                        read + write)
+//   BO_PEAK_MFMA_F16   — independent v_mfma_f32_16x16x32_f16 chains (flop/s)
 // Each runs a fixed amount of work over the whole chip (2048 workgroups of
 // 256 threads) on the given stream and times it with HIP events.
 #include <hip/hip_runtime.h>
@@ -18,6 +19,7 @@ namespace bo {
 namespace {
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef _Float16 halfx8 __attribute__((ext_vector_type(8)));
 constexpr int kGrid = 2048;
 constexpr int kBlock = 256;
 
@@ -71,6 +73,27 @@ __global__ __launch_bounds__(kBlock) void k_mfma(float* out, int iters) {
   if (s == 1.2345f) out[blockIdx.x * kBlock + threadIdx.x] = s;
 }
 
+__global__ __launch_bounds__(kBlock) void k_mfma_f16(float* out, int iters) {
+  floatx4 acc[kChains];
+#pragma unroll
+  for (int i = 0; i < kChains; ++i) acc[i] = floatx4{0.f, 0.f, 0.f, 0.f};
+  halfx8 a, b;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    a[i] = static_cast<_Float16>(static_cast<float>(threadIdx.x) * 1e-3f + i);
+    b[i] = static_cast<_Float16>(1.0f - i * 1e-2f);
+  }
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int i = 0; i < kChains; ++i)
+      acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, acc[i], 0, 0, 0);
+  }
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < kChains; ++i) s += acc[i][0] + acc[i][1] + acc[i][2] + acc[i][3];
+  if (s == 1.2345f) out[blockIdx.x * kBlock + threadIdx.x] = s;
+}
+
 __global__ __launch_bounds__(kBlock) void k_copy(const float4* __restrict__ src,
                                                  float4* __restrict__ dst, int64_t n4) {
   const int64_t stride = (int64_t)gridDim.x * kBlock;
@@ -105,6 +128,10 @@ hipError_t measure_peak(int what, int64_t iters, double* rate, hipStream_t st) {
       case BO_PEAK_MFMA_F32:
         hipLaunchKernelGGL(k_mfma, dim3(kGrid), dim3(kBlock), 0, st, scratch, it);
         work = (double)kGrid * (kBlock / 64) * kChains * 2048.0 * it;
+        break;
+      case BO_PEAK_MFMA_F16:
+        hipLaunchKernelGGL(k_mfma_f16, dim3(kGrid), dim3(kBlock), 0, st, scratch, it);
+        work = (double)kGrid * (kBlock / 64) * kChains * 16384.0 * it;
         break;
       case BO_PEAK_HBM_COPY: {
         const int64_t n4 = copy_bytes / 16;
