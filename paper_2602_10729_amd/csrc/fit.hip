@@ -73,84 +73,97 @@ __global__ __launch_bounds__(256) void k_gram(const float* __restrict__ X, int64
 
 // Factor the symmetric 64x64 block held in LDS `a` (lower triangle read) and
 // invert the factor: on return a = L (zeros above the diagonal) and
-// x = L^{-1}. All 256 threads take part; thread (c = tid % 64, g = tid / 64)
-// keeps rows 16g..16g+15 of column c in registers, indexed only by unrolled
-// constants; g is scalar. The structural masks (row >= column) are 0/1
-// multipliers fixed per thread, so the per-step update has no branches.
-// Factor step j: column j (published by its owners at the end of step j-1,
-// double-buffered) gives the pivot and the scaled column; the owners write
-// column j of L; every column c > j updates its rows; the owners of column
-// j+1 publish it. Inverse step j: row j of X (published the step before) is
-// scaled by 1/L_jj, written to x and applied to the rows below.
+// x = L^{-1}. One wave does the work without barriers (the other waves of the
+// workgroup only wait at the final barrier): lane c keeps column c in 64
+// registers, indexed only by unrolled constants.
+// Factor step j: the pivot is lane j's element j (read with readlane); lane j
+// publishes its (unscaled) column, from row j on, to lcol[j] (contiguous
+// doubles); every lane c > j then subtracts L_cj times column j of L from its
+// own (broadcast LDS reads that all lanes share). Inverse step j: lane c's
+// column of X = L^{-1} is swept the same way, X_j /= L_jj then
+// X_i -= L_ij X_j for i > j, reading L from lcol.
 // A non-positive or non-finite pivot sets *flag and is replaced by 1.
-// Scratch: colj [2*64], rowb [2*64], invd [64].
-__device__ __forceinline__ void chol_inv64(double (*__restrict__ a)[LDP],
-                                           double (*__restrict__ x)[LDP],
-                                           double* __restrict__ colj,
-                                           double* __restrict__ rowb,
-                                           double* __restrict__ invd, int* flag) {
-  const int tid = threadIdx.x;
-  const int c = tid & 63;
-  const int g = __builtin_amdgcn_readfirstlane(tid >> 6);
-  double r[16], mge[16];
+// Scratch: lcol [64][64] doubles, which is the storage of x itself (x is only
+// written after the last read of lcol), 16-byte aligned; invd [64].
+__device__ __forceinline__ double readlane_d(double v, int lane) {
+  const int64_t b = __double_as_longlong(v);
+  const int lo = __builtin_amdgcn_readlane(static_cast<int>(b), lane);
+  const int hi = __builtin_amdgcn_readlane(static_cast<int>(b >> 32), lane);
+  return __longlong_as_double((static_cast<int64_t>(hi) << 32) | static_cast<uint32_t>(lo));
+}
+
+// Makes this wave's LDS stores visible to its own later loads from other
+// lanes: without it the compiler may move those loads above the stores (lanes
+// of one wave are separate threads to the memory model).
+__device__ __forceinline__ void wave_sync_lds() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+__device__ __forceinline__ void chol_inv64_wave(double (*a)[LDP], double (*x)[LDP], double* lcol,
+                                                double* invd, int* flag) {
+  const int c = threadIdx.x & 63;
+  // r holds lane c's column of the partially eliminated matrix, unscaled:
+  // after step c, r[i] (i >= c) = L_ic * L_cc, so no per-element scaling is
+  // ever needed (the scale 1/L_cc is folded into the multipliers below and
+  // applied once at the end).
+  double r[B];
 #pragma unroll
-  for (int k = 0; k < 16; ++k) {
-    r[k] = a[16 * g + k][c];
-    mge[k] = (16 * g + k >= c) ? 1.0 : 0.0;
-  }
-  if (c == 0) {
+  for (int i = 0; i < B; ++i) r[i] = a[i][c];
+  bool bad_any = false;
 #pragma unroll
-    for (int k = 0; k < 16; ++k) colj[16 * g + k] = r[k];
-  }
   for (int j = 0; j < B; ++j) {
-    __syncthreads();
-    const double* cj = colj + (j & 1) * B;
-    double piv = cj[j];
+    double piv = readlane_d(r[j], j);
     const bool bad = !(piv > 0.0) || !isfinite(piv);
     if (bad) piv = 1.0;
-    const double d = sqrt(piv);
-    const double inv = 1.0 / d;
+    bad_any |= bad;
+    const double inv = 1.0 / sqrt(piv);
+    double* lc = lcol + j * B;
     if (c == j) {
+      // plain double stores (merged into 16-byte ones): the same type as the
+      // loads below, so alias analysis cannot move those above these
 #pragma unroll
-      for (int k = 0; k < 16; ++k) {
-        const int i = 16 * g + k;
-        a[i][j] = (i > j) ? r[k] * inv : ((i == j) ? d : 0.0);
-      }
-      if (g == 0) {
-        invd[j] = inv;
-        if (bad) atomicOr(flag, 1);
-      }
+      for (int i = (j + 1) & ~1; i < B; ++i) lc[i] = r[i];
+      invd[j] = inv;
     }
-    double cv[16];
+    wave_sync_lds();
+    if (j + 1 < B) {
+      // L_ij L_cj = lc[i] * lc[c] / piv for the columns c > j still open
+      const double m = (c > j) ? lc[c] * (inv * inv) : 0.0;
 #pragma unroll
-    for (int k = 0; k < 16; ++k) cv[k] = cj[16 * g + k];
-    const double lcj = (c > j) ? cj[c] * inv * inv : 0.0;   // l_cj / d folded in
-#pragma unroll
-    for (int k = 0; k < 16; ++k) r[k] = fma(-cv[k] * mge[k], lcj, r[k]);
-    if (c == j + 1) {
-      double* cn = colj + ((j + 1) & 1) * B;
-#pragma unroll
-      for (int k = 0; k < 16; ++k) cn[16 * g + k] = r[k];
+      for (int i = j + 1; i < B; ++i) r[i] = fma(-lc[i], m, r[i]);
     }
   }
-  // inverse: X = I; step j: X_j <- X_j / L_jj (final), X_i -= L_ij X_j (i > j)
+  if (bad_any && c == 0) atomicOr(flag, 1);
+  wave_sync_lds();
+  // L into a (zeros above the diagonal): column c scaled by 1/L_cc
+  const double ic = invd[c];
 #pragma unroll
-  for (int k = 0; k < 16; ++k) r[k] = (16 * g + k == c) ? 1.0 : 0.0;
-  if (g == 0) rowb[c] = r[0];               // row 0 of X before scaling
+  for (int i = 0; i < B; ++i) a[i][c] = (i >= c) ? r[i] * ic : 0.0;
+  // inverse, column c of X per lane: X_j /= L_jj, X_i -= L_ij X_j (i > j),
+  // with L_ij = lc[i] / L_jj
+  double xv[B];
+#pragma unroll
+  for (int i = 0; i < B; ++i) xv[i] = (i == c) ? 1.0 : 0.0;
+#pragma unroll
   for (int j = 0; j < B; ++j) {
-    __syncthreads();
-    const double xj = rowb[(j & 1) * B + c] * invd[j];
-    if (g == (j >> 4)) x[j][c] = xj;
-    double av[16];
+    const double ij = invd[j];
+    const double xj = xv[j] * ij;
+    xv[j] = xj;
+    const double* lc = lcol + j * B;
+    const double m = xj * ij;
 #pragma unroll
-    for (int k = 0; k < 16; ++k) av[k] = a[16 * g + k][j];
-#pragma unroll
-    for (int k = 0; k < 16; ++k)
-      if (16 * g + k > j) r[k] = fma(-av[k], xj, r[k]);
-#pragma unroll
-    for (int k = 0; k < 16; ++k)
-      if (16 * g + k == j + 1) rowb[((j + 1) & 1) * B + c] = r[k];
+    for (int i = j + 1; i < B; ++i) xv[i] = fma(-lc[i], m, xv[i]);
   }
+#pragma unroll
+  for (int i = 0; i < B; ++i) x[i][c] = xv[i];
+}
+
+// All threads call this; wave 0 factors and inverts (see above).
+__device__ __forceinline__ void chol_inv64(double (*a)[LDP], double (*x)[LDP], double* invd,
+                                           int* flag) {
+  if (threadIdx.x < 64) chol_inv64_wave(a, x, &x[0][0], invd, flag);
   __syncthreads();
 }
 
@@ -173,13 +186,13 @@ __global__ __launch_bounds__(256) void k_factor_first(double* __restrict__ A,
                                                       double* __restrict__ W, int nf,
                                                       int* __restrict__ flag) {
   __shared__ double a[B][LDP];
-  __shared__ double x[B][LDP];
-  __shared__ double colj[2 * B], rowb[2 * B], invd[B];
+  __shared__ __align__(16) double x[B][LDP];
+  __shared__ double invd[B];
   double* Ak = A + (int64_t)blockIdx.x * nf * nf;
   double* Wk = W + (int64_t)blockIdx.x * nf * nf;
   load_block(a, Ak, nf);
   __syncthreads();
-  chol_inv64(a, x, colj, rowb, invd, flag);
+  chol_inv64(a, x, invd, flag);
   store_block(Ak, nf, a);
   store_block(Wk, nf, x);
 }
@@ -246,8 +259,8 @@ __global__ __launch_bounds__(256) void k_panel(double* __restrict__ A, double* _
 __global__ __launch_bounds__(256) void k_update(double* __restrict__ A, double* __restrict__ W,
                                                 int nf, int kb, int* __restrict__ flag) {
   __shared__ double p[B][LDP];
-  __shared__ double q[B][LDP];
-  __shared__ double colj[2 * B], rowb[2 * B], invd[B];
+  __shared__ __align__(16) double q[B][LDP];
+  __shared__ double invd[B];
   const int k = blockIdx.y;
   const int nbk = nf / B;
   const int T = nbk - kb - 1;
@@ -299,7 +312,7 @@ __global__ __launch_bounds__(256) void k_update(double* __restrict__ A, double* 
 #pragma unroll
       for (int c = 0; c < 4; ++c) p[ty * 4 + rr][tx * 4 + c] = acc[rr][c];
     __syncthreads();
-    chol_inv64(p, q, colj, rowb, invd, flag);
+    chol_inv64(p, q, invd, flag);
     const int o1 = o + B;
     store_block(dst, nf, p);
     store_block(Wk + (int64_t)o1 * nf + o1, nf, q);
