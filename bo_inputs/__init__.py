@@ -36,6 +36,12 @@ standard deviation in fp64, as the outcome transform "Standardize" of the
 paper's implementation section does, and rounded to fp32. The reference point
 is the per-objective minimum of the standardised fp32 Y minus 0.1.
 
+Feasibility thresholds (for the constrained acquisition): per objective the
+given quantile (default 0.3) of the standardised fp32 Y, in fp64, rounded to
+fp32 — a latency cap and a quality floor that 70% of the observations meet
+on each objective. ``None`` in place of a quantile leaves that objective
+unconstrained (-inf).
+
 Random streams: ``numpy.random.Generator(PCG64(SeedSequence(seed,
 spawn_key=(family, stream))))`` with streams 0 X, 1 candidates, 2 noise,
 3 lengthscales, 4 weights w, 5 base samples Z; family is the config number
@@ -49,7 +55,8 @@ from typing import Optional
 
 import numpy as np
 
-__all__ = ["CONFIGS", "Workload", "make_config", "near_data_candidates"]
+__all__ = ["CONFIGS", "Workload", "make_config", "near_data_candidates",
+           "feasibility_thresholds"]
 
 # (m, q, d, n, M, S, noise_sd, family)
 CONFIGS = {
@@ -180,3 +187,15 @@ def near_data_candidates(wl: Workload, count: int, scale: float = 0.01,
     pts = wl.X.astype(np.float64)[idx] + scale * rng.standard_normal((count * wl.q, wl.d))
     pts = np.clip(pts, 0.0, 1.0)
     return pts.astype(np.float32).reshape(count, wl.q, wl.d)
+
+
+def feasibility_thresholds(wl: Workload, quantiles=0.3) -> np.ndarray:
+    """Lower bounds [m] on the standardised objectives for the constrained
+    acquisition: the per-objective quantile of the observed Y (fp32).
+    ``quantiles`` is one value or one per objective (None: unconstrained)."""
+    qs = [quantiles] * wl.m if np.isscalar(quantiles) or quantiles is None else list(quantiles)
+    Y = wl.Y.astype(np.float64)
+    out = np.empty(wl.m)
+    for k, qk in enumerate(qs):
+        out[k] = -np.inf if qk is None else np.quantile(Y[:, k], qk)
+    return out.astype(np.float32)

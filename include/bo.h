@@ -100,8 +100,9 @@ bo_status bo_fit(const float* X, const float* Y, int64_t n, int32_t d, int32_t m
  * bo_score — posterior plus Monte-Carlo (q)EHVI for M candidates.
  *
  * Paper: "Constrained qNEHVI" paragraph (expected HVI over samples of the
- * joint posterior, Monte-Carlo integration) without the feasibility factor,
- * against the fixed front of the observations.
+ * joint posterior, Monte-Carlo integration) without the feasibility factor
+ * (bo_score_constrained adds it), against the fixed front of the
+ * observations.
  *
  * Per candidate batch b (q points x_1..x_q) and objective k:
  *   mu_a = k(x_a, X) alpha_k;  v_a = L_k^{-1} k(X, x_a);
@@ -133,6 +134,33 @@ bo_status bo_fit(const float* X, const float* Y, int64_t n, int32_t d, int32_t m
 bo_status bo_score(bo_model model, const float* cand, int64_t M, int32_t q,
                    const float* ref_point, const float* base_samples, int32_t S,
                    float* ehvi, float* mu, float* sigma, void* stream);
+
+/*
+ * bo_score_constrained — bo_score with the feasibility factor.
+ *
+ * Paper: "Constrained qNEHVI" paragraph. The constraints bound the
+ * objectives themselves (a latency cap L <= L_max, a quality floor
+ * Q >= Q_min, written g_i <= 0), and the acquisition is the expectation of
+ * HVI times the indicator that every constraint holds, over the same joint
+ * posterior samples. On the maximised, standardised objectives each
+ * constraint reads y_k >= feas_lower[k]:
+ *   q = 1: ehvi[b] = 1/S sum_s HVI(y_s) * prod_k 1[y_s[k] >= feas_lower[k]]
+ *   q > 1: a batch member counts only on the samples where it is feasible:
+ *          each inclusion-exclusion term of a member subset J is multiplied
+ *          by the product of its members' indicators (= the HVI of the
+ *          feasible members).
+ * A sample exactly on a threshold is feasible.
+ *
+ * feas_lower host [m]: per-objective lower bound in standardised units;
+ *            -inf leaves that objective unconstrained, +inf makes every
+ *            sample infeasible (ehvi = 0); NULL is exactly bo_score.
+ * Other arguments, ownership and errors as bo_score; NONFINITE_INPUT also
+ * for a NaN threshold.
+ */
+bo_status bo_score_constrained(bo_model model, const float* cand, int64_t M, int32_t q,
+                               const float* ref_point, const float* feas_lower,
+                               const float* base_samples, int32_t S, float* ehvi,
+                               float* mu, float* sigma, void* stream);
 
 /*
  * bo_argmax — first index of the maximum of values[0..M).

@@ -18,7 +18,9 @@ workflow, the constrained qNEHVI paragraph, and the implementation section
                 decomposition of the region a new point can improve.
 * ``acq``     — hypervolume improvement of one point or of a q-batch
                 (inclusion-exclusion), Monte-Carlo EHVI / qEHVI with given
-                base samples, and the argmax over candidates.
+                base samples, optionally weighted by the feasibility
+                indicator of the constrained form, and the argmax over
+                candidates.
 
 All arithmetic is fp64 on fp32-rounded inputs. Readings of points the paper
 leaves open are listed in each function's docstring.
@@ -26,11 +28,11 @@ leaves open are listed in each function's docstring.
 from .gp import (GPModel, matern52, scaled_distance, fit, posterior,
                  chol_psd, NotPositiveDefinite)
 from .pareto import nondominated, pareto_front, boxes_2d, boxes_3d, box_decomposition
-from .acq import hvi, qhvi, ehvi_q1, qehvi, score, argmax
+from .acq import hvi, qhvi, feasible, ehvi_q1, qehvi, score, argmax
 
 __all__ = [
     "GPModel", "matern52", "scaled_distance", "fit", "posterior", "chol_psd",
     "NotPositiveDefinite", "nondominated", "pareto_front", "boxes_2d",
-    "boxes_3d", "box_decomposition", "hvi", "qhvi", "ehvi_q1", "qehvi",
+    "boxes_3d", "box_decomposition", "hvi", "qhvi", "feasible", "ehvi_q1", "qehvi",
     "score", "argmax",
 ]

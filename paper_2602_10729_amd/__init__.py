@@ -6,7 +6,8 @@ current stream. There is no CPU fallback: if the library is missing or a
 tensor is not on the GPU, the call raises.
 
 Functions mirror the C ABI in ``include/bo.h``:
-``fit``, ``score``, ``argmax``, ``cholesky_test`` (device) and
+``fit``, ``score`` (``bo_score``, or ``bo_score_constrained`` when feasibility
+thresholds are given), ``argmax``, ``cholesky_test`` (device) and
 ``pareto_front``, ``box_decomposition`` (host geometry, no GPU needed).
 """
 from __future__ import annotations
@@ -58,6 +59,8 @@ def lib() -> ctypes.CDLL:
     L.bo_fit.restype = ctypes.c_int
     L.bo_score.argtypes = [vp, vp, i64, i32, fp, vp, i32, vp, vp, vp, vp]
     L.bo_score.restype = ctypes.c_int
+    L.bo_score_constrained.argtypes = [vp, vp, i64, i32, fp, fp, vp, i32, vp, vp, vp, vp]
+    L.bo_score_constrained.restype = ctypes.c_int
     L.bo_argmax.argtypes = [vp, i64, vp, vp, vp]
     L.bo_argmax.restype = ctypes.c_int
     L.bo_model_front_size.argtypes = [vp]
@@ -167,11 +170,13 @@ def fit(X, Y, lengthscale, outputscale, noise, stream=None) -> Model:
     return Model(h.value, n, d, m)
 
 
-def score(model: Model, cand, ref, Z, ehvi=None, mu=None, sigma=None, stream=None):
+def score(model: Model, cand, ref, Z, ehvi=None, mu=None, sigma=None, stream=None,
+          lower=None):
     """bo_score: cand [M, q, d], Z [S, q, m] fp32 GPU tensors; ref host [m].
 
     Returns the ehvi tensor [M] (allocated if not given). mu/sigma
-    [M, q, m] are written only when passed.
+    [M, q, m] are written only when passed. ``lower`` (host [m], optional)
+    selects bo_score_constrained with these feasibility thresholds.
     """
     import torch
     M, q, d = cand.shape
@@ -181,10 +186,17 @@ def score(model: Model, cand, ref, Z, ehvi=None, mu=None, sigma=None, stream=Non
         ehvi = torch.empty(M, dtype=torch.float32, device=cand.device)
     mu_p = _dev(mu, "mu", torch.float32) if mu is not None else ctypes.c_void_p(0)
     sg_p = _dev(sigma, "sigma", torch.float32) if sigma is not None else ctypes.c_void_p(0)
-    st = lib().bo_score(model.handle, _dev(cand, "cand", torch.float32), M, q,
-                        r.ctypes.data_as(ctypes.c_void_p), _dev(Z, "Z", torch.float32), S,
-                        _dev(ehvi, "ehvi", torch.float32), mu_p, sg_p, _stream(stream))
-    _check(st, "bo_score")
+    args = (_dev(cand, "cand", torch.float32), M, q, r.ctypes.data_as(ctypes.c_void_p))
+    tail = (_dev(Z, "Z", torch.float32), S, _dev(ehvi, "ehvi", torch.float32), mu_p, sg_p,
+            _stream(stream))
+    if lower is None:
+        st = lib().bo_score(model.handle, *args, *tail)
+        _check(st, "bo_score")
+    else:
+        lw = _host_f32(lower, (model.m,), "lower")
+        st = lib().bo_score_constrained(model.handle, *args, lw.ctypes.data_as(ctypes.c_void_p),
+                                        *tail)
+        _check(st, "bo_score_constrained")
     return ehvi
 
 

@@ -3,7 +3,8 @@
 // bo_fit      — Gram (fp64) -> blocked Cholesky -> L^{-1} -> alpha -> pack,
 //               all on the caller's stream, then one synchronisation to read
 //               the positive-definiteness flag back.
-// bo_score    — per objective one posterior launch, then one (q)EHVI launch;
+// bo_score    — per objective one posterior launch, then one (q)EHVI launch
+//               (bo_score_constrained: the same with feasibility weights);
 //               asynchronous. The box decomposition is rebuilt on the host
 //               only when the reference point changes.
 // bo_argmax   — three tiny launches using the caller's index cell.
@@ -411,6 +412,14 @@ void bo_free(bo_model model) {
 bo_status bo_score(bo_model model, const float* cand, int64_t M_, int32_t q,
                    const float* ref_point, const float* base_samples, int32_t S,
                    float* ehvi, float* mu, float* sigma, void* stream) {
+  return bo_score_constrained(model, cand, M_, q, ref_point, nullptr, base_samples, S, ehvi,
+                              mu, sigma, stream);
+}
+
+bo_status bo_score_constrained(bo_model model, const float* cand, int64_t M_, int32_t q,
+                               const float* ref_point, const float* feas_lower,
+                               const float* base_samples, int32_t S, float* ehvi, float* mu,
+                               float* sigma, void* stream) {
   if (!model) return fail(BO_ERR_INVALID_ARGUMENT, "bo_score: model is NULL");
   Model& M = model->m;
   if (M_ < 0) return fail(BO_ERR_INVALID_ARGUMENT, "bo_score: M < 0");
@@ -420,6 +429,11 @@ bo_status bo_score(bo_model model, const float* cand, int64_t M_, int32_t q,
   if (!ref_point) return fail(BO_ERR_INVALID_ARGUMENT, "bo_score: ref_point is NULL");
   if (!all_finite(ref_point, M.m)) return fail(BO_ERR_NONFINITE_INPUT, "bo_score: ref_point not finite");
   if (M_ > (int64_t)1 << 40) return fail(BO_ERR_CAPACITY, "bo_score: M too large");
+  if (feas_lower) {
+    for (int k = 0; k < M.m; ++k)
+      if (std::isnan(feas_lower[k]))
+        return fail(BO_ERR_NONFINITE_INPUT, "bo_score: feasibility threshold is NaN");
+  }
   DeviceGuard g(M.device);
   if (!g.ok) return fail(BO_ERR_DEVICE, "bo_score: cannot select the model's device");
   hipStream_t st = static_cast<hipStream_t>(stream);
@@ -552,6 +566,9 @@ bo_status bo_score(bo_model model, const float* cand, int64_t M_, int32_t q,
   ea.mu = mu_buf; ea.sd = sd_buf; ea.chol = chol_buf;
   ea.Z = base_samples; ea.boxes = M.d_boxes;
   ea.nbat = M_; ea.q = q; ea.m = m; ea.S = S; ea.nbox = M.nbox;
+  ea.constrained = feas_lower != nullptr;
+  for (int k = 0; k < 3; ++k)
+    ea.lower[k] = (feas_lower && k < m) ? feas_lower[k] : -INFINITY;
   ea.ehvi = ehvi;
   if ((s = after_launch(launch_ehvi(ea, st), st, "ehvi")) != BO_OK) return s;
   if (rec) {

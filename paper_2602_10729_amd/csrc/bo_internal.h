@@ -121,6 +121,8 @@ struct EhviArgs {
   const float* boxes;  // [nbox][2m] lo then width
   int64_t nbat;
   int q, m, S, nbox;
+  bool constrained;    // weight samples by feasibility (y_k >= lower[k] for all k)
+  float lower[3];      // feasibility thresholds (-inf: objective unconstrained)
   float* ehvi;         // [nbat]
 };
 hipError_t launch_ehvi(const EhviArgs& a, hipStream_t st);

@@ -2,11 +2,19 @@
 //
 // Paper: "Constrained qNEHVI" paragraph — the acquisition is the expected
 // hypervolume improvement over samples of the joint posterior, estimated by
-// Monte-Carlo integration (without the feasibility factor here). With the
-// region the front does not dominate split into disjoint boxes [lo, lo + w):
+// Monte-Carlo integration, optionally restricted to feasible samples. With
+// the region the front does not dominate split into disjoint boxes
+// [lo, lo + w):
 //   HVI(y)  = sum_c prod_k clamp(y_k - lo_ck, 0, w_ck)
 //   qHVI(Y) = sum_{J != {}} (-1)^{|J|+1} sum_c prod_k min_{a in J} clamp(y_ak - lo_ck, 0, w_ck)
 // (the clamp is monotone, so the minimum over batch members commutes with it).
+//
+// Feasibility (the constrained form): the constraints bound the objectives
+// themselves, y_k >= t_k on the maximised objectives, and a sample (a batch
+// member) counts only where all of them hold. An infeasible member's first
+// objective is replaced by -inf: every clamp of it is then 0, so each box
+// product, and each subset term that contains the member, vanishes — the
+// same as multiplying those terms by the member's indicator.
 //
 // Mapping: one lane per candidate batch; the S base samples and the boxes
 // are the same for every lane, so they sit in LDS and every read is a
@@ -27,7 +35,16 @@ __device__ inline float clamp_ext(float y, float lo, float w) {
   return __builtin_amdgcn_fmed3f(y - lo, 0.0f, w);
 }
 
-template <int MO, int SC>
+// Member feasibility: all objectives at or above their thresholds.
+template <int MO>
+__device__ __forceinline__ float mask_infeasible(const float (&y)[MO], const EhviArgs& a) {
+  bool ok = true;
+#pragma unroll
+  for (int k = 0; k < MO; ++k) ok = ok && (y[k] >= a.lower[k]);
+  return ok ? y[0] : -__builtin_inff();
+}
+
+template <int MO, int SC, bool CONS>
 __global__ __launch_bounds__(kThreads) void k_ehvi_q1(EhviArgs a) {
   extern __shared__ float sm[];
   float* zs = sm;                                   // [S][MO]
@@ -55,6 +72,10 @@ __global__ __launch_bounds__(kThreads) void k_ehvi_q1(EhviArgs a) {
         // samples past S get -inf: every extent clamps to 0
         y[j][k] = (s < a.S) ? fmaf(sd[k], zs[sl * MO + k], mu[k]) : -__builtin_inff();
       }
+    if constexpr (CONS) {
+#pragma unroll
+      for (int j = 0; j < SC; ++j) y[j][0] = mask_infeasible<MO>(y[j], a);
+    }
     for (int c = 0; c < a.nbox; ++c) {
       float lo[MO], w[MO];
 #pragma unroll
@@ -77,7 +98,7 @@ __global__ __launch_bounds__(kThreads) void k_ehvi_q1(EhviArgs a) {
 // q-batch version: lane owns a batch of Q points; y_s[a][k] is sampled with
 // the lower factor of objective k, then the 2^Q - 1 member subsets are
 // expanded by inclusion-exclusion per box.
-template <int MO, int Q, int SC>
+template <int MO, int Q, int SC, bool CONS>
 __global__ __launch_bounds__(kThreads) void k_ehvi_q(EhviArgs a) {
   extern __shared__ float sm[];
   constexpr int T = Q * (Q + 1) / 2;
@@ -116,6 +137,10 @@ __global__ __launch_bounds__(kThreads) void k_ehvi_q(EhviArgs a) {
           for (int t = 0; t <= i; ++t) v = fmaf(C[k][i * (i + 1) / 2 + t], zs[(sl * Q + t) * MO + k], v);
           y[j][i][k] = (s < a.S) ? v : -__builtin_inff();
         }
+      if constexpr (CONS) {
+#pragma unroll
+        for (int i = 0; i < Q; ++i) y[j][i][0] = mask_infeasible<MO>(y[j][i], a);
+      }
     }
     for (int c = 0; c < a.nbox; ++c) {
       float lo[MO], w[MO];
@@ -150,24 +175,41 @@ __global__ __launch_bounds__(kThreads) void k_ehvi_q(EhviArgs a) {
   if (valid) a.ehvi[b] = (acc_pos - acc_neg) / static_cast<float>(a.S);
 }
 
-template <int MO>
+template <int MO, bool CONS>
 hipError_t launch_mo(const EhviArgs& a, hipStream_t st) {
   const unsigned grid = static_cast<unsigned>((a.nbat + kThreads - 1) / kThreads);
   const size_t lds = sizeof(float) * ((size_t)a.S * a.q * MO + (size_t)a.nbox * 2 * MO);
   switch (a.q) {
     case 1:
-      hipLaunchKernelGGL((k_ehvi_q1<MO, 16>), dim3(grid), dim3(kThreads), lds, st, a);
+      hipLaunchKernelGGL((k_ehvi_q1<MO, 16, CONS>), dim3(grid), dim3(kThreads), lds, st, a);
       break;
     case 2:
-      hipLaunchKernelGGL((k_ehvi_q<MO, 2, 4>), dim3(grid), dim3(kThreads), lds, st, a);
+      hipLaunchKernelGGL((k_ehvi_q<MO, 2, 4, CONS>), dim3(grid), dim3(kThreads), lds, st, a);
       break;
     case 4:
-      hipLaunchKernelGGL((k_ehvi_q<MO, 4, 2>), dim3(grid), dim3(kThreads), lds, st, a);
+      hipLaunchKernelGGL((k_ehvi_q<MO, 4, 2, CONS>), dim3(grid), dim3(kThreads), lds, st, a);
       break;
     default:
       return hipErrorInvalidValue;
   }
   return hipGetLastError();
+}
+
+template <bool CONS>
+hipError_t set_lds_limit() {
+  const void* fns[] = {
+      reinterpret_cast<const void*>(&k_ehvi_q1<2, 16, CONS>),
+      reinterpret_cast<const void*>(&k_ehvi_q1<3, 16, CONS>),
+      reinterpret_cast<const void*>(&k_ehvi_q<2, 2, 4, CONS>),
+      reinterpret_cast<const void*>(&k_ehvi_q<3, 2, 4, CONS>),
+      reinterpret_cast<const void*>(&k_ehvi_q<2, 4, 2, CONS>),
+      reinterpret_cast<const void*>(&k_ehvi_q<3, 4, 2, CONS>)};
+  for (const void* f : fns) {
+    hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       160 * 1024);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 }  // namespace
@@ -180,22 +222,13 @@ hipError_t launch_ehvi(const EhviArgs& a, hipStream_t st) {
   if (a.nbat <= 0) return hipSuccess;
   static bool attr_set = false;
   if (!attr_set) {
-    const void* fns[] = {
-        reinterpret_cast<const void*>(&k_ehvi_q1<2, 16>),
-        reinterpret_cast<const void*>(&k_ehvi_q1<3, 16>),
-        reinterpret_cast<const void*>(&k_ehvi_q<2, 2, 4>),
-        reinterpret_cast<const void*>(&k_ehvi_q<3, 2, 4>),
-        reinterpret_cast<const void*>(&k_ehvi_q<2, 4, 2>),
-        reinterpret_cast<const void*>(&k_ehvi_q<3, 4, 2>)};
-    for (const void* f : fns) {
-      hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                         160 * 1024);
-      if (e != hipSuccess) return e;
-    }
+    hipError_t e = set_lds_limit<false>();
+    if (e == hipSuccess) e = set_lds_limit<true>();
+    if (e != hipSuccess) return e;
     attr_set = true;
   }
-  if (a.m == 2) return launch_mo<2>(a, st);
-  if (a.m == 3) return launch_mo<3>(a, st);
+  if (a.m == 2) return a.constrained ? launch_mo<2, true>(a, st) : launch_mo<2, false>(a, st);
+  if (a.m == 3) return a.constrained ? launch_mo<3, true>(a, st) : launch_mo<3, false>(a, st);
   return hipErrorInvalidValue;
 }
 

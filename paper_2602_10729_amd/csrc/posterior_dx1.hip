@@ -1,0 +1,8 @@
+// Posterior kernel instantiations for coordinate width 4 (padded d <= 4).
+#include "posterior_kernel.h"
+
+namespace bo {
+hipError_t launch_posterior_dx1(const PosteriorArgs& a, hipStream_t st) {
+  return launch_for_dx<1>(a, st);
+}
+}  // namespace bo

@@ -1,0 +1,670 @@
+// Posterior kernel templates, included by the per-coordinate-width
+// translation units posterior_dx<N>.hip (each instantiates one width, so
+// the build compiles them in parallel) and by posterior.hip (shared helpers).
+//
+#pragma once
+// GP posterior of a batch of candidate points, one objective per launch.
+//
+// Paper: workflow step (ii) evaluates the acquisition on samples of the
+// joint posterior of the GP surrogates; the posterior of an exact GP at x*
+// is mu = k*^T alpha and Sigma = k(x*,x*) - v^T v with v = L^{-1} k*.
+//
+// Arithmetic. V = L^{-1} K*^T runs on the fp16 matrix cores with each
+// operand split into two fp16 halves, x = x_hi + x_lo (x_hi = fp16(x),
+// x_lo = fp16(x - x_hi)), and three products per pair,
+//   a b ~ a_hi b_hi + a_hi b_lo + a_lo b_hi,
+// accumulated in fp32 by the MFMA. The operands carry ~22 significant bits
+// and the dropped a_lo b_lo term is 2^-22 relative, so the result is within
+// a small factor of an fp32 product. On gfx950 this is the fast path: the
+// dense fp16 MFMA runs at 16x the fp32 MFMA rate, and (unlike fp32 MFMA) it
+// executes alongside VALU work, which hides the kernel evaluations below.
+// L^{-1} is split and packed once by the fit; K*^T is split as it is made.
+//
+// One workgroup (8 waves, two per SIMD) owns a tile of NT points and forms V
+// left-looking: the outer loop runs over 32-row blocks J of K*^T (the MFMA
+// k), and every wave adds L^{-1}[I][J] K*^T[J] into the accumulators of the
+// 16-row blocks I >= 2J that it owns. Row block I of V stays in the MFMA
+// accumulators until it is complete; then only its squared column sums
+// (q = 1: |v|^2; q > 1 also the cross products of batch members, which sit
+// in the same 4-lane group and are exchanged with DPP quad permutes) are
+// kept.
+//
+// K*^T is produced two blocks ahead of its use into an LDS ring of 16
+// blocks (512 rows) of fp16 hi/lo planes, from training rows staged through
+// LDS two blocks ahead of that. While the matrix cores work on block J, the
+// waves evaluate the ARD Matern-5/2 values of block J + 2 on the vector ALUs
+// (direct differences of lengthscale-scaled coordinates, no
+// |a|^2 + |b|^2 - 2ab cancellation) and accumulate mu = K* alpha in fp32.
+// A pass that starts while the ring still holds blocks 0.. reuses them, so
+// for n <= 1024 every kernel value is evaluated once.
+// The kernel evaluations and the MFMAs of a step are independent and are
+// interleaved, so each SIMD's matrix core and vector ALU stay busy together.
+// One barrier per step publishes the produced block and the staged rows.
+//
+// Each wave owns RB row-block slots, slot r holding row block
+// base + 8r + (r even ? wave : 7 - wave); this snake keeps the per-SIMD
+// share of the lower triangle even at every step of J. Row blocks past the
+// matrix (and finished slots) read a zero block appended to the packed
+// L^{-1}, so every load is unconditional and in bounds. Rows beyond 128 RB
+// are handled in further passes, K*^T being produced again for each pass
+// (RB = 4: two passes for n = 1024; the accumulators of more rows would not
+// fit the register file next to the operands).
+//
+// Fragments of v_mfma_f32_16x16x32_f16: A[i][k] from lane i + 16(k/8),
+// element k%8; B[k][j] from lane j + 16(k/8), element k%8; D[i][j] in lane
+// j + 16(i/4), element i%4. Only the pairing of A's and B's k matters, and
+// both sides use this one.
+#include <hip/hip_runtime.h>
+
+#include "bo_internal.h"
+
+namespace bo {
+namespace {
+
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef _Float16 halfx8 __attribute__((ext_vector_type(8)));
+
+#ifndef BO_POST_NT
+#define BO_POST_NT 64        // points per tile
+#endif
+#ifndef BO_POST_RB
+#define BO_POST_RB 4         // row-block slots per wave (rows per pass / 128)
+#endif
+constexpr int kWaves = 8;
+constexpr int kThreads = 64 * kWaves;
+constexpr int kJ = 32;                      // rows of K*^T per step (MFMA k)
+constexpr int kRing = 16;                   // K*^T blocks held in LDS
+constexpr int kCSH = kRing * kJ + 8;        // ring column stride in halves (260 dwords)
+
+__device__ __forceinline__ float matern52_f(float r2, float s) {
+  const float r = __builtin_amdgcn_sqrtf(r2);
+  // exp(-sqrt5 r) = 2^(-sqrt5 log2(e) r)
+  constexpr float kNegSqrt5Log2e = static_cast<float>(-2.23606797749978969641 * 1.44269504088896340736);
+  const float e = __builtin_amdgcn_exp2f(kNegSqrt5Log2e * r);
+  const float poly = fmaf(r, 2.23606798f, fmaf(r2, 1.66666667f, 1.0f));
+  return s * poly * e;
+}
+
+__device__ __forceinline__ float quad_xor(float v, int x) {
+  // DPP quad_perm: lane i of each group of 4 reads lane i ^ x.
+  int iv = __float_as_int(v);
+  int r;
+  if (x == 1) r = __builtin_amdgcn_mov_dpp(iv, 0xB1, 0xF, 0xF, false);      // [1,0,3,2]
+  else if (x == 2) r = __builtin_amdgcn_mov_dpp(iv, 0x4E, 0xF, 0xF, false); // [2,3,0,1]
+  else r = __builtin_amdgcn_mov_dpp(iv, 0x1B, 0xF, 0xF, false);             // [3,2,1,0]
+  return __int_as_float(r);
+}
+
+// LDS-only barrier: waits for this wave's LDS traffic, not for its global
+// loads in flight (the fragment prefetches), then joins the workgroup.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// Raw buffer resource over `bytes` bytes at p: loads take a 32-bit lane
+// offset plus a uniform offset, and read zero past the end.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, bytes, 0x00020000);
+}
+
+__device__ __forceinline__ float4 load4(__amdgpu_buffer_rsrc_t rs, int voff, int soff) {
+  return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rs, voff, soff, 0));
+}
+
+// Index of packed block (I, 0): row block I holds I/2 + 1 blocks of 32
+// columns, so rows 0..I-1 hold t(t+1) (I = 2t) or (t+1)^2 (I = 2t+1).
+__host__ __device__ __forceinline__ int frag_row_start(int I) {
+  const int t = I >> 1;
+  return (I & 1) ? (t + 1) * (t + 1) : t * (t + 1);
+}
+
+// Per-lane state of the K*^T producer. A wave makes NT/8 columns of each
+// 32-row block; lane l takes column l % CPW and RPL = CPW/2 consecutive rows.
+template <int NT, int DX4>
+struct Producer {
+  static constexpr int CPW = NT / kWaves;
+  static constexpr int RPL = kJ * CPW / 64;
+  float c[DX4 * 4];         // scaled candidate coordinates
+  bool valid;
+  float mu;
+  int col;                  // tile column of this lane
+  int row0;                 // first row of this lane inside a block
+};
+
+// Training rows staged in LDS, one 32-row block per slot, four slots: row
+// r of block b at slot b % 4, [kJ][dx + 4] floats per slot, the last float4
+// of a row holding (alpha, 0, 0, 0). Step J loads the rows of block J + 4
+// first and stores them last, while the producer reads block J + 2. Every
+// thread issues the same loads (a spare thread's store goes to a scratch
+// float4), so no branch makes the compiler drain the loads in flight.
+template <int DX4>
+struct Stager {
+  static constexpr int RS = DX4 * 4 + 4;                 // row stride (floats)
+  static constexpr int kF4 = kJ * (DX4 + 1);             // float4s per block
+  static constexpr int kSlot = kJ * RS;                  // floats per slot
+  static_assert(kF4 <= kThreads, "one float4 per thread");
+  float4 x;                 // the loads in flight (selected at the store,
+  float al;                 // so the loads are not waited for early)
+  int soff;                 // this thread's float offset inside a slot (or the scratch)
+  int row, t4;
+  __amdgpu_buffer_rsrc_t xs_rs, al_rs;
+};
+
+// Rows past n_pad read zeros (buffer range check), so blocks past the matrix
+// that the producer may evaluate carry zero alpha and add nothing to mu.
+template <int DX4>
+__device__ __forceinline__ void stage_load(Stager<DX4>& S, const PosteriorArgs& a, int jb) {
+  const int row = jb * kJ + S.row;
+  S.x = load4(S.xs_rs, (row * a.dx + 4 * min(S.t4, DX4 - 1)) * 4, 0);
+  S.al = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(S.al_rs, row * 4, 0, 0));
+}
+
+template <int DX4>
+__device__ __forceinline__ void stage_store(const Stager<DX4>& S, float* xst, int jb) {
+  const bool is_al = S.t4 == DX4;
+  const float4 v{is_al ? S.al : S.x.x, is_al ? 0.f : S.x.y, is_al ? 0.f : S.x.z,
+                 is_al ? 0.f : S.x.w};
+  *reinterpret_cast<float4*>(xst + (jb & 3) * Stager<DX4>::kSlot + S.soff) = v;
+}
+
+// Evaluate this lane's rows of block jb into the ring as fp16 hi/lo planes,
+// reading the training rows from jb's staging slot.
+template <int NT, int DX4>
+__device__ __forceinline__ void produce(Producer<NT, DX4>& P, const PosteriorArgs& a, int jb,
+                                        const float* xst, _Float16* ring) {
+  constexpr int RPL = Producer<NT, DX4>::RPL;
+  constexpr int RS = Stager<DX4>::RS;
+  typedef _Float16 halfr __attribute__((ext_vector_type(RPL)));
+  halfr hi, lo;
+  const float* xr = xst + (jb & 3) * Stager<DX4>::kSlot + P.row0 * RS;
+#pragma unroll
+  for (int u = 0; u < RPL; ++u) {
+    const int row = jb * kJ + P.row0 + u;
+    float r2 = 0.f;
+#pragma unroll
+    for (int t4 = 0; t4 < DX4; ++t4) {
+      const float4 x = *reinterpret_cast<const float4*>(xr + u * RS + 4 * t4);
+      const float d0 = P.c[4 * t4 + 0] - x.x;
+      const float d1 = P.c[4 * t4 + 1] - x.y;
+      const float d2 = P.c[4 * t4 + 2] - x.z;
+      const float d3 = P.c[4 * t4 + 3] - x.w;
+      r2 = fmaf(d0, d0, r2);
+      r2 = fmaf(d1, d1, r2);
+      r2 = fmaf(d2, d2, r2);
+      r2 = fmaf(d3, d3, r2);
+    }
+    // no mask: rows past n (zero coordinates) meet zero columns of L^{-1}
+    // and zero alpha; columns past the batch are never written
+    const float kv = matern52_f(r2, a.s);
+    P.mu = fmaf(xr[u * RS + 4 * DX4], kv, P.mu);
+    const _Float16 h = static_cast<_Float16>(kv);
+    hi[u] = h;
+    lo[u] = static_cast<_Float16>(kv - static_cast<float>(h));
+  }
+  _Float16* dst = ring + P.col * kCSH + (jb % kRing) * kJ + P.row0;
+  *reinterpret_cast<halfr*>(dst) = hi;
+  *reinterpret_cast<halfr*>(dst + NT * kCSH) = lo;
+}
+
+// Row block of slot r in the pass starting at row block `base`.
+__device__ __forceinline__ int slot_block(int base, int r, int wave) {
+  return base + 8 * r + ((r & 1) ? (kWaves - 1 - wave) : wave);
+}
+
+// Row-block slots of a wave in one pass: packed index of block (I, 0) and the
+// last live J (I / 2), or (zero block, -1) for a slot past the matrix.
+template <int RB>
+struct Slots {
+  int first[RB];
+  int last[RB];
+};
+
+__device__ __forceinline__ int frag_block(int first, int last, int J, int zero_blk) {
+  return (J <= last) ? first + J : zero_blk;
+}
+
+// A fragments of one slot: hi and lo planes (1 KiB each per block).
+struct AFrag {
+  halfx8 hi, lo;
+};
+
+__device__ __forceinline__ AFrag load_a(__amdgpu_buffer_rsrc_t rs, int voff, int blk) {
+  AFrag f;
+  f.hi = __builtin_bit_cast(halfx8, load4(rs, voff, blk * 2048));
+  f.lo = __builtin_bit_cast(halfx8, load4(rs, voff, blk * 2048 + 1024));
+  return f;
+}
+
+// B fragments of one half of a block (column blocks 2h and 2h + 1), hi and lo
+// planes.
+struct BHalf {
+  halfx8 hi[2], lo[2];
+};
+
+// MFMAs of slots r0, r0 + 1 (those below RB) against one half of a block's
+// columns: the three products of the pair's (up to) four accumulators.
+template <int RB, int NCB, int H>
+__device__ __forceinline__ void mfma_pair_half(int r0, const AFrag (&av)[RB], const BHalf& B,
+                                               floatx4 (&acc)[RB][NCB]) {
+#pragma unroll
+  for (int r = r0; r < r0 + 2 && r < RB; ++r)
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+      acc[r][2 * H + b] =
+          __builtin_amdgcn_mfma_f32_16x16x32_f16(av[r].hi, B.hi[b], acc[r][2 * H + b], 0, 0, 0);
+#pragma unroll
+  for (int r = r0; r < r0 + 2 && r < RB; ++r)
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+      acc[r][2 * H + b] =
+          __builtin_amdgcn_mfma_f32_16x16x32_f16(av[r].hi, B.lo[b], acc[r][2 * H + b], 0, 0, 0);
+#pragma unroll
+  for (int r = r0; r < r0 + 2 && r < RB; ++r)
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+      acc[r][2 * H + b] =
+          __builtin_amdgcn_mfma_f32_16x16x32_f16(av[r].lo, B.hi[b], acc[r][2 * H + b], 0, 0, 0);
+}
+
+// Workgroup-uniform context of the streaming loop.
+struct Ctx {
+  __amdgpu_buffer_rsrc_t lp_rs;   // packed fragments of this objective
+  int nb, nbj, zero_blk, n_pad, wave, tid;
+  int voff;                 // this lane's byte offset inside a fragment plane
+  const _Float16* Kb;       // this lane's B-fragment base inside the ring
+  float* xst;               // training-row staging (4 blocks)
+};
+
+// B fragments of half h of block J: columns (2h + b)*16 + lane%16, rows
+// 8*(lane/16) .. +7.
+template <int NT>
+__device__ __forceinline__ void load_b(const Ctx& C, int J, int h, BHalf& B) {
+  const _Float16* kb = C.Kb + (J % kRing) * kJ;
+#pragma unroll
+  for (int b = 0; b < 2; ++b) {
+    B.hi[b] = *reinterpret_cast<const halfx8*>(kb + (2 * h + b) * 16 * kCSH);
+    B.lo[b] = *reinterpret_cast<const halfx8*>(kb + (NT + (2 * h + b) * 16) * kCSH);
+  }
+}
+
+// One step J for slots [LO, RB). B0 holds the first half of block J's B
+// fragments on entry (read during the previous step) and the first half of
+// block J + 1's on exit; the second half is read at the start. The MFMAs of
+// block J (fragments for J + 1 requested on the way) and the producer's block
+// J + 2 (when PROD) are independent and are left to the scheduler to
+// interleave: the fp16 MFMAs overlap the VALU work. The step's barrier
+// publishes the produced block and the staged rows; block J + 1 was
+// published by the previous step's, so its B fragments can be read early.
+template <int LO, int RB, int NT, int DX4, bool PROD>
+__device__ __forceinline__ void step(const Ctx& C, const PosteriorArgs& a, Producer<NT, DX4>& P,
+                                     Stager<DX4>& S, _Float16* ring, const Slots<RB>& sl, int J,
+                                     BHalf& B0, AFrag (&av)[RB], floatx4 (&acc)[RB][NT / 16]) {
+  constexpr int NCB = NT / 16;
+  static_assert(NCB == 4, "two halves of two column blocks");
+  // the staging load goes first among the step's loads and its store last,
+  // so the store waits for it alone, a whole step after it was issued
+  stage_load(S, a, J + 4);
+  __builtin_amdgcn_sched_barrier(0);
+  BHalf B1;
+  load_b<NT>(C, J, 1, B1);
+  if constexpr (PROD) produce(P, a, J + 2, C.xst, ring);
+  // slot pairs in turn, each pair's fragments for J + 1 requested as soon as
+  // its MFMAs are issued (about half a step before the next step needs them);
+  // the next block's first B half is read once the last pair is done with it
+#pragma unroll
+  for (int r0 = LO; r0 < RB; r0 += 2) {
+    mfma_pair_half<RB, NCB, 0>(r0, av, B0, acc);
+    if (r0 + 2 >= RB) load_b<NT>(C, J + 1, 0, B0);
+    mfma_pair_half<RB, NCB, 1>(r0, av, B1, acc);
+#pragma unroll
+    for (int r = r0; r < r0 + 2 && r < RB; ++r)
+      av[r] = load_a(C.lp_rs, C.voff, frag_block(sl.first[r], sl.last[r], J + 1, C.zero_blk));
+  }
+  if constexpr (LO >= RB) load_b<NT>(C, J + 1, 0, B0);
+  if constexpr (PROD) {
+    // interleave: the scheduler otherwise runs the producer's VALU work and
+    // the MFMAs as two separate stretches, and the two waves of a SIMD
+    // (kept in step by the barriers) then contend for the same unit
+    constexpr int nM = 3 * NCB * (RB - LO);
+    constexpr int nV = Producer<NT, DX4>::RPL * (2 * 4 * DX4 + 14);
+    if constexpr (nM > 0) {
+#pragma unroll
+      for (int i = 0; i < nM; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                  // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x002, (nV + nM - 1) / nM, 0);  // VALU
+      }
+    }
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  stage_store(S, C.xst, J + 4);
+  lds_barrier();
+}
+
+// Steps [j0, j1) for slots [LO, RB); the producer runs at the steps whose
+// block J + 2 lies in the pass's production window [pw0, pw1).
+template <int LO, int RB, int NT, int DX4>
+__device__ __forceinline__ void span(const Ctx& C, const PosteriorArgs& a, Producer<NT, DX4>& P,
+                                     Stager<DX4>& S, _Float16* ring, const Slots<RB>& sl, int j0,
+                                     int j1, int pw0, int pw1, BHalf& B0, AFrag (&av)[RB],
+                                     floatx4 (&acc)[RB][NT / 16]) {
+  const int p0 = min(max(pw0 - 2, j0), j1), p1 = min(max(pw1 - 2, p0), j1);
+  int J = j0;
+  for (; J < p0; ++J) step<LO, RB, NT, DX4, false>(C, a, P, S, ring, sl, J, B0, av, acc);
+  for (; J < p1; ++J) step<LO, RB, NT, DX4, true>(C, a, P, S, ring, sl, J, B0, av, acc);
+  for (; J < j1; ++J) step<LO, RB, NT, DX4, false>(C, a, P, S, ring, sl, J, B0, av, acc);
+}
+
+// Rounds R.. of the triangular part of a pass: round R covers the row blocks
+// base + 8R .. base + 8R + 7, i.e. J in [base/2 + 4R, base/2 + 4R + 4); slot R
+// is live while J <= its row block / 2, slots above R throughout.
+template <int R, int RB, int NT, int DX4>
+__device__ __forceinline__ void rounds(const Ctx& C, const PosteriorArgs& a, Producer<NT, DX4>& P,
+                                       Stager<DX4>& S, _Float16* ring, const Slots<RB>& sl,
+                                       int base, int pw0, int pw1, BHalf& B0, AFrag (&av)[RB],
+                                       floatx4 (&acc)[RB][NT / 16]) {
+  if constexpr (R < RB) {
+    const int j0 = base / 2 + 4 * R;
+    if (j0 >= C.nbj) return;
+    const int jend = min(j0 + 4, C.nbj);
+    const int jlive = min(slot_block(base, R, C.wave) / 2 + 1, jend);
+    span<R, RB, NT, DX4>(C, a, P, S, ring, sl, j0, jlive, pw0, pw1, B0, av, acc);
+    span<R + 1, RB, NT, DX4>(C, a, P, S, ring, sl, jlive, jend, pw0, pw1, B0, av, acc);
+    rounds<R + 1, RB, NT, DX4>(C, a, P, S, ring, sl, base, pw0, pw1, B0, av, acc);
+  }
+}
+
+template <int NT, int DX4, int Q, int RB>
+__global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
+  extern __shared__ float smem[];
+  constexpr int NCB = NT / 16;          // 16-column blocks per tile
+  constexpr int NX = (Q > 1) ? Q : 1;   // per-point partial slots (diag + xors)
+  using Prod = Producer<NT, DX4>;
+  static_assert(Prod::RPL >= 2 && Prod::RPL <= 8 && 64 % Prod::CPW == 0, "tile width");
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  // wave index as a scalar: the loop control below stays uniform
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int n_pad = a.nb * kBlk;
+  _Float16* ring = reinterpret_cast<_Float16*>(smem);       // 2 planes x NT x kCSH halves
+  float* xst = smem + NT * kCSH;                            // 4 slots + a scratch float4
+  float* red = smem;                                        // kWaves * NT * NX, after the loop
+  float* mush = xst + 4 * Stager<DX4>::kSlot + 4;           // NT
+  float* kpp = mush + NT;                                   // NT * 4 (prior cross-cov)
+  const int64_t p0 = (int64_t)blockIdx.x * NT;
+
+  Prod P;
+  P.col = wave * Prod::CPW + lane % Prod::CPW;
+  P.row0 = (lane / Prod::CPW) * Prod::RPL;
+  {
+    const int64_t p = p0 + P.col;
+    P.valid = p < a.npts;
+#pragma unroll
+    for (int t = 0; t < DX4 * 4; ++t) P.c[t] = 0.f;
+    if (P.valid) {
+      const float* cp = a.cand + p * a.d;
+#pragma unroll
+      for (int t = 0; t < DX4 * 4; ++t)
+        if (t < a.d) P.c[t] = cp[t] * a.invls[t];
+    }
+  }
+
+  if (Q > 1) {
+    // prior covariance of each point with its batch mates (point ^ x), partner
+    // x on the lane of the column's group whose row group is x
+    const int x = lane / Prod::CPW;
+    if (x >= 1 && x < Q) {
+      const int64_t pm = (p0 + P.col) ^ x;
+      float r2 = 0.f;
+      if (P.valid && pm < a.npts) {
+        const float* cp = a.cand + pm * a.d;
+#pragma unroll
+        for (int t = 0; t < DX4 * 4; ++t)
+          if (t < a.d) {
+            const float dd = P.c[t] - cp[t] * a.invls[t];
+            r2 = fmaf(dd, dd, r2);
+          }
+      }
+      kpp[P.col * 4 + x] = matern52_f(r2, a.s);
+    }
+  }
+
+  Ctx C;
+  C.nb = a.nb;
+  C.nbj = (a.nb + 1) / 2;
+  C.zero_blk = frag_row_start(a.nb);
+  C.lp_rs = make_rsrc(a.Lp, (C.zero_blk + 1) * 2048);
+  Stager<DX4> S;
+  S.xs_rs = make_rsrc(a.Xs, n_pad * a.dx * 4);
+  S.al_rs = make_rsrc(a.alpha, n_pad * 4);
+  S.row = min(tid / (DX4 + 1), kJ - 1);
+  S.t4 = tid % (DX4 + 1);
+  S.soff = (tid < Stager<DX4>::kF4) ? S.row * Stager<DX4>::RS + 4 * S.t4 : 4 * Stager<DX4>::kSlot;
+  C.n_pad = n_pad;
+  C.wave = wave;
+  C.tid = tid;
+  C.xst = xst;
+  C.voff = lane * 16;
+  // B fragments: column (b*16 + lane%16), rows 8*(lane/16) .. +7 of a block
+  C.Kb = ring + (lane & 15) * kCSH + 8 * (lane >> 4);
+
+  float ss[NCB];
+  float gx[NCB][NX];
+#pragma unroll
+  for (int b = 0; b < NCB; ++b) {
+    ss[b] = 0.f;
+#pragma unroll
+    for (int x = 0; x < NX; ++x) gx[b][x] = 0.f;
+  }
+
+  // blocks 0 .. have-1 of K*^T are in the ring (have = 0: start over)
+  int have = 0;
+  for (int base = 0; base < a.nb; base += 8 * RB) {
+    const int jpass = min(C.nbj, base / 2 + 4 * RB);   // J range of this pass
+    floatx4 acc[RB][NCB];
+#pragma unroll
+    for (int r = 0; r < RB; ++r)
+#pragma unroll
+      for (int b = 0; b < NCB; ++b) acc[r][b] = floatx4{0.f, 0.f, 0.f, 0.f};
+    Slots<RB> sl;
+    AFrag av[RB];
+#pragma unroll
+    for (int r = 0; r < RB; ++r) {
+      const int I = slot_block(base, r, wave);
+      sl.first[r] = I < a.nb ? frag_row_start(I) : C.zero_blk;
+      sl.last[r] = I < a.nb ? I / 2 : -1;
+      av[r] = load_a(C.lp_rs, C.voff, frag_block(sl.first[r], sl.last[r], 0, C.zero_blk));
+    }
+    // the previous pass may still read the staging slots
+    lds_barrier();
+    {
+      // blocks 0..3 at once: one load latency, not four
+      Stager<DX4> S4[4];
+#pragma unroll
+      for (int jb = 0; jb < 4; ++jb) {
+        S4[jb] = S;
+        stage_load(S4[jb], a, jb);
+      }
+#pragma unroll
+      for (int jb = 0; jb < 4; ++jb) stage_store(S4[jb], xst, jb);
+    }
+    lds_barrier();
+    if (have == 0) {
+      // start over: blocks 0 and 1, and mu from scratch
+      P.mu = 0.f;
+      produce(P, a, 0, xst, ring);
+      produce(P, a, 1, xst, ring);
+      have = 2;
+      lds_barrier();
+    }
+    const int pw0 = have, pw1 = jpass;   // blocks this pass produces
+    BHalf B0;
+    load_b<NT>(C, 0, 0, B0);
+    // blocks left of this pass's triangle: every slot is live
+    span<0, RB, NT, DX4>(C, a, P, S, ring, sl, 0, base / 2, pw0, pw1, B0, av, acc);
+    rounds<0, RB, NT, DX4>(C, a, P, S, ring, sl, base, pw0, pw1, B0, av, acc);
+    have = (jpass <= kRing) ? max(have, jpass) : 0;
+
+#pragma unroll
+    for (int r = 0; r < RB; ++r)
+#pragma unroll
+      for (int b = 0; b < NCB; ++b)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float v = acc[r][b][e];
+          ss[b] = fmaf(v, v, ss[b]);
+          if (Q > 1) {
+#pragma unroll
+            for (int x = 1; x < NX; ++x) gx[b][x] = fmaf(v, quad_xor(v, x), gx[b][x]);
+          }
+        }
+  }
+
+  // mu: the last pass produced every block; reduce over the lanes of a column
+  {
+    float v = P.mu;
+#pragma unroll
+    for (int off = Prod::CPW; off < 64; off <<= 1) v += __shfl_xor(v, off);
+    if (lane < Prod::CPW) mush[P.col] = v;
+  }
+  // |v|^2 (and cross terms): over the four 16-lane row groups, then over
+  // waves in LDS (red overlays the ring: wait until every wave is done)
+  __syncthreads();
+#pragma unroll
+  for (int b = 0; b < NCB; ++b) {
+    ss[b] += __shfl_xor(ss[b], 16);
+    ss[b] += __shfl_xor(ss[b], 32);
+#pragma unroll
+    for (int x = 1; x < NX; ++x) {
+      gx[b][x] += __shfl_xor(gx[b][x], 16);
+      gx[b][x] += __shfl_xor(gx[b][x], 32);
+    }
+    if (lane < 16) {
+      const int cc = b * 16 + lane;
+      red[(wave * NT + cc) * NX + 0] = ss[b];
+#pragma unroll
+      for (int x = 1; x < NX; ++x) red[(wave * NT + cc) * NX + x] = gx[b][x];
+    }
+  }
+  __syncthreads();
+
+  // ---- epilogue -------------------------------------------------------------
+  if (tid < NT) {
+    const int64_t p = p0 + tid;
+    const bool valid = p < a.npts;
+    float tot[NX];
+#pragma unroll
+    for (int x = 0; x < NX; ++x) tot[x] = 0.f;
+    for (int w = 0; w < kWaves; ++w)
+#pragma unroll
+      for (int x = 0; x < NX; ++x) tot[x] += red[(w * NT + tid) * NX + x];
+    const float mu = mush[tid];
+    const float var = a.s - tot[0];
+    if (valid) {
+      a.mu[p * a.m + a.k] = mu;
+      a.sd[p * a.m + a.k] = __builtin_amdgcn_sqrtf(fmaxf(var, 0.f));
+    }
+    if (Q > 1) {
+      // covariance row of this point (diagonal, then partner p ^ x) for the
+      // batch owner; each thread rewrites only its own kpp slots
+      kpp[tid * 4 + 0] = var;
+#pragma unroll
+      for (int x = 1; x < NX; ++x) kpp[tid * 4 + x] -= tot[x];
+    }
+  }
+  if (Q > 1) {
+    __syncthreads();
+    constexpr int NB = NT / Q;
+    if (tid < NB) {
+      const int64_t bat = (int64_t)blockIdx.x * NB + tid;
+      if (bat * Q < a.npts) {
+        float S[Q][Q];
+#pragma unroll
+        for (int i = 0; i < Q; ++i)
+#pragma unroll
+          for (int j = 0; j < Q; ++j)
+            S[i][j] = (i == j) ? kpp[(tid * Q + i) * 4 + 0] : kpp[(tid * Q + i) * 4 + (i ^ j)];
+        float L[Q][Q];
+#pragma unroll
+        for (int i = 0; i < Q; ++i)
+#pragma unroll
+          for (int j = 0; j < Q; ++j) L[i][j] = 0.f;
+        const float tol = 1e-10f * a.s;
+#pragma unroll
+        for (int j = 0; j < Q; ++j) {
+          float pv = S[j][j];
+#pragma unroll
+          for (int t = 0; t < j; ++t) pv = fmaf(-L[j][t], L[j][t], pv);
+          if (pv > tol) {
+            const float ljj = __builtin_amdgcn_sqrtf(pv);
+            L[j][j] = ljj;
+            const float inv = 1.0f / ljj;
+#pragma unroll
+            for (int i = j + 1; i < Q; ++i) {
+              float num = S[i][j];
+#pragma unroll
+              for (int t = 0; t < j; ++t) num = fmaf(-L[i][t], L[j][t], num);
+              L[i][j] = num * inv;
+            }
+          }
+        }
+        constexpr int T = Q * (Q + 1) / 2;
+        float* dst = a.chol + (bat * a.m + a.k) * T;
+#pragma unroll
+        for (int i = 0; i < Q; ++i)
+#pragma unroll
+          for (int j = 0; j <= i; ++j) dst[i * (i + 1) / 2 + j] = L[i][j];
+      }
+    }
+  }
+}
+
+constexpr size_t lds_floats(int NT, int DX4, int q) {
+  // ring: 2 planes x NT columns x kCSH halves (the reduction overlays it);
+  // staging: 4 slots + a scratch float4; mu and the prior cross-covariances
+  return (size_t)NT * kCSH + (size_t)4 * kJ * (DX4 * 4 + 4) + 4 + NT + (size_t)NT * 4;
+}
+static_assert((size_t)kWaves * 64 * 4 <= (size_t)64 * kCSH, "reduction fits the ring");
+
+template <int NT, int DX4, int Q, int RB>
+hipError_t launch_t(const PosteriorArgs& a, hipStream_t st) {
+  const size_t lds = sizeof(float) * lds_floats(NT, DX4, Q);
+  // more than 64 KiB of dynamic LDS: opt in (cheap; set on every launch so
+  // that it holds on whichever device is current)
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_posterior<NT, DX4, Q, RB>),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize,
+                                     static_cast<int>(lds));
+  if (e != hipSuccess) return e;
+  const unsigned grid = static_cast<unsigned>((a.npts + NT - 1) / NT);
+  hipLaunchKernelGGL((k_posterior<NT, DX4, Q, RB>), dim3(grid), dim3(kThreads), lds, st, a);
+  return hipGetLastError();
+}
+
+// Launch for coordinate width 4*DX4: q in {1, 2, 4}; 2 row-block slots per
+// wave up to 256 rows, else BO_POST_RB (further rows in passes).
+template <int DX4>
+hipError_t launch_for_dx(const PosteriorArgs& a, hipStream_t st) {
+  const bool small = a.nb <= 16;
+  switch (a.q) {
+    case 1: return small ? launch_t<BO_POST_NT, DX4, 1, 2>(a, st)
+                         : launch_t<BO_POST_NT, DX4, 1, BO_POST_RB>(a, st);
+    case 2: return small ? launch_t<BO_POST_NT, DX4, 2, 2>(a, st)
+                         : launch_t<BO_POST_NT, DX4, 2, BO_POST_RB>(a, st);
+    case 4: return small ? launch_t<BO_POST_NT, DX4, 4, 2>(a, st)
+                         : launch_t<BO_POST_NT, DX4, 4, BO_POST_RB>(a, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace
+
+// One per coordinate width (posterior_dx<N>.hip).
+hipError_t launch_posterior_dx1(const PosteriorArgs& a, hipStream_t st);
+hipError_t launch_posterior_dx2(const PosteriorArgs& a, hipStream_t st);
+hipError_t launch_posterior_dx3(const PosteriorArgs& a, hipStream_t st);
+hipError_t launch_posterior_dx4(const PosteriorArgs& a, hipStream_t st);
+hipError_t launch_posterior_dx5(const PosteriorArgs& a, hipStream_t st);
+hipError_t launch_posterior_dx6(const PosteriorArgs& a, hipStream_t st);
+hipError_t launch_posterior_dx7(const PosteriorArgs& a, hipStream_t st);
+hipError_t launch_posterior_dx8(const PosteriorArgs& a, hipStream_t st);
+
+}  // namespace bo

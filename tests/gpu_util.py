@@ -18,7 +18,7 @@ def to_dev(a):
     return torch.from_numpy(np.ascontiguousarray(a)).cuda()
 
 
-def gpu_run(wl, cand=None, want_musd=True, ref=None, Z=None):
+def gpu_run(wl, cand=None, want_musd=True, ref=None, Z=None, lower=None):
     import torch
     import paper_2602_10729_amd as bo
     X, Y = to_dev(wl.X), to_dev(wl.Y)
@@ -31,7 +31,7 @@ def gpu_run(wl, cand=None, want_musd=True, ref=None, Z=None):
     if want_musd:
         mu = torch.empty((M, q, wl.m), dtype=torch.float32, device="cuda")
         sg = torch.empty_like(mu)
-    e = bo.score(model, c, r, z, mu=mu, sigma=sg)
+    e = bo.score(model, c, r, z, mu=mu, sigma=sg, lower=lower)
     idx, val = bo.argmax(e)
     torch.cuda.synchronize()
     out = dict(ehvi=e.cpu().numpy(), idx=int(idx.item()), val=float(val.item()),
@@ -46,10 +46,63 @@ def oracle_fit(wl):
     return O.fit(wl.X, wl.Y, wl.lengthscale, wl.outputscale, wl.noise)
 
 
-def oracle_score(model, wl, cand=None, ref=None, Z=None):
+def oracle_score(model, wl, cand=None, ref=None, Z=None, lower=None):
     c = wl.cand if cand is None else cand
     return O.score(model, c.astype(np.float64), wl.ref if ref is None else ref,
-                   (wl.Z if Z is None else Z).astype(np.float64))
+                   (wl.Z if Z is None else Z).astype(np.float64),
+                   lower=None if lower is None else np.asarray(lower, dtype=np.float64))
+
+
+def _tol(x, tol):
+    return tol[0] * np.abs(x) + tol[1]
+
+
+def constrained_bounds(o, Z, lower, safety=4.0):
+    """Range of the constrained acquisition over the samples whose
+    feasibility the GPU may decide differently from the oracle.
+
+    The feasibility decision y_s >= t is taken on each side's own y_s; the
+    two y_s differ by at most the mu tolerance plus |z| times the sigma
+    tolerance (q = 1), or that plus |z| times the sigma tolerance summed over
+    the factor row (q > 1, rows of the factor scaled from sigma). A sample
+    within `safety` times that band of a threshold is ambiguous: it counts in
+    the upper bound and not in the lower one. Returns (lo, hi) per candidate;
+    they coincide where no sample is ambiguous."""
+    lo_b, hi_b = o["lo"], o["hi"]
+    lower = np.asarray(lower, dtype=np.float64)
+    mu = o["mu"]                                   # [M, q, m]
+    M, q, m = mu.shape
+    Zd = np.asarray(Z, dtype=np.float64)           # [S, q, m]
+    if q == 1:
+        sd = o["sigma"][:, 0, :]
+        ys = mu[:, None, 0, :] + sd[:, None, :] * Zd[None, :, 0, :]       # [M, S, m]
+        band = safety * (_tol(mu[:, None, 0, :], (1e-4, 1e-5)) +
+                         np.abs(Zd[None, :, 0, :]) * _tol(sd[:, None, :], (1e-4, 1e-5)))
+        h = O.hvi(ys, lo_b, hi_b)
+        d = ys - lower
+        sure = np.all(d > band, axis=-1)
+        maybe = np.all(d >= -band, axis=-1)
+        return np.mean(h * sure, axis=1), np.mean(h * maybe, axis=1)
+    Cf = O.chol_psd(o["cov"], 1.0)                 # [M, m, q, q]
+    corr = np.einsum("ckab,sbk->csak", Cf, Zd)
+    ys = mu[:, None, :, :] + corr                  # [M, S, q, m]
+    rowabs = np.einsum("ckab,sbk->csak", np.abs(Cf), np.abs(Zd))
+    band = safety * (_tol(mu[:, None], (1e-4, 1e-5)) + 1e-4 * rowabs + 1e-5)
+    d = ys - lower
+    sure = np.all(d > band, axis=-1).astype(float)     # [M, S, q]
+    maybe = np.all(d >= -band, axis=-1).astype(float)
+    return (np.mean(O.qhvi(ys, lo_b, hi_b, sure), axis=1),
+            np.mean(O.qhvi(ys, lo_b, hi_b, maybe), axis=1))
+
+
+def assert_within_bounds(g, lo, hi, tol, what):
+    """g within [lo - tol(lo), hi + tol(hi)] elementwise."""
+    g = np.asarray(g, dtype=np.float64)
+    ok = (g >= lo - _tol(lo, tol)) & (g <= hi + _tol(hi, tol))
+    if not ok.all():
+        i = int(np.argmax(~ok))
+        raise AssertionError(f"{what}: {int((~ok).sum())} of {g.size} outside the bounds; "
+                             f"first at {i}: gpu={g[i]!r} bounds=[{lo[i]!r}, {hi[i]!r}]")
 
 
 def assert_close(g, o, tol, what):

@@ -128,3 +128,46 @@ def ehvi_closed_form(mu, sd, lo, hi) -> float:
             prod *= float(psi(mu[k], sd[k], lo[c, k]) - psi(mu[k], sd[k], hi[c, k]))
         total += prod
     return total
+
+
+def _tail_first_moment(mu, sd, l, a):
+    """E[(Y - l) 1[Y >= a]] for Y ~ N(mu, sd^2); 0 for a = +inf."""
+    if not np.isfinite(a):
+        return 0.0 if a > 0 else mu - l
+    t = (a - mu) / sd
+    return sd * math.exp(-0.5 * t * t) / math.sqrt(2 * math.pi) + (mu - l) * (1.0 - ndtr(t))
+
+
+def _tail_prob(mu, sd, a):
+    """P(Y >= a)."""
+    if not np.isfinite(a):
+        return 0.0 if a > 0 else 1.0
+    return 1.0 - ndtr((a - mu) / sd)
+
+
+def constrained_ehvi_closed_form(mu, sd, lo, hi, lower) -> float:
+    """Exact E[HVI(Y) * prod_k 1[Y_k >= t_k]] for independent Gaussian
+    objectives over disjoint boxes. The integrand factorises per objective;
+    with a = max(l, t) each factor is
+      E[(min(Y,u) - l) 1[Y >= a]]
+        = (u - l) P(Y >= a)                                   if a >= u
+        = E[(Y-l)1[Y>=a]] - E[(Y-l)1[Y>=u]] + (u-l) P(Y>=u)  otherwise,
+    since [min(y,u) - l]_+ vanishes below l and the indicator below t."""
+    mu = np.asarray(mu, dtype=np.float64)
+    sd = np.asarray(sd, dtype=np.float64)
+    lower = np.asarray(lower, dtype=np.float64)
+    total = 0.0
+    for c in range(lo.shape[0]):
+        prod = 1.0
+        for k in range(lo.shape[1]):
+            l, u, t = float(lo[c, k]), float(hi[c, k]), float(lower[k])
+            a = max(l, t)
+            if a >= u:
+                f = (u - l) * _tail_prob(mu[k], sd[k], a)
+            else:
+                f = _tail_first_moment(mu[k], sd[k], l, a)
+                if np.isfinite(u):
+                    f += -_tail_first_moment(mu[k], sd[k], l, u) + (u - l) * _tail_prob(mu[k], sd[k], u)
+            prod *= f
+        total += prod
+    return total
