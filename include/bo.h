@@ -87,10 +87,14 @@ typedef enum {
  * stream hipStream_t or NULL
  * out    receives a new model on BO_OK (untouched otherwise)
  *
- * Synchronous: returns after the device work has finished and the positive
- * definiteness check has been read back. Errors: INVALID_ARGUMENT,
- * NONFINITE_INPUT (hyperparameters or Y not finite), CAPACITY,
- * NOT_POSITIVE_DEFINITE, OUT_OF_MEMORY, DEVICE.
+ * Synchronous: enqueues all device work on the stream (behind earlier work,
+ * without waiting for it), then waits once and returns after the positive
+ * definiteness flag and Y have been read back. Y lives on the device, so its
+ * finiteness is checked at that point (its kernels have already run); the
+ * host arguments are validated before anything is enqueued. Concurrent fits
+ * on one device share a pinned staging buffer and run one at a time.
+ * Errors: INVALID_ARGUMENT, NONFINITE_INPUT (hyperparameters or Y not
+ * finite), CAPACITY, NOT_POSITIVE_DEFINITE, OUT_OF_MEMORY, DEVICE.
  */
 bo_status bo_fit(const float* X, const float* Y, int64_t n, int32_t d, int32_t m,
                  const float* lengthscale, const float* outputscale,

@@ -91,13 +91,20 @@ bool all_finite(const float* v, size_t n) {
 
 // Per-device library state: a stream-ordered memory pool (allocations made
 // and released inside the hot path come back from it without a device-wide
-// synchronisation) and one pinned staging buffer for box uploads.
+// synchronisation), one pinned staging buffer for box uploads, and one for
+// the fit's uploads and read-backs (pinned, so that bo_fit enqueues all of its
+// work without waiting for earlier work on the stream; bo_fit holds fit_mu
+// until its final synchronisation, so the buffer is never rewritten while a
+// copy from it is pending).
 struct DeviceState {
   std::mutex mu;
   hipMemPool_t pool = nullptr;
   float* stage = nullptr;
   size_t stage_floats = 0;
   hipEvent_t stage_evt = nullptr;
+  std::mutex fit_mu;
+  unsigned char* fit_stage = nullptr;
+  size_t fit_stage_bytes = 0;
 };
 constexpr int kMaxDevices = 64;
 
@@ -345,14 +352,6 @@ bo_status bo_fit(const float* X, const float* Y, int64_t n, int32_t d, int32_t m
     return st_;
   };
 
-  // Y to the host for the front (and to check finiteness)
-  M->Yh.resize((size_t)n * m);
-  hipError_t e = hipMemcpyAsync(M->Yh.data(), Y, sizeof(float) * n * m, hipMemcpyDeviceToHost, st);
-  if (e == hipSuccess) e = hipStreamSynchronize(st);
-  if (e != hipSuccess) return bail(hip_fail(e, "bo_fit: copy Y"));
-  if (!all_finite(M->Yh.data(), M->Yh.size())) return bail(fail(BO_ERR_NONFINITE_INPUT, "bo_fit: Y not finite"));
-  host_front(M->Yh.data(), n, m, nullptr, M->nd);
-
   const int nf = static_cast<int>((n + kFitBlk - 1) / kFitBlk) * kFitBlk;
   M->lp_per_obj = (size_t)posterior_frag_blocks(M->nb) * 512;   // 2 KiB per block
   FitScratch fs;
@@ -377,9 +376,31 @@ bo_status bo_fit(const float* X, const float* Y, int64_t n, int32_t d, int32_t m
   for (int k = 0; k < m; ++k)
     for (int t = 0; t < d; ++t) invls[(size_t)k * M->dx + t] = 1.0f / lengthscale[k * d + t];
 
-  e = hipMemcpyAsync(fs.hyp, hyp.data(), sizeof(double) * hyp.size(), hipMemcpyHostToDevice, st);
+  // pinned staging: [hyperparameters (fp64)][1/lengthscale (fp32)][flag][Y]
+  DeviceState* DS = device_state(M->device);
+  if (!DS) return bail(fail(BO_ERR_DEVICE, "bo_fit: device index out of range"));
+  std::lock_guard<std::mutex> stage_lock(DS->fit_mu);
+  const size_t off_inv = sizeof(double) * hyp.size();
+  const size_t off_flag = (off_inv + sizeof(float) * invls.size() + 15) / 16 * 16;
+  const size_t off_y = off_flag + 16;
+  const size_t need = off_y + sizeof(float) * n * m;
+  hipError_t e = hipSuccess;
+  if (need > DS->fit_stage_bytes) {
+    if (DS->fit_stage) (void)hipHostFree(DS->fit_stage);
+    DS->fit_stage = nullptr;
+    DS->fit_stage_bytes = 0;
+    const size_t cap = std::max<size_t>(need, size_t(1) << 16);
+    e = hipHostMalloc(reinterpret_cast<void**>(&DS->fit_stage), cap, hipHostMallocDefault);
+    if (e != hipSuccess) return bail(hip_fail(e, "bo_fit: pinned staging"));
+    DS->fit_stage_bytes = cap;
+  }
+  unsigned char* stage = DS->fit_stage;
+  std::memcpy(stage, hyp.data(), off_inv);
+  std::memcpy(stage + off_inv, invls.data(), sizeof(float) * invls.size());
+  e = hipMemcpyAsync(fs.hyp, stage, off_inv, hipMemcpyHostToDevice, st);
   if (e == hipSuccess)
-    e = hipMemcpyAsync(M->invls, invls.data(), sizeof(float) * invls.size(), hipMemcpyHostToDevice, st);
+    e = hipMemcpyAsync(M->invls, stage + off_inv, sizeof(float) * invls.size(),
+                       hipMemcpyHostToDevice, st);
   if (e == hipSuccess) e = hipMemsetAsync(fs.flag, 0, sizeof(int), st);
   if (e != hipSuccess) return bail(hip_fail(e, "bo_fit: upload"));
 
@@ -391,11 +412,21 @@ bo_status bo_fit(const float* X, const float* Y, int64_t n, int32_t d, int32_t m
   if ((s = after_launch(launch_alpha(fs.W, Y, n, m, nf, M->n_pad, fs.tmp, M->alpha, st), st, "alpha")) != BO_OK) return bail(s);
   if ((s = after_launch(launch_pack(fs.W, n, m, nf, M->nb, M->Lp, X, d, M->dx, M->invls, M->Xs, st), st, "pack")) != BO_OK) return bail(s);
 
-  int flag = 0;
-  e = hipMemcpyAsync(&flag, fs.flag, sizeof(int), hipMemcpyDeviceToHost, st);
+  // one synchronisation: the positive-definiteness flag and Y (for the front
+  // and its finiteness check) come back together
+  e = hipMemcpyAsync(stage + off_flag, fs.flag, sizeof(int), hipMemcpyDeviceToHost, st);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(stage + off_y, Y, sizeof(float) * n * m, hipMemcpyDeviceToHost, st);
   if (e == hipSuccess) e = hipStreamSynchronize(st);
   if (e != hipSuccess) return bail(hip_fail(e, "bo_fit: sync"));
+  int flag = 0;
+  std::memcpy(&flag, stage + off_flag, sizeof(int));
+  const float* yst = reinterpret_cast<const float*>(stage + off_y);
+  M->Yh.assign(yst, yst + (size_t)n * m);
+  if (!all_finite(M->Yh.data(), M->Yh.size()))
+    return bail(fail(BO_ERR_NONFINITE_INPUT, "bo_fit: Y not finite"));
   if (flag) return bail(fail(BO_ERR_NOT_POSITIVE_DEFINITE, "bo_fit: non-positive Cholesky pivot"));
+  host_front(M->Yh.data(), n, m, nullptr, M->nd);
 
   M->last_stream = st;
   *out = h;

@@ -22,8 +22,8 @@
 //           (i > kb, j <= kb), 64x64x64 tiles; the workgroup that updates
 //           the next diagonal tile factors and inverts it at once, so no
 //           separate factor launch is needed after the first.
-// Two launches per block column; the serial chain is one 64-step factor and
-// one 64-step inverse per block column.
+// Two launches per block column; the serial chain is one 64-step fused
+// factor and inverse of the diagonal block per block column.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -43,15 +43,28 @@ __device__ inline double matern52_d(double r2, double s) {
 }
 
 // Gram matrix in fp64, lower block triangle only (tiles above the diagonal
-// blocks are never read by the factorisation). ils: 1 / lengthscale.
+// blocks are never read by the factorisation). ils: 1 / lengthscale. One
+// 16x16 tile per workgroup; the tile's 32 rows of X and the lengthscales
+// are staged in LDS first, so every global load is issued up front.
 __global__ __launch_bounds__(256) void k_gram(const float* __restrict__ X, int64_t n, int d,
                                               int nf, const double* __restrict__ ils,
                                               const double* __restrict__ os,
                                               const double* __restrict__ noise,
                                               double* __restrict__ A) {
+  __shared__ float xs[2][16][BO_MAX_D + 1];
+  __shared__ double il[BO_MAX_D];
   const int k = blockIdx.z;
   const int bi = blockIdx.y, bj = blockIdx.x;      // 16x16 tiles
   if ((bj >> 2) > (bi >> 2)) return;                // strictly above the 64-block diagonal
+  const int tid = threadIdx.y * 16 + threadIdx.x;
+  // rows bi*16.. (s = 0) and bj*16.. (s = 1); rows past n read as 0
+  for (int e = tid; e < 32 * d; e += 256) {
+    const int s = e / (16 * d), rem = e % (16 * d), r = rem / d, t = rem % d;
+    const int64_t row = (int64_t)(s ? bj : bi) * 16 + r;
+    xs[s][r][t] = (row < n) ? X[row * d + t] : 0.f;
+  }
+  if (tid < d) il[tid] = ils[k * d + tid];
+  __syncthreads();
   const int i = bi * 16 + threadIdx.y;
   const int j = bj * 16 + threadIdx.x;
   if (i >= nf || j >= nf) return;
@@ -59,8 +72,8 @@ __global__ __launch_bounds__(256) void k_gram(const float* __restrict__ X, int64
   if (i < n && j < n) {
     double r2 = 0.0;
     for (int t = 0; t < d; ++t) {
-      const double diff = (static_cast<double>(X[(int64_t)i * d + t]) -
-                           static_cast<double>(X[(int64_t)j * d + t])) * ils[k * d + t];
+      const double diff = (static_cast<double>(xs[0][threadIdx.y][t]) -
+                           static_cast<double>(xs[1][threadIdx.x][t])) * il[t];
       r2 = fma(diff, diff, r2);
     }
     v = matern52_d(r2, os[k]);
@@ -71,107 +84,152 @@ __global__ __launch_bounds__(256) void k_gram(const float* __restrict__ X, int64
   A[((int64_t)k * nf + i) * nf + j] = v;
 }
 
+// 1 / sqrt(d), d > 0: the hardware estimate refined by two Newton steps
+// y <- y (3 - d y^2) / 2, each of which roughly squares the relative error.
+__device__ __forceinline__ double rsqrt_d(double d) {
+  double y = __builtin_amdgcn_rsq(d);
+  const double h = 0.5 * d;
+  y = y * fma(-h * y, y, 1.5);
+  return y * fma(-h * y, y, 1.5);
+}
+
 // Factor the symmetric 64x64 block held in LDS `a` (lower triangle read) and
 // invert the factor: on return a = L (zeros above the diagonal) and
-// x = L^{-1}. One wave does the work without barriers (the other waves of the
-// workgroup only wait at the final barrier): lane c keeps column c in 64
+// x = L^{-1} (zeros above the diagonal). All four waves of the 256-thread
+// workgroup take part (every thread must call this): thread (w, c) =
+// (wave, lane) keeps rows 16w .. 16w+15 of column c of both A and X in
 // registers, indexed only by unrolled constants.
-// Factor step j: the pivot is lane j's element j (read with readlane); lane j
-// publishes its (unscaled) column, from row j on, to lcol[j] (contiguous
-// doubles); every lane c > j then subtracts L_cj times column j of L from its
-// own (broadcast LDS reads that all lanes share). Inverse step j: lane c's
-// column of X = L^{-1} is swept the same way, X_j /= L_jj then
-// X_i -= L_ij X_j for i > j, reading L from lcol.
+//
+// The factor (right-looking, unscaled) and the inverse (forward
+// substitution, one column of X per thread column) advance together, one
+// barrier per step j:
+//   before the barrier, lane j of every wave publishes its rows i > j of
+//   column j of A as it stands (A_ij = L_ij L_jj; zeros for rows <= j) and
+//   the pivot A_jj, and the wave owning row j publishes row j of X as it
+//   stands (X_jc L_jj); the buffers are double-buffered by step parity;
+//   after it, every thread takes 1 / L_jj = A_jj^{-1/2} and updates all of
+//   its rows (the zeros leave rows <= j untouched):
+//     A_ic -= A_ij A_cj / A_jj   (A_cj is zero for c <= j)
+//     X_ic -= A_ij (X_jc L_jj) / A_jj.
+// Row j of X keeps the factor L_jj until the end, where every row of X and
+// every column of A is scaled by its 1 / L_jj. Only stores sit in branches,
+// so the update is straight-line code on fixed registers.
 // A non-positive or non-finite pivot sets *flag and is replaced by 1.
-// Scratch: lcol [64][64] doubles, which is the storage of x itself (x is only
-// written after the last read of lcol), 16-byte aligned; invd [64].
-__device__ __forceinline__ double readlane_d(double v, int lane) {
-  const int64_t b = __double_as_longlong(v);
-  const int lo = __builtin_amdgcn_readlane(static_cast<int>(b), lane);
-  const int hi = __builtin_amdgcn_readlane(static_cast<int>(b >> 32), lane);
-  return __longlong_as_double((static_cast<int64_t>(hi) << 32) | static_cast<uint32_t>(lo));
-}
-
-// Makes this wave's LDS stores visible to its own later loads from other
-// lanes: without it the compiler may move those loads above the stores (lanes
-// of one wave are separate threads to the memory model).
-__device__ __forceinline__ void wave_sync_lds() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
-
-__device__ __forceinline__ void chol_inv64_wave(double (*a)[LDP], double (*x)[LDP], double* lcol,
-                                                double* invd, int* flag) {
-  const int c = threadIdx.x & 63;
-  // r holds lane c's column of the partially eliminated matrix, unscaled:
-  // after step c, r[i] (i >= c) = L_ic * L_cc, so no per-element scaling is
-  // ever needed (the scale 1/L_cc is folded into the multipliers below and
-  // applied once at the end).
-  double r[B];
-#pragma unroll
-  for (int i = 0; i < B; ++i) r[i] = a[i][c];
-  bool bad_any = false;
-#pragma unroll
-  for (int j = 0; j < B; ++j) {
-    double piv = readlane_d(r[j], j);
-    const bool bad = !(piv > 0.0) || !isfinite(piv);
-    if (bad) piv = 1.0;
-    bad_any |= bad;
-    const double inv = 1.0 / sqrt(piv);
-    double* lc = lcol + j * B;
-    if (c == j) {
-      // plain double stores (merged into 16-byte ones): the same type as the
-      // loads below, so alias analysis cannot move those above these
-#pragma unroll
-      for (int i = (j + 1) & ~1; i < B; ++i) lc[i] = r[i];
-      invd[j] = inv;
-    }
-    wave_sync_lds();
-    if (j + 1 < B) {
-      // L_ij L_cj = lc[i] * lc[c] / piv for the columns c > j still open
-      const double m = (c > j) ? lc[c] * (inv * inv) : 0.0;
-#pragma unroll
-      for (int i = j + 1; i < B; ++i) r[i] = fma(-lc[i], m, r[i]);
-    }
-  }
-  if (bad_any && c == 0) atomicOr(flag, 1);
-  wave_sync_lds();
-  // L into a (zeros above the diagonal): column c scaled by 1/L_cc
-  const double ic = invd[c];
-#pragma unroll
-  for (int i = 0; i < B; ++i) a[i][c] = (i >= c) ? r[i] * ic : 0.0;
-  // inverse, column c of X per lane: X_j /= L_jj, X_i -= L_ij X_j (i > j),
-  // with L_ij = lc[i] / L_jj
-  double xv[B];
-#pragma unroll
-  for (int i = 0; i < B; ++i) xv[i] = (i == c) ? 1.0 : 0.0;
-#pragma unroll
-  for (int j = 0; j < B; ++j) {
-    const double ij = invd[j];
-    const double xj = xv[j] * ij;
-    xv[j] = xj;
-    const double* lc = lcol + j * B;
-    const double m = xj * ij;
-#pragma unroll
-    for (int i = j + 1; i < B; ++i) xv[i] = fma(-lc[i], m, xv[i]);
-  }
-#pragma unroll
-  for (int i = 0; i < B; ++i) x[i][c] = xv[i];
-}
-
-// All threads call this; wave 0 factors and inverts (see above).
-__device__ __forceinline__ void chol_inv64(double (*a)[LDP], double (*x)[LDP], double* invd,
+// Scratch: scr holds 6 x 64 doubles, 16-byte aligned (two published columns
+// of A, two published rows of X, two pivots, the 64 values 1 / L_jj).
+__device__ __forceinline__ void chol_inv64(double (*a)[LDP], double (*x)[LDP], double* scr,
                                            int* flag) {
-  if (threadIdx.x < 64) chol_inv64_wave(a, x, &x[0][0], invd, flag);
+  const int c = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // rows 16w ..
+  double* colbuf = scr;                      // [2][64] column j of A, rows > j
+  double* rowbuf = scr + 2 * B;              // [2][64] row j of X
+  double* pivbuf = scr + 4 * B;              // [2]     A_jj
+  double* rdiag = scr + 5 * B;               // [64]    1 / L_jj
+  double r[16], xv[16];
+#pragma unroll
+  for (int t = 0; t < 16; ++t) {
+    r[t] = a[16 * w + t][c];
+    xv[t] = (16 * w + t == c) ? 1.0 : 0.0;
+  }
+  bool bad_any = false;
+  // steps j = 16 jw + jt: the row group of the pivot is a loop variable and
+  // the row within it an unrolled constant (register indices stay constant
+  // while the straight-line code stays one row group long)
+#pragma unroll 1
+  for (int jw = 0; jw < 4; ++jw) {
+#pragma unroll
+  for (int jt = 0; jt < 16; ++jt) {
+    const int j = 16 * jw + jt;
+    double* col = colbuf + (jt & 1) * B;
+    double* row = rowbuf + (jt & 1) * B;
+    if (c == j) {
+      if (w > jw) {
+#pragma unroll
+        for (int t = 0; t < 16; t += 2)
+          *reinterpret_cast<double2*>(col + 16 * w + t) = double2{r[t], r[t + 1]};
+      } else if (w < jw) {
+#pragma unroll
+        for (int t = 0; t < 16; t += 2)
+          *reinterpret_cast<double2*>(col + 16 * w + t) = double2{0.0, 0.0};
+      } else {
+#pragma unroll
+        for (int t = 0; t < 16; ++t) col[16 * w + t] = (t > jt) ? r[t] : 0.0;
+        pivbuf[jt & 1] = r[jt];
+      }
+    }
+    if (w == jw) row[c] = xv[jt];
+    __syncthreads();
+    // all three reads issued together, ahead of the pivot's arithmetic
+    const double a_jj = pivbuf[jt & 1];
+    const double a_cj = col[c];
+    const double x_jc = row[c];
+    const bool bad = !(a_jj > 0.0) || !isfinite(a_jj);
+    const double d = bad ? 1.0 : a_jj;
+    bad_any = bad_any || bad;
+    const double isd = rsqrt_d(d);
+    const double id = isd * isd;
+    const double mcol = a_cj * id;
+    const double xs = x_jc * id;
+#pragma unroll
+    for (int t = 0; t < 16; t += 2) {
+      const double2 l = *reinterpret_cast<const double2*>(col + 16 * w + t);
+      r[t] = fma(-l.x, mcol, r[t]);
+      r[t + 1] = fma(-l.y, mcol, r[t + 1]);
+      xv[t] = fma(-l.x, xs, xv[t]);
+      xv[t + 1] = fma(-l.y, xs, xv[t + 1]);
+    }
+    if (threadIdx.x == 0) rdiag[j] = isd;
+  }
+  }
+  if (bad_any && threadIdx.x == 0) atomicOr(flag, 1);
+  __syncthreads();   // rdiag is complete; every published read is done
+  const double isc = rdiag[c];
+#pragma unroll
+  for (int t = 0; t < 16; ++t) {
+    const int i = 16 * w + t;
+    a[i][c] = (i >= c) ? r[t] * isc : 0.0;
+    x[i][c] = xv[t] * rdiag[i];
+  }
   __syncthreads();
 }
 
-__device__ inline void load_block(double (*dst)[LDP], const double* src, int ld) {
-  for (int e = threadIdx.x; e < B * B; e += blockDim.x) {
-    const int i = e >> 6, c = e & 63;
-    dst[i][c] = src[(int64_t)i * ld + c];
+// Copies of 64x64 tiles between global memory (leading dimension ld) and
+// padded LDS tiles, by a 256-thread workgroup. Every load of a call is
+// issued before the first LDS store, so the latencies overlap; two tiles
+// can be fetched in one call. Transposed variants store dst[c][i] = src[i][c].
+template <bool T>
+__device__ __forceinline__ void put_tile(double (*dst)[LDP], const double (&v)[16]) {
+#pragma unroll
+  for (int k = 0; k < 16; ++k) {
+    const int e = threadIdx.x + 256 * k, i = e >> 6, c = e & 63;
+    if (T) dst[c][i] = v[k];
+    else dst[i][c] = v[k];
   }
+}
+
+__device__ __forceinline__ void get_tile(double (&v)[16], const double* src, int ld) {
+#pragma unroll
+  for (int k = 0; k < 16; ++k) {
+    const int e = threadIdx.x + 256 * k, i = e >> 6, c = e & 63;
+    v[k] = src[(int64_t)i * ld + c];
+  }
+}
+
+template <bool T0 = false>
+__device__ inline void load_block(double (*dst)[LDP], const double* src, int ld) {
+  double v[16];
+  get_tile(v, src, ld);
+  put_tile<T0>(dst, v);
+}
+
+template <bool T0, bool T1>
+__device__ inline void load_blocks(double (*d0)[LDP], const double* s0, double (*d1)[LDP],
+                                   const double* s1, int ld) {
+  double v0[16], v1[16];
+  get_tile(v0, s0, ld);
+  get_tile(v1, s1, ld);
+  put_tile<T0>(d0, v0);
+  put_tile<T1>(d1, v1);
 }
 
 __device__ inline void store_block(double* dst, int ld, const double (*srcb)[LDP]) {
@@ -187,12 +245,12 @@ __global__ __launch_bounds__(256) void k_factor_first(double* __restrict__ A,
                                                       int* __restrict__ flag) {
   __shared__ double a[B][LDP];
   __shared__ __align__(16) double x[B][LDP];
-  __shared__ double invd[B];
+  __shared__ __align__(16) double scr[6 * B];
   double* Ak = A + (int64_t)blockIdx.x * nf * nf;
   double* Wk = W + (int64_t)blockIdx.x * nf * nf;
   load_block(a, Ak, nf);
   __syncthreads();
-  chol_inv64(a, x, invd, flag);
+  chol_inv64(a, x, scr, flag);
   store_block(Ak, nf, a);
   store_block(Wk, nf, x);
 }
@@ -233,16 +291,13 @@ __global__ __launch_bounds__(256) void k_panel(double* __restrict__ A, double* _
   if (t < T) {
     const int ib = kb + 1 + t;
     dst = Ak + (int64_t)ib * B * nf + o;
-    load_block(p, dst, nf);                 // P = A[ib][kb]
-    load_block(q, D, nf);                   // Q[c][s] = D[c][s]  ->  P D^T
+    // P = A[ib][kb]; Q[c][s] = D[c][s]  ->  P D^T
+    load_blocks<false, false>(p, dst, q, D, nf);
   } else {
     const int jb = t - T;
     dst = Wk + (int64_t)o * nf + jb * B;
-    load_block(p, D, nf);                   // P = D
-    for (int e = tid; e < B * B; e += 256) {  // Q = R^T  ->  D R
-      const int i = e >> 6, c = e & 63;
-      q[c][i] = dst[(int64_t)i * nf + c];
-    }
+    // P = D; Q = R^T  ->  D R
+    load_blocks<false, true>(p, D, q, dst, nf);
   }
   __syncthreads();
   double acc[4][4] = {};
@@ -260,7 +315,7 @@ __global__ __launch_bounds__(256) void k_update(double* __restrict__ A, double* 
                                                 int nf, int kb, int* __restrict__ flag) {
   __shared__ double p[B][LDP];
   __shared__ __align__(16) double q[B][LDP];
-  __shared__ double invd[B];
+  __shared__ __align__(16) double scr[6 * B];
   const int k = blockIdx.y;
   const int nbk = nf / B;
   const int T = nbk - kb - 1;
@@ -278,19 +333,16 @@ __global__ __launch_bounds__(256) void k_update(double* __restrict__ A, double* 
     while (r * (r + 1) / 2 > t) --r;
     const int ib = kb + 1 + r;
     const int cb = kb + 1 + (t - r * (r + 1) / 2);
-    load_block(p, Ak + (int64_t)ib * B * nf + o, nf);       // L[ib][kb]
-    load_block(q, Ak + (int64_t)cb * B * nf + o, nf);       // L[cb][kb]
+    load_blocks<false, false>(p, Ak + (int64_t)ib * B * nf + o,      // L[ib][kb]
+                              q, Ak + (int64_t)cb * B * nf + o, nf); // L[cb][kb]
     dst = Ak + (int64_t)ib * B * nf + cb * B;
   } else {
     // R tile (ib, jb): ib > kb, jb <= kb:  W[ib][jb] -= L[ib][kb] W[kb][jb]
     const int u = t - nsyrk;
     const int ib = kb + 1 + u / (kb + 1);
     const int jb = u % (kb + 1);
-    load_block(p, Ak + (int64_t)ib * B * nf + o, nf);       // L[ib][kb]
-    for (int e = tid; e < B * B; e += 256) {                 // q = W[kb][jb]^T
-      const int i = e >> 6, c = e & 63;
-      q[c][i] = Wk[(int64_t)(o + i) * nf + jb * B + c];
-    }
+    load_blocks<false, true>(p, Ak + (int64_t)ib * B * nf + o,        // L[ib][kb]
+                             q, Wk + (int64_t)o * nf + jb * B, nf);   // q = W[kb][jb]^T
     dst = Wk + (int64_t)ib * B * nf + jb * B;
   }
   __syncthreads();
@@ -312,7 +364,7 @@ __global__ __launch_bounds__(256) void k_update(double* __restrict__ A, double* 
 #pragma unroll
       for (int c = 0; c < 4; ++c) p[ty * 4 + rr][tx * 4 + c] = acc[rr][c];
     __syncthreads();
-    chol_inv64(p, q, invd, flag);
+    chol_inv64(p, q, scr, flag);
     const int o1 = o + B;
     store_block(dst, nf, p);
     store_block(Wk + (int64_t)o1 * nf + o1, nf, q);
