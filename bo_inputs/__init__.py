@@ -42,9 +42,18 @@ fp32 — a latency cap and a quality floor that 70% of the observations meet
 on each objective. ``None`` in place of a quantile leaves that objective
 unconstrained (-inf).
 
+Composite-kernel hyperparameters (for the paper's additive surrogate): the
+routing features are the first d/4 coordinates (4 for configs 2 and 3, the
+routing fractions), the rest are deployment features; output scales 0.7
+(routing Matern-5/2), 0.3 (preference-weighted deployment Matern-3/2) and
+0.05 (interaction); preference slopes 0.08 * U[0,1] per objective and
+deployment dimension (stream 6), so the weights exp(p . c) stay within
+[1, e^{0.96}]. Lengthscales are the workload's.
+
 Random streams: ``numpy.random.Generator(PCG64(SeedSequence(seed,
 spawn_key=(family, stream))))`` with streams 0 X, 1 candidates, 2 noise,
-3 lengthscales, 4 weights w, 5 base samples Z; family is the config number
+3 lengthscales, 4 weights w, 5 base samples Z, 6 preference slopes; family is
+the config number
 except that configs 2 and 3 share family 2. Candidates are drawn row by row,
 so a prefix of a larger M equals the smaller-M draw.
 """
@@ -56,7 +65,7 @@ from typing import Optional
 import numpy as np
 
 __all__ = ["CONFIGS", "Workload", "make_config", "near_data_candidates",
-           "feasibility_thresholds"]
+           "feasibility_thresholds", "CompositeParams", "composite_hyperparameters"]
 
 # (m, q, d, n, M, S, noise_sd, family)
 CONFIGS = {
@@ -71,7 +80,7 @@ OUTPUTSCALE = 1.0
 NOISE_VAR = 1e-4
 REF_OFFSET = 0.1
 
-STREAM_X, STREAM_CAND, STREAM_NOISE, STREAM_LS, STREAM_W, STREAM_Z = range(6)
+STREAM_X, STREAM_CAND, STREAM_NOISE, STREAM_LS, STREAM_W, STREAM_Z, STREAM_PREF = range(7)
 
 
 @dataclass
@@ -199,3 +208,23 @@ def feasibility_thresholds(wl: Workload, quantiles=0.3) -> np.ndarray:
     for k, qk in enumerate(qs):
         out[k] = -np.inf if qk is None else np.quantile(Y[:, k], qk)
     return out.astype(np.float32)
+
+
+@dataclass
+class CompositeParams:
+    d_route: int
+    s_route: np.ndarray      # [m] fp32
+    s_dep: np.ndarray        # [m] fp32
+    s_int: np.ndarray        # [m] fp32
+    pref: np.ndarray         # [m, d - d_route] fp32
+
+
+def composite_hyperparameters(wl: Workload, d_route: Optional[int] = None) -> CompositeParams:
+    """Seeded hyperparameters of the composite kernel for a workload."""
+    dr = max(1, wl.d // 4) if d_route is None else int(d_route)
+    if not 1 <= dr < wl.d:
+        raise ValueError("need 1 <= d_route < d")
+    fam = CONFIGS[wl.cfg]["family"]
+    pref = 0.08 * _rng(wl.seed, fam, STREAM_PREF).random((wl.m, wl.d - dr))
+    f = lambda v: np.full(wl.m, v, dtype=np.float32)
+    return CompositeParams(dr, f(0.7), f(0.3), f(0.05), pref.astype(np.float32))

@@ -9,7 +9,8 @@
  *   bo_fit    — condition one GP per objective on the observations
  *               (workflow step (i), "Surrogate model fitting"; ARD
  *               Matern-5/2 kernel with an output scale, implementation
- *               section "MOBO optimization kernels").
+ *               section "MOBO optimization kernels"); bo_fit_composite
+ *               with the paper's additive, preference-weighted kernel.
  *   bo_score  — GP posterior of every candidate plus Monte-Carlo expected
  *               hypervolume improvement against the Pareto front
  *               (workflow step (ii) and the "Constrained qNEHVI" paragraph:
@@ -99,6 +100,43 @@ typedef enum {
 bo_status bo_fit(const float* X, const float* Y, int64_t n, int32_t d, int32_t m,
                  const float* lengthscale, const float* outputscale,
                  const float* noise, void* stream, bo_model* out);
+
+/*
+ * bo_fit_composite — bo_fit with the paper's composite surrogate kernel.
+ *
+ * Paper: paragraphs "Additive kernels" and S5 "Model-GPU preference
+ * encoding" of the online phase, and the kernel list of the implementation
+ * section (ARD Matern-5/2 on the routing features, ARD Matern-3/2 on the
+ * deployment features wrapped in the preference-weighted kernel, their
+ * product as a low-weight interaction, each in its own scale kernel).
+ *
+ * With x = (tau, c): tau the first d_route coordinates (routing), c the
+ * other d - d_route (deployment), and for objective k
+ *   k(x, x') = s_route[k] M52(r_tau) + s_dep[k] w(c) w(c') M32(r_c)
+ *              + s_int[k] M52(r_tau) M32(r_c),
+ *   M52(r) = (1 + sqrt5 r + 5/3 r^2) exp(-sqrt5 r),
+ *   M32(r) = (1 + sqrt3 r) exp(-sqrt3 r),
+ *   r_tau, r_c the lengthscale-scaled distances over the two groups,
+ *   w(c) = exp(sum_j pref[k][j] c_j)   (pref[k][j] = beta_k times the
+ *          preference of the GPU type that deployment coordinate j counts).
+ * The rest is as bo_fit: K = [k(x_i, x_j)] + eta I in fp64, L^{-1} and
+ * alpha kept for scoring. The prior variance of a point is
+ * s_route + s_dep w(c)^2 + s_int.
+ *
+ * d_route     1 <= d_route < d; the padded routing and deployment groups
+ *             (each rounded up to a multiple of 4) must fit BO_MAX_D
+ * lengthscale host [m][d] > 0 (routing then deployment coordinates)
+ * scale_route host [m] > 0;  scale_dep, scale_int host [m] >= 0
+ * pref        host [m][d - d_route], finite
+ * Other arguments, behaviour and errors as bo_fit (CAPACITY when the padded
+ * groups exceed BO_MAX_D). Models fitted this way score q = 1 batches only
+ * (bo_score returns INVALID_ARGUMENT for q > 1).
+ */
+bo_status bo_fit_composite(const float* X, const float* Y, int64_t n, int32_t d, int32_t m,
+                           int32_t d_route, const float* lengthscale,
+                           const float* scale_route, const float* scale_dep,
+                           const float* scale_int, const float* pref, const float* noise,
+                           void* stream, bo_model* out);
 
 /*
  * bo_score — posterior plus Monte-Carlo (q)EHVI for M candidates.

@@ -25,13 +25,15 @@ workflow, the constrained qNEHVI paragraph, and the implementation section
 All arithmetic is fp64 on fp32-rounded inputs. Readings of points the paper
 leaves open are listed in each function's docstring.
 """
-from .gp import (GPModel, matern52, scaled_distance, fit, posterior,
+from .gp import (GPModel, Composite, matern52, matern32, composite_cov, pref_weight,
+                 scaled_distance, fit, posterior,
                  chol_psd, NotPositiveDefinite)
 from .pareto import nondominated, pareto_front, boxes_2d, boxes_3d, box_decomposition
 from .acq import hvi, qhvi, feasible, ehvi_q1, qehvi, score, argmax
 
 __all__ = [
-    "GPModel", "matern52", "scaled_distance", "fit", "posterior", "chol_psd",
+    "GPModel", "Composite", "matern52", "matern32", "composite_cov", "pref_weight",
+    "scaled_distance", "fit", "posterior", "chol_psd",
     "NotPositiveDefinite", "nondominated", "pareto_front", "boxes_2d",
     "boxes_3d", "box_decomposition", "hvi", "qhvi", "feasible", "ehvi_q1", "qehvi",
     "score", "argmax",

@@ -5,6 +5,13 @@ Paper: "Overall MOBO workflow" step (i) fits one GP per objective
 with an ARD Matern kernel of smoothness 5/2 wrapped in a scale kernel, in
 double precision. Hyperparameters are given here, not learned.
 
+The paper's own surrogate (paragraphs "Additive kernels" and S5 "Model-GPU
+preference encoding", and the implementation section's list of kernels) is
+the composite kernel of ``composite_cov``: an ARD Matern-5/2 term on the
+routing features, a preference-weighted ARD Matern-3/2 term on the
+deployment features and their product as a low-weight interaction, each with
+its own output scale.
+
 Readings of points the paper does not state:
 
 * Matern-5/2 is the standard form k(rho) = s (1 + sqrt5 rho + 5/3 rho^2)
@@ -16,17 +23,26 @@ Readings of points the paper does not state:
   predictive variance); variance is clamped at 0.
 * The q x q batch covariance is factorised without jitter; a Schur pivot
   <= 1e-10 * s zeroes that column of the factor.
+* Composite kernel (readings): the routing features are the first d_route
+  coordinates and the deployment features the rest; the interaction is the
+  product of the two unscaled Matern correlations with its own scale (the
+  preference weight wraps only the deployment term, as the paper writes
+  k~_c = w(c) w(c*) k_c); the weight is w(c) = exp(sum_j p_j c_j) with
+  p_j = beta * (preference of the GPU type whose count dimension j encodes)
+  folded into one slope per objective and deployment dimension. The
+  pivot scale s of the batch factorisation is the sum of the three scales.
 """
 from __future__ import annotations
 
 import math
 from dataclasses import dataclass, field
-from typing import List
+from typing import List, Optional
 
 import numpy as np
 from scipy.linalg import solve_triangular
 
 SQRT5 = math.sqrt(5.0)
+SQRT3 = math.sqrt(3.0)
 PIVOT_RTOL = 1e-10
 
 
@@ -49,6 +65,49 @@ def matern52(rho: np.ndarray, s: float) -> np.ndarray:
     return float(s) * (1.0 + SQRT5 * rho + (5.0 / 3.0) * rho * rho) * np.exp(-SQRT5 * rho)
 
 
+def matern32(rho: np.ndarray, s: float) -> np.ndarray:
+    """Matern nu=3/2 covariance: s (1 + sqrt3 rho) exp(-sqrt3 rho)
+    (Rasmussen & Williams 2006, eq. 4.17)."""
+    rho = np.asarray(rho, dtype=np.float64)
+    return float(s) * (1.0 + SQRT3 * rho) * np.exp(-SQRT3 * rho)
+
+
+@dataclass
+class Composite:
+    """Hyperparameters of the composite kernel for all objectives.
+
+    d_route: number of routing features (the first coordinates);
+    s_route, s_dep, s_int [m]: output scales of the routing term, the
+    preference-weighted deployment term and the interaction;
+    pref [m, d - d_route]: log-weight slopes of the deployment features."""
+    d_route: int
+    s_route: np.ndarray
+    s_dep: np.ndarray
+    s_int: np.ndarray
+    pref: np.ndarray
+
+
+def pref_weight(C: np.ndarray, p: np.ndarray) -> np.ndarray:
+    """w(c) = exp(sum_j p_j c_j) for deployment features C [N, d_c]."""
+    return np.exp(np.asarray(C, dtype=np.float64) @ np.asarray(p, dtype=np.float64))
+
+
+def composite_cov(U, V, ls, comp: Composite, k: int) -> np.ndarray:
+    """k(u, v) = s_route M52(rho_route) + s_dep w(u_c) w(v_c) M32(rho_dep)
+                 + s_int M52(rho_route) M32(rho_dep)
+    for objective k; M52, M32 unit-scale Matern correlations, rho_* the
+    ARD-scaled distances over the routing / deployment coordinates."""
+    U = np.asarray(U, dtype=np.float64)
+    V = np.asarray(V, dtype=np.float64)
+    dr = comp.d_route
+    k5 = matern52(scaled_distance(U[:, :dr], V[:, :dr], ls[:dr]), 1.0)
+    k3 = matern32(scaled_distance(U[:, dr:], V[:, dr:], ls[dr:]), 1.0)
+    wu = pref_weight(U[:, dr:], comp.pref[k])
+    wv = pref_weight(V[:, dr:], comp.pref[k])
+    return (comp.s_route[k] * k5 + comp.s_dep[k] * np.outer(wu, wv) * k3
+            + comp.s_int[k] * k5 * k3)
+
+
 @dataclass
 class GPModel:
     X: np.ndarray            # [n, d]
@@ -58,6 +117,29 @@ class GPModel:
     eta: np.ndarray          # [m]
     L: List[np.ndarray] = field(default_factory=list)      # m x [n, n] lower
     alpha: List[np.ndarray] = field(default_factory=list)  # m x [n]
+    comp: Optional[Composite] = None                       # None: Matern-5/2
+
+    def cov(self, k: int, U, V) -> np.ndarray:
+        """Covariance matrix of objective k between point sets U and V."""
+        if self.comp is None:
+            return matern52(scaled_distance(U, V, self.ls[k]), self.s[k])
+        return composite_cov(U, V, self.ls[k], self.comp, k)
+
+    def pair_cov(self, k: int, U, V) -> np.ndarray:
+        """k(U[i], V[i]) for paired rows (the diagonal of cov(k, U, V))."""
+        U = np.asarray(U, dtype=np.float64)
+        V = np.asarray(V, dtype=np.float64)
+
+        def rho(a, b, ls):
+            diff = (a - b) / ls
+            return np.sqrt(np.sum(diff * diff, axis=1))
+        if self.comp is None:
+            return matern52(rho(U, V, self.ls[k]), self.s[k])
+        c, dr, ls = self.comp, self.comp.d_route, self.ls[k]
+        k5 = matern52(rho(U[:, :dr], V[:, :dr], ls[:dr]), 1.0)
+        k3 = matern32(rho(U[:, dr:], V[:, dr:], ls[dr:]), 1.0)
+        w = pref_weight(U[:, dr:], c.pref[k]) * pref_weight(V[:, dr:], c.pref[k])
+        return c.s_route[k] * k5 + c.s_dep[k] * w * k3 + c.s_int[k] * k5 * k3
 
     @property
     def n(self) -> int:
@@ -68,22 +150,29 @@ class GPModel:
         return self.Y.shape[1]
 
 
-def fit(X, Y, ls, s, eta) -> GPModel:
+def fit(X, Y, ls, s, eta, composite: Optional[Composite] = None) -> GPModel:
     """Condition one GP per objective on (X, Y[:, k]).
 
     K_k = [k_k(x_i, x_j)] + eta_k I;  L_k = chol(K_k) (lower);
     alpha_k = L_k^T \\ (L_k \\ y_k).
+    k_k is the ARD Matern-5/2 with output scale s_k, or the composite kernel
+    when ``composite`` is given (then ``s`` is ignored).
     Raises NotPositiveDefinite when a factorisation fails.
     """
     X = np.asarray(X, dtype=np.float64)
     Y = np.asarray(Y, dtype=np.float64)
     ls = np.asarray(ls, dtype=np.float64).reshape(Y.shape[1], X.shape[1])
-    s = np.asarray(s, dtype=np.float64).reshape(-1)
     eta = np.asarray(eta, dtype=np.float64).reshape(-1)
-    model = GPModel(X=X, Y=Y, ls=ls, s=s, eta=eta)
+    if composite is not None:
+        c = composite
+        composite = Composite(int(c.d_route), *[np.asarray(v, dtype=np.float64) for v in
+                                                (c.s_route, c.s_dep, c.s_int, c.pref)])
+        s = composite.s_route + composite.s_dep + composite.s_int
+    s = np.asarray(s, dtype=np.float64).reshape(-1)
+    model = GPModel(X=X, Y=Y, ls=ls, s=s, eta=eta, comp=composite)
     n = X.shape[0]
     for k in range(Y.shape[1]):
-        K = matern52(scaled_distance(X, X, ls[k]), s[k]) + eta[k] * np.eye(n)
+        K = model.cov(k, X, X) + eta[k] * np.eye(n)
         try:
             L = np.linalg.cholesky(K)
         except np.linalg.LinAlgError as e:  # pragma: no cover - message path
@@ -115,7 +204,7 @@ def posterior(model: GPModel, cand: np.ndarray, chunk: int = 512):
         P = cand[b0:b1].reshape(-1, d)
         nb = b1 - b0
         for k in range(m):
-            Ks = matern52(scaled_distance(P, model.X, model.ls[k]), model.s[k])
+            Ks = model.cov(k, P, model.X)
             mu[b0:b1, :, k] = (Ks @ model.alpha[k]).reshape(nb, q)
             V = solve_triangular(model.L[k], Ks.T, lower=True)   # [n, nb*q]
             Vb = V.T.reshape(nb, q, -1)
@@ -123,9 +212,7 @@ def posterior(model: GPModel, cand: np.ndarray, chunk: int = 512):
             prior = np.empty((nb, q, q))
             for a in range(q):
                 for c in range(q):
-                    diff = (Pb[:, a, :] - Pb[:, c, :]) / model.ls[k]
-                    rho = np.sqrt(np.sum(diff * diff, axis=1))
-                    prior[:, a, c] = matern52(rho, model.s[k])
+                    prior[:, a, c] = model.pair_cov(k, Pb[:, a, :], Pb[:, c, :])
             S = prior - Vb @ np.transpose(Vb, (0, 2, 1))
             idx = np.arange(q)
             S[:, idx, idx] = np.maximum(S[:, idx, idx], 0.0)

@@ -6,7 +6,7 @@ current stream. There is no CPU fallback: if the library is missing or a
 tensor is not on the GPU, the call raises.
 
 Functions mirror the C ABI in ``include/bo.h``:
-``fit``, ``score`` (``bo_score``, or ``bo_score_constrained`` when feasibility
+``fit`` (``bo_fit``), ``fit_composite`` (``bo_fit_composite``), ``score`` (``bo_score``, or ``bo_score_constrained`` when feasibility
 thresholds are given), ``argmax``, ``cholesky_test`` (device) and
 ``pareto_front``, ``box_decomposition`` (host geometry, no GPU needed).
 """
@@ -18,7 +18,7 @@ from typing import Optional
 
 import numpy as np
 
-__all__ = ["BoError", "Model", "lib", "lib_path", "fit", "score", "argmax",
+__all__ = ["BoError", "Model", "lib", "lib_path", "fit", "fit_composite", "score", "argmax",
            "cholesky_test", "profile_enable", "profile_read", "measure_peak", "pareto_front", "box_decomposition", "STATUS",
            "MAX_N", "MAX_D", "MAX_S", "MAX_BOXES"]
 
@@ -57,6 +57,9 @@ def lib() -> ctypes.CDLL:
     vp, i64, i32, fp = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p
     L.bo_fit.argtypes = [vp, vp, i64, i32, i32, fp, fp, fp, vp, ctypes.POINTER(vp)]
     L.bo_fit.restype = ctypes.c_int
+    L.bo_fit_composite.argtypes = [vp, vp, i64, i32, i32, i32, fp, fp, fp, fp, fp, fp, vp,
+                                   ctypes.POINTER(vp)]
+    L.bo_fit_composite.restype = ctypes.c_int
     L.bo_score.argtypes = [vp, vp, i64, i32, fp, vp, i32, vp, vp, vp, vp]
     L.bo_score.restype = ctypes.c_int
     L.bo_score_constrained.argtypes = [vp, vp, i64, i32, fp, fp, vp, i32, vp, vp, vp, vp]
@@ -167,6 +170,29 @@ def fit(X, Y, lengthscale, outputscale, noise, stream=None) -> Model:
                       ls.ctypes.data_as(ctypes.c_void_p), os_.ctypes.data_as(ctypes.c_void_p),
                       nz.ctypes.data_as(ctypes.c_void_p), _stream(stream), ctypes.byref(h))
     _check(st, "bo_fit")
+    return Model(h.value, n, d, m)
+
+
+def fit_composite(X, Y, d_route, lengthscale, scale_route, scale_dep, scale_int, pref, noise,
+                  stream=None) -> Model:
+    """bo_fit_composite: the composite kernel (routing Matern-5/2 +
+    preference-weighted deployment Matern-3/2 + interaction). X [n, d],
+    Y [n, m] fp32 GPU tensors; hyperparameters on host (pref [m, d - d_route])."""
+    import torch
+    n, d = X.shape
+    m = Y.shape[1]
+    ls = _host_f32(lengthscale, (m, d), "lengthscale")
+    sr = _host_f32(scale_route, (m,), "scale_route")
+    sd = _host_f32(scale_dep, (m,), "scale_dep")
+    si = _host_f32(scale_int, (m,), "scale_int")
+    pf = _host_f32(pref, (m, max(d - int(d_route), 0)), "pref")
+    nz = _host_f32(noise, (m,), "noise")
+    h = ctypes.c_void_p()
+    p = lambda a: a.ctypes.data_as(ctypes.c_void_p)
+    st = lib().bo_fit_composite(_dev(X, "X", torch.float32), _dev(Y, "Y", torch.float32), n, d,
+                                m, int(d_route), p(ls), p(sr), p(sd), p(si), p(pf), p(nz),
+                                _stream(stream), ctypes.byref(h))
+    _check(st, "bo_fit_composite")
     return Model(h.value, n, d, m)
 
 

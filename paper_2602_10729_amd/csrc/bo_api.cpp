@@ -191,7 +191,7 @@ struct FitScratch {
 // object). The caller may have used the model on several streams, so wait
 // for the whole device before handing memory back to the pool.
 void release_buffers(Model* M) {
-  if (M->Xs || M->invls || M->alpha || M->Lp || M->ws || M->d_boxes)
+  if (M->Xs || M->invls || M->alpha || M->Lp || M->ws || M->d_boxes || M->wts || M->pref)
     (void)hipDeviceSynchronize();
   pfree(M->Xs, nullptr);
   pfree(M->invls, nullptr);
@@ -199,6 +199,8 @@ void release_buffers(Model* M) {
   pfree(M->Lp, nullptr);
   pfree(M->ws, nullptr);
   pfree(M->d_boxes, nullptr);
+  pfree(M->wts, nullptr);
+  pfree(M->pref, nullptr);
 }
 
 // Phase timing (bo_profile_enable / bo_profile_read).
@@ -310,24 +312,56 @@ bo_status bo_model_front_indices(bo_model model, int32_t* idx_host, int32_t cap)
   return BO_OK;
 }
 
-bo_status bo_fit(const float* X, const float* Y, int64_t n, int32_t d, int32_t m,
-                 const float* lengthscale, const float* outputscale, const float* noise,
-                 void* stream, bo_model* out) {
-  if (!out) return fail(BO_ERR_INVALID_ARGUMENT, "bo_fit: out is NULL");
+}  // extern "C"
+
+namespace {
+
+// Composite-kernel hyperparameters as passed to bo_fit_composite (host).
+struct CompositeSpec {
+  int dr;
+  const float* s_dep;
+  const float* s_int;
+  const float* pref;   // [m][d - dr]
+};
+
+bo_status fit_impl(const char* who, const float* X, const float* Y, int64_t n, int32_t d,
+                   int32_t m, const float* lengthscale, const float* outputscale,
+                   const float* noise, const CompositeSpec* comp, void* stream,
+                   bo_model* out) {
+  const std::string W(who);
+  if (!out) return fail(BO_ERR_INVALID_ARGUMENT, W + ": out is NULL");
   if (!lengthscale || !outputscale || !noise)
-    return fail(BO_ERR_INVALID_ARGUMENT, "bo_fit: NULL hyperparameter pointer");
+    return fail(BO_ERR_INVALID_ARGUMENT, W + ": NULL hyperparameter pointer");
   if (n < 1 || d < 1 || (m != 2 && m != 3))
-    return fail(BO_ERR_INVALID_ARGUMENT, "bo_fit: need n >= 1, d >= 1, m in {2,3}");
+    return fail(BO_ERR_INVALID_ARGUMENT, W + ": need n >= 1, d >= 1, m in {2,3}");
   if (n > BO_MAX_N || d > BO_MAX_D)
-    return fail(BO_ERR_CAPACITY, "bo_fit: n or d beyond compiled limits");
+    return fail(BO_ERR_CAPACITY, W + ": n or d beyond compiled limits");
   if (!all_finite(lengthscale, (size_t)m * d) || !all_finite(outputscale, m) ||
       !all_finite(noise, m))
-    return fail(BO_ERR_NONFINITE_INPUT, "bo_fit: non-finite hyperparameter");
+    return fail(BO_ERR_NONFINITE_INPUT, W + ": non-finite hyperparameter");
   for (int i = 0; i < m * d; ++i)
-    if (!(lengthscale[i] > 0.f)) return fail(BO_ERR_INVALID_ARGUMENT, "bo_fit: lengthscale <= 0");
+    if (!(lengthscale[i] > 0.f)) return fail(BO_ERR_INVALID_ARGUMENT, W + ": lengthscale <= 0");
   for (int k = 0; k < m; ++k) {
-    if (!(outputscale[k] > 0.f)) return fail(BO_ERR_INVALID_ARGUMENT, "bo_fit: outputscale <= 0");
-    if (!(noise[k] >= 0.f)) return fail(BO_ERR_INVALID_ARGUMENT, "bo_fit: noise < 0");
+    if (!(outputscale[k] > 0.f)) return fail(BO_ERR_INVALID_ARGUMENT, W + ": outputscale <= 0");
+    if (!(noise[k] >= 0.f)) return fail(BO_ERR_INVALID_ARGUMENT, W + ": noise < 0");
+  }
+  int dr = 0, dr4 = 0, dx = (d + 3) / 4 * 4;
+  if (comp) {
+    dr = comp->dr;
+    if (dr < 1 || dr >= d)
+      return fail(BO_ERR_INVALID_ARGUMENT, W + ": need 1 <= d_route < d");
+    if (!comp->s_dep || !comp->s_int || !comp->pref)
+      return fail(BO_ERR_INVALID_ARGUMENT, W + ": NULL hyperparameter pointer");
+    if (!all_finite(comp->s_dep, m) || !all_finite(comp->s_int, m) ||
+        !all_finite(comp->pref, (size_t)m * (d - dr)))
+      return fail(BO_ERR_NONFINITE_INPUT, W + ": non-finite hyperparameter");
+    for (int k = 0; k < m; ++k)
+      if (!(comp->s_dep[k] >= 0.f) || !(comp->s_int[k] >= 0.f))
+        return fail(BO_ERR_INVALID_ARGUMENT, W + ": scale_dep / scale_int < 0");
+    dr4 = (dr + 3) / 4;
+    dx = 4 * dr4 + (d - dr + 3) / 4 * 4;
+    if (dx > BO_MAX_D)
+      return fail(BO_ERR_CAPACITY, W + ": padded routing + deployment groups exceed BO_MAX_D");
   }
   bo_status s;
   if ((s = check_dev(X, sizeof(float) * n * d, "X")) != BO_OK) return s;
@@ -335,16 +369,21 @@ bo_status bo_fit(const float* X, const float* Y, int64_t n, int32_t d, int32_t m
   hipStream_t st = static_cast<hipStream_t>(stream);
 
   bo_model_s* h = new (std::nothrow) bo_model_s();
-  if (!h) return fail(BO_ERR_OUT_OF_MEMORY, "bo_fit: host allocation");
+  if (!h) return fail(BO_ERR_OUT_OF_MEMORY, W + ": host allocation");
   Model* M = &h->m;
   (void)hipGetDevice(&M->device);
   M->n = n; M->d = d; M->m = m;
   M->n_pad = static_cast<int>((n + kBlk - 1) / kBlk) * kBlk;
   M->nb = M->n_pad / kBlk;
-  M->dx = (d + 3) / 4 * 4;
+  M->dx = dx;
+  M->dr = dr; M->dr4 = dr4;
   M->ls.assign(lengthscale, lengthscale + (size_t)m * d);
   M->os.assign(outputscale, outputscale + m);
   M->noise.assign(noise, noise + m);
+  if (comp) {
+    M->s_dep.assign(comp->s_dep, comp->s_dep + m);
+    M->s_int.assign(comp->s_int, comp->s_int + m);
+  }
 
   auto bail = [&](bo_status st_) {
     release_buffers(M);
@@ -353,35 +392,54 @@ bo_status bo_fit(const float* X, const float* Y, int64_t n, int32_t d, int32_t m
   };
 
   const int nf = static_cast<int>((n + kFitBlk - 1) / kFitBlk) * kFitBlk;
+  const int dc = d - dr;
   M->lp_per_obj = (size_t)posterior_frag_blocks(M->nb) * 512;   // 2 KiB per block
   FitScratch fs;
   fs.st = st;
+  // fp64 hyperparameters: [1/ls m*d][os m][noise m] (+ [s_dep m][s_int m][pref m*dc])
+  const size_t nhyp = (size_t)m * d + 2 * m + (comp ? 2 * m + (size_t)m * dc : 0);
   if ((s = palloc(&fs.A, (size_t)m * nf * nf, st, "fit matrix")) != BO_OK) return bail(s);
   if ((s = palloc(&fs.W, (size_t)m * nf * nf, st, "fit inverse")) != BO_OK) return bail(s);
-  if ((s = palloc(&fs.hyp, (size_t)m * d + 2 * m, st, "hyperparameters")) != BO_OK) return bail(s);
+  if ((s = palloc(&fs.hyp, nhyp, st, "hyperparameters")) != BO_OK) return bail(s);
   if ((s = palloc(&fs.tmp, (size_t)m * nf, st, "fit vector")) != BO_OK) return bail(s);
   if ((s = palloc(&fs.flag, 1, st, "flag")) != BO_OK) return bail(s);
   if ((s = palloc(&M->Xs, (size_t)m * M->n_pad * M->dx, st, "scaled X")) != BO_OK) return bail(s);
   if ((s = palloc(&M->invls, (size_t)m * M->dx, st, "inverse lengthscales")) != BO_OK) return bail(s);
   if ((s = palloc(&M->alpha, (size_t)m * M->n_pad, st, "alpha")) != BO_OK) return bail(s);
   if ((s = palloc(&M->Lp, (size_t)m * M->lp_per_obj, st, "packed inverse")) != BO_OK) return bail(s);
+  if (comp) {
+    if ((s = palloc(&M->wts, (size_t)m * M->n_pad, st, "preference weights")) != BO_OK) return bail(s);
+    if ((s = palloc(&M->pref, (size_t)m * dc, st, "preference slopes")) != BO_OK) return bail(s);
+  }
 
-  std::vector<double> hyp((size_t)m * d + 2 * m);
+  std::vector<double> hyp(nhyp);
   for (int i = 0; i < m * d; ++i) hyp[i] = 1.0 / static_cast<double>(lengthscale[i]);
   for (int k = 0; k < m; ++k) {
     hyp[(size_t)m * d + k] = outputscale[k];
     hyp[(size_t)m * d + m + k] = noise[k];
+    if (comp) {
+      hyp[(size_t)m * d + 2 * m + k] = comp->s_dep[k];
+      hyp[(size_t)m * d + 3 * m + k] = comp->s_int[k];
+    }
   }
+  if (comp)
+    for (size_t i = 0; i < (size_t)m * dc; ++i) hyp[(size_t)m * d + 4 * m + i] = comp->pref[i];
+  // per-slot inverse lengthscales (zero for padding slots)
   std::vector<float> invls((size_t)m * M->dx, 0.f);
   for (int k = 0; k < m; ++k)
-    for (int t = 0; t < d; ++t) invls[(size_t)k * M->dx + t] = 1.0f / lengthscale[k * d + t];
+    for (int t = 0; t < M->dx; ++t) {
+      const int c = slot_dim(t, d, dr, dr4);
+      if (c >= 0) invls[(size_t)k * M->dx + t] = 1.0f / lengthscale[k * d + c];
+    }
 
-  // pinned staging: [hyperparameters (fp64)][1/lengthscale (fp32)][flag][Y]
+  // pinned staging: [hyperparameters (fp64)][1/lengthscale (fp32)][pref (fp32)][flag][Y]
   DeviceState* DS = device_state(M->device);
-  if (!DS) return bail(fail(BO_ERR_DEVICE, "bo_fit: device index out of range"));
+  if (!DS) return bail(fail(BO_ERR_DEVICE, W + ": device index out of range"));
   std::lock_guard<std::mutex> stage_lock(DS->fit_mu);
   const size_t off_inv = sizeof(double) * hyp.size();
-  const size_t off_flag = (off_inv + sizeof(float) * invls.size() + 15) / 16 * 16;
+  const size_t off_pref = off_inv + sizeof(float) * invls.size();
+  const size_t npref = comp ? (size_t)m * dc : 0;
+  const size_t off_flag = (off_pref + sizeof(float) * npref + 15) / 16 * 16;
   const size_t off_y = off_flag + 16;
   const size_t need = off_y + sizeof(float) * n * m;
   hipError_t e = hipSuccess;
@@ -397,20 +455,32 @@ bo_status bo_fit(const float* X, const float* Y, int64_t n, int32_t d, int32_t m
   unsigned char* stage = DS->fit_stage;
   std::memcpy(stage, hyp.data(), off_inv);
   std::memcpy(stage + off_inv, invls.data(), sizeof(float) * invls.size());
+  if (comp) std::memcpy(stage + off_pref, comp->pref, sizeof(float) * npref);
   e = hipMemcpyAsync(fs.hyp, stage, off_inv, hipMemcpyHostToDevice, st);
   if (e == hipSuccess)
     e = hipMemcpyAsync(M->invls, stage + off_inv, sizeof(float) * invls.size(),
                        hipMemcpyHostToDevice, st);
+  if (e == hipSuccess && comp)
+    e = hipMemcpyAsync(M->pref, stage + off_pref, sizeof(float) * npref, hipMemcpyHostToDevice,
+                       st);
   if (e == hipSuccess) e = hipMemsetAsync(fs.flag, 0, sizeof(int), st);
   if (e != hipSuccess) return bail(hip_fail(e, "bo_fit: upload"));
 
-  const double* d_ils = fs.hyp;
-  const double* d_os = fs.hyp + (size_t)m * d;
-  const double* d_noise = d_os + m;
-  if ((s = after_launch(launch_gram(X, n, d, m, nf, d_ils, d_os, d_noise, fs.A, st), st, "gram")) != BO_OK) return bail(s);
+  GramParams gp;
+  gp.dr = dr;
+  gp.ils = fs.hyp;
+  gp.os = fs.hyp + (size_t)m * d;
+  gp.noise = gp.os + m;
+  if (comp) {
+    gp.s_dep = gp.noise + m;
+    gp.s_int = gp.s_dep + m;
+    gp.pref = gp.s_int + m;
+  }
+  if ((s = after_launch(launch_gram(X, n, d, m, nf, gp, fs.A, st), st, "gram")) != BO_OK) return bail(s);
+  if (comp && (s = after_launch(launch_weights(X, n, d, m, M->n_pad, gp, M->wts, st), st, "weights")) != BO_OK) return bail(s);
   if ((s = after_launch(launch_cholesky(fs.A, fs.W, nf, m, fs.flag, st), st, "cholesky")) != BO_OK) return bail(s);
   if ((s = after_launch(launch_alpha(fs.W, Y, n, m, nf, M->n_pad, fs.tmp, M->alpha, st), st, "alpha")) != BO_OK) return bail(s);
-  if ((s = after_launch(launch_pack(fs.W, n, m, nf, M->nb, M->Lp, X, d, M->dx, M->invls, M->Xs, st), st, "pack")) != BO_OK) return bail(s);
+  if ((s = after_launch(launch_pack(fs.W, n, m, nf, M->nb, M->Lp, X, d, M->dx, dr, dr4, M->invls, M->Xs, st), st, "pack")) != BO_OK) return bail(s);
 
   // one synchronisation: the positive-definiteness flag and Y (for the front
   // and its finiteness check) come back together
@@ -424,13 +494,34 @@ bo_status bo_fit(const float* X, const float* Y, int64_t n, int32_t d, int32_t m
   const float* yst = reinterpret_cast<const float*>(stage + off_y);
   M->Yh.assign(yst, yst + (size_t)n * m);
   if (!all_finite(M->Yh.data(), M->Yh.size()))
-    return bail(fail(BO_ERR_NONFINITE_INPUT, "bo_fit: Y not finite"));
-  if (flag) return bail(fail(BO_ERR_NOT_POSITIVE_DEFINITE, "bo_fit: non-positive Cholesky pivot"));
+    return bail(fail(BO_ERR_NONFINITE_INPUT, W + ": Y not finite"));
+  if (flag) return bail(fail(BO_ERR_NOT_POSITIVE_DEFINITE, W + ": non-positive Cholesky pivot"));
   host_front(M->Yh.data(), n, m, nullptr, M->nd);
 
   M->last_stream = st;
   *out = h;
   return BO_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+bo_status bo_fit(const float* X, const float* Y, int64_t n, int32_t d, int32_t m,
+                 const float* lengthscale, const float* outputscale, const float* noise,
+                 void* stream, bo_model* out) {
+  return fit_impl("bo_fit", X, Y, n, d, m, lengthscale, outputscale, noise, nullptr, stream,
+                  out);
+}
+
+bo_status bo_fit_composite(const float* X, const float* Y, int64_t n, int32_t d, int32_t m,
+                           int32_t d_route, const float* lengthscale,
+                           const float* scale_route, const float* scale_dep,
+                           const float* scale_int, const float* pref, const float* noise,
+                           void* stream, bo_model* out) {
+  const CompositeSpec c{d_route, scale_dep, scale_int, pref};
+  return fit_impl("bo_fit_composite", X, Y, n, d, m, lengthscale, scale_route, noise, &c,
+                  stream, out);
 }
 
 void bo_free(bo_model model) {
@@ -472,6 +563,8 @@ bo_status bo_score_constrained(bo_model model, const float* cand, int64_t M_, in
   const int64_t npts = M_ * q;
   bo_status s;
   if (M_ == 0) return BO_OK;
+  if (M.dr > 0 && q != 1)
+    return fail(BO_ERR_INVALID_ARGUMENT, "bo_score: composite-kernel models score q = 1 only");
   if ((s = check_dev(cand, sizeof(float) * npts * M.d, "cand")) != BO_OK) return s;
   if ((s = check_dev(base_samples, sizeof(float) * (size_t)S * q * m, "base_samples")) != BO_OK) return s;
   if ((s = check_dev(ehvi, sizeof(float) * M_, "ehvi")) != BO_OK) return s;
@@ -586,6 +679,11 @@ bo_status bo_score_constrained(bo_model model, const float* cand, int64_t M_, in
     pa.n = static_cast<int>(M.n); pa.nb = M.nb;
     pa.s = M.os[k];
     pa.m = m; pa.k = k;
+    pa.dr = M.dr; pa.dr4 = M.dr4;
+    pa.s_dep = M.dr > 0 ? M.s_dep[k] : 0.f;
+    pa.s_int = M.dr > 0 ? M.s_int[k] : 0.f;
+    pa.wts = M.dr > 0 ? M.wts + (size_t)k * M.n_pad : nullptr;
+    pa.pref = M.dr > 0 ? M.pref + (size_t)k * (M.d - M.dr) : nullptr;
     pa.mu = mu_buf; pa.sd = sd_buf; pa.chol = chol_buf;
     if ((s = after_launch(launch_posterior(pa, st), st, "posterior")) != BO_OK) return s;
   }

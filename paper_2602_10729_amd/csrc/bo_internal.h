@@ -37,13 +37,19 @@ struct Model {
   int n_pad = 0;                 // n rounded up to kBlk
   int nb = 0;                    // n_pad / kBlk
   int dx = 0;                    // padded coordinate stride (multiple of 4)
-  std::vector<float> ls, os, noise;
+  // composite kernel (dr > 0): routing coordinates 0..dr-1 sit in slots
+  // 0..4*dr4-1 of the scaled layout, deployment coordinates from slot 4*dr4
+  int dr = 0, dr4 = 0;
+  std::vector<float> ls, os, noise;   // os: the (routing) output scale
+  std::vector<float> s_dep, s_int;    // composite: deployment / interaction scales
   std::vector<float> Yh;         // host copy of Y [n][m]
   std::vector<int32_t> nd;       // non-dominated rows (no reference filter)
 
   float* Xs = nullptr;           // [m][n_pad][dx] X / lengthscale (fp32)
   float* invls = nullptr;        // [m][dx] 1 / lengthscale (fp32, 0-padded)
   float* alpha = nullptr;        // [m][n_pad]
+  float* wts = nullptr;          // composite: [m][n_pad] preference weights of X (0 past n)
+  float* pref = nullptr;         // composite: [m][d - dr] preference slopes
   float* Lp = nullptr;           // [m][frag blocks][2 KiB] packed fp16 hi/lo L^{-1} + zero block
   size_t lp_per_obj = 0;         // floats per objective in Lp
 
@@ -61,12 +67,27 @@ struct Model {
 // Kernel launchers (fit.hip / posterior.hip / ehvi.hip / argmax.hip) -------
 // All return hipSuccess or the launch error.
 
+// Kernel hyperparameters on the device (fp64). Plain Matern-5/2: dr = 0 and
+// only ils, os, noise are read; composite: os is the routing scale and
+// s_dep, s_int, pref [m][d - dr] are read too.
+struct GramParams {
+  int dr = 0;
+  const double* ils = nullptr;     // [m][d] 1 / lengthscale
+  const double* os = nullptr;      // [m]
+  const double* noise = nullptr;   // [m]
+  const double* s_dep = nullptr;   // [m]
+  const double* s_int = nullptr;   // [m]
+  const double* pref = nullptr;    // [m][d - dr]
+};
 // Gram matrices K_k + eta_k I in fp64 for all objectives, padded to
 // n_fit x n_fit with an identity tail; only the lower block triangle (64x64
-// blocks) is written. ils: 1 / lengthscale [m][d]. A: [m][n_fit][n_fit].
+// blocks) is written. A: [m][n_fit][n_fit].
 hipError_t launch_gram(const float* X, int64_t n, int d, int m, int n_fit,
-                       const double* ils, const double* os, const double* noise,
-                       double* A, hipStream_t st);
+                       const GramParams& g, double* A, hipStream_t st);
+// Composite: wts[k][i] = fp32(exp(sum_j pref[k][j] X[i][dr + j])), 0 for
+// n <= i < n_pad.
+hipError_t launch_weights(const float* X, int64_t n, int d, int m, int n_pad,
+                          const GramParams& g, float* wts, hipStream_t st);
 // Blocked right-looking Cholesky of m matrices [m][nf][nf] (lower, in place);
 // also leaves W = L^{-1} (lower, [m][nf][nf]).
 // *flag is set non-zero on a non-positive or non-finite pivot.
@@ -79,10 +100,20 @@ hipError_t launch_alpha(const double* W, const float* Y, int64_t n, int m,
 // Pack W into the posterior's A-fragment format (fp16 hi/lo planes of 16x32
 // lower blocks, zeros beyond n, then one all-zero block; 2 KiB per block,
 // posterior_frag_blocks(nb) blocks per objective) and write the
-// lengthscale-scaled X.
+// lengthscale-scaled X in the slot layout (invls is per slot, [m][dx]).
 hipError_t launch_pack(const double* W, int64_t n, int m, int nf, int nb,
-                       float* Lp, const float* X, int d, int dx,
+                       float* Lp, const float* X, int d, int dx, int dr, int dr4,
                        const float* invls, float* Xs, hipStream_t st);
+
+// Coordinate held by slot t of the scaled layout, or -1 for padding: the
+// identity for plain models (dr = dr4 = 0); for composite ones the routing
+// coordinates fill slots 0..dr-1 (zero up to 4*dr4) and the deployment
+// coordinates start at slot 4*dr4.
+__host__ __device__ inline int slot_dim(int t, int d, int dr, int dr4) {
+  if (t < 4 * dr4) return t < dr ? t : -1;
+  const int c = dr + t - 4 * dr4;
+  return c < d ? c : -1;
+}
 // Convert a fp64 [n][n] lower factor (leading dimension nf) to fp32 [n][n].
 hipError_t launch_lower_to_f32(const double* A, int64_t n, int nf, float* L,
                                hipStream_t st);
@@ -102,8 +133,12 @@ struct PosteriorArgs {
   const float* alpha;  // [n_pad]
   const float* Lp;     // packed fragments of this objective
   int n, nb;
-  float s;             // output scale
+  float s;             // output scale (composite: of the routing term)
   int m, k;            // objective count / index (output strides)
+  int dr, dr4;         // composite kernel (dr > 0): routing coordinates / slot chunks
+  float s_dep, s_int;  // composite: deployment and interaction scales
+  const float* wts;    // composite: [n_pad] preference weights of the training points
+  const float* pref;   // composite: [d - dr] preference slopes
   float* mu;           // [npts][m]   (mu of objective k at [p*m+k])
   float* sd;           // [npts][m]   marginal posterior std
   float* chol;         // q > 1: [npts/q][m][q(q+1)/2] lower factor, row-major

@@ -42,17 +42,25 @@ __device__ inline double matern52_d(double r2, double s) {
   return s * (1.0 + c * r + (5.0 / 3.0) * r2) * exp(-c * r);
 }
 
+__device__ inline double matern32_d(double r2) {
+  const double r = sqrt(r2);
+  const double c = 1.73205080756887729353;   // sqrt(3)
+  return (1.0 + c * r) * exp(-c * r);
+}
+
 // Gram matrix in fp64, lower block triangle only (tiles above the diagonal
-// blocks are never read by the factorisation). ils: 1 / lengthscale. One
-// 16x16 tile per workgroup; the tile's 32 rows of X and the lengthscales
-// are staged in LDS first, so every global load is issued up front.
+// blocks are never read by the factorisation). One 16x16 tile per
+// workgroup; the tile's 32 rows of X, the inverse lengthscales and (for the
+// composite kernel) the rows' preference weights are staged in LDS first,
+// so every global load is issued up front.
+//   plain:     k = os M52(r)
+//   composite: k = os M52(r_route) + s_dep w_i w_j M32(r_dep)
+//                  + s_int M52(r_route) M32(r_dep)
 __global__ __launch_bounds__(256) void k_gram(const float* __restrict__ X, int64_t n, int d,
-                                              int nf, const double* __restrict__ ils,
-                                              const double* __restrict__ os,
-                                              const double* __restrict__ noise,
-                                              double* __restrict__ A) {
+                                              int nf, GramParams g, double* __restrict__ A) {
   __shared__ float xs[2][16][BO_MAX_D + 1];
   __shared__ double il[BO_MAX_D];
+  __shared__ double wrow[2][16];
   const int k = blockIdx.z;
   const int bi = blockIdx.y, bj = blockIdx.x;      // 16x16 tiles
   if ((bj >> 2) > (bi >> 2)) return;                // strictly above the 64-block diagonal
@@ -63,25 +71,58 @@ __global__ __launch_bounds__(256) void k_gram(const float* __restrict__ X, int64
     const int64_t row = (int64_t)(s ? bj : bi) * 16 + r;
     xs[s][r][t] = (row < n) ? X[row * d + t] : 0.f;
   }
-  if (tid < d) il[tid] = ils[k * d + tid];
+  if (tid < d) il[tid] = g.ils[k * d + tid];
+  __syncthreads();
+  const int dr = g.dr;
+  if (dr > 0 && tid < 32) {
+    const int s = tid >> 4, r = tid & 15;
+    const double* p = g.pref + (int64_t)k * (d - dr);
+    double e = 0.0;
+    for (int t = dr; t < d; ++t) e = fma(p[t - dr], static_cast<double>(xs[s][r][t]), e);
+    wrow[s][r] = exp(e);
+  }
   __syncthreads();
   const int i = bi * 16 + threadIdx.y;
   const int j = bj * 16 + threadIdx.x;
   if (i >= nf || j >= nf) return;
   double v;
   if (i < n && j < n) {
-    double r2 = 0.0;
+    double ra = 0.0, rb = 0.0;          // routing / deployment (plain: all in ra)
     for (int t = 0; t < d; ++t) {
       const double diff = (static_cast<double>(xs[0][threadIdx.y][t]) -
                            static_cast<double>(xs[1][threadIdx.x][t])) * il[t];
-      r2 = fma(diff, diff, r2);
+      if (dr > 0 && t >= dr) rb = fma(diff, diff, rb);
+      else ra = fma(diff, diff, ra);
     }
-    v = matern52_d(r2, os[k]);
-    if (i == j) v += noise[k];
+    if (dr == 0) {
+      v = matern52_d(ra, g.os[k]);
+    } else {
+      const double k5 = matern52_d(ra, 1.0), k3 = matern32_d(rb);
+      v = g.os[k] * k5 + g.s_dep[k] * wrow[0][threadIdx.y] * wrow[1][threadIdx.x] * k3 +
+          g.s_int[k] * k5 * k3;
+    }
+    if (i == j) v += g.noise[k];
   } else {
     v = (i == j) ? 1.0 : 0.0;
   }
   A[((int64_t)k * nf + i) * nf + j] = v;
+}
+
+// Composite: fp32 preference weights of the training points for scoring.
+__global__ __launch_bounds__(256) void k_weights(const float* __restrict__ X, int64_t n, int d,
+                                                 int n_pad, GramParams g,
+                                                 float* __restrict__ wts) {
+  const int k = blockIdx.y;
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n_pad) return;
+  float w = 0.f;
+  if (i < n) {
+    const double* p = g.pref + (int64_t)k * (d - g.dr);
+    double e = 0.0;
+    for (int t = g.dr; t < d; ++t) e = fma(p[t - g.dr], static_cast<double>(X[i * d + t]), e);
+    w = static_cast<float>(exp(e));
+  }
+  wts[(int64_t)k * n_pad + i] = w;
 }
 
 // 1 / sqrt(d), d > 0: the hardware estimate refined by two Newton steps
@@ -473,9 +514,10 @@ __global__ __launch_bounds__(256) void k_pack(const double* __restrict__ W, int6
   }
 }
 
-// Xs[k][i][t] = X[i][t] * invls[k][t] (zero padding beyond n and d)
+// Xs[k][i][t] = X[i][slot_dim(t)] * invls[k][t] (zero for padding slots and
+// rows beyond n)
 __global__ __launch_bounds__(256) void k_scale_x(const float* __restrict__ X, int64_t n,
-                                                 int d, int dx, int n_pad,
+                                                 int d, int dx, int dr, int dr4, int n_pad,
                                                  const float* __restrict__ invls,
                                                  float* __restrict__ Xs) {
   const int k = blockIdx.y;
@@ -483,8 +525,9 @@ __global__ __launch_bounds__(256) void k_scale_x(const float* __restrict__ X, in
   if (e >= (int64_t)n_pad * dx) return;
   const int64_t i = e / dx;
   const int t = static_cast<int>(e % dx);
+  const int c = slot_dim(t, d, dr, dr4);
   float v = 0.f;
-  if (i < n && t < d) v = X[i * d + t] * invls[k * dx + t];
+  if (i < n && c >= 0) v = X[i * d + c] * invls[k * dx + t];
   Xs[(int64_t)k * n_pad * dx + e] = v;
 }
 
@@ -510,10 +553,16 @@ __global__ void k_f32_to_padded(const float* __restrict__ Asrc, int64_t n, int n
 }  // namespace
 
 hipError_t launch_gram(const float* X, int64_t n, int d, int m, int n_fit,
-                       const double* ils, const double* os, const double* noise,
-                       double* A, hipStream_t st) {
+                       const GramParams& g, double* A, hipStream_t st) {
   dim3 grid((n_fit + 15) / 16, (n_fit + 15) / 16, m), block(16, 16);
-  hipLaunchKernelGGL(k_gram, grid, block, 0, st, X, n, d, n_fit, ils, os, noise, A);
+  hipLaunchKernelGGL(k_gram, grid, block, 0, st, X, n, d, n_fit, g, A);
+  return hipGetLastError();
+}
+
+hipError_t launch_weights(const float* X, int64_t n, int d, int m, int n_pad,
+                          const GramParams& g, float* wts, hipStream_t st) {
+  hipLaunchKernelGGL(k_weights, dim3((n_pad + 255) / 256, m), dim3(256), 0, st, X, n, d,
+                     n_pad, g, wts);
   return hipGetLastError();
 }
 
@@ -545,15 +594,15 @@ hipError_t launch_alpha(const double* W, const float* Y, int64_t n, int m, int n
 }
 
 hipError_t launch_pack(const double* W, int64_t n, int m, int nf, int nb, float* Lp,
-                       const float* X, int d, int dx, const float* invls, float* Xs,
-                       hipStream_t st) {
+                       const float* X, int d, int dx, int dr, int dr4, const float* invls,
+                       float* Xs, hipStream_t st) {
   const int64_t nblk = posterior_frag_blocks(nb);   // with the zero block
   const unsigned gx = static_cast<unsigned>((nblk * 64 + 255) / 256);
   hipLaunchKernelGGL(k_pack, dim3(gx, m), dim3(256), 0, st, W, n, nf, nblk,
                      reinterpret_cast<_Float16*>(Lp));
   const int n_pad = nb * kBlk;
   const unsigned gx2 = static_cast<unsigned>(((int64_t)n_pad * dx + 255) / 256);
-  hipLaunchKernelGGL(k_scale_x, dim3(gx2, m), dim3(256), 0, st, X, n, d, dx, n_pad,
+  hipLaunchKernelGGL(k_scale_x, dim3(gx2, m), dim3(256), 0, st, X, n, d, dx, dr, dr4, n_pad,
                      invls, Xs);
   return hipGetLastError();
 }

@@ -85,6 +85,14 @@ __device__ __forceinline__ float matern52_f(float r2, float s) {
   return s * poly * e;
 }
 
+// Matern-3/2 correlation of squared scaled distance r2:
+// (1 + sqrt3 r) exp(-sqrt3 r).
+__device__ __forceinline__ float matern32_f(float r2) {
+  const float r = __builtin_amdgcn_sqrtf(r2);
+  constexpr float kNegSqrt3Log2e = static_cast<float>(-1.73205080756887729353 * 1.44269504088896340736);
+  return fmaf(r, 1.73205081f, 1.0f) * __builtin_amdgcn_exp2f(kNegSqrt3Log2e * r);
+}
+
 __device__ __forceinline__ float quad_xor(float v, int x) {
   // DPP quad_perm: lane i of each group of 4 reads lane i ^ x.
   int iv = __float_as_int(v);
@@ -120,69 +128,84 @@ __host__ __device__ __forceinline__ int frag_row_start(int I) {
 
 // Per-lane state of the K*^T producer. A wave makes NT/8 columns of each
 // 32-row block; lane l takes column l % CPW and RPL = CPW/2 consecutive rows.
-template <int NT, int DX4>
+template <int NT, int DX4, bool COMP>
 struct Producer {
   static constexpr int CPW = NT / kWaves;
   static constexpr int RPL = kJ * CPW / 64;
-  float c[DX4 * 4];         // scaled candidate coordinates
+  float c[DX4 * 4];         // scaled candidate coordinates (slot layout)
   bool valid;
   float mu;
+  float wsd;                // composite: s_dep * w(candidate)
   int col;                  // tile column of this lane
   int row0;                 // first row of this lane inside a block
 };
 
 // Training rows staged in LDS, one 32-row block per slot, four slots: row
 // r of block b at slot b % 4, [kJ][dx + 4] floats per slot, the last float4
-// of a row holding (alpha, 0, 0, 0). Step J loads the rows of block J + 4
+// of a row holding (alpha, w, 0, 0), w the preference weight of the row
+// (composite kernel; 0 otherwise). Step J loads the rows of block J + 4
 // first and stores them last, while the producer reads block J + 2. Every
 // thread issues the same loads (a spare thread's store goes to a scratch
 // float4), so no branch makes the compiler drain the loads in flight.
-template <int DX4>
+template <int DX4, bool COMP>
 struct Stager {
   static constexpr int RS = DX4 * 4 + 4;                 // row stride (floats)
   static constexpr int kF4 = kJ * (DX4 + 1);             // float4s per block
   static constexpr int kSlot = kJ * RS;                  // floats per slot
   static_assert(kF4 <= kThreads, "one float4 per thread");
   float4 x;                 // the loads in flight (selected at the store,
-  float al;                 // so the loads are not waited for early)
-  int soff;                 // this thread's float offset inside a slot (or the scratch)
+  float al, wt;             // so the loads are not waited for early)
+  int soff;                 // this thread's float offset inside a slot (-1: spare thread)
   int row, t4;
-  __amdgpu_buffer_rsrc_t xs_rs, al_rs;
+  __amdgpu_buffer_rsrc_t xs_rs, al_rs, wt_rs;
 };
 
 // Rows past n_pad read zeros (buffer range check), so blocks past the matrix
 // that the producer may evaluate carry zero alpha and add nothing to mu.
-template <int DX4>
-__device__ __forceinline__ void stage_load(Stager<DX4>& S, const PosteriorArgs& a, int jb) {
+template <int DX4, bool COMP>
+__device__ __forceinline__ void stage_load(Stager<DX4, COMP>& S, const PosteriorArgs& a, int jb) {
   const int row = jb * kJ + S.row;
   S.x = load4(S.xs_rs, (row * a.dx + 4 * min(S.t4, DX4 - 1)) * 4, 0);
   S.al = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(S.al_rs, row * 4, 0, 0));
+  if constexpr (COMP)
+    S.wt = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(S.wt_rs, row * 4, 0, 0));
 }
 
-template <int DX4>
-__device__ __forceinline__ void stage_store(const Stager<DX4>& S, float* xst, int jb) {
+template <int DX4, bool COMP>
+__device__ __forceinline__ void stage_store(const Stager<DX4, COMP>& S, float* xst, int jb) {
   const bool is_al = S.t4 == DX4;
-  const float4 v{is_al ? S.al : S.x.x, is_al ? 0.f : S.x.y, is_al ? 0.f : S.x.z,
+  const float wt = COMP ? S.wt : 0.f;
+  const float4 v{is_al ? S.al : S.x.x, is_al ? wt : S.x.y, is_al ? 0.f : S.x.z,
                  is_al ? 0.f : S.x.w};
-  *reinterpret_cast<float4*>(xst + (jb & 3) * Stager<DX4>::kSlot + S.soff) = v;
+  // a spare thread writes the scratch float4 after the four slots (at a fixed
+  // place, whatever the slot)
+  constexpr int kSlot = Stager<DX4, COMP>::kSlot;
+  const int off = (S.soff < 0) ? 4 * kSlot : (jb & 3) * kSlot + S.soff;
+  *reinterpret_cast<float4*>(xst + off) = v;
 }
 
 // Evaluate this lane's rows of block jb into the ring as fp16 hi/lo planes,
 // reading the training rows from jb's staging slot.
-template <int NT, int DX4>
-__device__ __forceinline__ void produce(Producer<NT, DX4>& P, const PosteriorArgs& a, int jb,
+template <int NT, int DX4, bool COMP>
+__device__ __forceinline__ void produce(Producer<NT, DX4, COMP>& P, const PosteriorArgs& a, int jb,
                                         const float* xst, _Float16* ring) {
-  constexpr int RPL = Producer<NT, DX4>::RPL;
-  constexpr int RS = Stager<DX4>::RS;
+  constexpr int RPL = Producer<NT, DX4, COMP>::RPL;
+  constexpr int RS = Stager<DX4, COMP>::RS;
   typedef _Float16 halfr __attribute__((ext_vector_type(RPL)));
   halfr hi, lo;
-  const float* xr = xst + (jb & 3) * Stager<DX4>::kSlot + P.row0 * RS;
+  const float* xr = xst + (jb & 3) * Stager<DX4, COMP>::kSlot + P.row0 * RS;
 #pragma unroll
   for (int u = 0; u < RPL; ++u) {
-    const int row = jb * kJ + P.row0 + u;
-    float r2 = 0.f;
+    float r2 = 0.f, r2r = 0.f;    // r2r: composite, the routing part
 #pragma unroll
     for (int t4 = 0; t4 < DX4; ++t4) {
+      if constexpr (COMP) {
+        // routing slots come first: restart the sum where deployment begins
+        if (t4 == a.dr4) {
+          r2r = r2;
+          r2 = 0.f;
+        }
+      }
       const float4 x = *reinterpret_cast<const float4*>(xr + u * RS + 4 * t4);
       const float d0 = P.c[4 * t4 + 0] - x.x;
       const float d1 = P.c[4 * t4 + 1] - x.y;
@@ -195,7 +218,15 @@ __device__ __forceinline__ void produce(Producer<NT, DX4>& P, const PosteriorArg
     }
     // no mask: rows past n (zero coordinates) meet zero columns of L^{-1}
     // and zero alpha; columns past the batch are never written
-    const float kv = matern52_f(r2, a.s);
+    float kv;
+    if constexpr (COMP) {
+      // s_route M52(r_route) + s_dep w* w_i M32(r_dep) + s_int M52 M32
+      const float k5 = matern52_f(r2r, 1.0f);
+      const float k3 = matern32_f(r2);
+      kv = fmaf(P.wsd * xr[u * RS + 4 * DX4 + 1], k3, k5 * fmaf(a.s_int, k3, a.s));
+    } else {
+      kv = matern52_f(r2, a.s);
+    }
     P.mu = fmaf(xr[u * RS + 4 * DX4], kv, P.mu);
     const _Float16 h = static_cast<_Float16>(kv);
     hi[u] = h;
@@ -295,9 +326,9 @@ __device__ __forceinline__ void load_b(const Ctx& C, int J, int h, BHalf& B) {
 // interleave: the fp16 MFMAs overlap the VALU work. The step's barrier
 // publishes the produced block and the staged rows; block J + 1 was
 // published by the previous step's, so its B fragments can be read early.
-template <int LO, int RB, int NT, int DX4, bool PROD>
-__device__ __forceinline__ void step(const Ctx& C, const PosteriorArgs& a, Producer<NT, DX4>& P,
-                                     Stager<DX4>& S, _Float16* ring, const Slots<RB>& sl, int J,
+template <int LO, int RB, int NT, int DX4, bool COMP, bool PROD>
+__device__ __forceinline__ void step(const Ctx& C, const PosteriorArgs& a, Producer<NT, DX4, COMP>& P,
+                                     Stager<DX4, COMP>& S, _Float16* ring, const Slots<RB>& sl, int J,
                                      BHalf& B0, AFrag (&av)[RB], floatx4 (&acc)[RB][NT / 16]) {
   constexpr int NCB = NT / 16;
   static_assert(NCB == 4, "two halves of two column blocks");
@@ -326,7 +357,7 @@ __device__ __forceinline__ void step(const Ctx& C, const PosteriorArgs& a, Produ
     // the MFMAs as two separate stretches, and the two waves of a SIMD
     // (kept in step by the barriers) then contend for the same unit
     constexpr int nM = 3 * NCB * (RB - LO);
-    constexpr int nV = Producer<NT, DX4>::RPL * (2 * 4 * DX4 + 14);
+    constexpr int nV = Producer<NT, DX4, COMP>::RPL * (2 * 4 * DX4 + (COMP ? 24 : 14));
     if constexpr (nM > 0) {
 #pragma unroll
       for (int i = 0; i < nM; ++i) {
@@ -342,24 +373,24 @@ __device__ __forceinline__ void step(const Ctx& C, const PosteriorArgs& a, Produ
 
 // Steps [j0, j1) for slots [LO, RB); the producer runs at the steps whose
 // block J + 2 lies in the pass's production window [pw0, pw1).
-template <int LO, int RB, int NT, int DX4>
-__device__ __forceinline__ void span(const Ctx& C, const PosteriorArgs& a, Producer<NT, DX4>& P,
-                                     Stager<DX4>& S, _Float16* ring, const Slots<RB>& sl, int j0,
+template <int LO, int RB, int NT, int DX4, bool COMP>
+__device__ __forceinline__ void span(const Ctx& C, const PosteriorArgs& a, Producer<NT, DX4, COMP>& P,
+                                     Stager<DX4, COMP>& S, _Float16* ring, const Slots<RB>& sl, int j0,
                                      int j1, int pw0, int pw1, BHalf& B0, AFrag (&av)[RB],
                                      floatx4 (&acc)[RB][NT / 16]) {
   const int p0 = min(max(pw0 - 2, j0), j1), p1 = min(max(pw1 - 2, p0), j1);
   int J = j0;
-  for (; J < p0; ++J) step<LO, RB, NT, DX4, false>(C, a, P, S, ring, sl, J, B0, av, acc);
-  for (; J < p1; ++J) step<LO, RB, NT, DX4, true>(C, a, P, S, ring, sl, J, B0, av, acc);
-  for (; J < j1; ++J) step<LO, RB, NT, DX4, false>(C, a, P, S, ring, sl, J, B0, av, acc);
+  for (; J < p0; ++J) step<LO, RB, NT, DX4, COMP, false>(C, a, P, S, ring, sl, J, B0, av, acc);
+  for (; J < p1; ++J) step<LO, RB, NT, DX4, COMP, true>(C, a, P, S, ring, sl, J, B0, av, acc);
+  for (; J < j1; ++J) step<LO, RB, NT, DX4, COMP, false>(C, a, P, S, ring, sl, J, B0, av, acc);
 }
 
 // Rounds R.. of the triangular part of a pass: round R covers the row blocks
 // base + 8R .. base + 8R + 7, i.e. J in [base/2 + 4R, base/2 + 4R + 4); slot R
 // is live while J <= its row block / 2, slots above R throughout.
-template <int R, int RB, int NT, int DX4>
-__device__ __forceinline__ void rounds(const Ctx& C, const PosteriorArgs& a, Producer<NT, DX4>& P,
-                                       Stager<DX4>& S, _Float16* ring, const Slots<RB>& sl,
+template <int R, int RB, int NT, int DX4, bool COMP>
+__device__ __forceinline__ void rounds(const Ctx& C, const PosteriorArgs& a, Producer<NT, DX4, COMP>& P,
+                                       Stager<DX4, COMP>& S, _Float16* ring, const Slots<RB>& sl,
                                        int base, int pw0, int pw1, BHalf& B0, AFrag (&av)[RB],
                                        floatx4 (&acc)[RB][NT / 16]) {
   if constexpr (R < RB) {
@@ -367,19 +398,20 @@ __device__ __forceinline__ void rounds(const Ctx& C, const PosteriorArgs& a, Pro
     if (j0 >= C.nbj) return;
     const int jend = min(j0 + 4, C.nbj);
     const int jlive = min(slot_block(base, R, C.wave) / 2 + 1, jend);
-    span<R, RB, NT, DX4>(C, a, P, S, ring, sl, j0, jlive, pw0, pw1, B0, av, acc);
-    span<R + 1, RB, NT, DX4>(C, a, P, S, ring, sl, jlive, jend, pw0, pw1, B0, av, acc);
-    rounds<R + 1, RB, NT, DX4>(C, a, P, S, ring, sl, base, pw0, pw1, B0, av, acc);
+    span<R, RB, NT, DX4, COMP>(C, a, P, S, ring, sl, j0, jlive, pw0, pw1, B0, av, acc);
+    span<R + 1, RB, NT, DX4, COMP>(C, a, P, S, ring, sl, jlive, jend, pw0, pw1, B0, av, acc);
+    rounds<R + 1, RB, NT, DX4, COMP>(C, a, P, S, ring, sl, base, pw0, pw1, B0, av, acc);
   }
 }
 
-template <int NT, int DX4, int Q, int RB>
+template <int NT, int DX4, int Q, int RB, bool COMP>
 __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
   extern __shared__ float smem[];
   constexpr int NCB = NT / 16;          // 16-column blocks per tile
   constexpr int NX = (Q > 1) ? Q : 1;   // per-point partial slots (diag + xors)
-  using Prod = Producer<NT, DX4>;
+  using Prod = Producer<NT, DX4, COMP>;
   static_assert(Prod::RPL >= 2 && Prod::RPL <= 8 && 64 % Prod::CPW == 0, "tile width");
+  static_assert(!(COMP && Q > 1), "the composite kernel scores single points");
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   // wave index as a scalar: the loop control below stays uniform
@@ -388,8 +420,9 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
   _Float16* ring = reinterpret_cast<_Float16*>(smem);       // 2 planes x NT x kCSH halves
   float* xst = smem + NT * kCSH;                            // 4 slots + a scratch float4
   float* red = smem;                                        // kWaves * NT * NX, after the loop
-  float* mush = xst + 4 * Stager<DX4>::kSlot + 4;           // NT
+  float* mush = xst + 4 * Stager<DX4, COMP>::kSlot + 4;           // NT
   float* kpp = mush + NT;                                   // NT * 4 (prior cross-cov)
+  float* wsh = kpp + NT * 4;                                // NT: w(candidate), composite
   const int64_t p0 = (int64_t)blockIdx.x * NT;
 
   Prod P;
@@ -400,12 +433,23 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
     P.valid = p < a.npts;
 #pragma unroll
     for (int t = 0; t < DX4 * 4; ++t) P.c[t] = 0.f;
+    P.wsd = 0.f;
+    float wstar = 0.f;
     if (P.valid) {
       const float* cp = a.cand + p * a.d;
 #pragma unroll
-      for (int t = 0; t < DX4 * 4; ++t)
-        if (t < a.d) P.c[t] = cp[t] * a.invls[t];
+      for (int t = 0; t < DX4 * 4; ++t) {
+        const int c = slot_dim(t, a.d, a.dr, a.dr4);
+        if (c >= 0) P.c[t] = cp[c] * a.invls[t];
+      }
+      if constexpr (COMP) {
+        float e = 0.f;
+        for (int t = a.dr; t < a.d; ++t) e = fmaf(a.pref[t - a.dr], cp[t], e);
+        wstar = expf(e);
+        P.wsd = a.s_dep * wstar;
+      }
     }
+    if (COMP && P.row0 == 0) wsh[P.col] = wstar;
   }
 
   if (Q > 1) {
@@ -433,12 +477,13 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
   C.nbj = (a.nb + 1) / 2;
   C.zero_blk = frag_row_start(a.nb);
   C.lp_rs = make_rsrc(a.Lp, (C.zero_blk + 1) * 2048);
-  Stager<DX4> S;
+  Stager<DX4, COMP> S;
   S.xs_rs = make_rsrc(a.Xs, n_pad * a.dx * 4);
   S.al_rs = make_rsrc(a.alpha, n_pad * 4);
+  if constexpr (COMP) S.wt_rs = make_rsrc(a.wts, n_pad * 4);
   S.row = min(tid / (DX4 + 1), kJ - 1);
   S.t4 = tid % (DX4 + 1);
-  S.soff = (tid < Stager<DX4>::kF4) ? S.row * Stager<DX4>::RS + 4 * S.t4 : 4 * Stager<DX4>::kSlot;
+  S.soff = (tid < Stager<DX4, COMP>::kF4) ? S.row * Stager<DX4, COMP>::RS + 4 * S.t4 : -1;
   C.n_pad = n_pad;
   C.wave = wave;
   C.tid = tid;
@@ -478,7 +523,7 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
     lds_barrier();
     {
       // blocks 0..3 at once: one load latency, not four
-      Stager<DX4> S4[4];
+      Stager<DX4, COMP> S4[4];
 #pragma unroll
       for (int jb = 0; jb < 4; ++jb) {
         S4[jb] = S;
@@ -500,8 +545,8 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
     BHalf B0;
     load_b<NT>(C, 0, 0, B0);
     // blocks left of this pass's triangle: every slot is live
-    span<0, RB, NT, DX4>(C, a, P, S, ring, sl, 0, base / 2, pw0, pw1, B0, av, acc);
-    rounds<0, RB, NT, DX4>(C, a, P, S, ring, sl, base, pw0, pw1, B0, av, acc);
+    span<0, RB, NT, DX4, COMP>(C, a, P, S, ring, sl, 0, base / 2, pw0, pw1, B0, av, acc);
+    rounds<0, RB, NT, DX4, COMP>(C, a, P, S, ring, sl, base, pw0, pw1, B0, av, acc);
     have = (jpass <= kRing) ? max(have, jpass) : 0;
 
 #pragma unroll
@@ -558,7 +603,12 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
 #pragma unroll
       for (int x = 0; x < NX; ++x) tot[x] += red[(w * NT + tid) * NX + x];
     const float mu = mush[tid];
-    const float var = a.s - tot[0];
+    float prior = a.s;
+    if constexpr (COMP) {
+      const float w = wsh[tid];
+      prior = fmaf(a.s_dep * w, w, a.s + a.s_int);     // s_route + s_dep w*^2 + s_int
+    }
+    const float var = prior - tot[0];
     if (valid) {
       a.mu[p * a.m + a.k] = mu;
       a.sd[p * a.m + a.k] = __builtin_amdgcn_sqrtf(fmaxf(var, 0.f));
@@ -620,22 +670,23 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
 
 constexpr size_t lds_floats(int NT, int DX4, int q) {
   // ring: 2 planes x NT columns x kCSH halves (the reduction overlays it);
-  // staging: 4 slots + a scratch float4; mu and the prior cross-covariances
-  return (size_t)NT * kCSH + (size_t)4 * kJ * (DX4 * 4 + 4) + 4 + NT + (size_t)NT * 4;
+  // staging: 4 slots + a scratch float4; mu, the prior cross-covariances and
+  // the candidates' preference weights
+  return (size_t)NT * kCSH + (size_t)4 * kJ * (DX4 * 4 + 4) + 4 + NT + (size_t)NT * 4 + NT;
 }
 static_assert((size_t)kWaves * 64 * 4 <= (size_t)64 * kCSH, "reduction fits the ring");
 
-template <int NT, int DX4, int Q, int RB>
+template <int NT, int DX4, int Q, int RB, bool COMP>
 hipError_t launch_t(const PosteriorArgs& a, hipStream_t st) {
   const size_t lds = sizeof(float) * lds_floats(NT, DX4, Q);
   // more than 64 KiB of dynamic LDS: opt in (cheap; set on every launch so
   // that it holds on whichever device is current)
-  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_posterior<NT, DX4, Q, RB>),
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_posterior<NT, DX4, Q, RB, COMP>),
                                      hipFuncAttributeMaxDynamicSharedMemorySize,
                                      static_cast<int>(lds));
   if (e != hipSuccess) return e;
   const unsigned grid = static_cast<unsigned>((a.npts + NT - 1) / NT);
-  hipLaunchKernelGGL((k_posterior<NT, DX4, Q, RB>), dim3(grid), dim3(kThreads), lds, st, a);
+  hipLaunchKernelGGL((k_posterior<NT, DX4, Q, RB, COMP>), dim3(grid), dim3(kThreads), lds, st, a);
   return hipGetLastError();
 }
 
@@ -644,13 +695,19 @@ hipError_t launch_t(const PosteriorArgs& a, hipStream_t st) {
 template <int DX4>
 hipError_t launch_for_dx(const PosteriorArgs& a, hipStream_t st) {
   const bool small = a.nb <= 16;
+  if (a.dr > 0) {
+    // composite kernel: single points only
+    if (a.q != 1) return hipErrorInvalidValue;
+    return small ? launch_t<BO_POST_NT, DX4, 1, 2, true>(a, st)
+                 : launch_t<BO_POST_NT, DX4, 1, BO_POST_RB, true>(a, st);
+  }
   switch (a.q) {
-    case 1: return small ? launch_t<BO_POST_NT, DX4, 1, 2>(a, st)
-                         : launch_t<BO_POST_NT, DX4, 1, BO_POST_RB>(a, st);
-    case 2: return small ? launch_t<BO_POST_NT, DX4, 2, 2>(a, st)
-                         : launch_t<BO_POST_NT, DX4, 2, BO_POST_RB>(a, st);
-    case 4: return small ? launch_t<BO_POST_NT, DX4, 4, 2>(a, st)
-                         : launch_t<BO_POST_NT, DX4, 4, BO_POST_RB>(a, st);
+    case 1: return small ? launch_t<BO_POST_NT, DX4, 1, 2, false>(a, st)
+                         : launch_t<BO_POST_NT, DX4, 1, BO_POST_RB, false>(a, st);
+    case 2: return small ? launch_t<BO_POST_NT, DX4, 2, 2, false>(a, st)
+                         : launch_t<BO_POST_NT, DX4, 2, BO_POST_RB, false>(a, st);
+    case 4: return small ? launch_t<BO_POST_NT, DX4, 4, 2, false>(a, st)
+                         : launch_t<BO_POST_NT, DX4, 4, BO_POST_RB, false>(a, st);
     default: return hipErrorInvalidValue;
   }
 }

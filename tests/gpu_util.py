@@ -18,11 +18,15 @@ def to_dev(a):
     return torch.from_numpy(np.ascontiguousarray(a)).cuda()
 
 
-def gpu_run(wl, cand=None, want_musd=True, ref=None, Z=None, lower=None):
+def gpu_run(wl, cand=None, want_musd=True, ref=None, Z=None, lower=None, comp=None):
     import torch
     import paper_2602_10729_amd as bo
     X, Y = to_dev(wl.X), to_dev(wl.Y)
-    model = bo.fit(X, Y, wl.lengthscale, wl.outputscale, wl.noise)
+    if comp is None:
+        model = bo.fit(X, Y, wl.lengthscale, wl.outputscale, wl.noise)
+    else:
+        model = bo.fit_composite(X, Y, comp.d_route, wl.lengthscale, comp.s_route, comp.s_dep,
+                                 comp.s_int, comp.pref, wl.noise)
     c = to_dev(wl.cand if cand is None else cand)
     z = to_dev(wl.Z if Z is None else Z)
     r = wl.ref if ref is None else ref
@@ -42,8 +46,11 @@ def gpu_run(wl, cand=None, want_musd=True, ref=None, Z=None, lower=None):
     return out
 
 
-def oracle_fit(wl):
-    return O.fit(wl.X, wl.Y, wl.lengthscale, wl.outputscale, wl.noise)
+def oracle_fit(wl, comp=None):
+    if comp is None:
+        return O.fit(wl.X, wl.Y, wl.lengthscale, wl.outputscale, wl.noise)
+    c = O.Composite(comp.d_route, comp.s_route, comp.s_dep, comp.s_int, comp.pref)
+    return O.fit(wl.X, wl.Y, wl.lengthscale, wl.outputscale, wl.noise, composite=c)
 
 
 def oracle_score(model, wl, cand=None, ref=None, Z=None, lower=None):

@@ -1,0 +1,100 @@
+"""GPU parity of the composite surrogate kernel (bo_fit_composite + bo_score)
+against the fp64 oracle."""
+import numpy as np
+import pytest
+
+import bo_inputs as bi
+from gpu_util import (TOL_MU, TOL_SIGMA, TOL_EHVI, gpu_run, oracle_fit, oracle_score,
+                      assert_close, check_argmax, to_dev)
+
+pytestmark = pytest.mark.gpu
+
+
+def _announce(*a):
+    print("[case]", *a, flush=True)
+
+
+@pytest.mark.parametrize("cfg,M,seed,d_route", [(2, 2003, 0, None), (2, 2003, 1, None),
+                                                (1, 3001, 0, 5), (0, 777, 2, 2),
+                                                (4, 300, 0, 9)])
+def test_composite_parity(cfg, M, seed, d_route):
+    wl = bi.make_config(cfg, seed=seed, M=M)
+    if wl.q > 1:   # single points from config 4's observations
+        wl.cand = wl.cand.reshape(-1, 1, wl.d)[:M].copy()
+        wl.Z = wl.Z[:, :1, :].copy()
+        wl.q, wl.M = 1, M
+    comp = bi.composite_hyperparameters(wl, d_route)
+    _announce("composite", cfg, seed, M, comp.d_route)
+    g = gpu_run(wl, comp=comp)
+    o = oracle_score(oracle_fit(wl, comp), wl)
+    assert_close(g["mu"], o["mu"], TOL_MU, "mu")
+    assert_close(g["sigma"], o["sigma"], TOL_SIGMA, "sigma")
+    assert_close(g["ehvi"], o["ehvi"], TOL_EHVI, "ehvi")
+    check_argmax(g["idx"], o["ehvi"])
+
+
+def test_composite_near_data():
+    _announce("composite near data")
+    wl = bi.make_config(2, seed=2, M=8)
+    comp = bi.composite_hyperparameters(wl)
+    cand = bi.near_data_candidates(wl, 600, scale=0.01)
+    g = gpu_run(wl, cand=cand, comp=comp)
+    o = oracle_score(oracle_fit(wl, comp), wl, cand=cand)
+    assert_close(g["mu"], o["mu"], TOL_MU, "mu near data")
+    # variance through sigma^2 with the absolute bound of the plain kernel's
+    # near-data test (unit prior variance), scaled by the largest prior
+    # variance s_route + s_dep w^2 + s_int of these points
+    c = cand[:, 0, :].astype(np.float64)
+    w = np.exp(c[:, comp.d_route:] @ comp.pref.astype(np.float64).T)       # [N, m]
+    prior_max = float(np.max(comp.s_route + comp.s_int + comp.s_dep * w * w))
+    var_tol = (1e-4, 4e-6 * (wl.n ** 0.5) / 32.0 * 8 * max(prior_max, 1.0))
+    assert_close(g["sigma"] ** 2, o["sigma"] ** 2, var_tol, "variance near data")
+    assert_close(g["ehvi"], o["ehvi"], (2e-3, 1e-5), "ehvi near data")
+
+
+def test_composite_config3_full_size_sampled():
+    _announce("composite config3 full sampled")
+    wl = bi.make_config(3, seed=0)
+    comp = bi.composite_hyperparameters(wl)
+    g = gpu_run(wl, comp=comp)
+    r = np.random.default_rng(21)
+    idx = np.unique(np.concatenate([[0, 1, wl.M - 1, wl.M // 2], r.integers(0, wl.M, 300)]))
+    model = oracle_fit(wl, comp)
+    o = oracle_score(model, wl, cand=wl.cand[idx])
+    assert_close(g["mu"][idx], o["mu"], TOL_MU, "mu (sampled)")
+    assert_close(g["sigma"][idx], o["sigma"], TOL_SIGMA, "sigma (sampled)")
+    assert_close(g["ehvi"][idx], o["ehvi"], TOL_EHVI, "ehvi (sampled)")
+    e = g["ehvi"].astype(np.float64)
+    top = e.max()
+    pool = np.nonzero(e >= top - 2 * (TOL_EHVI[0] * abs(top) + TOL_EHVI[1]) - 1e-3 * abs(top))[0]
+    assert pool.size < 4096, pool.size
+    op = oracle_score(model, wl, cand=wl.cand[pool])
+    assert_close(e[pool], op["ehvi"], TOL_EHVI, "ehvi (top pool)")
+    check_argmax(g["idx"], op["ehvi"], idx_pool=pool)
+
+
+def test_composite_rejects_batches_and_bad_arguments():
+    import paper_2602_10729_amd as bo
+    _announce("composite argument checks")
+    wl = bi.make_config(4, seed=0, M=4)
+    comp = bi.composite_hyperparameters(wl)
+    X, Y = to_dev(wl.X), to_dev(wl.Y)
+    model = bo.fit_composite(X, Y, comp.d_route, wl.lengthscale, comp.s_route, comp.s_dep,
+                             comp.s_int, comp.pref, wl.noise)
+    with pytest.raises(bo.BoError) as ei:
+        bo.score(model, to_dev(wl.cand), wl.ref, to_dev(wl.Z))
+    assert ei.value.name == "BO_ERR_INVALID_ARGUMENT"
+    for dr in (0, wl.d):
+        with pytest.raises(bo.BoError) as ei:
+            bo.fit_composite(X, Y, dr, wl.lengthscale, comp.s_route, comp.s_dep, comp.s_int,
+                             np.zeros((wl.m, max(wl.d - dr, 0)), np.float32), wl.noise)
+        assert ei.value.name == "BO_ERR_INVALID_ARGUMENT"
+    # d = 32 with one routing coordinate: padded groups need 4 + 32 slots
+    r = np.random.default_rng(0)
+    X32 = to_dev(r.random((8, 32)).astype(np.float32))
+    Y32 = to_dev(r.standard_normal((8, 2)).astype(np.float32))
+    with pytest.raises(bo.BoError) as ei:
+        bo.fit_composite(X32, Y32, 1, np.ones((2, 32), np.float32), np.ones(2, np.float32),
+                         np.ones(2, np.float32), np.zeros(2, np.float32),
+                         np.zeros((2, 31), np.float32), np.full(2, 1e-4, np.float32))
+    assert ei.value.name == "BO_ERR_CAPACITY"

@@ -223,3 +223,26 @@ def test_score_reuses_model_with_new_reference_point():
         torch.cuda.synchronize()
         o = oracle_score(om, wl, ref=ref)
         assert_close(e.cpu().numpy(), o["ehvi"], TOL_EHVI, f"ehvi ref shift {shift}")
+
+
+def test_low_dimension_batches():
+    """d <= 4 (one float4 of coordinates) with q = 2 and 4: every column of a
+    64-point tile, including the prior cross-covariances of batch mates kept
+    next to the staging area."""
+    r = np.random.default_rng(31)
+    # lengthscales short enough for a well-conditioned K (cond < 50)
+    for d, q, n, lo, hi in [(3, 2, 40, 0.05, 0.12), (4, 4, 40, 0.08, 0.16), (2, 4, 32, 0.03, 0.06)]:
+        _announce("low-d batches", d, q)
+        wl = bi.make_config(0, seed=1, M=8)
+        X = r.random((n, d)).astype(np.float32)
+        Y = r.standard_normal((n, 2)).astype(np.float32)
+        wl.X, wl.Y, wl.d, wl.n, wl.q = X, Y, d, n, q
+        wl.lengthscale = r.uniform(lo, hi, size=(2, d)).astype(np.float32)
+        wl.cand = r.random((300, q, d)).astype(np.float32)
+        wl.Z = r.standard_normal((128, q, 2)).astype(np.float32)
+        wl.ref = (Y.astype(np.float64).min(0) - 0.1).astype(np.float32)
+        g = gpu_run(wl)
+        o = oracle_score(oracle_fit(wl), wl)
+        assert_close(g["mu"], o["mu"], TOL_MU, f"mu d={d} q={q}")
+        assert_close(g["sigma"], o["sigma"], TOL_SIGMA, f"sigma d={d} q={q}")
+        assert_close(g["ehvi"], o["ehvi"], TOL_EHVI, f"ehvi d={d} q={q}")
