@@ -301,6 +301,7 @@ __device__ __forceinline__ void mfma_pair_half(int r0, const AFrag (&av)[RB], co
 struct Ctx {
   __amdgpu_buffer_rsrc_t lp_rs;   // packed fragments of this objective
   int nb, nbj, zero_blk, n_pad, wave, tid;
+  int poff;                 // the block produced at step J is J + poff (this pass)
   int voff;                 // this lane's byte offset inside a fragment plane
   const _Float16* Kb;       // this lane's B-fragment base inside the ring
   float* xst;               // training-row staging (4 blocks)
@@ -334,11 +335,11 @@ __device__ __forceinline__ void step(const Ctx& C, const PosteriorArgs& a, Produ
   static_assert(NCB == 4, "two halves of two column blocks");
   // the staging load goes first among the step's loads and its store last,
   // so the store waits for it alone, a whole step after it was issued
-  stage_load(S, a, J + 4);
+  stage_load(S, a, J + C.poff + 2);
   __builtin_amdgcn_sched_barrier(0);
   BHalf B1;
   load_b<NT>(C, J, 1, B1);
-  if constexpr (PROD) produce(P, a, J + 2, C.xst, ring);
+  if constexpr (PROD) produce(P, a, J + C.poff, C.xst, ring);
   // slot pairs in turn, each pair's fragments for J + 1 requested as soon as
   // its MFMAs are issued (about half a step before the next step needs them);
   // the next block's first B half is read once the last pair is done with it
@@ -367,18 +368,18 @@ __device__ __forceinline__ void step(const Ctx& C, const PosteriorArgs& a, Produ
     }
   }
   __builtin_amdgcn_sched_barrier(0);
-  stage_store(S, C.xst, J + 4);
+  stage_store(S, C.xst, J + C.poff + 2);
   lds_barrier();
 }
 
 // Steps [j0, j1) for slots [LO, RB); the producer runs at the steps whose
-// block J + 2 lies in the pass's production window [pw0, pw1).
+// block J + poff lies in the pass's production window [pw0, pw1).
 template <int LO, int RB, int NT, int DX4, bool COMP>
 __device__ __forceinline__ void span(const Ctx& C, const PosteriorArgs& a, Producer<NT, DX4, COMP>& P,
                                      Stager<DX4, COMP>& S, _Float16* ring, const Slots<RB>& sl, int j0,
                                      int j1, int pw0, int pw1, BHalf& B0, AFrag (&av)[RB],
                                      floatx4 (&acc)[RB][NT / 16]) {
-  const int p0 = min(max(pw0 - 2, j0), j1), p1 = min(max(pw1 - 2, p0), j1);
+  const int p0 = min(max(pw0 - C.poff, j0), j1), p1 = min(max(pw1 - C.poff, p0), j1);
   int J = j0;
   for (; J < p0; ++J) step<LO, RB, NT, DX4, COMP, false>(C, a, P, S, ring, sl, J, B0, av, acc);
   for (; J < p1; ++J) step<LO, RB, NT, DX4, COMP, true>(C, a, P, S, ring, sl, J, B0, av, acc);
@@ -519,18 +520,27 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
       sl.last[r] = I < a.nb ? I / 2 : -1;
       av[r] = load_a(C.lp_rs, C.voff, frag_block(sl.first[r], sl.last[r], 0, C.zero_blk));
     }
+    // Production schedule. Starting over, blocks 0 and 1 are made here and
+    // block J + 2 at step J (poff = 2). A pass that finds blocks 0..have-1
+    // in the ring makes block have - 1 + J at step J >= 1 (poff = have - 1),
+    // into the slot of block J - 1, which no wave reads after step J - 1:
+    // the new blocks are made during the pass's first steps, where every
+    // slot is live and the matrix cores have the most work to hide them
+    // behind. Staging runs two blocks ahead of production.
+    const int have0 = have;
+    const int sb = have0 ? have0 : 0;    // first block staged here
     // the previous pass may still read the staging slots
     lds_barrier();
     {
-      // blocks 0..3 at once: one load latency, not four
+      // four blocks at once: one load latency, not four
       Stager<DX4, COMP> S4[4];
 #pragma unroll
       for (int jb = 0; jb < 4; ++jb) {
         S4[jb] = S;
-        stage_load(S4[jb], a, jb);
+        stage_load(S4[jb], a, sb + jb);
       }
 #pragma unroll
-      for (int jb = 0; jb < 4; ++jb) stage_store(S4[jb], xst, jb);
+      for (int jb = 0; jb < 4; ++jb) stage_store(S4[jb], xst, sb + jb);
     }
     lds_barrier();
     if (have == 0) {
@@ -541,6 +551,7 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
       have = 2;
       lds_barrier();
     }
+    C.poff = have0 ? have0 - 1 : 2;
     const int pw0 = have, pw1 = jpass;   // blocks this pass produces
     BHalf B0;
     load_b<NT>(C, 0, 0, B0);
