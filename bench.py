@@ -293,6 +293,21 @@ def main(argv=None):
             "unit": "TFLOP/s", "frac": f16_launch / (c_launch / 1e3) / 1e12 / PEAK_FP16_MFMA_TFLOPS,
             "score_candidates_per_s": wl.M / ((cpost_ms / max(cc, 1) + ehvi_launch_ms) / 1e3),
         }
+    # hyperparameter fit: one exact log marginal likelihood + gradient
+    # evaluation (synchronous), the unit of work of the host optimiser's loop
+    bo.mll(X, Y, wl.lengthscale, wl.outputscale, wl.noise, stream=stream)
+    t0 = time.perf_counter()
+    reps = 5
+    for _ in range(reps):
+        bo.mll(X, Y, wl.lengthscale, wl.outputscale, wl.noise, stream=stream)
+    mll_ms = (time.perf_counter() - t0) * 1e3 / reps
+    n3 = float(wl.n) ** 3
+    rec["mll"] = {
+        "ms_per_evaluation": mll_ms, "evaluations_per_s": 1e3 / mll_ms,
+        "gradient_entries": wl.m * (wl.d + 2),
+        "fp64_flops": wl.m * (n3 / 3 + n3 / 3 + n3 / 3),
+        "note": "fp64: factor n^3/3 + carried inverse n^3/3 + K^-1 = W^T W n^3/3 per objective",
+    }
     if not a.no_peaks:
         rec["measured_peaks"] = {
             "valu_fma_lane_ops_per_s": bo.measure_peak(bo.PEAK_VALU_FMA, 65536),

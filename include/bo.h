@@ -139,6 +139,32 @@ bo_status bo_fit_composite(const float* X, const float* Y, int64_t n, int32_t d,
                            void* stream, bo_model* out);
 
 /*
+ * bo_mll — exact log marginal likelihood of each objective's GP and its
+ * gradient, for fitting the hyperparameters.
+ *
+ * Paper: implementation section (the ARD lengthscales and the scales are
+ * learned by maximising the GP marginal likelihood). The outer optimiser
+ * runs on the host and calls this for each trial point.
+ *
+ * For objective k, with K = s M52 + eta I exactly as in bo_fit:
+ *   value[k] = -1/2 y^T K^{-1} y - 1/2 log det K - n/2 log(2 pi)
+ *   grad[k][j] = d value[k] / d theta_j,
+ *     theta = (log l_1 .. log l_d, log s, log eta)
+ *           = 1/2 tr((alpha alpha^T - K^{-1}) dK/dtheta_j),  alpha = K^{-1} y.
+ * Everything runs in fp64 on the device: the Cholesky factor and L^{-1} as
+ * in bo_fit, K^{-1} = L^{-T} L^{-1}, the log-determinant from the diagonal
+ * of L, and the trace terms over all pairs of observations.
+ *
+ * X, Y, n, d, m, lengthscale, outputscale, noise: as bo_fit
+ * value  host [m] out;  grad  host [m][d + 2] out (fp64)
+ * Synchronous; no model is created. Errors: as bo_fit (NOT_POSITIVE_DEFINITE
+ * when K is not positive definite).
+ */
+bo_status bo_mll(const float* X, const float* Y, int64_t n, int32_t d, int32_t m,
+                 const float* lengthscale, const float* outputscale, const float* noise,
+                 void* stream, double* value, double* grad);
+
+/*
  * bo_score — posterior plus Monte-Carlo (q)EHVI for M candidates.
  *
  * Paper: "Constrained qNEHVI" paragraph (expected HVI over samples of the

@@ -11,9 +11,11 @@ the surrogate-fitting and acquisition-optimisation steps of the MOBO
 workflow, the constrained qNEHVI paragraph, and the implementation section
 "MOBO optimization kernels"):
 
-* ``gp``      — ARD Matern-5/2 covariance with an output scale, exact GP
-                conditioning by Cholesky, posterior mean / variance / q-batch
-                covariance and its PSD Cholesky factor.
+* ``gp``      — ARD Matern-5/2 covariance with an output scale (and the
+                paper's composite kernel), exact GP conditioning by
+                Cholesky, posterior mean / variance / q-batch covariance and
+                its PSD Cholesky factor, and the exact log marginal
+                likelihood with its gradient.
 * ``pareto``  — non-dominated set of the observations and a disjoint box
                 decomposition of the region a new point can improve.
 * ``acq``     — hypervolume improvement of one point or of a q-batch
@@ -26,14 +28,14 @@ All arithmetic is fp64 on fp32-rounded inputs. Readings of points the paper
 leaves open are listed in each function's docstring.
 """
 from .gp import (GPModel, Composite, matern52, matern32, composite_cov, pref_weight,
-                 scaled_distance, fit, posterior,
+                 scaled_distance, fit, posterior, mll,
                  chol_psd, NotPositiveDefinite)
 from .pareto import nondominated, pareto_front, boxes_2d, boxes_3d, box_decomposition
 from .acq import hvi, qhvi, feasible, ehvi_q1, qehvi, score, argmax
 
 __all__ = [
     "GPModel", "Composite", "matern52", "matern32", "composite_cov", "pref_weight",
-    "scaled_distance", "fit", "posterior", "chol_psd",
+    "scaled_distance", "fit", "posterior", "mll", "chol_psd",
     "NotPositiveDefinite", "nondominated", "pareto_front", "boxes_2d",
     "boxes_3d", "box_decomposition", "hvi", "qhvi", "feasible", "ehvi_q1", "qehvi",
     "score", "argmax",

@@ -241,3 +241,45 @@ def chol_psd(Sig: np.ndarray, s) -> np.ndarray:
             num = Sig[..., i, j] - np.sum(C[..., i, :j] * C[..., j, :j], axis=-1)
             C[..., i, j] = np.where(ok, num / np.where(ok, cjj, 1.0), 0.0)
     return C
+
+
+def mll(X, Y, ls, s, eta):
+    """Exact log marginal likelihood of each objective's GP and its gradient.
+
+    Paper: implementation section (lengthscales learned by maximising the GP
+    marginal likelihood). For objective k with K = s M52 + eta I:
+      log p(y) = -1/2 y^T K^{-1} y - 1/2 log det K - n/2 log(2 pi),
+    log det K = 2 sum_i log L_ii. Gradient with respect to
+    theta = (log l_1 .. log l_d, log s, log eta):
+      d log p / d theta_j = 1/2 tr((alpha alpha^T - K^{-1}) dK/dtheta_j),
+    with dK/dlog l_t = (5/3) s (1 + sqrt5 r) exp(-sqrt5 r) u_t^2
+    (u_t = (x_it - x_i't) / l_t), dK/dlog s = s M52, dK/dlog eta = eta I.
+    Returns (value [m], grad [m, d + 2]).
+    """
+    X = np.asarray(X, dtype=np.float64)
+    Y = np.asarray(Y, dtype=np.float64)
+    n, d = X.shape
+    m = Y.shape[1]
+    ls = np.asarray(ls, dtype=np.float64).reshape(m, d)
+    s = np.asarray(s, dtype=np.float64).reshape(-1)
+    eta = np.asarray(eta, dtype=np.float64).reshape(-1)
+    value = np.zeros(m)
+    grad = np.zeros((m, d + 2))
+    for k in range(m):
+        U = X / ls[k]                                      # scaled coordinates
+        D = U[:, None, :] - U[None, :, :]                  # [n, n, d]
+        r = np.sqrt(np.sum(D * D, axis=2))
+        K0 = matern52(r, s[k])
+        K = K0 + eta[k] * np.eye(n)
+        L = np.linalg.cholesky(K)
+        alpha = solve_triangular(L.T, solve_triangular(L, Y[:, k], lower=True), lower=False)
+        value[k] = (-0.5 * Y[:, k] @ alpha - np.sum(np.log(np.diag(L)))
+                    - 0.5 * n * math.log(2.0 * math.pi))
+        Linv = solve_triangular(L, np.eye(n), lower=True)
+        A = np.outer(alpha, alpha) - Linv.T @ Linv
+        common = (5.0 / 3.0) * s[k] * (1.0 + SQRT5 * r) * np.exp(-SQRT5 * r)
+        for t in range(d):
+            grad[k, t] = 0.5 * np.sum(A * common * D[:, :, t] ** 2)
+        grad[k, d] = 0.5 * np.sum(A * K0)
+        grad[k, d + 1] = 0.5 * eta[k] * np.trace(A)
+    return value, grad

@@ -6,7 +6,8 @@ current stream. There is no CPU fallback: if the library is missing or a
 tensor is not on the GPU, the call raises.
 
 Functions mirror the C ABI in ``include/bo.h``:
-``fit`` (``bo_fit``), ``fit_composite`` (``bo_fit_composite``), ``score`` (``bo_score``, or ``bo_score_constrained`` when feasibility
+``fit`` (``bo_fit``), ``fit_composite`` (``bo_fit_composite``), ``mll``
+(``bo_mll``), ``score`` (``bo_score``, or ``bo_score_constrained`` when feasibility
 thresholds are given), ``argmax``, ``cholesky_test`` (device) and
 ``pareto_front``, ``box_decomposition`` (host geometry, no GPU needed).
 """
@@ -18,7 +19,7 @@ from typing import Optional
 
 import numpy as np
 
-__all__ = ["BoError", "Model", "lib", "lib_path", "fit", "fit_composite", "score", "argmax",
+__all__ = ["BoError", "Model", "lib", "lib_path", "fit", "fit_composite", "mll", "score", "argmax",
            "cholesky_test", "profile_enable", "profile_read", "measure_peak", "pareto_front", "box_decomposition", "STATUS",
            "MAX_N", "MAX_D", "MAX_S", "MAX_BOXES"]
 
@@ -60,6 +61,8 @@ def lib() -> ctypes.CDLL:
     L.bo_fit_composite.argtypes = [vp, vp, i64, i32, i32, i32, fp, fp, fp, fp, fp, fp, vp,
                                    ctypes.POINTER(vp)]
     L.bo_fit_composite.restype = ctypes.c_int
+    L.bo_mll.argtypes = [vp, vp, i64, i32, i32, fp, fp, fp, vp, vp, vp]
+    L.bo_mll.restype = ctypes.c_int
     L.bo_score.argtypes = [vp, vp, i64, i32, fp, vp, i32, vp, vp, vp, vp]
     L.bo_score.restype = ctypes.c_int
     L.bo_score_constrained.argtypes = [vp, vp, i64, i32, fp, fp, vp, i32, vp, vp, vp, vp]
@@ -194,6 +197,24 @@ def fit_composite(X, Y, d_route, lengthscale, scale_route, scale_dep, scale_int,
                                 _stream(stream), ctypes.byref(h))
     _check(st, "bo_fit_composite")
     return Model(h.value, n, d, m)
+
+
+def mll(X, Y, lengthscale, outputscale, noise, stream=None):
+    """bo_mll: (value [m], gradient [m, d + 2]) of the exact log marginal
+    likelihood with respect to (log lengthscales, log outputscale, log noise)."""
+    import torch
+    n, d = X.shape
+    m = Y.shape[1]
+    ls = _host_f32(lengthscale, (m, d), "lengthscale")
+    os_ = _host_f32(outputscale, (m,), "outputscale")
+    nz = _host_f32(noise, (m,), "noise")
+    val = np.zeros(m, dtype=np.float64)
+    grad = np.zeros((m, d + 2), dtype=np.float64)
+    p = lambda a: a.ctypes.data_as(ctypes.c_void_p)
+    st = lib().bo_mll(_dev(X, "X", torch.float32), _dev(Y, "Y", torch.float32), n, d, m, p(ls),
+                      p(os_), p(nz), _stream(stream), p(val), p(grad))
+    _check(st, "bo_mll")
+    return val, grad
 
 
 def score(model: Model, cand, ref, Z, ehvi=None, mu=None, sigma=None, stream=None,

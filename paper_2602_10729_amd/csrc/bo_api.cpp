@@ -503,9 +503,125 @@ bo_status fit_impl(const char* who, const float* X, const float* Y, int64_t n, i
   return BO_OK;
 }
 
+// Log marginal likelihood and gradient: the fit's Gram, factor and alpha in
+// fp64, then the likelihood kernels; no model is kept.
+bo_status mll_impl(const float* X, const float* Y, int64_t n, int32_t d, int32_t m,
+                   const float* lengthscale, const float* outputscale, const float* noise,
+                   void* stream, double* value, double* grad) {
+  if (!value || !grad) return fail(BO_ERR_INVALID_ARGUMENT, "bo_mll: NULL output");
+  if (!lengthscale || !outputscale || !noise)
+    return fail(BO_ERR_INVALID_ARGUMENT, "bo_mll: NULL hyperparameter pointer");
+  if (n < 1 || d < 1 || (m != 2 && m != 3))
+    return fail(BO_ERR_INVALID_ARGUMENT, "bo_mll: need n >= 1, d >= 1, m in {2,3}");
+  if (n > BO_MAX_N || d > BO_MAX_D)
+    return fail(BO_ERR_CAPACITY, "bo_mll: n or d beyond compiled limits");
+  if (!all_finite(lengthscale, (size_t)m * d) || !all_finite(outputscale, m) ||
+      !all_finite(noise, m))
+    return fail(BO_ERR_NONFINITE_INPUT, "bo_mll: non-finite hyperparameter");
+  for (int i = 0; i < m * d; ++i)
+    if (!(lengthscale[i] > 0.f)) return fail(BO_ERR_INVALID_ARGUMENT, "bo_mll: lengthscale <= 0");
+  for (int k = 0; k < m; ++k) {
+    if (!(outputscale[k] > 0.f)) return fail(BO_ERR_INVALID_ARGUMENT, "bo_mll: outputscale <= 0");
+    if (!(noise[k] >= 0.f)) return fail(BO_ERR_INVALID_ARGUMENT, "bo_mll: noise < 0");
+  }
+  bo_status s;
+  if ((s = check_dev(X, sizeof(float) * n * d, "X")) != BO_OK) return s;
+  if ((s = check_dev(Y, sizeof(float) * n * m, "Y")) != BO_OK) return s;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  int dev = 0;
+  (void)hipGetDevice(&dev);
+
+  const int nf = static_cast<int>((n + kFitBlk - 1) / kFitBlk) * kFitBlk;
+  const int n_pad = static_cast<int>((n + kBlk - 1) / kBlk) * kBlk;
+  const int64_t tiles = mll_tiles(nf);
+  FitScratch fs;
+  fs.st = st;
+  struct Extra {
+    hipStream_t st = nullptr;
+    float* alpha = nullptr;
+    double* alpha64 = nullptr;
+    double* partials = nullptr;
+    double* out = nullptr;
+    ~Extra() { pfree(alpha, st); pfree(alpha64, st); pfree(partials, st); pfree(out, st); }
+  } ex;
+  ex.st = st;
+  const size_t nhyp = (size_t)m * d + 2 * m;
+  if ((s = palloc(&fs.A, (size_t)m * nf * nf, st, "fit matrix")) != BO_OK) return s;
+  if ((s = palloc(&fs.W, (size_t)m * nf * nf, st, "fit inverse")) != BO_OK) return s;
+  if ((s = palloc(&fs.hyp, nhyp, st, "hyperparameters")) != BO_OK) return s;
+  if ((s = palloc(&fs.tmp, (size_t)m * nf, st, "fit vector")) != BO_OK) return s;
+  if ((s = palloc(&fs.flag, 1, st, "flag")) != BO_OK) return s;
+  if ((s = palloc(&ex.alpha, (size_t)m * n_pad, st, "alpha")) != BO_OK) return s;
+  if ((s = palloc(&ex.alpha64, (size_t)m * nf, st, "alpha (fp64)")) != BO_OK) return s;
+  if ((s = palloc(&ex.partials, (size_t)m * tiles * (d + 2), st, "gradient partials")) != BO_OK) return s;
+  if ((s = palloc(&ex.out, (size_t)m * (d + 3), st, "likelihood")) != BO_OK) return s;
+
+  std::vector<double> hyp(nhyp);
+  for (int i = 0; i < m * d; ++i) hyp[i] = 1.0 / static_cast<double>(lengthscale[i]);
+  for (int k = 0; k < m; ++k) {
+    hyp[(size_t)m * d + k] = outputscale[k];
+    hyp[(size_t)m * d + m + k] = noise[k];
+  }
+  // pinned staging: [hyperparameters][flag][value, gradient]
+  DeviceState* DS = device_state(dev);
+  if (!DS) return fail(BO_ERR_DEVICE, "bo_mll: device index out of range");
+  std::lock_guard<std::mutex> stage_lock(DS->fit_mu);
+  const size_t off_flag = (sizeof(double) * nhyp + 15) / 16 * 16;
+  const size_t off_out = off_flag + 16;
+  const size_t need = off_out + sizeof(double) * m * (d + 3);
+  hipError_t e = hipSuccess;
+  if (need > DS->fit_stage_bytes) {
+    if (DS->fit_stage) (void)hipHostFree(DS->fit_stage);
+    DS->fit_stage = nullptr;
+    DS->fit_stage_bytes = 0;
+    const size_t cap = std::max<size_t>(need, size_t(1) << 16);
+    e = hipHostMalloc(reinterpret_cast<void**>(&DS->fit_stage), cap, hipHostMallocDefault);
+    if (e != hipSuccess) return hip_fail(e, "bo_mll: pinned staging");
+    DS->fit_stage_bytes = cap;
+  }
+  unsigned char* stage = DS->fit_stage;
+  std::memcpy(stage, hyp.data(), sizeof(double) * nhyp);
+  auto sync_fail = [&](bo_status st_) {
+    (void)hipStreamSynchronize(st);   // copies from the staging buffer may be pending
+    return st_;
+  };
+  e = hipMemcpyAsync(fs.hyp, stage, sizeof(double) * nhyp, hipMemcpyHostToDevice, st);
+  if (e == hipSuccess) e = hipMemsetAsync(fs.flag, 0, sizeof(int), st);
+  if (e != hipSuccess) return sync_fail(hip_fail(e, "bo_mll: upload"));
+
+  GramParams gp;
+  gp.ils = fs.hyp;
+  gp.os = fs.hyp + (size_t)m * d;
+  gp.noise = gp.os + m;
+  if ((s = after_launch(launch_gram(X, n, d, m, nf, gp, fs.A, st), st, "gram")) != BO_OK) return sync_fail(s);
+  if ((s = after_launch(launch_cholesky(fs.A, fs.W, nf, m, fs.flag, st), st, "cholesky")) != BO_OK) return sync_fail(s);
+  if ((s = after_launch(launch_alpha(fs.W, Y, n, m, nf, n_pad, fs.tmp, ex.alpha, st, ex.alpha64), st, "alpha")) != BO_OK) return sync_fail(s);
+  if ((s = after_launch(launch_mll(X, n, d, m, nf, gp, fs.A, fs.W, fs.tmp, ex.alpha64, ex.partials, ex.out, st), st, "likelihood")) != BO_OK) return sync_fail(s);
+  e = hipMemcpyAsync(stage + off_flag, fs.flag, sizeof(int), hipMemcpyDeviceToHost, st);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(stage + off_out, ex.out, sizeof(double) * m * (d + 3), hipMemcpyDeviceToHost, st);
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  if (e != hipSuccess) return hip_fail(e, "bo_mll: sync");
+  int flag = 0;
+  std::memcpy(&flag, stage + off_flag, sizeof(int));
+  if (flag) return fail(BO_ERR_NOT_POSITIVE_DEFINITE, "bo_mll: non-positive Cholesky pivot");
+  const double* o = reinterpret_cast<const double*>(stage + off_out);
+  for (int k = 0; k < m; ++k) {
+    value[k] = o[k * (d + 3)];
+    for (int j = 0; j < d + 2; ++j) grad[(size_t)k * (d + 2) + j] = o[k * (d + 3) + 1 + j];
+  }
+  return BO_OK;
+}
+
 }  // namespace
 
 extern "C" {
+
+bo_status bo_mll(const float* X, const float* Y, int64_t n, int32_t d, int32_t m,
+                 const float* lengthscale, const float* outputscale, const float* noise,
+                 void* stream, double* value, double* grad) {
+  return mll_impl(X, Y, n, d, m, lengthscale, outputscale, noise, stream, value, grad);
+}
 
 bo_status bo_fit(const float* X, const float* Y, int64_t n, int32_t d, int32_t m,
                  const float* lengthscale, const float* outputscale, const float* noise,

@@ -93,10 +93,20 @@ hipError_t launch_weights(const float* X, int64_t n, int d, int m, int n_pad,
 // *flag is set non-zero on a non-positive or non-finite pivot.
 hipError_t launch_cholesky(double* A, double* W, int nf, int m, int* flag,
                            hipStream_t st);
-// alpha_k = W_k^T (W_k y_k), y from Y [n][m] (fp32), written fp32 [m][n_pad].
+// alpha_k = W_k^T (W_k y_k), y from Y [n][m] (fp32), written fp32 [m][n_pad]
+// (and, when alpha64 is not NULL, fp64 [m][nf]). tmp [m][nf] keeps W_k y_k.
 hipError_t launch_alpha(const double* W, const float* Y, int64_t n, int m,
                         int nf, int n_pad, double* tmp, float* alpha,
-                        hipStream_t st);
+                        hipStream_t st, double* alpha64 = nullptr);
+// Log marginal likelihood parts and gradient (fp64) from the factored fit
+// scratch: A holds L (lower), W = L^{-1}, tmp = W y, alpha64 = K^{-1} y.
+// Overwrites A's lower 64-blocks with K^{-1} = W^T W. partials:
+// [m][tiles16][d + 2] scratch with tiles16 = mll_tiles(nf); out [m][1 + d + 2]
+// = (value, gradient).
+int64_t mll_tiles(int nf);
+hipError_t launch_mll(const float* X, int64_t n, int d, int m, int nf, const GramParams& g,
+                      double* A, const double* W, const double* tmp, const double* alpha64,
+                      double* partials, double* out, hipStream_t st);
 // Pack W into the posterior's A-fragment format (fp16 hi/lo planes of 16x32
 // lower blocks, zeros beyond n, then one all-zero block; 2 KiB per block,
 // posterior_frag_blocks(nb) blocks per objective) and write the

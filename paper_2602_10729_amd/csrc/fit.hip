@@ -442,7 +442,8 @@ __global__ __launch_bounds__(256) void k_wy(const double* __restrict__ W,
 __global__ __launch_bounds__(256) void k_wty(const double* __restrict__ W,
                                              const double* __restrict__ tmp,
                                              int64_t n, int nf, int n_pad,
-                                             float* __restrict__ alpha) {
+                                             float* __restrict__ alpha,
+                                             double* __restrict__ alpha64) {
   __shared__ double part[16][17];
   const int k = blockIdx.y;
   const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
@@ -465,6 +466,7 @@ __global__ __launch_bounds__(256) void k_wty(const double* __restrict__ W,
 #pragma unroll
     for (int t = 0; t < 16; ++t) v += part[t][tx];
     alpha[(int64_t)k * n_pad + j] = (j < n) ? static_cast<float>(v) : 0.f;
+    if (alpha64 && j < nf) alpha64[(int64_t)k * nf + j] = (j < n) ? v : 0.0;
   }
 }
 
@@ -531,6 +533,152 @@ __global__ __launch_bounds__(256) void k_scale_x(const float* __restrict__ X, in
   Xs[(int64_t)k * n_pad * dx + e] = v;
 }
 
+// ---- log marginal likelihood and its gradient ------------------------------
+//
+// value = -1/2 y^T K^{-1} y - sum_i log L_ii - n/2 log(2 pi), with
+// y^T K^{-1} y = |W y|^2 (tmp = W y); gradient over theta = (log l, log s,
+// log eta): 1/2 sum_{i,i'} (alpha_i alpha_i' - Kinv_ii') dK_ii'/dtheta.
+
+// out[k][0] = value (one workgroup per objective)
+__global__ __launch_bounds__(256) void k_logdet_quad(const double* __restrict__ A,
+                                                     const double* __restrict__ tmp,
+                                                     int64_t n, int nf, double* __restrict__ out,
+                                                     int d) {
+  __shared__ double red[2][4];
+  const int k = blockIdx.x;
+  const double* Ak = A + (int64_t)k * nf * nf;
+  const double* tk = tmp + (int64_t)k * nf;
+  double q = 0.0, ld = 0.0;
+  for (int64_t i = threadIdx.x; i < n; i += 256) {
+    q = fma(tk[i], tk[i], q);
+    ld += log(Ak[i * nf + i]);
+  }
+  for (int off = 32; off > 0; off >>= 1) {
+    q += __shfl_xor(q, off);
+    ld += __shfl_xor(ld, off);
+  }
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) {
+    red[0][w] = q;
+    red[1][w] = ld;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const double qq = red[0][0] + red[0][1] + red[0][2] + red[0][3];
+    const double ll = red[1][0] + red[1][1] + red[1][2] + red[1][3];
+    out[(int64_t)k * (d + 3)] =
+        -0.5 * qq - ll - 0.5 * static_cast<double>(n) * 1.83787706640934548356;   // log(2 pi)
+  }
+}
+
+// K^{-1} = W^T W into the lower 64-blocks of A: tile (I, J), I >= J, sums
+// W[K][I]^T W[K][J] over K >= I (W is zero above its diagonal).
+__global__ __launch_bounds__(256) void k_kinv(double* __restrict__ A, const double* __restrict__ W,
+                                              int nf) {
+  __shared__ double p[B][LDP];
+  __shared__ double q[B][LDP];
+  const int k = blockIdx.y;
+  const int t = blockIdx.x;
+  int I = static_cast<int>((sqrt(8.0 * t + 1.0) - 1.0) * 0.5);
+  while ((I + 1) * (I + 2) / 2 <= t) ++I;
+  while (I * (I + 1) / 2 > t) --I;
+  const int J = t - I * (I + 1) / 2;
+  const int nbk = nf / B;
+  const double* Wk = W + (int64_t)k * nf * nf;
+  const int tx = threadIdx.x % 16, ty = threadIdx.x / 16;
+  double acc[4][4] = {};
+  for (int K = I; K < nbk; ++K) {
+    __syncthreads();   // the previous step's tiles are no longer read
+    load_blocks<true, true>(p, Wk + (int64_t)K * B * nf + I * B,
+                            q, Wk + (int64_t)K * B * nf + J * B, nf);
+    __syncthreads();
+    gemm_nt_64(p, q, acc, ty, tx);
+  }
+  double* dst = A + (int64_t)k * nf * nf + (int64_t)I * B * nf + J * B;
+#pragma unroll
+  for (int r = 0; r < 4; ++r)
+#pragma unroll
+    for (int c = 0; c < 4; ++c) dst[(int64_t)(ty * 4 + r) * nf + tx * 4 + c] = acc[r][c];
+}
+
+// Gradient partials of one 16x16 tile of observation pairs (i >= i') per
+// workgroup: [tile][d + 2] = 1/2 sum w (alpha_i alpha_i' - Kinv_ii') dK/dtheta,
+// w = 2 off the diagonal (the symmetric partner), 1 on it.
+__global__ __launch_bounds__(256) void k_mll_grad(const float* __restrict__ X, int64_t n, int d,
+                                                  int nf, GramParams g,
+                                                  const double* __restrict__ A,
+                                                  const double* __restrict__ alpha64,
+                                                  double* __restrict__ partials) {
+  __shared__ double red[4][BO_MAX_D + 2];
+  const int k = blockIdx.y;
+  const int64_t t = blockIdx.x;
+  int64_t bi = static_cast<int64_t>((sqrt(8.0 * t + 1.0) - 1.0) * 0.5);
+  while ((bi + 1) * (bi + 2) / 2 <= t) ++bi;
+  while (bi * (bi + 1) / 2 > t) --bi;
+  const int64_t bj = t - bi * (bi + 1) / 2;
+  const int64_t i = bi * 16 + threadIdx.x / 16;
+  const int64_t j = bj * 16 + threadIdx.x % 16;
+  double acc[BO_MAX_D + 2];
+#pragma unroll
+  for (int e = 0; e < BO_MAX_D + 2; ++e) acc[e] = 0.0;
+  if (i < n && j < n && j <= i) {
+    const double* ils = g.ils + k * d;
+    const double s = g.os[k];
+    const double a = alpha64[(int64_t)k * nf + i] * alpha64[(int64_t)k * nf + j] -
+                     A[((int64_t)k * nf + i) * nf + j];
+    const double wgt = (i == j) ? 0.5 : 1.0;     // 1/2 x (2 off the diagonal)
+    double r2 = 0.0;
+    double u2[BO_MAX_D];
+#pragma unroll
+    for (int e = 0; e < BO_MAX_D; ++e) {
+      u2[e] = 0.0;
+      if (e < d) {
+        const double u = (static_cast<double>(X[i * d + e]) - static_cast<double>(X[j * d + e])) * ils[e];
+        u2[e] = u * u;
+        r2 += u2[e];
+      }
+    }
+    const double r = sqrt(r2);
+    const double c5 = 2.23606797749978969641;
+    const double ex = exp(-c5 * r);
+    const double common = (5.0 / 3.0) * s * (1.0 + c5 * r) * ex;
+    const double k0 = s * (1.0 + c5 * r + (5.0 / 3.0) * r2) * ex;
+#pragma unroll
+    for (int e = 0; e < BO_MAX_D; ++e)
+      if (e < d) acc[e] = wgt * a * common * u2[e];
+    acc[d] = wgt * a * k0;
+    acc[d + 1] = (i == j) ? 0.5 * a * g.noise[k] : 0.0;
+  }
+  // reduce the d + 2 sums over the workgroup
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+#pragma unroll
+  for (int e = 0; e < BO_MAX_D + 2; ++e) {
+    if (e < d + 2) {
+      double v = acc[e];
+      for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+      if (lane == 0) red[w][e] = v;
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x < d + 2) {
+    const int e = threadIdx.x;
+    partials[((int64_t)k * gridDim.x + t) * (d + 2) + e] =
+        red[0][e] + red[1][e] + red[2][e] + red[3][e];
+  }
+}
+
+// out[k][1 + e] = sum over tiles of partials (fixed order: deterministic)
+__global__ __launch_bounds__(64) void k_mll_reduce(const double* __restrict__ partials,
+                                                   int64_t tiles, int d,
+                                                   double* __restrict__ out) {
+  const int k = blockIdx.x;
+  for (int e = threadIdx.x; e < d + 2; e += 64) {
+    double v = 0.0;
+    for (int64_t t = 0; t < tiles; ++t) v += partials[((int64_t)k * tiles + t) * (d + 2) + e];
+    out[(int64_t)k * (d + 3) + 1 + e] = v;
+  }
+}
+
 __global__ void k_lower_to_f32(const double* __restrict__ A, int64_t n, int nf,
                                float* __restrict__ L) {
   const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
@@ -586,10 +734,29 @@ hipError_t launch_cholesky(double* A, double* W, int nf, int m, int* flag,
 }
 
 hipError_t launch_alpha(const double* W, const float* Y, int64_t n, int m, int nf,
-                        int n_pad, double* tmp, float* alpha, hipStream_t st) {
+                        int n_pad, double* tmp, float* alpha, hipStream_t st,
+                        double* alpha64) {
   hipLaunchKernelGGL(k_wy, dim3((nf + 3) / 4, m), dim3(256), 0, st, W, Y, n, m, nf, tmp);
   hipLaunchKernelGGL(k_wty, dim3((n_pad + 15) / 16, m), dim3(256), 0, st, W, tmp, n,
-                     nf, n_pad, alpha);
+                     nf, n_pad, alpha, alpha64);
+  return hipGetLastError();
+}
+
+int64_t mll_tiles(int nf) {
+  const int64_t t = nf / 16;
+  return t * (t + 1) / 2;
+}
+
+hipError_t launch_mll(const float* X, int64_t n, int d, int m, int nf, const GramParams& g,
+                      double* A, const double* W, const double* tmp, const double* alpha64,
+                      double* partials, double* out, hipStream_t st) {
+  hipLaunchKernelGGL(k_logdet_quad, dim3(m), dim3(256), 0, st, A, tmp, n, nf, out, d);
+  const int nbk = nf / B;
+  hipLaunchKernelGGL(k_kinv, dim3(nbk * (nbk + 1) / 2, m), dim3(256), 0, st, A, W, nf);
+  const int64_t tiles = mll_tiles(nf);
+  hipLaunchKernelGGL(k_mll_grad, dim3(static_cast<unsigned>(tiles), m), dim3(256), 0, st, X, n,
+                     d, nf, g, A, alpha64, partials);
+  hipLaunchKernelGGL(k_mll_reduce, dim3(m), dim3(64), 0, st, partials, tiles, d, out);
   return hipGetLastError();
 }
 
