@@ -141,7 +141,8 @@ struct Producer {
 };
 
 // Training rows staged in LDS, one 32-row block per slot, four slots: row
-// r of block b at slot b % 4, [kJ][dx + 4] floats per slot, the last float4
+// r of block b at slot b % 4 (position stage_pos(r)), [kJ][dx + 4] floats
+// per slot, the last float4
 // of a row holding (alpha, w, 0, 0), w the preference weight of the row
 // (composite kernel; 0 otherwise). Step J loads the rows of block J + 4
 // first and stores them last, while the producer reads block J + 2. Every
@@ -159,6 +160,16 @@ struct Stager {
   int row, t4;
   __amdgpu_buffer_rsrc_t xs_rs, al_rs, wt_rs;
 };
+
+// Position of staged row r inside its slot: rows are interleaved so that the
+// producer's lane groups, which read rows g*RPL + u (g = 0 .. kJ/RPL - 1) at
+// the same time, find them kJ/RPL positions apart in consecutive row
+// positions; with an odd number of float4s per row the groups' reads then
+// fall in distinct LDS bank groups (contiguous rows would collide 4 ways).
+template <int RPL>
+__device__ __forceinline__ int stage_pos(int r) {
+  return (r % RPL) * (kJ / RPL) + r / RPL;
+}
 
 // Rows past n_pad read zeros (buffer range check), so blocks past the matrix
 // that the producer may evaluate carry zero alpha and add nothing to mu.
@@ -193,7 +204,10 @@ __device__ __forceinline__ void produce(Producer<NT, DX4, COMP>& P, const Poster
   constexpr int RS = Stager<DX4, COMP>::RS;
   typedef _Float16 halfr __attribute__((ext_vector_type(RPL)));
   halfr hi, lo;
-  const float* xr = xst + (jb & 3) * Stager<DX4, COMP>::kSlot + P.row0 * RS;
+  // staged rows are interleaved (see stage_pos): this lane's row row0 + u
+  // sits at position u * (kJ / RPL) + row0 / RPL
+  constexpr int US = (kJ / RPL) * RS;
+  const float* xr = xst + (jb & 3) * Stager<DX4, COMP>::kSlot + (P.row0 / RPL) * RS;
 #pragma unroll
   for (int u = 0; u < RPL; ++u) {
     float r2 = 0.f, r2r = 0.f;    // r2r: composite, the routing part
@@ -206,7 +220,7 @@ __device__ __forceinline__ void produce(Producer<NT, DX4, COMP>& P, const Poster
           r2 = 0.f;
         }
       }
-      const float4 x = *reinterpret_cast<const float4*>(xr + u * RS + 4 * t4);
+      const float4 x = *reinterpret_cast<const float4*>(xr + u * US + 4 * t4);
       const float d0 = P.c[4 * t4 + 0] - x.x;
       const float d1 = P.c[4 * t4 + 1] - x.y;
       const float d2 = P.c[4 * t4 + 2] - x.z;
@@ -223,11 +237,11 @@ __device__ __forceinline__ void produce(Producer<NT, DX4, COMP>& P, const Poster
       // s_route M52(r_route) + s_dep w* w_i M32(r_dep) + s_int M52 M32
       const float k5 = matern52_f(r2r, 1.0f);
       const float k3 = matern32_f(r2);
-      kv = fmaf(P.wsd * xr[u * RS + 4 * DX4 + 1], k3, k5 * fmaf(a.s_int, k3, a.s));
+      kv = fmaf(P.wsd * xr[u * US + 4 * DX4 + 1], k3, k5 * fmaf(a.s_int, k3, a.s));
     } else {
       kv = matern52_f(r2, a.s);
     }
-    P.mu = fmaf(xr[u * RS + 4 * DX4], kv, P.mu);
+    P.mu = fmaf(xr[u * US + 4 * DX4], kv, P.mu);
     const _Float16 h = static_cast<_Float16>(kv);
     hi[u] = h;
     lo[u] = static_cast<_Float16>(kv - static_cast<float>(h));
@@ -484,7 +498,9 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
   if constexpr (COMP) S.wt_rs = make_rsrc(a.wts, n_pad * 4);
   S.row = min(tid / (DX4 + 1), kJ - 1);
   S.t4 = tid % (DX4 + 1);
-  S.soff = (tid < Stager<DX4, COMP>::kF4) ? S.row * Stager<DX4, COMP>::RS + 4 * S.t4 : -1;
+  S.soff = (tid < Stager<DX4, COMP>::kF4)
+               ? stage_pos<Prod::RPL>(S.row) * Stager<DX4, COMP>::RS + 4 * S.t4
+               : -1;
   C.n_pad = n_pad;
   C.wave = wave;
   C.tid = tid;
