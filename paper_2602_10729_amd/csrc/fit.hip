@@ -200,10 +200,15 @@ __device__ __forceinline__ void chol_inv64(double (*a)[LDP], double (*x)[LDP], d
     }
     if (w == jw) row[c] = xv[jt];
     __syncthreads();
-    // all three reads issued together, ahead of the pivot's arithmetic
+    // every read of the step is issued together, ahead of the arithmetic,
+    // so their latencies overlap (one wait, not one per read)
     const double a_jj = pivbuf[jt & 1];
     const double a_cj = col[c];
     const double x_jc = row[c];
+    double2 l[8];
+#pragma unroll
+    for (int t = 0; t < 8; ++t) l[t] = *reinterpret_cast<const double2*>(col + 16 * w + 2 * t);
+    __builtin_amdgcn_sched_barrier(0);
     const bool bad = !(a_jj > 0.0) || !isfinite(a_jj);
     const double d = bad ? 1.0 : a_jj;
     bad_any = bad_any || bad;
@@ -213,11 +218,10 @@ __device__ __forceinline__ void chol_inv64(double (*a)[LDP], double (*x)[LDP], d
     const double xs = x_jc * id;
 #pragma unroll
     for (int t = 0; t < 16; t += 2) {
-      const double2 l = *reinterpret_cast<const double2*>(col + 16 * w + t);
-      r[t] = fma(-l.x, mcol, r[t]);
-      r[t + 1] = fma(-l.y, mcol, r[t + 1]);
-      xv[t] = fma(-l.x, xs, xv[t]);
-      xv[t + 1] = fma(-l.y, xs, xv[t + 1]);
+      r[t] = fma(-l[t / 2].x, mcol, r[t]);
+      r[t + 1] = fma(-l[t / 2].y, mcol, r[t + 1]);
+      xv[t] = fma(-l[t / 2].x, xs, xv[t]);
+      xv[t + 1] = fma(-l[t / 2].y, xs, xv[t + 1]);
     }
     if (threadIdx.x == 0) rdiag[j] = isd;
   }

@@ -34,7 +34,14 @@ namespace bo {
 
 void host_front(const float* Y, int64_t n, int m, const float* ref,
                 std::vector<int32_t>& out) {
+  // Visit the rows in decreasing lexicographic order (objective 0, 1, ...,
+  // then increasing index). A row can only be dominated, or duplicated with a
+  // lower index, by a row visited before it, and if it is, some row already
+  // kept dominates or duplicates it too (dominance is transitive), so each
+  // row is checked against the kept rows only: O(n log n + n P).
   out.clear();
+  std::vector<int32_t> order;
+  order.reserve(static_cast<size_t>(n));
   for (int64_t i = 0; i < n; ++i) {
     const float* yi = Y + i * m;
     if (ref) {
@@ -42,22 +49,44 @@ void host_front(const float* Y, int64_t n, int m, const float* ref,
       for (int k = 0; k < m; ++k) above = above && (yi[k] > ref[k]);
       if (!above) continue;
     }
-    bool keep = true;
-    for (int64_t j = 0; j < n && keep; ++j) {
-      if (j == i) continue;
-      const float* yj = Y + j * m;
-      bool ge = true, gt = false;
-      for (int k = 0; k < m; ++k) {
-        ge = ge && (yj[k] >= yi[k]);
-        gt = gt || (yj[k] > yi[k]);
+    order.push_back(static_cast<int32_t>(i));
+  }
+  std::sort(order.begin(), order.end(), [&](int32_t a, int32_t b) {
+    const float* ya = Y + static_cast<int64_t>(a) * m;
+    const float* yb = Y + static_cast<int64_t>(b) * m;
+    for (int k = 0; k < m; ++k)
+      if (ya[k] != yb[k]) return ya[k] > yb[k];
+    return a < b;
+  });
+  if (m == 2) {
+    // two objectives: kept iff objective 1 beats every row visited before
+    float best = -std::numeric_limits<float>::infinity();
+    for (int32_t i : order) {
+      const float y1 = Y[static_cast<int64_t>(i) * 2 + 1];
+      if (out.empty() || y1 > best) {
+        out.push_back(i);
+        best = y1;
       }
-      if (ge && gt) keep = false;            // strictly dominated
-      else if (ge && !gt && j < i) keep = false;  // duplicate, keep lowest
     }
-    if (keep) out.push_back(static_cast<int32_t>(i));
+  } else {
+    for (int32_t i : order) {
+      const float* yi = Y + static_cast<int64_t>(i) * m;
+      bool keep = true;
+      for (int32_t j : out) {
+        const float* yj = Y + static_cast<int64_t>(j) * m;
+        bool ge = true;
+        for (int k = 0; k < m; ++k) ge = ge && (yj[k] >= yi[k]);
+        if (ge) {            // dominated, or an exact duplicate of a lower index
+          keep = false;
+          break;
+        }
+      }
+      if (keep) out.push_back(i);
+    }
   }
   std::stable_sort(out.begin(), out.end(), [&](int32_t a, int32_t b) {
-    return Y[static_cast<int64_t>(a) * m] < Y[static_cast<int64_t>(b) * m];
+    const float ya = Y[static_cast<int64_t>(a) * m], yb = Y[static_cast<int64_t>(b) * m];
+    return ya < yb || (ya == yb && a < b);
   });
 }
 

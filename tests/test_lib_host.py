@@ -137,3 +137,20 @@ def test_box_decomposition_rejects_rows_below_reference(bo):
     with pytest.raises(bo.BoError) as ei:
         bo.box_decomposition(np.array([[1.0, -1.0]], dtype=np.float32), np.zeros(2, np.float32))
     assert ei.value.status == 1
+
+
+def test_host_front_with_ties_and_duplicates_matches_oracle(bo):
+    """Coarse values (many exact ties and duplicate rows) in two and three
+    objectives, with and without the reference filter."""
+    r = np.random.default_rng(0)
+    for trial in range(300):
+        m = 2 if trial % 2 else 3
+        Y = (np.round(r.standard_normal((int(r.integers(1, 60)), m)) * 2) / 2).astype(np.float32)
+        ref = None if trial % 3 == 0 else (Y.min(0) - 0.1).astype(np.float32)
+        got = bo.pareto_front(Y, ref)
+        if ref is None:
+            o = O.nondominated(Y.astype(np.float64))
+            o = o[np.lexsort((o, Y[o, 0]))]
+        else:
+            o = O.pareto_front(Y.astype(np.float64), ref.astype(np.float64))
+        assert list(got) == list(o), (trial, got, o)
