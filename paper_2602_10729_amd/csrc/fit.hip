@@ -138,30 +138,32 @@ __device__ __forceinline__ double rsqrt_d(double d) {
 // invert the factor: on return a = L (zeros above the diagonal) and
 // x = L^{-1} (zeros above the diagonal). All four waves of the 256-thread
 // workgroup take part (every thread must call this): thread (w, c) =
-// (wave, lane) keeps rows 16w .. 16w+15 of column c of both A and X in
-// registers, indexed only by unrolled constants.
+// (wave, lane) keeps, in registers indexed only by unrolled constants,
+//   row c of A, columns 16w .. 16w+15, and
+//   column c of X, rows 16w .. 16w+15.
 //
 // The factor (right-looking, unscaled) and the inverse (forward
-// substitution, one column of X per thread column) advance together, one
-// barrier per step j:
-//   before the barrier, lane j of every wave publishes its rows i > j of
-//   column j of A as it stands (A_ij = L_ij L_jj; zeros for rows <= j) and
-//   the pivot A_jj, and the wave owning row j publishes row j of X as it
-//   stands (X_jc L_jj); the buffers are double-buffered by step parity;
-//   after it, every thread takes 1 / L_jj = A_jj^{-1/2} and updates all of
-//   its rows (the zeros leave rows <= j untouched):
-//     A_ic -= A_ij A_cj / A_jj   (A_cj is zero for c <= j)
-//     X_ic -= A_ij (X_jc L_jj) / A_jj.
+// substitution, one column of X per lane) advance together, one barrier per
+// step j; only the wave holding column j of A and row j of X writes:
+//   before the barrier it publishes column j of A as it stands
+//   (A_ij = L_ij L_jj for rows i > j, zeros for rows <= j; one write of the
+//   whole wave), the pivot A_jj, and row j of X as it stands (X_jc L_jj);
+//   the buffers are double-buffered by step parity;
+//   after it, every thread takes 1 / L_jj = A_jj^{-1/2} and updates
+//     A_ic -= A_ij A_cj / A_jj   (its row i, its 16 columns c)
+//     X_ic -= A_ij (X_jc L_jj) / A_jj   (its column c, its 16 rows i);
+//   the zeros of the published column leave rows and columns <= j as they
+//   are (above the diagonal A is never read again; rows of X up to j are
+//   final).
 // Row j of X keeps the factor L_jj until the end, where every row of X and
-// every column of A is scaled by its 1 / L_jj. Only stores sit in branches,
-// so the update is straight-line code on fixed registers.
+// every column of A is scaled by its 1 / L_jj.
 // A non-positive or non-finite pivot sets *flag and is replaced by 1.
 // Scratch: scr holds 6 x 64 doubles, 16-byte aligned (two published columns
 // of A, two published rows of X, two pivots, the 64 values 1 / L_jj).
 __device__ __forceinline__ void chol_inv64(double (*a)[LDP], double (*x)[LDP], double* scr,
                                            int* flag) {
   const int c = threadIdx.x & 63;
-  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // rows 16w ..
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // column group 16w ..
   double* colbuf = scr;                      // [2][64] column j of A, rows > j
   double* rowbuf = scr + 2 * B;              // [2][64] row j of X
   double* pivbuf = scr + 4 * B;              // [2]     A_jj
@@ -169,13 +171,13 @@ __device__ __forceinline__ void chol_inv64(double (*a)[LDP], double (*x)[LDP], d
   double r[16], xv[16];
 #pragma unroll
   for (int t = 0; t < 16; ++t) {
-    r[t] = a[16 * w + t][c];
+    r[t] = a[c][16 * w + t];
     xv[t] = (16 * w + t == c) ? 1.0 : 0.0;
   }
   bool bad_any = false;
-  // steps j = 16 jw + jt: the row group of the pivot is a loop variable and
-  // the row within it an unrolled constant (register indices stay constant
-  // while the straight-line code stays one row group long)
+  // steps j = 16 jw + jt: the group of the pivot is a loop variable and the
+  // position within it an unrolled constant (register indices stay constant
+  // while the straight-line code stays one group long)
 #pragma unroll 1
   for (int jw = 0; jw < 4; ++jw) {
 #pragma unroll
@@ -183,25 +185,13 @@ __device__ __forceinline__ void chol_inv64(double (*a)[LDP], double (*x)[LDP], d
     const int j = 16 * jw + jt;
     double* col = colbuf + (jt & 1) * B;
     double* row = rowbuf + (jt & 1) * B;
-    if (c == j) {
-      if (w > jw) {
-#pragma unroll
-        for (int t = 0; t < 16; t += 2)
-          *reinterpret_cast<double2*>(col + 16 * w + t) = double2{r[t], r[t + 1]};
-      } else if (w < jw) {
-#pragma unroll
-        for (int t = 0; t < 16; t += 2)
-          *reinterpret_cast<double2*>(col + 16 * w + t) = double2{0.0, 0.0};
-      } else {
-#pragma unroll
-        for (int t = 0; t < 16; ++t) col[16 * w + t] = (t > jt) ? r[t] : 0.0;
-        pivbuf[jt & 1] = r[jt];
-      }
+    if (w == jw) {
+      col[c] = (c > j) ? r[jt] : 0.0;       // A_cj of this lane's row c
+      row[c] = xv[jt];                      // X_jc before its division by L_jj
+      if (c == j) pivbuf[jt & 1] = r[jt];
     }
-    if (w == jw) row[c] = xv[jt];
     __syncthreads();
-    // every read of the step is issued together, ahead of the arithmetic,
-    // so their latencies overlap (one wait, not one per read)
+    // every read of the step is issued together, ahead of the arithmetic
     const double a_jj = pivbuf[jt & 1];
     const double a_cj = col[c];
     const double x_jc = row[c];
@@ -214,12 +204,12 @@ __device__ __forceinline__ void chol_inv64(double (*a)[LDP], double (*x)[LDP], d
     bad_any = bad_any || bad;
     const double isd = rsqrt_d(d);
     const double id = isd * isd;
-    const double mcol = a_cj * id;
-    const double xs = x_jc * id;
+    const double mrow = a_cj * id;          // A_cj / A_jj for this lane's row c
+    const double xs = x_jc * id;            // (X_jc / L_jj) / L_jj
 #pragma unroll
     for (int t = 0; t < 16; t += 2) {
-      r[t] = fma(-l[t / 2].x, mcol, r[t]);
-      r[t + 1] = fma(-l[t / 2].y, mcol, r[t + 1]);
+      r[t] = fma(-mrow, l[t / 2].x, r[t]);
+      r[t + 1] = fma(-mrow, l[t / 2].y, r[t + 1]);
       xv[t] = fma(-l[t / 2].x, xs, xv[t]);
       xv[t + 1] = fma(-l[t / 2].y, xs, xv[t + 1]);
     }
@@ -228,12 +218,11 @@ __device__ __forceinline__ void chol_inv64(double (*a)[LDP], double (*x)[LDP], d
   }
   if (bad_any && threadIdx.x == 0) atomicOr(flag, 1);
   __syncthreads();   // rdiag is complete; every published read is done
-  const double isc = rdiag[c];
 #pragma unroll
   for (int t = 0; t < 16; ++t) {
-    const int i = 16 * w + t;
-    a[i][c] = (i >= c) ? r[t] * isc : 0.0;
-    x[i][c] = xv[t] * rdiag[i];
+    const int k = 16 * w + t;               // column of A / row of X
+    a[c][k] = (c >= k) ? r[t] * rdiag[k] : 0.0;
+    x[k][c] = xv[t] * rdiag[k];
   }
   __syncthreads();
 }
