@@ -50,9 +50,14 @@ routing fractions), the rest are deployment features; output scales 0.7
 deployment dimension (stream 6), so the weights exp(p . c) stay within
 [1, e^{0.96}]. Lengthscales are the workload's.
 
+In-sample base samples (for the noisy acquisition, which also samples the
+latent objectives at the observed points): iid N(0,1) of shape [S, n, m]
+from stream 7, rounded to fp32.
+
 Random streams: ``numpy.random.Generator(PCG64(SeedSequence(seed,
 spawn_key=(family, stream))))`` with streams 0 X, 1 candidates, 2 noise,
-3 lengthscales, 4 weights w, 5 base samples Z, 6 preference slopes; family is
+3 lengthscales, 4 weights w, 5 base samples Z, 6 preference slopes, 7 the
+in-sample base samples of the noisy acquisition; family is
 the config number
 except that configs 2 and 3 share family 2. Candidates are drawn row by row,
 so a prefix of a larger M equals the smaller-M draw.
@@ -65,7 +70,8 @@ from typing import Optional
 import numpy as np
 
 __all__ = ["CONFIGS", "Workload", "make_config", "near_data_candidates",
-           "feasibility_thresholds", "CompositeParams", "composite_hyperparameters"]
+           "feasibility_thresholds", "CompositeParams", "composite_hyperparameters",
+           "insample_base_samples"]
 
 # (m, q, d, n, M, S, noise_sd, family)
 CONFIGS = {
@@ -80,7 +86,8 @@ OUTPUTSCALE = 1.0
 NOISE_VAR = 1e-4
 REF_OFFSET = 0.1
 
-STREAM_X, STREAM_CAND, STREAM_NOISE, STREAM_LS, STREAM_W, STREAM_Z, STREAM_PREF = range(7)
+(STREAM_X, STREAM_CAND, STREAM_NOISE, STREAM_LS, STREAM_W, STREAM_Z, STREAM_PREF,
+ STREAM_ZX) = range(8)
 
 
 @dataclass
@@ -228,3 +235,12 @@ def composite_hyperparameters(wl: Workload, d_route: Optional[int] = None) -> Co
     pref = 0.08 * _rng(wl.seed, fam, STREAM_PREF).random((wl.m, wl.d - dr))
     f = lambda v: np.full(wl.m, v, dtype=np.float32)
     return CompositeParams(dr, f(0.7), f(0.3), f(0.05), pref.astype(np.float32))
+
+
+def insample_base_samples(wl: Workload, S: Optional[int] = None) -> np.ndarray:
+    """Base samples [S, n, m] (fp32) of the latent objectives at the observed
+    points, for the noisy acquisition; S defaults to the workload's."""
+    Sv = wl.S if S is None else int(S)
+    fam = CONFIGS[wl.cfg]["family"]
+    z = _rng(wl.seed, fam, STREAM_ZX).standard_normal((Sv, wl.n, wl.m))
+    return z.astype(np.float32)

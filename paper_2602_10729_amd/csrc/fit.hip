@@ -611,9 +611,12 @@ __global__ __launch_bounds__(256) void k_mll_grad(const float* __restrict__ X, i
   const int64_t bj = t - bi * (bi + 1) / 2;
   const int64_t i = bi * 16 + threadIdx.x / 16;
   const int64_t j = bj * 16 + threadIdx.x % 16;
-  double acc[BO_MAX_D + 2];
+  // gradient parts: lengthscales (gl), output scale (go), noise (gn); kept
+  // apart so every register index is a compile-time constant
+  double gl[BO_MAX_D];
 #pragma unroll
-  for (int e = 0; e < BO_MAX_D + 2; ++e) acc[e] = 0.0;
+  for (int e = 0; e < BO_MAX_D; ++e) gl[e] = 0.0;
+  double go = 0.0, gn = 0.0;
   if (i < n && j < n && j <= i) {
     const double* ils = g.ils + k * d;
     const double s = g.os[k];
@@ -621,35 +624,31 @@ __global__ __launch_bounds__(256) void k_mll_grad(const float* __restrict__ X, i
                      A[((int64_t)k * nf + i) * nf + j];
     const double wgt = (i == j) ? 0.5 : 1.0;     // 1/2 x (2 off the diagonal)
     double r2 = 0.0;
-    double u2[BO_MAX_D];
 #pragma unroll
     for (int e = 0; e < BO_MAX_D; ++e) {
-      u2[e] = 0.0;
       if (e < d) {
         const double u = (static_cast<double>(X[i * d + e]) - static_cast<double>(X[j * d + e])) * ils[e];
-        u2[e] = u * u;
-        r2 += u2[e];
+        gl[e] = u * u;
+        r2 += gl[e];
       }
     }
     const double r = sqrt(r2);
     const double c5 = 2.23606797749978969641;
     const double ex = exp(-c5 * r);
-    const double common = (5.0 / 3.0) * s * (1.0 + c5 * r) * ex;
-    const double k0 = s * (1.0 + c5 * r + (5.0 / 3.0) * r2) * ex;
+    const double common = wgt * a * (5.0 / 3.0) * s * (1.0 + c5 * r) * ex;
 #pragma unroll
-    for (int e = 0; e < BO_MAX_D; ++e)
-      if (e < d) acc[e] = wgt * a * common * u2[e];
-    acc[d] = wgt * a * k0;
-    acc[d + 1] = (i == j) ? 0.5 * a * g.noise[k] : 0.0;
+    for (int e = 0; e < BO_MAX_D; ++e) gl[e] *= common;   // 0 past d
+    go = wgt * a * s * (1.0 + c5 * r + (5.0 / 3.0) * r2) * ex;
+    gn = (i == j) ? 0.5 * a * g.noise[k] : 0.0;
   }
   // reduce the d + 2 sums over the workgroup
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
 #pragma unroll
   for (int e = 0; e < BO_MAX_D + 2; ++e) {
-    if (e < d + 2) {
-      double v = acc[e];
+    if (e < d || e >= BO_MAX_D) {
+      double v = (e < BO_MAX_D) ? gl[e] : (e == BO_MAX_D ? go : gn);
       for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
-      if (lane == 0) red[w][e] = v;
+      if (lane == 0) red[w][e < BO_MAX_D ? e : d + (e - BO_MAX_D)] = v;
     }
   }
   __syncthreads();
@@ -660,16 +659,25 @@ __global__ __launch_bounds__(256) void k_mll_grad(const float* __restrict__ X, i
   }
 }
 
-// out[k][1 + e] = sum over tiles of partials (fixed order: deterministic)
-__global__ __launch_bounds__(64) void k_mll_reduce(const double* __restrict__ partials,
-                                                   int64_t tiles, int d,
-                                                   double* __restrict__ out) {
-  const int k = blockIdx.x;
-  for (int e = threadIdx.x; e < d + 2; e += 64) {
-    double v = 0.0;
-    for (int64_t t = 0; t < tiles; ++t) v += partials[((int64_t)k * tiles + t) * (d + 2) + e];
-    out[(int64_t)k * (d + 3) + 1 + e] = v;
+// Sum of the per-tile gradient partials: one workgroup per (objective,
+// gradient entry); each thread adds a strided subset of the tiles, then a
+// fixed-shape tree over the workgroup (the order, so the result, does not
+// depend on timing).
+__global__ __launch_bounds__(256) void k_mll_reduce(const double* __restrict__ partials,
+                                                    int64_t tiles, int d,
+                                                    double* __restrict__ out) {
+  __shared__ double red[256];
+  const int k = blockIdx.x, e = blockIdx.y;
+  double v = 0.0;
+  for (int64_t t = threadIdx.x; t < tiles; t += 256)
+    v += partials[((int64_t)k * tiles + t) * (d + 2) + e];
+  red[threadIdx.x] = v;
+  __syncthreads();
+  for (int h = 128; h > 0; h >>= 1) {
+    if (threadIdx.x < h) red[threadIdx.x] += red[threadIdx.x + h];
+    __syncthreads();
   }
+  if (threadIdx.x == 0) out[(int64_t)k * (d + 3) + 1 + e] = red[0];
 }
 
 __global__ void k_lower_to_f32(const double* __restrict__ A, int64_t n, int nf,
@@ -749,7 +757,7 @@ hipError_t launch_mll(const float* X, int64_t n, int d, int m, int nf, const Gra
   const int64_t tiles = mll_tiles(nf);
   hipLaunchKernelGGL(k_mll_grad, dim3(static_cast<unsigned>(tiles), m), dim3(256), 0, st, X, n,
                      d, nf, g, A, alpha64, partials);
-  hipLaunchKernelGGL(k_mll_reduce, dim3(m), dim3(64), 0, st, partials, tiles, d, out);
+  hipLaunchKernelGGL(k_mll_reduce, dim3(m, d + 2), dim3(256), 0, st, partials, tiles, d, out);
   return hipGetLastError();
 }
 
