@@ -231,6 +231,60 @@ bo_status bo_score_constrained(bo_model model, const float* cand, int64_t M, int
                                float* mu, float* sigma, void* stream);
 
 /*
+ * bo_nehvi_prepare / bo_score_nehvi — the noisy acquisition (qNEHVI, q = 1,
+ * two objectives, Matern-5/2 models).
+ *
+ * Paper: workflow step (ii) and the "Constrained qNEHVI" paragraph (after
+ * Daulton et al. 2021). The observations are noisy, so the latent objective
+ * values at the observed points X are sampled too: sample s draws the latent
+ * f jointly at X and at the candidate x from the GP posterior, by the lower
+ * Cholesky factor of the joint covariance applied to (z_X^s, z*^s):
+ *   f_X^s = mu_X + L_XX z_X^s            (Sigma_XX = L_XX L_XX^T),
+ *   f*^s  = E[f* | f_X^s] + tau z*^s,
+ *   E[f* | f_X] = k*^T K_XX^{-1} f_X,  tau^2 = s - k*^T K_XX^{-1} k*
+ *   (K_XX the noise-free Gram matrix; the noisy y adds nothing once f_X is
+ *   known), and
+ *   ehvi[b] = 1/S sum_s HVI_s(f*^s) [* feasibility indicator of f*^s],
+ * where HVI_s is the hypervolume improvement over the Pareto front of the
+ * in-sample values f_X^s (maximise, strictly above ref_point; with
+ * feasibility thresholds only the in-sample vectors meeting all of them).
+ *
+ * bo_nehvi_prepare(model, base_samples_X, S, ref_point, feas_lower, stream):
+ *   base_samples_X device [S][n][2] iid N(0,1), row-major (sample, observed
+ *                  point, objective); 1 <= S <= 512
+ *   ref_point      host [2];  feas_lower host [2] or NULL (as in
+ *                  bo_score_constrained)
+ *   Builds, in fp64 on the device, the in-sample posterior and its factor,
+ *   the S in-sample draws, each sample's front and box decomposition, the
+ *   factor of K_XX and G = K_XX^{-1} L_XX Z_X; keeps them in the model
+ *   (replacing an earlier preparation). Synchronous (reads the per-sample
+ *   front sizes back).
+ *   Errors: INVALID_ARGUMENT (m != 2, composite-kernel model, bad S or
+ *   pointer), CAPACITY (S > 512, per-sample boxes beyond LDS),
+ *   NOT_POSITIVE_DEFINITE (K, the in-sample covariance or K_XX),
+ *   NONFINITE_INPUT, OUT_OF_MEMORY, DEVICE.
+ *
+ * bo_score_nehvi(model, cand, M, base_samples, S, ehvi, stream):
+ *   cand device [M][d]; base_samples device [S][2] (z*, shared by all
+ *   candidates); S must equal the prepared S; ehvi device [M] out.
+ *   Asynchronous; candidates are processed in chunks of 262144, whose
+ *   per-sample conditional means (2 x S x chunk floats) live in a model-owned
+ *   workspace that grows on first use.
+ *   Errors: INVALID_ARGUMENT (not prepared, S mismatch, pointers), CAPACITY,
+ *   OUT_OF_MEMORY, DEVICE.
+ *
+ * bo_nehvi_front(model, sample, idx_host, cap, count): the front of one
+ *   sample (indices into the observations, sorted by objective 0 ascending),
+ *   min(cap, size) entries to host memory, *count = its size. Synchronous.
+ */
+bo_status bo_nehvi_prepare(bo_model model, const float* base_samples_X, int32_t S,
+                           const float* ref_point, const float* feas_lower, void* stream);
+bo_status bo_score_nehvi(bo_model model, const float* cand, int64_t M,
+                         const float* base_samples, int32_t S, float* ehvi, void* stream);
+bo_status bo_nehvi_front(bo_model model, int32_t sample, int32_t* idx_host, int32_t cap,
+                         int32_t* count);
+
+/*
  * bo_argmax — first index of the maximum of values[0..M).
  *
  * Paper: workflow step (ii), choosing theta* as the maximiser of the

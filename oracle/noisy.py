@@ -74,10 +74,11 @@ def insample_samples(model: GPModel, ZX: np.ndarray):
 
 
 def candidate_samples(model: GPModel, cand: np.ndarray, ZX: np.ndarray, Zs: np.ndarray,
-                      Ls=None):
+                      Ls=None, Kxx=None):
     """Joint-posterior samples of the candidates: f* [M, S, m].
 
-    cand [M, d]; ZX [S, n, m]; Zs [S, m]. Ls: the in-sample factors (computed
+    cand [M, d]; ZX [S, n, m]; Zs [S, m]. Ls: the in-sample factors, Kxx: the
+    noise-free training covariances (both lists over objectives; computed
     when not given)."""
     cand = np.asarray(cand, dtype=np.float64).reshape(-1, model.X.shape[1])
     ZX = np.asarray(ZX, dtype=np.float64)
@@ -89,11 +90,11 @@ def candidate_samples(model: GPModel, cand: np.ndarray, ZX: np.ndarray, Zs: np.n
     out = np.empty((M, ZX.shape[0], model.m))
     for k in range(model.m):
         Ks = model.cov(k, cand, X)                              # [M, n] = k*^T
-        Kxx = model.cov(k, X, X)
+        Kk = model.cov(k, X, X) if Kxx is None else Kxx[k]
         mu_s = Ks @ model.alpha[k]
         KinvKs = cho_solve((model.L[k], True), Ks.T)            # [n, M] = K^{-1} k*
         var_s = model.pair_cov(k, cand, cand) - np.sum(Ks.T * KinvKs, axis=0)
-        Sx = Ks.T - Kxx @ KinvKs                                # [n, M] = Sigma_X*
+        Sx = Ks.T - Kk @ KinvKs                                 # [n, M] = Sigma_X*
         Bm = solve_triangular(Ls[k], Sx, lower=True)            # [n, M]
         c2 = np.maximum(var_s - np.sum(Bm * Bm, axis=0), 0.0)
         out[:, :, k] = (mu_s[:, None] + Bm.T @ ZX[:, :, k].T
@@ -131,12 +132,13 @@ def nehvi(model: GPModel, cand: np.ndarray, ref: np.ndarray, ZX: np.ndarray,
     S = ZX.shape[0]
     Zs = np.asarray(Zs, dtype=np.float64).reshape(S, model.m)
     F, Ls = insample_samples(model, ZX)
+    Kxx = [model.cov(k, model.X, model.X) for k in range(model.m)]
     boxes = sample_boxes(F, ref, lower)
     M = cand.shape[0]
     out = np.empty(M)
     for i0 in range(0, M, chunk):
         i1 = min(M, i0 + chunk)
-        ys = candidate_samples(model, cand[i0:i1], ZX, Zs, Ls)    # [c, S, m]
+        ys = candidate_samples(model, cand[i0:i1], ZX, Zs, Ls, Kxx)    # [c, S, m]
         h = np.empty((i1 - i0, S))
         for s in range(S):
             lo, hi = boxes[s]

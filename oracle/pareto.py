@@ -25,22 +25,21 @@ import numpy as np
 def nondominated(Y: np.ndarray) -> np.ndarray:
     """Indices of non-dominated rows of Y (maximise), duplicates dropped.
 
-    Brute force over all pairs; returned in increasing index order.
+    Brute force over all pairs (one n x n comparison per objective);
+    returned in increasing index order. Row i is dropped when some row j is
+    >= it in every objective and differs in one, or equals it with j < i.
     """
     Y = np.asarray(Y, dtype=np.float64)
     n = Y.shape[0]
-    keep = np.ones(n, dtype=bool)
-    for i in range(n):
-        ge = np.all(Y >= Y[i], axis=1)
-        ne = np.any(Y != Y[i], axis=1)
-        if np.any(ge & ne):
-            keep[i] = False
-            continue
-        eq = ~ne
-        eq[i] = False
-        if np.any(eq[:i]):
-            keep[i] = False
-    return np.nonzero(keep)[0]
+    ge = np.ones((n, n), dtype=bool)        # ge[i, j]: Y[j] >= Y[i] componentwise
+    ne = np.zeros((n, n), dtype=bool)       # ne[i, j]: Y[j] != Y[i] somewhere
+    for k in range(Y.shape[1]):
+        col = Y[:, k]
+        ge &= col[None, :] >= col[:, None]
+        ne |= col[None, :] != col[:, None]
+    dominated = np.any(ge & ne, axis=1)
+    earlier_dup = np.any(np.tril(~ne, -1), axis=1)     # an equal row j < i
+    return np.nonzero(~(dominated | earlier_dup))[0]
 
 
 def pareto_front(Y: np.ndarray, ref: np.ndarray) -> np.ndarray:

@@ -8,7 +8,9 @@ tensor is not on the GPU, the call raises.
 Functions mirror the C ABI in ``include/bo.h``:
 ``fit`` (``bo_fit``), ``fit_composite`` (``bo_fit_composite``), ``mll``
 (``bo_mll``), ``score`` (``bo_score``, or ``bo_score_constrained`` when feasibility
-thresholds are given), ``argmax``, ``cholesky_test`` (device) and
+thresholds are given), ``nehvi_prepare`` / ``score_nehvi`` / ``Model.nehvi_front``
+(``bo_nehvi_prepare``, ``bo_score_nehvi``, ``bo_nehvi_front``), ``argmax``,
+``cholesky_test`` (device) and
 ``pareto_front``, ``box_decomposition`` (host geometry, no GPU needed).
 """
 from __future__ import annotations
@@ -19,7 +21,7 @@ from typing import Optional
 
 import numpy as np
 
-__all__ = ["BoError", "Model", "lib", "lib_path", "fit", "fit_composite", "mll", "score", "argmax",
+__all__ = ["BoError", "Model", "lib", "lib_path", "fit", "fit_composite", "mll", "score", "nehvi_prepare", "score_nehvi", "argmax",
            "cholesky_test", "profile_enable", "profile_read", "measure_peak", "pareto_front", "box_decomposition", "STATUS",
            "MAX_N", "MAX_D", "MAX_S", "MAX_BOXES"]
 
@@ -67,6 +69,12 @@ def lib() -> ctypes.CDLL:
     L.bo_score.restype = ctypes.c_int
     L.bo_score_constrained.argtypes = [vp, vp, i64, i32, fp, fp, vp, i32, vp, vp, vp, vp]
     L.bo_score_constrained.restype = ctypes.c_int
+    L.bo_nehvi_prepare.argtypes = [vp, vp, i32, fp, fp, vp]
+    L.bo_nehvi_prepare.restype = ctypes.c_int
+    L.bo_score_nehvi.argtypes = [vp, vp, i64, vp, i32, vp, vp]
+    L.bo_score_nehvi.restype = ctypes.c_int
+    L.bo_nehvi_front.argtypes = [vp, i32, vp, i32, ctypes.POINTER(i32)]
+    L.bo_nehvi_front.restype = ctypes.c_int
     L.bo_argmax.argtypes = [vp, i64, vp, vp, vp]
     L.bo_argmax.restype = ctypes.c_int
     L.bo_model_front_size.argtypes = [vp]
@@ -146,6 +154,17 @@ class Model:
         out = np.zeros(max(P, 0), dtype=np.int32)
         _check(L.bo_model_front_indices(self._h, out.ctypes.data_as(ctypes.c_void_p), P),
                "bo_model_front_indices")
+        return out
+
+    def nehvi_front(self, sample: int) -> np.ndarray:
+        """Front of one prepared in-sample draw (bo_nehvi_front): indices into
+        the observations, sorted by objective 0 ascending."""
+        L = lib()
+        cnt = ctypes.c_int32(0)
+        _check(L.bo_nehvi_front(self._h, int(sample), None, 0, ctypes.byref(cnt)), "bo_nehvi_front")
+        out = np.zeros(cnt.value, dtype=np.int32)
+        _check(L.bo_nehvi_front(self._h, int(sample), out.ctypes.data_as(ctypes.c_void_p),
+                                cnt.value, ctypes.byref(cnt)), "bo_nehvi_front")
         return out
 
     def close(self):
@@ -244,6 +263,35 @@ def score(model: Model, cand, ref, Z, ehvi=None, mu=None, sigma=None, stream=Non
         st = lib().bo_score_constrained(model.handle, *args, lw.ctypes.data_as(ctypes.c_void_p),
                                         *tail)
         _check(st, "bo_score_constrained")
+    return ehvi
+
+
+def nehvi_prepare(model: Model, ZX, ref, lower=None, stream=None):
+    """bo_nehvi_prepare: ZX [S, n, 2] fp32 GPU tensor (in-sample base
+    samples); ref host [2]; lower host [2] or None. Synchronous."""
+    import torch
+    S = ZX.shape[0]
+    r = _host_f32(ref, (model.m,), "ref")
+    lw = None if lower is None else _host_f32(lower, (model.m,), "lower")
+    st = lib().bo_nehvi_prepare(model.handle, _dev(ZX, "ZX", torch.float32), S,
+                                r.ctypes.data_as(ctypes.c_void_p),
+                                lw.ctypes.data_as(ctypes.c_void_p) if lw is not None else None,
+                                _stream(stream))
+    _check(st, "bo_nehvi_prepare")
+
+
+def score_nehvi(model: Model, cand, Z, ehvi=None, stream=None):
+    """bo_score_nehvi: cand [M, d] (or [M, 1, d]) and Z [S, 2] (or [S, 1, 2])
+    fp32 GPU tensors. Returns the ehvi tensor [M] (allocated if not given)."""
+    import torch
+    M = cand.shape[0]
+    S = Z.shape[0]
+    if ehvi is None:
+        ehvi = torch.empty(M, dtype=torch.float32, device=cand.device)
+    st = lib().bo_score_nehvi(model.handle, _dev(cand, "cand", torch.float32), M,
+                              _dev(Z, "Z", torch.float32), S, _dev(ehvi, "ehvi", torch.float32),
+                              _stream(stream))
+    _check(st, "bo_score_nehvi")
     return ehvi
 
 

@@ -190,9 +190,26 @@ struct FitScratch {
 // Releases the device buffers of a model after all device work (not the host
 // object). The caller may have used the model on several streams, so wait
 // for the whole device before handing memory back to the pool.
+void release_noisy(Model* M) {
+  Model::Noisy& z = M->nz;
+  if (z.Lp0 || z.Gp || z.boxes || z.off || z.front || z.ws) (void)hipDeviceSynchronize();
+  pfree(z.Lp0, nullptr);
+  pfree(z.Gp, nullptr);
+  pfree(z.boxes, nullptr);
+  pfree(z.off, nullptr);
+  pfree(z.front, nullptr);
+  pfree(z.ws, nullptr);
+  z.ws_floats = 0;
+  z.S = z.Sp = z.n32 = z.total = 0;
+  z.counts.clear();
+}
+
 void release_buffers(Model* M) {
-  if (M->Xs || M->invls || M->alpha || M->Lp || M->ws || M->d_boxes || M->wts || M->pref)
+  release_noisy(M);
+  if (M->Xs || M->invls || M->alpha || M->Lp || M->ws || M->d_boxes || M->wts || M->pref ||
+      M->Xd)
     (void)hipDeviceSynchronize();
+  pfree(M->Xd, nullptr);
   pfree(M->Xs, nullptr);
   pfree(M->invls, nullptr);
   pfree(M->alpha, nullptr);
@@ -407,6 +424,7 @@ bo_status fit_impl(const char* who, const float* X, const float* Y, int64_t n, i
   if ((s = palloc(&M->invls, (size_t)m * M->dx, st, "inverse lengthscales")) != BO_OK) return bail(s);
   if ((s = palloc(&M->alpha, (size_t)m * M->n_pad, st, "alpha")) != BO_OK) return bail(s);
   if ((s = palloc(&M->Lp, (size_t)m * M->lp_per_obj, st, "packed inverse")) != BO_OK) return bail(s);
+  if ((s = palloc(&M->Xd, (size_t)n * d, st, "training inputs")) != BO_OK) return bail(s);
   if (comp) {
     if ((s = palloc(&M->wts, (size_t)m * M->n_pad, st, "preference weights")) != BO_OK) return bail(s);
     if ((s = palloc(&M->pref, (size_t)m * dc, st, "preference slopes")) != BO_OK) return bail(s);
@@ -464,6 +482,8 @@ bo_status fit_impl(const char* who, const float* X, const float* Y, int64_t n, i
     e = hipMemcpyAsync(M->pref, stage + off_pref, sizeof(float) * npref, hipMemcpyHostToDevice,
                        st);
   if (e == hipSuccess) e = hipMemsetAsync(fs.flag, 0, sizeof(int), st);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(M->Xd, X, sizeof(float) * n * d, hipMemcpyDeviceToDevice, st);
   if (e != hipSuccess) return bail(hip_fail(e, "bo_fit: upload"));
 
   GramParams gp;
@@ -821,6 +841,315 @@ bo_status bo_score_constrained(bo_model model, const float* cand, int64_t M_, in
     if (e != hipSuccess) return hip_fail(e, "bo_score: profile event");
   }
   M.last_stream = st;
+  return BO_OK;
+}
+
+}  // extern "C"
+
+namespace {
+
+// Candidates per scoring chunk of the noisy acquisition: the conditional
+// means of a chunk, m x S x chunk floats (1 GiB at S = 512), stay in HBM
+// between the matrix-core kernel and the HVI kernel.
+constexpr int64_t kNehviChunk = 262144;
+constexpr int kNehviMaxS = 512;
+
+struct NoisyScratch {
+  hipStream_t st = nullptr;
+  double *A = nullptr, *W = nullptr, *A0 = nullptr, *W0 = nullptr;
+  double *hyp = nullptr, *tmp = nullptr, *alpha64 = nullptr, *gmax = nullptr;
+  double *Zk = nullptr, *T1 = nullptr, *G = nullptr;
+  float *Y = nullptr, *alpha = nullptr, *btmp = nullptr;
+  int *flag = nullptr, *counts = nullptr, *off = nullptr;
+  ~NoisyScratch() {
+    pfree(A, st); pfree(W, st); pfree(A0, st); pfree(W0, st); pfree(hyp, st); pfree(tmp, st);
+    pfree(alpha64, st); pfree(gmax, st); pfree(Zk, st); pfree(T1, st); pfree(G, st);
+    pfree(Y, st); pfree(alpha, st); pfree(btmp, st); pfree(flag, st); pfree(counts, st);
+    pfree(off, st);
+  }
+};
+
+bo_status nehvi_prepare_impl(bo_model model, const float* ZX, int32_t S, const float* ref,
+                             const float* lower, void* stream) {
+  const char* W_ = "bo_nehvi_prepare";
+  if (!model) return fail(BO_ERR_INVALID_ARGUMENT, std::string(W_) + ": model is NULL");
+  Model& M = model->m;
+  if (M.m != 2) return fail(BO_ERR_INVALID_ARGUMENT, std::string(W_) + ": two objectives only");
+  if (M.dr > 0)
+    return fail(BO_ERR_INVALID_ARGUMENT, std::string(W_) + ": Matern-5/2 models only");
+  if (S < 1) return fail(BO_ERR_INVALID_ARGUMENT, std::string(W_) + ": S < 1");
+  if (S > kNehviMaxS) return fail(BO_ERR_CAPACITY, std::string(W_) + ": S beyond 512");
+  if (!ref) return fail(BO_ERR_INVALID_ARGUMENT, std::string(W_) + ": ref_point is NULL");
+  if (!all_finite(ref, 2)) return fail(BO_ERR_NONFINITE_INPUT, std::string(W_) + ": ref_point not finite");
+  if (lower && (std::isnan(lower[0]) || std::isnan(lower[1])))
+    return fail(BO_ERR_NONFINITE_INPUT, std::string(W_) + ": feasibility threshold is NaN");
+  DeviceGuard g(M.device);
+  if (!g.ok) return fail(BO_ERR_DEVICE, std::string(W_) + ": cannot select the model's device");
+  const int64_t n = M.n;
+  const int m = 2, d = M.d;
+  bo_status s;
+  if ((s = check_dev(ZX, sizeof(float) * (size_t)S * n * m, "base_samples_X")) != BO_OK) return s;
+  if (nehvi_front_lds_bytes(n) > 64 * 1024)
+    return fail(BO_ERR_CAPACITY, std::string(W_) + ": n beyond the front kernel's LDS");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int nf = static_cast<int>((n + kFitBlk - 1) / kFitBlk) * kFitBlk;
+  const int Sp = nehvi_padded_samples(S);
+  const int n32 = static_cast<int>((n + 31) / 32);
+  const int nrb = Sp / 16;
+
+  // earlier scoring calls may still read the state being replaced
+  release_noisy(&M);
+  Model::Noisy& z = M.nz;
+
+  NoisyScratch sc;
+  sc.st = st;
+  const size_t nhyp = (size_t)m * d + 3 * m;     // [1/ls][os][noise][zeros]
+  const size_t mat = (size_t)m * nf * nf, vec = (size_t)m * nf * Sp;
+  if ((s = palloc(&sc.A, mat, st, "noisy: matrix")) != BO_OK) return s;
+  if ((s = palloc(&sc.W, mat, st, "noisy: inverse")) != BO_OK) return s;
+  if ((s = palloc(&sc.A0, mat, st, "noisy: noise-free matrix")) != BO_OK) return s;
+  if ((s = palloc(&sc.W0, mat, st, "noisy: noise-free inverse")) != BO_OK) return s;
+  if ((s = palloc(&sc.hyp, nhyp, st, "noisy: hyperparameters")) != BO_OK) return s;
+  if ((s = palloc(&sc.tmp, (size_t)m * nf, st, "noisy: vector")) != BO_OK) return s;
+  if ((s = palloc(&sc.alpha64, (size_t)m * nf, st, "noisy: alpha")) != BO_OK) return s;
+  if ((s = palloc(&sc.gmax, (size_t)m, st, "noisy: maxima")) != BO_OK) return s;
+  if ((s = palloc(&sc.Zk, vec, st, "noisy: base samples")) != BO_OK) return s;
+  if ((s = palloc(&sc.T1, vec, st, "noisy: in-sample offsets")) != BO_OK) return s;
+  if ((s = palloc(&sc.G, vec, st, "noisy: G")) != BO_OK) return s;
+  if ((s = palloc(&sc.Y, (size_t)n * m, st, "noisy: Y")) != BO_OK) return s;
+  if ((s = palloc(&sc.alpha, (size_t)m * M.n_pad, st, "noisy: alpha (fp32)")) != BO_OK) return s;
+  if ((s = palloc(&sc.btmp, (size_t)S * (n + 1) * 4, st, "noisy: boxes")) != BO_OK) return s;
+  if ((s = palloc(&sc.flag, 4, st, "noisy: flags")) != BO_OK) return s;
+  if ((s = palloc(&sc.counts, (size_t)S, st, "noisy: counts")) != BO_OK) return s;
+  if ((s = palloc(&sc.off, (size_t)S + 1, st, "noisy: offsets")) != BO_OK) return s;
+  if ((s = palloc(&z.Lp0, (size_t)m * M.lp_per_obj, st, "noisy: packed factor")) != BO_OK) return s;
+  if ((s = palloc(&z.front, (size_t)S * n, st, "noisy: fronts")) != BO_OK) return s;
+
+  std::vector<double> hyp(nhyp, 0.0);
+  for (int i = 0; i < m * d; ++i) hyp[i] = 1.0 / static_cast<double>(M.ls[i]);
+  for (int k = 0; k < m; ++k) {
+    hyp[(size_t)m * d + k] = M.os[k];
+    hyp[(size_t)m * d + m + k] = M.noise[k];
+  }
+  // pinned staging: [hyp][flags 16 B][Y][counts][gmax][off]
+  DeviceState* DS = device_state(M.device);
+  if (!DS) return fail(BO_ERR_DEVICE, std::string(W_) + ": device index out of range");
+  std::lock_guard<std::mutex> stage_lock(DS->fit_mu);
+  const size_t off_flag = (sizeof(double) * nhyp + 15) / 16 * 16;
+  const size_t off_y = off_flag + 16;
+  const size_t off_cnt = (off_y + sizeof(float) * n * m + 15) / 16 * 16;
+  const size_t off_gmax = (off_cnt + sizeof(int) * S + 15) / 16 * 16;
+  const size_t off_off = off_gmax + 16;
+  const size_t need = off_off + sizeof(int) * ((size_t)S + 1);
+  hipError_t e = hipSuccess;
+  if (need > DS->fit_stage_bytes) {
+    if (DS->fit_stage) (void)hipHostFree(DS->fit_stage);
+    DS->fit_stage = nullptr;
+    DS->fit_stage_bytes = 0;
+    const size_t cap = std::max<size_t>(need, size_t(1) << 16);
+    e = hipHostMalloc(reinterpret_cast<void**>(&DS->fit_stage), cap, hipHostMallocDefault);
+    if (e != hipSuccess) return hip_fail(e, "bo_nehvi_prepare: pinned staging");
+    DS->fit_stage_bytes = cap;
+  }
+  unsigned char* stage = DS->fit_stage;
+  auto sync_fail = [&](bo_status st_) {
+    (void)hipStreamSynchronize(st);   // copies from the staging buffer may be pending
+    release_noisy(&M);
+    return st_;
+  };
+  std::memcpy(stage, hyp.data(), sizeof(double) * nhyp);
+  std::memcpy(stage + off_y, M.Yh.data(), sizeof(float) * n * m);
+  e = hipMemcpyAsync(sc.hyp, stage, sizeof(double) * nhyp, hipMemcpyHostToDevice, st);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(sc.Y, stage + off_y, sizeof(float) * n * m, hipMemcpyHostToDevice, st);
+  if (e == hipSuccess) e = hipMemsetAsync(sc.flag, 0, 4 * sizeof(int), st);
+  if (e != hipSuccess) return sync_fail(hip_fail(e, "bo_nehvi_prepare: upload"));
+
+  GramParams gp;
+  gp.ils = sc.hyp;
+  gp.os = sc.hyp + (size_t)m * d;
+  gp.noise = gp.os + m;
+  GramParams g0 = gp;
+  g0.noise = gp.noise + m;                  // zeros: the noise-free K_XX
+  auto step = [&](hipError_t err, const char* what) { return after_launch(err, st, what); };
+  // K = K_XX + eta I: factor, inverse, alpha (fp64), then K^{-1}
+  if ((s = step(launch_gram(M.Xd, n, d, m, nf, gp, sc.A, st), "gram")) != BO_OK) return sync_fail(s);
+  if ((s = step(launch_cholesky(sc.A, sc.W, nf, m, sc.flag, st), "cholesky")) != BO_OK) return sync_fail(s);
+  if ((s = step(launch_alpha(sc.W, sc.Y, n, m, nf, M.n_pad, sc.tmp, sc.alpha, st, sc.alpha64), "alpha")) != BO_OK) return sync_fail(s);
+  if ((s = step(launch_kinv(sc.A, sc.W, nf, m, st), "inverse")) != BO_OK) return sync_fail(s);
+  // in-sample posterior covariance eta (I - eta K^{-1}) and its factor
+  if ((s = step(launch_sigma_xx(sc.A, n, nf, m, gp.noise, st), "in-sample covariance")) != BO_OK) return sync_fail(s);
+  if ((s = step(launch_cholesky(sc.A, sc.W, nf, m, sc.flag + 1, st), "cholesky")) != BO_OK) return sync_fail(s);
+  // noise-free K_XX: factor, inverse, packed for the conditional variance
+  if ((s = step(launch_gram(M.Xd, n, d, m, nf, g0, sc.A0, st), "gram")) != BO_OK) return sync_fail(s);
+  if ((s = step(launch_cholesky(sc.A0, sc.W0, nf, m, sc.flag + 2, st), "cholesky")) != BO_OK) return sync_fail(s);
+  if ((s = step(launch_pack_factor(sc.W0, n, m, nf, M.nb, z.Lp0, st), "pack")) != BO_OK) return sync_fail(s);
+  // T1 = L_XX Z_X, G = K_XX^{-1} T1 = W0^T (W0 T1)
+  if ((s = step(launch_gather_z(ZX, n, m, S, nf, Sp, sc.Zk, st), "gather")) != BO_OK) return sync_fail(s);
+  if ((s = step(launch_trmm(false, sc.A, sc.Zk, sc.T1, nf, Sp, m, st), "trmm")) != BO_OK) return sync_fail(s);
+  if ((s = step(launch_trmm(false, sc.W0, sc.T1, sc.Zk, nf, Sp, m, st), "trmm")) != BO_OK) return sync_fail(s);
+  if ((s = step(launch_trmm(true, sc.W0, sc.Zk, sc.G, nf, Sp, m, st), "trmm")) != BO_OK) return sync_fail(s);
+  // fronts and boxes of every sample
+  NehviFrontArgs fa;
+  fa.Y = sc.Y; fa.alpha64 = sc.alpha64; fa.noise = gp.noise; fa.T1 = sc.T1;
+  fa.n = n; fa.nf = nf; fa.Sp = Sp; fa.S = S;
+  fa.ref0 = ref[0]; fa.ref1 = ref[1];
+  fa.cons = lower != nullptr;
+  fa.low0 = lower ? lower[0] : -INFINITY;
+  fa.low1 = lower ? lower[1] : -INFINITY;
+  fa.boxes = sc.btmp; fa.counts = sc.counts; fa.front = z.front;
+  if ((s = step(launch_sample_fronts(fa, st), "fronts")) != BO_OK) return sync_fail(s);
+  if ((s = step(launch_absmax(sc.G, (int64_t)nf * Sp, m, sc.gmax, st), "absmax")) != BO_OK) return sync_fail(s);
+  e = hipMemcpyAsync(stage + off_flag, sc.flag, 3 * sizeof(int), hipMemcpyDeviceToHost, st);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(stage + off_cnt, sc.counts, sizeof(int) * S, hipMemcpyDeviceToHost, st);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(stage + off_gmax, sc.gmax, sizeof(double) * m, hipMemcpyDeviceToHost, st);
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  if (e != hipSuccess) return sync_fail(hip_fail(e, "bo_nehvi_prepare: sync"));
+  int flags[3];
+  std::memcpy(flags, stage + off_flag, sizeof(flags));
+  if (flags[0]) return sync_fail(fail(BO_ERR_NOT_POSITIVE_DEFINITE, std::string(W_) + ": K not positive definite"));
+  if (flags[1]) return sync_fail(fail(BO_ERR_NOT_POSITIVE_DEFINITE, std::string(W_) + ": in-sample posterior covariance not positive definite"));
+  if (flags[2]) return sync_fail(fail(BO_ERR_NOT_POSITIVE_DEFINITE, std::string(W_) + ": noise-free K_XX not positive definite"));
+  z.counts.assign(reinterpret_cast<const int*>(stage + off_cnt),
+                  reinterpret_cast<const int*>(stage + off_cnt) + S);
+  int* off = reinterpret_cast<int*>(stage + off_off);
+  int64_t total = 0;
+  for (int i = 0; i < S; ++i) {
+    off[i] = static_cast<int>(total);
+    total += z.counts[i];
+  }
+  off[S] = static_cast<int>(total);
+  if (nehvi_ehvi_lds_bytes(S, static_cast<int>(total)) > kLdsLimit)
+    return sync_fail(fail(BO_ERR_CAPACITY, std::string(W_) + ": per-sample boxes exceed LDS"));
+  double gmax[2];
+  std::memcpy(gmax, stage + off_gmax, sizeof(gmax));
+  float scale[2];
+  for (int k = 0; k < m; ++k) {
+    // a power of two that brings max |G| into [2^13, 2^14): the fp16 low
+    // halves then stay clear of the subnormal range
+    int ex = 0;
+    if (gmax[k] > 0.0 && std::isfinite(gmax[k])) ex = 13 - static_cast<int>(std::floor(std::log2(gmax[k])));
+    ex = std::max(-60, std::min(60, ex));
+    scale[k] = std::ldexp(1.0f, ex);
+    z.ginv[k] = std::ldexp(1.0f, -ex);
+  }
+  if ((s = palloc(&z.Gp, (size_t)m * n32 * nrb * 1024, st, "noisy: G fragments")) != BO_OK) return sync_fail(s);
+  if ((s = palloc(&z.boxes, (size_t)total * 4, st, "noisy: boxes")) != BO_OK) return sync_fail(s);
+  if ((s = palloc(&z.off, (size_t)S + 1, st, "noisy: box offsets")) != BO_OK) return sync_fail(s);
+  e = hipMemcpyAsync(z.off, off, sizeof(int) * (S + 1), hipMemcpyHostToDevice, st);
+  if (e != hipSuccess) return sync_fail(hip_fail(e, "bo_nehvi_prepare: offsets"));
+  if ((s = step(launch_compact_boxes(sc.btmp, (int64_t)(n + 1) * 4, z.off, S, z.boxes, st), "boxes")) != BO_OK) return sync_fail(s);
+  if ((s = step(launch_pack_g(sc.G, nf, Sp, n32, m, scale, z.Gp, st), "pack G")) != BO_OK) return sync_fail(s);
+  e = hipStreamSynchronize(st);
+  if (e != hipSuccess) return sync_fail(hip_fail(e, "bo_nehvi_prepare: sync"));
+  z.S = S; z.Sp = Sp; z.n32 = n32; z.total = static_cast<int>(total);
+  z.cons = lower != nullptr;
+  z.low[0] = lower ? lower[0] : -INFINITY;
+  z.low[1] = lower ? lower[1] : -INFINITY;
+  M.last_stream = st;
+  return BO_OK;
+}
+
+bo_status score_nehvi_impl(bo_model model, const float* cand, int64_t M_, const float* Z,
+                           int32_t S, float* ehvi, void* stream) {
+  if (!model) return fail(BO_ERR_INVALID_ARGUMENT, "bo_score_nehvi: model is NULL");
+  Model& M = model->m;
+  Model::Noisy& z = M.nz;
+  if (z.S == 0) return fail(BO_ERR_INVALID_ARGUMENT, "bo_score_nehvi: call bo_nehvi_prepare first");
+  if (S != z.S) return fail(BO_ERR_INVALID_ARGUMENT, "bo_score_nehvi: S differs from the prepared S");
+  if (M_ < 0) return fail(BO_ERR_INVALID_ARGUMENT, "bo_score_nehvi: M < 0");
+  if (M_ > (int64_t)1 << 40) return fail(BO_ERR_CAPACITY, "bo_score_nehvi: M too large");
+  if (M_ == 0) return BO_OK;
+  DeviceGuard g(M.device);
+  if (!g.ok) return fail(BO_ERR_DEVICE, "bo_score_nehvi: cannot select the model's device");
+  bo_status s;
+  if ((s = check_dev(cand, sizeof(float) * M_ * M.d, "cand")) != BO_OK) return s;
+  if ((s = check_dev(Z, sizeof(float) * (size_t)S * 2, "base_samples")) != BO_OK) return s;
+  if ((s = check_dev(ehvi, sizeof(float) * M_, "ehvi")) != BO_OK) return s;
+  if (posterior_lds_bytes(M.nb, 1) > kLdsLimit)
+    return fail(BO_ERR_CAPACITY, "bo_score_nehvi: posterior tile exceeds LDS");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int m = 2;
+  const int64_t C = std::min<int64_t>(M_, kNehviChunk);
+  const size_t need = (size_t)C * m * 2 + (size_t)m * S * C;
+  if (need > z.ws_floats) {
+    if (z.ws) {
+      hipError_t e = hipDeviceSynchronize();      // earlier launches may use it
+      if (e != hipSuccess) return hip_fail(e, "bo_score_nehvi: sync before workspace growth");
+      pfree(z.ws, st);
+    }
+    z.ws_floats = 0;
+    if ((s = palloc(&z.ws, need, st, "noisy: scoring workspace")) != BO_OK) return s;
+    z.ws_floats = need;
+  }
+  float* mu_buf = z.ws;
+  float* sd_buf = z.ws + (size_t)C * m;
+  float* dbuf = z.ws + (size_t)C * m * 2;
+  for (int64_t c0 = 0; c0 < M_; c0 += C) {
+    const int64_t np_ = std::min<int64_t>(C, M_ - c0);
+    for (int k = 0; k < m; ++k) {
+      PosteriorArgs pa;
+      pa.cand = cand + c0 * M.d; pa.npts = np_; pa.d = M.d; pa.dx = M.dx; pa.q = 1;
+      pa.Xs = M.Xs + (size_t)k * M.n_pad * M.dx;
+      pa.invls = M.invls + (size_t)k * M.dx;
+      pa.alpha = M.alpha + (size_t)k * M.n_pad;
+      pa.Lp = z.Lp0 + (size_t)k * M.lp_per_obj;
+      pa.n = static_cast<int>(M.n); pa.nb = M.nb;
+      pa.s = M.os[k];
+      pa.m = m; pa.k = k;
+      pa.dr = 0; pa.dr4 = 0; pa.s_dep = 0.f; pa.s_int = 0.f; pa.wts = nullptr; pa.pref = nullptr;
+      pa.mu = mu_buf; pa.sd = sd_buf; pa.chol = nullptr;
+      if ((s = after_launch(launch_posterior(pa, st), st, "posterior")) != BO_OK) return s;
+    }
+    NehviMeansArgs ma;
+    ma.cand = cand + c0 * M.d; ma.npts = np_; ma.d = M.d; ma.dx = M.dx; ma.n32 = z.n32;
+    ma.n_pad = M.n_pad; ma.S = S; ma.Xs = M.Xs; ma.invls = M.invls; ma.Gp = z.Gp;
+    for (int k = 0; k < m; ++k) { ma.s[k] = M.os[k]; ma.ginv[k] = z.ginv[k]; }
+    ma.out = dbuf; ma.ldo = C;
+    if ((s = after_launch(launch_nehvi_means(ma, m, st), st, "conditional means")) != BO_OK) return s;
+    NehviEhviArgs ea;
+    ea.mu = mu_buf; ea.sd = sd_buf; ea.D = dbuf; ea.ldd = C; ea.Z = Z;
+    ea.boxes = z.boxes; ea.off = z.off; ea.total = z.total; ea.npts = np_; ea.S = S;
+    ea.cons = z.cons; ea.low0 = z.low[0]; ea.low1 = z.low[1]; ea.ehvi = ehvi + c0;
+    if ((s = after_launch(launch_nehvi_ehvi(ea, st), st, "noisy ehvi")) != BO_OK) return s;
+  }
+  M.last_stream = st;
+  return BO_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+bo_status bo_nehvi_prepare(bo_model model, const float* base_samples_X, int32_t S,
+                           const float* ref_point, const float* feas_lower, void* stream) {
+  return nehvi_prepare_impl(model, base_samples_X, S, ref_point, feas_lower, stream);
+}
+
+bo_status bo_score_nehvi(bo_model model, const float* cand, int64_t M, const float* base_samples,
+                         int32_t S, float* ehvi, void* stream) {
+  return score_nehvi_impl(model, cand, M, base_samples, S, ehvi, stream);
+}
+
+bo_status bo_nehvi_front(bo_model model, int32_t sample, int32_t* idx_host, int32_t cap,
+                         int32_t* count) {
+  if (!model || !count || cap < 0 || (cap > 0 && !idx_host))
+    return fail(BO_ERR_INVALID_ARGUMENT, "bo_nehvi_front: bad argument");
+  Model& M = model->m;
+  if (M.nz.S == 0) return fail(BO_ERR_INVALID_ARGUMENT, "bo_nehvi_front: not prepared");
+  if (sample < 0 || sample >= M.nz.S)
+    return fail(BO_ERR_INVALID_ARGUMENT, "bo_nehvi_front: sample out of range");
+  const int32_t P = M.nz.counts[sample] - 1;
+  *count = P;
+  const int32_t k = std::min(cap, P);
+  if (k > 0) {
+    DeviceGuard g(M.device);
+    hipError_t e = hipMemcpy(idx_host, M.nz.front + (size_t)sample * M.n, sizeof(int32_t) * k,
+                             hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return hip_fail(e, "bo_nehvi_front: copy");
+  }
   return BO_OK;
 }
 

@@ -56,6 +56,24 @@ struct Model {
   // scoring workspace (grown on demand)
   float* ws = nullptr;
   size_t ws_floats = 0;
+  // noisy acquisition (bo_nehvi_prepare): per-sample fronts and the factors
+  // of the in-sample conditional
+  struct Noisy {
+    int S = 0, Sp = 0, n32 = 0, total = 0;
+    float* Lp0 = nullptr;        // [m][lp_per_obj] packed inverse factor of K_XX (no noise)
+    uint16_t* Gp = nullptr;      // [m][n32][Sp/16][1024] fp16 hi/lo fragments of G^T
+    float ginv[2] = {1.f, 1.f};  // 1 / scale applied to G before the split
+    float* boxes = nullptr;      // [total][4] per-sample boxes, sample s at off[s]
+    int* off = nullptr;          // [S + 1]
+    int32_t* front = nullptr;    // [S][n] per-sample front indices, sorted by objective 0
+    std::vector<int> counts;     // [S] boxes per sample (front size + 1)
+    bool cons = false;
+    float low[2] = {0.f, 0.f};
+    float* ws = nullptr;         // scoring workspace
+    size_t ws_floats = 0;
+  } nz;
+  float* Xd = nullptr;           // [n][d] copy of the training inputs
+
   // box cache (rebuilt when the reference point changes)
   float* d_boxes = nullptr;      // [nbox][2m]: lo then width
   int box_cap = 0;
@@ -114,6 +132,76 @@ hipError_t launch_mll(const float* X, int64_t n, int d, int m, int nf, const Gra
 hipError_t launch_pack(const double* W, int64_t n, int m, int nf, int nb,
                        float* Lp, const float* X, int d, int dx, int dr, int dr4,
                        const float* invls, float* Xs, hipStream_t st);
+
+// Noisy acquisition, fp64 preparation (fit.hip).
+// A holds K^{-1} in its lower 64-blocks on return (from W = L^{-1}).
+hipError_t launch_kinv(double* A, const double* W, int nf, int m, hipStream_t st);
+// A (lower 64-blocks, K^{-1} on entry) <- eta (I - eta K^{-1}), identity tail.
+hipError_t launch_sigma_xx(double* A, int64_t n, int nf, int m, const double* noise,
+                           hipStream_t st);
+// Zk[k][i][s] = ZX[s][i][k] (fp64 [m][nf][Sp], zero-padded).
+hipError_t launch_gather_z(const float* ZX, int64_t n, int m, int S, int nf, int Sp,
+                           double* Zk, hipStream_t st);
+// C[k] = op(T[k]) Bm[k]: T lower [nf][nf], Bm and C [nf][ldb], op = T or T^T.
+hipError_t launch_trmm(bool trans, const double* T, const double* Bm, double* C, int nf,
+                       int ldb, int m, hipStream_t st);
+// The posterior's A-fragment packing of W alone (no coordinate scaling).
+hipError_t launch_pack_factor(const double* W, int64_t n, int m, int nf, int nb, float* Lp,
+                              hipStream_t st);
+
+// Noisy acquisition kernels (nehvi.hip).
+struct NehviFrontArgs {
+  const float* Y;          // [n][2] observations (fp32)
+  const double* alpha64;   // [2][nf] K^{-1} y
+  const double* noise;     // [2] noise variances
+  const double* T1;        // [2][nf][Sp] L_XX Z_X
+  int64_t n;
+  int nf, Sp, S;
+  float ref0, ref1;
+  bool cons;
+  float low0, low1;
+  float* boxes;            // [S][n + 1][4]
+  int* counts;             // [S] boxes per sample
+  int32_t* front;          // [S][n]
+};
+hipError_t launch_sample_fronts(const NehviFrontArgs& a, hipStream_t st);
+size_t nehvi_front_lds_bytes(int64_t n);
+hipError_t launch_absmax(const double* G, int64_t count, int m, double* out, hipStream_t st);
+hipError_t launch_pack_g(const double* G, int nf, int Sp, int n32, int m, const float* scale,
+                         uint16_t* Gp, hipStream_t st);
+hipError_t launch_compact_boxes(const float* tmp, int64_t stride, const int* off, int S,
+                                float* out, hipStream_t st);
+struct NehviMeansArgs {
+  const float* cand;       // [npts][d]
+  int64_t npts;
+  int d, dx, n32, n_pad, S;
+  const float* Xs;         // [m][n_pad][dx] scaled training inputs
+  const float* invls;      // [m][dx]
+  const uint16_t* Gp;      // packed G^T fragments (fp16 bits)
+  float s[2];              // output scales
+  float ginv[2];           // 1 / scale of G
+  float* out;              // [m][S][ldo]
+  int64_t ldo;
+};
+hipError_t launch_nehvi_means(const NehviMeansArgs& a, int m, hipStream_t st);
+struct NehviEhviArgs {
+  const float* mu;         // [npts][2] posterior mean
+  const float* sd;         // [npts][2] noise-free conditional std (tau)
+  const float* D;          // [2][S][ldd] K* G
+  int64_t ldd;
+  const float* Z;          // [S][2] candidate base samples
+  const float* boxes;      // [total][4]
+  const int* off;          // [S + 1]
+  int total;
+  int64_t npts;
+  int S;
+  bool cons;
+  float low0, low1;
+  float* ehvi;             // [npts]
+};
+hipError_t launch_nehvi_ehvi(const NehviEhviArgs& a, hipStream_t st);
+size_t nehvi_ehvi_lds_bytes(int S, int total);
+int nehvi_padded_samples(int S);
 
 // Coordinate held by slot t of the scaled layout, or -1 for padding: the
 // identity for plain models (dr = dr4 = 0); for composite ones the routing

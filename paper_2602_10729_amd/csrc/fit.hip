@@ -699,6 +699,77 @@ __global__ void k_f32_to_padded(const float* __restrict__ Asrc, int64_t n, int n
   P[e] = v;
 }
 
+// ---- noisy acquisition: in-sample posterior and its products --------------
+
+// In-sample posterior covariance of the latent objective from K^{-1}:
+// Sigma_XX = K_XX - K_XX K^{-1} K_XX = eta (I - eta K^{-1}) (K = K_XX + eta I,
+// so K_XX = K - eta I). A holds K^{-1} in its lower 64-blocks on entry and
+// Sigma_XX there on return, with an identity tail past n.
+__global__ __launch_bounds__(256) void k_sigma_xx(double* __restrict__ A, int64_t n, int nf,
+                                                  const double* __restrict__ noise) {
+  const int k = blockIdx.y;
+  const int t = blockIdx.x;
+  int I = static_cast<int>((sqrt(8.0 * t + 1.0) - 1.0) * 0.5);
+  while ((I + 1) * (I + 2) / 2 <= t) ++I;
+  while (I * (I + 1) / 2 > t) --I;
+  const int J = t - I * (I + 1) / 2;
+  const double eta = noise[k];
+  double* Ak = A + (int64_t)k * nf * nf;
+  for (int e = threadIdx.x; e < B * B; e += 256) {
+    const int64_t i = (int64_t)I * B + e / B, j = (int64_t)J * B + e % B;
+    double* a = Ak + i * nf + j;
+    if (i < n && j < n) *a = ((i == j) ? eta : 0.0) - eta * eta * *a;
+    else *a = (i == j) ? 1.0 : 0.0;
+  }
+}
+
+// Zk[k][i][s] = ZX[s][i][k] (fp64), zero for i >= n or s >= S.
+__global__ __launch_bounds__(256) void k_gather_z(const float* __restrict__ ZX, int64_t n, int m,
+                                                  int S, int nf, int Sp, double* __restrict__ Zk) {
+  const int k = blockIdx.y;
+  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (e >= (int64_t)nf * Sp) return;
+  const int64_t i = e / Sp;
+  const int s = static_cast<int>(e % Sp);
+  Zk[(int64_t)k * nf * Sp + e] =
+      (i < n && s < S) ? static_cast<double>(ZX[((int64_t)s * n + i) * m + k]) : 0.0;
+}
+
+// C[k] = op(T[k]) Bm[k] for lower-triangular T [nf][nf] (only its lower
+// 64-blocks are read; diagonal blocks hold zeros above the diagonal), op =
+// identity or transpose; Bm, C [nf][ldb]. One 64x64 tile of C per workgroup,
+// over the 64-blocks of T that the triangle leaves non-zero.
+template <bool TRANS>
+__global__ __launch_bounds__(256) void k_trmm(const double* __restrict__ T,
+                                              const double* __restrict__ Bm,
+                                              double* __restrict__ C, int nf, int ldb) {
+  __shared__ double p[B][LDP];
+  __shared__ double q[B][LDP];
+  const int k = blockIdx.z, I = blockIdx.y, Jc = blockIdx.x;
+  const int nbk = nf / B;
+  const double* Tk = T + (int64_t)k * nf * nf;
+  const double* Bk = Bm + (int64_t)k * nf * ldb;
+  const int tx = threadIdx.x % 16, ty = threadIdx.x / 16;
+  double acc[4][4] = {};
+  const int k0 = TRANS ? I : 0, k1 = TRANS ? nbk : I + 1;
+  for (int K = k0; K < k1; ++K) {
+    __syncthreads();   // the previous step's tiles are no longer read
+    double v0[16], v1[16];
+    // P[i][t] = op(T)[I*B + i][K*B + t]; Q[c][t] = Bm[K*B + t][Jc*B + c]
+    get_tile(v0, TRANS ? Tk + (int64_t)K * B * nf + I * B : Tk + (int64_t)I * B * nf + K * B, nf);
+    get_tile(v1, Bk + (int64_t)K * B * ldb + Jc * B, ldb);
+    put_tile<TRANS>(p, v0);
+    put_tile<true>(q, v1);
+    __syncthreads();
+    gemm_nt_64(p, q, acc, ty, tx);
+  }
+  double* dst = C + (int64_t)k * nf * ldb + (int64_t)I * B * ldb + Jc * B;
+#pragma unroll
+  for (int r = 0; r < 4; ++r)
+#pragma unroll
+    for (int c = 0; c < 4; ++c) dst[(int64_t)(ty * 4 + r) * ldb + tx * 4 + c] = acc[r][c];
+}
+
 }  // namespace
 
 hipError_t launch_gram(const float* X, int64_t n, int d, int m, int n_fit,
@@ -772,6 +843,44 @@ hipError_t launch_pack(const double* W, int64_t n, int m, int nf, int nb, float*
   const unsigned gx2 = static_cast<unsigned>(((int64_t)n_pad * dx + 255) / 256);
   hipLaunchKernelGGL(k_scale_x, dim3(gx2, m), dim3(256), 0, st, X, n, d, dx, dr, dr4, n_pad,
                      invls, Xs);
+  return hipGetLastError();
+}
+
+hipError_t launch_kinv(double* A, const double* W, int nf, int m, hipStream_t st) {
+  const int nbk = nf / B;
+  hipLaunchKernelGGL(k_kinv, dim3(nbk * (nbk + 1) / 2, m), dim3(256), 0, st, A, W, nf);
+  return hipGetLastError();
+}
+
+hipError_t launch_sigma_xx(double* A, int64_t n, int nf, int m, const double* noise,
+                           hipStream_t st) {
+  const int nbk = nf / B;
+  hipLaunchKernelGGL(k_sigma_xx, dim3(nbk * (nbk + 1) / 2, m), dim3(256), 0, st, A, n, nf, noise);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather_z(const float* ZX, int64_t n, int m, int S, int nf, int Sp,
+                           double* Zk, hipStream_t st) {
+  const unsigned g = static_cast<unsigned>(((int64_t)nf * Sp + 255) / 256);
+  hipLaunchKernelGGL(k_gather_z, dim3(g, m), dim3(256), 0, st, ZX, n, m, S, nf, Sp, Zk);
+  return hipGetLastError();
+}
+
+hipError_t launch_trmm(bool trans, const double* T, const double* Bm, double* C, int nf,
+                       int ldb, int m, hipStream_t st) {
+  if (nf % B != 0 || ldb % B != 0) return hipErrorInvalidValue;
+  const dim3 grid(ldb / B, nf / B, m);
+  if (trans) hipLaunchKernelGGL(k_trmm<true>, grid, dim3(256), 0, st, T, Bm, C, nf, ldb);
+  else hipLaunchKernelGGL(k_trmm<false>, grid, dim3(256), 0, st, T, Bm, C, nf, ldb);
+  return hipGetLastError();
+}
+
+hipError_t launch_pack_factor(const double* W, int64_t n, int m, int nf, int nb, float* Lp,
+                              hipStream_t st) {
+  const int64_t nblk = posterior_frag_blocks(nb);   // with the zero block
+  const unsigned gx = static_cast<unsigned>((nblk * 64 + 255) / 256);
+  hipLaunchKernelGGL(k_pack, dim3(gx, m), dim3(256), 0, st, W, n, nf, nblk,
+                     reinterpret_cast<_Float16*>(Lp));
   return hipGetLastError();
 }
 

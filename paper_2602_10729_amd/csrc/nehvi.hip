@@ -1,0 +1,499 @@
+// Noisy expected hypervolume improvement (qNEHVI, q = 1, two objectives).
+//
+// Paper: "Overall MOBO workflow" step (ii) and the constrained qNEHVI
+// paragraph: the acquisition averages, over Monte-Carlo samples of the joint
+// posterior, the hypervolume improvement of the candidate; the noisy form
+// (after Daulton et al. 2021) samples the latent objectives at the observed
+// points too and measures each sample's improvement against the Pareto front
+// of that sample's in-sample values.
+//
+// Given the in-sample draw f_X^s, the candidate's latent value is Gaussian
+// with mean k*^T K_XX^{-1} f_X^s and variance tau^2 = s - k*^T K_XX^{-1} k*
+// (once f_X is known the noisy y adds nothing, so this is the noise-free GP).
+// With f_X^s = mu_X + L_XX z_X^s (L_XX the factor of the in-sample posterior
+// covariance) and K_XX^{-1} mu_X = K^{-1} y:
+//   y_s = mu* + (K* G)[s] + tau z*_s,   G = K_XX^{-1} L_XX Z_X  [n][S],
+// mu* the ordinary posterior mean.
+//
+// bo_nehvi_prepare (fp64, once per set of in-sample base samples) builds
+// f_X^s, every sample's front and staircase boxes (k_sample_front), G and
+// its fp16 hi/lo fragments (k_pack_g), and the packed inverse factor of K_XX.
+// Scoring runs per chunk of candidates: the posterior kernel on the
+// noise-free factor (mu*, tau), k_nehvi_means (K* G on the matrix cores, K*
+// evaluated on the fly), then k_nehvi_ehvi (per-sample HVI against that
+// sample's boxes).
+#include <hip/hip_runtime.h>
+
+#include "bo_internal.h"
+
+namespace bo {
+namespace {
+
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef _Float16 halfx8 __attribute__((ext_vector_type(8)));
+typedef _Float16 halfx4 __attribute__((ext_vector_type(4)));
+
+// ---- per-sample fronts --------------------------------------------------------
+
+// One workgroup per sample s. In-sample values
+//   f_ik = y_ik - eta_k alpha_k,i + (L_XX Z_X)[k][i][s]   (mu_X = y - eta alpha),
+// points strictly above ref (and meeting the feasibility thresholds) take
+// part; the front is the non-dominated set (maximise; exact duplicates keep
+// the lowest index), sorted by objective 0 ascending. Box r (r < P) spans
+// objective 0 from the previous front value (ref for r = 0) to f_r,0 and
+// objective 1 from f_r,1 up; box P spans objective 0 from the last front
+// value up and objective 1 from ref up. Boxes are (lo0, lo1, width0, width1),
+// widths in fp32 (inf for unbounded sides).
+__global__ __launch_bounds__(256) void k_sample_front(NehviFrontArgs a) {
+  extern __shared__ double fsh[];
+  __shared__ int tsum[256];
+  __shared__ int np;
+  const int n = static_cast<int>(a.n);
+  double* f0 = fsh;
+  double* f1 = fsh + n;
+  int* flag = reinterpret_cast<int*>(fsh + 2 * n);
+  int* pidx = flag + n;
+  int* sorted = pidx + n;
+  const int s = blockIdx.x, tid = threadIdx.x;
+  const double e0 = a.noise[0], e1 = a.noise[1];
+  for (int i = tid; i < n; i += 256) {
+    const double v0 = static_cast<double>(a.Y[2 * i]) - e0 * a.alpha64[i] +
+                      a.T1[(int64_t)i * a.Sp + s];
+    const double v1 = static_cast<double>(a.Y[2 * i + 1]) - e1 * a.alpha64[a.nf + i] +
+                      a.T1[((int64_t)a.nf + i) * a.Sp + s];
+    bool ok = v0 > static_cast<double>(a.ref0) && v1 > static_cast<double>(a.ref1);
+    if (a.cons) ok = ok && v0 >= static_cast<double>(a.low0) && v1 >= static_cast<double>(a.low1);
+    // points that take no part can dominate nothing
+    f0[i] = ok ? v0 : -__builtin_inf();
+    f1[i] = ok ? v1 : -__builtin_inf();
+    flag[i] = ok ? 1 : 0;
+  }
+  __syncthreads();
+  for (int i = tid; i < n; i += 256) {
+    if (!flag[i]) continue;
+    const double a0 = f0[i], a1 = f1[i];
+    bool dom = false;
+    for (int j = 0; j < n; ++j) {
+      const double b0 = f0[j], b1 = f1[j];
+      const bool ge = b0 >= a0 && b1 >= a1;
+      dom = dom || (ge && (b0 > a0 || b1 > a1)) || (ge && b0 == a0 && b1 == a1 && j < i);
+    }
+    pidx[i] = dom ? 0 : 1;          // front flags (flag[] is still read by others)
+  }
+  __syncthreads();
+  for (int i = tid; i < n; i += 256) flag[i] = flag[i] ? pidx[i] : 0;
+  __syncthreads();
+  // compaction in index order: thread t owns a contiguous chunk
+  const int per = (n + 255) / 256;
+  const int i0 = min(n, tid * per), i1 = min(n, i0 + per);
+  int cnt = 0;
+  for (int i = i0; i < i1; ++i) cnt += flag[i];
+  tsum[tid] = cnt;
+  __syncthreads();
+  if (tid == 0) {
+    int run = 0;
+    for (int t = 0; t < 256; ++t) {
+      const int c = tsum[t];
+      tsum[t] = run;
+      run += c;
+    }
+    np = run;
+  }
+  __syncthreads();
+  {
+    int p = tsum[tid];
+    for (int i = i0; i < i1; ++i)
+      if (flag[i]) pidx[p++] = i;
+  }
+  __syncthreads();
+  const int P = np;
+  // rank by objective 0 (ties by position, i.e. by index)
+  for (int q = tid; q < P; q += 256) {
+    const double v = f0[pidx[q]];
+    int rank = 0;
+    for (int r = 0; r < P; ++r) {
+      const double w = f0[pidx[r]];
+      rank += (w < v || (w == v && r < q)) ? 1 : 0;
+    }
+    sorted[rank] = pidx[q];
+  }
+  __syncthreads();
+  float* bx = a.boxes + (int64_t)s * (n + 1) * 4;
+  for (int r = tid; r <= P; r += 256) {
+    float lo0, lo1, w0, w1 = __builtin_inff();
+    lo0 = (r == 0) ? a.ref0 : static_cast<float>(f0[sorted[r - 1]]);
+    if (r < P) {
+      const int i = sorted[r];
+      w0 = static_cast<float>(f0[i]) - lo0;
+      lo1 = static_cast<float>(f1[i]);
+      a.front[(int64_t)s * n + r] = i;
+    } else {
+      w0 = __builtin_inff();
+      lo1 = a.ref1;
+    }
+    *reinterpret_cast<float4*>(bx + 4 * r) = float4{lo0, lo1, w0, w1};
+  }
+  if (tid == 0) a.counts[s] = P + 1;
+}
+
+// out[k] = max |G[k][e]| over count entries.
+__global__ __launch_bounds__(256) void k_absmax(const double* __restrict__ G, int64_t count,
+                                                double* __restrict__ out) {
+  __shared__ double red[256];
+  const int k = blockIdx.x;
+  const double* g = G + (int64_t)k * count;
+  double v = 0.0;
+  for (int64_t e = threadIdx.x; e < count; e += 256) v = fmax(v, fabs(g[e]));
+  red[threadIdx.x] = v;
+  __syncthreads();
+  for (int h = 128; h > 0; h >>= 1) {
+    if (threadIdx.x < h) red[threadIdx.x] = fmax(red[threadIdx.x], red[threadIdx.x + h]);
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) out[k] = red[0];
+}
+
+// A fragments of G^T (scaled by sc[k]) for v_mfma_f32_16x16x32_f16: block
+// (J, rb) covers training rows 32J .. 32J+31 and samples 16rb .. 16rb+15;
+// lane l element e holds G[32J + 8(l/16) + e][16rb + l%16], split as
+// hi = fp16(g), lo = fp16(g - hi). Layout [k][J][rb][plane][64][8].
+__global__ __launch_bounds__(256) void k_pack_g(const double* __restrict__ G, int nf, int Sp,
+                                                int n32, int nrb, float sc0, float sc1,
+                                                _Float16* __restrict__ Gp) {
+  const int k = blockIdx.y;
+  const int64_t g = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (g >= (int64_t)n32 * nrb * 64) return;
+  const int lane = static_cast<int>(g % 64);
+  const int64_t blk = g / 64;
+  const int J = static_cast<int>(blk / nrb), rb = static_cast<int>(blk % nrb);
+  const double sc = (k == 0) ? sc0 : sc1;
+  const int col = 16 * rb + lane % 16;
+  _Float16* dst = Gp + ((int64_t)k * n32 * nrb + blk) * 1024 + lane * 8;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int row = 32 * J + 8 * (lane / 16) + e;
+    const double w = sc * G[((int64_t)k * nf + row) * Sp + col];
+    const _Float16 h = static_cast<_Float16>(static_cast<float>(w));
+    dst[e] = h;
+    dst[512 + e] = static_cast<_Float16>(static_cast<float>(w - static_cast<double>(h)));
+  }
+}
+
+// Boxes of sample s from the per-sample layout [S][stride] to the compact
+// one at off[s].
+__global__ __launch_bounds__(64) void k_compact_boxes(const float* __restrict__ tmp,
+                                                      int64_t stride, const int* __restrict__ off,
+                                                      float* __restrict__ out) {
+  const int s = blockIdx.x;
+  const int b0 = off[s], nb = off[s + 1] - b0;
+  for (int b = threadIdx.x; b < nb; b += 64)
+    *reinterpret_cast<float4*>(out + 4 * (int64_t)(b0 + b)) =
+        *reinterpret_cast<const float4*>(tmp + (int64_t)s * stride + 4 * b);
+}
+
+// ---- conditional means K* G on the matrix cores -------------------------------
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* p, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, bytes, 0x00020000);
+}
+
+__device__ __forceinline__ float4 ld4(__amdgpu_buffer_rsrc_t rs, int voff, int soff) {
+  return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rs, voff, soff, 0));
+}
+
+// LDS-only barrier: waits for this wave's LDS traffic, not for its global
+// loads in flight (the next step's fragments), then joins the workgroup.
+__device__ __forceinline__ void lds_sync() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+__device__ __forceinline__ float m52(float r2, float s) {
+  const float r = __builtin_amdgcn_sqrtf(r2);
+  constexpr float kNegSqrt5Log2e = static_cast<float>(-2.23606797749978969641 * 1.44269504088896340736);
+  const float e = __builtin_amdgcn_exp2f(kNegSqrt5Log2e * r);
+  return s * fmaf(r, 2.23606798f, fmaf(r2, 1.66666667f, 1.0f)) * e;
+}
+
+constexpr int kMW = 8;                 // waves per workgroup
+constexpr int kMT = 64;                // candidates per tile
+constexpr int kKS = 40;                // ring: halves per candidate row (32 + 8 pad)
+constexpr int kPlane = kMT * kKS;      // halves per fp16 plane
+constexpr int kRingSlot = 2 * kPlane;  // hi + lo planes of one 32-row block
+
+// D[k][s][c] = sum_i G[k][i][s] K*_k(c, i) for the candidates of one tile and
+// every sample: blockIdx.x = tile of 64 candidates, blockIdx.y = objective.
+// Each 32-row block J of K*^T (training rows x candidates) is evaluated two
+// steps ahead into a three-slot LDS ring as fp16 hi/lo planes (wave w makes
+// rows 4w .. 4w+3 for all 64 candidates, one candidate per lane, from
+// training rows staged in LDS three steps ahead), while the matrix cores add
+// G^T[slots of this wave][J] K*^T[J] into accumulators that stay in registers
+// for the whole tile: wave w owns the sample blocks w + 8r (r < CB), all four
+// candidate blocks. Three products per pair (hi hi, hi lo, lo hi), fp32
+// accumulate. Training rows past the matrix read as zero; their G rows are
+// zero, so they add nothing.
+template <int DX4, int CB>
+__global__ __launch_bounds__(kMW * 64) void k_nehvi_means(NehviMeansArgs a) {
+  constexpr int RS = 4 * DX4;
+  __shared__ __align__(16) float xst[2][32 * RS];
+  __shared__ __align__(16) _Float16 ring[3 * kRingSlot];
+  const int k = blockIdx.y;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  const int64_t c0 = (int64_t)blockIdx.x * kMT;
+  const int nrb = 8 * CB;
+  const float* Xs = a.Xs + (int64_t)k * a.n_pad * a.dx;
+  const float* il = a.invls + k * a.dx;
+  const float sk = a.s[k];
+  const __amdgpu_buffer_rsrc_t xs_rs = rsrc(Xs, a.n_pad * a.dx * 4);
+  const __amdgpu_buffer_rsrc_t g_rs = rsrc(a.Gp + (int64_t)k * a.n32 * nrb * 1024,
+                                           a.n32 * nrb * 2048);
+  // this lane's candidate, scaled (zero past npts and past d)
+  float cx[RS];
+  {
+    const int64_t c = c0 + lane;
+    const bool ok = c < a.npts;
+#pragma unroll
+    for (int t = 0; t < RS; ++t)
+      cx[t] = (ok && t < a.d) ? a.cand[c * a.d + t] * il[t] : 0.f;
+  }
+  // staging: thread t < 32 * DX4 moves one float4 of row t / DX4
+  const bool stager = threadIdx.x < 32 * DX4;
+  const int srow = stager ? threadIdx.x / DX4 : 0, st4 = threadIdx.x % DX4;
+  auto stage_load = [&](int jb) {
+    return ld4(xs_rs, ((jb * 32 + srow) * a.dx + 4 * st4) * 4, 0);
+  };
+  auto stage_store = [&](int jb, float4 v) {
+    if (stager) *reinterpret_cast<float4*>(&xst[jb & 1][srow * RS + 4 * st4]) = v;
+  };
+  auto produce = [&](int jb) {
+    const float* xr = &xst[jb & 1][4 * wave * RS];
+    halfx4 hi, lo;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      float r2 = 0.f;
+#pragma unroll
+      for (int t4 = 0; t4 < DX4; ++t4) {
+        const float4 x = *reinterpret_cast<const float4*>(xr + u * RS + 4 * t4);
+        const float d0 = cx[4 * t4 + 0] - x.x, d1 = cx[4 * t4 + 1] - x.y;
+        const float d2 = cx[4 * t4 + 2] - x.z, d3 = cx[4 * t4 + 3] - x.w;
+        r2 = fmaf(d0, d0, r2);
+        r2 = fmaf(d1, d1, r2);
+        r2 = fmaf(d2, d2, r2);
+        r2 = fmaf(d3, d3, r2);
+      }
+      const float kv = m52(r2, sk);
+      const _Float16 h = static_cast<_Float16>(kv);
+      hi[u] = h;
+      lo[u] = static_cast<_Float16>(kv - static_cast<float>(h));
+    }
+    _Float16* dst = ring + (jb % 3) * kRingSlot + lane * kKS + 4 * wave;
+    *reinterpret_cast<halfx4*>(dst) = hi;
+    *reinterpret_cast<halfx4*>(dst + kPlane) = lo;
+  };
+  auto load_a = [&](int J, halfx8 (&ah)[CB], halfx8 (&al)[CB]) {
+#pragma unroll
+    for (int r = 0; r < CB; ++r) {
+      const int blk = J * nrb + wave + 8 * r;
+      ah[r] = __builtin_bit_cast(halfx8, ld4(g_rs, lane * 16, blk * 2048));
+      al[r] = __builtin_bit_cast(halfx8, ld4(g_rs, lane * 16, blk * 2048 + 1024));
+    }
+  };
+
+  floatx4 acc[CB][4];
+#pragma unroll
+  for (int r = 0; r < CB; ++r)
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb) acc[r][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+  // prologue: rows of blocks 0, 1 staged; blocks 0, 1 produced; rows of 2 staged
+  stage_store(0, stage_load(0));
+  stage_store(1, stage_load(1));
+  __syncthreads();
+  produce(0);
+  if (a.n32 > 1) produce(1);
+  __syncthreads();
+  stage_store(2, stage_load(2));
+  halfx8 ah[CB], al[CB];
+  load_a(0, ah, al);
+  __syncthreads();
+
+  for (int J = 0; J < a.n32; ++J) {
+    const float4 nx = stage_load(J + 3);
+    halfx8 bh[4], bl[4];
+    const _Float16* kb = ring + (J % 3) * kRingSlot + (lane % 16) * kKS + 8 * (lane / 16);
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb) {
+      bh[cb] = *reinterpret_cast<const halfx8*>(kb + 16 * cb * kKS);
+      bl[cb] = *reinterpret_cast<const halfx8*>(kb + 16 * cb * kKS + kPlane);
+    }
+    halfx8 nh[CB], nl[CB];
+    load_a(min(J + 1, a.n32 - 1), nh, nl);
+    if (J + 2 < a.n32) produce(J + 2);
+#pragma unroll
+    for (int r = 0; r < CB; ++r)
+#pragma unroll
+      for (int cb = 0; cb < 4; ++cb) {
+        acc[r][cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah[r], bh[cb], acc[r][cb], 0, 0, 0);
+        acc[r][cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah[r], bl[cb], acc[r][cb], 0, 0, 0);
+        acc[r][cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(al[r], bh[cb], acc[r][cb], 0, 0, 0);
+      }
+#pragma unroll
+    for (int r = 0; r < CB; ++r) {
+      ah[r] = nh[r];
+      al[r] = nl[r];
+    }
+    stage_store(J + 3, nx);
+    lds_sync();
+  }
+
+  const float gi = a.ginv[k];
+#pragma unroll
+  for (int r = 0; r < CB; ++r)
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb) {
+      const int64_t c = c0 + 16 * cb + lane % 16;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int smp = 16 * (wave + 8 * r) + 4 * (lane / 16) + e;
+        if (smp < a.S && c < a.npts) a.out[((int64_t)k * a.S + smp) * a.ldo + c] = acc[r][cb][e] * gi;
+      }
+    }
+}
+
+// ---- per-sample HVI -----------------------------------------------------------
+
+// One lane per candidate: y_s,k = mu_k + D[k][s][c] + tau_k z*_s,k, then the
+// staircase HVI of y_s against the boxes of sample s (all lanes are at the
+// same sample, so every box read is an LDS broadcast). The constrained form
+// replaces an infeasible sample's first objective by -inf, which zeroes every
+// box term.
+template <bool CONS>
+__global__ __launch_bounds__(256) void k_nehvi_ehvi(NehviEhviArgs a) {
+  extern __shared__ float esm[];
+  float* zs = esm;                                          // [S][2]
+  float* bx = esm + 2 * a.S;                                // [total][4]
+  int* off = reinterpret_cast<int*>(bx + 4 * a.total);      // [S + 1]
+  for (int i = threadIdx.x; i < 2 * a.S; i += 256) zs[i] = a.Z[i];
+  for (int i = threadIdx.x; i < 4 * a.total; i += 256) bx[i] = a.boxes[i];
+  for (int i = threadIdx.x; i <= a.S; i += 256) off[i] = a.off[i];
+  __syncthreads();
+  const int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const bool valid = c < a.npts;
+  const int64_t cc = valid ? c : a.npts - 1;
+  const float mu0 = a.mu[2 * cc], mu1 = a.mu[2 * cc + 1];
+  const float t0 = a.sd[2 * cc], t1 = a.sd[2 * cc + 1];
+  const float* d0 = a.D + cc;
+  const float* d1 = a.D + (int64_t)a.S * a.ldd + cc;
+  float acc = 0.f;
+  constexpr int U = 8;
+  for (int s0 = 0; s0 < a.S; s0 += U) {
+    float v0[U], v1[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int s = min(s0 + u, a.S - 1);
+      v0[u] = d0[(int64_t)s * a.ldd];
+      v1[u] = d1[(int64_t)s * a.ldd];
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int s = s0 + u;
+      if (s >= a.S) break;
+      float y0 = mu0 + v0[u] + t0 * zs[2 * s];
+      const float y1 = mu1 + v1[u] + t1 * zs[2 * s + 1];
+      if constexpr (CONS) y0 = (y0 >= a.low0 && y1 >= a.low1) ? y0 : -__builtin_inff();
+      const int b1 = off[s + 1];
+      for (int b = off[s]; b < b1; ++b) {
+        const float4 q = *reinterpret_cast<const float4*>(bx + 4 * b);
+        acc += __builtin_amdgcn_fmed3f(y0 - q.x, 0.f, q.z) * __builtin_amdgcn_fmed3f(y1 - q.y, 0.f, q.w);
+      }
+    }
+  }
+  if (valid) a.ehvi[c] = acc / static_cast<float>(a.S);
+}
+
+template <int DX4>
+hipError_t means_dx(const NehviMeansArgs& a, dim3 grid, hipStream_t st) {
+  switch (a.S <= 128 ? 1 : a.S <= 256 ? 2 : a.S <= 384 ? 3 : 4) {
+    case 1: hipLaunchKernelGGL((k_nehvi_means<DX4, 1>), grid, dim3(kMW * 64), 0, st, a); break;
+    case 2: hipLaunchKernelGGL((k_nehvi_means<DX4, 2>), grid, dim3(kMW * 64), 0, st, a); break;
+    case 3: hipLaunchKernelGGL((k_nehvi_means<DX4, 3>), grid, dim3(kMW * 64), 0, st, a); break;
+    default: hipLaunchKernelGGL((k_nehvi_means<DX4, 4>), grid, dim3(kMW * 64), 0, st, a); break;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace
+
+size_t nehvi_front_lds_bytes(int64_t n) {
+  return sizeof(double) * 2 * n + sizeof(int) * 3 * n;
+}
+
+size_t nehvi_ehvi_lds_bytes(int S, int total) {
+  return sizeof(float) * (2 * (size_t)S + 4 * (size_t)total) + sizeof(int) * ((size_t)S + 1);
+}
+
+int nehvi_padded_samples(int S) { return (S + 127) / 128 * 128; }
+
+hipError_t launch_sample_fronts(const NehviFrontArgs& a, hipStream_t st) {
+  // at most 28 n bytes (57 KiB at n = 2048): within the default limit
+  const size_t lds = nehvi_front_lds_bytes(a.n);
+  hipLaunchKernelGGL(k_sample_front, dim3(a.S), dim3(256), lds, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_absmax(const double* G, int64_t count, int m, double* out, hipStream_t st) {
+  hipLaunchKernelGGL(k_absmax, dim3(m), dim3(256), 0, st, G, count, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_pack_g(const double* G, int nf, int Sp, int n32, int m, const float* scale,
+                         uint16_t* Gp, hipStream_t st) {
+  const int nrb = Sp / 16;
+  const unsigned g = static_cast<unsigned>(((int64_t)n32 * nrb * 64 + 255) / 256);
+  hipLaunchKernelGGL(k_pack_g, dim3(g, m), dim3(256), 0, st, G, nf, Sp, n32, nrb, scale[0],
+                     m > 1 ? scale[1] : 1.f, reinterpret_cast<_Float16*>(Gp));
+  return hipGetLastError();
+}
+
+hipError_t launch_compact_boxes(const float* tmp, int64_t stride, const int* off, int S,
+                                float* out, hipStream_t st) {
+  hipLaunchKernelGGL(k_compact_boxes, dim3(S), dim3(64), 0, st, tmp, stride, off, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_nehvi_means(const NehviMeansArgs& a, int m, hipStream_t st) {
+  if (a.npts <= 0) return hipSuccess;
+  if (a.S < 1 || a.S > 512 || a.dx % 4 != 0 || a.dx > BO_MAX_D) return hipErrorInvalidValue;
+  const dim3 grid(static_cast<unsigned>((a.npts + kMT - 1) / kMT), m);
+  switch (a.dx / 4) {
+    case 1: return means_dx<1>(a, grid, st);
+    case 2: return means_dx<2>(a, grid, st);
+    case 3: return means_dx<3>(a, grid, st);
+    case 4: return means_dx<4>(a, grid, st);
+    case 5: return means_dx<5>(a, grid, st);
+    case 6: return means_dx<6>(a, grid, st);
+    case 7: return means_dx<7>(a, grid, st);
+    case 8: return means_dx<8>(a, grid, st);
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_nehvi_ehvi(const NehviEhviArgs& a, hipStream_t st) {
+  if (a.npts <= 0) return hipSuccess;
+  static bool attr = false;
+  if (!attr) {
+    for (const void* f : {reinterpret_cast<const void*>(&k_nehvi_ehvi<false>),
+                          reinterpret_cast<const void*>(&k_nehvi_ehvi<true>)}) {
+      hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+      if (e != hipSuccess) return e;
+    }
+    attr = true;
+  }
+  const size_t lds = nehvi_ehvi_lds_bytes(a.S, a.total);
+  const unsigned grid = static_cast<unsigned>((a.npts + 255) / 256);
+  if (a.cons) hipLaunchKernelGGL(k_nehvi_ehvi<true>, dim3(grid), dim3(256), lds, st, a);
+  else hipLaunchKernelGGL(k_nehvi_ehvi<false>, dim3(grid), dim3(256), lds, st, a);
+  return hipGetLastError();
+}
+
+}  // namespace bo
