@@ -912,7 +912,7 @@ bo_status nehvi_prepare_impl(bo_model model, const float* ZX, int32_t S, const f
   if ((s = palloc(&sc.hyp, nhyp, st, "noisy: hyperparameters")) != BO_OK) return s;
   if ((s = palloc(&sc.tmp, (size_t)m * nf, st, "noisy: vector")) != BO_OK) return s;
   if ((s = palloc(&sc.alpha64, (size_t)m * nf, st, "noisy: alpha")) != BO_OK) return s;
-  if ((s = palloc(&sc.gmax, (size_t)m, st, "noisy: maxima")) != BO_OK) return s;
+  if ((s = palloc(&sc.gmax, (size_t)m * kAbsmaxParts, st, "noisy: maxima")) != BO_OK) return s;
   if ((s = palloc(&sc.Zk, vec, st, "noisy: base samples")) != BO_OK) return s;
   if ((s = palloc(&sc.T1, vec, st, "noisy: in-sample offsets")) != BO_OK) return s;
   if ((s = palloc(&sc.G, vec, st, "noisy: G")) != BO_OK) return s;
@@ -939,7 +939,7 @@ bo_status nehvi_prepare_impl(bo_model model, const float* ZX, int32_t S, const f
   const size_t off_y = off_flag + 16;
   const size_t off_cnt = (off_y + sizeof(float) * n * m + 15) / 16 * 16;
   const size_t off_gmax = (off_cnt + sizeof(int) * S + 15) / 16 * 16;
-  const size_t off_off = off_gmax + 16;
+  const size_t off_off = off_gmax + sizeof(double) * m * kAbsmaxParts;
   const size_t need = off_off + sizeof(int) * ((size_t)S + 1);
   hipError_t e = hipSuccess;
   if (need > DS->fit_stage_bytes) {
@@ -1004,7 +1004,8 @@ bo_status nehvi_prepare_impl(bo_model model, const float* ZX, int32_t S, const f
   if (e == hipSuccess)
     e = hipMemcpyAsync(stage + off_cnt, sc.counts, sizeof(int) * S, hipMemcpyDeviceToHost, st);
   if (e == hipSuccess)
-    e = hipMemcpyAsync(stage + off_gmax, sc.gmax, sizeof(double) * m, hipMemcpyDeviceToHost, st);
+    e = hipMemcpyAsync(stage + off_gmax, sc.gmax, sizeof(double) * m * kAbsmaxParts,
+                       hipMemcpyDeviceToHost, st);
   if (e == hipSuccess) e = hipStreamSynchronize(st);
   if (e != hipSuccess) return sync_fail(hip_fail(e, "bo_nehvi_prepare: sync"));
   int flags[3];
@@ -1023,8 +1024,12 @@ bo_status nehvi_prepare_impl(bo_model model, const float* ZX, int32_t S, const f
   off[S] = static_cast<int>(total);
   if (nehvi_ehvi_lds_bytes(S, static_cast<int>(total)) > kLdsLimit)
     return sync_fail(fail(BO_ERR_CAPACITY, std::string(W_) + ": per-sample boxes exceed LDS"));
-  double gmax[2];
-  std::memcpy(gmax, stage + off_gmax, sizeof(gmax));
+  double gmax[2] = {0.0, 0.0};
+  {
+    const double* parts = reinterpret_cast<const double*>(stage + off_gmax);
+    for (int k = 0; k < m; ++k)
+      for (int b = 0; b < kAbsmaxParts; ++b) gmax[k] = std::max(gmax[k], parts[k * kAbsmaxParts + b]);
+  }
   float scale[2];
   for (int k = 0; k < m; ++k) {
     // a power of two that brings max |G| into [2^13, 2^14): the fp16 low

@@ -166,7 +166,9 @@ struct NehviFrontArgs {
 };
 hipError_t launch_sample_fronts(const NehviFrontArgs& a, hipStream_t st);
 size_t nehvi_front_lds_bytes(int64_t n);
-hipError_t launch_absmax(const double* G, int64_t count, int m, double* out, hipStream_t st);
+// part [m][kAbsmaxParts]: partial maxima of |G[k]| (count entries per objective)
+constexpr int kAbsmaxParts = 128;
+hipError_t launch_absmax(const double* G, int64_t count, int m, double* part, hipStream_t st);
 hipError_t launch_pack_g(const double* G, int nf, int Sp, int n32, int m, const float* scale,
                          uint16_t* Gp, hipStream_t st);
 hipError_t launch_compact_boxes(const float* tmp, int64_t stride, const int* off, int S,

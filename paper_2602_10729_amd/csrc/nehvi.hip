@@ -24,6 +24,8 @@
 // sample's boxes).
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "bo_internal.h"
 
 namespace bo {
@@ -136,21 +138,23 @@ __global__ __launch_bounds__(256) void k_sample_front(NehviFrontArgs a) {
   if (tid == 0) a.counts[s] = P + 1;
 }
 
-// out[k] = max |G[k][e]| over count entries.
+// part[k][b] = max |G[k][e]| over the entries e = b*256 + t (mod 256 x
+// gridDim.x) of workgroup b; the host takes the maximum of the parts.
 __global__ __launch_bounds__(256) void k_absmax(const double* __restrict__ G, int64_t count,
-                                                double* __restrict__ out) {
+                                                double* __restrict__ part) {
   __shared__ double red[256];
-  const int k = blockIdx.x;
+  const int k = blockIdx.y;
   const double* g = G + (int64_t)k * count;
   double v = 0.0;
-  for (int64_t e = threadIdx.x; e < count; e += 256) v = fmax(v, fabs(g[e]));
+  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < count; e += (int64_t)gridDim.x * 256)
+    v = fmax(v, fabs(g[e]));
   red[threadIdx.x] = v;
   __syncthreads();
   for (int h = 128; h > 0; h >>= 1) {
     if (threadIdx.x < h) red[threadIdx.x] = fmax(red[threadIdx.x], red[threadIdx.x + h]);
     __syncthreads();
   }
-  if (threadIdx.x == 0) out[k] = red[0];
+  if (threadIdx.x == 0) part[(int64_t)k * gridDim.x + blockIdx.x] = red[0];
 }
 
 // A fragments of G^T (scaled by sc[k]) for v_mfma_f32_16x16x32_f16: block
@@ -317,7 +321,11 @@ __global__ __launch_bounds__(kMW * 64) void k_nehvi_means(NehviMeansArgs a) {
   load_a(0, ah, al);
   __syncthreads();
 
-  for (int J = 0; J < a.n32; ++J) {
+  // One step: the MFMAs of block J (each product pass over all accumulators
+  // before the next, so no MFMA waits on the one before it) and, when PROD,
+  // the evaluation of block J + 2, interleaved by the scheduler pattern below.
+  auto step = [&](int J, auto prod) {
+    constexpr bool PROD = decltype(prod)::value;
     const float4 nx = stage_load(J + 3);
     halfx8 bh[4], bl[4];
     const _Float16* kb = ring + (J % 3) * kRingSlot + (lane % 16) * kKS + 8 * (lane / 16);
@@ -328,15 +336,33 @@ __global__ __launch_bounds__(kMW * 64) void k_nehvi_means(NehviMeansArgs a) {
     }
     halfx8 nh[CB], nl[CB];
     load_a(min(J + 1, a.n32 - 1), nh, nl);
-    if (J + 2 < a.n32) produce(J + 2);
+    if constexpr (PROD) produce(J + 2);
 #pragma unroll
     for (int r = 0; r < CB; ++r)
 #pragma unroll
-      for (int cb = 0; cb < 4; ++cb) {
+      for (int cb = 0; cb < 4; ++cb)
         acc[r][cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah[r], bh[cb], acc[r][cb], 0, 0, 0);
+#pragma unroll
+    for (int r = 0; r < CB; ++r)
+#pragma unroll
+      for (int cb = 0; cb < 4; ++cb)
         acc[r][cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah[r], bl[cb], acc[r][cb], 0, 0, 0);
+#pragma unroll
+    for (int r = 0; r < CB; ++r)
+#pragma unroll
+      for (int cb = 0; cb < 4; ++cb)
         acc[r][cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(al[r], bh[cb], acc[r][cb], 0, 0, 0);
+    if constexpr (PROD) {
+      // interleave the kernel-value VALU work with the MFMAs
+      constexpr int nM = 12 * CB;
+      constexpr int nV = 4 * (8 * DX4 + 14);
+#pragma unroll
+      for (int i = 0; i < nM; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                  // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x002, (nV + nM - 1) / nM, 0);  // VALU
       }
+    }
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int r = 0; r < CB; ++r) {
       ah[r] = nh[r];
@@ -344,7 +370,10 @@ __global__ __launch_bounds__(kMW * 64) void k_nehvi_means(NehviMeansArgs a) {
     }
     stage_store(J + 3, nx);
     lds_sync();
-  }
+  };
+  int J = 0;
+  for (; J + 2 < a.n32; ++J) step(J, std::true_type{});
+  for (; J < a.n32; ++J) step(J, std::false_type{});
 
   const float gi = a.ginv[k];
 #pragma unroll
@@ -367,17 +396,19 @@ __global__ __launch_bounds__(kMW * 64) void k_nehvi_means(NehviMeansArgs a) {
 // same sample, so every box read is an LDS broadcast). The constrained form
 // replaces an infeasible sample's first objective by -inf, which zeroes every
 // box term.
+constexpr int kET = 512;   // threads per workgroup of the HVI kernel
+
 template <bool CONS>
-__global__ __launch_bounds__(256) void k_nehvi_ehvi(NehviEhviArgs a) {
+__global__ __launch_bounds__(kET) void k_nehvi_ehvi(NehviEhviArgs a) {
   extern __shared__ float esm[];
   float* zs = esm;                                          // [S][2]
   float* bx = esm + 2 * a.S;                                // [total][4]
   int* off = reinterpret_cast<int*>(bx + 4 * a.total);      // [S + 1]
-  for (int i = threadIdx.x; i < 2 * a.S; i += 256) zs[i] = a.Z[i];
-  for (int i = threadIdx.x; i < 4 * a.total; i += 256) bx[i] = a.boxes[i];
-  for (int i = threadIdx.x; i <= a.S; i += 256) off[i] = a.off[i];
+  for (int i = threadIdx.x; i < 2 * a.S; i += kET) zs[i] = a.Z[i];
+  for (int i = threadIdx.x; i < 4 * a.total; i += kET) bx[i] = a.boxes[i];
+  for (int i = threadIdx.x; i <= a.S; i += kET) off[i] = a.off[i];
   __syncthreads();
-  const int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t c = (int64_t)blockIdx.x * kET + threadIdx.x;
   const bool valid = c < a.npts;
   const int64_t cc = valid ? c : a.npts - 1;
   const float mu0 = a.mu[2 * cc], mu1 = a.mu[2 * cc + 1];
@@ -385,7 +416,7 @@ __global__ __launch_bounds__(256) void k_nehvi_ehvi(NehviEhviArgs a) {
   const float* d0 = a.D + cc;
   const float* d1 = a.D + (int64_t)a.S * a.ldd + cc;
   float acc = 0.f;
-  constexpr int U = 8;
+  constexpr int U = 16;   // draws whose means are in flight together
   for (int s0 = 0; s0 < a.S; s0 += U) {
     float v0[U], v1[U];
 #pragma unroll
@@ -441,8 +472,8 @@ hipError_t launch_sample_fronts(const NehviFrontArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
-hipError_t launch_absmax(const double* G, int64_t count, int m, double* out, hipStream_t st) {
-  hipLaunchKernelGGL(k_absmax, dim3(m), dim3(256), 0, st, G, count, out);
+hipError_t launch_absmax(const double* G, int64_t count, int m, double* part, hipStream_t st) {
+  hipLaunchKernelGGL(k_absmax, dim3(kAbsmaxParts, m), dim3(256), 0, st, G, count, part);
   return hipGetLastError();
 }
 
@@ -490,9 +521,9 @@ hipError_t launch_nehvi_ehvi(const NehviEhviArgs& a, hipStream_t st) {
     attr = true;
   }
   const size_t lds = nehvi_ehvi_lds_bytes(a.S, a.total);
-  const unsigned grid = static_cast<unsigned>((a.npts + 255) / 256);
-  if (a.cons) hipLaunchKernelGGL(k_nehvi_ehvi<true>, dim3(grid), dim3(256), lds, st, a);
-  else hipLaunchKernelGGL(k_nehvi_ehvi<false>, dim3(grid), dim3(256), lds, st, a);
+  const unsigned grid = static_cast<unsigned>((a.npts + kET - 1) / kET);
+  if (a.cons) hipLaunchKernelGGL(k_nehvi_ehvi<true>, dim3(grid), dim3(kET), lds, st, a);
+  else hipLaunchKernelGGL(k_nehvi_ehvi<false>, dim3(grid), dim3(kET), lds, st, a);
   return hipGetLastError();
 }
 
