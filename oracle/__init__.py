@@ -23,9 +23,9 @@ workflow, the constrained qNEHVI paragraph, and the implementation section
                 base samples, optionally weighted by the feasibility
                 indicator of the constrained form, and the argmax over
                 candidates.
-* ``noisy``   — the noisy form (qNEHVI, q = 1): joint posterior samples of
+* ``noisy``   — the noisy form (qNEHVI): joint posterior samples of
                 the latent objectives at the observed points and the
-                candidate, a Pareto front per sample of the in-sample values,
+                candidate (or q-batch), a Pareto front per sample of the in-sample values,
                 and the candidate's HVI against it, optionally constrained.
 
 All arithmetic is fp64 on fp32-rounded inputs. Readings of points the paper
@@ -36,8 +36,8 @@ from .gp import (GPModel, Composite, matern52, matern32, composite_cov, pref_wei
                  chol_psd, NotPositiveDefinite)
 from .pareto import nondominated, pareto_front, boxes_2d, boxes_3d, box_decomposition
 from .acq import hvi, qhvi, feasible, ehvi_q1, qehvi, score, argmax
-from .noisy import (insample_posterior, insample_samples, candidate_samples, sample_boxes,
-                    nehvi)
+from .noisy import (insample_posterior, insample_samples, candidate_samples, batch_samples,
+                    sample_boxes, nehvi)
 
 __all__ = [
     "GPModel", "Composite", "matern52", "matern32", "composite_cov", "pref_weight",
@@ -45,5 +45,5 @@ __all__ = [
     "NotPositiveDefinite", "nondominated", "pareto_front", "boxes_2d",
     "boxes_3d", "box_decomposition", "hvi", "qhvi", "feasible", "ehvi_q1", "qehvi",
     "score", "argmax", "insample_posterior", "insample_samples", "candidate_samples",
-    "sample_boxes", "nehvi",
+    "batch_samples", "sample_boxes", "nehvi",
 ]

@@ -1,4 +1,4 @@
-"""Noisy expected hypervolume improvement (qNEHVI) of single points, fp64.
+"""Noisy expected hypervolume improvement (qNEHVI) of candidates and q-batches, fp64.
 
 Test infrastructure only: the GPU library never imports this module.
 
@@ -32,16 +32,22 @@ Readings (the paper names the acquisition but does not spell it out):
   thresholds, only in-sample vectors meeting all of them take part.
 * HVI of f*^s against the disjoint boxes of that front; the constrained
   form multiplies it by the feasibility indicator of f*^s.
-* qNEHVI = plain mean over the S samples. q = 1 (one candidate per batch).
+* qNEHVI = plain mean over the S samples.
+* q-batches (the paper's q): the members x*_1..x*_q are drawn jointly with
+  f_X the same way, with B = L_XX^{-1} Sigma_XB [n, q] and the conditional
+  batch covariance Sigma_BB - B^T B factored by the PSD Cholesky rule of
+  ``gp.chol_psd``; the batch improvement of a draw is the joint HVI of its
+  members (inclusion-exclusion, ``acq.qhvi``) against that draw's boxes, a
+  member counting only where it is feasible.
 """
 from __future__ import annotations
 
 import numpy as np
 from scipy.linalg import cho_solve, solve_triangular
 
-from .gp import GPModel
+from .gp import GPModel, chol_psd
 from .pareto import pareto_front, box_decomposition
-from .acq import hvi, feasible
+from .acq import hvi, qhvi, feasible
 
 
 def insample_posterior(model: GPModel):
@@ -102,6 +108,46 @@ def candidate_samples(model: GPModel, cand: np.ndarray, ZX: np.ndarray, Zs: np.n
     return out
 
 
+def batch_samples(model: GPModel, cand: np.ndarray, ZX: np.ndarray, Zs: np.ndarray,
+                  Ls=None, Kxx=None):
+    """Joint-posterior samples of q-batches: f* [M, S, q, m].
+
+    cand [M, q, d]; ZX [S, n, m]; Zs [S, q, m]. The batch block of the joint
+    factor is the PSD Cholesky factor of Sigma_BB - B^T B (B = L_XX^{-1}
+    Sigma_XB), applied to z*_s."""
+    cand = np.asarray(cand, dtype=np.float64)
+    M, q, d = cand.shape
+    ZX = np.asarray(ZX, dtype=np.float64)
+    S = ZX.shape[0]
+    Zs = np.asarray(Zs, dtype=np.float64).reshape(S, q, model.m)
+    if Ls is None:
+        _, Ls = insample_samples(model, ZX)
+    X = model.X
+    P = cand.reshape(M * q, d)
+    out = np.empty((M, S, q, model.m))
+    for k in range(model.m):
+        Ks = model.cov(k, P, X)                                 # [Mq, n]
+        Kk = model.cov(k, X, X) if Kxx is None else Kxx[k]
+        mu_s = (Ks @ model.alpha[k]).reshape(M, q)
+        KinvKs = cho_solve((model.L[k], True), Ks.T)            # [n, Mq]
+        Sx = Ks.T - Kk @ KinvKs                                 # [n, Mq] = Sigma_X*
+        Bm = solve_triangular(Ls[k], Sx, lower=True)            # [n, Mq]
+        Bb = Bm.T.reshape(M, q, -1)                             # [M, q, n]
+        prior = np.empty((M, q, q))
+        for a in range(q):
+            for c in range(q):
+                prior[:, a, c] = model.pair_cov(k, cand[:, a, :], cand[:, c, :])
+        Kb = Ks.reshape(M, q, -1)
+        KinvKb = KinvKs.T.reshape(M, q, -1)
+        post = prior - np.einsum("mai,mbi->mab", Kb, KinvKb)    # Sigma_BB
+        cond = post - np.einsum("mai,mbi->mab", Bb, Bb)
+        C = chol_psd(cond, model.s[k])                          # [M, q, q]
+        off = np.einsum("mai,si->msa", Bb, ZX[:, :, k])         # [M, S, q]
+        out[:, :, :, k] = (mu_s[:, None, :] + off
+                           + np.einsum("mab,sb->msa", C, Zs[:, :, k]))
+    return out
+
+
 def sample_boxes(F: np.ndarray, ref: np.ndarray, lower=None):
     """Boxes of each sample's in-sample front: list of (lo, hi) per sample.
 
@@ -119,31 +165,43 @@ def sample_boxes(F: np.ndarray, ref: np.ndarray, lower=None):
 
 def nehvi(model: GPModel, cand: np.ndarray, ref: np.ndarray, ZX: np.ndarray,
           Zs: np.ndarray, lower=None, chunk: int = 1024):
-    """qNEHVI (q = 1) of M candidates [M, d] (or [M, 1, d]).
+    """qNEHVI of M candidates [M, d] (q = 1) or q-batches [M, q, d].
 
-    ZX [S, n, m] in-sample base samples; Zs [S, m] (or [S, 1, m]) candidate
-    base samples; lower [m] optional feasibility thresholds.
+    ZX [S, n, m] in-sample base samples; Zs [S, m] (q = 1) or [S, q, m]
+    candidate base samples; lower [m] optional feasibility thresholds.
     Returns a dict with ``ehvi`` [M], the in-sample samples ``F`` [S, n, m]
     and the per-sample ``boxes``.
     """
     cand = np.asarray(cand, dtype=np.float64)
-    cand = cand.reshape(cand.shape[0], -1)
     ZX = np.asarray(ZX, dtype=np.float64)
     S = ZX.shape[0]
-    Zs = np.asarray(Zs, dtype=np.float64).reshape(S, model.m)
+    batched = cand.ndim == 3 and cand.shape[1] > 1
+    if not batched:
+        cand = cand.reshape(cand.shape[0], -1)
+        Zs = np.asarray(Zs, dtype=np.float64).reshape(S, model.m)
     F, Ls = insample_samples(model, ZX)
     Kxx = [model.cov(k, model.X, model.X) for k in range(model.m)]
     boxes = sample_boxes(F, ref, lower)
     M = cand.shape[0]
     out = np.empty(M)
+    if batched:
+        chunk = max(1, chunk // cand.shape[1])
     for i0 in range(0, M, chunk):
         i1 = min(M, i0 + chunk)
-        ys = candidate_samples(model, cand[i0:i1], ZX, Zs, Ls, Kxx)    # [c, S, m]
-        h = np.empty((i1 - i0, S))
-        for s in range(S):
-            lo, hi = boxes[s]
-            h[:, s] = hvi(ys[:, s, :], lo, hi)
-        if lower is not None:
-            h = h * feasible(ys, lower)
+        if not batched:
+            ys = candidate_samples(model, cand[i0:i1], ZX, Zs, Ls, Kxx)    # [c, S, m]
+            h = np.empty((i1 - i0, S))
+            for s in range(S):
+                lo, hi = boxes[s]
+                h[:, s] = hvi(ys[:, s, :], lo, hi)
+            if lower is not None:
+                h = h * feasible(ys, lower)
+        else:
+            ys = batch_samples(model, cand[i0:i1], ZX, Zs, Ls, Kxx)        # [c, S, q, m]
+            feas = None if lower is None else feasible(ys, lower)           # [c, S, q]
+            h = np.empty((i1 - i0, S))
+            for s in range(S):
+                lo, hi = boxes[s]
+                h[:, s] = qhvi(ys[:, s], lo, hi, None if feas is None else feas[:, s])
         out[i0:i1] = np.mean(h, axis=1)
     return dict(ehvi=out, F=F, boxes=boxes)

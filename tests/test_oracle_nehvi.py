@@ -167,3 +167,77 @@ def test_planted_transposed_factor_in_the_conditional_is_caught(monkeypatch):
     want = W.T @ F[0, :, k] + tau * Zs[0, k]
     np.testing.assert_allclose(good[:, 0, k], want, rtol=1e-7, atol=1e-9)
     assert np.max(np.abs(bad[:, 0, k] - want)) > 1e-4
+
+
+def _problem3(n=14, d=3, M=4, q=2, S=6, eta=2e-2, seed=21):
+    r = np.random.default_rng(seed)
+    X = r.random((n, d))
+    Y = r.standard_normal((n, 3))
+    ls = r.uniform(0.3, 0.8, size=(3, d))
+    s = r.uniform(0.5, 1.5, size=3)
+    cand = r.random((M, q, d))
+    ZX = r.standard_normal((S, n, 3))
+    Zs = r.standard_normal((S, q, 3))
+    return X, Y, ls, s, np.full(3, eta), cand, ZX, Zs
+
+
+def test_batch_samples_equal_cholesky_of_the_joint_posterior():
+    X, Y, ls, s, eta, cand, ZX, Zs = _problem3()
+    model = O.fit(X, Y, ls, s, eta)
+    F, Ls = O.insample_samples(model, ZX)
+    ys = O.batch_samples(model, cand, ZX, Zs, Ls)          # [M, S, q, m]
+    n, q = X.shape[0], cand.shape[1]
+    for k in range(3):
+        K = _kernel(X, X, ls[k], s[k]) + eta[k] * np.eye(n)
+        for c in range(cand.shape[0]):
+            U = np.vstack([X, cand[c]])
+            KU = _kernel(U, U, ls[k], s[k])
+            KUX = _kernel(U, X, ls[k], s[k])
+            Lj = np.linalg.cholesky(KU - KUX @ np.linalg.solve(K, KUX.T))
+            mean = KUX @ np.linalg.solve(K, Y[:, k])
+            for smp in range(ZX.shape[0]):
+                f = mean + Lj @ np.concatenate([ZX[smp, :, k], Zs[smp, :, k]])
+                np.testing.assert_allclose(F[smp, :, k], f[:n], rtol=1e-9, atol=1e-11)
+                np.testing.assert_allclose(ys[c, smp, :, k], f[n:], rtol=1e-8, atol=1e-10)
+
+
+@pytest.mark.parametrize("lower", [None, "q"])
+def test_batch_hvi_equals_exact_hypervolume_difference(lower):
+    X, Y, ls, s, eta, cand, ZX, Zs = _problem3(n=20, M=5, S=5, eta=5e-2, seed=23)
+    model = O.fit(X, Y, ls, s, eta)
+    ref = Y.min(axis=0) - 0.1
+    low = None if lower is None else np.quantile(Y, 0.3, axis=0)
+    got = O.nehvi(model, cand, ref, ZX, Zs, lower=low)["ehvi"]
+    F, Ls = O.insample_samples(model, ZX)
+    ys = O.batch_samples(model, cand, ZX, Zs, Ls)
+    want = np.zeros(cand.shape[0])
+    for smp in range(ZX.shape[0]):
+        Fs = F[smp]
+        if low is not None:
+            Fs = Fs[np.all(Fs >= low, axis=1)]
+        front = Fs[front_bruteforce(Fs, ref)]
+        base = hv_exact(front, ref)
+        for c in range(cand.shape[0]):
+            mem = ys[c, smp]
+            if low is not None:
+                mem = mem[np.all(mem >= low, axis=1)]
+            want[c] += hv_exact(np.vstack([front, mem]), ref) - base
+    want /= ZX.shape[0]
+    np.testing.assert_allclose(got, want, rtol=1e-9, atol=1e-12)
+
+
+def test_batch_small_noise_limit_is_the_plain_qehvi():
+    r = np.random.default_rng(31)
+    n, d, M, S, q = 25, 3, 12, 48, 2
+    X = r.random((n, d))
+    Y = r.standard_normal((n, 3))
+    ls = np.full((3, d), 0.45)
+    s = np.ones(3)
+    cand = r.random((M, q, d))
+    ZX = r.standard_normal((S, n, 3))
+    Zs = r.standard_normal((S, q, 3))
+    ref = Y.min(axis=0) - 0.1
+    model = O.fit(X, Y, ls, s, np.full(3, 1e-9))
+    got = O.nehvi(model, cand, ref, ZX, Zs)["ehvi"]
+    plain = O.score(model, cand, ref, Zs)["ehvi"]
+    np.testing.assert_allclose(got, plain, rtol=2e-3, atol=1e-6)
