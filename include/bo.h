@@ -231,55 +231,56 @@ bo_status bo_score_constrained(bo_model model, const float* cand, int64_t M, int
                                float* mu, float* sigma, void* stream);
 
 /*
- * bo_nehvi_prepare / bo_score_nehvi — the noisy acquisition (qNEHVI, q = 1,
- * two objectives, Matern-5/2 models).
+ * bo_nehvi_prepare / bo_score_nehvi — the noisy acquisition (qNEHVI;
+ * candidates or q-batches, two or three objectives, Matern-5/2 models).
  *
  * Paper: workflow step (ii) and the "Constrained qNEHVI" paragraph (after
  * Daulton et al. 2021). The observations are noisy, so the latent objective
- * values at the observed points X are sampled too: sample s draws the latent
- * f jointly at X and at the candidate x from the GP posterior, by the lower
+ * values at the observed points X are sampled too: draw s takes the latent f
+ * jointly at X and at the batch B from the GP posterior, by the lower
  * Cholesky factor of the joint covariance applied to (z_X^s, z*^s):
  *   f_X^s = mu_X + L_XX z_X^s            (Sigma_XX = L_XX L_XX^T),
- *   f*^s  = E[f* | f_X^s] + tau z*^s,
- *   E[f* | f_X] = k*^T K_XX^{-1} f_X,  tau^2 = s - k*^T K_XX^{-1} k*
+ *   f_B^s = E[f_B | f_X^s] + C z*^s,
+ *   E[f_B | f_X] = K_BX K_XX^{-1} f_X,  C C^T = k(B,B) - K_BX K_XX^{-1} K_XB
  *   (K_XX the noise-free Gram matrix; the noisy y adds nothing once f_X is
- *   known), and
- *   ehvi[b] = 1/S sum_s HVI_s(f*^s) [* feasibility indicator of f*^s],
- * where HVI_s is the hypervolume improvement over the Pareto front of the
- * in-sample values f_X^s (maximise, strictly above ref_point; with
- * feasibility thresholds only the in-sample vectors meeting all of them).
+ *   known; C by the PSD rule of bo_score's batch factor), and
+ *   ehvi[b] = 1/S sum_s HVI_s(f_B^s),
+ * where HVI_s is the joint hypervolume improvement of the members over the
+ * Pareto front of the in-sample values f_X^s (maximise, strictly above
+ * ref_point). With feasibility thresholds only the in-sample vectors meeting
+ * all of them form the fronts, and a member counts only on the draws where it
+ * is feasible (as in bo_score_constrained).
  *
  * bo_nehvi_prepare(model, base_samples_X, S, ref_point, feas_lower, stream):
- *   base_samples_X device [S][n][2] iid N(0,1), row-major (sample, observed
+ *   base_samples_X device [S][n][m] iid N(0,1), row-major (draw, observed
  *                  point, objective); 1 <= S <= 512
- *   ref_point      host [2];  feas_lower host [2] or NULL (as in
- *                  bo_score_constrained)
- *   Builds, in fp64 on the device, the in-sample posterior and its factor,
- *   the S in-sample draws, each sample's front and box decomposition, the
- *   factor of K_XX and G = K_XX^{-1} L_XX Z_X; keeps them in the model
- *   (replacing an earlier preparation). Synchronous (reads the per-sample
- *   front sizes back).
- *   Errors: INVALID_ARGUMENT (m != 2, composite-kernel model, bad S or
- *   pointer), CAPACITY (S > 512, per-sample boxes beyond LDS),
- *   NOT_POSITIVE_DEFINITE (K, the in-sample covariance or K_XX),
- *   NONFINITE_INPUT, OUT_OF_MEMORY, DEVICE.
+ *   ref_point      host [m];  feas_lower host [m] or NULL
+ *   Builds, in fp64, the in-sample posterior and its factor, the S in-sample
+ *   draws, each draw's front and box decomposition (on the device for two
+ *   objectives, on the host's threads for three), the factor of K_XX and
+ *   G = K_XX^{-1} L_XX Z_X; keeps them in the model (replacing an earlier
+ *   preparation). Synchronous.
+ *   Errors: INVALID_ARGUMENT (m not 2 or 3, composite-kernel model, bad S or
+ *   pointer), CAPACITY (S > 512, too many boxes), NOT_POSITIVE_DEFINITE (K,
+ *   the in-sample covariance or K_XX), NONFINITE_INPUT, OUT_OF_MEMORY,
+ *   DEVICE.
  *
- * bo_score_nehvi(model, cand, M, base_samples, S, ehvi, stream):
- *   cand device [M][d]; base_samples device [S][2] (z*, shared by all
- *   candidates); S must equal the prepared S; ehvi device [M] out.
- *   Asynchronous; candidates are processed in chunks of 262144, whose
- *   per-sample conditional means (2 x S x chunk floats) live in a model-owned
- *   workspace that grows on first use.
- *   Errors: INVALID_ARGUMENT (not prepared, S mismatch, pointers), CAPACITY,
- *   OUT_OF_MEMORY, DEVICE.
+ * bo_score_nehvi(model, cand, M, q, base_samples, S, ehvi, stream):
+ *   cand device [M][q][d] (q in {1, 2, 4}); base_samples device [S][q][m]
+ *   (z*, shared by all batches); S must equal the prepared S; ehvi device [M]
+ *   out. Asynchronous; batches are processed in chunks of 262144 points,
+ *   whose per-draw conditional means (m x S x chunk floats) live in a
+ *   model-owned workspace that grows on first use.
+ *   Errors: INVALID_ARGUMENT (not prepared, S mismatch, bad q, pointers),
+ *   CAPACITY, OUT_OF_MEMORY, DEVICE.
  *
  * bo_nehvi_front(model, sample, idx_host, cap, count): the front of one
- *   sample (indices into the observations, sorted by objective 0 ascending),
+ *   draw (indices into the observations, sorted by objective 0 ascending),
  *   min(cap, size) entries to host memory, *count = its size. Synchronous.
  */
 bo_status bo_nehvi_prepare(bo_model model, const float* base_samples_X, int32_t S,
                            const float* ref_point, const float* feas_lower, void* stream);
-bo_status bo_score_nehvi(bo_model model, const float* cand, int64_t M,
+bo_status bo_score_nehvi(bo_model model, const float* cand, int64_t M, int32_t q,
                          const float* base_samples, int32_t S, float* ehvi, void* stream);
 bo_status bo_nehvi_front(bo_model model, int32_t sample, int32_t* idx_host, int32_t cap,
                          int32_t* count);

@@ -71,7 +71,7 @@ def lib() -> ctypes.CDLL:
     L.bo_score_constrained.restype = ctypes.c_int
     L.bo_nehvi_prepare.argtypes = [vp, vp, i32, fp, fp, vp]
     L.bo_nehvi_prepare.restype = ctypes.c_int
-    L.bo_score_nehvi.argtypes = [vp, vp, i64, vp, i32, vp, vp]
+    L.bo_score_nehvi.argtypes = [vp, vp, i64, i32, vp, i32, vp, vp]
     L.bo_score_nehvi.restype = ctypes.c_int
     L.bo_nehvi_front.argtypes = [vp, i32, vp, i32, ctypes.POINTER(i32)]
     L.bo_nehvi_front.restype = ctypes.c_int
@@ -267,8 +267,8 @@ def score(model: Model, cand, ref, Z, ehvi=None, mu=None, sigma=None, stream=Non
 
 
 def nehvi_prepare(model: Model, ZX, ref, lower=None, stream=None):
-    """bo_nehvi_prepare: ZX [S, n, 2] fp32 GPU tensor (in-sample base
-    samples); ref host [2]; lower host [2] or None. Synchronous."""
+    """bo_nehvi_prepare: ZX [S, n, m] fp32 GPU tensor (in-sample base
+    samples); ref host [m]; lower host [m] or None. Synchronous."""
     import torch
     S = ZX.shape[0]
     r = _host_f32(ref, (model.m,), "ref")
@@ -281,14 +281,15 @@ def nehvi_prepare(model: Model, ZX, ref, lower=None, stream=None):
 
 
 def score_nehvi(model: Model, cand, Z, ehvi=None, stream=None):
-    """bo_score_nehvi: cand [M, d] (or [M, 1, d]) and Z [S, 2] (or [S, 1, 2])
-    fp32 GPU tensors. Returns the ehvi tensor [M] (allocated if not given)."""
+    """bo_score_nehvi: cand [M, d] or [M, q, d] and Z [S, m] or [S, q, m] fp32
+    GPU tensors. Returns the ehvi tensor [M] (allocated if not given)."""
     import torch
     M = cand.shape[0]
+    q = cand.shape[1] if cand.dim() == 3 else 1
     S = Z.shape[0]
     if ehvi is None:
         ehvi = torch.empty(M, dtype=torch.float32, device=cand.device)
-    st = lib().bo_score_nehvi(model.handle, _dev(cand, "cand", torch.float32), M,
+    st = lib().bo_score_nehvi(model.handle, _dev(cand, "cand", torch.float32), M, q,
                               _dev(Z, "Z", torch.float32), S, _dev(ehvi, "ehvi", torch.float32),
                               _stream(stream))
     _check(st, "bo_score_nehvi")

@@ -16,6 +16,7 @@
 #include <cstring>
 #include <mutex>
 #include <string>
+#include <thread>
 #include <vector>
 
 #include "bo_internal.h"
@@ -81,6 +82,12 @@ bo_status after_launch(hipError_t e, hipStream_t st, const char* what) {
     if (e != hipSuccess) return hip_fail(e, what);
   }
   return BO_OK;
+}
+
+bool all_finite_d(const std::vector<double>& v) {
+  for (double x : v)
+    if (!std::isfinite(x)) return false;
+  return true;
 }
 
 bool all_finite(const float* v, size_t n) {
@@ -202,6 +209,7 @@ void release_noisy(Model* M) {
   z.ws_floats = 0;
   z.S = z.Sp = z.n32 = z.total = 0;
   z.counts.clear();
+  z.fsize.clear();
 }
 
 void release_buffers(Model* M) {
@@ -301,7 +309,7 @@ bo_status bo_box_decomposition(const float* F, int32_t P, int32_t m, const float
   if (m == 2) {
     // the staircase needs the 2-D non-dominated points sorted by objective 0
     std::vector<int32_t> nd;
-    host_front(F, P, 2, nullptr, nd);
+    host_front<float>(F, P, 2, nullptr, nd);
     for (int32_t i : nd) { Fs.push_back(F[2 * i]); Fs.push_back(F[2 * i + 1]); }
     Fp = Fs.data();
     P = static_cast<int32_t>(nd.size());
@@ -516,7 +524,7 @@ bo_status fit_impl(const char* who, const float* X, const float* Y, int64_t n, i
   if (!all_finite(M->Yh.data(), M->Yh.size()))
     return bail(fail(BO_ERR_NONFINITE_INPUT, W + ": Y not finite"));
   if (flag) return bail(fail(BO_ERR_NOT_POSITIVE_DEFINITE, W + ": non-positive Cholesky pivot"));
-  host_front(M->Yh.data(), n, m, nullptr, M->nd);
+  host_front<float>(M->Yh.data(), n, m, nullptr, M->nd);
 
   M->last_stream = st;
   *out = h;
@@ -858,39 +866,93 @@ struct NoisyScratch {
   hipStream_t st = nullptr;
   double *A = nullptr, *W = nullptr, *A0 = nullptr, *W0 = nullptr;
   double *hyp = nullptr, *tmp = nullptr, *alpha64 = nullptr, *gmax = nullptr;
-  double *Zk = nullptr, *T1 = nullptr, *G = nullptr;
+  double *Zk = nullptr, *T1 = nullptr, *G = nullptr, *Fd = nullptr;
   float *Y = nullptr, *alpha = nullptr, *btmp = nullptr;
   int *flag = nullptr, *counts = nullptr, *off = nullptr;
   ~NoisyScratch() {
     pfree(A, st); pfree(W, st); pfree(A0, st); pfree(W0, st); pfree(hyp, st); pfree(tmp, st);
-    pfree(alpha64, st); pfree(gmax, st); pfree(Zk, st); pfree(T1, st); pfree(G, st);
+    pfree(alpha64, st); pfree(gmax, st); pfree(Zk, st); pfree(T1, st); pfree(G, st); pfree(Fd, st);
     pfree(Y, st); pfree(alpha, st); pfree(btmp, st); pfree(flag, st); pfree(counts, st);
     pfree(off, st);
   }
 };
 
+// Per-draw fronts and boxes of three-objective in-sample draws on the host
+// (fp64, the same rules as the device kernel for two objectives): rows failing
+// a threshold are left out, the front keeps rows strictly above ref, boxes
+// are (lo, width) in fp32. Draws are split over host threads.
+void host_draw_boxes(const std::vector<double>& F, int S, int64_t n, int m, const float* ref,
+                     const float* lower, std::vector<int>& counts,
+                     std::vector<std::vector<float>>& boxes,
+                     std::vector<std::vector<int32_t>>& fronts) {
+  counts.assign(S, 0);
+  boxes.assign(S, {});
+  fronts.assign(S, {});
+  const double r[3] = {ref[0], ref[1], m > 2 ? static_cast<double>(ref[2]) : 0.0};
+  auto work = [&](int s0, int s1) {
+    std::vector<double> rows;
+    std::vector<int32_t> map, front;
+    std::vector<double> Ff, lo, hi;
+    for (int s = s0; s < s1; ++s) {
+      const double* Fs = F.data() + (size_t)s * n * m;
+      rows.clear();
+      map.clear();
+      for (int64_t i = 0; i < n; ++i) {
+        bool ok = true;
+        if (lower)
+          for (int k = 0; k < m; ++k) ok = ok && Fs[i * m + k] >= static_cast<double>(lower[k]);
+        if (!ok) continue;
+        rows.insert(rows.end(), Fs + i * m, Fs + (i + 1) * m);
+        map.push_back(static_cast<int32_t>(i));
+      }
+      host_front<double>(rows.data(), static_cast<int64_t>(map.size()), m, r, front);
+      Ff.clear();
+      for (int32_t j : front) {
+        Ff.insert(Ff.end(), rows.begin() + (size_t)j * m, rows.begin() + (size_t)(j + 1) * m);
+        fronts[s].push_back(map[j]);
+      }
+      host_boxes<double>(Ff.data(), static_cast<int>(front.size()), m, r, lo, hi);
+      const int nb = static_cast<int>(lo.size() / m);
+      std::vector<float>& out = boxes[s];
+      out.resize((size_t)nb * 2 * m);
+      for (int c = 0; c < nb; ++c)
+        for (int k = 0; k < m; ++k) {
+          const float l = static_cast<float>(lo[(size_t)c * m + k]);
+          out[(size_t)c * 2 * m + k] = l;
+          out[(size_t)c * 2 * m + m + k] = static_cast<float>(hi[(size_t)c * m + k]) - l;
+        }
+      counts[s] = nb;
+    }
+  };
+  const int nt = std::max(1, std::min<int>(16, static_cast<int>(std::thread::hardware_concurrency())));
+  const int per = (S + nt - 1) / nt;
+  std::vector<std::thread> th;
+  for (int t = 0; t < nt && t * per < S; ++t) th.emplace_back(work, t * per, std::min(S, (t + 1) * per));
+  for (auto& x : th) x.join();
+}
+
 bo_status nehvi_prepare_impl(bo_model model, const float* ZX, int32_t S, const float* ref,
                              const float* lower, void* stream) {
-  const char* W_ = "bo_nehvi_prepare";
-  if (!model) return fail(BO_ERR_INVALID_ARGUMENT, std::string(W_) + ": model is NULL");
+  const std::string W_("bo_nehvi_prepare");
+  if (!model) return fail(BO_ERR_INVALID_ARGUMENT, W_ + ": model is NULL");
   Model& M = model->m;
-  if (M.m != 2) return fail(BO_ERR_INVALID_ARGUMENT, std::string(W_) + ": two objectives only");
-  if (M.dr > 0)
-    return fail(BO_ERR_INVALID_ARGUMENT, std::string(W_) + ": Matern-5/2 models only");
-  if (S < 1) return fail(BO_ERR_INVALID_ARGUMENT, std::string(W_) + ": S < 1");
-  if (S > kNehviMaxS) return fail(BO_ERR_CAPACITY, std::string(W_) + ": S beyond 512");
-  if (!ref) return fail(BO_ERR_INVALID_ARGUMENT, std::string(W_) + ": ref_point is NULL");
-  if (!all_finite(ref, 2)) return fail(BO_ERR_NONFINITE_INPUT, std::string(W_) + ": ref_point not finite");
-  if (lower && (std::isnan(lower[0]) || std::isnan(lower[1])))
-    return fail(BO_ERR_NONFINITE_INPUT, std::string(W_) + ": feasibility threshold is NaN");
+  const int m = M.m, d = M.d;
+  if (m != 2 && m != 3) return fail(BO_ERR_INVALID_ARGUMENT, W_ + ": two or three objectives");
+  if (M.dr > 0) return fail(BO_ERR_INVALID_ARGUMENT, W_ + ": Matern-5/2 models only");
+  if (S < 1) return fail(BO_ERR_INVALID_ARGUMENT, W_ + ": S < 1");
+  if (S > kNehviMaxS) return fail(BO_ERR_CAPACITY, W_ + ": S beyond 512");
+  if (!ref) return fail(BO_ERR_INVALID_ARGUMENT, W_ + ": ref_point is NULL");
+  if (!all_finite(ref, m)) return fail(BO_ERR_NONFINITE_INPUT, W_ + ": ref_point not finite");
+  if (lower)
+    for (int k = 0; k < m; ++k)
+      if (std::isnan(lower[k])) return fail(BO_ERR_NONFINITE_INPUT, W_ + ": feasibility threshold is NaN");
   DeviceGuard g(M.device);
-  if (!g.ok) return fail(BO_ERR_DEVICE, std::string(W_) + ": cannot select the model's device");
+  if (!g.ok) return fail(BO_ERR_DEVICE, W_ + ": cannot select the model's device");
   const int64_t n = M.n;
-  const int m = 2, d = M.d;
   bo_status s;
   if ((s = check_dev(ZX, sizeof(float) * (size_t)S * n * m, "base_samples_X")) != BO_OK) return s;
-  if (nehvi_front_lds_bytes(n) > 64 * 1024)
-    return fail(BO_ERR_CAPACITY, std::string(W_) + ": n beyond the front kernel's LDS");
+  if (m == 2 && nehvi_front_lds_bytes(n) > 64 * 1024)
+    return fail(BO_ERR_CAPACITY, W_ + ": n beyond the front kernel's LDS");
   hipStream_t st = static_cast<hipStream_t>(stream);
   const int nf = static_cast<int>((n + kFitBlk - 1) / kFitBlk) * kFitBlk;
   const int Sp = nehvi_padded_samples(S);
@@ -918,10 +980,14 @@ bo_status nehvi_prepare_impl(bo_model model, const float* ZX, int32_t S, const f
   if ((s = palloc(&sc.G, vec, st, "noisy: G")) != BO_OK) return s;
   if ((s = palloc(&sc.Y, (size_t)n * m, st, "noisy: Y")) != BO_OK) return s;
   if ((s = palloc(&sc.alpha, (size_t)m * M.n_pad, st, "noisy: alpha (fp32)")) != BO_OK) return s;
-  if ((s = palloc(&sc.btmp, (size_t)S * (n + 1) * 4, st, "noisy: boxes")) != BO_OK) return s;
   if ((s = palloc(&sc.flag, 4, st, "noisy: flags")) != BO_OK) return s;
   if ((s = palloc(&sc.counts, (size_t)S, st, "noisy: counts")) != BO_OK) return s;
   if ((s = palloc(&sc.off, (size_t)S + 1, st, "noisy: offsets")) != BO_OK) return s;
+  if (m == 2) {
+    if ((s = palloc(&sc.btmp, (size_t)S * (n + 1) * 4, st, "noisy: boxes")) != BO_OK) return s;
+  } else {
+    if ((s = palloc(&sc.Fd, (size_t)S * n * m, st, "noisy: in-sample draws")) != BO_OK) return s;
+  }
   if ((s = palloc(&z.Lp0, (size_t)m * M.lp_per_obj, st, "noisy: packed factor")) != BO_OK) return s;
   if ((s = palloc(&z.front, (size_t)S * n, st, "noisy: fronts")) != BO_OK) return s;
 
@@ -931,9 +997,9 @@ bo_status nehvi_prepare_impl(bo_model model, const float* ZX, int32_t S, const f
     hyp[(size_t)m * d + k] = M.os[k];
     hyp[(size_t)m * d + m + k] = M.noise[k];
   }
-  // pinned staging: [hyp][flags 16 B][Y][counts][gmax][off]
+  // pinned staging: [hyp][flags 16 B][Y][counts][maxima][offsets]
   DeviceState* DS = device_state(M.device);
-  if (!DS) return fail(BO_ERR_DEVICE, std::string(W_) + ": device index out of range");
+  if (!DS) return fail(BO_ERR_DEVICE, W_ + ": device index out of range");
   std::lock_guard<std::mutex> stage_lock(DS->fit_mu);
   const size_t off_flag = (sizeof(double) * nhyp + 15) / 16 * 16;
   const size_t off_y = off_flag + 16;
@@ -980,7 +1046,7 @@ bo_status nehvi_prepare_impl(bo_model model, const float* ZX, int32_t S, const f
   // in-sample posterior covariance eta (I - eta K^{-1}) and its factor
   if ((s = step(launch_sigma_xx(sc.A, n, nf, m, gp.noise, st), "in-sample covariance")) != BO_OK) return sync_fail(s);
   if ((s = step(launch_cholesky(sc.A, sc.W, nf, m, sc.flag + 1, st), "cholesky")) != BO_OK) return sync_fail(s);
-  // noise-free K_XX: factor, inverse, packed for the conditional variance
+  // noise-free K_XX: factor, inverse, packed for the conditional (co)variance
   if ((s = step(launch_gram(M.Xd, n, d, m, nf, g0, sc.A0, st), "gram")) != BO_OK) return sync_fail(s);
   if ((s = step(launch_cholesky(sc.A0, sc.W0, nf, m, sc.flag + 2, st), "cholesky")) != BO_OK) return sync_fail(s);
   if ((s = step(launch_pack_factor(sc.W0, n, m, nf, M.nb, z.Lp0, st), "pack")) != BO_OK) return sync_fail(s);
@@ -989,20 +1055,28 @@ bo_status nehvi_prepare_impl(bo_model model, const float* ZX, int32_t S, const f
   if ((s = step(launch_trmm(false, sc.A, sc.Zk, sc.T1, nf, Sp, m, st), "trmm")) != BO_OK) return sync_fail(s);
   if ((s = step(launch_trmm(false, sc.W0, sc.T1, sc.Zk, nf, Sp, m, st), "trmm")) != BO_OK) return sync_fail(s);
   if ((s = step(launch_trmm(true, sc.W0, sc.Zk, sc.G, nf, Sp, m, st), "trmm")) != BO_OK) return sync_fail(s);
-  // fronts and boxes of every sample
-  NehviFrontArgs fa;
-  fa.Y = sc.Y; fa.alpha64 = sc.alpha64; fa.noise = gp.noise; fa.T1 = sc.T1;
-  fa.n = n; fa.nf = nf; fa.Sp = Sp; fa.S = S;
-  fa.ref0 = ref[0]; fa.ref1 = ref[1];
-  fa.cons = lower != nullptr;
-  fa.low0 = lower ? lower[0] : -INFINITY;
-  fa.low1 = lower ? lower[1] : -INFINITY;
-  fa.boxes = sc.btmp; fa.counts = sc.counts; fa.front = z.front;
-  if ((s = step(launch_sample_fronts(fa, st), "fronts")) != BO_OK) return sync_fail(s);
+  std::vector<double> Fh;
+  if (m == 2) {
+    // fronts and boxes of every draw on the device
+    NehviFrontArgs fa;
+    fa.Y = sc.Y; fa.alpha64 = sc.alpha64; fa.noise = gp.noise; fa.T1 = sc.T1;
+    fa.n = n; fa.nf = nf; fa.Sp = Sp; fa.S = S;
+    fa.ref0 = ref[0]; fa.ref1 = ref[1];
+    fa.cons = lower != nullptr;
+    fa.low0 = lower ? lower[0] : -INFINITY;
+    fa.low1 = lower ? lower[1] : -INFINITY;
+    fa.boxes = sc.btmp; fa.counts = sc.counts; fa.front = z.front;
+    if ((s = step(launch_sample_fronts(fa, st), "fronts")) != BO_OK) return sync_fail(s);
+    e = hipMemcpyAsync(stage + off_cnt, sc.counts, sizeof(int) * S, hipMemcpyDeviceToHost, st);
+    if (e != hipSuccess) return sync_fail(hip_fail(e, "bo_nehvi_prepare: counts"));
+  } else {
+    if ((s = step(launch_insample_values(sc.Y, sc.alpha64, gp.noise, sc.T1, n, m, nf, Sp, S, sc.Fd, st), "draws")) != BO_OK) return sync_fail(s);
+    Fh.resize((size_t)S * n * m);
+    e = hipMemcpyAsync(Fh.data(), sc.Fd, sizeof(double) * Fh.size(), hipMemcpyDeviceToHost, st);
+    if (e != hipSuccess) return sync_fail(hip_fail(e, "bo_nehvi_prepare: draws"));
+  }
   if ((s = step(launch_absmax(sc.G, (int64_t)nf * Sp, m, sc.gmax, st), "absmax")) != BO_OK) return sync_fail(s);
   e = hipMemcpyAsync(stage + off_flag, sc.flag, 3 * sizeof(int), hipMemcpyDeviceToHost, st);
-  if (e == hipSuccess)
-    e = hipMemcpyAsync(stage + off_cnt, sc.counts, sizeof(int) * S, hipMemcpyDeviceToHost, st);
   if (e == hipSuccess)
     e = hipMemcpyAsync(stage + off_gmax, sc.gmax, sizeof(double) * m * kAbsmaxParts,
                        hipMemcpyDeviceToHost, st);
@@ -1010,11 +1084,22 @@ bo_status nehvi_prepare_impl(bo_model model, const float* ZX, int32_t S, const f
   if (e != hipSuccess) return sync_fail(hip_fail(e, "bo_nehvi_prepare: sync"));
   int flags[3];
   std::memcpy(flags, stage + off_flag, sizeof(flags));
-  if (flags[0]) return sync_fail(fail(BO_ERR_NOT_POSITIVE_DEFINITE, std::string(W_) + ": K not positive definite"));
-  if (flags[1]) return sync_fail(fail(BO_ERR_NOT_POSITIVE_DEFINITE, std::string(W_) + ": in-sample posterior covariance not positive definite"));
-  if (flags[2]) return sync_fail(fail(BO_ERR_NOT_POSITIVE_DEFINITE, std::string(W_) + ": noise-free K_XX not positive definite"));
-  z.counts.assign(reinterpret_cast<const int*>(stage + off_cnt),
-                  reinterpret_cast<const int*>(stage + off_cnt) + S);
+  if (flags[0]) return sync_fail(fail(BO_ERR_NOT_POSITIVE_DEFINITE, W_ + ": K not positive definite"));
+  if (flags[1]) return sync_fail(fail(BO_ERR_NOT_POSITIVE_DEFINITE, W_ + ": in-sample posterior covariance not positive definite"));
+  if (flags[2]) return sync_fail(fail(BO_ERR_NOT_POSITIVE_DEFINITE, W_ + ": noise-free K_XX not positive definite"));
+  std::vector<std::vector<float>> hboxes;
+  std::vector<std::vector<int32_t>> hfronts;
+  if (m == 2) {
+    z.counts.assign(reinterpret_cast<const int*>(stage + off_cnt),
+                    reinterpret_cast<const int*>(stage + off_cnt) + S);
+    z.fsize.resize(S);
+    for (int i = 0; i < S; ++i) z.fsize[i] = z.counts[i] - 1;     // the staircase has P + 1 boxes
+  } else {
+    if (!all_finite_d(Fh)) return sync_fail(fail(BO_ERR_NONFINITE_INPUT, W_ + ": non-finite in-sample draw"));
+    host_draw_boxes(Fh, S, n, m, ref, lower, z.counts, hboxes, hfronts);
+    z.fsize.resize(S);
+    for (int i = 0; i < S; ++i) z.fsize[i] = static_cast<int>(hfronts[i].size());
+  }
   int* off = reinterpret_cast<int*>(stage + off_off);
   int64_t total = 0;
   for (int i = 0; i < S; ++i) {
@@ -1022,15 +1107,17 @@ bo_status nehvi_prepare_impl(bo_model model, const float* ZX, int32_t S, const f
     total += z.counts[i];
   }
   off[S] = static_cast<int>(total);
-  if (nehvi_ehvi_lds_bytes(S, static_cast<int>(total)) > kLdsLimit)
-    return sync_fail(fail(BO_ERR_CAPACITY, std::string(W_) + ": per-sample boxes exceed LDS"));
-  double gmax[2] = {0.0, 0.0};
+  if (total > (int64_t)1 << 28)
+    return sync_fail(fail(BO_ERR_CAPACITY, W_ + ": too many per-draw boxes"));
+  if (nehvi_ehvi_lds_bytes(S, 4, m, 0, false) > kLdsLimit)
+    return sync_fail(fail(BO_ERR_CAPACITY, W_ + ": base samples exceed LDS"));
+  double gmax[3] = {0.0, 0.0, 0.0};
   {
     const double* parts = reinterpret_cast<const double*>(stage + off_gmax);
     for (int k = 0; k < m; ++k)
       for (int b = 0; b < kAbsmaxParts; ++b) gmax[k] = std::max(gmax[k], parts[k * kAbsmaxParts + b]);
   }
-  float scale[2];
+  float scale[3] = {1.f, 1.f, 1.f};
   for (int k = 0; k < m; ++k) {
     // a power of two that brings max |G| into [2^13, 2^14): the fp16 low
     // halves then stay clear of the subnormal range
@@ -1041,44 +1128,63 @@ bo_status nehvi_prepare_impl(bo_model model, const float* ZX, int32_t S, const f
     z.ginv[k] = std::ldexp(1.0f, -ex);
   }
   if ((s = palloc(&z.Gp, (size_t)m * n32 * nrb * 1024, st, "noisy: G fragments")) != BO_OK) return sync_fail(s);
-  if ((s = palloc(&z.boxes, (size_t)total * 4, st, "noisy: boxes")) != BO_OK) return sync_fail(s);
+  if ((s = palloc(&z.boxes, (size_t)std::max<int64_t>(total, 1) * 2 * m, st, "noisy: boxes")) != BO_OK) return sync_fail(s);
   if ((s = palloc(&z.off, (size_t)S + 1, st, "noisy: box offsets")) != BO_OK) return sync_fail(s);
   e = hipMemcpyAsync(z.off, off, sizeof(int) * (S + 1), hipMemcpyHostToDevice, st);
   if (e != hipSuccess) return sync_fail(hip_fail(e, "bo_nehvi_prepare: offsets"));
-  if ((s = step(launch_compact_boxes(sc.btmp, (int64_t)(n + 1) * 4, z.off, S, z.boxes, st), "boxes")) != BO_OK) return sync_fail(s);
+  if (m == 2) {
+    if ((s = step(launch_compact_boxes(sc.btmp, (int64_t)(n + 1) * 4, z.off, S, z.boxes, st), "boxes")) != BO_OK) return sync_fail(s);
+  } else {
+    // boxes and fronts built on the host: one pageable upload each
+    std::vector<float> flat((size_t)total * 2 * m);
+    std::vector<int32_t> fr((size_t)S * n, -1);
+    for (int i = 0; i < S; ++i) {
+      std::copy(hboxes[i].begin(), hboxes[i].end(), flat.begin() + (size_t)off[i] * 2 * m);
+      std::copy(hfronts[i].begin(), hfronts[i].end(), fr.begin() + (size_t)i * n);
+    }
+    e = hipMemcpy(z.boxes, flat.data(), sizeof(float) * flat.size(), hipMemcpyHostToDevice);
+    if (e == hipSuccess)
+      e = hipMemcpy(z.front, fr.data(), sizeof(int32_t) * fr.size(), hipMemcpyHostToDevice);
+    if (e != hipSuccess) return sync_fail(hip_fail(e, "bo_nehvi_prepare: boxes"));
+  }
   if ((s = step(launch_pack_g(sc.G, nf, Sp, n32, m, scale, z.Gp, st), "pack G")) != BO_OK) return sync_fail(s);
   e = hipStreamSynchronize(st);
   if (e != hipSuccess) return sync_fail(hip_fail(e, "bo_nehvi_prepare: sync"));
-  z.S = S; z.Sp = Sp; z.n32 = n32; z.total = static_cast<int>(total);
+  z.S = S; z.Sp = Sp; z.n32 = n32; z.total = static_cast<int>(total); z.m = m;
   z.cons = lower != nullptr;
-  z.low[0] = lower ? lower[0] : -INFINITY;
-  z.low[1] = lower ? lower[1] : -INFINITY;
+  for (int k = 0; k < 3; ++k) z.low[k] = (lower && k < m) ? lower[k] : -INFINITY;
   M.last_stream = st;
   return BO_OK;
 }
 
-bo_status score_nehvi_impl(bo_model model, const float* cand, int64_t M_, const float* Z,
-                           int32_t S, float* ehvi, void* stream) {
+bo_status score_nehvi_impl(bo_model model, const float* cand, int64_t M_, int32_t q,
+                           const float* Z, int32_t S, float* ehvi, void* stream) {
   if (!model) return fail(BO_ERR_INVALID_ARGUMENT, "bo_score_nehvi: model is NULL");
   Model& M = model->m;
   Model::Noisy& z = M.nz;
   if (z.S == 0) return fail(BO_ERR_INVALID_ARGUMENT, "bo_score_nehvi: call bo_nehvi_prepare first");
   if (S != z.S) return fail(BO_ERR_INVALID_ARGUMENT, "bo_score_nehvi: S differs from the prepared S");
+  if (q != 1 && q != 2 && q != 4) return fail(BO_ERR_INVALID_ARGUMENT, "bo_score_nehvi: q must be 1, 2 or 4");
   if (M_ < 0) return fail(BO_ERR_INVALID_ARGUMENT, "bo_score_nehvi: M < 0");
   if (M_ > (int64_t)1 << 40) return fail(BO_ERR_CAPACITY, "bo_score_nehvi: M too large");
   if (M_ == 0) return BO_OK;
   DeviceGuard g(M.device);
   if (!g.ok) return fail(BO_ERR_DEVICE, "bo_score_nehvi: cannot select the model's device");
+  const int m = M.m;
   bo_status s;
-  if ((s = check_dev(cand, sizeof(float) * M_ * M.d, "cand")) != BO_OK) return s;
-  if ((s = check_dev(Z, sizeof(float) * (size_t)S * 2, "base_samples")) != BO_OK) return s;
+  if ((s = check_dev(cand, sizeof(float) * M_ * q * M.d, "cand")) != BO_OK) return s;
+  if ((s = check_dev(Z, sizeof(float) * (size_t)S * q * m, "base_samples")) != BO_OK) return s;
   if ((s = check_dev(ehvi, sizeof(float) * M_, "ehvi")) != BO_OK) return s;
-  if (posterior_lds_bytes(M.nb, 1) > kLdsLimit)
+  if (posterior_lds_bytes(M.nb, q) > kLdsLimit)
     return fail(BO_ERR_CAPACITY, "bo_score_nehvi: posterior tile exceeds LDS");
+  if (nehvi_ehvi_lds_bytes(S, q, m, 0, false) > kLdsLimit)
+    return fail(BO_ERR_CAPACITY, "bo_score_nehvi: base samples exceed LDS");
   hipStream_t st = static_cast<hipStream_t>(stream);
-  const int m = 2;
-  const int64_t C = std::min<int64_t>(M_, kNehviChunk);
-  const size_t need = (size_t)C * m * 2 + (size_t)m * S * C;
+  const int T = q * (q + 1) / 2;
+  const int64_t Cb = std::min<int64_t>(M_, kNehviChunk / q);   // batches per chunk
+  const int64_t C = Cb * q;                                     // points per chunk
+  const size_t need = 2 * (size_t)C * m + (q > 1 ? (size_t)Cb * m * T : 0) +
+                      (size_t)m * S * C;
   if (need > z.ws_floats) {
     if (z.ws) {
       hipError_t e = hipDeviceSynchronize();      // earlier launches may use it
@@ -1089,14 +1195,17 @@ bo_status score_nehvi_impl(bo_model model, const float* cand, int64_t M_, const 
     if ((s = palloc(&z.ws, need, st, "noisy: scoring workspace")) != BO_OK) return s;
     z.ws_floats = need;
   }
-  float* mu_buf = z.ws;
-  float* sd_buf = z.ws + (size_t)C * m;
-  float* dbuf = z.ws + (size_t)C * m * 2;
-  for (int64_t c0 = 0; c0 < M_; c0 += C) {
-    const int64_t np_ = std::min<int64_t>(C, M_ - c0);
+  float* mu_buf = z.ws;                                          // [C][m]
+  float* sd_buf = z.ws + (size_t)C * m;                          // [C][m] marginal tau
+  float* ch_buf = sd_buf + (size_t)C * m;                        // q > 1: [Cb][m][T] factors
+  float* dbuf = ch_buf + (q > 1 ? (size_t)Cb * m * T : 0);       // [m][S][C]
+  for (int64_t b0 = 0; b0 < M_; b0 += Cb) {
+    const int64_t nb_ = std::min<int64_t>(Cb, M_ - b0);
+    const int64_t np_ = nb_ * q;
+    const float* cc = cand + b0 * q * M.d;
     for (int k = 0; k < m; ++k) {
       PosteriorArgs pa;
-      pa.cand = cand + c0 * M.d; pa.npts = np_; pa.d = M.d; pa.dx = M.dx; pa.q = 1;
+      pa.cand = cc; pa.npts = np_; pa.d = M.d; pa.dx = M.dx; pa.q = q;
       pa.Xs = M.Xs + (size_t)k * M.n_pad * M.dx;
       pa.invls = M.invls + (size_t)k * M.dx;
       pa.alpha = M.alpha + (size_t)k * M.n_pad;
@@ -1105,21 +1214,27 @@ bo_status score_nehvi_impl(bo_model model, const float* cand, int64_t M_, const 
       pa.s = M.os[k];
       pa.m = m; pa.k = k;
       pa.dr = 0; pa.dr4 = 0; pa.s_dep = 0.f; pa.s_int = 0.f; pa.wts = nullptr; pa.pref = nullptr;
-      pa.mu = mu_buf; pa.sd = sd_buf; pa.chol = nullptr;
+      pa.mu = mu_buf; pa.sd = sd_buf; pa.chol = (q > 1) ? ch_buf : nullptr;
       if ((s = after_launch(launch_posterior(pa, st), st, "posterior")) != BO_OK) return s;
     }
     NehviMeansArgs ma;
-    ma.cand = cand + c0 * M.d; ma.npts = np_; ma.d = M.d; ma.dx = M.dx; ma.n32 = z.n32;
+    ma.cand = cc; ma.npts = np_; ma.d = M.d; ma.dx = M.dx; ma.n32 = z.n32;
     ma.n_pad = M.n_pad; ma.S = S; ma.Xs = M.Xs; ma.invls = M.invls; ma.Gp = z.Gp;
-    for (int k = 0; k < m; ++k) { ma.s[k] = M.os[k]; ma.ginv[k] = z.ginv[k]; }
+    for (int k = 0; k < 3; ++k) {
+      ma.s[k] = k < m ? M.os[k] : 0.f;
+      ma.ginv[k] = z.ginv[k];
+    }
     ma.out = dbuf; ma.ldo = C;
     if ((s = after_launch(launch_nehvi_means(ma, m, st), st, "conditional means")) != BO_OK) return s;
     NehviEhviArgs ea;
-    ea.mu = mu_buf; ea.sd = sd_buf; ea.D = dbuf; ea.ldd = C; ea.Z = Z;
-    ea.boxes = z.boxes; ea.off = z.off; ea.total = z.total; ea.npts = np_; ea.S = S;
-    ea.cons = z.cons; ea.low0 = z.low[0]; ea.low1 = z.low[1]; ea.ehvi = ehvi + c0;
+    ea.mu = mu_buf; ea.sd = sd_buf; ea.chol = ch_buf; ea.D = dbuf; ea.ldd = C; ea.Z = Z;
+    ea.boxes = z.boxes; ea.off = z.off; ea.total = z.total; ea.nbat = nb_; ea.S = S;
+    ea.q = q; ea.m = m; ea.cons = z.cons;
+    for (int k = 0; k < 3; ++k) ea.low[k] = z.low[k];
+    ea.ehvi = ehvi + b0;
     if ((s = after_launch(launch_nehvi_ehvi(ea, st), st, "noisy ehvi")) != BO_OK) return s;
   }
+  z.q = q;
   M.last_stream = st;
   return BO_OK;
 }
@@ -1133,9 +1248,9 @@ bo_status bo_nehvi_prepare(bo_model model, const float* base_samples_X, int32_t 
   return nehvi_prepare_impl(model, base_samples_X, S, ref_point, feas_lower, stream);
 }
 
-bo_status bo_score_nehvi(bo_model model, const float* cand, int64_t M, const float* base_samples,
-                         int32_t S, float* ehvi, void* stream) {
-  return score_nehvi_impl(model, cand, M, base_samples, S, ehvi, stream);
+bo_status bo_score_nehvi(bo_model model, const float* cand, int64_t M, int32_t q,
+                         const float* base_samples, int32_t S, float* ehvi, void* stream) {
+  return score_nehvi_impl(model, cand, M, q, base_samples, S, ehvi, stream);
 }
 
 bo_status bo_nehvi_front(bo_model model, int32_t sample, int32_t* idx_host, int32_t cap,
@@ -1146,7 +1261,7 @@ bo_status bo_nehvi_front(bo_model model, int32_t sample, int32_t* idx_host, int3
   if (M.nz.S == 0) return fail(BO_ERR_INVALID_ARGUMENT, "bo_nehvi_front: not prepared");
   if (sample < 0 || sample >= M.nz.S)
     return fail(BO_ERR_INVALID_ARGUMENT, "bo_nehvi_front: sample out of range");
-  const int32_t P = M.nz.counts[sample] - 1;
+  const int32_t P = M.nz.fsize[sample];
   *count = P;
   const int32_t k = std::min(cap, P);
   if (k > 0) {

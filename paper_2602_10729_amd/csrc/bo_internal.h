@@ -22,12 +22,13 @@ bo_status hip_fail(hipError_t e, const char* what);
 // Host geometry (host_geom.cpp) -------------------------------------------
 // Non-dominated rows of Y (maximise, duplicates keep the lowest index),
 // optionally only rows strictly above ref, sorted by objective 0 then index.
-void host_front(const float* Y, int64_t n, int m, const float* ref,
-                std::vector<int32_t>& out);
+// (instantiated for float and double)
+template <typename T>
+void host_front(const T* Y, int64_t n, int m, const T* ref, std::vector<int32_t>& out);
 // Disjoint boxes of the region the front does not dominate; lo/hi row-major
 // [count][m]; hi may be +inf.
-void host_boxes(const float* F, int P, int m, const float* ref,
-                std::vector<float>& lo, std::vector<float>& hi);
+template <typename T>
+void host_boxes(const T* F, int P, int m, const T* ref, std::vector<T>& lo, std::vector<T>& hi);
 
 // Device layout of a fitted model ----------------------------------------
 struct Model {
@@ -62,13 +63,15 @@ struct Model {
     int S = 0, Sp = 0, n32 = 0, total = 0;
     float* Lp0 = nullptr;        // [m][lp_per_obj] packed inverse factor of K_XX (no noise)
     uint16_t* Gp = nullptr;      // [m][n32][Sp/16][1024] fp16 hi/lo fragments of G^T
-    float ginv[2] = {1.f, 1.f};  // 1 / scale applied to G before the split
-    float* boxes = nullptr;      // [total][4] per-sample boxes, sample s at off[s]
+    int m = 0, q = 1;            // objectives; batch size of the last scoring call
+    float ginv[3] = {1.f, 1.f, 1.f};  // 1 / scale applied to G before the split
+    float* boxes = nullptr;      // [total][2m] per-sample boxes (lo, width), sample s at off[s]
     int* off = nullptr;          // [S + 1]
     int32_t* front = nullptr;    // [S][n] per-sample front indices, sorted by objective 0
-    std::vector<int> counts;     // [S] boxes per sample (front size + 1)
+    std::vector<int> counts;     // [S] boxes per sample
+    std::vector<int> fsize;      // [S] front size per sample
     bool cons = false;
-    float low[2] = {0.f, 0.f};
+    float low[3] = {0.f, 0.f, 0.f};
     float* ws = nullptr;         // scoring workspace
     size_t ws_floats = 0;
   } nz;
@@ -165,6 +168,10 @@ struct NehviFrontArgs {
   int32_t* front;          // [S][n]
 };
 hipError_t launch_sample_fronts(const NehviFrontArgs& a, hipStream_t st);
+// F[s][i][k] = y_ik - eta_k alpha_k,i + T1[k][i][s] (fp64, the in-sample draws)
+hipError_t launch_insample_values(const float* Y, const double* alpha64, const double* noise,
+                                  const double* T1, int64_t n, int m, int nf, int Sp, int S,
+                                  double* F, hipStream_t st);
 size_t nehvi_front_lds_bytes(int64_t n);
 // part [m][kAbsmaxParts]: partial maxima of |G[k]| (count entries per objective)
 constexpr int kAbsmaxParts = 128;
@@ -180,29 +187,30 @@ struct NehviMeansArgs {
   const float* Xs;         // [m][n_pad][dx] scaled training inputs
   const float* invls;      // [m][dx]
   const uint16_t* Gp;      // packed G^T fragments (fp16 bits)
-  float s[2];              // output scales
-  float ginv[2];           // 1 / scale of G
+  float s[3];              // output scales
+  float ginv[3];           // 1 / scale of G
   float* out;              // [m][S][ldo]
   int64_t ldo;
 };
 hipError_t launch_nehvi_means(const NehviMeansArgs& a, int m, hipStream_t st);
 struct NehviEhviArgs {
-  const float* mu;         // [npts][2] posterior mean
-  const float* sd;         // [npts][2] noise-free conditional std (tau)
-  const float* D;          // [2][S][ldd] K* G
+  const float* mu;         // [nbat * q][m] posterior mean
+  const float* sd;         // q = 1: [nbat][m] noise-free conditional std (tau)
+  const float* chol;       // q > 1: [nbat][m][q(q+1)/2] factor of the conditional batch covariance
+  const float* D;          // [m][S][ldd] K* G (point index b * q + member)
   int64_t ldd;
-  const float* Z;          // [S][2] candidate base samples
-  const float* boxes;      // [total][4]
+  const float* Z;          // [S][q][m] candidate base samples
+  const float* boxes;      // [total][2m] (lo, width)
   const int* off;          // [S + 1]
   int total;
-  int64_t npts;
-  int S;
+  int64_t nbat;
+  int S, q, m;
   bool cons;
-  float low0, low1;
-  float* ehvi;             // [npts]
+  float low[3];
+  float* ehvi;             // [nbat]
 };
 hipError_t launch_nehvi_ehvi(const NehviEhviArgs& a, hipStream_t st);
-size_t nehvi_ehvi_lds_bytes(int S, int total);
+size_t nehvi_ehvi_lds_bytes(int S, int q, int m, int total, bool boxes_in_lds);
 int nehvi_padded_samples(int S);
 
 // Coordinate held by slot t of the scaled layout, or -1 for padding: the

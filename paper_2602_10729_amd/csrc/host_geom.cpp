@@ -32,8 +32,8 @@
 
 namespace bo {
 
-void host_front(const float* Y, int64_t n, int m, const float* ref,
-                std::vector<int32_t>& out) {
+template <typename T>
+void host_front(const T* Y, int64_t n, int m, const T* ref, std::vector<int32_t>& out) {
   // Visit the rows in decreasing lexicographic order (objective 0, 1, ...,
   // then increasing index). A row can only be dominated, or duplicated with a
   // lower index, by a row visited before it, and if it is, some row already
@@ -43,7 +43,7 @@ void host_front(const float* Y, int64_t n, int m, const float* ref,
   std::vector<int32_t> order;
   order.reserve(static_cast<size_t>(n));
   for (int64_t i = 0; i < n; ++i) {
-    const float* yi = Y + i * m;
+    const T* yi = Y + i * m;
     if (ref) {
       bool above = true;
       for (int k = 0; k < m; ++k) above = above && (yi[k] > ref[k]);
@@ -52,17 +52,17 @@ void host_front(const float* Y, int64_t n, int m, const float* ref,
     order.push_back(static_cast<int32_t>(i));
   }
   std::sort(order.begin(), order.end(), [&](int32_t a, int32_t b) {
-    const float* ya = Y + static_cast<int64_t>(a) * m;
-    const float* yb = Y + static_cast<int64_t>(b) * m;
+    const T* ya = Y + static_cast<int64_t>(a) * m;
+    const T* yb = Y + static_cast<int64_t>(b) * m;
     for (int k = 0; k < m; ++k)
       if (ya[k] != yb[k]) return ya[k] > yb[k];
     return a < b;
   });
   if (m == 2) {
     // two objectives: kept iff objective 1 beats every row visited before
-    float best = -std::numeric_limits<float>::infinity();
+    T best = -std::numeric_limits<T>::infinity();
     for (int32_t i : order) {
-      const float y1 = Y[static_cast<int64_t>(i) * 2 + 1];
+      const T y1 = Y[static_cast<int64_t>(i) * 2 + 1];
       if (out.empty() || y1 > best) {
         out.push_back(i);
         best = y1;
@@ -70,10 +70,10 @@ void host_front(const float* Y, int64_t n, int m, const float* ref,
     }
   } else {
     for (int32_t i : order) {
-      const float* yi = Y + static_cast<int64_t>(i) * m;
+      const T* yi = Y + static_cast<int64_t>(i) * m;
       bool keep = true;
       for (int32_t j : out) {
-        const float* yj = Y + static_cast<int64_t>(j) * m;
+        const T* yj = Y + static_cast<int64_t>(j) * m;
         bool ge = true;
         for (int k = 0; k < m; ++k) ge = ge && (yj[k] >= yi[k]);
         if (ge) {            // dominated, or an exact duplicate of a lower index
@@ -85,17 +85,15 @@ void host_front(const float* Y, int64_t n, int m, const float* ref,
     }
   }
   std::stable_sort(out.begin(), out.end(), [&](int32_t a, int32_t b) {
-    const float ya = Y[static_cast<int64_t>(a) * m], yb = Y[static_cast<int64_t>(b) * m];
+    const T ya = Y[static_cast<int64_t>(a) * m], yb = Y[static_cast<int64_t>(b) * m];
     return ya < yb || (ya == yb && a < b);
   });
 }
 
 namespace {
 
-constexpr float kInf = std::numeric_limits<float>::infinity();
-
-void push_box(std::vector<float>& lo, std::vector<float>& hi,
-              float l0, float l1, float l2, float h0, float h1, float h2, int m) {
+template <typename T>
+void push_box(std::vector<T>& lo, std::vector<T>& hi, T l0, T l1, T l2, T h0, T h1, T h2, int m) {
   lo.push_back(l0); lo.push_back(l1);
   hi.push_back(h0); hi.push_back(h1);
   if (m == 3) { lo.push_back(l2); hi.push_back(h2); }
@@ -103,20 +101,21 @@ void push_box(std::vector<float>& lo, std::vector<float>& hi,
 
 }  // namespace
 
-void host_boxes(const float* F, int P, int m, const float* ref,
-                std::vector<float>& lo, std::vector<float>& hi) {
+template <typename T>
+void host_boxes(const T* F, int P, int m, const T* ref, std::vector<T>& lo, std::vector<T>& hi) {
+  constexpr T kInf = std::numeric_limits<T>::infinity();
   lo.clear();
   hi.clear();
   if (m == 2) {
     // F sorted by objective 0 ascending: box i covers objective 0 in
     // [x_{i-1}, x_i) (x_0 = ref_0) and objective 1 above y_i; the last box
     // covers [x_P, inf) above ref_1.
-    float xlo = ref[0];
+    T xlo = ref[0];
     for (int i = 0; i < P; ++i) {
-      push_box(lo, hi, xlo, F[2 * i + 1], 0.f, F[2 * i], kInf, 0.f, 2);
+      push_box<T>(lo, hi, xlo, F[2 * i + 1], T(0), F[2 * i], kInf, T(0), 2);
       xlo = F[2 * i];
     }
-    push_box(lo, hi, xlo, ref[1], 0.f, kInf, kInf, 0.f, 2);
+    push_box<T>(lo, hi, xlo, ref[1], T(0), kInf, kInf, T(0), 2);
     return;
   }
   // m == 3
@@ -124,14 +123,14 @@ void host_boxes(const float* F, int P, int m, const float* ref,
   std::iota(order.begin(), order.end(), 0);
   std::stable_sort(order.begin(), order.end(),
                    [&](int a, int b) { return F[3 * a + 2] > F[3 * b + 2]; });
-  struct Step { float y; float ztop; };          // box (prev.x, x) x [y, inf)
-  std::map<float, Step> stair;                    // keyed by x ascending
-  float tail_ztop = kInf;                         // box [last.x, inf) x [ref1, inf)
-  auto close = [&](float xl, float xh, float yl, float zl, float zt) {
-    if (zt > zl) push_box(lo, hi, xl, yl, zl, xh, kInf, zt, 3);
+  struct Step { T y; T ztop; };          // box (prev.x, x) x [y, inf)
+  std::map<T, Step> stair;                    // keyed by x ascending
+  T tail_ztop = kInf;                         // box [last.x, inf) x [ref1, inf)
+  auto close = [&](T xl, T xh, T yl, T zl, T zt) {
+    if (zt > zl) push_box<T>(lo, hi, xl, yl, zl, xh, kInf, zt, 3);
   };
   for (int idx : order) {
-    const float px = F[3 * idx], py = F[3 * idx + 1], zb = F[3 * idx + 2];
+    const T px = F[3 * idx], py = F[3 * idx + 1], zb = F[3 * idx + 2];
     // dominated in 2-D by an active point (x >= px and y >= py)?
     auto it = stair.lower_bound(px);              // first x >= px
     if (it != stair.end() && it->second.y >= py) continue;
@@ -150,9 +149,9 @@ void host_boxes(const float* F, int P, int m, const float* ref,
       if (prev->second.y <= py) left = prev; else break;
     }
     // range [left, first_rm) is removed; compute the x just before it
-    float pred_x = (left == stair.begin()) ? ref[0] : std::prev(left)->first;
+    T pred_x = (left == stair.begin()) ? ref[0] : std::prev(left)->first;
     // close removed steps
-    float xl = pred_x;
+    T xl = pred_x;
     for (auto r = left; r != first_rm; ++r) {
       close(xl, r->first, r->second.y, zb, r->second.ztop);
       xl = r->first;
@@ -170,12 +169,19 @@ void host_boxes(const float* F, int P, int m, const float* ref,
     stair[px] = Step{py, zb};
   }
   // close everything at ref_2
-  float xl = ref[0];
+  T xl = ref[0];
   for (auto& kv : stair) {
     close(xl, kv.first, kv.second.y, ref[2], kv.second.ztop);
     xl = kv.first;
   }
   close(xl, kInf, ref[1], ref[2], tail_ztop);
 }
+
+template void host_front<float>(const float*, int64_t, int, const float*, std::vector<int32_t>&);
+template void host_front<double>(const double*, int64_t, int, const double*, std::vector<int32_t>&);
+template void host_boxes<float>(const float*, int, int, const float*, std::vector<float>&,
+                                std::vector<float>&);
+template void host_boxes<double>(const double*, int, int, const double*, std::vector<double>&,
+                                 std::vector<double>&);
 
 }  // namespace bo

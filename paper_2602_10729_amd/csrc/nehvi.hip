@@ -1,4 +1,4 @@
-// Noisy expected hypervolume improvement (qNEHVI, q = 1, two objectives).
+// Noisy expected hypervolume improvement (qNEHVI; q-batches, two or three objectives).
 //
 // Paper: "Overall MOBO workflow" step (ii) and the constrained qNEHVI
 // paragraph: the acquisition averages, over Monte-Carlo samples of the joint
@@ -157,20 +157,37 @@ __global__ __launch_bounds__(256) void k_absmax(const double* __restrict__ G, in
   if (threadIdx.x == 0) part[(int64_t)k * gridDim.x + blockIdx.x] = red[0];
 }
 
+// The in-sample draws f_ik = y_ik - eta_k alpha_k,i + T1[k][i][s] (mu_X =
+// y - eta alpha) as F [S][n][m], fp64, for the host's per-draw fronts.
+__global__ __launch_bounds__(256) void k_insample_values(const float* __restrict__ Y,
+                                                         const double* __restrict__ alpha64,
+                                                         const double* __restrict__ noise,
+                                                         const double* __restrict__ T1,
+                                                         int64_t n, int m, int nf, int Sp, int S,
+                                                         double* __restrict__ F) {
+  const int k = blockIdx.y;
+  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;   // s * n + i
+  if (e >= (int64_t)S * n) return;
+  const int64_t i = e % n;
+  const int s = static_cast<int>(e / n);
+  F[e * m + k] = static_cast<double>(Y[i * m + k]) - noise[k] * alpha64[(int64_t)k * nf + i] +
+                 T1[((int64_t)k * nf + i) * Sp + s];
+}
+
 // A fragments of G^T (scaled by sc[k]) for v_mfma_f32_16x16x32_f16: block
 // (J, rb) covers training rows 32J .. 32J+31 and samples 16rb .. 16rb+15;
 // lane l element e holds G[32J + 8(l/16) + e][16rb + l%16], split as
 // hi = fp16(g), lo = fp16(g - hi). Layout [k][J][rb][plane][64][8].
 __global__ __launch_bounds__(256) void k_pack_g(const double* __restrict__ G, int nf, int Sp,
                                                 int n32, int nrb, float sc0, float sc1,
-                                                _Float16* __restrict__ Gp) {
+                                                float sc2, _Float16* __restrict__ Gp) {
   const int k = blockIdx.y;
   const int64_t g = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (g >= (int64_t)n32 * nrb * 64) return;
   const int lane = static_cast<int>(g % 64);
   const int64_t blk = g / 64;
   const int J = static_cast<int>(blk / nrb), rb = static_cast<int>(blk % nrb);
-  const double sc = (k == 0) ? sc0 : sc1;
+  const double sc = (k == 0) ? sc0 : (k == 1) ? sc1 : sc2;
   const int col = 16 * rb + lane % 16;
   _Float16* dst = Gp + ((int64_t)k * n32 * nrb + blk) * 1024 + lane * 8;
 #pragma unroll
@@ -391,55 +408,152 @@ __global__ __launch_bounds__(kMW * 64) void k_nehvi_means(NehviMeansArgs a) {
 
 // ---- per-sample HVI -----------------------------------------------------------
 
-// One lane per candidate: y_s,k = mu_k + D[k][s][c] + tau_k z*_s,k, then the
-// staircase HVI of y_s against the boxes of sample s (all lanes are at the
-// same sample, so every box read is an LDS broadcast). The constrained form
-// replaces an infeasible sample's first objective by -inf, which zeroes every
-// box term.
+// One lane per candidate batch. Draw s of member a, objective k:
+//   y = mu_ak + D[k][s][b q + a] + (q = 1: tau_k z_s,k;
+//                                   q > 1: sum_t C_k[a][t] z_s,t,k),
+// then the HVI of the batch against the boxes of draw s (inclusion-exclusion
+// over the member subsets for q > 1). All lanes are at the same draw, so the
+// box loop is uniform and every box read is a broadcast: from LDS when the
+// boxes fit there (LDSB), else from global memory. The constrained form
+// replaces an infeasible member's first objective by -inf, which zeroes every
+// term that contains it.
 constexpr int kET = 512;   // threads per workgroup of the HVI kernel
 
-template <bool CONS>
+template <int MO>
+__device__ __forceinline__ float nz_mask(const float (&y)[MO], const NehviEhviArgs& a) {
+  bool ok = true;
+#pragma unroll
+  for (int k = 0; k < MO; ++k) ok = ok && (y[k] >= a.low[k]);
+  return ok ? y[0] : -__builtin_inff();
+}
+
+template <int MO, int Q, bool CONS, bool LDSB>
 __global__ __launch_bounds__(kET) void k_nehvi_ehvi(NehviEhviArgs a) {
   extern __shared__ float esm[];
-  float* zs = esm;                                          // [S][2]
-  float* bx = esm + 2 * a.S;                                // [total][4]
-  int* off = reinterpret_cast<int*>(bx + 4 * a.total);      // [S + 1]
-  for (int i = threadIdx.x; i < 2 * a.S; i += kET) zs[i] = a.Z[i];
-  for (int i = threadIdx.x; i < 4 * a.total; i += kET) bx[i] = a.boxes[i];
+  constexpr int BW = 2 * MO;
+  constexpr int T = Q * (Q + 1) / 2;
+  constexpr int NS = 1 << Q;
+  constexpr int U = (Q * MO <= 2) ? 16 : (Q * MO <= 4) ? 8 : (Q * MO <= 8) ? 4 : 2;
+  float* zs = esm;                                                  // [S][Q][MO]
+  int* off = reinterpret_cast<int*>(zs + a.S * Q * MO);            // [S + 1]
+  float* bxl = reinterpret_cast<float*>(off + a.S + 1);            // [total][BW] (LDSB)
+  for (int i = threadIdx.x; i < a.S * Q * MO; i += kET) zs[i] = a.Z[i];
   for (int i = threadIdx.x; i <= a.S; i += kET) off[i] = a.off[i];
+  if constexpr (LDSB)
+    for (int i = threadIdx.x; i < a.total * BW; i += kET) bxl[i] = a.boxes[i];
   __syncthreads();
-  const int64_t c = (int64_t)blockIdx.x * kET + threadIdx.x;
-  const bool valid = c < a.npts;
-  const int64_t cc = valid ? c : a.npts - 1;
-  const float mu0 = a.mu[2 * cc], mu1 = a.mu[2 * cc + 1];
-  const float t0 = a.sd[2 * cc], t1 = a.sd[2 * cc + 1];
-  const float* d0 = a.D + cc;
-  const float* d1 = a.D + (int64_t)a.S * a.ldd + cc;
-  float acc = 0.f;
-  constexpr int U = 16;   // draws whose means are in flight together
+  const float* bx = LDSB ? bxl : a.boxes;
+  const int64_t b = (int64_t)blockIdx.x * kET + threadIdx.x;
+  const bool valid = b < a.nbat;
+  const int64_t bb = valid ? b : a.nbat - 1;
+  float mu[Q][MO];
+  float C[MO][T];                       // q = 1: C[k][0] = tau_k
+#pragma unroll
+  for (int i = 0; i < Q; ++i)
+#pragma unroll
+    for (int k = 0; k < MO; ++k) mu[i][k] = a.mu[(bb * Q + i) * MO + k];
+#pragma unroll
+  for (int k = 0; k < MO; ++k)
+#pragma unroll
+    for (int e = 0; e < T; ++e)
+      C[k][e] = (Q == 1) ? a.sd[bb * MO + k] : a.chol[(bb * MO + k) * T + e];
+  const float* dp = a.D + bb * Q;
+  const int64_t kstride = (int64_t)a.S * a.ldd;
+  float acc_pos = 0.f, acc_neg = 0.f;
   for (int s0 = 0; s0 < a.S; s0 += U) {
-    float v0[U], v1[U];
+    float dv[U][Q][MO];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int s = min(s0 + u, a.S - 1);
-      v0[u] = d0[(int64_t)s * a.ldd];
-      v1[u] = d1[(int64_t)s * a.ldd];
+#pragma unroll
+      for (int k = 0; k < MO; ++k)
+#pragma unroll
+        for (int i = 0; i < Q; ++i) dv[u][i][k] = dp[k * kstride + (int64_t)s * a.ldd + i];
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int s = s0 + u;
-      if (s >= a.S) break;
-      float y0 = mu0 + v0[u] + t0 * zs[2 * s];
-      const float y1 = mu1 + v1[u] + t1 * zs[2 * s + 1];
-      if constexpr (CONS) y0 = (y0 >= a.low0 && y1 >= a.low1) ? y0 : -__builtin_inff();
-      const int b1 = off[s + 1];
-      for (int b = off[s]; b < b1; ++b) {
-        const float4 q = *reinterpret_cast<const float4*>(bx + 4 * b);
-        acc += __builtin_amdgcn_fmed3f(y0 - q.x, 0.f, q.z) * __builtin_amdgcn_fmed3f(y1 - q.y, 0.f, q.w);
+      if (s >= a.S) continue;     // uniform: the tail of the last group
+      float y[Q][MO];
+#pragma unroll
+      for (int k = 0; k < MO; ++k)
+#pragma unroll
+        for (int i = 0; i < Q; ++i) {
+          float v = mu[i][k] + dv[u][i][k];
+#pragma unroll
+          for (int t = 0; t <= i; ++t) v = fmaf(C[k][i * (i + 1) / 2 + t], zs[(s * Q + t) * MO + k], v);
+          y[i][k] = v;
+        }
+      if constexpr (CONS) {
+#pragma unroll
+        for (int i = 0; i < Q; ++i) y[i][0] = nz_mask<MO>(y[i], a);
+      }
+      const int c0 = __builtin_amdgcn_readfirstlane(off[s]);
+      const int c1 = __builtin_amdgcn_readfirstlane(off[s + 1]);
+      for (int c = c0; c < c1; ++c) {
+        float lo[MO], w[MO];
+#pragma unroll
+        for (int k = 0; k < MO; ++k) {
+          lo[k] = bx[c * BW + k];
+          w[k] = bx[c * BW + MO + k];
+        }
+        if constexpr (Q == 1) {
+          float t = __builtin_amdgcn_fmed3f(y[0][0] - lo[0], 0.f, w[0]);
+#pragma unroll
+          for (int k = 1; k < MO; ++k) t *= __builtin_amdgcn_fmed3f(y[0][k] - lo[k], 0.f, w[k]);
+          acc_pos += t;
+        } else {
+          float ext[NS][MO];
+#pragma unroll
+          for (int i = 0; i < Q; ++i)
+#pragma unroll
+            for (int k = 0; k < MO; ++k)
+              ext[1 << i][k] = __builtin_amdgcn_fmed3f(y[i][k] - lo[k], 0.f, w[k]);
+#pragma unroll
+          for (int mask = 1; mask < NS; ++mask) {
+            const int low = mask & (-mask);
+            if (mask != low) {
+#pragma unroll
+              for (int k = 0; k < MO; ++k) ext[mask][k] = fminf(ext[mask ^ low][k], ext[low][k]);
+            }
+            float t = ext[mask][0];
+#pragma unroll
+            for (int k = 1; k < MO; ++k) t *= ext[mask][k];
+            if (__builtin_popcount(mask) & 1) acc_pos += t;
+            else acc_neg += t;
+          }
+        }
       }
     }
   }
-  if (valid) a.ehvi[c] = acc / static_cast<float>(a.S);
+  if (valid) a.ehvi[b] = (acc_pos - acc_neg) / static_cast<float>(a.S);
+}
+
+template <int MO, int Q, bool CONS>
+hipError_t nz_ehvi_launch(const NehviEhviArgs& a, bool ldsb, size_t lds, unsigned grid,
+                          hipStream_t st) {
+  static bool attr = false;
+  if (!attr) {
+    for (const void* f : {reinterpret_cast<const void*>(&k_nehvi_ehvi<MO, Q, CONS, true>),
+                          reinterpret_cast<const void*>(&k_nehvi_ehvi<MO, Q, CONS, false>)}) {
+      hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+      if (e != hipSuccess) return e;
+    }
+    attr = true;
+  }
+  if (ldsb) hipLaunchKernelGGL((k_nehvi_ehvi<MO, Q, CONS, true>), dim3(grid), dim3(kET), lds, st, a);
+  else hipLaunchKernelGGL((k_nehvi_ehvi<MO, Q, CONS, false>), dim3(grid), dim3(kET), lds, st, a);
+  return hipGetLastError();
+}
+
+template <int MO, bool CONS>
+hipError_t nz_ehvi_q(const NehviEhviArgs& a, bool ldsb, size_t lds, unsigned grid, hipStream_t st) {
+  switch (a.q) {
+    case 1: return nz_ehvi_launch<MO, 1, CONS>(a, ldsb, lds, grid, st);
+    case 2: return nz_ehvi_launch<MO, 2, CONS>(a, ldsb, lds, grid, st);
+    case 4: return nz_ehvi_launch<MO, 4, CONS>(a, ldsb, lds, grid, st);
+  }
+  return hipErrorInvalidValue;
 }
 
 template <int DX4>
@@ -459,8 +573,9 @@ size_t nehvi_front_lds_bytes(int64_t n) {
   return sizeof(double) * 2 * n + sizeof(int) * 3 * n;
 }
 
-size_t nehvi_ehvi_lds_bytes(int S, int total) {
-  return sizeof(float) * (2 * (size_t)S + 4 * (size_t)total) + sizeof(int) * ((size_t)S + 1);
+size_t nehvi_ehvi_lds_bytes(int S, int q, int m, int total, bool boxes_in_lds) {
+  return sizeof(float) * ((size_t)S * q * m + (boxes_in_lds ? 2 * (size_t)m * total : 0)) +
+         sizeof(int) * ((size_t)S + 1);
 }
 
 int nehvi_padded_samples(int S) { return (S + 127) / 128 * 128; }
@@ -482,7 +597,8 @@ hipError_t launch_pack_g(const double* G, int nf, int Sp, int n32, int m, const 
   const int nrb = Sp / 16;
   const unsigned g = static_cast<unsigned>(((int64_t)n32 * nrb * 64 + 255) / 256);
   hipLaunchKernelGGL(k_pack_g, dim3(g, m), dim3(256), 0, st, G, nf, Sp, n32, nrb, scale[0],
-                     m > 1 ? scale[1] : 1.f, reinterpret_cast<_Float16*>(Gp));
+                     m > 1 ? scale[1] : 1.f, m > 2 ? scale[2] : 1.f,
+                     reinterpret_cast<_Float16*>(Gp));
   return hipGetLastError();
 }
 
@@ -510,20 +626,24 @@ hipError_t launch_nehvi_means(const NehviMeansArgs& a, int m, hipStream_t st) {
 }
 
 hipError_t launch_nehvi_ehvi(const NehviEhviArgs& a, hipStream_t st) {
-  if (a.npts <= 0) return hipSuccess;
-  static bool attr = false;
-  if (!attr) {
-    for (const void* f : {reinterpret_cast<const void*>(&k_nehvi_ehvi<false>),
-                          reinterpret_cast<const void*>(&k_nehvi_ehvi<true>)}) {
-      hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-      if (e != hipSuccess) return e;
-    }
-    attr = true;
-  }
-  const size_t lds = nehvi_ehvi_lds_bytes(a.S, a.total);
-  const unsigned grid = static_cast<unsigned>((a.npts + kET - 1) / kET);
-  if (a.cons) hipLaunchKernelGGL(k_nehvi_ehvi<true>, dim3(grid), dim3(kET), lds, st, a);
-  else hipLaunchKernelGGL(k_nehvi_ehvi<false>, dim3(grid), dim3(kET), lds, st, a);
+  if (a.nbat <= 0) return hipSuccess;
+  const bool ldsb = nehvi_ehvi_lds_bytes(a.S, a.q, a.m, a.total, true) <= 160 * 1024;
+  const size_t lds = nehvi_ehvi_lds_bytes(a.S, a.q, a.m, a.total, ldsb);
+  if (lds > 160 * 1024) return hipErrorInvalidValue;
+  const unsigned grid = static_cast<unsigned>((a.nbat + kET - 1) / kET);
+  if (a.m == 2) return a.cons ? nz_ehvi_q<2, true>(a, ldsb, lds, grid, st)
+                              : nz_ehvi_q<2, false>(a, ldsb, lds, grid, st);
+  if (a.m == 3) return a.cons ? nz_ehvi_q<3, true>(a, ldsb, lds, grid, st)
+                              : nz_ehvi_q<3, false>(a, ldsb, lds, grid, st);
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_insample_values(const float* Y, const double* alpha64, const double* noise,
+                                  const double* T1, int64_t n, int m, int nf, int Sp, int S,
+                                  double* F, hipStream_t st) {
+  const unsigned g = static_cast<unsigned>(((int64_t)S * n + 255) / 256);
+  hipLaunchKernelGGL(k_insample_values, dim3(g, m), dim3(256), 0, st, Y, alpha64, noise, T1, n, m,
+                     nf, Sp, S, F);
   return hipGetLastError();
 }
 

@@ -27,8 +27,7 @@ def _gpu(wl, cand, ZX, Zs, ref=None, lower=None, model=None):
     if model is None:
         model = bo.fit(to_dev(wl.X), to_dev(wl.Y), wl.lengthscale, wl.outputscale, wl.noise)
     bo.nehvi_prepare(model, to_dev(ZX), wl.ref if ref is None else ref, lower=lower)
-    e = bo.score_nehvi(model, to_dev(np.ascontiguousarray(cand.reshape(cand.shape[0], -1))),
-                       to_dev(np.ascontiguousarray(Zs.reshape(Zs.shape[0], -1))))
+    e = bo.score_nehvi(model, to_dev(np.ascontiguousarray(cand)), to_dev(np.ascontiguousarray(Zs)))
     idx, val = bo.argmax(e)
     torch.cuda.synchronize()
     return dict(ehvi=e.cpu().numpy(), idx=int(idx.item()), val=float(val.item()), model=model)
@@ -36,8 +35,7 @@ def _gpu(wl, cand, ZX, Zs, ref=None, lower=None, model=None):
 
 def _oracle(wl, cand, ZX, Zs, ref=None, lower=None, model=None):
     om = oracle_fit(wl) if model is None else model
-    return O.nehvi(om, cand.reshape(cand.shape[0], -1), wl.ref if ref is None else ref,
-                   ZX, Zs.reshape(Zs.shape[0], -1),
+    return O.nehvi(om, cand, wl.ref if ref is None else ref, ZX, Zs,
                    lower=None if lower is None else np.asarray(lower, dtype=np.float64))
 
 
@@ -177,14 +175,89 @@ def test_noisy_reprepare_and_edges():
     big = np.zeros((513, wl.n, 2), dtype=np.float32)
     with pytest.raises(bo.BoError, match="CAPACITY"):
         bo.nehvi_prepare(model, to_dev(big), wl.ref)
-    # three objectives and composite-kernel models are not supported
-    wl4 = bi.make_config(4, seed=0, M=4)
-    m3 = bo.fit(to_dev(wl4.X), to_dev(wl4.Y), wl4.lengthscale, wl4.outputscale, wl4.noise)
+    # batches of three and composite-kernel models are not supported
     with pytest.raises(bo.BoError, match="INVALID_ARGUMENT"):
-        bo.nehvi_prepare(m3, to_dev(np.zeros((8, wl4.n, 3), np.float32)), wl4.ref)
+        bo.score_nehvi(model, to_dev(np.ascontiguousarray(wl.cand[:6, 0, :].reshape(2, 3, -1))),
+                       to_dev(np.zeros((64, 3, 2), np.float32)))
     comp = bi.composite_hyperparameters(wl)
     mc = bo.fit_composite(to_dev(wl.X), to_dev(wl.Y), comp.d_route, wl.lengthscale, comp.s_route,
                           comp.s_dep, comp.s_int, comp.pref, wl.noise)
     with pytest.raises(bo.BoError, match="INVALID_ARGUMENT"):
         bo.nehvi_prepare(mc, to_dev(ZX), wl.ref)
     torch.cuda.synchronize()
+
+
+def _batched(wl, ZX, M, q, seed):
+    """q-batches from the workload's candidate stream and their base samples."""
+    d = wl.cand.shape[-1]
+    pts = wl.cand.reshape(-1, d)[:M * q]
+    Zs = np.random.default_rng(seed + 7).standard_normal((ZX.shape[0], q, wl.m)).astype(np.float32)
+    return np.ascontiguousarray(pts.reshape(M, q, d)), Zs
+
+
+@pytest.mark.parametrize("cfg,M,q,seed", [(0, 1500, 2, 0), (1, 700, 4, 1), (0, 333, 4, 2)])
+def test_noisy_batch_parity_two_objectives(cfg, M, q, seed):
+    _announce("nehvi batches", cfg, M, q, seed)
+    wl = bi.make_config(cfg, seed=seed, M=M * q)
+    ZX = bi.insample_base_samples(wl)
+    cand, Zs = _batched(wl, ZX, M, q, seed)
+    g = _gpu(wl, cand, ZX, Zs)
+    o = _oracle(wl, cand, ZX, Zs)
+    assert_close(g["ehvi"], o["ehvi"], TOL_EHVI, "nehvi batches")
+    check_argmax(g["idx"], o["ehvi"])
+
+
+@pytest.mark.parametrize("q,M,S,seed", [(1, 400, 128, 0), (4, 48, 512, 0), (2, 96, 200, 1)])
+def test_noisy_three_objectives(q, M, S, seed):
+    # config 4's observations (n = 2048, d = 24, three objectives): per-draw
+    # fronts and 3-D boxes built on the host, boxes read from global memory
+    _announce("nehvi three objectives", q, M, S, seed)
+    wl = bi.make_config(4, seed=seed, M=M)
+    ZX = bi.insample_base_samples(wl, S)
+    if q == 4 and S == wl.S:
+        cand, Zs = np.ascontiguousarray(wl.cand), wl.Z
+    else:
+        cand, Zs = _batched(wl, ZX, M, q, seed)
+        if q == 1:
+            cand, Zs = cand[:, 0, :], Zs[:, 0, :]
+    g = _gpu(wl, cand, ZX, Zs)
+    o = _oracle(wl, cand, ZX, Zs)
+    assert_close(g["ehvi"], o["ehvi"], TOL_EHVI, "nehvi three objectives")
+    check_argmax(g["idx"], o["ehvi"])
+    _check_fronts(g, o, wl.ref, None, range(0, S, max(1, S // 8)))
+
+
+def test_noisy_three_objectives_constrained():
+    _announce("nehvi three objectives constrained")
+    wl = bi.make_config(4, seed=2, M=40)
+    ZX = bi.insample_base_samples(wl, 256)
+    cand, Zs = _batched(wl, ZX, 40, 4, 2)
+    lower = bi.feasibility_thresholds(wl, [0.3, None, 0.2])
+    g = _gpu(wl, cand, ZX, Zs, lower=lower)
+    om = oracle_fit(wl)
+    o = _oracle(wl, cand, ZX, Zs, lower=lower, model=om)
+    # bounds over the member draws whose feasibility is ambiguous (module doc)
+    F, Ls = O.insample_samples(om, ZX)
+    ys = O.batch_samples(om, cand, ZX, Zs, Ls)                       # [M, S, q, m]
+    low = np.asarray(lower, dtype=np.float64)
+    # each side's member draw differs by at most the mean tolerance plus the
+    # std tolerance times sum_t |z_t| (factor entries are at most sqrt(s) = 1)
+    zsum = np.abs(Zs).sum(axis=1)[None, :, None, :]                  # [1, S, 1, m]
+    band = 4.0 * (1e-4 * np.abs(ys) + 1e-4 * zsum + 1e-5)
+    d = ys - low
+    sure = np.all(d > band, axis=-1).astype(float)
+    maybe = np.all(d >= -band, axis=-1).astype(float)
+    lo = np.empty(len(cand))
+    hi = np.empty(len(cand))
+    hs_lo = np.empty((len(cand), ZX.shape[0]))
+    hs_hi = np.empty_like(hs_lo)
+    for s in range(ZX.shape[0]):
+        blo, bhi = o["boxes"][s]
+        hs_lo[:, s] = O.qhvi(ys[:, s], blo, bhi, sure[:, s])
+        hs_hi[:, s] = O.qhvi(ys[:, s], blo, bhi, maybe[:, s])
+    lo, hi = hs_lo.mean(axis=1), hs_hi.mean(axis=1)
+    assert_within_bounds(g["ehvi"], lo, hi, TOL_EHVI, "constrained nehvi, three objectives")
+    exact = lo == hi
+    assert exact.mean() > 0.3, exact.mean()
+    assert_close(g["ehvi"][exact], o["ehvi"][exact], TOL_EHVI, "constrained nehvi (unambiguous)")
+    _check_fronts(g, o, wl.ref, lower, range(0, 256, 32))
