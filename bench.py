@@ -269,8 +269,8 @@ def main(argv=None):
         "launch_ms": c_ms, "lane_ops_per_launch": c_ops,
     }
     # the paper's composite surrogate (routing Matern-5/2 + preference-weighted
-    # deployment Matern-3/2 + interaction), q = 1 workloads only
-    if wl.q == 1:
+    # deployment Matern-3/2 + interaction)
+    if True:
         comp = bi.composite_hyperparameters(wl)
         t0 = time.perf_counter()
         mc = bo.fit_composite(X, Y, comp.d_route, wl.lengthscale, comp.s_route, comp.s_dep,

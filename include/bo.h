@@ -129,8 +129,10 @@ bo_status bo_fit(const float* X, const float* Y, int64_t n, int32_t d, int32_t m
  * scale_route host [m] > 0;  scale_dep, scale_int host [m] >= 0
  * pref        host [m][d - d_route], finite
  * Other arguments, behaviour and errors as bo_fit (CAPACITY when the padded
- * groups exceed BO_MAX_D). Models fitted this way score q = 1 batches only
- * (bo_score returns INVALID_ARGUMENT for q > 1).
+ * groups exceed BO_MAX_D). Models fitted this way score single points and
+ * q-batches through bo_score; the batch factor's pivot rule takes the sum
+ * of the three scales as the prior scale. bo_nehvi_prepare does not accept
+ * them.
  */
 bo_status bo_fit_composite(const float* X, const float* Y, int64_t n, int32_t d, int32_t m,
                            int32_t d_route, const float* lengthscale,

@@ -11,6 +11,7 @@ from __future__ import annotations
 import argparse
 import concurrent.futures as cf
 import os
+import re
 import shutil
 import subprocess
 import sys
@@ -38,11 +39,17 @@ def hipcc() -> str:
 
 
 def sources():
+    """Every source, the widest posterior instantiations first: they take
+    longest to compile, so starting them first shortens a parallel build."""
     out = []
     for f in sorted(os.listdir(CSRC)):
         if f.endswith(".hip") or f.endswith(".cpp"):
             out.append(os.path.join(CSRC, f))
-    return out
+
+    def cost(path):
+        m = re.match(r"posterior_dx(\d)", os.path.basename(path))
+        return -int(m.group(1)) if m else 0
+    return sorted(out, key=cost)
 
 
 def _compile(src: str, verbose: bool, extra=(), bdir=BUILD) -> str:

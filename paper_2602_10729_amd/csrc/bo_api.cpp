@@ -707,8 +707,6 @@ bo_status bo_score_constrained(bo_model model, const float* cand, int64_t M_, in
   const int64_t npts = M_ * q;
   bo_status s;
   if (M_ == 0) return BO_OK;
-  if (M.dr > 0 && q != 1)
-    return fail(BO_ERR_INVALID_ARGUMENT, "bo_score: composite-kernel models score q = 1 only");
   if ((s = check_dev(cand, sizeof(float) * npts * M.d, "cand")) != BO_OK) return s;
   if ((s = check_dev(base_samples, sizeof(float) * (size_t)S * q * m, "base_samples")) != BO_OK) return s;
   if ((s = check_dev(ehvi, sizeof(float) * M_, "ehvi")) != BO_OK) return s;

@@ -426,7 +426,6 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
   constexpr int NX = (Q > 1) ? Q : 1;   // per-point partial slots (diag + xors)
   using Prod = Producer<NT, DX4, COMP>;
   static_assert(Prod::RPL >= 2 && Prod::RPL <= 8 && 64 % Prod::CPW == 0, "tile width");
-  static_assert(!(COMP && Q > 1), "the composite kernel scores single points");
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   // wave index as a scalar: the loop control below stays uniform
@@ -441,6 +440,7 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
   const int64_t p0 = (int64_t)blockIdx.x * NT;
 
   Prod P;
+  float wstar = 0.f;        // composite: w(candidate)
   P.col = wave * Prod::CPW + lane % Prod::CPW;
   P.row0 = (lane / Prod::CPW) * Prod::RPL;
   {
@@ -449,7 +449,6 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
 #pragma unroll
     for (int t = 0; t < DX4 * 4; ++t) P.c[t] = 0.f;
     P.wsd = 0.f;
-    float wstar = 0.f;
     if (P.valid) {
       const float* cp = a.cand + p * a.d;
 #pragma unroll
@@ -473,17 +472,37 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
     const int x = lane / Prod::CPW;
     if (x >= 1 && x < Q) {
       const int64_t pm = (p0 + P.col) ^ x;
-      float r2 = 0.f;
+      float r2 = 0.f, r2r = 0.f, wm = 0.f;     // r2r, wm: composite routing part, w(partner)
       if (P.valid && pm < a.npts) {
         const float* cp = a.cand + pm * a.d;
 #pragma unroll
-        for (int t = 0; t < DX4 * 4; ++t)
-          if (t < a.d) {
-            const float dd = P.c[t] - cp[t] * a.invls[t];
+        for (int t = 0; t < DX4 * 4; ++t) {
+          if constexpr (COMP) {
+            if (t == 4 * a.dr4) {
+              r2r = r2;
+              r2 = 0.f;
+            }
+          }
+          const int c = slot_dim(t, a.d, a.dr, a.dr4);
+          if (c >= 0) {
+            const float dd = P.c[t] - cp[c] * a.invls[t];
             r2 = fmaf(dd, dd, r2);
           }
+        }
+        if constexpr (COMP) {
+          float e = 0.f;
+          for (int t = a.dr; t < a.d; ++t) e = fmaf(a.pref[t - a.dr], cp[t], e);
+          wm = expf(e);
+        }
       }
-      kpp[P.col * 4 + x] = matern52_f(r2, a.s);
+      if constexpr (COMP) {
+        // s_route M52(r_route) + s_dep w w' M32(r_dep) + s_int M52 M32
+        const float k5 = matern52_f(r2r, 1.0f);
+        const float k3 = matern32_f(r2);
+        kpp[P.col * 4 + x] = fmaf(a.s_dep * wstar * wm, k3, k5 * fmaf(a.s_int, k3, a.s));
+      } else {
+        kpp[P.col * 4 + x] = matern52_f(r2, a.s);
+      }
     }
   }
 
@@ -665,7 +684,8 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
         for (int i = 0; i < Q; ++i)
 #pragma unroll
           for (int j = 0; j < Q; ++j) L[i][j] = 0.f;
-        const float tol = 1e-10f * a.s;
+        // pivot scale: the prior scale (composite: the sum of the three)
+        const float tol = 1e-10f * (COMP ? a.s + a.s_dep + a.s_int : a.s);
 #pragma unroll
         for (int j = 0; j < Q; ++j) {
           float pv = S[j][j];
@@ -717,31 +737,28 @@ hipError_t launch_t(const PosteriorArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
-// Launch for coordinate width 4*DX4: q in {1, 2, 4}; 2 row-block slots per
-// wave up to 256 rows, else BO_POST_RB (further rows in passes).
-template <int DX4>
+// Launch for coordinate width 4*DX4 and kernel family COMP: q in {1, 2, 4};
+// 2 row-block slots per wave up to 256 rows, else BO_POST_RB (further rows
+// in passes).
+template <int DX4, bool COMP>
 hipError_t launch_for_dx(const PosteriorArgs& a, hipStream_t st) {
   const bool small = a.nb <= 16;
-  if (a.dr > 0) {
-    // composite kernel: single points only
-    if (a.q != 1) return hipErrorInvalidValue;
-    return small ? launch_t<BO_POST_NT, DX4, 1, 2, true>(a, st)
-                 : launch_t<BO_POST_NT, DX4, 1, BO_POST_RB, true>(a, st);
-  }
   switch (a.q) {
-    case 1: return small ? launch_t<BO_POST_NT, DX4, 1, 2, false>(a, st)
-                         : launch_t<BO_POST_NT, DX4, 1, BO_POST_RB, false>(a, st);
-    case 2: return small ? launch_t<BO_POST_NT, DX4, 2, 2, false>(a, st)
-                         : launch_t<BO_POST_NT, DX4, 2, BO_POST_RB, false>(a, st);
-    case 4: return small ? launch_t<BO_POST_NT, DX4, 4, 2, false>(a, st)
-                         : launch_t<BO_POST_NT, DX4, 4, BO_POST_RB, false>(a, st);
+    case 1: return small ? launch_t<BO_POST_NT, DX4, 1, 2, COMP>(a, st)
+                         : launch_t<BO_POST_NT, DX4, 1, BO_POST_RB, COMP>(a, st);
+    case 2: return small ? launch_t<BO_POST_NT, DX4, 2, 2, COMP>(a, st)
+                         : launch_t<BO_POST_NT, DX4, 2, BO_POST_RB, COMP>(a, st);
+    case 4: return small ? launch_t<BO_POST_NT, DX4, 4, 2, COMP>(a, st)
+                         : launch_t<BO_POST_NT, DX4, 4, BO_POST_RB, COMP>(a, st);
     default: return hipErrorInvalidValue;
   }
 }
 
 }  // namespace
 
-// One per coordinate width (posterior_dx<N>.hip).
+// One per coordinate width and kernel family (posterior_dx<N>.hip: Matern-5/2,
+// posterior_dx<N>c.hip: composite kernel; a composite model needs at least two
+// coordinate groups, so width 4 has no composite instantiation).
 hipError_t launch_posterior_dx1(const PosteriorArgs& a, hipStream_t st);
 hipError_t launch_posterior_dx2(const PosteriorArgs& a, hipStream_t st);
 hipError_t launch_posterior_dx3(const PosteriorArgs& a, hipStream_t st);
@@ -750,5 +767,12 @@ hipError_t launch_posterior_dx5(const PosteriorArgs& a, hipStream_t st);
 hipError_t launch_posterior_dx6(const PosteriorArgs& a, hipStream_t st);
 hipError_t launch_posterior_dx7(const PosteriorArgs& a, hipStream_t st);
 hipError_t launch_posterior_dx8(const PosteriorArgs& a, hipStream_t st);
+hipError_t launch_posterior_comp_dx2(const PosteriorArgs& a, hipStream_t st);
+hipError_t launch_posterior_comp_dx3(const PosteriorArgs& a, hipStream_t st);
+hipError_t launch_posterior_comp_dx4(const PosteriorArgs& a, hipStream_t st);
+hipError_t launch_posterior_comp_dx5(const PosteriorArgs& a, hipStream_t st);
+hipError_t launch_posterior_comp_dx6(const PosteriorArgs& a, hipStream_t st);
+hipError_t launch_posterior_comp_dx7(const PosteriorArgs& a, hipStream_t st);
+hipError_t launch_posterior_comp_dx8(const PosteriorArgs& a, hipStream_t st);
 
 }  // namespace bo
