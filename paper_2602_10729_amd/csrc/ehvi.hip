@@ -142,6 +142,18 @@ __global__ __launch_bounds__(kThreads) void k_ehvi_q(EhviArgs a) {
         for (int i = 0; i < Q; ++i) y[j][i][0] = mask_infeasible<MO>(y[j][i], a);
       }
     }
+    // per sample, the batch's best value in each objective: a box whose
+    // lower corner no member exceeds in some objective adds exactly zero
+    float ymax[SC][MO];
+#pragma unroll
+    for (int j = 0; j < SC; ++j)
+#pragma unroll
+      for (int k = 0; k < MO; ++k) {
+        float v = y[j][0][k];
+#pragma unroll
+        for (int i = 1; i < Q; ++i) v = fmaxf(v, y[j][i][k]);
+        ymax[j][k] = v;
+      }
     for (int c = 0; c < a.nbox; ++c) {
       float lo[MO], w[MO];
 #pragma unroll
@@ -149,6 +161,15 @@ __global__ __launch_bounds__(kThreads) void k_ehvi_q(EhviArgs a) {
         lo[k] = bx[c * 2 * MO + k];
         w[k] = bx[c * 2 * MO + MO + k];
       }
+      bool live = false;
+#pragma unroll
+      for (int j = 0; j < SC; ++j) {
+        bool nz = true;
+#pragma unroll
+        for (int k = 0; k < MO; ++k) nz = nz && (ymax[j][k] > lo[k]);
+        live = live || nz;
+      }
+      if (__ballot(live) == 0) continue;   // the whole wave would add zeros
 #pragma unroll
       for (int j = 0; j < SC; ++j) {
         float ext[NS][MO];

@@ -488,6 +488,14 @@ __global__ __launch_bounds__(kET) void k_nehvi_ehvi(NehviEhviArgs a) {
 #pragma unroll
         for (int i = 0; i < Q; ++i) y[i][0] = nz_mask<MO>(y[i], a);
       }
+      float ymax[MO];       // the batch's best value per objective in this draw
+#pragma unroll
+      for (int k = 0; k < MO; ++k) {
+        float v = y[0][k];
+#pragma unroll
+        for (int i = 1; i < Q; ++i) v = fmaxf(v, y[i][k]);
+        ymax[k] = v;
+      }
       const int c0 = __builtin_amdgcn_readfirstlane(off[s]);
       const int c1 = __builtin_amdgcn_readfirstlane(off[s + 1]);
       for (int c = c0; c < c1; ++c) {
@@ -496,6 +504,14 @@ __global__ __launch_bounds__(kET) void k_nehvi_ehvi(NehviEhviArgs a) {
         for (int k = 0; k < MO; ++k) {
           lo[k] = bx[c * BW + k];
           w[k] = bx[c * BW + MO + k];
+        }
+        if constexpr (Q > 1 || MO > 2) {
+          // a box whose lower corner no member exceeds in some objective adds
+          // exactly zero; skip it when that holds on every lane
+          bool nz = true;
+#pragma unroll
+          for (int k = 0; k < MO; ++k) nz = nz && (ymax[k] > lo[k]);
+          if (__ballot(nz) == 0) continue;
         }
         if constexpr (Q == 1) {
           float t = __builtin_amdgcn_fmed3f(y[0][0] - lo[0], 0.f, w[0]);
