@@ -196,41 +196,27 @@ __global__ __launch_bounds__(kThreads) void k_ehvi_q(EhviArgs a) {
   if (valid) a.ehvi[b] = (acc_pos - acc_neg) / static_cast<float>(a.S);
 }
 
+// Launch with the dynamic-LDS limit raised for that kernel (set on every
+// launch, so that it holds on whichever device is current).
+template <typename K>
+hipError_t launch_k(K kern, unsigned grid, size_t lds, hipStream_t st, const EhviArgs& a) {
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(kThreads), lds, st, a);
+  return hipGetLastError();
+}
+
 template <int MO, bool CONS>
 hipError_t launch_mo(const EhviArgs& a, hipStream_t st) {
   const unsigned grid = static_cast<unsigned>((a.nbat + kThreads - 1) / kThreads);
   const size_t lds = sizeof(float) * ((size_t)a.S * a.q * MO + (size_t)a.nbox * 2 * MO);
   switch (a.q) {
-    case 1:
-      hipLaunchKernelGGL((k_ehvi_q1<MO, 16, CONS>), dim3(grid), dim3(kThreads), lds, st, a);
-      break;
-    case 2:
-      hipLaunchKernelGGL((k_ehvi_q<MO, 2, 4, CONS>), dim3(grid), dim3(kThreads), lds, st, a);
-      break;
-    case 4:
-      hipLaunchKernelGGL((k_ehvi_q<MO, 4, 2, CONS>), dim3(grid), dim3(kThreads), lds, st, a);
-      break;
-    default:
-      return hipErrorInvalidValue;
+    case 1: return launch_k(&k_ehvi_q1<MO, 16, CONS>, grid, lds, st, a);
+    case 2: return launch_k(&k_ehvi_q<MO, 2, 4, CONS>, grid, lds, st, a);
+    case 4: return launch_k(&k_ehvi_q<MO, 4, 2, CONS>, grid, lds, st, a);
+    default: return hipErrorInvalidValue;
   }
-  return hipGetLastError();
-}
-
-template <bool CONS>
-hipError_t set_lds_limit() {
-  const void* fns[] = {
-      reinterpret_cast<const void*>(&k_ehvi_q1<2, 16, CONS>),
-      reinterpret_cast<const void*>(&k_ehvi_q1<3, 16, CONS>),
-      reinterpret_cast<const void*>(&k_ehvi_q<2, 2, 4, CONS>),
-      reinterpret_cast<const void*>(&k_ehvi_q<3, 2, 4, CONS>),
-      reinterpret_cast<const void*>(&k_ehvi_q<2, 4, 2, CONS>),
-      reinterpret_cast<const void*>(&k_ehvi_q<3, 4, 2, CONS>)};
-  for (const void* f : fns) {
-    hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                       160 * 1024);
-    if (e != hipSuccess) return e;
-  }
-  return hipSuccess;
 }
 
 }  // namespace
@@ -241,13 +227,6 @@ size_t ehvi_lds_bytes(int S, int q, int m, int nbox) {
 
 hipError_t launch_ehvi(const EhviArgs& a, hipStream_t st) {
   if (a.nbat <= 0) return hipSuccess;
-  static bool attr_set = false;
-  if (!attr_set) {
-    hipError_t e = set_lds_limit<false>();
-    if (e == hipSuccess) e = set_lds_limit<true>();
-    if (e != hipSuccess) return e;
-    attr_set = true;
-  }
   if (a.m == 2) return a.constrained ? launch_mo<2, true>(a, st) : launch_mo<2, false>(a, st);
   if (a.m == 3) return a.constrained ? launch_mo<3, true>(a, st) : launch_mo<3, false>(a, st);
   return hipErrorInvalidValue;

@@ -548,15 +548,12 @@ __global__ __launch_bounds__(kET) void k_nehvi_ehvi(NehviEhviArgs a) {
 template <int MO, int Q, bool CONS>
 hipError_t nz_ehvi_launch(const NehviEhviArgs& a, bool ldsb, size_t lds, unsigned grid,
                           hipStream_t st) {
-  static bool attr = false;
-  if (!attr) {
-    for (const void* f : {reinterpret_cast<const void*>(&k_nehvi_ehvi<MO, Q, CONS, true>),
-                          reinterpret_cast<const void*>(&k_nehvi_ehvi<MO, Q, CONS, false>)}) {
-      hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-      if (e != hipSuccess) return e;
-    }
-    attr = true;
-  }
+  // more than 64 KiB of dynamic LDS: opt in on every launch, so that it holds
+  // on whichever device is current
+  const void* f = ldsb ? reinterpret_cast<const void*>(&k_nehvi_ehvi<MO, Q, CONS, true>)
+                       : reinterpret_cast<const void*>(&k_nehvi_ehvi<MO, Q, CONS, false>);
+  hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+  if (e != hipSuccess) return e;
   if (ldsb) hipLaunchKernelGGL((k_nehvi_ehvi<MO, Q, CONS, true>), dim3(grid), dim3(kET), lds, st, a);
   else hipLaunchKernelGGL((k_nehvi_ehvi<MO, Q, CONS, false>), dim3(grid), dim3(kET), lds, st, a);
   return hipGetLastError();
