@@ -17,6 +17,13 @@
  *               expectation of HVI over samples of the joint posterior).
  *   bo_argmax — index of the best candidate ("selecting the next candidate
  *               configuration theta*").
+ *   bo_score_constrained — bo_score with the feasibility indicator of the
+ *               constrained form.
+ *   bo_nehvi_prepare / bo_score_nehvi — the noisy form (qNEHVI): the latent
+ *               objectives at the observations are sampled jointly with the
+ *               candidates, with a Pareto front per sample.
+ *   bo_mll    — exact log marginal likelihood and its gradient, for fitting
+ *               the hyperparameters on the host.
  *
  * Conventions shared by every entry point:
  *   - All floating-point arrays are fp32, row-major, contiguous.
