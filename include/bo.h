@@ -138,8 +138,8 @@ bo_status bo_fit(const float* X, const float* Y, int64_t n, int32_t d, int32_t m
  * Other arguments, behaviour and errors as bo_fit (CAPACITY when the padded
  * groups exceed BO_MAX_D). Models fitted this way score single points and
  * q-batches through bo_score; the batch factor's pivot rule takes the sum
- * of the three scales as the prior scale. bo_nehvi_prepare does not accept
- * them.
+ * of the three scales as the prior scale. They are also accepted by
+ * bo_nehvi_prepare / bo_score_nehvi.
  */
 bo_status bo_fit_composite(const float* X, const float* Y, int64_t n, int32_t d, int32_t m,
                            int32_t d_route, const float* lengthscale,
@@ -241,7 +241,8 @@ bo_status bo_score_constrained(bo_model model, const float* cand, int64_t M, int
 
 /*
  * bo_nehvi_prepare / bo_score_nehvi — the noisy acquisition (qNEHVI;
- * candidates or q-batches, two or three objectives, Matern-5/2 models).
+ * candidates or q-batches, two or three objectives, Matern-5/2 or
+ * composite-kernel models).
  *
  * Paper: workflow step (ii) and the "Constrained qNEHVI" paragraph (after
  * Daulton et al. 2021). The observations are noisy, so the latent objective
@@ -269,8 +270,7 @@ bo_status bo_score_constrained(bo_model model, const float* cand, int64_t M, int
  *   objectives, on the host's threads for three), the factor of K_XX and
  *   G = K_XX^{-1} L_XX Z_X; keeps them in the model (replacing an earlier
  *   preparation). Synchronous.
- *   Errors: INVALID_ARGUMENT (m not 2 or 3, composite-kernel model, bad S or
- *   pointer), CAPACITY (S > 512, too many boxes), NOT_POSITIVE_DEFINITE (K,
+ *   Errors: INVALID_ARGUMENT (m not 2 or 3, bad S or pointer), CAPACITY (S > 512, too many boxes), NOT_POSITIVE_DEFINITE (K,
  *   the in-sample covariance or K_XX), NONFINITE_INPUT, OUT_OF_MEMORY,
  *   DEVICE.
  *

@@ -408,6 +408,7 @@ bo_status fit_impl(const char* who, const float* X, const float* Y, int64_t n, i
   if (comp) {
     M->s_dep.assign(comp->s_dep, comp->s_dep + m);
     M->s_int.assign(comp->s_int, comp->s_int + m);
+    M->prefh.assign(comp->pref, comp->pref + (size_t)m * (d - comp->dr));
   }
 
   auto bail = [&](bo_status st_) {
@@ -936,7 +937,6 @@ bo_status nehvi_prepare_impl(bo_model model, const float* ZX, int32_t S, const f
   Model& M = model->m;
   const int m = M.m, d = M.d;
   if (m != 2 && m != 3) return fail(BO_ERR_INVALID_ARGUMENT, W_ + ": two or three objectives");
-  if (M.dr > 0) return fail(BO_ERR_INVALID_ARGUMENT, W_ + ": Matern-5/2 models only");
   if (S < 1) return fail(BO_ERR_INVALID_ARGUMENT, W_ + ": S < 1");
   if (S > kNehviMaxS) return fail(BO_ERR_CAPACITY, W_ + ": S beyond 512");
   if (!ref) return fail(BO_ERR_INVALID_ARGUMENT, W_ + ": ref_point is NULL");
@@ -963,7 +963,10 @@ bo_status nehvi_prepare_impl(bo_model model, const float* ZX, int32_t S, const f
 
   NoisyScratch sc;
   sc.st = st;
-  const size_t nhyp = (size_t)m * d + 3 * m;     // [1/ls][os][noise][zeros]
+  // fp64 hyperparameters: [1/ls][os][noise][zeros] (+ [s_dep][s_int][pref])
+  const int dc = d - M.dr;
+  const bool comp = M.dr > 0;
+  const size_t nhyp = (size_t)m * d + 3 * m + (comp ? 2 * (size_t)m + (size_t)m * dc : 0);
   const size_t mat = (size_t)m * nf * nf, vec = (size_t)m * nf * Sp;
   if ((s = palloc(&sc.A, mat, st, "noisy: matrix")) != BO_OK) return s;
   if ((s = palloc(&sc.W, mat, st, "noisy: inverse")) != BO_OK) return s;
@@ -994,7 +997,13 @@ bo_status nehvi_prepare_impl(bo_model model, const float* ZX, int32_t S, const f
   for (int k = 0; k < m; ++k) {
     hyp[(size_t)m * d + k] = M.os[k];
     hyp[(size_t)m * d + m + k] = M.noise[k];
+    if (comp) {
+      hyp[(size_t)m * d + 3 * m + k] = M.s_dep[k];
+      hyp[(size_t)m * d + 4 * m + k] = M.s_int[k];
+    }
   }
+  if (comp)
+    for (size_t i = 0; i < (size_t)m * dc; ++i) hyp[(size_t)m * d + 5 * m + i] = M.prefh[i];
   // pinned staging: [hyp][flags 16 B][Y][counts][maxima][offsets]
   DeviceState* DS = device_state(M.device);
   if (!DS) return fail(BO_ERR_DEVICE, W_ + ": device index out of range");
@@ -1033,6 +1042,12 @@ bo_status nehvi_prepare_impl(bo_model model, const float* ZX, int32_t S, const f
   gp.ils = sc.hyp;
   gp.os = sc.hyp + (size_t)m * d;
   gp.noise = gp.os + m;
+  if (comp) {
+    gp.dr = M.dr;
+    gp.s_dep = gp.noise + 2 * m;
+    gp.s_int = gp.s_dep + m;
+    gp.pref = gp.s_int + m;
+  }
   GramParams g0 = gp;
   g0.noise = gp.noise + m;                  // zeros: the noise-free K_XX
   auto step = [&](hipError_t err, const char* what) { return after_launch(err, st, what); };
@@ -1211,7 +1226,11 @@ bo_status score_nehvi_impl(bo_model model, const float* cand, int64_t M_, int32_
       pa.n = static_cast<int>(M.n); pa.nb = M.nb;
       pa.s = M.os[k];
       pa.m = m; pa.k = k;
-      pa.dr = 0; pa.dr4 = 0; pa.s_dep = 0.f; pa.s_int = 0.f; pa.wts = nullptr; pa.pref = nullptr;
+      pa.dr = M.dr; pa.dr4 = M.dr4;
+      pa.s_dep = M.dr > 0 ? M.s_dep[k] : 0.f;
+      pa.s_int = M.dr > 0 ? M.s_int[k] : 0.f;
+      pa.wts = M.dr > 0 ? M.wts + (size_t)k * M.n_pad : nullptr;
+      pa.pref = M.dr > 0 ? M.pref + (size_t)k * (M.d - M.dr) : nullptr;
       pa.mu = mu_buf; pa.sd = sd_buf; pa.chol = (q > 1) ? ch_buf : nullptr;
       if ((s = after_launch(launch_posterior(pa, st), st, "posterior")) != BO_OK) return s;
     }
@@ -1221,7 +1240,10 @@ bo_status score_nehvi_impl(bo_model model, const float* cand, int64_t M_, int32_
     for (int k = 0; k < 3; ++k) {
       ma.s[k] = k < m ? M.os[k] : 0.f;
       ma.ginv[k] = z.ginv[k];
+      ma.s_dep[k] = (M.dr > 0 && k < m) ? M.s_dep[k] : 0.f;
+      ma.s_int[k] = (M.dr > 0 && k < m) ? M.s_int[k] : 0.f;
     }
+    ma.dr = M.dr; ma.dr4 = M.dr4; ma.wts = M.wts; ma.pref = M.pref;
     ma.out = dbuf; ma.ldo = C;
     if ((s = after_launch(launch_nehvi_means(ma, m, st), st, "conditional means")) != BO_OK) return s;
     NehviEhviArgs ea;

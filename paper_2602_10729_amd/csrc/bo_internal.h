@@ -43,6 +43,7 @@ struct Model {
   int dr = 0, dr4 = 0;
   std::vector<float> ls, os, noise;   // os: the (routing) output scale
   std::vector<float> s_dep, s_int;    // composite: deployment / interaction scales
+  std::vector<float> prefh;           // composite: host copy of pref [m][d - dr]
   std::vector<float> Yh;         // host copy of Y [n][m]
   std::vector<int32_t> nd;       // non-dominated rows (no reference filter)
 
@@ -187,10 +188,15 @@ struct NehviMeansArgs {
   const float* Xs;         // [m][n_pad][dx] scaled training inputs
   const float* invls;      // [m][dx]
   const uint16_t* Gp;      // packed G^T fragments (fp16 bits)
-  float s[3];              // output scales
+  float s[3];              // output scales (composite: of the routing term)
   float ginv[3];           // 1 / scale of G
   float* out;              // [m][S][ldo]
   int64_t ldo;
+  // composite kernel (dr > 0): slot layout, scales and preference weights
+  int dr = 0, dr4 = 0;
+  float s_dep[3] = {0.f, 0.f, 0.f}, s_int[3] = {0.f, 0.f, 0.f};
+  const float* wts = nullptr;    // [m][n_pad] weights of the training points
+  const float* pref = nullptr;   // [m][d - dr] preference slopes
 };
 hipError_t launch_nehvi_means(const NehviMeansArgs& a, int m, hipStream_t st);
 struct NehviEhviArgs {

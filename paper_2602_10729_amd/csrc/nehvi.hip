@@ -228,6 +228,12 @@ __device__ __forceinline__ void lds_sync() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
+__device__ __forceinline__ float m32(float r2) {
+  const float r = __builtin_amdgcn_sqrtf(r2);
+  constexpr float kNegSqrt3Log2e = static_cast<float>(-1.73205080756887729353 * 1.44269504088896340736);
+  return fmaf(r, 1.73205081f, 1.0f) * __builtin_amdgcn_exp2f(kNegSqrt3Log2e * r);
+}
+
 __device__ __forceinline__ float m52(float r2, float s) {
   const float r = __builtin_amdgcn_sqrtf(r2);
   constexpr float kNegSqrt5Log2e = static_cast<float>(-2.23606797749978969641 * 1.44269504088896340736);
@@ -251,11 +257,15 @@ constexpr int kRingSlot = 2 * kPlane;  // hi + lo planes of one 32-row block
 // for the whole tile: wave w owns the sample blocks w + 8r (r < CB), all four
 // candidate blocks. Three products per pair (hi hi, hi lo, lo hi), fp32
 // accumulate. Training rows past the matrix read as zero; their G rows are
-// zero, so they add nothing.
-template <int DX4, int CB>
+// zero, so they add nothing. COMP: the composite kernel
+//   s_route M52(r_route) + s_dep w(c) w(x) M32(r_dep) + s_int M52 M32,
+// the routing coordinates in the first 4 dr4 slots, the training rows'
+// weights staged beside them.
+template <int DX4, int CB, bool COMP>
 __global__ __launch_bounds__(kMW * 64) void k_nehvi_means(NehviMeansArgs a) {
   constexpr int RS = 4 * DX4;
   __shared__ __align__(16) float xst[2][32 * RS];
+  __shared__ float wst[2][32];             // COMP: weights of the staged rows
   __shared__ __align__(16) _Float16 ring[3 * kRingSlot];
   const int k = blockIdx.y;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -268,32 +278,64 @@ __global__ __launch_bounds__(kMW * 64) void k_nehvi_means(NehviMeansArgs a) {
   const __amdgpu_buffer_rsrc_t xs_rs = rsrc(Xs, a.n_pad * a.dx * 4);
   const __amdgpu_buffer_rsrc_t g_rs = rsrc(a.Gp + (int64_t)k * a.n32 * nrb * 1024,
                                            a.n32 * nrb * 2048);
-  // this lane's candidate, scaled (zero past npts and past d)
+  // this lane's candidate, scaled, in the slot layout (zero past npts and in
+  // padding slots); COMP: s_dep times its preference weight
   float cx[RS];
+  float wsd = 0.f;
+  const float sint = COMP ? a.s_int[k] : 0.f;
   {
     const int64_t c = c0 + lane;
     const bool ok = c < a.npts;
 #pragma unroll
-    for (int t = 0; t < RS; ++t)
-      cx[t] = (ok && t < a.d) ? a.cand[c * a.d + t] * il[t] : 0.f;
+    for (int t = 0; t < RS; ++t) {
+      const int cd = slot_dim(t, a.d, a.dr, a.dr4);
+      cx[t] = (ok && cd >= 0) ? a.cand[c * a.d + cd] * il[t] : 0.f;
+    }
+    if constexpr (COMP) {
+      if (ok) {
+        const float* pr = a.pref + (int64_t)k * (a.d - a.dr);
+        float e = 0.f;
+        for (int t = a.dr; t < a.d; ++t) e = fmaf(pr[t - a.dr], a.cand[c * a.d + t], e);
+        wsd = a.s_dep[k] * expf(e);
+      }
+    }
   }
+  const __amdgpu_buffer_rsrc_t w_rs = rsrc(COMP ? a.wts + (int64_t)k * a.n_pad : a.Xs,
+                                           COMP ? a.n_pad * 4 : 0);
+  const int wrow = threadIdx.x - 256;       // COMP: threads 256 .. 287 stage the weights
   // staging: thread t < 32 * DX4 moves one float4 of row t / DX4
   const bool stager = threadIdx.x < 32 * DX4;
   const int srow = stager ? threadIdx.x / DX4 : 0, st4 = threadIdx.x % DX4;
   auto stage_load = [&](int jb) {
-    return ld4(xs_rs, ((jb * 32 + srow) * a.dx + 4 * st4) * 4, 0);
+    float4 v = ld4(xs_rs, ((jb * 32 + srow) * a.dx + 4 * st4) * 4, 0);
+    if constexpr (COMP) {
+      // the weight rides in the thread's fourth float when it stages one
+      if (wrow >= 0 && wrow < 32)
+        v.w = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                                            w_rs, (jb * 32 + wrow) * 4, 0, 0));
+    }
+    return v;
   };
   auto stage_store = [&](int jb, float4 v) {
     if (stager) *reinterpret_cast<float4*>(&xst[jb & 1][srow * RS + 4 * st4]) = v;
+    if constexpr (COMP) {
+      if (wrow >= 0 && wrow < 32) wst[jb & 1][wrow] = v.w;
+    }
   };
   auto produce = [&](int jb) {
     const float* xr = &xst[jb & 1][4 * wave * RS];
     halfx4 hi, lo;
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      float r2 = 0.f;
+      float r2 = 0.f, r2r = 0.f;    // r2r: composite, the routing part
 #pragma unroll
       for (int t4 = 0; t4 < DX4; ++t4) {
+        if constexpr (COMP) {
+          if (t4 == a.dr4) {         // routing slots come first
+            r2r = r2;
+            r2 = 0.f;
+          }
+        }
         const float4 x = *reinterpret_cast<const float4*>(xr + u * RS + 4 * t4);
         const float d0 = cx[4 * t4 + 0] - x.x, d1 = cx[4 * t4 + 1] - x.y;
         const float d2 = cx[4 * t4 + 2] - x.z, d3 = cx[4 * t4 + 3] - x.w;
@@ -302,7 +344,14 @@ __global__ __launch_bounds__(kMW * 64) void k_nehvi_means(NehviMeansArgs a) {
         r2 = fmaf(d2, d2, r2);
         r2 = fmaf(d3, d3, r2);
       }
-      const float kv = m52(r2, sk);
+      float kv;
+      if constexpr (COMP) {
+        const float k5 = m52(r2r, 1.0f);
+        const float k3 = m32(r2);
+        kv = fmaf(wsd * wst[jb & 1][4 * wave + u], k3, k5 * fmaf(sint, k3, sk));
+      } else {
+        kv = m52(r2, sk);
+      }
       const _Float16 h = static_cast<_Float16>(kv);
       hi[u] = h;
       lo[u] = static_cast<_Float16>(kv - static_cast<float>(h));
@@ -569,13 +618,13 @@ hipError_t nz_ehvi_q(const NehviEhviArgs& a, bool ldsb, size_t lds, unsigned gri
   return hipErrorInvalidValue;
 }
 
-template <int DX4>
+template <int DX4, bool COMP>
 hipError_t means_dx(const NehviMeansArgs& a, dim3 grid, hipStream_t st) {
   switch (a.S <= 128 ? 1 : a.S <= 256 ? 2 : a.S <= 384 ? 3 : 4) {
-    case 1: hipLaunchKernelGGL((k_nehvi_means<DX4, 1>), grid, dim3(kMW * 64), 0, st, a); break;
-    case 2: hipLaunchKernelGGL((k_nehvi_means<DX4, 2>), grid, dim3(kMW * 64), 0, st, a); break;
-    case 3: hipLaunchKernelGGL((k_nehvi_means<DX4, 3>), grid, dim3(kMW * 64), 0, st, a); break;
-    default: hipLaunchKernelGGL((k_nehvi_means<DX4, 4>), grid, dim3(kMW * 64), 0, st, a); break;
+    case 1: hipLaunchKernelGGL((k_nehvi_means<DX4, 1, COMP>), grid, dim3(kMW * 64), 0, st, a); break;
+    case 2: hipLaunchKernelGGL((k_nehvi_means<DX4, 2, COMP>), grid, dim3(kMW * 64), 0, st, a); break;
+    case 3: hipLaunchKernelGGL((k_nehvi_means<DX4, 3, COMP>), grid, dim3(kMW * 64), 0, st, a); break;
+    default: hipLaunchKernelGGL((k_nehvi_means<DX4, 4, COMP>), grid, dim3(kMW * 64), 0, st, a); break;
   }
   return hipGetLastError();
 }
@@ -625,15 +674,28 @@ hipError_t launch_nehvi_means(const NehviMeansArgs& a, int m, hipStream_t st) {
   if (a.npts <= 0) return hipSuccess;
   if (a.S < 1 || a.S > 512 || a.dx % 4 != 0 || a.dx > BO_MAX_D) return hipErrorInvalidValue;
   const dim3 grid(static_cast<unsigned>((a.npts + kMT - 1) / kMT), m);
+  if (a.dr > 0) {
+    // a composite model has at least two coordinate groups
+    switch (a.dx / 4) {
+      case 2: return means_dx<2, true>(a, grid, st);
+      case 3: return means_dx<3, true>(a, grid, st);
+      case 4: return means_dx<4, true>(a, grid, st);
+      case 5: return means_dx<5, true>(a, grid, st);
+      case 6: return means_dx<6, true>(a, grid, st);
+      case 7: return means_dx<7, true>(a, grid, st);
+      case 8: return means_dx<8, true>(a, grid, st);
+    }
+    return hipErrorInvalidValue;
+  }
   switch (a.dx / 4) {
-    case 1: return means_dx<1>(a, grid, st);
-    case 2: return means_dx<2>(a, grid, st);
-    case 3: return means_dx<3>(a, grid, st);
-    case 4: return means_dx<4>(a, grid, st);
-    case 5: return means_dx<5>(a, grid, st);
-    case 6: return means_dx<6>(a, grid, st);
-    case 7: return means_dx<7>(a, grid, st);
-    case 8: return means_dx<8>(a, grid, st);
+    case 1: return means_dx<1, false>(a, grid, st);
+    case 2: return means_dx<2, false>(a, grid, st);
+    case 3: return means_dx<3, false>(a, grid, st);
+    case 4: return means_dx<4, false>(a, grid, st);
+    case 5: return means_dx<5, false>(a, grid, st);
+    case 6: return means_dx<6, false>(a, grid, st);
+    case 7: return means_dx<7, false>(a, grid, st);
+    case 8: return means_dx<8, false>(a, grid, st);
   }
   return hipErrorInvalidValue;
 }

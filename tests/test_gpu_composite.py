@@ -82,10 +82,6 @@ def test_composite_bad_arguments():
     X, Y = to_dev(wl.X), to_dev(wl.Y)
     model = bo.fit_composite(X, Y, comp.d_route, wl.lengthscale, comp.s_route, comp.s_dep,
                              comp.s_int, comp.pref, wl.noise)
-    # the noisy acquisition takes Matern-5/2 models only
-    with pytest.raises(bo.BoError) as ei:
-        bo.nehvi_prepare(model, to_dev(np.zeros((8, wl.n, wl.m), np.float32)), wl.ref)
-    assert ei.value.name == "BO_ERR_INVALID_ARGUMENT"
     for dr in (0, wl.d):
         with pytest.raises(bo.BoError) as ei:
             bo.fit_composite(X, Y, dr, wl.lengthscale, comp.s_route, comp.s_dep, comp.s_int,

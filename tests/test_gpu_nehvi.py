@@ -21,11 +21,14 @@ def _announce(*a):
     print("[case]", *a, flush=True)
 
 
-def _gpu(wl, cand, ZX, Zs, ref=None, lower=None, model=None):
+def _gpu(wl, cand, ZX, Zs, ref=None, lower=None, model=None, comp=None):
     import torch
     import paper_2602_10729_amd as bo
-    if model is None:
+    if model is None and comp is None:
         model = bo.fit(to_dev(wl.X), to_dev(wl.Y), wl.lengthscale, wl.outputscale, wl.noise)
+    elif model is None:
+        model = bo.fit_composite(to_dev(wl.X), to_dev(wl.Y), comp.d_route, wl.lengthscale,
+                                 comp.s_route, comp.s_dep, comp.s_int, comp.pref, wl.noise)
     bo.nehvi_prepare(model, to_dev(ZX), wl.ref if ref is None else ref, lower=lower)
     e = bo.score_nehvi(model, to_dev(np.ascontiguousarray(cand)), to_dev(np.ascontiguousarray(Zs)))
     idx, val = bo.argmax(e)
@@ -175,15 +178,10 @@ def test_noisy_reprepare_and_edges():
     big = np.zeros((513, wl.n, 2), dtype=np.float32)
     with pytest.raises(bo.BoError, match="CAPACITY"):
         bo.nehvi_prepare(model, to_dev(big), wl.ref)
-    # batches of three and composite-kernel models are not supported
+    # batches of three are not supported
     with pytest.raises(bo.BoError, match="INVALID_ARGUMENT"):
         bo.score_nehvi(model, to_dev(np.ascontiguousarray(wl.cand[:6, 0, :].reshape(2, 3, -1))),
                        to_dev(np.zeros((64, 3, 2), np.float32)))
-    comp = bi.composite_hyperparameters(wl)
-    mc = bo.fit_composite(to_dev(wl.X), to_dev(wl.Y), comp.d_route, wl.lengthscale, comp.s_route,
-                          comp.s_dep, comp.s_int, comp.pref, wl.noise)
-    with pytest.raises(bo.BoError, match="INVALID_ARGUMENT"):
-        bo.nehvi_prepare(mc, to_dev(ZX), wl.ref)
     torch.cuda.synchronize()
 
 
@@ -261,3 +259,41 @@ def test_noisy_three_objectives_constrained():
     assert exact.mean() > 0.3, exact.mean()
     assert_close(g["ehvi"][exact], o["ehvi"][exact], TOL_EHVI, "constrained nehvi (unambiguous)")
     _check_fronts(g, o, wl.ref, lower, range(0, 256, 32))
+
+
+@pytest.mark.parametrize("cfg,M,q,seed,d_route,cons", [(2, 1500, 1, 0, None, False),
+                                                       (0, 400, 2, 1, 2, False),
+                                                       (4, 40, 4, 0, None, False),
+                                                       (2, 800, 1, 2, None, True)])
+def test_noisy_composite_kernel(cfg, M, q, seed, d_route, cons):
+    """The paper's surrogate (composite kernel) inside its acquisition (the
+    noisy form, optionally constrained)."""
+    _announce("nehvi composite", cfg, M, q, seed, d_route, cons)
+    wl = bi.make_config(cfg, seed=seed, M=M * q if q != wl_q(cfg) else M)
+    comp = bi.composite_hyperparameters(wl, d_route)
+    S = 256 if cfg == 4 else None
+    ZX = bi.insample_base_samples(wl, S)
+    if q == 1:
+        cand, Zs = np.ascontiguousarray(wl.cand[:M, 0, :]), np.ascontiguousarray(wl.Z[:, 0, :])
+        if S is not None:
+            Zs = Zs[:S]
+    else:
+        cand, Zs = _batched(wl, ZX, M, q, seed)
+    lower = bi.feasibility_thresholds(wl, 0.3) if cons else None
+    g = _gpu(wl, cand, ZX, Zs, lower=lower, comp=comp)
+    om = oracle_fit(wl, comp)
+    o = _oracle(wl, cand, ZX, Zs, lower=lower, model=om)
+    if not cons:
+        assert_close(g["ehvi"], o["ehvi"], TOL_EHVI, "nehvi composite")
+        check_argmax(g["idx"], o["ehvi"])
+    else:
+        lo, hi = _noisy_constrained_bounds(om, cand, ZX, Zs.astype(np.float64), o, lower)
+        assert_within_bounds(g["ehvi"], lo, hi, TOL_EHVI, "constrained nehvi composite")
+        exact = lo == hi
+        assert exact.mean() > 0.5, exact.mean()
+        assert_close(g["ehvi"][exact], o["ehvi"][exact], TOL_EHVI, "constrained nehvi composite")
+    _check_fronts(g, o, wl.ref, lower, range(0, ZX.shape[0], max(1, ZX.shape[0] // 8)))
+
+
+def wl_q(cfg):
+    return bi.CONFIGS[cfg]["q"]
