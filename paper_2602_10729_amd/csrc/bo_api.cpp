@@ -215,8 +215,11 @@ void release_noisy(Model* M) {
 void release_buffers(Model* M) {
   release_noisy(M);
   if (M->Xs || M->invls || M->alpha || M->Lp || M->ws || M->d_boxes || M->wts || M->pref ||
-      M->Xd)
+      M->Xd || M->xf || M->x2 || M->ctr)
     (void)hipDeviceSynchronize();
+  pfree(M->xf, nullptr);
+  pfree(M->x2, nullptr);
+  pfree(M->ctr, nullptr);
   pfree(M->Xd, nullptr);
   pfree(M->Xs, nullptr);
   pfree(M->invls, nullptr);
@@ -434,6 +437,9 @@ bo_status fit_impl(const char* who, const float* X, const float* Y, int64_t n, i
   if ((s = palloc(&M->alpha, (size_t)m * M->n_pad, st, "alpha")) != BO_OK) return bail(s);
   if ((s = palloc(&M->Lp, (size_t)m * M->lp_per_obj, st, "packed inverse")) != BO_OK) return bail(s);
   if ((s = palloc(&M->Xd, (size_t)n * d, st, "training inputs")) != BO_OK) return bail(s);
+  if ((s = palloc(&M->xf, (size_t)m * M->nb * dist_frags(M->dx) * 512, st, "distance fragments")) != BO_OK) return bail(s);
+  if ((s = palloc(&M->x2, (size_t)m * 2 * M->n_pad, st, "row norms")) != BO_OK) return bail(s);
+  if ((s = palloc(&M->ctr, (size_t)m * M->dx, st, "coordinate centre")) != BO_OK) return bail(s);
   if (comp) {
     if ((s = palloc(&M->wts, (size_t)m * M->n_pad, st, "preference weights")) != BO_OK) return bail(s);
     if ((s = palloc(&M->pref, (size_t)m * dc, st, "preference slopes")) != BO_OK) return bail(s);
@@ -510,6 +516,7 @@ bo_status fit_impl(const char* who, const float* X, const float* Y, int64_t n, i
   if ((s = after_launch(launch_cholesky(fs.A, fs.W, nf, m, fs.flag, st), st, "cholesky")) != BO_OK) return bail(s);
   if ((s = after_launch(launch_alpha(fs.W, Y, n, m, nf, M->n_pad, fs.tmp, M->alpha, st), st, "alpha")) != BO_OK) return bail(s);
   if ((s = after_launch(launch_pack(fs.W, n, m, nf, M->nb, M->Lp, X, d, M->dx, dr, dr4, M->invls, M->Xs, st), st, "pack")) != BO_OK) return bail(s);
+  if ((s = after_launch(launch_pack_x(M->Xs, n, m, M->nb, M->dx, dr4, M->ctr, M->xf, M->x2, st), st, "pack X")) != BO_OK) return bail(s);
 
   // one synchronisation: the positive-definiteness flag and Y (for the front
   // and its finiteness check) come back together
@@ -819,6 +826,9 @@ bo_status bo_score_constrained(bo_model model, const float* cand, int64_t M_, in
     pa.invls = M.invls + (size_t)k * M.dx;
     pa.alpha = M.alpha + (size_t)k * M.n_pad;
     pa.Lp = M.Lp + (size_t)k * M.lp_per_obj;
+    pa.xf = M.xf + (size_t)k * M.nb * dist_frags(M.dx) * 512;
+    pa.x2 = M.x2 + (size_t)k * 2 * M.n_pad;
+    pa.ctr = M.ctr + (size_t)k * M.dx;
     pa.n = static_cast<int>(M.n); pa.nb = M.nb;
     pa.s = M.os[k];
     pa.m = m; pa.k = k;
@@ -1223,6 +1233,9 @@ bo_status score_nehvi_impl(bo_model model, const float* cand, int64_t M_, int32_
       pa.invls = M.invls + (size_t)k * M.dx;
       pa.alpha = M.alpha + (size_t)k * M.n_pad;
       pa.Lp = z.Lp0 + (size_t)k * M.lp_per_obj;
+      pa.xf = M.xf + (size_t)k * M.nb * dist_frags(M.dx) * 512;
+      pa.x2 = M.x2 + (size_t)k * 2 * M.n_pad;
+      pa.ctr = M.ctr + (size_t)k * M.dx;
       pa.n = static_cast<int>(M.n); pa.nb = M.nb;
       pa.s = M.os[k];
       pa.m = m; pa.k = k;

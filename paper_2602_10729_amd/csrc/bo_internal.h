@@ -54,6 +54,9 @@ struct Model {
   float* pref = nullptr;         // composite: [m][d - dr] preference slopes
   float* Lp = nullptr;           // [m][frag blocks][2 KiB] packed fp16 hi/lo L^{-1} + zero block
   size_t lp_per_obj = 0;         // floats per objective in Lp
+  uint16_t* xf = nullptr;        // [m][nb][dist_frags(dx)][512] distance fragments of X
+  float* x2 = nullptr;           // [m][2][n_pad] squared norms of the centred rows
+  float* ctr = nullptr;          // [m][dx] centre of the scaled coordinates
 
   // scoring workspace (grown on demand)
   float* ws = nullptr;
@@ -136,6 +139,23 @@ hipError_t launch_mll(const float* X, int64_t n, int d, int m, int nf, const Gra
 hipError_t launch_pack(const double* W, int64_t n, int m, int nf, int nb,
                        float* Lp, const float* X, int d, int dx, int dr, int dr4,
                        const float* invls, float* Xs, hipStream_t st);
+
+// Squared distances in the posterior kernel come from the expansion
+// |c|^2 + |x|^2 - 2 c.x of centred scaled coordinates, with c.x on the fp16
+// matrix cores: each value splits into hi = fp16(v) and lo = fp16(2^11 (v -
+// hi)); one accumulator takes sum x_hi c_hi over the D = dx slots (stream 0),
+// another sum x_lo c_hi + x_hi c_lo over 2D positions (stream 1), and c.x =
+// acc0 + 2^-11 acc1. Fragments of 32 k-positions per 16-row group: stream 0
+// first, then stream 1.
+__host__ __device__ constexpr int dist_frags0(int dx) { return (dx + 31) / 32; }
+__host__ __device__ constexpr int dist_frags(int dx) { return (dx + 31) / 32 + (2 * dx + 31) / 32; }
+constexpr float kDistLoScale = 2048.0f;
+// Centre the scaled coordinates (ctr = mean over the n rows), then write the
+// A fragments of the centred rows (xf, zero for rows past n) and their
+// squared norms per coordinate group (x2 [2][n_pad]: routing slots t < 4*dr4,
+// then the rest; a plain model has everything in the second group).
+hipError_t launch_pack_x(const float* Xs, int64_t n, int m, int nb, int dx, int dr4,
+                         float* ctr, uint16_t* xf, float* x2, hipStream_t st);
 
 // Noisy acquisition, fp64 preparation (fit.hip).
 // A holds K^{-1} in its lower 64-blocks on return (from W = L^{-1}).
@@ -246,6 +266,9 @@ struct PosteriorArgs {
   const float* invls;  // [dx]
   const float* alpha;  // [n_pad]
   const float* Lp;     // packed fragments of this objective
+  const uint16_t* xf;  // [nb][dist_frags(dx)][512] centred-X distance fragments
+  const float* x2;     // [2][n_pad] squared norms of the centred rows per coordinate group
+  const float* ctr;    // [dx] centre subtracted from the scaled coordinates
   int n, nb;
   float s;             // output scale (composite: of the routing term)
   int m, k;            // objective count / index (output strides)

@@ -526,6 +526,87 @@ __global__ __launch_bounds__(256) void k_scale_x(const float* __restrict__ X, in
   Xs[(int64_t)k * n_pad * dx + e] = v;
 }
 
+// ctr[k][t] = mean over the n rows of Xs[k][i][t] (fp64 sum, fp32 result):
+// one block per (coordinate t, objective k), rows strided over the threads,
+// then a tree sum in LDS
+__global__ __launch_bounds__(256) void k_center_x(const float* __restrict__ Xs, int64_t n,
+                                                  int n_pad, int dx, float* __restrict__ ctr) {
+  __shared__ double part[256];
+  const int t = blockIdx.x, k = blockIdx.y;
+  const float* x = Xs + (int64_t)k * n_pad * dx + t;
+  double acc = 0.0;
+  for (int64_t i = threadIdx.x; i < n; i += 256) acc += x[i * dx];
+  part[threadIdx.x] = acc;
+  __syncthreads();
+  for (int h = 128; h > 0; h >>= 1) {
+    if (static_cast<int>(threadIdx.x) < h) part[threadIdx.x] += part[threadIdx.x + h];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) ctr[k * dx + t] = static_cast<float>(part[0] / static_cast<double>(n));
+}
+
+// One thread per (row group g, fragment f, lane l): the eight fp16 values of
+// the A fragment of v_mfma_f32_16x16x32_f16 that lane l supplies (row 16g +
+// l%16, positions 8(l/16) .. +7 of the fragment's 32), from the centred row
+// xc = Xs - ctr: stream 0 holds hi(xc[p]) at p < dx, stream 1 lo(xc[p]) at
+// p < dx and hi(xc[p - dx]) at dx <= p < 2dx; zero elsewhere and for rows
+// past n.
+__global__ __launch_bounds__(256) void k_pack_x(const float* __restrict__ Xs, int64_t n,
+                                                int n_pad, int nb, int dx,
+                                                const float* __restrict__ ctr,
+                                                _Float16* __restrict__ xf) {
+  const int k = blockIdx.y;
+  const int nf = dist_frags(dx), f0 = dist_frags0(dx);
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= (int64_t)nb * nf * 64) return;
+  const int l = static_cast<int>(idx % 64);
+  const int f = static_cast<int>((idx / 64) % nf);
+  const int64_t g = idx / (64 * nf);
+  const int64_t i = 16 * g + (l & 15);
+  const float* x = Xs + ((int64_t)k * n_pad + i) * dx;
+  const float* c = ctr + k * dx;
+  _Float16* dst = xf + (((int64_t)k * nb + g) * nf + f) * 512 + l * 8;
+  for (int e = 0; e < 8; ++e) {
+    const int p = 32 * (f < f0 ? f : f - f0) + 8 * (l >> 4) + e;
+    _Float16 v = static_cast<_Float16>(0.0f);
+    if (i < n) {
+      if (f < f0) {
+        if (p < dx) v = static_cast<_Float16>(x[p] - c[p]);
+      } else if (p < dx) {
+        const float xc = x[p] - c[p];
+        const _Float16 h = static_cast<_Float16>(xc);
+        v = static_cast<_Float16>((xc - static_cast<float>(h)) * kDistLoScale);
+      } else if (p < 2 * dx) {
+        v = static_cast<_Float16>(x[p - dx] - c[p - dx]);
+      }
+    }
+    dst[e] = v;
+  }
+}
+
+// x2[k][0][i] = sum over routing slots (t < 4*dr4) of (Xs - ctr)^2, x2[k][1][i]
+// over the others, both fp32 in slot order; zero for rows past n
+__global__ __launch_bounds__(256) void k_norm_x(const float* __restrict__ Xs, int64_t n,
+                                                int n_pad, int dx, int dr4,
+                                                const float* __restrict__ ctr,
+                                                float* __restrict__ x2) {
+  const int k = blockIdx.y;
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n_pad) return;
+  float g0 = 0.f, g1 = 0.f;
+  if (i < n) {
+    const float* x = Xs + ((int64_t)k * n_pad + i) * dx;
+    const float* c = ctr + k * dx;
+    for (int t = 0; t < dx; ++t) {
+      const float v = x[t] - c[t];
+      if (t < 4 * dr4) g0 = fmaf(v, v, g0);
+      else g1 = fmaf(v, v, g1);
+    }
+  }
+  x2[((int64_t)k * 2 + 0) * n_pad + i] = g0;
+  x2[((int64_t)k * 2 + 1) * n_pad + i] = g1;
+}
+
 // ---- log marginal likelihood and its gradient ------------------------------
 //
 // value = -1/2 y^T K^{-1} y - sum_i log L_ii - n/2 log(2 pi), with
@@ -843,6 +924,19 @@ hipError_t launch_pack(const double* W, int64_t n, int m, int nf, int nb, float*
   const unsigned gx2 = static_cast<unsigned>(((int64_t)n_pad * dx + 255) / 256);
   hipLaunchKernelGGL(k_scale_x, dim3(gx2, m), dim3(256), 0, st, X, n, d, dx, dr, dr4, n_pad,
                      invls, Xs);
+  return hipGetLastError();
+}
+
+hipError_t launch_pack_x(const float* Xs, int64_t n, int m, int nb, int dx, int dr4,
+                         float* ctr, uint16_t* xf, float* x2, hipStream_t st) {
+  if (dx > 64 || n < 1) return hipErrorInvalidValue;
+  const int n_pad = nb * kBlk;
+  hipLaunchKernelGGL(k_center_x, dim3(dx, m), dim3(256), 0, st, Xs, n, n_pad, dx, ctr);
+  const int64_t th = (int64_t)nb * dist_frags(dx) * 64;
+  hipLaunchKernelGGL(k_pack_x, dim3(static_cast<unsigned>((th + 255) / 256), m), dim3(256), 0, st,
+                     Xs, n, n_pad, nb, dx, ctr, reinterpret_cast<_Float16*>(xf));
+  hipLaunchKernelGGL(k_norm_x, dim3(static_cast<unsigned>((n_pad + 255) / 256), m), dim3(256), 0,
+                     st, Xs, n, n_pad, dx, dr4, ctr, x2);
   return hipGetLastError();
 }
 

@@ -126,129 +126,156 @@ __host__ __device__ __forceinline__ int frag_row_start(int I) {
   return (I & 1) ? (t + 1) * (t + 1) : t * (t + 1);
 }
 
-// Per-lane state of the K*^T producer. A wave makes NT/8 columns of each
-// 32-row block; lane l takes column l % CPW and RPL = CPW/2 consecutive rows.
+typedef _Float16 halfx4 __attribute__((ext_vector_type(4)));
+
+// Per-lane state of the K*^T producer. Wave w makes rows 16(w/4) .. +15 and
+// columns 16(w%4) .. +15 of every 32-row block, in the MFMA result layout:
+// lane l holds column 16(w%4) + l%16 and rows 16(w/4) + 4(l/16) .. +3.
+//
+// Squared distances: r^2 = |c|^2 + |x|^2 - 2 c.x over coordinates centred on
+// the training mean, c.x on the matrix cores from fp16 hi and 2^11-scaled lo
+// halves (the fit packs the rows, the kernel the candidates; two accumulator
+// streams, see dist_frags). Where the expansion can cancel badly, i.e. for a
+// pair whose approximate r^2 is below 1 + (|c|^2 + |x|^2)/256, the pair is
+// recomputed from exact differences of the scaled coordinates: near a
+// training point k(x*, x_i) is close to its maximum and sigma^2 cancels,
+// elsewhere the expansion's error (about 2^-20 (|c|^2 + |x|^2)) changes sigma
+// by far less than its fp32 rounding. The choice is made per pair, so a
+// point's result does not depend on its neighbours in the tile.
+// Composite kernel: one expansion per coordinate group (routing slots first,
+// then deployment), the candidate fragments masked to the group; the test
+// above uses the total over both groups.
 template <int NT, int DX4, bool COMP>
 struct Producer {
-  static constexpr int CPW = NT / kWaves;
-  static constexpr int RPL = kJ * CPW / 64;
-  float c[DX4 * 4];         // scaled candidate coordinates (slot layout)
-  bool valid;
+  static constexpr int D = 4 * DX4;
+  static constexpr int F0 = dist_frags0(D);
+  static constexpr int NF = dist_frags(D);
+  static constexpr int NS = COMP ? 2 : 1;
+  static_assert(F0 == 1 && NF <= 3, "at most 32 coordinate slots");
+  halfx8 cb[NS][NF];        // B fragments of this lane's candidate, per group
+  float c2[NS];             // squared norm of the centred candidate, per group
   float mu;
   float wsd;                // composite: s_dep * w(candidate)
   int col;                  // tile column of this lane
-  int row0;                 // first row of this lane inside a block
+  int rq;                   // first of this lane's rows inside a block
+  int half;                 // row half of this wave
+  // operands of the block made at the next step, loaded a step ahead
+  halfx8 xa[NF];
+  floatx4 x2[NS], al, wt;
+  __amdgpu_buffer_rsrc_t xf_rs, x2_rs, al_rs, wt_rs, xs_rs;
 };
 
-// Training rows staged in LDS, one 32-row block per slot, four slots: row
-// r of block b at slot b % 4 (position stage_pos(r)), [kJ][dx + 4] floats
-// per slot, the last float4
-// of a row holding (alpha, w, 0, 0), w the preference weight of the row
-// (composite kernel; 0 otherwise). Step J loads the rows of block J + 4
-// first and stores them last, while the producer reads block J + 2. Every
-// thread issues the same loads (a spare thread's store goes to a scratch
-// float4), so no branch makes the compiler drain the loads in flight.
-template <int DX4, bool COMP>
-struct Stager {
-  static constexpr int RS = DX4 * 4 + 4;                 // row stride (floats)
-  static constexpr int kF4 = kJ * (DX4 + 1);             // float4s per block
-  static constexpr int kSlot = kJ * RS;                  // floats per slot
-  static_assert(kF4 <= kThreads, "one float4 per thread");
-  float4 x;                 // the loads in flight (selected at the store,
-  float al, wt;             // so the loads are not waited for early)
-  int soff;                 // this thread's float offset inside a slot (-1: spare thread)
-  int row, t4;
-  __amdgpu_buffer_rsrc_t xs_rs, al_rs, wt_rs;
-};
-
-// Position of staged row r inside its slot: rows are interleaved so that the
-// producer's lane groups, which read rows g*RPL + u (g = 0 .. kJ/RPL - 1) at
-// the same time, find them kJ/RPL positions apart in consecutive row
-// positions; with an odd number of float4s per row the groups' reads then
-// fall in distinct LDS bank groups (contiguous rows would collide 4 ways).
-template <int RPL>
-__device__ __forceinline__ int stage_pos(int r) {
-  return (r % RPL) * (kJ / RPL) + r / RPL;
+// Load the operands of block jb (rows past the packed arrays read zero).
+template <int NT, int DX4, bool COMP>
+__device__ __forceinline__ void prod_load(Producer<NT, DX4, COMP>& P, int n_pad, int jb, int lane) {
+  using Pr = Producer<NT, DX4, COMP>;
+  const int vo = (2 * jb + P.half) * (Pr::NF * 1024) + lane * 16;
+#pragma unroll
+  for (int f = 0; f < Pr::NF; ++f)
+    P.xa[f] = __builtin_bit_cast(halfx8, load4(P.xf_rs, vo + f * 1024, 0));
+  const int row = jb * kJ + P.rq;
+#pragma unroll
+  for (int g = 0; g < Pr::NS; ++g)
+    P.x2[g] = __builtin_bit_cast(floatx4, load4(P.x2_rs, ((COMP ? g : 1) * n_pad + row) * 4, 0));
+  P.al = __builtin_bit_cast(floatx4, load4(P.al_rs, row * 4, 0));
+  if constexpr (COMP) P.wt = __builtin_bit_cast(floatx4, load4(P.wt_rs, row * 4, 0));
 }
 
-// Rows past n_pad read zeros (buffer range check), so blocks past the matrix
-// that the producer may evaluate carry zero alpha and add nothing to mu.
-template <int DX4, bool COMP>
-__device__ __forceinline__ void stage_load(Stager<DX4, COMP>& S, const PosteriorArgs& a, int jb) {
-  const int row = jb * kJ + S.row;
-  S.x = load4(S.xs_rs, (row * a.dx + 4 * min(S.t4, DX4 - 1)) * 4, 0);
-  S.al = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(S.al_rs, row * 4, 0, 0));
-  if constexpr (COMP)
-    S.wt = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(S.wt_rs, row * 4, 0, 0));
-}
-
-template <int DX4, bool COMP>
-__device__ __forceinline__ void stage_store(const Stager<DX4, COMP>& S, float* xst, int jb) {
-  const bool is_al = S.t4 == DX4;
-  const float wt = COMP ? S.wt : 0.f;
-  const float4 v{is_al ? S.al : S.x.x, is_al ? wt : S.x.y, is_al ? 0.f : S.x.z,
-                 is_al ? 0.f : S.x.w};
-  // a spare thread writes the scratch float4 after the four slots (at a fixed
-  // place, whatever the slot)
-  constexpr int kSlot = Stager<DX4, COMP>::kSlot;
-  const int off = (S.soff < 0) ? 4 * kSlot : (jb & 3) * kSlot + S.soff;
-  *reinterpret_cast<float4*>(xst + off) = v;
-}
-
-// Evaluate this lane's rows of block jb into the ring as fp16 hi/lo planes,
-// reading the training rows from jb's staging slot.
+// Evaluate this lane's four rows of block jb (operands loaded by prod_load)
+// into the ring as fp16 hi/lo planes. ctile: the tile's exact scaled
+// candidate coordinates [NT][D].
 template <int NT, int DX4, bool COMP>
 __device__ __forceinline__ void produce(Producer<NT, DX4, COMP>& P, const PosteriorArgs& a, int jb,
-                                        const float* xst, _Float16* ring) {
-  constexpr int RPL = Producer<NT, DX4, COMP>::RPL;
-  constexpr int RS = Stager<DX4, COMP>::RS;
-  typedef _Float16 halfr __attribute__((ext_vector_type(RPL)));
-  halfr hi, lo;
-  // staged rows are interleaved (see stage_pos): this lane's row row0 + u
-  // sits at position u * (kJ / RPL) + row0 / RPL
-  constexpr int US = (kJ / RPL) * RS;
-  const float* xr = xst + (jb & 3) * Stager<DX4, COMP>::kSlot + (P.row0 / RPL) * RS;
+                                        const float* ctile, _Float16* ring) {
+  using Pr = Producer<NT, DX4, COMP>;
+  constexpr int NS = Pr::NS, F0 = Pr::F0, NF = Pr::NF;
+  floatx4 d0[NS], d1[NS];
 #pragma unroll
-  for (int u = 0; u < RPL; ++u) {
-    float r2 = 0.f, r2r = 0.f;    // r2r: composite, the routing part
+  for (int g = 0; g < NS; ++g) {
+    d0[g] = floatx4{0.f, 0.f, 0.f, 0.f};
+    d1[g] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int t4 = 0; t4 < DX4; ++t4) {
-      if constexpr (COMP) {
-        // routing slots come first: restart the sum where deployment begins
-        if (t4 == a.dr4) {
-          r2r = r2;
-          r2 = 0.f;
+    for (int f = 0; f < F0; ++f)
+      d0[g] = __builtin_amdgcn_mfma_f32_16x16x32_f16(P.xa[f], P.cb[g][f], d0[g], 0, 0, 0);
+#pragma unroll
+    for (int f = F0; f < NF; ++f)
+      d1[g] = __builtin_amdgcn_mfma_f32_16x16x32_f16(P.xa[f], P.cb[g][f], d1[g], 0, 0, 0);
+  }
+  float r2[NS][4];
+  bool ex[4];
+  bool any = false;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    float rt = 0.f, nt = 0.f;
+#pragma unroll
+    for (int g = 0; g < NS; ++g) {
+      const float nrm = P.c2[g] + P.x2[g][e];
+      const float dot = fmaf(d1[g][e], 1.0f / kDistLoScale, d0[g][e]);
+      r2[g][e] = fmaxf(fmaf(-2.0f, dot, nrm), 0.f);
+      rt += r2[g][e];
+      nt += nrm;
+    }
+    ex[e] = rt < fmaf(nt, 1.0f / 256.0f, 1.0f);
+    any = any || ex[e];
+  }
+  if (__builtin_amdgcn_ballot_w64(any) != 0) {
+    // exact differences for the pairs that need them (rows past n_pad read
+    // zero coordinates)
+    const float* cx = ctile + P.col * Pr::D;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int row = jb * kJ + P.rq + e;
+      float s0 = 0.f, s1 = 0.f;   // routing / deployment (plain: s1 only)
+#pragma unroll
+      for (int t4 = 0; t4 < DX4; ++t4) {
+        const float4 x = load4(P.xs_rs, (row * a.dx + 4 * t4) * 4, 0);
+        const float4 c = *reinterpret_cast<const float4*>(cx + 4 * t4);
+        const float e0 = c.x - x.x, e1 = c.y - x.y, e2 = c.z - x.z, e3 = c.w - x.w;
+        float t = fmaf(e0, e0, 0.f);
+        t = fmaf(e1, e1, t);
+        t = fmaf(e2, e2, t);
+        t = fmaf(e3, e3, t);
+        if (COMP && t4 < a.dr4) s0 += t;
+        else s1 += t;
+      }
+      if (ex[e]) {
+        if constexpr (COMP) {
+          r2[0][e] = s0;
+          r2[1][e] = s1;
+        } else {
+          r2[0][e] = s1;
         }
       }
-      const float4 x = *reinterpret_cast<const float4*>(xr + u * US + 4 * t4);
-      const float d0 = P.c[4 * t4 + 0] - x.x;
-      const float d1 = P.c[4 * t4 + 1] - x.y;
-      const float d2 = P.c[4 * t4 + 2] - x.z;
-      const float d3 = P.c[4 * t4 + 3] - x.w;
-      r2 = fmaf(d0, d0, r2);
-      r2 = fmaf(d1, d1, r2);
-      r2 = fmaf(d2, d2, r2);
-      r2 = fmaf(d3, d3, r2);
     }
-    // no mask: rows past n (zero coordinates) meet zero columns of L^{-1}
-    // and zero alpha; columns past the batch are never written
+  }
+  halfx4 hi, lo;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    // no mask: rows past n meet zero columns of L^{-1} and zero alpha;
+    // columns past the batch are never written
     float kv;
     if constexpr (COMP) {
       // s_route M52(r_route) + s_dep w* w_i M32(r_dep) + s_int M52 M32
-      const float k5 = matern52_f(r2r, 1.0f);
-      const float k3 = matern32_f(r2);
-      kv = fmaf(P.wsd * xr[u * US + 4 * DX4 + 1], k3, k5 * fmaf(a.s_int, k3, a.s));
+      const float k5 = matern52_f(r2[0][e], 1.0f);
+      const float k3 = matern32_f(r2[1][e]);
+      kv = fmaf(P.wsd * P.wt[e], k3, k5 * fmaf(a.s_int, k3, a.s));
     } else {
-      kv = matern52_f(r2, a.s);
+      kv = matern52_f(r2[0][e], a.s);
     }
-    P.mu = fmaf(xr[u * US + 4 * DX4], kv, P.mu);
+    // kv is rounded to fp32 here, once: otherwise the compiler may fuse its
+    // last product into the fp16 conversions and derive the high half twice
+    // (once exactly, once from the fp32 value); within an fp32 ulp of an
+    // fp16 rounding midpoint the stored high and low halves then disagree by
+    // one fp16 ulp
+    asm volatile("" : "+v"(kv));
+    P.mu = fmaf(P.al[e], kv, P.mu);
     const _Float16 h = static_cast<_Float16>(kv);
-    hi[u] = h;
-    lo[u] = static_cast<_Float16>(kv - static_cast<float>(h));
+    hi[e] = h;
+    lo[e] = static_cast<_Float16>(kv - static_cast<float>(h));
   }
-  _Float16* dst = ring + P.col * kCSH + (jb % kRing) * kJ + P.row0;
-  *reinterpret_cast<halfr*>(dst) = hi;
-  *reinterpret_cast<halfr*>(dst + NT * kCSH) = lo;
+  _Float16* dst = ring + P.col * kCSH + (jb % kRing) * kJ + P.rq;
+  *reinterpret_cast<halfx4*>(dst) = hi;
+  *reinterpret_cast<halfx4*>(dst + NT * kCSH) = lo;
 }
 
 // Row block of slot r in the pass starting at row block `base`.
@@ -318,7 +345,7 @@ struct Ctx {
   int poff;                 // the block produced at step J is J + poff (this pass)
   int voff;                 // this lane's byte offset inside a fragment plane
   const _Float16* Kb;       // this lane's B-fragment base inside the ring
-  float* xst;               // training-row staging (4 blocks)
+  const float* ctile;       // the tile's exact scaled candidate coordinates [NT][D]
 };
 
 // B fragments of half h of block J: columns (2h + b)*16 + lane%16, rows
@@ -343,17 +370,13 @@ __device__ __forceinline__ void load_b(const Ctx& C, int J, int h, BHalf& B) {
 // published by the previous step's, so its B fragments can be read early.
 template <int LO, int RB, int NT, int DX4, bool COMP, bool PROD>
 __device__ __forceinline__ void step(const Ctx& C, const PosteriorArgs& a, Producer<NT, DX4, COMP>& P,
-                                     Stager<DX4, COMP>& S, _Float16* ring, const Slots<RB>& sl, int J,
+                                     _Float16* ring, const Slots<RB>& sl, int J,
                                      BHalf& B0, AFrag (&av)[RB], floatx4 (&acc)[RB][NT / 16]) {
   constexpr int NCB = NT / 16;
   static_assert(NCB == 4, "two halves of two column blocks");
-  // the staging load goes first among the step's loads and its store last,
-  // so the store waits for it alone, a whole step after it was issued
-  stage_load(S, a, J + C.poff + 2);
-  __builtin_amdgcn_sched_barrier(0);
   BHalf B1;
   load_b<NT>(C, J, 1, B1);
-  if constexpr (PROD) produce(P, a, J + C.poff, C.xst, ring);
+  if constexpr (PROD) produce(P, a, J + C.poff, C.ctile, ring);
   // slot pairs in turn, each pair's fragments for J + 1 requested as soon as
   // its MFMAs are issued (about half a step before the next step needs them);
   // the next block's first B half is read once the last pair is done with it
@@ -371,8 +394,9 @@ __device__ __forceinline__ void step(const Ctx& C, const PosteriorArgs& a, Produ
     // interleave: the scheduler otherwise runs the producer's VALU work and
     // the MFMAs as two separate stretches, and the two waves of a SIMD
     // (kept in step by the barriers) then contend for the same unit
-    constexpr int nM = 3 * NCB * (RB - LO);
-    constexpr int nV = Producer<NT, DX4, COMP>::RPL * (2 * 4 * DX4 + (COMP ? 24 : 14));
+    using Pr = Producer<NT, DX4, COMP>;
+    constexpr int nM = 3 * NCB * (RB - LO) + Pr::NS * Pr::NF;
+    constexpr int nV = 4 * (COMP ? 40 : 22);
     if constexpr (nM > 0) {
 #pragma unroll
       for (int i = 0; i < nM; ++i) {
@@ -382,7 +406,8 @@ __device__ __forceinline__ void step(const Ctx& C, const PosteriorArgs& a, Produ
     }
   }
   __builtin_amdgcn_sched_barrier(0);
-  stage_store(S, C.xst, J + C.poff + 2);
+  // operands of the next step's block
+  prod_load(P, C.n_pad, J + 1 + C.poff, C.tid & 63);
   lds_barrier();
 }
 
@@ -390,14 +415,14 @@ __device__ __forceinline__ void step(const Ctx& C, const PosteriorArgs& a, Produ
 // block J + poff lies in the pass's production window [pw0, pw1).
 template <int LO, int RB, int NT, int DX4, bool COMP>
 __device__ __forceinline__ void span(const Ctx& C, const PosteriorArgs& a, Producer<NT, DX4, COMP>& P,
-                                     Stager<DX4, COMP>& S, _Float16* ring, const Slots<RB>& sl, int j0,
+                                     _Float16* ring, const Slots<RB>& sl, int j0,
                                      int j1, int pw0, int pw1, BHalf& B0, AFrag (&av)[RB],
                                      floatx4 (&acc)[RB][NT / 16]) {
   const int p0 = min(max(pw0 - C.poff, j0), j1), p1 = min(max(pw1 - C.poff, p0), j1);
   int J = j0;
-  for (; J < p0; ++J) step<LO, RB, NT, DX4, COMP, false>(C, a, P, S, ring, sl, J, B0, av, acc);
-  for (; J < p1; ++J) step<LO, RB, NT, DX4, COMP, true>(C, a, P, S, ring, sl, J, B0, av, acc);
-  for (; J < j1; ++J) step<LO, RB, NT, DX4, COMP, false>(C, a, P, S, ring, sl, J, B0, av, acc);
+  for (; J < p0; ++J) step<LO, RB, NT, DX4, COMP, false>(C, a, P, ring, sl, J, B0, av, acc);
+  for (; J < p1; ++J) step<LO, RB, NT, DX4, COMP, true>(C, a, P, ring, sl, J, B0, av, acc);
+  for (; J < j1; ++J) step<LO, RB, NT, DX4, COMP, false>(C, a, P, ring, sl, J, B0, av, acc);
 }
 
 // Rounds R.. of the triangular part of a pass: round R covers the row blocks
@@ -405,7 +430,7 @@ __device__ __forceinline__ void span(const Ctx& C, const PosteriorArgs& a, Produ
 // is live while J <= its row block / 2, slots above R throughout.
 template <int R, int RB, int NT, int DX4, bool COMP>
 __device__ __forceinline__ void rounds(const Ctx& C, const PosteriorArgs& a, Producer<NT, DX4, COMP>& P,
-                                       Stager<DX4, COMP>& S, _Float16* ring, const Slots<RB>& sl,
+                                       _Float16* ring, const Slots<RB>& sl,
                                        int base, int pw0, int pw1, BHalf& B0, AFrag (&av)[RB],
                                        floatx4 (&acc)[RB][NT / 16]) {
   if constexpr (R < RB) {
@@ -413,9 +438,9 @@ __device__ __forceinline__ void rounds(const Ctx& C, const PosteriorArgs& a, Pro
     if (j0 >= C.nbj) return;
     const int jend = min(j0 + 4, C.nbj);
     const int jlive = min(slot_block(base, R, C.wave) / 2 + 1, jend);
-    span<R, RB, NT, DX4, COMP>(C, a, P, S, ring, sl, j0, jlive, pw0, pw1, B0, av, acc);
-    span<R + 1, RB, NT, DX4, COMP>(C, a, P, S, ring, sl, jlive, jend, pw0, pw1, B0, av, acc);
-    rounds<R + 1, RB, NT, DX4, COMP>(C, a, P, S, ring, sl, base, pw0, pw1, B0, av, acc);
+    span<R, RB, NT, DX4, COMP>(C, a, P, ring, sl, j0, jlive, pw0, pw1, B0, av, acc);
+    span<R + 1, RB, NT, DX4, COMP>(C, a, P, ring, sl, jlive, jend, pw0, pw1, B0, av, acc);
+    rounds<R + 1, RB, NT, DX4, COMP>(C, a, P, ring, sl, base, pw0, pw1, B0, av, acc);
   }
 }
 
@@ -425,58 +450,113 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
   constexpr int NCB = NT / 16;          // 16-column blocks per tile
   constexpr int NX = (Q > 1) ? Q : 1;   // per-point partial slots (diag + xors)
   using Prod = Producer<NT, DX4, COMP>;
-  static_assert(Prod::RPL >= 2 && Prod::RPL <= 8 && 64 % Prod::CPW == 0, "tile width");
+  static_assert(NT == 64, "eight 16x16 tiles per 32-row block");
+  constexpr int D = Prod::D;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   // wave index as a scalar: the loop control below stays uniform
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n_pad = a.nb * kBlk;
   _Float16* ring = reinterpret_cast<_Float16*>(smem);       // 2 planes x NT x kCSH halves
-  float* xst = smem + NT * kCSH;                            // 4 slots + a scratch float4
   float* red = smem;                                        // kWaves * NT * NX, after the loop
-  float* mush = xst + 4 * Stager<DX4, COMP>::kSlot + 4;           // NT
-  float* kpp = mush + NT;                                   // NT * 4 (prior cross-cov)
+  float* ctile = smem + NT * kCSH;                          // NT * D exact scaled candidates
+  float* mush = ctile + NT * D;                             // 2 * NT (mu per row half)
+  float* kpp = mush + 2 * NT;                               // NT * 4 (prior cross-cov)
   float* wsh = kpp + NT * 4;                                // NT: w(candidate), composite
   const int64_t p0 = (int64_t)blockIdx.x * NT;
 
   Prod P;
   float wstar = 0.f;        // composite: w(candidate)
-  P.col = wave * Prod::CPW + lane % Prod::CPW;
-  P.row0 = (lane / Prod::CPW) * Prod::RPL;
-  {
-    const int64_t p = p0 + P.col;
-    P.valid = p < a.npts;
+  P.half = wave >> 2;
+  P.col = 16 * (wave & 3) + (lane & 15);
+  P.rq = 16 * P.half + 4 * (lane >> 4);
+  const int64_t pcol = p0 + P.col;
+  const bool valid = pcol < a.npts;
+  float cc[D];              // this lane's candidate, scaled (slot layout)
 #pragma unroll
-    for (int t = 0; t < DX4 * 4; ++t) P.c[t] = 0.f;
-    P.wsd = 0.f;
-    if (P.valid) {
-      const float* cp = a.cand + p * a.d;
+  for (int t = 0; t < D; ++t) cc[t] = 0.f;
+  P.wsd = 0.f;
+  if (valid) {
+    const float* cp = a.cand + pcol * a.d;
 #pragma unroll
-      for (int t = 0; t < DX4 * 4; ++t) {
-        const int c = slot_dim(t, a.d, a.dr, a.dr4);
-        if (c >= 0) P.c[t] = cp[c] * a.invls[t];
-      }
-      if constexpr (COMP) {
-        float e = 0.f;
-        for (int t = a.dr; t < a.d; ++t) e = fmaf(a.pref[t - a.dr], cp[t], e);
-        wstar = expf(e);
-        P.wsd = a.s_dep * wstar;
-      }
+    for (int t = 0; t < D; ++t) {
+      const int c = slot_dim(t, a.d, a.dr, a.dr4);
+      if (c >= 0) cc[t] = cp[c] * a.invls[t];
     }
-    if (COMP && P.row0 == 0) wsh[P.col] = wstar;
+    if constexpr (COMP) {
+      float e = 0.f;
+      for (int t = a.dr; t < a.d; ++t) e = fmaf(a.pref[t - a.dr], cp[t], e);
+      wstar = expf(e);
+      P.wsd = a.s_dep * wstar;
+    }
+  }
+  // distance operands of the candidate: centred coordinates, their squared
+  // norms per group, and the B fragments, laid out per group and column in
+  // the (not yet used) ring as 96 halves: [0, 32) stream 0 (hi, zero past D),
+  // [32, 96) stream 1 (hi at p < D, lo at D <= p < 2D, zero beyond)
+  {
+    float ct[D];
+#pragma unroll
+    for (int t = 0; t < D; ++t) ct[t] = cc[t] - a.ctr[t];
+#pragma unroll
+    for (int g = 0; g < Prod::NS; ++g) {
+      float n2 = 0.f;
+#pragma unroll
+      for (int t = 0; t < D; ++t) {
+        const bool in = !COMP || ((t < 4 * a.dr4) == (g == 0));
+        if (in) n2 = fmaf(ct[t], ct[t], n2);
+      }
+      P.c2[g] = n2;
+    }
+    _Float16* hs = ring;
+    if (P.half == 0 && (lane >> 4) == 0) {
+#pragma unroll
+      for (int g = 0; g < Prod::NS; ++g) {
+        _Float16* h = hs + (g * NT + P.col) * 96;
+        halfx8 v[12];
+#pragma unroll
+        for (int i = 0; i < 12; ++i) v[i] = halfx8{};
+#pragma unroll
+        for (int t = 0; t < D; ++t) {
+          const bool in = !COMP || ((t < 4 * a.dr4) == (g == 0));
+          const _Float16 hi = static_cast<_Float16>(in ? ct[t] : 0.f);
+          const _Float16 lo = static_cast<_Float16>(
+              in ? (ct[t] - static_cast<float>(static_cast<_Float16>(ct[t]))) * kDistLoScale : 0.f);
+          v[t / 8][t % 8] = hi;
+          v[(32 + t) / 8][(32 + t) % 8] = hi;
+          v[(32 + D + t) / 8][(32 + D + t) % 8] = lo;
+        }
+#pragma unroll
+        for (int i = 0; i < 12; ++i) *reinterpret_cast<halfx8*>(h + 8 * i) = v[i];
+      }
+#pragma unroll
+      for (int t4 = 0; t4 < DX4; ++t4)
+        *reinterpret_cast<float4*>(ctile + P.col * D + 4 * t4) =
+            float4{cc[4 * t4], cc[4 * t4 + 1], cc[4 * t4 + 2], cc[4 * t4 + 3]};
+      if (COMP) wsh[P.col] = wstar;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int g = 0; g < Prod::NS; ++g)
+#pragma unroll
+      for (int f = 0; f < Prod::NF; ++f)
+        P.cb[g][f] = *reinterpret_cast<const halfx8*>(hs + (g * NT + P.col) * 96 + 32 * f +
+                                                      8 * (lane >> 4));
+    // the ring is written from here on
+    __syncthreads();
   }
 
   if (Q > 1) {
     // prior covariance of each point with its batch mates (point ^ x), partner
-    // x on the lane of the column's group whose row group is x
-    const int x = lane / Prod::CPW;
-    if (x >= 1 && x < Q) {
-      const int64_t pm = (p0 + P.col) ^ x;
+    // x on the lane of the column (first row half) whose row group is x
+    const int x = lane >> 4;
+    if (P.half == 0 && x >= 1 && x < Q) {
+      const int64_t pm = pcol ^ x;
       float r2 = 0.f, r2r = 0.f, wm = 0.f;     // r2r, wm: composite routing part, w(partner)
-      if (P.valid && pm < a.npts) {
+      if (valid && pm < a.npts) {
         const float* cp = a.cand + pm * a.d;
 #pragma unroll
-        for (int t = 0; t < DX4 * 4; ++t) {
+        for (int t = 0; t < D; ++t) {
           if constexpr (COMP) {
             if (t == 4 * a.dr4) {
               r2r = r2;
@@ -485,7 +565,7 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
           }
           const int c = slot_dim(t, a.d, a.dr, a.dr4);
           if (c >= 0) {
-            const float dd = P.c[t] - cp[c] * a.invls[t];
+            const float dd = cc[t] - cp[c] * a.invls[t];
             r2 = fmaf(dd, dd, r2);
           }
         }
@@ -511,19 +591,15 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
   C.nbj = (a.nb + 1) / 2;
   C.zero_blk = frag_row_start(a.nb);
   C.lp_rs = make_rsrc(a.Lp, (C.zero_blk + 1) * 2048);
-  Stager<DX4, COMP> S;
-  S.xs_rs = make_rsrc(a.Xs, n_pad * a.dx * 4);
-  S.al_rs = make_rsrc(a.alpha, n_pad * 4);
-  if constexpr (COMP) S.wt_rs = make_rsrc(a.wts, n_pad * 4);
-  S.row = min(tid / (DX4 + 1), kJ - 1);
-  S.t4 = tid % (DX4 + 1);
-  S.soff = (tid < Stager<DX4, COMP>::kF4)
-               ? stage_pos<Prod::RPL>(S.row) * Stager<DX4, COMP>::RS + 4 * S.t4
-               : -1;
+  P.xf_rs = make_rsrc(a.xf, a.nb * Prod::NF * 1024);
+  P.x2_rs = make_rsrc(a.x2, 2 * n_pad * 4);
+  P.al_rs = make_rsrc(a.alpha, n_pad * 4);
+  P.xs_rs = make_rsrc(a.Xs, n_pad * a.dx * 4);
+  if constexpr (COMP) P.wt_rs = make_rsrc(a.wts, n_pad * 4);
   C.n_pad = n_pad;
   C.wave = wave;
   C.tid = tid;
-  C.xst = xst;
+  C.ctile = ctile;
   C.voff = lane * 16;
   // B fragments: column (b*16 + lane%16), rows 8*(lane/16) .. +7 of a block
   C.Kb = ring + (lane & 15) * kCSH + 8 * (lane >> 4);
@@ -561,38 +637,26 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
     // into the slot of block J - 1, which no wave reads after step J - 1:
     // the new blocks are made during the pass's first steps, where every
     // slot is live and the matrix cores have the most work to hide them
-    // behind. Staging runs two blocks ahead of production.
+    // behind. The operands of a block are loaded a step before it is made.
     const int have0 = have;
-    const int sb = have0 ? have0 : 0;    // first block staged here
-    // the previous pass may still read the staging slots
-    lds_barrier();
-    {
-      // four blocks at once: one load latency, not four
-      Stager<DX4, COMP> S4[4];
-#pragma unroll
-      for (int jb = 0; jb < 4; ++jb) {
-        S4[jb] = S;
-        stage_load(S4[jb], a, sb + jb);
-      }
-#pragma unroll
-      for (int jb = 0; jb < 4; ++jb) stage_store(S4[jb], xst, sb + jb);
-    }
-    lds_barrier();
     if (have == 0) {
       // start over: blocks 0 and 1, and mu from scratch
       P.mu = 0.f;
-      produce(P, a, 0, xst, ring);
-      produce(P, a, 1, xst, ring);
+      prod_load(P, n_pad, 0, lane);
+      produce(P, a, 0, ctile, ring);
+      prod_load(P, n_pad, 1, lane);
+      produce(P, a, 1, ctile, ring);
       have = 2;
       lds_barrier();
     }
     C.poff = have0 ? have0 - 1 : 2;
+    prod_load(P, n_pad, C.poff, lane);   // block poff: made at step 0 when new
     const int pw0 = have, pw1 = jpass;   // blocks this pass produces
     BHalf B0;
     load_b<NT>(C, 0, 0, B0);
     // blocks left of this pass's triangle: every slot is live
-    span<0, RB, NT, DX4, COMP>(C, a, P, S, ring, sl, 0, base / 2, pw0, pw1, B0, av, acc);
-    rounds<0, RB, NT, DX4, COMP>(C, a, P, S, ring, sl, base, pw0, pw1, B0, av, acc);
+    span<0, RB, NT, DX4, COMP>(C, a, P, ring, sl, 0, base / 2, pw0, pw1, B0, av, acc);
+    rounds<0, RB, NT, DX4, COMP>(C, a, P, ring, sl, base, pw0, pw1, B0, av, acc);
     have = (jpass <= kRing) ? max(have, jpass) : 0;
 
 #pragma unroll
@@ -613,9 +677,9 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
   // mu: the last pass produced every block; reduce over the lanes of a column
   {
     float v = P.mu;
-#pragma unroll
-    for (int off = Prod::CPW; off < 64; off <<= 1) v += __shfl_xor(v, off);
-    if (lane < Prod::CPW) mush[P.col] = v;
+    v += __shfl_xor(v, 16);
+    v += __shfl_xor(v, 32);
+    if (lane < 16) mush[P.half * NT + P.col] = v;
   }
   // |v|^2 (and cross terms): over the four 16-lane row groups, then over
   // waves in LDS (red overlays the ring: wait until every wave is done)
@@ -648,7 +712,7 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
     for (int w = 0; w < kWaves; ++w)
 #pragma unroll
       for (int x = 0; x < NX; ++x) tot[x] += red[(w * NT + tid) * NX + x];
-    const float mu = mush[tid];
+    const float mu = mush[tid] + mush[NT + tid];
     float prior = a.s;
     if constexpr (COMP) {
       const float w = wsh[tid];
@@ -716,12 +780,14 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
 }
 
 constexpr size_t lds_floats(int NT, int DX4, int q) {
-  // ring: 2 planes x NT columns x kCSH halves (the reduction overlays it);
-  // staging: 4 slots + a scratch float4; mu, the prior cross-covariances and
-  // the candidates' preference weights
-  return (size_t)NT * kCSH + (size_t)4 * kJ * (DX4 * 4 + 4) + 4 + NT + (size_t)NT * 4 + NT;
+  // ring: 2 planes x NT columns x kCSH halves (the reduction and, before the
+  // loop, the candidates' distance fragments overlay it); the exact scaled
+  // candidates; mu per row half, the prior cross-covariances and the
+  // candidates' preference weights
+  return (size_t)NT * kCSH + (size_t)NT * 4 * DX4 + 2 * NT + (size_t)NT * 4 + NT;
 }
 static_assert((size_t)kWaves * 64 * 4 <= (size_t)64 * kCSH, "reduction fits the ring");
+static_assert(2 * 64 * 96 <= 2 * 64 * kCSH, "distance fragments fit the ring");
 
 template <int NT, int DX4, int Q, int RB, bool COMP>
 hipError_t launch_t(const PosteriorArgs& a, hipStream_t st) {
