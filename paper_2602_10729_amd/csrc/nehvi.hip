@@ -352,6 +352,9 @@ __global__ __launch_bounds__(kMW * 64) void k_nehvi_means(NehviMeansArgs a) {
       } else {
         kv = m52(r2, sk);
       }
+      // one fp32 kv for both halves (the compiler may otherwise fuse the last
+      // product into the fp16 conversions and derive the high half twice)
+      asm volatile("" : "+v"(kv));
       const _Float16 h = static_cast<_Float16>(kv);
       hi[u] = h;
       lo[u] = static_cast<_Float16>(kv - static_cast<float>(h));
