@@ -131,6 +131,48 @@ def test_small_models_and_odd_shapes():
         assert_close(g["ehvi"], o["ehvi"], TOL_EHVI, f"ehvi n={n} d={d}")
 
 
+def _m52_root(target):
+    """Distance r with (1 + sqrt5 r + 5 r^2 / 3) exp(-sqrt5 r) = target (fp64
+    bisection; the correlation falls monotonically in r)."""
+    lo, hi = 0.0, 10.0
+    for _ in range(200):
+        mid = 0.5 * (lo + hi)
+        v = (1 + 5 ** 0.5 * mid + 5 * mid * mid / 3) * np.exp(-(5 ** 0.5) * mid)
+        lo, hi = (mid, hi) if v > target else (lo, mid)
+    return 0.5 * (lo + hi)
+
+
+def test_kernel_values_at_fp16_rounding_midpoints():
+    """Regression: each kernel value is split into fp16 halves hi + lo for
+    the triangle's matrix-core products. Both halves must come from one value;
+    a split whose high half is rounded from a different representation than
+    the one the low half is taken against is off by one fp16 ulp exactly when
+    the value lies at an fp16 rounding midpoint. One training point at the
+    origin (unit lengthscale, unit scale), and candidates on consecutive fp32
+    steps across the distances where k(x*, x) crosses the midpoints
+    0.5517578125 + 2^-12 (near pair: exact differences) and 0.5 + 2^-12
+    (r^2 > 1: the distance expansion)."""
+    _announce("fp16 midpoints", 1, 1)
+    wl = bi.make_config(0, seed=1, M=50)
+    wl.X = np.zeros((1, 1), np.float32)
+    wl.Y = np.array([[0.3, -0.2]], np.float32)
+    wl.d, wl.n = 1, 1
+    wl.lengthscale = np.ones((2, 1), np.float32)
+    wl.outputscale = np.ones(2, np.float32)
+    wl.noise = np.full(2, 1e-3, np.float32)
+    steps = np.arange(-2048, 2048, dtype=np.int32)
+    cands = []
+    for mid in (0.5517578125 + 2.0 ** -12, 0.5 + 2.0 ** -12):
+        r0 = np.float32(_m52_root(mid))
+        cands.append((r0.view(np.int32) + steps).view(np.float32))
+    wl.cand = np.concatenate(cands).reshape(-1, 1, 1)
+    wl.ref = (wl.Y.astype(np.float64).min(0) - 0.1).astype(np.float32)
+    g = gpu_run(wl)
+    o = oracle_score(oracle_fit(wl), wl)
+    assert_close(g["mu"], o["mu"], TOL_MU, "mu at fp16 midpoints")
+    assert_close(g["sigma"], o["sigma"], TOL_SIGMA, "sigma at fp16 midpoints")
+
+
 def test_q2_path_and_three_objectives_q1():
     """q = 2 (pairs) with m = 2, and m = 3 with q = 1, built from config 4's
     observations."""
