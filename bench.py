@@ -209,7 +209,7 @@ def main(argv=None):
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32 (posterior contraction: fp16x3 split products, fp32 accumulate)",
+        "dtype": "f32 (posterior contraction and distance dot products: fp16x3 split products, fp32 accumulate)",
         "data": "synthetic",
         "config": {
             "workload": f"config {a.config}: M={wl.M} candidates (q={wl.q}), n={wl.n} "
