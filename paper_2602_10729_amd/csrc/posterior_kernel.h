@@ -30,16 +30,18 @@
 // kept.
 //
 // K*^T is produced two blocks ahead of its use into an LDS ring of 16
-// blocks (512 rows) of fp16 hi/lo planes, from training rows staged through
-// LDS two blocks ahead of that. While the matrix cores work on block J, the
-// waves evaluate the ARD Matern-5/2 values of block J + 2 on the vector ALUs
-// (direct differences of lengthscale-scaled coordinates, no
-// |a|^2 + |b|^2 - 2ab cancellation) and accumulate mu = K* alpha in fp32.
+// blocks (512 rows) of fp16 hi/lo planes, from the training rows' distance
+// fragments, norms and alpha, which each lane loads one step ahead into
+// registers. While the matrix cores work on block J, the waves form the
+// squared distances of block J + 2 with a few more MFMAs (the expansion
+// |c|^2 + |x|^2 - 2c.x over centred coordinates, exact differences for pairs
+// near a training point, see Producer), evaluate the ARD Matern-5/2 values on
+// the vector ALUs and accumulate mu = K* alpha in fp32.
 // A pass that starts while the ring still holds blocks 0.. reuses them, so
 // for n <= 1024 every kernel value is evaluated once.
 // The kernel evaluations and the MFMAs of a step are independent and are
 // interleaved, so each SIMD's matrix core and vector ALU stay busy together.
-// One barrier per step publishes the produced block and the staged rows.
+// One barrier per step publishes the produced block.
 //
 // Each wave owns RB row-block slots, slot r holding row block
 // base + 8r + (r even ? wave : 7 - wave); this snake keeps the per-SIMD
@@ -366,7 +368,7 @@ __device__ __forceinline__ void load_b(const Ctx& C, int J, int h, BHalf& B) {
 // block J (fragments for J + 1 requested on the way) and the producer's block
 // J + 2 (when PROD) are independent and are left to the scheduler to
 // interleave: the fp16 MFMAs overlap the VALU work. The step's barrier
-// publishes the produced block and the staged rows; block J + 1 was
+// publishes the produced block; block J + 1 was
 // published by the previous step's, so its B fragments can be read early.
 template <int LO, int RB, int NT, int DX4, bool COMP, bool PROD>
 __device__ __forceinline__ void step(const Ctx& C, const PosteriorArgs& a, Producer<NT, DX4, COMP>& P,
