@@ -173,6 +173,27 @@ def test_kernel_values_at_fp16_rounding_midpoints():
     assert_close(g["sigma"], o["sigma"], TOL_SIGMA, "sigma at fp16 midpoints")
 
 
+def test_translation_invariance_of_the_posterior():
+    """The Matern kernel is stationary, so shifting the training points and
+    the candidates by one offset must not change the result beyond what fp32
+    inputs carry. Squared distances come from |c|^2 + |x|^2 - 2c.x over
+    coordinates centred on the training mean, so large offsets must not reach
+    the expansion's error. Each shifted run is held to the oracle's bar on the
+    same (fp32) shifted inputs: offset 3 with near-data candidates included,
+    offset 100 (scaled coordinates up to 1000) on the config's candidates."""
+    for off, with_near in ((3.0, True), (100.0, False)):
+        _announce("translation", off, with_near)
+        wl = bi.make_config(1, seed=2, M=1500)
+        if with_near:
+            wl.cand = np.concatenate([wl.cand, bi.near_data_candidates(wl, 500, scale=0.01)], 0)
+        wl.cand = (wl.cand.astype(np.float64) + off).astype(np.float32)
+        wl.X = (wl.X.astype(np.float64) + off).astype(np.float32)
+        g = gpu_run(wl)
+        o = oracle_score(oracle_fit(wl), wl)
+        assert_close(g["mu"], o["mu"], TOL_MU, f"mu offset {off}")
+        assert_close(g["sigma"], o["sigma"], TOL_SIGMA, f"sigma offset {off}")
+
+
 def test_q2_path_and_three_objectives_q1():
     """q = 2 (pairs) with m = 2, and m = 3 with q = 1, built from config 4's
     observations."""
