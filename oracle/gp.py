@@ -50,13 +50,19 @@ class NotPositiveDefinite(ValueError):
     """The training covariance matrix of some objective is not PD."""
 
 
-def scaled_distance(U: np.ndarray, V: np.ndarray, ls: np.ndarray) -> np.ndarray:
-    """rho[i, j] = sqrt(sum_t ((U[i,t] - V[j,t]) / ls[t])^2), direct differences."""
+def scaled_distance(U: np.ndarray, V: np.ndarray, ls: np.ndarray, rows: int = 16) -> np.ndarray:
+    """rho[i, j] = sqrt(sum_t ((U[i,t] - V[j,t]) / ls[t])^2), direct differences.
+
+    Computed ``rows`` rows of U at a time, so the [rows, len(V), d] array of
+    differences stays small."""
     U = np.asarray(U, dtype=np.float64)
     V = np.asarray(V, dtype=np.float64)
     ls = np.asarray(ls, dtype=np.float64)
-    D = (U[:, None, :] - V[None, :, :]) / ls
-    return np.sqrt(np.einsum("ijt,ijt->ij", D, D))
+    out = np.empty((U.shape[0], V.shape[0]))
+    for i0 in range(0, U.shape[0], rows):
+        D = (U[i0:i0 + rows, None, :] - V[None, :, :]) / ls
+        out[i0:i0 + rows] = np.sqrt(np.einsum("ijt,ijt->ij", D, D))
+    return out
 
 
 def matern52(rho: np.ndarray, s: float) -> np.ndarray:
