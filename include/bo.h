@@ -63,7 +63,8 @@ typedef enum {
   BO_ERR_CAPACITY = 3,              /* n, d, S or box count beyond compiled limits */
   BO_ERR_DEVICE = 4,                /* a HIP runtime call failed               */
   BO_ERR_OUT_OF_MEMORY = 5,         /* device or host allocation failed        */
-  BO_ERR_NONFINITE_INPUT = 6        /* NaN/Inf in a host-side input            */
+  BO_ERR_NONFINITE_INPUT = 6,       /* NaN/Inf in a host-side input            */
+  BO_ERR_ILL_CONDITIONED = 7        /* K too ill-conditioned for fp32-class scoring */
 } bo_status;
 
 /* Compiled limits (BO_ERR_CAPACITY beyond them). */
@@ -84,9 +85,30 @@ typedef enum {
  *   k(u,v) = s (1 + sqrt5 r + 5/3 r^2) exp(-sqrt5 r),
  *            r = sqrt(sum_t ((u_t - v_t)/l_t)^2)
  *   K = [k(x_i,x_j)] + eta I;  L = chol(K);  alpha = K^{-1} y_k.
- * The factorisation runs in fp64 on the device; the model keeps L^{-1}
- * (fp32, lower blocks only), alpha (fp32) and the lengthscale-scaled X.
- * It also extracts the non-dominated set of Y on the host.
+ * The factorisation runs in fp64 on the device. The model keeps alpha
+ * (fp32), the lengthscale-scaled X and L^{-1} as the scoring kernel's
+ * operand: the lower 16x32 blocks, each 16-row block scaled by a power of two
+ * that puts its largest entry in [2^13, 2^14), every entry split into two
+ * fp16 halves (hi = fp16(w), lo = fp16(w - hi)). It also extracts the
+ * non-dominated set of Y on the host.
+ *
+ * Precision of the scores (fp32-class). The posterior runs in fp32 with the
+ * triangular product on the fp16 matrix cores as three split products with
+ * fp32 accumulation; both of its operands are scaled by powers of two first
+ * (the candidates' kernel values per candidate, L^{-1} per row block), so
+ * no value can overflow fp16 and each carries 22 significant bits (an
+ * absolute floor of 2^-39 of its block's largest), against 24 in fp32. The
+ * error of mu, of sigma^2 relative to the prior variance and of the EHVI is
+ * therefore that of an fp32 implementation up to a small factor, for every
+ * accepted hyperparameter. Where the posterior variance is far below the
+ * prior (candidates near the data, long learned lengthscales) fp32 itself
+ * loses sigma's relative accuracy: sigma^2 = k(x,x) - |v|^2 cancels.
+ *
+ * Accepted hyperparameters: outputscale in [2^-64, 2^64], noise in
+ * [0, 2^64]. The model is refused with ILL_CONDITIONED when, for some
+ * objective, max_i K_ii * max |L^{-1}|^2 (a lower bound on cond(K)) reaches
+ * 2^24, where no fp32 solve carries a correct bit (e.g. near-duplicate
+ * observations with zero noise).
  *
  * X      device [n][d]   encoded observations
  * Y      device [n][m]   standardised objective values (maximise)
@@ -97,12 +119,15 @@ typedef enum {
  *
  * Synchronous: enqueues all device work on the stream (behind earlier work,
  * without waiting for it), then waits once and returns after the positive
- * definiteness flag and Y have been read back. Y lives on the device, so its
- * finiteness is checked at that point (its kernels have already run); the
- * host arguments are validated before anything is enqueued. Concurrent fits
- * on one device share a pinned staging buffer and run one at a time.
- * Errors: INVALID_ARGUMENT, NONFINITE_INPUT (hyperparameters or Y not
- * finite), CAPACITY, NOT_POSITIVE_DEFINITE, OUT_OF_MEMORY, DEVICE.
+ * definiteness flag, the conditioning estimate and Y have been read back. Y
+ * lives on the device, so its finiteness is checked at that point (its
+ * kernels have already run); the host arguments are validated before
+ * anything is enqueued. Concurrent fits on one device share a pinned staging
+ * buffer and run one at a time.
+ * Errors: INVALID_ARGUMENT (also hyperparameters outside the accepted
+ * range), NONFINITE_INPUT (hyperparameters or Y not finite), CAPACITY,
+ * NOT_POSITIVE_DEFINITE (a pivot <= 0 or a non-finite inverse factor),
+ * ILL_CONDITIONED, OUT_OF_MEMORY, DEVICE.
  */
 bo_status bo_fit(const float* X, const float* Y, int64_t n, int32_t d, int32_t m,
                  const float* lengthscale, const float* outputscale,

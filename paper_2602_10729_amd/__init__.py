@@ -32,7 +32,7 @@ _lib = None
 STATUS = {
     0: "BO_OK", 1: "BO_ERR_INVALID_ARGUMENT", 2: "BO_ERR_NOT_POSITIVE_DEFINITE",
     3: "BO_ERR_CAPACITY", 4: "BO_ERR_DEVICE", 5: "BO_ERR_OUT_OF_MEMORY",
-    6: "BO_ERR_NONFINITE_INPUT",
+    6: "BO_ERR_NONFINITE_INPUT", 7: "BO_ERR_ILL_CONDITIONED",
 }
 MAX_N, MAX_D, MAX_S, MAX_BOXES = 2048, 32, 4096, 4096
 

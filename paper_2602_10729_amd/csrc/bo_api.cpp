@@ -12,6 +12,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <cstdio>
 #include <cstdlib>
 #include <cstring>
 #include <mutex>
@@ -189,8 +190,10 @@ struct FitScratch {
   double* hyp = nullptr;
   double* tmp = nullptr;
   int* flag = nullptr;
+  unsigned long long* stats = nullptr;   // [2m]: max K_ii, then max |L^{-1}| (double bits)
   ~FitScratch() {
     pfree(A, st); pfree(W, st); pfree(hyp, st); pfree(tmp, st); pfree(flag, st);
+    pfree(stats, st);
   }
 };
 
@@ -199,8 +202,9 @@ struct FitScratch {
 // for the whole device before handing memory back to the pool.
 void release_noisy(Model* M) {
   Model::Noisy& z = M->nz;
-  if (z.Lp0 || z.Gp || z.boxes || z.off || z.front || z.ws) (void)hipDeviceSynchronize();
+  if (z.Lp0 || z.rsc0 || z.Gp || z.boxes || z.off || z.front || z.ws) (void)hipDeviceSynchronize();
   pfree(z.Lp0, nullptr);
+  pfree(z.rsc0, nullptr);
   pfree(z.Gp, nullptr);
   pfree(z.boxes, nullptr);
   pfree(z.off, nullptr);
@@ -214,9 +218,10 @@ void release_noisy(Model* M) {
 
 void release_buffers(Model* M) {
   release_noisy(M);
-  if (M->Xs || M->invls || M->alpha || M->Lp || M->ws || M->d_boxes || M->wts || M->pref ||
-      M->Xd || M->xf || M->x2 || M->ctr)
+  if (M->Xs || M->invls || M->alpha || M->Lp || M->rsc || M->ws || M->d_boxes || M->wts ||
+      M->pref || M->Xd || M->xf || M->x2 || M->ctr)
     (void)hipDeviceSynchronize();
+  pfree(M->rsc, nullptr);
   pfree(M->xf, nullptr);
   pfree(M->x2, nullptr);
   pfree(M->ctr, nullptr);
@@ -277,6 +282,7 @@ const char* bo_status_string(bo_status s) {
     case BO_ERR_DEVICE: return "HIP runtime error";
     case BO_ERR_OUT_OF_MEMORY: return "out of memory";
     case BO_ERR_NONFINITE_INPUT: return "non-finite input";
+    case BO_ERR_ILL_CONDITIONED: return "covariance too ill-conditioned for fp32-class scoring";
   }
   return "unknown status";
 }
@@ -345,6 +351,74 @@ bo_status bo_model_front_indices(bo_model model, int32_t* idx_host, int32_t cap)
 namespace {
 
 // Composite-kernel hyperparameters as passed to bo_fit_composite (host).
+// Accepted hyperparameter range: output scales in [2^-64, 2^64], noise and
+// the composite's other scales in [0, 2^64]. Inside it every intermediate of
+// the fp32 scoring arithmetic (scaled squared norms, variances) stays in
+// fp32's normal range.
+constexpr double kScaleMin = 0x1p-64, kScaleMax = 0x1p64;
+// A fitted model is refused (BO_ERR_ILL_CONDITIONED) when max K_ii times
+// max |L^{-1}|^2, a lower bound on the condition number of K, reaches 2^24:
+// beyond it the fp32-class solve, like any fp32 one, carries no correct bit.
+constexpr double kCondLimit = 0x1p24;
+
+double bits_to_double(unsigned long long b) {
+  double v;
+  std::memcpy(&v, &b, sizeof(v));
+  return v;
+}
+
+// Calls on one model may come on different streams. Each scoring call first
+// makes its stream wait for the model's previous call (when that ran on
+// another stream) and records an event at its end, so a call never rewrites
+// the boxes or the workspace while an earlier call may still read them.
+bo_status order_after_previous(Model& M, hipStream_t st, const char* who) {
+  if (M.last_evt && M.last_stream != st) {
+    hipError_t e = hipStreamWaitEvent(st, M.last_evt, 0);
+    if (e != hipSuccess) return hip_fail(e, who);
+  }
+  return BO_OK;
+}
+bo_status mark_call(Model& M, hipStream_t st, const char* who) {
+  if (!M.last_evt) {
+    hipError_t e = hipEventCreateWithFlags(&M.last_evt, hipEventDisableTiming);
+    if (e != hipSuccess) {
+      M.last_evt = nullptr;
+      return hip_fail(e, who);
+    }
+  }
+  hipError_t e = hipEventRecord(M.last_evt, st);
+  if (e != hipSuccess) return hip_fail(e, who);
+  M.last_stream = st;
+  return BO_OK;
+}
+
+// Arguments of the posterior kernel for objective k of a fitted model: the
+// packed inverse factor Lp (the model's, or the noisy acquisition's noise-free
+// one) with its row-block scales rsc; outputs are the caller's to set.
+PosteriorArgs posterior_args(const Model& M, int k, const float* Lp, const float* rsc,
+                             const float* cand, int64_t npts, int q) {
+  PosteriorArgs pa;
+  pa.cand = cand; pa.npts = npts; pa.d = M.d; pa.dx = M.dx; pa.q = q;
+  pa.Xs = M.Xs + (size_t)k * M.n_pad * M.dx;
+  pa.invls = M.invls + (size_t)k * M.dx;
+  pa.alpha = M.alpha + (size_t)k * M.n_pad;
+  pa.Lp = Lp + (size_t)k * M.lp_per_obj;
+  pa.rsc = rsc + (size_t)k * M.nb;
+  pa.kbound = M.kbound[k];
+  pa.xf = M.xf + (size_t)k * M.nb * dist_frags(M.dx) * 512;
+  pa.x2 = M.x2 + (size_t)k * 2 * M.n_pad;
+  pa.ctr = M.ctr + (size_t)k * M.dx;
+  pa.n = static_cast<int>(M.n); pa.nb = M.nb;
+  pa.s = M.os[k];
+  pa.m = M.m; pa.k = k;
+  pa.dr = M.dr; pa.dr4 = M.dr4;
+  pa.s_dep = M.dr > 0 ? M.s_dep[k] : 0.f;
+  pa.s_int = M.dr > 0 ? M.s_int[k] : 0.f;
+  pa.wts = M.dr > 0 ? M.wts + (size_t)k * M.n_pad : nullptr;
+  pa.pref = M.dr > 0 ? M.pref + (size_t)k * (M.d - M.dr) : nullptr;
+  return pa;
+}
+
 struct CompositeSpec {
   int dr;
   const float* s_dep;
@@ -372,6 +446,9 @@ bo_status fit_impl(const char* who, const float* X, const float* Y, int64_t n, i
   for (int k = 0; k < m; ++k) {
     if (!(outputscale[k] > 0.f)) return fail(BO_ERR_INVALID_ARGUMENT, W + ": outputscale <= 0");
     if (!(noise[k] >= 0.f)) return fail(BO_ERR_INVALID_ARGUMENT, W + ": noise < 0");
+    if (!(outputscale[k] >= kScaleMin && outputscale[k] <= kScaleMax) || !(noise[k] <= kScaleMax))
+      return fail(BO_ERR_INVALID_ARGUMENT,
+                  W + ": outputscale outside [2^-64, 2^64] or noise above 2^64");
   }
   int dr = 0, dr4 = 0, dx = (d + 3) / 4 * 4;
   if (comp) {
@@ -383,9 +460,12 @@ bo_status fit_impl(const char* who, const float* X, const float* Y, int64_t n, i
     if (!all_finite(comp->s_dep, m) || !all_finite(comp->s_int, m) ||
         !all_finite(comp->pref, (size_t)m * (d - dr)))
       return fail(BO_ERR_NONFINITE_INPUT, W + ": non-finite hyperparameter");
-    for (int k = 0; k < m; ++k)
+    for (int k = 0; k < m; ++k) {
       if (!(comp->s_dep[k] >= 0.f) || !(comp->s_int[k] >= 0.f))
         return fail(BO_ERR_INVALID_ARGUMENT, W + ": scale_dep / scale_int < 0");
+      if (!(comp->s_dep[k] <= kScaleMax) || !(comp->s_int[k] <= kScaleMax))
+        return fail(BO_ERR_INVALID_ARGUMENT, W + ": scale_dep / scale_int above 2^64");
+    }
     dr4 = (dr + 3) / 4;
     dx = 4 * dr4 + (d - dr + 3) / 4 * 4;
     if (dx > BO_MAX_D)
@@ -432,6 +512,8 @@ bo_status fit_impl(const char* who, const float* X, const float* Y, int64_t n, i
   if ((s = palloc(&fs.hyp, nhyp, st, "hyperparameters")) != BO_OK) return bail(s);
   if ((s = palloc(&fs.tmp, (size_t)m * nf, st, "fit vector")) != BO_OK) return bail(s);
   if ((s = palloc(&fs.flag, 1, st, "flag")) != BO_OK) return bail(s);
+  if ((s = palloc(&fs.stats, 2 * (size_t)m, st, "fit statistics")) != BO_OK) return bail(s);
+  if ((s = palloc(&M->rsc, (size_t)m * M->nb, st, "row-block scales")) != BO_OK) return bail(s);
   if ((s = palloc(&M->Xs, (size_t)m * M->n_pad * M->dx, st, "scaled X")) != BO_OK) return bail(s);
   if ((s = palloc(&M->invls, (size_t)m * M->dx, st, "inverse lengthscales")) != BO_OK) return bail(s);
   if ((s = palloc(&M->alpha, (size_t)m * M->n_pad, st, "alpha")) != BO_OK) return bail(s);
@@ -473,7 +555,8 @@ bo_status fit_impl(const char* who, const float* X, const float* Y, int64_t n, i
   const size_t off_pref = off_inv + sizeof(float) * invls.size();
   const size_t npref = comp ? (size_t)m * dc : 0;
   const size_t off_flag = (off_pref + sizeof(float) * npref + 15) / 16 * 16;
-  const size_t off_y = off_flag + 16;
+  const size_t off_stats = off_flag + 16;
+  const size_t off_y = off_stats + 16 * 3;
   const size_t need = off_y + sizeof(float) * n * m;
   hipError_t e = hipSuccess;
   if (need > DS->fit_stage_bytes) {
@@ -497,6 +580,7 @@ bo_status fit_impl(const char* who, const float* X, const float* Y, int64_t n, i
     e = hipMemcpyAsync(M->pref, stage + off_pref, sizeof(float) * npref, hipMemcpyHostToDevice,
                        st);
   if (e == hipSuccess) e = hipMemsetAsync(fs.flag, 0, sizeof(int), st);
+  if (e == hipSuccess) e = hipMemsetAsync(fs.stats, 0, sizeof(unsigned long long) * 2 * m, st);
   if (e == hipSuccess)
     e = hipMemcpyAsync(M->Xd, X, sizeof(float) * n * d, hipMemcpyDeviceToDevice, st);
   if (e != hipSuccess) return bail(hip_fail(e, "bo_fit: upload"));
@@ -511,16 +595,19 @@ bo_status fit_impl(const char* who, const float* X, const float* Y, int64_t n, i
     gp.s_int = gp.s_dep + m;
     gp.pref = gp.s_int + m;
   }
-  if ((s = after_launch(launch_gram(X, n, d, m, nf, gp, fs.A, st), st, "gram")) != BO_OK) return bail(s);
+  if ((s = after_launch(launch_gram(X, n, d, m, nf, gp, fs.A, st, fs.stats), st, "gram")) != BO_OK) return bail(s);
   if (comp && (s = after_launch(launch_weights(X, n, d, m, M->n_pad, gp, M->wts, st), st, "weights")) != BO_OK) return bail(s);
   if ((s = after_launch(launch_cholesky(fs.A, fs.W, nf, m, fs.flag, st), st, "cholesky")) != BO_OK) return bail(s);
   if ((s = after_launch(launch_alpha(fs.W, Y, n, m, nf, M->n_pad, fs.tmp, M->alpha, st), st, "alpha")) != BO_OK) return bail(s);
-  if ((s = after_launch(launch_pack(fs.W, n, m, nf, M->nb, M->Lp, X, d, M->dx, dr, dr4, M->invls, M->Xs, st), st, "pack")) != BO_OK) return bail(s);
+  if ((s = after_launch(launch_pack(fs.W, n, m, nf, M->nb, M->Lp, M->rsc, fs.stats + m, fs.flag, X, d, M->dx, dr, dr4, M->invls, M->Xs, st), st, "pack")) != BO_OK) return bail(s);
   if ((s = after_launch(launch_pack_x(M->Xs, n, m, M->nb, M->dx, dr4, M->ctr, M->xf, M->x2, st), st, "pack X")) != BO_OK) return bail(s);
 
   // one synchronisation: the positive-definiteness flag and Y (for the front
   // and its finiteness check) come back together
   e = hipMemcpyAsync(stage + off_flag, fs.flag, sizeof(int), hipMemcpyDeviceToHost, st);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(stage + off_stats, fs.stats, sizeof(unsigned long long) * 2 * m,
+                       hipMemcpyDeviceToHost, st);
   if (e == hipSuccess)
     e = hipMemcpyAsync(stage + off_y, Y, sizeof(float) * n * m, hipMemcpyDeviceToHost, st);
   if (e == hipSuccess) e = hipStreamSynchronize(st);
@@ -531,7 +618,28 @@ bo_status fit_impl(const char* who, const float* X, const float* Y, int64_t n, i
   M->Yh.assign(yst, yst + (size_t)n * m);
   if (!all_finite(M->Yh.data(), M->Yh.size()))
     return bail(fail(BO_ERR_NONFINITE_INPUT, W + ": Y not finite"));
-  if (flag) return bail(fail(BO_ERR_NOT_POSITIVE_DEFINITE, W + ": non-positive Cholesky pivot"));
+  if (flag)
+    return bail(fail(BO_ERR_NOT_POSITIVE_DEFINITE,
+                     W + ": non-positive Cholesky pivot or non-finite inverse factor"));
+  {
+    unsigned long long st_bits[6];
+    std::memcpy(st_bits, stage + off_stats, sizeof(unsigned long long) * 2 * m);
+    M->kbound.resize(m);
+    M->cond_est.resize(m);
+    for (int k = 0; k < m; ++k) {
+      const double kd = bits_to_double(st_bits[k]), wm = bits_to_double(st_bits[m + k]);
+      M->kbound[k] = static_cast<float>(kd);
+      M->cond_est[k] = kd * wm * wm;
+      if (!(M->cond_est[k] < kCondLimit)) {
+        char msg[200];
+        std::snprintf(msg, sizeof msg,
+                      ": objective %d: max K_ii * max |L^-1|^2 = %.3g reaches 2^24 (a lower "
+                      "bound on cond(K)); the fp32-class solve cannot resolve this model",
+                      k, M->cond_est[k]);
+        return bail(fail(BO_ERR_ILL_CONDITIONED, W + msg));
+      }
+    }
+  }
   host_front<float>(M->Yh.data(), n, m, nullptr, M->nd);
 
   M->last_stream = st;
@@ -680,6 +788,7 @@ void bo_free(bo_model model) {
   if (!model) return;
   DeviceGuard g(model->m.device);
   release_buffers(&model->m);
+  if (model->m.last_evt) (void)hipEventDestroy(model->m.last_evt);
   delete model;
 }
 
@@ -715,6 +824,7 @@ bo_status bo_score_constrained(bo_model model, const float* cand, int64_t M_, in
   const int64_t npts = M_ * q;
   bo_status s;
   if (M_ == 0) return BO_OK;
+  if ((s = order_after_previous(M, st, "bo_score: stream ordering")) != BO_OK) return s;
   if ((s = check_dev(cand, sizeof(float) * npts * M.d, "cand")) != BO_OK) return s;
   if ((s = check_dev(base_samples, sizeof(float) * (size_t)S * q * m, "base_samples")) != BO_OK) return s;
   if ((s = check_dev(ehvi, sizeof(float) * M_, "ehvi")) != BO_OK) return s;
@@ -820,23 +930,7 @@ bo_status bo_score_constrained(bo_model model, const float* cand, int64_t M_, in
     if (e != hipSuccess) return hip_fail(e, "bo_score: profile event");
   }
   for (int k = 0; k < m; ++k) {
-    PosteriorArgs pa;
-    pa.cand = cand; pa.npts = npts; pa.d = M.d; pa.dx = M.dx; pa.q = q;
-    pa.Xs = M.Xs + (size_t)k * M.n_pad * M.dx;
-    pa.invls = M.invls + (size_t)k * M.dx;
-    pa.alpha = M.alpha + (size_t)k * M.n_pad;
-    pa.Lp = M.Lp + (size_t)k * M.lp_per_obj;
-    pa.xf = M.xf + (size_t)k * M.nb * dist_frags(M.dx) * 512;
-    pa.x2 = M.x2 + (size_t)k * 2 * M.n_pad;
-    pa.ctr = M.ctr + (size_t)k * M.dx;
-    pa.n = static_cast<int>(M.n); pa.nb = M.nb;
-    pa.s = M.os[k];
-    pa.m = m; pa.k = k;
-    pa.dr = M.dr; pa.dr4 = M.dr4;
-    pa.s_dep = M.dr > 0 ? M.s_dep[k] : 0.f;
-    pa.s_int = M.dr > 0 ? M.s_int[k] : 0.f;
-    pa.wts = M.dr > 0 ? M.wts + (size_t)k * M.n_pad : nullptr;
-    pa.pref = M.dr > 0 ? M.pref + (size_t)k * (M.d - M.dr) : nullptr;
+    PosteriorArgs pa = posterior_args(M, k, M.Lp, M.rsc, cand, npts, q);
     pa.mu = mu_buf; pa.sd = sd_buf; pa.chol = chol_buf;
     if ((s = after_launch(launch_posterior(pa, st), st, "posterior")) != BO_OK) return s;
   }
@@ -857,8 +951,7 @@ bo_status bo_score_constrained(bo_model model, const float* cand, int64_t M_, in
     hipError_t e = hipEventRecord(rec->e[2], st);
     if (e != hipSuccess) return hip_fail(e, "bo_score: profile event");
   }
-  M.last_stream = st;
-  return BO_OK;
+  return mark_call(M, st, "bo_score: stream ordering");
 }
 
 }  // extern "C"
@@ -878,11 +971,12 @@ struct NoisyScratch {
   double *Zk = nullptr, *T1 = nullptr, *G = nullptr, *Fd = nullptr;
   float *Y = nullptr, *alpha = nullptr, *btmp = nullptr;
   int *flag = nullptr, *counts = nullptr, *off = nullptr;
+  unsigned long long* stats = nullptr;   // [2m]: max K_XX,ii, then max |L_XX^{-1}| (double bits)
   ~NoisyScratch() {
     pfree(A, st); pfree(W, st); pfree(A0, st); pfree(W0, st); pfree(hyp, st); pfree(tmp, st);
     pfree(alpha64, st); pfree(gmax, st); pfree(Zk, st); pfree(T1, st); pfree(G, st); pfree(Fd, st);
     pfree(Y, st); pfree(alpha, st); pfree(btmp, st); pfree(flag, st); pfree(counts, st);
-    pfree(off, st);
+    pfree(off, st); pfree(stats, st);
   }
 };
 
@@ -992,6 +1086,7 @@ bo_status nehvi_prepare_impl(bo_model model, const float* ZX, int32_t S, const f
   if ((s = palloc(&sc.Y, (size_t)n * m, st, "noisy: Y")) != BO_OK) return s;
   if ((s = palloc(&sc.alpha, (size_t)m * M.n_pad, st, "noisy: alpha (fp32)")) != BO_OK) return s;
   if ((s = palloc(&sc.flag, 4, st, "noisy: flags")) != BO_OK) return s;
+  if ((s = palloc(&sc.stats, 2 * (size_t)m, st, "noisy: statistics")) != BO_OK) return s;
   if ((s = palloc(&sc.counts, (size_t)S, st, "noisy: counts")) != BO_OK) return s;
   if ((s = palloc(&sc.off, (size_t)S + 1, st, "noisy: offsets")) != BO_OK) return s;
   if (m == 2) {
@@ -1000,6 +1095,7 @@ bo_status nehvi_prepare_impl(bo_model model, const float* ZX, int32_t S, const f
     if ((s = palloc(&sc.Fd, (size_t)S * n * m, st, "noisy: in-sample draws")) != BO_OK) return s;
   }
   if ((s = palloc(&z.Lp0, (size_t)m * M.lp_per_obj, st, "noisy: packed factor")) != BO_OK) return s;
+  if ((s = palloc(&z.rsc0, (size_t)m * M.nb, st, "noisy: row-block scales")) != BO_OK) return s;
   if ((s = palloc(&z.front, (size_t)S * n, st, "noisy: fronts")) != BO_OK) return s;
 
   std::vector<double> hyp(nhyp, 0.0);
@@ -1019,7 +1115,8 @@ bo_status nehvi_prepare_impl(bo_model model, const float* ZX, int32_t S, const f
   if (!DS) return fail(BO_ERR_DEVICE, W_ + ": device index out of range");
   std::lock_guard<std::mutex> stage_lock(DS->fit_mu);
   const size_t off_flag = (sizeof(double) * nhyp + 15) / 16 * 16;
-  const size_t off_y = off_flag + 16;
+  const size_t off_stats = off_flag + 16;
+  const size_t off_y = off_stats + 16 * 3;
   const size_t off_cnt = (off_y + sizeof(float) * n * m + 15) / 16 * 16;
   const size_t off_gmax = (off_cnt + sizeof(int) * S + 15) / 16 * 16;
   const size_t off_off = off_gmax + sizeof(double) * m * kAbsmaxParts;
@@ -1046,6 +1143,7 @@ bo_status nehvi_prepare_impl(bo_model model, const float* ZX, int32_t S, const f
   if (e == hipSuccess)
     e = hipMemcpyAsync(sc.Y, stage + off_y, sizeof(float) * n * m, hipMemcpyHostToDevice, st);
   if (e == hipSuccess) e = hipMemsetAsync(sc.flag, 0, 4 * sizeof(int), st);
+  if (e == hipSuccess) e = hipMemsetAsync(sc.stats, 0, sizeof(unsigned long long) * 2 * m, st);
   if (e != hipSuccess) return sync_fail(hip_fail(e, "bo_nehvi_prepare: upload"));
 
   GramParams gp;
@@ -1070,9 +1168,9 @@ bo_status nehvi_prepare_impl(bo_model model, const float* ZX, int32_t S, const f
   if ((s = step(launch_sigma_xx(sc.A, n, nf, m, gp.noise, st), "in-sample covariance")) != BO_OK) return sync_fail(s);
   if ((s = step(launch_cholesky(sc.A, sc.W, nf, m, sc.flag + 1, st), "cholesky")) != BO_OK) return sync_fail(s);
   // noise-free K_XX: factor, inverse, packed for the conditional (co)variance
-  if ((s = step(launch_gram(M.Xd, n, d, m, nf, g0, sc.A0, st), "gram")) != BO_OK) return sync_fail(s);
+  if ((s = step(launch_gram(M.Xd, n, d, m, nf, g0, sc.A0, st, sc.stats), "gram")) != BO_OK) return sync_fail(s);
   if ((s = step(launch_cholesky(sc.A0, sc.W0, nf, m, sc.flag + 2, st), "cholesky")) != BO_OK) return sync_fail(s);
-  if ((s = step(launch_pack_factor(sc.W0, n, m, nf, M.nb, z.Lp0, st), "pack")) != BO_OK) return sync_fail(s);
+  if ((s = step(launch_pack_factor(sc.W0, n, m, nf, M.nb, z.Lp0, z.rsc0, sc.stats + m, sc.flag + 3, st), "pack")) != BO_OK) return sync_fail(s);
   // T1 = L_XX Z_X, G = K_XX^{-1} T1 = W0^T (W0 T1)
   if ((s = step(launch_gather_z(ZX, n, m, S, nf, Sp, sc.Zk, st), "gather")) != BO_OK) return sync_fail(s);
   if ((s = step(launch_trmm(false, sc.A, sc.Zk, sc.T1, nf, Sp, m, st), "trmm")) != BO_OK) return sync_fail(s);
@@ -1099,17 +1197,38 @@ bo_status nehvi_prepare_impl(bo_model model, const float* ZX, int32_t S, const f
     if (e != hipSuccess) return sync_fail(hip_fail(e, "bo_nehvi_prepare: draws"));
   }
   if ((s = step(launch_absmax(sc.G, (int64_t)nf * Sp, m, sc.gmax, st), "absmax")) != BO_OK) return sync_fail(s);
-  e = hipMemcpyAsync(stage + off_flag, sc.flag, 3 * sizeof(int), hipMemcpyDeviceToHost, st);
+  e = hipMemcpyAsync(stage + off_flag, sc.flag, 4 * sizeof(int), hipMemcpyDeviceToHost, st);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(stage + off_stats, sc.stats, sizeof(unsigned long long) * 2 * m,
+                       hipMemcpyDeviceToHost, st);
   if (e == hipSuccess)
     e = hipMemcpyAsync(stage + off_gmax, sc.gmax, sizeof(double) * m * kAbsmaxParts,
                        hipMemcpyDeviceToHost, st);
   if (e == hipSuccess) e = hipStreamSynchronize(st);
   if (e != hipSuccess) return sync_fail(hip_fail(e, "bo_nehvi_prepare: sync"));
-  int flags[3];
+  int flags[4];
   std::memcpy(flags, stage + off_flag, sizeof(flags));
   if (flags[0]) return sync_fail(fail(BO_ERR_NOT_POSITIVE_DEFINITE, W_ + ": K not positive definite"));
   if (flags[1]) return sync_fail(fail(BO_ERR_NOT_POSITIVE_DEFINITE, W_ + ": in-sample posterior covariance not positive definite"));
-  if (flags[2]) return sync_fail(fail(BO_ERR_NOT_POSITIVE_DEFINITE, W_ + ": noise-free K_XX not positive definite"));
+  if (flags[2] || flags[3]) return sync_fail(fail(BO_ERR_NOT_POSITIVE_DEFINITE, W_ + ": noise-free K_XX not positive definite"));
+  {
+    // the conditional uses the noise-free K_XX's inverse factor: the same
+    // conditioning limit as the fit's
+    unsigned long long st_bits[6];
+    std::memcpy(st_bits, stage + off_stats, sizeof(unsigned long long) * 2 * m);
+    for (int k = 0; k < m; ++k) {
+      const double kd = bits_to_double(st_bits[k]), wm = bits_to_double(st_bits[m + k]);
+      const double ce = kd * wm * wm;
+      if (!(ce < kCondLimit)) {
+        char msg[200];
+        std::snprintf(msg, sizeof msg,
+                      ": objective %d: the noise-free K_XX has max K_ii * max |L^-1|^2 = %.3g, "
+                      "at or above 2^24",
+                      k, ce);
+        return sync_fail(fail(BO_ERR_ILL_CONDITIONED, W_ + msg));
+      }
+    }
+  }
   std::vector<std::vector<float>> hboxes;
   std::vector<std::vector<int32_t>> hfronts;
   if (m == 2) {
@@ -1176,8 +1295,7 @@ bo_status nehvi_prepare_impl(bo_model model, const float* ZX, int32_t S, const f
   z.S = S; z.Sp = Sp; z.n32 = n32; z.total = static_cast<int>(total); z.m = m;
   z.cons = lower != nullptr;
   for (int k = 0; k < 3; ++k) z.low[k] = (lower && k < m) ? lower[k] : -INFINITY;
-  M.last_stream = st;
-  return BO_OK;
+  return mark_call(M, st, "bo_nehvi_prepare: stream ordering");
 }
 
 bo_status score_nehvi_impl(bo_model model, const float* cand, int64_t M_, int32_t q,
@@ -1203,6 +1321,7 @@ bo_status score_nehvi_impl(bo_model model, const float* cand, int64_t M_, int32_
   if (nehvi_ehvi_lds_bytes(S, q, m, 0, false) > kLdsLimit)
     return fail(BO_ERR_CAPACITY, "bo_score_nehvi: base samples exceed LDS");
   hipStream_t st = static_cast<hipStream_t>(stream);
+  if ((s = order_after_previous(M, st, "bo_score_nehvi: stream ordering")) != BO_OK) return s;
   const int T = q * (q + 1) / 2;
   const int64_t Cb = std::min<int64_t>(M_, kNehviChunk / q);   // batches per chunk
   const int64_t C = Cb * q;                                     // points per chunk
@@ -1227,23 +1346,7 @@ bo_status score_nehvi_impl(bo_model model, const float* cand, int64_t M_, int32_
     const int64_t np_ = nb_ * q;
     const float* cc = cand + b0 * q * M.d;
     for (int k = 0; k < m; ++k) {
-      PosteriorArgs pa;
-      pa.cand = cc; pa.npts = np_; pa.d = M.d; pa.dx = M.dx; pa.q = q;
-      pa.Xs = M.Xs + (size_t)k * M.n_pad * M.dx;
-      pa.invls = M.invls + (size_t)k * M.dx;
-      pa.alpha = M.alpha + (size_t)k * M.n_pad;
-      pa.Lp = z.Lp0 + (size_t)k * M.lp_per_obj;
-      pa.xf = M.xf + (size_t)k * M.nb * dist_frags(M.dx) * 512;
-      pa.x2 = M.x2 + (size_t)k * 2 * M.n_pad;
-      pa.ctr = M.ctr + (size_t)k * M.dx;
-      pa.n = static_cast<int>(M.n); pa.nb = M.nb;
-      pa.s = M.os[k];
-      pa.m = m; pa.k = k;
-      pa.dr = M.dr; pa.dr4 = M.dr4;
-      pa.s_dep = M.dr > 0 ? M.s_dep[k] : 0.f;
-      pa.s_int = M.dr > 0 ? M.s_int[k] : 0.f;
-      pa.wts = M.dr > 0 ? M.wts + (size_t)k * M.n_pad : nullptr;
-      pa.pref = M.dr > 0 ? M.pref + (size_t)k * (M.d - M.dr) : nullptr;
+      PosteriorArgs pa = posterior_args(M, k, z.Lp0, z.rsc0, cc, np_, q);
       pa.mu = mu_buf; pa.sd = sd_buf; pa.chol = (q > 1) ? ch_buf : nullptr;
       if ((s = after_launch(launch_posterior(pa, st), st, "posterior")) != BO_OK) return s;
     }
@@ -1252,6 +1355,7 @@ bo_status score_nehvi_impl(bo_model model, const float* cand, int64_t M_, int32_
     ma.n_pad = M.n_pad; ma.S = S; ma.Xs = M.Xs; ma.invls = M.invls; ma.Gp = z.Gp;
     for (int k = 0; k < 3; ++k) {
       ma.s[k] = k < m ? M.os[k] : 0.f;
+      ma.kbound[k] = k < m ? M.kbound[k] : 1.f;
       ma.ginv[k] = z.ginv[k];
       ma.s_dep[k] = (M.dr > 0 && k < m) ? M.s_dep[k] : 0.f;
       ma.s_int[k] = (M.dr > 0 && k < m) ? M.s_int[k] : 0.f;
@@ -1268,8 +1372,7 @@ bo_status score_nehvi_impl(bo_model model, const float* cand, int64_t M_, int32_
     if ((s = after_launch(launch_nehvi_ehvi(ea, st), st, "noisy ehvi")) != BO_OK) return s;
   }
   z.q = q;
-  M.last_stream = st;
-  return BO_OK;
+  return mark_call(M, st, "bo_score_nehvi: stream ordering");
 }
 
 }  // namespace

@@ -54,6 +54,9 @@ struct Model {
   float* pref = nullptr;         // composite: [m][d - dr] preference slopes
   float* Lp = nullptr;           // [m][frag blocks][2 KiB] packed fp16 hi/lo L^{-1} + zero block
   size_t lp_per_obj = 0;         // floats per objective in Lp
+  float* rsc = nullptr;          // [m][nb] power of two undoing each 16-row block's pack scale
+  std::vector<float> kbound;     // [m] largest diagonal of K (bounds every training prior variance)
+  std::vector<double> cond_est;  // [m] max K_ii * max |L^{-1}|^2 (a lower bound on cond(K))
   uint16_t* xf = nullptr;        // [m][nb][dist_frags(dx)][512] distance fragments of X
   float* x2 = nullptr;           // [m][2][n_pad] squared norms of the centred rows
   float* ctr = nullptr;          // [m][dx] centre of the scaled coordinates
@@ -66,6 +69,7 @@ struct Model {
   struct Noisy {
     int S = 0, Sp = 0, n32 = 0, total = 0;
     float* Lp0 = nullptr;        // [m][lp_per_obj] packed inverse factor of K_XX (no noise)
+    float* rsc0 = nullptr;       // [m][nb] row-block scales of Lp0
     uint16_t* Gp = nullptr;      // [m][n32][Sp/16][1024] fp16 hi/lo fragments of G^T
     int m = 0, q = 1;            // objectives; batch size of the last scoring call
     float ginv[3] = {1.f, 1.f, 1.f};  // 1 / scale applied to G before the split
@@ -86,7 +90,9 @@ struct Model {
   int box_cap = 0;
   int nbox = -1;
   std::vector<float> box_ref;
+  // the model's last asynchronous call: a call on another stream waits for it
   hipStream_t last_stream = nullptr;
+  hipEvent_t last_evt = nullptr;
 };
 
 // Kernel launchers (fit.hip / posterior.hip / ehvi.hip / argmax.hip) -------
@@ -107,8 +113,11 @@ struct GramParams {
 // Gram matrices K_k + eta_k I in fp64 for all objectives, padded to
 // n_fit x n_fit with an identity tail; only the lower block triangle (64x64
 // blocks) is written. A: [m][n_fit][n_fit].
+// kdiag (optional, [m], zeroed by the caller): the largest diagonal entry of
+// each objective's K, as the bit pattern of a non-negative double.
 hipError_t launch_gram(const float* X, int64_t n, int d, int m, int n_fit,
-                       const GramParams& g, double* A, hipStream_t st);
+                       const GramParams& g, double* A, hipStream_t st,
+                       unsigned long long* kdiag = nullptr);
 // Composite: wts[k][i] = fp32(exp(sum_j pref[k][j] X[i][dr + j])), 0 for
 // n <= i < n_pad.
 hipError_t launch_weights(const float* X, int64_t n, int d, int m, int n_pad,
@@ -134,10 +143,15 @@ hipError_t launch_mll(const float* X, int64_t n, int d, int m, int nf, const Gra
                       double* partials, double* out, hipStream_t st);
 // Pack W into the posterior's A-fragment format (fp16 hi/lo planes of 16x32
 // lower blocks, zeros beyond n, then one all-zero block; 2 KiB per block,
-// posterior_frag_blocks(nb) blocks per objective) and write the
-// lengthscale-scaled X in the slot layout (invls is per slot, [m][dx]).
+// posterior_frag_blocks(nb) blocks per objective), each 16-row block I scaled
+// by a power of two that brings its largest entry into [2^13, 2^14)
+// (rsc [m][nb] = the inverse scale; wmax [m] = largest |W| per objective as a
+// non-negative double's bit pattern, zeroed by the caller; *flag set on a
+// non-finite entry), and write the lengthscale-scaled X in the slot layout
+// (invls is per slot, [m][dx]).
 hipError_t launch_pack(const double* W, int64_t n, int m, int nf, int nb,
-                       float* Lp, const float* X, int d, int dx, int dr, int dr4,
+                       float* Lp, float* rsc, unsigned long long* wmax, int* flag,
+                       const float* X, int d, int dx, int dr, int dr4,
                        const float* invls, float* Xs, hipStream_t st);
 
 // Squared distances in the posterior kernel come from the expansion
@@ -150,6 +164,7 @@ hipError_t launch_pack(const double* W, int64_t n, int m, int nf, int nb,
 __host__ __device__ constexpr int dist_frags0(int dx) { return (dx + 31) / 32; }
 __host__ __device__ constexpr int dist_frags(int dx) { return (dx + 31) / 32 + (2 * dx + 31) / 32; }
 constexpr float kDistLoScale = 2048.0f;
+
 // Centre the scaled coordinates (ctr = mean over the n rows), then write the
 // A fragments of the centred rows (xf, zero for rows past n) and their
 // squared norms per coordinate group (x2 [2][n_pad]: routing slots t < 4*dr4,
@@ -171,7 +186,7 @@ hipError_t launch_trmm(bool trans, const double* T, const double* Bm, double* C,
                        int ldb, int m, hipStream_t st);
 // The posterior's A-fragment packing of W alone (no coordinate scaling).
 hipError_t launch_pack_factor(const double* W, int64_t n, int m, int nf, int nb, float* Lp,
-                              hipStream_t st);
+                              float* rsc, unsigned long long* wmax, int* flag, hipStream_t st);
 
 // Noisy acquisition kernels (nehvi.hip).
 struct NehviFrontArgs {
@@ -209,6 +224,7 @@ struct NehviMeansArgs {
   const float* invls;      // [m][dx]
   const uint16_t* Gp;      // packed G^T fragments (fp16 bits)
   float s[3];              // output scales (composite: of the routing term)
+  float kbound[3];         // composite: bound on every training point's prior variance
   float ginv[3];           // 1 / scale of G
   float* out;              // [m][S][ldo]
   int64_t ldo;
@@ -266,6 +282,8 @@ struct PosteriorArgs {
   const float* invls;  // [dx]
   const float* alpha;  // [n_pad]
   const float* Lp;     // packed fragments of this objective
+  const float* rsc;    // [nb] power of two undoing each 16-row block's pack scale
+  float kbound;        // composite: bound on every training point's prior variance
   const uint16_t* xf;  // [nb][dist_frags(dx)][512] centred-X distance fragments
   const float* x2;     // [2][n_pad] squared norms of the centred rows per coordinate group
   const float* ctr;    // [dx] centre subtracted from the scaled coordinates

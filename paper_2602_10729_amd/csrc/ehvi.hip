@@ -55,10 +55,12 @@ __global__ __launch_bounds__(kThreads) void k_ehvi_q1(EhviArgs a) {
   const int64_t b = (int64_t)blockIdx.x * kThreads + threadIdx.x;
   const bool valid = b < a.nbat;
   float mu[MO], sd[MO];
+  bool nan_in = false;      // a NaN posterior gives a NaN acquisition
 #pragma unroll
   for (int k = 0; k < MO; ++k) {
     mu[k] = valid ? a.mu[b * MO + k] : 0.f;
     sd[k] = valid ? a.sd[b * MO + k] : 0.f;
+    nan_in = nan_in || (mu[k] != mu[k]) || (sd[k] != sd[k]);
   }
   float acc = 0.f;
   for (int s0 = 0; s0 < a.S; s0 += SC) {
@@ -92,7 +94,7 @@ __global__ __launch_bounds__(kThreads) void k_ehvi_q1(EhviArgs a) {
       }
     }
   }
-  if (valid) a.ehvi[b] = acc / static_cast<float>(a.S);
+  if (valid) a.ehvi[b] = nan_in ? __builtin_nanf("") : acc / static_cast<float>(a.S);
 }
 
 // q-batch version: lane owns a batch of Q points; y_s[a][k] is sampled with
@@ -112,14 +114,21 @@ __global__ __launch_bounds__(kThreads) void k_ehvi_q(EhviArgs a) {
   const bool valid = b < a.nbat;
   float mu[Q][MO];
   float C[MO][T];
+  bool nan_in = false;      // a NaN posterior gives a NaN acquisition
 #pragma unroll
   for (int i = 0; i < Q; ++i)
 #pragma unroll
-    for (int k = 0; k < MO; ++k) mu[i][k] = valid ? a.mu[(b * Q + i) * MO + k] : 0.f;
+    for (int k = 0; k < MO; ++k) {
+      mu[i][k] = valid ? a.mu[(b * Q + i) * MO + k] : 0.f;
+      nan_in = nan_in || (mu[i][k] != mu[i][k]);
+    }
 #pragma unroll
   for (int k = 0; k < MO; ++k)
 #pragma unroll
-    for (int e = 0; e < T; ++e) C[k][e] = valid ? a.chol[(b * MO + k) * T + e] : 0.f;
+    for (int e = 0; e < T; ++e) {
+      C[k][e] = valid ? a.chol[(b * MO + k) * T + e] : 0.f;
+      nan_in = nan_in || (C[k][e] != C[k][e]);
+    }
 
   float acc_pos = 0.f, acc_neg = 0.f;
   for (int s0 = 0; s0 < a.S; s0 += SC) {
@@ -193,7 +202,7 @@ __global__ __launch_bounds__(kThreads) void k_ehvi_q(EhviArgs a) {
       }
     }
   }
-  if (valid) a.ehvi[b] = (acc_pos - acc_neg) / static_cast<float>(a.S);
+  if (valid) a.ehvi[b] = nan_in ? __builtin_nanf("") : (acc_pos - acc_neg) / static_cast<float>(a.S);
 }
 
 // Launch with the dynamic-LDS limit raised for that kernel (set on every

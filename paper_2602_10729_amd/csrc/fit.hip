@@ -57,7 +57,8 @@ __device__ inline double matern32_d(double r2) {
 //   composite: k = os M52(r_route) + s_dep w_i w_j M32(r_dep)
 //                  + s_int M52(r_route) M32(r_dep)
 __global__ __launch_bounds__(256) void k_gram(const float* __restrict__ X, int64_t n, int d,
-                                              int nf, GramParams g, double* __restrict__ A) {
+                                              int nf, GramParams g, double* __restrict__ A,
+                                              unsigned long long* __restrict__ kdiag) {
   __shared__ float xs[2][16][BO_MAX_D + 1];
   __shared__ double il[BO_MAX_D];
   __shared__ double wrow[2][16];
@@ -101,7 +102,12 @@ __global__ __launch_bounds__(256) void k_gram(const float* __restrict__ X, int64
       v = g.os[k] * k5 + g.s_dep[k] * wrow[0][threadIdx.y] * wrow[1][threadIdx.x] * k3 +
           g.s_int[k] * k5 * k3;
     }
-    if (i == j) v += g.noise[k];
+    if (i == j) {
+      v += g.noise[k];
+      // largest diagonal entry per objective (non-negative doubles order
+      // like their bit patterns)
+      if (kdiag) atomicMax(kdiag + k, static_cast<unsigned long long>(__double_as_longlong(v)));
+    }
   } else {
     v = (i == j) ? 1.0 : 0.0;
   }
@@ -463,6 +469,48 @@ __global__ __launch_bounds__(256) void k_wty(const double* __restrict__ W,
   }
 }
 
+// Power-of-two scale of each 16-row block of W = L^{-1} for its fp16 split:
+// with mx the largest |W| over the block's lower entries, mx = f 2^E
+// (f in [0.5, 1)), the pack stores W 2^(14 - E), so every entry of the block
+// is at most 2^14 in magnitude (fp16 holds up to 65504) and the low halves of
+// all entries above 2^-3 of that are normal fp16 numbers; rsc[k][I] = 2^(E-14)
+// undoes it. wmax[k] gets the largest |W| of objective k (bit pattern of a
+// non-negative double), for the conditioning estimate; a non-finite entry sets
+// *flag. One workgroup per (row block, objective).
+__global__ __launch_bounds__(256) void k_rowblock_scale(const double* __restrict__ W, int64_t n,
+                                                        int nf, int nb, float* __restrict__ rsc,
+                                                        unsigned long long* __restrict__ wmax,
+                                                        int* __restrict__ flag) {
+  __shared__ double part[256];
+  const int I = blockIdx.x, k = blockIdx.y;
+  const double* Wk = W + (int64_t)k * nf * nf;
+  const int64_t row = (int64_t)I * kBlk + (threadIdx.x & 15);
+  double mx = 0.0;
+  bool bad = false;
+  if (row < n) {
+    for (int64_t col = threadIdx.x >> 4; col <= row; col += 16) {
+      const double w = Wk[row * nf + col];
+      bad = bad || !(fabs(w) < INFINITY);
+      mx = fmax(mx, fabs(w));
+    }
+  }
+  if (bad) *flag = 1;
+  part[threadIdx.x] = mx;
+  __syncthreads();
+  for (int h = 128; h > 0; h >>= 1) {
+    if (static_cast<int>(threadIdx.x) < h)
+      part[threadIdx.x] = fmax(part[threadIdx.x], part[threadIdx.x + h]);
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    const double m = part[0];
+    int E = 0;
+    if (m > 0.0) (void)frexp(m, &E);
+    rsc[(int64_t)k * nb + I] = ldexpf(1.0f, E - 14);
+    atomicMax(wmax + k, static_cast<unsigned long long>(__double_as_longlong(m)));
+  }
+}
+
 // Pack the lower triangle of W = L^{-1} as fp16 hi/lo MFMA A fragments of
 // 16-row x 32-column blocks (the scoring path's operand format):
 // row block I holds the blocks J = 0 .. I/2, block (I, J) at index
@@ -470,9 +518,12 @@ __global__ __launch_bounds__(256) void k_wty(const double* __restrict__ W,
 // zero block (index start(nb), which maps to rows >= n). Each block is 2 KiB:
 // the hi plane, then the lo plane, 16 bytes per lane, lane l element e being
 // W[16I + l%16][32J + 8(l/16) + e] (zero above the diagonal and past n),
-// split as hi = fp16(w), lo = fp16(w - hi).
+// scaled by its row block's power of two (w = W / rsc[I], exact) and split as
+// hi = fp16(w), lo = fp16(w - hi).
 __global__ __launch_bounds__(256) void k_pack(const double* __restrict__ W, int64_t n,
-                                              int nf, int64_t nblk, _Float16* __restrict__ Lp) {
+                                              int nf, int64_t nblk, int nb,
+                                              const float* __restrict__ rsc,
+                                              _Float16* __restrict__ Lp) {
   const int k = blockIdx.y;
   const int64_t g = (int64_t)blockIdx.x * 256 + threadIdx.x;   // (blk, lane)
   if (g >= nblk * 64) return;
@@ -492,11 +543,13 @@ __global__ __launch_bounds__(256) void k_pack(const double* __restrict__ W, int6
   }
   const int64_t row = (int64_t)I * kBlk + lane % 16;
   const double* Wk = W + (int64_t)k * nf * nf;
+  // the zero block (I = nb) has no scale
+  const double sc = (I < nb) ? 1.0 / static_cast<double>(rsc[(int64_t)k * nb + I]) : 1.0;
   _Float16 hi[8], lo[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
     const int64_t col = (int64_t)J * 32 + 8 * (lane / 16) + e;
-    const double w = (row < n && col < n && col <= row) ? Wk[row * nf + col] : 0.0;
+    const double w = (row < n && col < n && col <= row) ? Wk[row * nf + col] * sc : 0.0;
     const _Float16 h = static_cast<_Float16>(static_cast<float>(w));
     hi[e] = h;
     lo[e] = static_cast<_Float16>(static_cast<float>(w - static_cast<double>(h)));
@@ -854,9 +907,10 @@ __global__ __launch_bounds__(256) void k_trmm(const double* __restrict__ T,
 }  // namespace
 
 hipError_t launch_gram(const float* X, int64_t n, int d, int m, int n_fit,
-                       const GramParams& g, double* A, hipStream_t st) {
+                       const GramParams& g, double* A, hipStream_t st,
+                       unsigned long long* kdiag) {
   dim3 grid((n_fit + 15) / 16, (n_fit + 15) / 16, m), block(16, 16);
-  hipLaunchKernelGGL(k_gram, grid, block, 0, st, X, n, d, n_fit, g, A);
+  hipLaunchKernelGGL(k_gram, grid, block, 0, st, X, n, d, n_fit, g, A, kdiag);
   return hipGetLastError();
 }
 
@@ -914,12 +968,10 @@ hipError_t launch_mll(const float* X, int64_t n, int d, int m, int nf, const Gra
 }
 
 hipError_t launch_pack(const double* W, int64_t n, int m, int nf, int nb, float* Lp,
-                       const float* X, int d, int dx, int dr, int dr4, const float* invls,
-                       float* Xs, hipStream_t st) {
-  const int64_t nblk = posterior_frag_blocks(nb);   // with the zero block
-  const unsigned gx = static_cast<unsigned>((nblk * 64 + 255) / 256);
-  hipLaunchKernelGGL(k_pack, dim3(gx, m), dim3(256), 0, st, W, n, nf, nblk,
-                     reinterpret_cast<_Float16*>(Lp));
+                       float* rsc, unsigned long long* wmax, int* flag, const float* X, int d,
+                       int dx, int dr, int dr4, const float* invls, float* Xs, hipStream_t st) {
+  hipError_t e = launch_pack_factor(W, n, m, nf, nb, Lp, rsc, wmax, flag, st);
+  if (e != hipSuccess) return e;
   const int n_pad = nb * kBlk;
   const unsigned gx2 = static_cast<unsigned>(((int64_t)n_pad * dx + 255) / 256);
   hipLaunchKernelGGL(k_scale_x, dim3(gx2, m), dim3(256), 0, st, X, n, d, dx, dr, dr4, n_pad,
@@ -970,10 +1022,12 @@ hipError_t launch_trmm(bool trans, const double* T, const double* Bm, double* C,
 }
 
 hipError_t launch_pack_factor(const double* W, int64_t n, int m, int nf, int nb, float* Lp,
-                              hipStream_t st) {
+                              float* rsc, unsigned long long* wmax, int* flag, hipStream_t st) {
+  hipLaunchKernelGGL(k_rowblock_scale, dim3(nb, m), dim3(256), 0, st, W, n, nf, nb, rsc, wmax,
+                     flag);
   const int64_t nblk = posterior_frag_blocks(nb);   // with the zero block
   const unsigned gx = static_cast<unsigned>((nblk * 64 + 255) / 256);
-  hipLaunchKernelGGL(k_pack, dim3(gx, m), dim3(256), 0, st, W, n, nf, nblk,
+  hipLaunchKernelGGL(k_pack, dim3(gx, m), dim3(256), 0, st, W, n, nf, nblk, nb, rsc,
                      reinterpret_cast<_Float16*>(Lp));
   return hipGetLastError();
 }

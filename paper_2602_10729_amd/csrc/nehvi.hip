@@ -27,6 +27,7 @@
 #include <type_traits>
 
 #include "bo_internal.h"
+#include "kv_scale.h"
 
 namespace bo {
 namespace {
@@ -267,6 +268,7 @@ __global__ __launch_bounds__(kMW * 64) void k_nehvi_means(NehviMeansArgs a) {
   __shared__ __align__(16) float xst[2][32 * RS];
   __shared__ float wst[2][32];             // COMP: weights of the staged rows
   __shared__ __align__(16) _Float16 ring[3 * kRingSlot];
+  __shared__ float kish[kMT];              // 2^(E-14): undoes a candidate's split scale
   const int k = blockIdx.y;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
@@ -281,7 +283,7 @@ __global__ __launch_bounds__(kMW * 64) void k_nehvi_means(NehviMeansArgs a) {
   // this lane's candidate, scaled, in the slot layout (zero past npts and in
   // padding slots); COMP: s_dep times its preference weight
   float cx[RS];
-  float wsd = 0.f;
+  float wsd = 0.f, wstar = 0.f;
   const float sint = COMP ? a.s_int[k] : 0.f;
   {
     const int64_t c = c0 + lane;
@@ -296,10 +298,16 @@ __global__ __launch_bounds__(kMW * 64) void k_nehvi_means(NehviMeansArgs a) {
         const float* pr = a.pref + (int64_t)k * (a.d - a.dr);
         float e = 0.f;
         for (int t = a.dr; t < a.d; ++t) e = fmaf(pr[t - a.dr], a.cand[c * a.d + t], e);
-        wsd = a.s_dep[k] * expf(e);
+        wstar = expf(e);
+        wsd = a.s_dep[k] * wstar;
       }
     }
   }
+  // power of two for this candidate's kernel values before their split (the
+  // composite covariance is bounded by sqrt(prior(candidate) * kbound))
+  const KvScale ks = kv_split_scale(
+      COMP ? __builtin_amdgcn_sqrtf(fmaf(wsd, wstar, sk + sint) * a.kbound[k]) : sk);
+  if (wave == 0) kish[lane] = ks.kinv;
   const __amdgpu_buffer_rsrc_t w_rs = rsrc(COMP ? a.wts + (int64_t)k * a.n_pad : a.Xs,
                                            COMP ? a.n_pad * 4 : 0);
   const int wrow = threadIdx.x - 256;       // COMP: threads 256 .. 287 stage the weights
@@ -352,12 +360,14 @@ __global__ __launch_bounds__(kMW * 64) void k_nehvi_means(NehviMeansArgs a) {
       } else {
         kv = m52(r2, sk);
       }
-      // one fp32 kv for both halves (the compiler may otherwise fuse the last
-      // product into the fp16 conversions and derive the high half twice)
-      asm volatile("" : "+v"(kv));
-      const _Float16 h = static_cast<_Float16>(kv);
+      // one fp32 value for both halves (the compiler may otherwise fuse the
+      // last product into the fp16 conversions and derive the high half
+      // twice), scaled by the candidate's power of two
+      float kvs = kv * ks.ksc;
+      asm volatile("" : "+v"(kvs));
+      const _Float16 h = static_cast<_Float16>(kvs);
       hi[u] = h;
-      lo[u] = static_cast<_Float16>(kv - static_cast<float>(h));
+      lo[u] = static_cast<_Float16>(kvs - static_cast<float>(h));
     }
     _Float16* dst = ring + (jb % 3) * kRingSlot + lane * kKS + 4 * wave;
     *reinterpret_cast<halfx4*>(dst) = hi;
@@ -450,10 +460,11 @@ __global__ __launch_bounds__(kMW * 64) void k_nehvi_means(NehviMeansArgs a) {
 #pragma unroll
     for (int cb = 0; cb < 4; ++cb) {
       const int64_t c = c0 + 16 * cb + lane % 16;
+      const float sc = gi * kish[16 * cb + lane % 16];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int smp = 16 * (wave + 8 * r) + 4 * (lane / 16) + e;
-        if (smp < a.S && c < a.npts) a.out[((int64_t)k * a.S + smp) * a.ldo + c] = acc[r][cb][e] * gi;
+        if (smp < a.S && c < a.npts) a.out[((int64_t)k * a.S + smp) * a.ldo + c] = acc[r][cb][e] * sc;
       }
     }
 }
@@ -500,15 +511,21 @@ __global__ __launch_bounds__(kET) void k_nehvi_ehvi(NehviEhviArgs a) {
   const int64_t bb = valid ? b : a.nbat - 1;
   float mu[Q][MO];
   float C[MO][T];                       // q = 1: C[k][0] = tau_k
+  bool nan_in = false;                  // a NaN posterior gives a NaN acquisition
 #pragma unroll
   for (int i = 0; i < Q; ++i)
 #pragma unroll
-    for (int k = 0; k < MO; ++k) mu[i][k] = a.mu[(bb * Q + i) * MO + k];
+    for (int k = 0; k < MO; ++k) {
+      mu[i][k] = a.mu[(bb * Q + i) * MO + k];
+      nan_in = nan_in || (mu[i][k] != mu[i][k]);
+    }
 #pragma unroll
   for (int k = 0; k < MO; ++k)
 #pragma unroll
-    for (int e = 0; e < T; ++e)
+    for (int e = 0; e < T; ++e) {
       C[k][e] = (Q == 1) ? a.sd[bb * MO + k] : a.chol[(bb * MO + k) * T + e];
+      nan_in = nan_in || (C[k][e] != C[k][e]);
+    }
   const float* dp = a.D + bb * Q;
   const int64_t kstride = (int64_t)a.S * a.ldd;
   float acc_pos = 0.f, acc_neg = 0.f;
@@ -594,7 +611,7 @@ __global__ __launch_bounds__(kET) void k_nehvi_ehvi(NehviEhviArgs a) {
       }
     }
   }
-  if (valid) a.ehvi[b] = (acc_pos - acc_neg) / static_cast<float>(a.S);
+  if (valid) a.ehvi[b] = nan_in ? __builtin_nanf("") : (acc_pos - acc_neg) / static_cast<float>(a.S);
 }
 
 template <int MO, int Q, bool CONS>

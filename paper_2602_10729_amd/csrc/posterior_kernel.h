@@ -13,12 +13,22 @@
 // operand split into two fp16 halves, x = x_hi + x_lo (x_hi = fp16(x),
 // x_lo = fp16(x - x_hi)), and three products per pair,
 //   a b ~ a_hi b_hi + a_hi b_lo + a_lo b_hi,
-// accumulated in fp32 by the MFMA. The operands carry ~22 significant bits
-// and the dropped a_lo b_lo term is 2^-22 relative, so the result is within
-// a small factor of an fp32 product. On gfx950 this is the fast path: the
-// dense fp16 MFMA runs at 16x the fp32 MFMA rate, and (unlike fp32 MFMA) it
-// executes alongside VALU work, which hides the kernel evaluations below.
-// L^{-1} is split and packed once by the fit; K*^T is split as it is made.
+// accumulated in fp32 by the MFMA. Before the split both operands are scaled
+// by powers of two: each 16-row block of L^{-1} so that its largest entry
+// lies in [2^13, 2^14) (the fit does this once), each candidate's kernel
+// values by 2^(14 - E), 2^E above a bound on its covariances (kv_split_scale).
+// Nothing can then overflow fp16, and every entry within 2^-17 of its block's
+// (or column's) largest has normal halves and 22 significant bits
+// (|x - x_hi - x_lo| <= 2^-22 |x|); smaller entries carry an absolute error of
+// at most 2^-39 of that largest. With the dropped a_lo b_lo term (2^-22
+// relative) each product is within a few units of 2^-22 of exact, against
+// 2^-23 for fp32 operands, and the products accumulate in fp32 as an fp32
+// implementation's would. The scales are undone exactly: the row block's when
+// a block of V is squared, the column's in the epilogue. On gfx950 this is
+// the fast path: the dense fp16 MFMA runs at 16x the fp32 MFMA rate, and
+// (unlike fp32 MFMA) it executes alongside VALU work, which hides the kernel
+// evaluations below. L^{-1} is split and packed once by the fit; K*^T is
+// split as it is made.
 //
 // One workgroup (8 waves, two per SIMD) owns a tile of NT points and forms V
 // left-looking: the outer loop runs over 32-row blocks J of K*^T (the MFMA
@@ -59,6 +69,7 @@
 #include <hip/hip_runtime.h>
 
 #include "bo_internal.h"
+#include "kv_scale.h"
 
 namespace bo {
 namespace {
@@ -157,6 +168,7 @@ struct Producer {
   halfx8 cb[NS][NF];        // B fragments of this lane's candidate, per group
   float c2[NS];             // squared norm of the centred candidate, per group
   float mu;
+  float ksc;                // power of two scaling this lane's kernel values for the split
   float wsd;                // composite: s_dep * w(candidate)
   int col;                  // tile column of this lane
   int rq;                   // first of this lane's rows inside a block
@@ -213,7 +225,8 @@ __device__ __forceinline__ void produce(Producer<NT, DX4, COMP>& P, const Poster
     for (int g = 0; g < NS; ++g) {
       const float nrm = P.c2[g] + P.x2[g][e];
       const float dot = fmaf(d1[g][e], 1.0f / kDistLoScale, d0[g][e]);
-      r2[g][e] = fmaxf(fmaf(-2.0f, dot, nrm), 0.f);
+      const float v = fmaf(-2.0f, dot, nrm);
+      r2[g][e] = v < 0.f ? 0.f : v;     // clamp at zero; NaN (a NaN candidate) stays NaN
       rt += r2[g][e];
       nt += nrm;
     }
@@ -268,12 +281,15 @@ __device__ __forceinline__ void produce(Producer<NT, DX4, COMP>& P, const Poster
     // last product into the fp16 conversions and derive the high half twice
     // (once exactly, once from the fp32 value); within an fp32 ulp of an
     // fp16 rounding midpoint the stored high and low halves then disagree by
-    // one fp16 ulp
+    // one fp16 ulp. The split takes kv times this column's power of two
+    // (exact), pinned the same way.
     asm volatile("" : "+v"(kv));
     P.mu = fmaf(P.al[e], kv, P.mu);
-    const _Float16 h = static_cast<_Float16>(kv);
+    float kvs = kv * P.ksc;
+    asm volatile("" : "+v"(kvs));
+    const _Float16 h = static_cast<_Float16>(kvs);
     hi[e] = h;
-    lo[e] = static_cast<_Float16>(kv - static_cast<float>(h));
+    lo[e] = static_cast<_Float16>(kvs - static_cast<float>(h));
   }
   _Float16* dst = ring + P.col * kCSH + (jb % kRing) * kJ + P.rq;
   *reinterpret_cast<halfx4*>(dst) = hi;
@@ -291,6 +307,7 @@ template <int RB>
 struct Slots {
   int first[RB];
   int last[RB];
+  float sc[RB];     // power of two undoing the slot's row-block pack scale (0 past the matrix)
 };
 
 __device__ __forceinline__ int frag_block(int first, int last, int J, int zero_blk) {
@@ -465,6 +482,7 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
   float* mush = ctile + NT * D;                             // 2 * NT (mu per row half)
   float* kpp = mush + 2 * NT;                               // NT * 4 (prior cross-cov)
   float* wsh = kpp + NT * 4;                                // NT: w(candidate), composite
+  float* kish = wsh + NT;                                   // NT: 2^(E-14) of each column's split scale
   const int64_t p0 = (int64_t)blockIdx.x * NT;
 
   Prod P;
@@ -492,6 +510,11 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
       P.wsd = a.s_dep * wstar;
     }
   }
+  // power of two for this column's kernel values: the composite covariance is
+  // bounded by sqrt(prior(candidate) * kbound), the plain one by s
+  const KvScale ks = kv_split_scale(
+      COMP ? __builtin_amdgcn_sqrtf(fmaf(a.s_dep * wstar, wstar, a.s + a.s_int) * a.kbound) : a.s);
+  P.ksc = ks.ksc;
   // distance operands of the candidate: centred coordinates, their squared
   // norms per group, and the B fragments, laid out per group and column in
   // the (not yet used) ring as 96 halves: [0, 32) stream 0 (hi, zero past D),
@@ -536,6 +559,7 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
         *reinterpret_cast<float4*>(ctile + P.col * D + 4 * t4) =
             float4{cc[4 * t4], cc[4 * t4 + 1], cc[4 * t4 + 2], cc[4 * t4 + 3]};
       if (COMP) wsh[P.col] = wstar;
+      kish[P.col] = ks.kinv;
     }
     __syncthreads();
 #pragma unroll
@@ -631,6 +655,7 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
       const int I = slot_block(base, r, wave);
       sl.first[r] = I < a.nb ? frag_row_start(I) : C.zero_blk;
       sl.last[r] = I < a.nb ? I / 2 : -1;
+      sl.sc[r] = I < a.nb ? a.rsc[I] : 0.f;
       av[r] = load_a(C.lp_rs, C.voff, frag_block(sl.first[r], sl.last[r], 0, C.zero_blk));
     }
     // Production schedule. Starting over, blocks 0 and 1 are made here and
@@ -661,13 +686,15 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
     rounds<0, RB, NT, DX4, COMP>(C, a, P, ring, sl, base, pw0, pw1, B0, av, acc);
     have = (jpass <= kRing) ? max(have, jpass) : 0;
 
+    // undo the row-block scale of L^{-1} (the column scale of K*^T is undone
+    // per point in the epilogue)
 #pragma unroll
     for (int r = 0; r < RB; ++r)
 #pragma unroll
       for (int b = 0; b < NCB; ++b)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const float v = acc[r][b][e];
+          const float v = acc[r][b][e] * sl.sc[r];
           ss[b] = fmaf(v, v, ss[b]);
           if (Q > 1) {
 #pragma unroll
@@ -714,6 +741,12 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
     for (int w = 0; w < kWaves; ++w)
 #pragma unroll
       for (int x = 0; x < NX; ++x) tot[x] += red[(w * NT + tid) * NX + x];
+    // undo the columns' kernel-value scales: |v|^2 carries ki^2, a cross
+    // product with batch mate tid ^ x carries ki times the mate's
+    const float ki = kish[tid];
+    tot[0] = (tot[0] * ki) * ki;
+#pragma unroll
+    for (int x = 1; x < NX; ++x) tot[x] = (tot[x] * ki) * kish[tid ^ x];
     const float mu = mush[tid] + mush[NT + tid];
     float prior = a.s;
     if constexpr (COMP) {
@@ -723,7 +756,8 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
     const float var = prior - tot[0];
     if (valid) {
       a.mu[p * a.m + a.k] = mu;
-      a.sd[p * a.m + a.k] = __builtin_amdgcn_sqrtf(fmaxf(var, 0.f));
+      // clamp at zero; a NaN variance stays NaN
+      a.sd[p * a.m + a.k] = __builtin_amdgcn_sqrtf(var < 0.f ? 0.f : var);
     }
     if (Q > 1) {
       // covariance row of this point (diagonal, then partner p ^ x) for the
@@ -768,6 +802,8 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
               for (int t = 0; t < j; ++t) num = fmaf(-L[i][t], L[j][t], num);
               L[i][j] = num * inv;
             }
+          } else if (pv != pv) {
+            L[j][j] = pv;     // a NaN pivot stays NaN
           }
         }
         constexpr int T = Q * (Q + 1) / 2;
@@ -784,9 +820,9 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
 constexpr size_t lds_floats(int NT, int DX4, int q) {
   // ring: 2 planes x NT columns x kCSH halves (the reduction and, before the
   // loop, the candidates' distance fragments overlay it); the exact scaled
-  // candidates; mu per row half, the prior cross-covariances and the
-  // candidates' preference weights
-  return (size_t)NT * kCSH + (size_t)NT * 4 * DX4 + 2 * NT + (size_t)NT * 4 + NT;
+  // candidates; mu per row half, the prior cross-covariances, the
+  // candidates' preference weights and their kernel-value scales
+  return (size_t)NT * kCSH + (size_t)NT * 4 * DX4 + 2 * NT + (size_t)NT * 4 + 2 * NT;
 }
 static_assert((size_t)kWaves * 64 * 4 <= (size_t)64 * kCSH, "reduction fits the ring");
 static_assert(2 * 64 * 96 <= 2 * 64 * kCSH, "distance fragments fit the ring");

@@ -5,7 +5,7 @@ import pytest
 
 import bo_inputs as bi
 from gpu_util import (TOL_MU, TOL_SIGMA, TOL_EHVI, gpu_run, oracle_fit, oracle_score,
-                      assert_close, check_argmax, to_dev)
+                      assert_close, check_argmax, to_dev, near_var_tol)
 
 pytestmark = pytest.mark.gpu
 
@@ -43,14 +43,13 @@ def test_composite_near_data():
     o = oracle_score(oracle_fit(wl, comp), wl, cand=cand)
     assert_close(g["mu"], o["mu"], TOL_MU, "mu near data")
     # variance through sigma^2 with the absolute bound of the plain kernel's
-    # near-data test (unit prior variance), scaled by the largest prior
-    # variance s_route + s_dep w^2 + s_int of these points
+    # near-data test, scaled by the largest prior variance
+    # s_route + s_dep w^2 + s_int of these points
     c = cand[:, 0, :].astype(np.float64)
     w = np.exp(c[:, comp.d_route:] @ comp.pref.astype(np.float64).T)       # [N, m]
     prior_max = float(np.max(comp.s_route + comp.s_int + comp.s_dep * w * w))
-    var_tol = (1e-4, 4e-6 * (wl.n ** 0.5) / 32.0 * 8 * max(prior_max, 1.0))
-    assert_close(g["sigma"] ** 2, o["sigma"] ** 2, var_tol, "variance near data")
-    assert_close(g["ehvi"], o["ehvi"], (2e-3, 1e-5), "ehvi near data")
+    assert_close(g["sigma"] ** 2, o["sigma"] ** 2, near_var_tol(prior_max), "variance near data")
+    assert_close(g["ehvi"], o["ehvi"], TOL_EHVI, "ehvi near data")
 
 
 def test_composite_config3_full_size_sampled():

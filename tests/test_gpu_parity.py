@@ -9,7 +9,7 @@ import pytest
 import bo_inputs as bi
 import oracle as O
 from gpu_util import (TOL_MU, TOL_SIGMA, TOL_EHVI, gpu_run, oracle_fit,
-                      oracle_score, assert_close, check_argmax, to_dev)
+                      oracle_score, assert_close, check_argmax, near_var_tol, to_dev)
 
 pytestmark = pytest.mark.gpu
 
@@ -36,8 +36,6 @@ SMALL = [(0, 4096), (1, 3001), (2, 2003), (4, 61)]
 @pytest.mark.parametrize("cfg,M", SMALL)
 @pytest.mark.parametrize("seed", [0, 1, 2])
 def test_small_config_parity(cfg, M, seed):
-    if cfg == 4 and seed == 2:
-        pytest.skip("config 4 checked on seeds 0 and 1 (oracle cost)")
     _announce("small", cfg, seed, M)
     wl = bi.make_config(cfg, seed=seed, M=M)
     g = gpu_run(wl)
@@ -92,25 +90,27 @@ def test_config3_full_size_sampled():
 
 def test_config4_full_size_sampled():
     _announce("config4 full sampled", 0)
-    _sampled_full_size(4, 12)
+    _sampled_full_size(4, 256)
 
 
-def test_near_data_candidates():
+@pytest.mark.parametrize("cfg", [0, 2, 4])
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_near_data_candidates(cfg, seed):
     """Candidates at distance ~0.01 from observations: large k*, the solve
-    does real work and sigma approaches the noise level. sigma is compared
-    through the variance with an absolute bound derived from fp32 rounding
-    of |v|^2 ~ 1 (see DESIGN)."""
-    for cfg in (0, 2):
-        _announce("near-data", cfg)
-        wl = bi.make_config(cfg, seed=0, M=8)
-        cand = bi.near_data_candidates(wl, 512, scale=0.01)
-        g = gpu_run(wl, cand=cand)
-        o = oracle_score(oracle_fit(wl), wl, cand=cand)
-        assert_close(g["mu"], o["mu"], TOL_MU, "mu near data")
-        var_tol = (1e-4, 4e-6 * (wl.n ** 0.5) / 32.0 * 8)
-        assert_close(g["sigma"] ** 2, o["sigma"] ** 2, var_tol, "variance near data")
-        # EHVI is a smooth function of (mu, sigma): same relative bar
-        assert_close(g["ehvi"], o["ehvi"], (2e-3, 1e-5), "ehvi near data")
+    does real work and sigma approaches the noise level, where
+    sigma^2 = k(x,x) - |v|^2 cancels. sigma is compared through the variance
+    with an absolute bound, NEAR_VAR_ULPS units of 2^-24 of the prior variance
+    (twice the worst error these cases show); mu and the EHVI at the usual
+    bar. The worst error/bound ratios are logged."""
+    _announce("near-data", cfg, seed)
+    wl = bi.make_config(cfg, seed=seed, M=8)
+    cand = bi.near_data_candidates(wl, 512 if cfg != 4 else 64, scale=0.01)
+    g = gpu_run(wl, cand=cand)
+    o = oracle_score(oracle_fit(wl), wl, cand=cand)
+    assert_close(g["mu"], o["mu"], TOL_MU, f"mu near data cfg{cfg} seed{seed}")
+    assert_close(g["sigma"] ** 2, o["sigma"] ** 2, near_var_tol(1.0),
+                 f"variance near data cfg{cfg} seed{seed}")
+    assert_close(g["ehvi"], o["ehvi"], TOL_EHVI, f"ehvi near data cfg{cfg} seed{seed}")
 
 
 def test_small_models_and_odd_shapes():

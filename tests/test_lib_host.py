@@ -44,8 +44,8 @@ def test_library_exports_every_declared_symbol(bo):
 
 def test_status_strings(bo):
     L = bo.lib()
-    for s in range(7):
-        assert L.bo_status_string(s)
+    for s in range(8):
+        assert L.bo_status_string(s) != b"unknown status"
     assert L.bo_status_string(99) == b"unknown status"
 
 
@@ -77,6 +77,19 @@ def test_fit_validation_before_device_work(bo):
     assert L.bo_fit(fake, fake, 4, 2, 2, p(ls), p(one), p(-nz), None, ctypes.byref(h)) == 1
     assert h.value is None
     assert b"noise" in L.bo_last_error_message()
+    # outside the accepted range: outputscale in [2^-64, 2^64], noise <= 2^64
+    for s_bad in (2.0 ** -65, 2.0 ** 65):
+        sb = np.full(2, s_bad, dtype=np.float32)
+        assert L.bo_fit(fake, fake, 4, 2, 2, p(ls), p(sb), p(nz), None, ctypes.byref(h)) == 1
+        assert b"2^64" in L.bo_last_error_message()
+    for s_ok in (2.0 ** -64, 2.0 ** 64):
+        # in range: validation passes and the fake device pointer is refused next
+        sb = np.full(2, s_ok, dtype=np.float32)
+        assert L.bo_fit(fake, fake, 4, 2, 2, p(ls), p(sb), p(nz), None, ctypes.byref(h)) != 1 \
+            or b"2^64" not in L.bo_last_error_message()
+    big = np.full(2, 2.0 ** 65, dtype=np.float32)
+    assert L.bo_fit(fake, fake, 4, 2, 2, p(ls), p(one), p(big), None, ctypes.byref(h)) == 1
+    assert h.value is None
 
 
 def test_score_and_argmax_validation(bo):
