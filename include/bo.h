@@ -265,6 +265,35 @@ bo_status bo_score_constrained(bo_model model, const float* cand, int64_t M, int
                                float* mu, float* sigma, void* stream);
 
 /*
+ * bo_score_noalloc — bo_score (mu and sigma not returned) that allocates
+ * nothing, for callers that cannot allocate device memory: code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc.
+ *
+ * The same kernels and results as bo_score with mu = sigma = NULL (bitwise),
+ * but the boxes and the posterior workspace live in a fixed 32 MiB device
+ * array that the library holds on every device it runs on until the process
+ * ends; no hipMalloc, hipFree, pinned host allocation or other allocating
+ * library routine is called. Limit: M * q * m * 2 floats of workspace, plus
+ * M * m * q(q+1)/2 for q > 1, must fit 32 MiB less the boxes' 96 KiB
+ * (2,091,008 single points of two objectives; 154,889 q = 4 batches of three),
+ * else CAPACITY before any device work.
+ *
+ * Every call on a device shares that device's array. Calls ordered on one
+ * stream are safe (the box upload is stream-ordered behind the previous
+ * call's kernels); calls that overlap on one device (different streams, or
+ * threads) race on it and must be ordered by the caller. Nothing in the
+ * array needs clearing: every call writes all of what it reads. The box
+ * decomposition is rebuilt on the host and copied from pageable memory on
+ * every call (that copy completes before the call returns).
+ *
+ * Arguments, asynchrony and errors: as bo_score (CAPACITY also for the limit
+ * above).
+ */
+bo_status bo_score_noalloc(bo_model model, const float* cand, int64_t M, int32_t q,
+                           const float* ref_point, const float* base_samples, int32_t S,
+                           float* ehvi, void* stream);
+
+/*
  * bo_nehvi_prepare / bo_score_nehvi — the noisy acquisition (qNEHVI;
  * candidates or q-batches, two or three objectives, Matern-5/2 or
  * composite-kernel models).

@@ -21,7 +21,7 @@ from typing import Optional
 
 import numpy as np
 
-__all__ = ["BoError", "Model", "lib", "lib_path", "fit", "fit_composite", "mll", "score", "nehvi_prepare", "score_nehvi", "argmax",
+__all__ = ["BoError", "Model", "lib", "lib_path", "fit", "fit_composite", "mll", "score", "score_noalloc", "nehvi_prepare", "score_nehvi", "argmax",
            "cholesky_test", "profile_enable", "profile_read", "measure_peak", "pareto_front", "box_decomposition", "STATUS",
            "MAX_N", "MAX_D", "MAX_S", "MAX_BOXES"]
 
@@ -69,6 +69,8 @@ def lib() -> ctypes.CDLL:
     L.bo_score.restype = ctypes.c_int
     L.bo_score_constrained.argtypes = [vp, vp, i64, i32, fp, fp, vp, i32, vp, vp, vp, vp]
     L.bo_score_constrained.restype = ctypes.c_int
+    L.bo_score_noalloc.argtypes = [vp, vp, i64, i32, fp, vp, i32, vp, vp]
+    L.bo_score_noalloc.restype = ctypes.c_int
     L.bo_nehvi_prepare.argtypes = [vp, vp, i32, fp, fp, vp]
     L.bo_nehvi_prepare.restype = ctypes.c_int
     L.bo_score_nehvi.argtypes = [vp, vp, i64, i32, vp, i32, vp, vp]
@@ -263,6 +265,22 @@ def score(model: Model, cand, ref, Z, ehvi=None, mu=None, sigma=None, stream=Non
         st = lib().bo_score_constrained(model.handle, *args, lw.ctypes.data_as(ctypes.c_void_p),
                                         *tail)
         _check(st, "bo_score_constrained")
+    return ehvi
+
+
+def score_noalloc(model: Model, cand, ref, Z, ehvi, stream=None):
+    """bo_score_noalloc: bo_score without mu/sigma outputs that allocates no
+    device memory (its workspace is the library's fixed per-device scratch).
+    cand [M, q, d], Z [S, q, m], ehvi [M] fp32 GPU tensors (ehvi must be
+    given: this call allocates nothing, the binding neither); ref host [m]."""
+    import torch
+    M, q, d = cand.shape
+    S = Z.shape[0]
+    r = _host_f32(ref, (model.m,), "ref")
+    st = lib().bo_score_noalloc(model.handle, _dev(cand, "cand", torch.float32), M, q,
+                                r.ctypes.data_as(ctypes.c_void_p), _dev(Z, "Z", torch.float32), S,
+                                _dev(ehvi, "ehvi", torch.float32), _stream(stream))
+    _check(st, "bo_score_noalloc")
     return ehvi
 
 

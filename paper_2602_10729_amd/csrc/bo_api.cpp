@@ -419,6 +419,127 @@ PosteriorArgs posterior_args(const Model& M, int k, const float* Lp, const float
   return pa;
 }
 
+// ---- scoring, shared by bo_score and the no-allocation variant ----------
+
+// Host-side validation of a scoring call (nothing is enqueued).
+bo_status score_validate(const char* who, bo_model model, const float* cand, int64_t M_,
+                         int32_t q, const float* ref_point, const float* feas_lower,
+                         const float* base_samples, int32_t S, float* ehvi, float* mu,
+                         float* sigma) {
+  (void)cand; (void)base_samples; (void)ehvi; (void)mu; (void)sigma;
+  const std::string W(who);
+  if (!model) return fail(BO_ERR_INVALID_ARGUMENT, W + ": model is NULL");
+  Model& M = model->m;
+  if (M_ < 0) return fail(BO_ERR_INVALID_ARGUMENT, W + ": M < 0");
+  if (q != 1 && q != 2 && q != 4) return fail(BO_ERR_INVALID_ARGUMENT, W + ": q must be 1, 2 or 4");
+  if (S < 1) return fail(BO_ERR_INVALID_ARGUMENT, W + ": S < 1");
+  if (S > BO_MAX_S) return fail(BO_ERR_CAPACITY, W + ": S beyond compiled limit");
+  if (!ref_point) return fail(BO_ERR_INVALID_ARGUMENT, W + ": ref_point is NULL");
+  if (!all_finite(ref_point, M.m)) return fail(BO_ERR_NONFINITE_INPUT, W + ": ref_point not finite");
+  if (M_ > (int64_t)1 << 40) return fail(BO_ERR_CAPACITY, W + ": M too large");
+  if (feas_lower) {
+    for (int k = 0; k < M.m; ++k)
+      if (std::isnan(feas_lower[k]))
+        return fail(BO_ERR_NONFINITE_INPUT, W + ": feasibility threshold is NaN");
+  }
+  return BO_OK;
+}
+
+// Device pointers of a scoring call (the model's device must be current).
+bo_status score_check_pointers(const Model& M, const float* cand, int64_t M_, int q,
+                               const float* base_samples, int S, const float* ehvi,
+                               const float* mu, const float* sigma) {
+  const int64_t npts = M_ * q;
+  bo_status s;
+  if ((s = check_dev(cand, sizeof(float) * npts * M.d, "cand")) != BO_OK) return s;
+  if ((s = check_dev(base_samples, sizeof(float) * (size_t)S * q * M.m, "base_samples")) != BO_OK) return s;
+  if ((s = check_dev(ehvi, sizeof(float) * M_, "ehvi")) != BO_OK) return s;
+  if (mu && (s = check_dev(mu, sizeof(float) * npts * M.m, "mu")) != BO_OK) return s;
+  if (sigma && (s = check_dev(sigma, sizeof(float) * npts * M.m, "sigma")) != BO_OK) return s;
+  if (posterior_lds_bytes(M.nb, q) > kLdsLimit)
+    return fail(BO_ERR_CAPACITY, "bo_score: posterior tile exceeds LDS");
+  return BO_OK;
+}
+
+// The disjoint boxes of the region the model's front (points strictly above
+// ref) does not dominate, staged as [nbox][2m] (lower corners, then widths;
+// +inf widths stay +inf), with the capacity checks of a scoring call.
+bo_status host_score_boxes(const Model& M, const float* ref_point, int S, int q,
+                           std::vector<float>& staged, int* nbox_out) {
+  const int m = M.m;
+  std::vector<float> F;
+  for (int32_t i : M.nd) {
+    const float* y = &M.Yh[(size_t)i * m];
+    bool above = true;
+    for (int k = 0; k < m; ++k) above = above && (y[k] > ref_point[k]);
+    if (above) F.insert(F.end(), y, y + m);
+  }
+  std::vector<float> lo, hi;
+  host_boxes(F.data(), static_cast<int>(F.size() / m), m, ref_point, lo, hi);
+  const int nbox = static_cast<int>(lo.size() / m);
+  if (nbox > BO_MAX_BOXES) return fail(BO_ERR_CAPACITY, "bo_score: too many boxes");
+  if (ehvi_lds_bytes(S, q, m, nbox) > kLdsLimit)
+    return fail(BO_ERR_CAPACITY, "bo_score: samples and boxes exceed LDS");
+  staged.resize((size_t)nbox * 2 * m);
+  for (int c = 0; c < nbox; ++c)
+    for (int k = 0; k < m; ++k) {
+      const float l = lo[(size_t)c * m + k], h = hi[(size_t)c * m + k];
+      staged[(size_t)c * 2 * m + k] = l;
+      staged[(size_t)c * 2 * m + m + k] = h - l;     // inf stays inf
+    }
+  *nbox_out = nbox;
+  return BO_OK;
+}
+
+// Floats of scoring workspace: mu and sigma [M q][m] unless the caller takes
+// them, and the batch factors [M][m][q(q+1)/2] for q > 1.
+size_t score_workspace_floats(const Model& M, int64_t M_, int q, bool have_mu, bool have_sigma) {
+  const int64_t npts = M_ * q;
+  const int T = q * (q + 1) / 2;
+  return (have_mu ? 0 : (size_t)npts * M.m) + (have_sigma ? 0 : (size_t)npts * M.m) +
+         (q > 1 ? (size_t)M_ * M.m * T : 0);
+}
+
+// The kernels of one scoring call on stream st: the posterior of every
+// objective (into mu_buf, sd_buf and, for q > 1, chol_buf), then the EHVI
+// over `boxes` (device, [nbox][2m]). rec (optional) gets profile events.
+bo_status score_launches(const Model& M, const float* cand, int64_t M_, int q,
+                         const float* feas_lower, const float* base_samples, int S,
+                         const float* boxes, int nbox, float* ehvi, float* mu_buf,
+                         float* sd_buf, float* chol_buf, hipStream_t st, Profile::Rec* rec) {
+  const int m = M.m;
+  const int64_t npts = M_ * q;
+  bo_status s;
+  if (rec) {
+    rec->launches = m;
+    hipError_t e = hipEventRecord(rec->e[0], st);
+    if (e != hipSuccess) return hip_fail(e, "bo_score: profile event");
+  }
+  for (int k = 0; k < m; ++k) {
+    PosteriorArgs pa = posterior_args(M, k, M.Lp, M.rsc, cand, npts, q);
+    pa.mu = mu_buf; pa.sd = sd_buf; pa.chol = chol_buf;
+    if ((s = after_launch(launch_posterior(pa, st), st, "posterior")) != BO_OK) return s;
+  }
+  if (rec) {
+    hipError_t e = hipEventRecord(rec->e[1], st);
+    if (e != hipSuccess) return hip_fail(e, "bo_score: profile event");
+  }
+  EhviArgs ea;
+  ea.mu = mu_buf; ea.sd = sd_buf; ea.chol = chol_buf;
+  ea.Z = base_samples; ea.boxes = boxes;
+  ea.nbat = M_; ea.q = q; ea.m = m; ea.S = S; ea.nbox = nbox;
+  ea.constrained = feas_lower != nullptr;
+  for (int k = 0; k < 3; ++k)
+    ea.lower[k] = (feas_lower && k < m) ? feas_lower[k] : -INFINITY;
+  ea.ehvi = ehvi;
+  if ((s = after_launch(launch_ehvi(ea, st), st, "ehvi")) != BO_OK) return s;
+  if (rec) {
+    hipError_t e = hipEventRecord(rec->e[2], st);
+    if (e != hipSuccess) return hip_fail(e, "bo_score: profile event");
+  }
+  return BO_OK;
+}
+
 struct CompositeSpec {
   int dr;
   const float* s_dep;
@@ -803,53 +924,27 @@ bo_status bo_score_constrained(bo_model model, const float* cand, int64_t M_, in
                                const float* ref_point, const float* feas_lower,
                                const float* base_samples, int32_t S, float* ehvi, float* mu,
                                float* sigma, void* stream) {
-  if (!model) return fail(BO_ERR_INVALID_ARGUMENT, "bo_score: model is NULL");
+  bo_status s;
+  if ((s = score_validate("bo_score", model, cand, M_, q, ref_point, feas_lower, base_samples, S,
+                          ehvi, mu, sigma)) != BO_OK)
+    return s;
   Model& M = model->m;
-  if (M_ < 0) return fail(BO_ERR_INVALID_ARGUMENT, "bo_score: M < 0");
-  if (q != 1 && q != 2 && q != 4) return fail(BO_ERR_INVALID_ARGUMENT, "bo_score: q must be 1, 2 or 4");
-  if (S < 1) return fail(BO_ERR_INVALID_ARGUMENT, "bo_score: S < 1");
-  if (S > BO_MAX_S) return fail(BO_ERR_CAPACITY, "bo_score: S beyond compiled limit");
-  if (!ref_point) return fail(BO_ERR_INVALID_ARGUMENT, "bo_score: ref_point is NULL");
-  if (!all_finite(ref_point, M.m)) return fail(BO_ERR_NONFINITE_INPUT, "bo_score: ref_point not finite");
-  if (M_ > (int64_t)1 << 40) return fail(BO_ERR_CAPACITY, "bo_score: M too large");
-  if (feas_lower) {
-    for (int k = 0; k < M.m; ++k)
-      if (std::isnan(feas_lower[k]))
-        return fail(BO_ERR_NONFINITE_INPUT, "bo_score: feasibility threshold is NaN");
-  }
+  if (M_ == 0) return BO_OK;
   DeviceGuard g(M.device);
   if (!g.ok) return fail(BO_ERR_DEVICE, "bo_score: cannot select the model's device");
   hipStream_t st = static_cast<hipStream_t>(stream);
   const int m = M.m;
   const int64_t npts = M_ * q;
-  bo_status s;
-  if (M_ == 0) return BO_OK;
+  if ((s = score_check_pointers(M, cand, M_, q, base_samples, S, ehvi, mu, sigma)) != BO_OK) return s;
   if ((s = order_after_previous(M, st, "bo_score: stream ordering")) != BO_OK) return s;
-  if ((s = check_dev(cand, sizeof(float) * npts * M.d, "cand")) != BO_OK) return s;
-  if ((s = check_dev(base_samples, sizeof(float) * (size_t)S * q * m, "base_samples")) != BO_OK) return s;
-  if ((s = check_dev(ehvi, sizeof(float) * M_, "ehvi")) != BO_OK) return s;
-  if (mu && (s = check_dev(mu, sizeof(float) * npts * m, "mu")) != BO_OK) return s;
-  if (sigma && (s = check_dev(sigma, sizeof(float) * npts * m, "sigma")) != BO_OK) return s;
-  if (posterior_lds_bytes(M.nb, q) > kLdsLimit)
-    return fail(BO_ERR_CAPACITY, "bo_score: posterior tile exceeds LDS");
 
   // ---- boxes (host, cached per reference point) ------------------------
   const bool same_ref = M.nbox >= 0 && M.box_ref.size() == (size_t)m &&
                         std::memcmp(M.box_ref.data(), ref_point, sizeof(float) * m) == 0;
   if (!same_ref) {
-    std::vector<float> F;
-    for (int32_t i : M.nd) {
-      const float* y = &M.Yh[(size_t)i * m];
-      bool above = true;
-      for (int k = 0; k < m; ++k) above = above && (y[k] > ref_point[k]);
-      if (above) F.insert(F.end(), y, y + m);
-    }
-    std::vector<float> lo, hi;
-    host_boxes(F.data(), static_cast<int>(F.size() / m), m, ref_point, lo, hi);
-    const int nbox = static_cast<int>(lo.size() / m);
-    if (nbox > BO_MAX_BOXES) return fail(BO_ERR_CAPACITY, "bo_score: too many boxes");
-    if (ehvi_lds_bytes(S, q, m, nbox) > kLdsLimit)
-      return fail(BO_ERR_CAPACITY, "bo_score: samples and boxes exceed LDS");
+    std::vector<float> staged;
+    int nbox = 0;
+    if ((s = host_score_boxes(M, ref_point, S, q, staged, &nbox)) != BO_OK) return s;
     if (nbox > M.box_cap) {
       if (M.d_boxes) {
         hipError_t e = hipDeviceSynchronize();   // earlier launches may read it
@@ -870,7 +965,7 @@ bo_status bo_score_constrained(bo_model model, const float* cand, int64_t M_, in
       if (!DS->stage_evt) e = hipEventCreateWithFlags(&DS->stage_evt, hipEventDisableTiming);
       else e = hipEventSynchronize(DS->stage_evt);
       if (e != hipSuccess) return hip_fail(e, "bo_score: staging event");
-      const size_t need_f = (size_t)nbox * 2 * m;
+      const size_t need_f = staged.size();
       if (need_f > DS->stage_floats) {
         if (DS->stage) (void)hipHostFree(DS->stage);
         DS->stage = nullptr;
@@ -880,12 +975,7 @@ bo_status bo_score_constrained(bo_model model, const float* cand, int64_t M_, in
         if (e != hipSuccess) return hip_fail(e, "bo_score: pinned staging");
         DS->stage_floats = cap;
       }
-      for (int c = 0; c < nbox; ++c)
-        for (int k = 0; k < m; ++k) {
-          const float l = lo[(size_t)c * m + k], h = hi[(size_t)c * m + k];
-          DS->stage[(size_t)c * 2 * m + k] = l;
-          DS->stage[(size_t)c * 2 * m + m + k] = h - l;     // inf stays inf
-        }
+      std::memcpy(DS->stage, staged.data(), sizeof(float) * need_f);
       e = hipMemcpyAsync(M.d_boxes, DS->stage, sizeof(float) * need_f, hipMemcpyHostToDevice, st);
       if (e == hipSuccess) e = hipEventRecord(DS->stage_evt, st);
       if (e != hipSuccess) return hip_fail(e, "bo_score: box upload");
@@ -897,9 +987,7 @@ bo_status bo_score_constrained(bo_model model, const float* cand, int64_t M_, in
   }
 
   // ---- workspace ----------------------------------------------------------
-  const int T = q * (q + 1) / 2;
-  const size_t need = (mu ? 0 : (size_t)npts * m) + (sigma ? 0 : (size_t)npts * m) +
-                      (q > 1 ? (size_t)M_ * m * T : 0);
+  const size_t need = score_workspace_floats(M, M_, q, mu != nullptr, sigma != nullptr);
   if (need > M.ws_floats) {
     if (M.ws) {
       hipError_t e = hipDeviceSynchronize();      // earlier launches may use it
@@ -924,34 +1012,47 @@ bo_status bo_score_constrained(bo_model model, const float* cand, int64_t M_, in
     std::lock_guard<std::mutex> lk(P.mu);
     if (P.on && P.used < P.pool.size()) rec = &P.pool[P.used++];
   }
-  if (rec) {
-    rec->launches = m;
-    hipError_t e = hipEventRecord(rec->e[0], st);
-    if (e != hipSuccess) return hip_fail(e, "bo_score: profile event");
-  }
-  for (int k = 0; k < m; ++k) {
-    PosteriorArgs pa = posterior_args(M, k, M.Lp, M.rsc, cand, npts, q);
-    pa.mu = mu_buf; pa.sd = sd_buf; pa.chol = chol_buf;
-    if ((s = after_launch(launch_posterior(pa, st), st, "posterior")) != BO_OK) return s;
-  }
-  if (rec) {
-    hipError_t e = hipEventRecord(rec->e[1], st);
-    if (e != hipSuccess) return hip_fail(e, "bo_score: profile event");
-  }
-  EhviArgs ea;
-  ea.mu = mu_buf; ea.sd = sd_buf; ea.chol = chol_buf;
-  ea.Z = base_samples; ea.boxes = M.d_boxes;
-  ea.nbat = M_; ea.q = q; ea.m = m; ea.S = S; ea.nbox = M.nbox;
-  ea.constrained = feas_lower != nullptr;
-  for (int k = 0; k < 3; ++k)
-    ea.lower[k] = (feas_lower && k < m) ? feas_lower[k] : -INFINITY;
-  ea.ehvi = ehvi;
-  if ((s = after_launch(launch_ehvi(ea, st), st, "ehvi")) != BO_OK) return s;
-  if (rec) {
-    hipError_t e = hipEventRecord(rec->e[2], st);
-    if (e != hipSuccess) return hip_fail(e, "bo_score: profile event");
-  }
+  if ((s = score_launches(M, cand, M_, q, feas_lower, base_samples, S, M.d_boxes, M.nbox, ehvi,
+                          mu_buf, sd_buf, chol_buf, st, rec)) != BO_OK)
+    return s;
   return mark_call(M, st, "bo_score: stream ordering");
+}
+
+bo_status bo_score_noalloc(bo_model model, const float* cand, int64_t M_, int32_t q,
+                           const float* ref_point, const float* base_samples, int32_t S,
+                           float* ehvi, void* stream) {
+  bo_status s;
+  if ((s = score_validate("bo_score_noalloc", model, cand, M_, q, ref_point, nullptr,
+                          base_samples, S, ehvi, nullptr, nullptr)) != BO_OK)
+    return s;
+  Model& M = model->m;
+  if (M_ == 0) return BO_OK;
+  const size_t need = score_workspace_floats(M, M_, q, false, false);
+  if (need > kNoallocScratchFloats - kNoallocBoxFloats)
+    return fail(BO_ERR_CAPACITY, "bo_score_noalloc: M * q * m beyond the 32 MiB scratch");
+  DeviceGuard g(M.device);
+  if (!g.ok) return fail(BO_ERR_DEVICE, "bo_score_noalloc: cannot select the model's device");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int m = M.m;
+  const int64_t npts = M_ * q;
+  if ((s = score_check_pointers(M, cand, M_, q, base_samples, S, ehvi, nullptr, nullptr)) != BO_OK)
+    return s;
+  float* scr = nullptr;
+  if ((s = noalloc_scratch(M.device, &scr)) != BO_OK) return s;
+  if ((s = order_after_previous(M, st, "bo_score_noalloc: stream ordering")) != BO_OK) return s;
+  // boxes into the scratch: from pageable host memory the copy completes
+  // before hipMemcpyAsync returns, after the earlier work on the stream
+  std::vector<float> staged;
+  int nbox = 0;
+  if ((s = host_score_boxes(M, ref_point, S, q, staged, &nbox)) != BO_OK) return s;
+  hipError_t e = hipMemcpyAsync(scr, staged.data(), sizeof(float) * staged.size(),
+                                hipMemcpyHostToDevice, st);
+  if (e != hipSuccess) return hip_fail(e, "bo_score_noalloc: box upload");
+  float* mu_buf = scr + kNoallocBoxFloats;
+  float* sd_buf = mu_buf + (size_t)npts * m;
+  float* chol_buf = (q > 1) ? sd_buf + (size_t)npts * m : nullptr;
+  return score_launches(M, cand, M_, q, nullptr, base_samples, S, scr, nbox, ehvi, mu_buf,
+                        sd_buf, chol_buf, st, nullptr);
 }
 
 }  // extern "C"

@@ -15,6 +15,15 @@ namespace bo {
 constexpr int kBlk = 16;        // MFMA 16x16x4 fp32 block edge
 constexpr int kFitBlk = 64;     // Cholesky / inverse block edge (fp64)
 
+// Scratch of the no-allocation scoring entry point (noalloc.hip): 32 MiB
+// per device, the boxes first (room for BO_MAX_BOXES boxes of three
+// objectives), then the posterior workspace.
+constexpr size_t kNoallocScratchFloats = (size_t)32 << 18;          // 32 MiB
+constexpr size_t kNoallocBoxFloats = (size_t)BO_MAX_BOXES * 2 * 3;
+// Device address of this device's scratch (the device must be current);
+// looked up once per device with hipGetSymbolAddress.
+bo_status noalloc_scratch(int dev, float** out);
+
 // Thread-local error detail; returns the status for chaining.
 bo_status fail(bo_status st, const std::string& msg);
 bo_status hip_fail(hipError_t e, const char* what);
