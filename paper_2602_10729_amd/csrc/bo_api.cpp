@@ -202,9 +202,8 @@ struct FitScratch {
 // for the whole device before handing memory back to the pool.
 void release_noisy(Model* M) {
   Model::Noisy& z = M->nz;
-  if (z.Lp0 || z.rsc0 || z.Gp || z.boxes || z.off || z.front || z.ws) (void)hipDeviceSynchronize();
+  if (z.Lp0 || z.Gp || z.boxes || z.off || z.front || z.ws) (void)hipDeviceSynchronize();
   pfree(z.Lp0, nullptr);
-  pfree(z.rsc0, nullptr);
   pfree(z.Gp, nullptr);
   pfree(z.boxes, nullptr);
   pfree(z.off, nullptr);
@@ -218,10 +217,9 @@ void release_noisy(Model* M) {
 
 void release_buffers(Model* M) {
   release_noisy(M);
-  if (M->Xs || M->invls || M->alpha || M->Lp || M->rsc || M->ws || M->d_boxes || M->wts ||
+  if (M->Xs || M->invls || M->alpha || M->Lp || M->ws || M->d_boxes || M->wts ||
       M->pref || M->Xd || M->xf || M->x2 || M->ctr)
     (void)hipDeviceSynchronize();
-  pfree(M->rsc, nullptr);
   pfree(M->xf, nullptr);
   pfree(M->x2, nullptr);
   pfree(M->ctr, nullptr);
@@ -394,8 +392,9 @@ bo_status mark_call(Model& M, hipStream_t st, const char* who) {
 
 // Arguments of the posterior kernel for objective k of a fitted model: the
 // packed inverse factor Lp (the model's, or the noisy acquisition's noise-free
-// one) with its row-block scales rsc; outputs are the caller's to set.
-PosteriorArgs posterior_args(const Model& M, int k, const float* Lp, const float* rsc,
+// one, its row-block scales after its fragments); outputs are the caller's to
+// set.
+PosteriorArgs posterior_args(const Model& M, int k, const float* Lp,
                              const float* cand, int64_t npts, int q) {
   PosteriorArgs pa;
   pa.cand = cand; pa.npts = npts; pa.d = M.d; pa.dx = M.dx; pa.q = q;
@@ -403,8 +402,15 @@ PosteriorArgs posterior_args(const Model& M, int k, const float* Lp, const float
   pa.invls = M.invls + (size_t)k * M.dx;
   pa.alpha = M.alpha + (size_t)k * M.n_pad;
   pa.Lp = Lp + (size_t)k * M.lp_per_obj;
-  pa.rsc = rsc + (size_t)k * M.nb;
   pa.kbound = M.kbound[k];
+  {
+    // a plain model's kernel values are at most s: scale them by 2^(14 - E)
+    // for the split (the kernel multiplies s by it, exactly)
+    int E = 0;
+    (void)std::frexp(static_cast<double>(M.os[k]), &E);
+    pa.ss = static_cast<float>(std::ldexp(static_cast<double>(M.os[k]), 14 - E));
+    pa.kinv0 = static_cast<float>(std::ldexp(1.0, E - 14));
+  }
   pa.xf = M.xf + (size_t)k * M.nb * dist_frags(M.dx) * 512;
   pa.x2 = M.x2 + (size_t)k * 2 * M.n_pad;
   pa.ctr = M.ctr + (size_t)k * M.dx;
@@ -516,7 +522,7 @@ bo_status score_launches(const Model& M, const float* cand, int64_t M_, int q,
     if (e != hipSuccess) return hip_fail(e, "bo_score: profile event");
   }
   for (int k = 0; k < m; ++k) {
-    PosteriorArgs pa = posterior_args(M, k, M.Lp, M.rsc, cand, npts, q);
+    PosteriorArgs pa = posterior_args(M, k, M.Lp, cand, npts, q);
     pa.mu = mu_buf; pa.sd = sd_buf; pa.chol = chol_buf;
     if ((s = after_launch(launch_posterior(pa, st), st, "posterior")) != BO_OK) return s;
   }
@@ -623,7 +629,7 @@ bo_status fit_impl(const char* who, const float* X, const float* Y, int64_t n, i
 
   const int nf = static_cast<int>((n + kFitBlk - 1) / kFitBlk) * kFitBlk;
   const int dc = d - dr;
-  M->lp_per_obj = (size_t)posterior_frag_blocks(M->nb) * 512;   // 2 KiB per block
+  M->lp_per_obj = packed_factor_floats(M->nb);
   FitScratch fs;
   fs.st = st;
   // fp64 hyperparameters: [1/ls m*d][os m][noise m] (+ [s_dep m][s_int m][pref m*dc])
@@ -634,7 +640,6 @@ bo_status fit_impl(const char* who, const float* X, const float* Y, int64_t n, i
   if ((s = palloc(&fs.tmp, (size_t)m * nf, st, "fit vector")) != BO_OK) return bail(s);
   if ((s = palloc(&fs.flag, 1, st, "flag")) != BO_OK) return bail(s);
   if ((s = palloc(&fs.stats, 2 * (size_t)m, st, "fit statistics")) != BO_OK) return bail(s);
-  if ((s = palloc(&M->rsc, (size_t)m * M->nb, st, "row-block scales")) != BO_OK) return bail(s);
   if ((s = palloc(&M->Xs, (size_t)m * M->n_pad * M->dx, st, "scaled X")) != BO_OK) return bail(s);
   if ((s = palloc(&M->invls, (size_t)m * M->dx, st, "inverse lengthscales")) != BO_OK) return bail(s);
   if ((s = palloc(&M->alpha, (size_t)m * M->n_pad, st, "alpha")) != BO_OK) return bail(s);
@@ -720,7 +725,7 @@ bo_status fit_impl(const char* who, const float* X, const float* Y, int64_t n, i
   if (comp && (s = after_launch(launch_weights(X, n, d, m, M->n_pad, gp, M->wts, st), st, "weights")) != BO_OK) return bail(s);
   if ((s = after_launch(launch_cholesky(fs.A, fs.W, nf, m, fs.flag, st), st, "cholesky")) != BO_OK) return bail(s);
   if ((s = after_launch(launch_alpha(fs.W, Y, n, m, nf, M->n_pad, fs.tmp, M->alpha, st), st, "alpha")) != BO_OK) return bail(s);
-  if ((s = after_launch(launch_pack(fs.W, n, m, nf, M->nb, M->Lp, M->rsc, fs.stats + m, fs.flag, X, d, M->dx, dr, dr4, M->invls, M->Xs, st), st, "pack")) != BO_OK) return bail(s);
+  if ((s = after_launch(launch_pack(fs.W, n, m, nf, M->nb, M->Lp, fs.stats + m, fs.flag, X, d, M->dx, dr, dr4, M->invls, M->Xs, st), st, "pack")) != BO_OK) return bail(s);
   if ((s = after_launch(launch_pack_x(M->Xs, n, m, M->nb, M->dx, dr4, M->ctr, M->xf, M->x2, st), st, "pack X")) != BO_OK) return bail(s);
 
   // one synchronisation: the positive-definiteness flag and Y (for the front
@@ -1196,7 +1201,6 @@ bo_status nehvi_prepare_impl(bo_model model, const float* ZX, int32_t S, const f
     if ((s = palloc(&sc.Fd, (size_t)S * n * m, st, "noisy: in-sample draws")) != BO_OK) return s;
   }
   if ((s = palloc(&z.Lp0, (size_t)m * M.lp_per_obj, st, "noisy: packed factor")) != BO_OK) return s;
-  if ((s = palloc(&z.rsc0, (size_t)m * M.nb, st, "noisy: row-block scales")) != BO_OK) return s;
   if ((s = palloc(&z.front, (size_t)S * n, st, "noisy: fronts")) != BO_OK) return s;
 
   std::vector<double> hyp(nhyp, 0.0);
@@ -1271,7 +1275,7 @@ bo_status nehvi_prepare_impl(bo_model model, const float* ZX, int32_t S, const f
   // noise-free K_XX: factor, inverse, packed for the conditional (co)variance
   if ((s = step(launch_gram(M.Xd, n, d, m, nf, g0, sc.A0, st, sc.stats), "gram")) != BO_OK) return sync_fail(s);
   if ((s = step(launch_cholesky(sc.A0, sc.W0, nf, m, sc.flag + 2, st), "cholesky")) != BO_OK) return sync_fail(s);
-  if ((s = step(launch_pack_factor(sc.W0, n, m, nf, M.nb, z.Lp0, z.rsc0, sc.stats + m, sc.flag + 3, st), "pack")) != BO_OK) return sync_fail(s);
+  if ((s = step(launch_pack_factor(sc.W0, n, m, nf, M.nb, z.Lp0, sc.stats + m, sc.flag + 3, st), "pack")) != BO_OK) return sync_fail(s);
   // T1 = L_XX Z_X, G = K_XX^{-1} T1 = W0^T (W0 T1)
   if ((s = step(launch_gather_z(ZX, n, m, S, nf, Sp, sc.Zk, st), "gather")) != BO_OK) return sync_fail(s);
   if ((s = step(launch_trmm(false, sc.A, sc.Zk, sc.T1, nf, Sp, m, st), "trmm")) != BO_OK) return sync_fail(s);
@@ -1447,7 +1451,7 @@ bo_status score_nehvi_impl(bo_model model, const float* cand, int64_t M_, int32_
     const int64_t np_ = nb_ * q;
     const float* cc = cand + b0 * q * M.d;
     for (int k = 0; k < m; ++k) {
-      PosteriorArgs pa = posterior_args(M, k, z.Lp0, z.rsc0, cc, np_, q);
+      PosteriorArgs pa = posterior_args(M, k, z.Lp0, cc, np_, q);
       pa.mu = mu_buf; pa.sd = sd_buf; pa.chol = (q > 1) ? ch_buf : nullptr;
       if ((s = after_launch(launch_posterior(pa, st), st, "posterior")) != BO_OK) return s;
     }

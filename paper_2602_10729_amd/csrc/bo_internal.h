@@ -61,9 +61,9 @@ struct Model {
   float* alpha = nullptr;        // [m][n_pad]
   float* wts = nullptr;          // composite: [m][n_pad] preference weights of X (0 past n)
   float* pref = nullptr;         // composite: [m][d - dr] preference slopes
-  float* Lp = nullptr;           // [m][frag blocks][2 KiB] packed fp16 hi/lo L^{-1} + zero block
+  float* Lp = nullptr;           // [m][lp_per_obj]: packed fp16 hi/lo L^{-1} blocks, the zero
+                                 // block, then the nb row-block scales (packed_factor_floats)
   size_t lp_per_obj = 0;         // floats per objective in Lp
-  float* rsc = nullptr;          // [m][nb] power of two undoing each 16-row block's pack scale
   std::vector<float> kbound;     // [m] largest diagonal of K (bounds every training prior variance)
   std::vector<double> cond_est;  // [m] max K_ii * max |L^{-1}|^2 (a lower bound on cond(K))
   uint16_t* xf = nullptr;        // [m][nb][dist_frags(dx)][512] distance fragments of X
@@ -78,7 +78,6 @@ struct Model {
   struct Noisy {
     int S = 0, Sp = 0, n32 = 0, total = 0;
     float* Lp0 = nullptr;        // [m][lp_per_obj] packed inverse factor of K_XX (no noise)
-    float* rsc0 = nullptr;       // [m][nb] row-block scales of Lp0
     uint16_t* Gp = nullptr;      // [m][n32][Sp/16][1024] fp16 hi/lo fragments of G^T
     int m = 0, q = 1;            // objectives; batch size of the last scoring call
     float ginv[3] = {1.f, 1.f, 1.f};  // 1 / scale applied to G before the split
@@ -153,13 +152,13 @@ hipError_t launch_mll(const float* X, int64_t n, int d, int m, int nf, const Gra
 // Pack W into the posterior's A-fragment format (fp16 hi/lo planes of 16x32
 // lower blocks, zeros beyond n, then one all-zero block; 2 KiB per block,
 // posterior_frag_blocks(nb) blocks per objective), each 16-row block I scaled
-// by a power of two that brings its largest entry into [2^13, 2^14)
-// (rsc [m][nb] = the inverse scale; wmax [m] = largest |W| per objective as a
-// non-negative double's bit pattern, zeroed by the caller; *flag set on a
-// non-finite entry), and write the lengthscale-scaled X in the slot layout
-// (invls is per slot, [m][dx]).
+// by a power of two that brings its largest entry into [2^13, 2^14), followed
+// by the nb inverse scales (packed_factor_floats(nb) floats per objective;
+// wmax [m] = largest |W| per objective as a non-negative double's bit
+// pattern, zeroed by the caller; *flag set on a non-finite entry), and write
+// the lengthscale-scaled X in the slot layout (invls is per slot, [m][dx]).
 hipError_t launch_pack(const double* W, int64_t n, int m, int nf, int nb,
-                       float* Lp, float* rsc, unsigned long long* wmax, int* flag,
+                       float* Lp, unsigned long long* wmax, int* flag,
                        const float* X, int d, int dx, int dr, int dr4,
                        const float* invls, float* Xs, hipStream_t st);
 
@@ -195,7 +194,7 @@ hipError_t launch_trmm(bool trans, const double* T, const double* Bm, double* C,
                        int ldb, int m, hipStream_t st);
 // The posterior's A-fragment packing of W alone (no coordinate scaling).
 hipError_t launch_pack_factor(const double* W, int64_t n, int m, int nf, int nb, float* Lp,
-                              float* rsc, unsigned long long* wmax, int* flag, hipStream_t st);
+                              unsigned long long* wmax, int* flag, hipStream_t st);
 
 // Noisy acquisition kernels (nehvi.hip).
 struct NehviFrontArgs {
@@ -290,9 +289,11 @@ struct PosteriorArgs {
   const float* Xs;     // [n_pad][dx]
   const float* invls;  // [dx]
   const float* alpha;  // [n_pad]
-  const float* Lp;     // packed fragments of this objective
-  const float* rsc;    // [nb] power of two undoing each 16-row block's pack scale
+  const float* Lp;     // packed fragments of this objective, then its row-block scales
   float kbound;        // composite: bound on every training point's prior variance
+  // plain Matern-5/2: the output scale times the kernel values' power-of-two
+  // split scale 2^(14 - E) (s = f 2^E, f in [0.5, 1)), and 2^(E - 14)
+  float ss, kinv0;
   const uint16_t* xf;  // [nb][dist_frags(dx)][512] centred-X distance fragments
   const float* x2;     // [2][n_pad] squared norms of the centred rows per coordinate group
   const float* ctr;    // [dx] centre subtracted from the scaled coordinates
@@ -310,6 +311,12 @@ struct PosteriorArgs {
 hipError_t launch_posterior(const PosteriorArgs& a, hipStream_t st);
 // Packed L^{-1} blocks per objective (lower 16x32 blocks + the zero block).
 int64_t posterior_frag_blocks(int nb);
+// Floats per objective of the packed inverse factor: the fragment blocks
+// (512 floats each), then the nb row-block scales and a zero (the scale of
+// a row block past the matrix), padded to 64 floats.
+inline size_t packed_factor_floats(int nb) {
+  return (size_t)posterior_frag_blocks(nb) * 512 + (size_t)(nb + 1 + 63) / 64 * 64;
+}
 
 // Monte-Carlo EHVI over boxes for nbat batches.
 struct EhviArgs {

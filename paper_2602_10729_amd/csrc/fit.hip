@@ -474,11 +474,14 @@ __global__ __launch_bounds__(256) void k_wty(const double* __restrict__ W,
 // (f in [0.5, 1)), the pack stores W 2^(14 - E), so every entry of the block
 // is at most 2^14 in magnitude (fp16 holds up to 65504) and the low halves of
 // all entries above 2^-3 of that are normal fp16 numbers; rsc[k][I] = 2^(E-14)
-// undoes it. wmax[k] gets the largest |W| of objective k (bit pattern of a
-// non-negative double), for the conditioning estimate; a non-finite entry sets
-// *flag. One workgroup per (row block, objective).
+// undoes it (stored after objective k's fragment blocks: rsc + k * stride,
+// followed by a zero at entry nb for row blocks past the matrix).
+// wmax[k] gets the largest |W| of objective k (bit pattern of a non-negative
+// double), for the conditioning estimate; a non-finite entry sets *flag. One
+// workgroup per (row block, objective).
 __global__ __launch_bounds__(256) void k_rowblock_scale(const double* __restrict__ W, int64_t n,
-                                                        int nf, int nb, float* __restrict__ rsc,
+                                                        int nf, float* __restrict__ rsc,
+                                                        int64_t stride,
                                                         unsigned long long* __restrict__ wmax,
                                                         int* __restrict__ flag) {
   __shared__ double part[256];
@@ -506,7 +509,8 @@ __global__ __launch_bounds__(256) void k_rowblock_scale(const double* __restrict
     const double m = part[0];
     int E = 0;
     if (m > 0.0) (void)frexp(m, &E);
-    rsc[(int64_t)k * nb + I] = ldexpf(1.0f, E - 14);
+    rsc[(int64_t)k * stride + I] = ldexpf(1.0f, E - 14);
+    if (I == 0) rsc[(int64_t)k * stride + gridDim.x] = 0.f;   // entry nb: past the matrix
     atomicMax(wmax + k, static_cast<unsigned long long>(__double_as_longlong(m)));
   }
 }
@@ -522,7 +526,7 @@ __global__ __launch_bounds__(256) void k_rowblock_scale(const double* __restrict
 // hi = fp16(w), lo = fp16(w - hi).
 __global__ __launch_bounds__(256) void k_pack(const double* __restrict__ W, int64_t n,
                                               int nf, int64_t nblk, int nb,
-                                              const float* __restrict__ rsc,
+                                              const float* __restrict__ rsc, int64_t stride,
                                               _Float16* __restrict__ Lp) {
   const int k = blockIdx.y;
   const int64_t g = (int64_t)blockIdx.x * 256 + threadIdx.x;   // (blk, lane)
@@ -544,7 +548,7 @@ __global__ __launch_bounds__(256) void k_pack(const double* __restrict__ W, int6
   const int64_t row = (int64_t)I * kBlk + lane % 16;
   const double* Wk = W + (int64_t)k * nf * nf;
   // the zero block (I = nb) has no scale
-  const double sc = (I < nb) ? 1.0 / static_cast<double>(rsc[(int64_t)k * nb + I]) : 1.0;
+  const double sc = (I < nb) ? 1.0 / static_cast<double>(rsc[(int64_t)k * stride + I]) : 1.0;
   _Float16 hi[8], lo[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
@@ -554,7 +558,7 @@ __global__ __launch_bounds__(256) void k_pack(const double* __restrict__ W, int6
     hi[e] = h;
     lo[e] = static_cast<_Float16>(static_cast<float>(w - static_cast<double>(h)));
   }
-  _Float16* dst = Lp + ((int64_t)k * nblk + blk) * 1024 + lane * 8;
+  _Float16* dst = Lp + (int64_t)k * 2 * stride + blk * 1024 + lane * 8;
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
     dst[e] = hi[e];
@@ -968,9 +972,9 @@ hipError_t launch_mll(const float* X, int64_t n, int d, int m, int nf, const Gra
 }
 
 hipError_t launch_pack(const double* W, int64_t n, int m, int nf, int nb, float* Lp,
-                       float* rsc, unsigned long long* wmax, int* flag, const float* X, int d,
+                       unsigned long long* wmax, int* flag, const float* X, int d,
                        int dx, int dr, int dr4, const float* invls, float* Xs, hipStream_t st) {
-  hipError_t e = launch_pack_factor(W, n, m, nf, nb, Lp, rsc, wmax, flag, st);
+  hipError_t e = launch_pack_factor(W, n, m, nf, nb, Lp, wmax, flag, st);
   if (e != hipSuccess) return e;
   const int n_pad = nb * kBlk;
   const unsigned gx2 = static_cast<unsigned>(((int64_t)n_pad * dx + 255) / 256);
@@ -1022,12 +1026,14 @@ hipError_t launch_trmm(bool trans, const double* T, const double* Bm, double* C,
 }
 
 hipError_t launch_pack_factor(const double* W, int64_t n, int m, int nf, int nb, float* Lp,
-                              float* rsc, unsigned long long* wmax, int* flag, hipStream_t st) {
-  hipLaunchKernelGGL(k_rowblock_scale, dim3(nb, m), dim3(256), 0, st, W, n, nf, nb, rsc, wmax,
-                     flag);
+                              unsigned long long* wmax, int* flag, hipStream_t st) {
   const int64_t nblk = posterior_frag_blocks(nb);   // with the zero block
+  const int64_t stride = static_cast<int64_t>(packed_factor_floats(nb));
+  float* rsc = Lp + nblk * 512;                     // objective k's scales at rsc + k * stride
+  hipLaunchKernelGGL(k_rowblock_scale, dim3(nb, m), dim3(256), 0, st, W, n, nf, rsc, stride, wmax,
+                     flag);
   const unsigned gx = static_cast<unsigned>((nblk * 64 + 255) / 256);
-  hipLaunchKernelGGL(k_pack, dim3(gx, m), dim3(256), 0, st, W, n, nf, nblk, nb, rsc,
+  hipLaunchKernelGGL(k_pack, dim3(gx, m), dim3(256), 0, st, W, n, nf, nblk, nb, rsc, stride,
                      reinterpret_cast<_Float16*>(Lp));
   return hipGetLastError();
 }

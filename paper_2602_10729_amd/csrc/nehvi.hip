@@ -308,6 +308,9 @@ __global__ __launch_bounds__(kMW * 64) void k_nehvi_means(NehviMeansArgs a) {
   const KvScale ks = kv_split_scale(
       COMP ? __builtin_amdgcn_sqrtf(fmaf(wsd, wstar, sk + sint) * a.kbound[k]) : sk);
   if (wave == 0) kish[lane] = ks.kinv;
+  // the kernel values are made scaled: the scale rides in the output scales
+  const float sks = sk * ks.ksc, sints = sint * ks.ksc;
+  wsd *= ks.ksc;
   const __amdgpu_buffer_rsrc_t w_rs = rsrc(COMP ? a.wts + (int64_t)k * a.n_pad : a.Xs,
                                            COMP ? a.n_pad * 4 : 0);
   const int wrow = threadIdx.x - 256;       // COMP: threads 256 .. 287 stage the weights
@@ -356,18 +359,16 @@ __global__ __launch_bounds__(kMW * 64) void k_nehvi_means(NehviMeansArgs a) {
       if constexpr (COMP) {
         const float k5 = m52(r2r, 1.0f);
         const float k3 = m32(r2);
-        kv = fmaf(wsd * wst[jb & 1][4 * wave + u], k3, k5 * fmaf(sint, k3, sk));
+        kv = fmaf(wsd * wst[jb & 1][4 * wave + u], k3, k5 * fmaf(sints, k3, sks));
       } else {
-        kv = m52(r2, sk);
+        kv = m52(r2, sks);
       }
       // one fp32 value for both halves (the compiler may otherwise fuse the
-      // last product into the fp16 conversions and derive the high half
-      // twice), scaled by the candidate's power of two
-      float kvs = kv * ks.ksc;
-      asm volatile("" : "+v"(kvs));
-      const _Float16 h = static_cast<_Float16>(kvs);
+      // last product into the fp16 conversions and derive the high half twice)
+      asm volatile("" : "+v"(kv));
+      const _Float16 h = static_cast<_Float16>(kv);
       hi[u] = h;
-      lo[u] = static_cast<_Float16>(kvs - static_cast<float>(h));
+      lo[u] = static_cast<_Float16>(kv - static_cast<float>(h));
     }
     _Float16* dst = ring + (jb % 3) * kRingSlot + lane * kKS + 4 * wave;
     *reinterpret_cast<halfx4*>(dst) = hi;

@@ -167,9 +167,10 @@ struct Producer {
   static_assert(F0 == 1 && NF <= 3, "at most 32 coordinate slots");
   halfx8 cb[NS][NF];        // B fragments of this lane's candidate, per group
   float c2[NS];             // squared norm of the centred candidate, per group
-  float mu;
-  float ksc;                // power of two scaling this lane's kernel values for the split
-  float wsd;                // composite: s_dep * w(candidate)
+  float mu;                 // sum of alpha times the scaled kernel values
+  // composite: s_dep w(candidate), s_route and s_int, each times this column's
+  // power-of-two split scale (a plain model's scaled s is uniform: a.ss)
+  float wsd, ss, sis;
   int col;                  // tile column of this lane
   int rq;                   // first of this lane's rows inside a block
   int half;                 // row half of this wave
@@ -225,8 +226,7 @@ __device__ __forceinline__ void produce(Producer<NT, DX4, COMP>& P, const Poster
     for (int g = 0; g < NS; ++g) {
       const float nrm = P.c2[g] + P.x2[g][e];
       const float dot = fmaf(d1[g][e], 1.0f / kDistLoScale, d0[g][e]);
-      const float v = fmaf(-2.0f, dot, nrm);
-      r2[g][e] = v < 0.f ? 0.f : v;     // clamp at zero; NaN (a NaN candidate) stays NaN
+      r2[g][e] = fmaxf(fmaf(-2.0f, dot, nrm), 0.f);
       rt += r2[g][e];
       nt += nrm;
     }
@@ -268,28 +268,27 @@ __device__ __forceinline__ void produce(Producer<NT, DX4, COMP>& P, const Poster
   for (int e = 0; e < 4; ++e) {
     // no mask: rows past n meet zero columns of L^{-1} and zero alpha;
     // columns past the batch are never written
+    // the kernel value times this column's power-of-two split scale (the
+    // scale rides in the output scales, so the product is exact)
     float kv;
     if constexpr (COMP) {
       // s_route M52(r_route) + s_dep w* w_i M32(r_dep) + s_int M52 M32
       const float k5 = matern52_f(r2[0][e], 1.0f);
       const float k3 = matern32_f(r2[1][e]);
-      kv = fmaf(P.wsd * P.wt[e], k3, k5 * fmaf(a.s_int, k3, a.s));
+      kv = fmaf(P.wsd * P.wt[e], k3, k5 * fmaf(P.sis, k3, P.ss));
     } else {
-      kv = matern52_f(r2[0][e], a.s);
+      kv = matern52_f(r2[0][e], a.ss);
     }
     // kv is rounded to fp32 here, once: otherwise the compiler may fuse its
     // last product into the fp16 conversions and derive the high half twice
     // (once exactly, once from the fp32 value); within an fp32 ulp of an
     // fp16 rounding midpoint the stored high and low halves then disagree by
-    // one fp16 ulp. The split takes kv times this column's power of two
-    // (exact), pinned the same way.
+    // one fp16 ulp
     asm volatile("" : "+v"(kv));
     P.mu = fmaf(P.al[e], kv, P.mu);
-    float kvs = kv * P.ksc;
-    asm volatile("" : "+v"(kvs));
-    const _Float16 h = static_cast<_Float16>(kvs);
+    const _Float16 h = static_cast<_Float16>(kv);
     hi[e] = h;
-    lo[e] = static_cast<_Float16>(kvs - static_cast<float>(h));
+    lo[e] = static_cast<_Float16>(kv - static_cast<float>(h));
   }
   _Float16* dst = ring + P.col * kCSH + (jb % kRing) * kJ + P.rq;
   *reinterpret_cast<halfx4*>(dst) = hi;
@@ -307,7 +306,6 @@ template <int RB>
 struct Slots {
   int first[RB];
   int last[RB];
-  float sc[RB];     // power of two undoing the slot's row-block pack scale (0 past the matrix)
 };
 
 __device__ __forceinline__ int frag_block(int first, int last, int J, int zero_blk) {
@@ -510,11 +508,18 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
       P.wsd = a.s_dep * wstar;
     }
   }
-  // power of two for this column's kernel values: the composite covariance is
-  // bounded by sqrt(prior(candidate) * kbound), the plain one by s
-  const KvScale ks = kv_split_scale(
-      COMP ? __builtin_amdgcn_sqrtf(fmaf(a.s_dep * wstar, wstar, a.s + a.s_int) * a.kbound) : a.s);
-  P.ksc = ks.ksc;
+  // power of two for this column's kernel values: a plain model's is uniform
+  // (its covariances are bounded by s; the host folds it into a.ss), a
+  // composite column's follows from the bound sqrt(prior(candidate) * kbound)
+  float kinv = a.kinv0;
+  if constexpr (COMP) {
+    const KvScale ks = kv_split_scale(
+        __builtin_amdgcn_sqrtf(fmaf(a.s_dep * wstar, wstar, a.s + a.s_int) * a.kbound));
+    P.wsd *= ks.ksc;
+    P.ss = a.s * ks.ksc;
+    P.sis = a.s_int * ks.ksc;
+    kinv = ks.kinv;
+  }
   // distance operands of the candidate: centred coordinates, their squared
   // norms per group, and the B fragments, laid out per group and column in
   // the (not yet used) ring as 96 halves: [0, 32) stream 0 (hi, zero past D),
@@ -533,6 +538,9 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
       }
       P.c2[g] = n2;
     }
+    // a candidate with a non-finite coordinate: its unscale factor is NaN, so
+    // its mu and variance read NaN (the hot loop's clamps would hide it)
+    if (!(P.c2[0] + P.c2[Prod::NS - 1] < __builtin_huge_valf())) kinv = __builtin_nanf("");
     _Float16* hs = ring;
     if (P.half == 0 && (lane >> 4) == 0) {
 #pragma unroll
@@ -559,7 +567,7 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
         *reinterpret_cast<float4*>(ctile + P.col * D + 4 * t4) =
             float4{cc[4 * t4], cc[4 * t4 + 1], cc[4 * t4 + 2], cc[4 * t4 + 3]};
       if (COMP) wsh[P.col] = wstar;
-      kish[P.col] = ks.kinv;
+      kish[P.col] = kinv;
     }
     __syncthreads();
 #pragma unroll
@@ -616,7 +624,7 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
   C.nb = a.nb;
   C.nbj = (a.nb + 1) / 2;
   C.zero_blk = frag_row_start(a.nb);
-  C.lp_rs = make_rsrc(a.Lp, (C.zero_blk + 1) * 2048);
+  C.lp_rs = make_rsrc(a.Lp, (C.zero_blk + 1) * 2048 + 4 * (a.nb + 1));
   P.xf_rs = make_rsrc(a.xf, a.nb * Prod::NF * 1024);
   P.x2_rs = make_rsrc(a.x2, 2 * n_pad * 4);
   P.al_rs = make_rsrc(a.alpha, n_pad * 4);
@@ -650,12 +658,18 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
       for (int b = 0; b < NCB; ++b) acc[r][b] = floatx4{0.f, 0.f, 0.f, 0.f};
     Slots<RB> sl;
     AFrag av[RB];
+    // the slots' row-block scales, stored after the packed fragments (and the
+    // zero block): entry I < nb, and a zero at nb for slots past the matrix.
+    // Loaded into vector registers: held in scalar ones across the pass they
+    // would spill.
+    float scv[RB];
 #pragma unroll
     for (int r = 0; r < RB; ++r) {
       const int I = slot_block(base, r, wave);
       sl.first[r] = I < a.nb ? frag_row_start(I) : C.zero_blk;
       sl.last[r] = I < a.nb ? I / 2 : -1;
-      sl.sc[r] = I < a.nb ? a.rsc[I] : 0.f;
+      scv[r] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+          C.lp_rs, 4 * min(I, a.nb) + 0 * lane, (C.zero_blk + 1) * 2048, 0));
       av[r] = load_a(C.lp_rs, C.voff, frag_block(sl.first[r], sl.last[r], 0, C.zero_blk));
     }
     // Production schedule. Starting over, blocks 0 and 1 are made here and
@@ -687,20 +701,22 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
     have = (jpass <= kRing) ? max(have, jpass) : 0;
 
     // undo the row-block scale of L^{-1} (the column scale of K*^T is undone
-    // per point in the epilogue)
+    // per point in the epilogue); slots past the matrix hold zeros
 #pragma unroll
-    for (int r = 0; r < RB; ++r)
+    for (int r = 0; r < RB; ++r) {
+      const float sc = scv[r];
 #pragma unroll
       for (int b = 0; b < NCB; ++b)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const float v = acc[r][b][e] * sl.sc[r];
+          const float v = acc[r][b][e] * sc;
           ss[b] = fmaf(v, v, ss[b]);
           if (Q > 1) {
 #pragma unroll
             for (int x = 1; x < NX; ++x) gx[b][x] = fmaf(v, quad_xor(v, x), gx[b][x]);
           }
         }
+    }
   }
 
   // mu: the last pass produced every block; reduce over the lanes of a column
@@ -744,16 +760,19 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
     // undo the columns' kernel-value scales: |v|^2 carries ki^2, a cross
     // product with batch mate tid ^ x carries ki times the mate's
     const float ki = kish[tid];
-    tot[0] = (tot[0] * ki) * ki;
 #pragma unroll
     for (int x = 1; x < NX; ++x) tot[x] = (tot[x] * ki) * kish[tid ^ x];
-    const float mu = mush[tid] + mush[NT + tid];
-    float prior = a.s;
+    const float mu = (mush[tid] + mush[NT + tid]) * ki;
+    float var;
     if constexpr (COMP) {
       const float w = wsh[tid];
-      prior = fmaf(a.s_dep * w, w, a.s + a.s_int);     // s_route + s_dep w*^2 + s_int
+      const float prior = fmaf(a.s_dep * w, w, a.s + a.s_int);     // s_route + s_dep w*^2 + s_int
+      var = prior - (tot[0] * ki) * ki;
+    } else {
+      // in the column's scaled units (s 2^(14-E) - |v|^2 2^(14-E)), then
+      // unscaled: the same rounding as s - |v|^2
+      var = (a.ss - tot[0] * ki) * ki;
     }
-    const float var = prior - tot[0];
     if (valid) {
       a.mu[p * a.m + a.k] = mu;
       // clamp at zero; a NaN variance stays NaN
