@@ -46,6 +46,7 @@ if ROOT not in sys.path:
 
 PEAK_FP32_MFMA_TFLOPS = 157.3
 PEAK_FP16_MFMA_TFLOPS = 2500.0   # dense (no 2:1 sparsity)
+PEAK_FP64_MFMA_TFLOPS = 78.6
 # VALU issue peak derived from the unit counts: 256 CUs x 128 fp32 lanes per
 # clock (the 157.3 TFLOP/s vector figure counted as 2 flops per FMA lane-op)
 # x 2.4 GHz.
@@ -393,6 +394,27 @@ def main(argv=None):
             "flops": "as the roofline (triangle counted once)",
             "score_candidates_per_s": wl.M / ((cpost_ms / max(cc, 1) + ehvi_launch_ms) / 1e3),
         }
+    # fp64 scoring (bo_fit_f64): the same scoring calls with the posterior in
+    # double precision on the fp64 matrix cores
+    mf = bo.fit(X, Y, wl.lengthscale, wl.outputscale, wl.noise, stream=stream, f64=True)
+    bo.score(mf, cand, wl.ref, Z, ehvi=ehvi, stream=stream)
+    torch.cuda.synchronize()
+    bo.profile_enable(True)
+    fsteps = max(1, min(a.steps, 5))
+    for _ in range(fsteps):
+        bo.score(mf, cand, wl.ref, Z, ehvi=ehvi, stream=stream)
+    torch.cuda.synchronize()
+    fpost_ms, fehvi_ms, fc, fl = bo.profile_read()
+    bo.profile_enable(False)
+    del mf
+    f_launch = fpost_ms / max(fl, 1)
+    rec["f64_posterior"] = {
+        "bound": "mfma", "kernel": "k_posterior_f64 (one launch per objective)",
+        "launch_ms": f_launch, "achieved": flops_launch / (f_launch / 1e3) / 1e12,
+        "peak": PEAK_FP64_MFMA_TFLOPS, "unit": "TFLOP/s",
+        "frac": flops_launch / (f_launch / 1e3) / 1e12 / PEAK_FP64_MFMA_TFLOPS,
+        "score_candidates_per_s": wl.M / ((fpost_ms + fehvi_ms) / max(fc, 1) / 1e3),
+    }
     # the noisy acquisition (qNEHVI): in-sample draws and per-draw fronts
     # prepared once, then whole-workload scoring calls
     if wl.m in (2, 3):

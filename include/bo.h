@@ -173,6 +173,37 @@ bo_status bo_fit_composite(const float* X, const float* Y, int64_t n, int32_t d,
                            void* stream, bo_model* out);
 
 /*
+ * bo_fit_f64 / bo_fit_composite_f64 — bo_fit and bo_fit_composite for scoring
+ * in double precision.
+ *
+ * Paper: implementation section (the GP kernels are executed in double
+ * precision; the hyperparameters are learned by maximising the marginal
+ * likelihood). The fit is the same fp64 factorisation; the model also keeps
+ * L^{-1} as fp64 fragments of the fp64 matrix cores, alpha and the inverse
+ * lengthscales in fp64, and bo_score / bo_score_constrained / bo_score_noalloc
+ * then compute the posterior in fp64 (scaled differences from the fp32
+ * inputs, kernel values, mu, V = L^{-1} K*^T with fp64 accumulation, sigma^2
+ * and the q x q factor), rounding mu, sigma and the factor to fp32 for the
+ * acquisition, which is unchanged. Use it where the posterior variance lies
+ * far below the prior (long learned lengthscales, candidates near the data):
+ * there sigma^2 = k(x,x) - |v|^2 cancels beyond what fp32 resolves. The
+ * triangle runs at the fp64 matrix rate, roughly 10x the fp32-class time.
+ *
+ * Arguments, behaviour and errors as bo_fit / bo_fit_composite, except that
+ * the conditioning limit of ILL_CONDITIONED is 2^50 instead of 2^24. The
+ * noisy acquisition (bo_nehvi_prepare) refuses these models
+ * (INVALID_ARGUMENT).
+ */
+bo_status bo_fit_f64(const float* X, const float* Y, int64_t n, int32_t d, int32_t m,
+                     const float* lengthscale, const float* outputscale,
+                     const float* noise, void* stream, bo_model* out);
+bo_status bo_fit_composite_f64(const float* X, const float* Y, int64_t n, int32_t d, int32_t m,
+                               int32_t d_route, const float* lengthscale,
+                               const float* scale_route, const float* scale_dep,
+                               const float* scale_int, const float* pref, const float* noise,
+                               void* stream, bo_model* out);
+
+/*
  * bo_mll — exact log marginal likelihood of each objective's GP and its
  * gradient, for fitting the hyperparameters.
  *

@@ -62,6 +62,10 @@ def lib() -> ctypes.CDLL:
     L.bo_fit.restype = ctypes.c_int
     L.bo_fit_composite.argtypes = [vp, vp, i64, i32, i32, i32, fp, fp, fp, fp, fp, fp, vp,
                                    ctypes.POINTER(vp)]
+    L.bo_fit_f64.argtypes = L.bo_fit.argtypes
+    L.bo_fit_f64.restype = ctypes.c_int
+    L.bo_fit_composite_f64.argtypes = L.bo_fit_composite.argtypes
+    L.bo_fit_composite_f64.restype = ctypes.c_int
     L.bo_fit_composite.restype = ctypes.c_int
     L.bo_mll.argtypes = [vp, vp, i64, i32, i32, fp, fp, fp, vp, vp, vp]
     L.bo_mll.restype = ctypes.c_int
@@ -181,8 +185,9 @@ class Model:
             pass
 
 
-def fit(X, Y, lengthscale, outputscale, noise, stream=None) -> Model:
-    """bo_fit: X [n, d], Y [n, m] fp32 GPU tensors; hyperparameters on host."""
+def fit(X, Y, lengthscale, outputscale, noise, stream=None, f64=False) -> Model:
+    """bo_fit (bo_fit_f64 when f64: scoring in double precision): X [n, d],
+    Y [n, m] fp32 GPU tensors; hyperparameters on host."""
     import torch
     n, d = X.shape
     m = Y.shape[1]
@@ -190,18 +195,20 @@ def fit(X, Y, lengthscale, outputscale, noise, stream=None) -> Model:
     os_ = _host_f32(outputscale, (m,), "outputscale")
     nz = _host_f32(noise, (m,), "noise")
     h = ctypes.c_void_p()
-    st = lib().bo_fit(_dev(X, "X", torch.float32), _dev(Y, "Y", torch.float32), n, d, m,
-                      ls.ctypes.data_as(ctypes.c_void_p), os_.ctypes.data_as(ctypes.c_void_p),
-                      nz.ctypes.data_as(ctypes.c_void_p), _stream(stream), ctypes.byref(h))
-    _check(st, "bo_fit")
+    fn = lib().bo_fit_f64 if f64 else lib().bo_fit
+    st = fn(_dev(X, "X", torch.float32), _dev(Y, "Y", torch.float32), n, d, m,
+            ls.ctypes.data_as(ctypes.c_void_p), os_.ctypes.data_as(ctypes.c_void_p),
+            nz.ctypes.data_as(ctypes.c_void_p), _stream(stream), ctypes.byref(h))
+    _check(st, "bo_fit_f64" if f64 else "bo_fit")
     return Model(h.value, n, d, m)
 
 
 def fit_composite(X, Y, d_route, lengthscale, scale_route, scale_dep, scale_int, pref, noise,
-                  stream=None) -> Model:
-    """bo_fit_composite: the composite kernel (routing Matern-5/2 +
-    preference-weighted deployment Matern-3/2 + interaction). X [n, d],
-    Y [n, m] fp32 GPU tensors; hyperparameters on host (pref [m, d - d_route])."""
+                  stream=None, f64=False) -> Model:
+    """bo_fit_composite (bo_fit_composite_f64 when f64): the composite kernel
+    (routing Matern-5/2 + preference-weighted deployment Matern-3/2 +
+    interaction). X [n, d], Y [n, m] fp32 GPU tensors; hyperparameters on host
+    (pref [m, d - d_route])."""
     import torch
     n, d = X.shape
     m = Y.shape[1]
@@ -213,10 +220,11 @@ def fit_composite(X, Y, d_route, lengthscale, scale_route, scale_dep, scale_int,
     nz = _host_f32(noise, (m,), "noise")
     h = ctypes.c_void_p()
     p = lambda a: a.ctypes.data_as(ctypes.c_void_p)
-    st = lib().bo_fit_composite(_dev(X, "X", torch.float32), _dev(Y, "Y", torch.float32), n, d,
-                                m, int(d_route), p(ls), p(sr), p(sd), p(si), p(pf), p(nz),
-                                _stream(stream), ctypes.byref(h))
-    _check(st, "bo_fit_composite")
+    fn = lib().bo_fit_composite_f64 if f64 else lib().bo_fit_composite
+    st = fn(_dev(X, "X", torch.float32), _dev(Y, "Y", torch.float32), n, d,
+            m, int(d_route), p(ls), p(sr), p(sd), p(si), p(pf), p(nz),
+            _stream(stream), ctypes.byref(h))
+    _check(st, "bo_fit_composite_f64" if f64 else "bo_fit_composite")
     return Model(h.value, n, d, m)
 
 

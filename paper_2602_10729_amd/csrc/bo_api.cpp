@@ -218,8 +218,11 @@ void release_noisy(Model* M) {
 void release_buffers(Model* M) {
   release_noisy(M);
   if (M->Xs || M->invls || M->alpha || M->Lp || M->ws || M->d_boxes || M->wts ||
-      M->pref || M->Xd || M->xf || M->x2 || M->ctr)
+      M->pref || M->Xd || M->xf || M->x2 || M->ctr || M->Lp64)
     (void)hipDeviceSynchronize();
+  pfree(M->Lp64, nullptr);
+  pfree(M->alpha64, nullptr);
+  pfree(M->ils64, nullptr);
   pfree(M->xf, nullptr);
   pfree(M->x2, nullptr);
   pfree(M->ctr, nullptr);
@@ -358,6 +361,8 @@ constexpr double kScaleMin = 0x1p-64, kScaleMax = 0x1p64;
 // max |L^{-1}|^2, a lower bound on the condition number of K, reaches 2^24:
 // beyond it the fp32-class solve, like any fp32 one, carries no correct bit.
 constexpr double kCondLimit = 0x1p24;
+// The same estimate's limit for fp64 scoring (bo_fit_f64): 2^50.
+constexpr double kCondLimitF64 = 0x1p50;
 
 double bits_to_double(unsigned long long b) {
   double v;
@@ -422,6 +427,12 @@ PosteriorArgs posterior_args(const Model& M, int k, const float* Lp,
   pa.s_int = M.dr > 0 ? M.s_int[k] : 0.f;
   pa.wts = M.dr > 0 ? M.wts + (size_t)k * M.n_pad : nullptr;
   pa.pref = M.dr > 0 ? M.pref + (size_t)k * (M.d - M.dr) : nullptr;
+  if (M.f64) {
+    pa.Lp64 = M.Lp64 + (size_t)k * posterior_f64_blocks(M.nb) * 512;
+    pa.alpha64 = M.alpha64 + (size_t)k * M.n_fit;
+    pa.ils64 = M.ils64 + (size_t)k * M.d;
+    pa.Xraw = M.Xd;
+  }
   return pa;
 }
 
@@ -524,7 +535,8 @@ bo_status score_launches(const Model& M, const float* cand, int64_t M_, int q,
   for (int k = 0; k < m; ++k) {
     PosteriorArgs pa = posterior_args(M, k, M.Lp, cand, npts, q);
     pa.mu = mu_buf; pa.sd = sd_buf; pa.chol = chol_buf;
-    if ((s = after_launch(launch_posterior(pa, st), st, "posterior")) != BO_OK) return s;
+    const hipError_t e = M.f64 ? launch_posterior_f64(pa, st) : launch_posterior(pa, st);
+    if ((s = after_launch(e, st, "posterior")) != BO_OK) return s;
   }
   if (rec) {
     hipError_t e = hipEventRecord(rec->e[1], st);
@@ -556,7 +568,7 @@ struct CompositeSpec {
 bo_status fit_impl(const char* who, const float* X, const float* Y, int64_t n, int32_t d,
                    int32_t m, const float* lengthscale, const float* outputscale,
                    const float* noise, const CompositeSpec* comp, void* stream,
-                   bo_model* out) {
+                   bo_model* out, bool f64 = false) {
   const std::string W(who);
   if (!out) return fail(BO_ERR_INVALID_ARGUMENT, W + ": out is NULL");
   if (!lengthscale || !outputscale || !noise)
@@ -612,6 +624,7 @@ bo_status fit_impl(const char* who, const float* X, const float* Y, int64_t n, i
   M->nb = M->n_pad / kBlk;
   M->dx = dx;
   M->dr = dr; M->dr4 = dr4;
+  M->f64 = f64;
   M->ls.assign(lengthscale, lengthscale + (size_t)m * d);
   M->os.assign(outputscale, outputscale + m);
   M->noise.assign(noise, noise + m);
@@ -648,6 +661,12 @@ bo_status fit_impl(const char* who, const float* X, const float* Y, int64_t n, i
   if ((s = palloc(&M->xf, (size_t)m * M->nb * dist_frags(M->dx) * 512, st, "distance fragments")) != BO_OK) return bail(s);
   if ((s = palloc(&M->x2, (size_t)m * 2 * M->n_pad, st, "row norms")) != BO_OK) return bail(s);
   if ((s = palloc(&M->ctr, (size_t)m * M->dx, st, "coordinate centre")) != BO_OK) return bail(s);
+  M->n_fit = nf;
+  if (f64) {
+    if ((s = palloc(&M->Lp64, (size_t)m * posterior_f64_blocks(M->nb) * 512, st, "fp64 fragments")) != BO_OK) return bail(s);
+    if ((s = palloc(&M->alpha64, (size_t)m * nf, st, "fp64 alpha")) != BO_OK) return bail(s);
+    if ((s = palloc(&M->ils64, (size_t)m * d, st, "fp64 inverse lengthscales")) != BO_OK) return bail(s);
+  }
   if (comp) {
     if ((s = palloc(&M->wts, (size_t)m * M->n_pad, st, "preference weights")) != BO_OK) return bail(s);
     if ((s = palloc(&M->pref, (size_t)m * dc, st, "preference slopes")) != BO_OK) return bail(s);
@@ -724,7 +743,13 @@ bo_status fit_impl(const char* who, const float* X, const float* Y, int64_t n, i
   if ((s = after_launch(launch_gram(X, n, d, m, nf, gp, fs.A, st, fs.stats), st, "gram")) != BO_OK) return bail(s);
   if (comp && (s = after_launch(launch_weights(X, n, d, m, M->n_pad, gp, M->wts, st), st, "weights")) != BO_OK) return bail(s);
   if ((s = after_launch(launch_cholesky(fs.A, fs.W, nf, m, fs.flag, st), st, "cholesky")) != BO_OK) return bail(s);
-  if ((s = after_launch(launch_alpha(fs.W, Y, n, m, nf, M->n_pad, fs.tmp, M->alpha, st), st, "alpha")) != BO_OK) return bail(s);
+  if ((s = after_launch(launch_alpha(fs.W, Y, n, m, nf, M->n_pad, fs.tmp, M->alpha, st, M->alpha64), st, "alpha")) != BO_OK) return bail(s);
+  if (f64) {
+    if ((s = after_launch(launch_pack_f64(fs.W, n, m, nf, M->nb, M->Lp64, st), st, "pack fp64")) != BO_OK) return bail(s);
+    // 1 / lengthscale in fp64: the first m d hyperparameters
+    e = hipMemcpyAsync(M->ils64, fs.hyp, sizeof(double) * m * d, hipMemcpyDeviceToDevice, st);
+    if (e != hipSuccess) return bail(hip_fail(e, "bo_fit: fp64 lengthscales"));
+  }
   if ((s = after_launch(launch_pack(fs.W, n, m, nf, M->nb, M->Lp, fs.stats + m, fs.flag, X, d, M->dx, dr, dr4, M->invls, M->Xs, st), st, "pack")) != BO_OK) return bail(s);
   if ((s = after_launch(launch_pack_x(M->Xs, n, m, M->nb, M->dx, dr4, M->ctr, M->xf, M->x2, st), st, "pack X")) != BO_OK) return bail(s);
 
@@ -756,12 +781,12 @@ bo_status fit_impl(const char* who, const float* X, const float* Y, int64_t n, i
       const double kd = bits_to_double(st_bits[k]), wm = bits_to_double(st_bits[m + k]);
       M->kbound[k] = static_cast<float>(kd);
       M->cond_est[k] = kd * wm * wm;
-      if (!(M->cond_est[k] < kCondLimit)) {
+      if (!(M->cond_est[k] < (f64 ? kCondLimitF64 : kCondLimit))) {
         char msg[200];
         std::snprintf(msg, sizeof msg,
-                      ": objective %d: max K_ii * max |L^-1|^2 = %.3g reaches 2^24 (a lower "
-                      "bound on cond(K)); the fp32-class solve cannot resolve this model",
-                      k, M->cond_est[k]);
+                      ": objective %d: max K_ii * max |L^-1|^2 = %.3g reaches %s (a lower "
+                      "bound on cond(K)); the %s scoring cannot resolve this model",
+                      k, M->cond_est[k], f64 ? "2^50" : "2^24", f64 ? "fp64" : "fp32-class");
         return bail(fail(BO_ERR_ILL_CONDITIONED, W + msg));
       }
     }
@@ -908,6 +933,23 @@ bo_status bo_fit_composite(const float* X, const float* Y, int64_t n, int32_t d,
   const CompositeSpec c{d_route, scale_dep, scale_int, pref};
   return fit_impl("bo_fit_composite", X, Y, n, d, m, lengthscale, scale_route, noise, &c,
                   stream, out);
+}
+
+bo_status bo_fit_f64(const float* X, const float* Y, int64_t n, int32_t d, int32_t m,
+                     const float* lengthscale, const float* outputscale, const float* noise,
+                     void* stream, bo_model* out) {
+  return fit_impl("bo_fit_f64", X, Y, n, d, m, lengthscale, outputscale, noise, nullptr, stream,
+                  out, true);
+}
+
+bo_status bo_fit_composite_f64(const float* X, const float* Y, int64_t n, int32_t d, int32_t m,
+                               int32_t d_route, const float* lengthscale,
+                               const float* scale_route, const float* scale_dep,
+                               const float* scale_int, const float* pref, const float* noise,
+                               void* stream, bo_model* out) {
+  const CompositeSpec c{d_route, scale_dep, scale_int, pref};
+  return fit_impl("bo_fit_composite_f64", X, Y, n, d, m, lengthscale, scale_route, noise, &c,
+                  stream, out, true);
 }
 
 void bo_free(bo_model model) {
@@ -1146,6 +1188,9 @@ bo_status nehvi_prepare_impl(bo_model model, const float* ZX, int32_t S, const f
   if (!model) return fail(BO_ERR_INVALID_ARGUMENT, W_ + ": model is NULL");
   Model& M = model->m;
   const int m = M.m, d = M.d;
+  if (M.f64)
+    return fail(BO_ERR_INVALID_ARGUMENT, W_ + ": the noisy acquisition is fp32-class only "
+                                              "(fit with bo_fit or bo_fit_composite)");
   if (m != 2 && m != 3) return fail(BO_ERR_INVALID_ARGUMENT, W_ + ": two or three objectives");
   if (S < 1) return fail(BO_ERR_INVALID_ARGUMENT, W_ + ": S < 1");
   if (S > kNehviMaxS) return fail(BO_ERR_CAPACITY, W_ + ": S beyond 512");

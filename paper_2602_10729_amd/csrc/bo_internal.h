@@ -66,6 +66,13 @@ struct Model {
   size_t lp_per_obj = 0;         // floats per objective in Lp
   std::vector<float> kbound;     // [m] largest diagonal of K (bounds every training prior variance)
   std::vector<double> cond_est;  // [m] max K_ii * max |L^{-1}|^2 (a lower bound on cond(K))
+  // fp64 scoring (bo_fit_f64 / bo_fit_composite_f64): L^{-1} as fp64 MFMA
+  // fragments, alpha and the inverse lengthscales in fp64; the raw X is Xd
+  bool f64 = false;
+  double* Lp64 = nullptr;        // [m][posterior_f64_blocks(nb)][512]
+  double* alpha64 = nullptr;     // [m][n_fit]
+  double* ils64 = nullptr;       // [m][d]
+  int n_fit = 0;
   uint16_t* xf = nullptr;        // [m][nb][dist_frags(dx)][512] distance fragments of X
   float* x2 = nullptr;           // [m][2][n_pad] squared norms of the centred rows
   float* ctr = nullptr;          // [m][dx] centre of the scaled coordinates
@@ -304,11 +311,25 @@ struct PosteriorArgs {
   float s_dep, s_int;  // composite: deployment and interaction scales
   const float* wts;    // composite: [n_pad] preference weights of the training points
   const float* pref;   // composite: [d - dr] preference slopes
+  // fp64 scoring: packed fp64 fragments, alpha and 1 / lengthscale of this
+  // objective, and the raw training inputs [n][d]
+  const double* Lp64 = nullptr;
+  const double* alpha64 = nullptr;
+  const double* ils64 = nullptr;
+  const float* Xraw = nullptr;
   float* mu;           // [npts][m]   (mu of objective k at [p*m+k])
   float* sd;           // [npts][m]   marginal posterior std
   float* chol;         // q > 1: [npts/q][m][q(q+1)/2] lower factor, row-major
 };
 hipError_t launch_posterior(const PosteriorArgs& a, hipStream_t st);
+// The fp64 posterior (posterior_f64.hip): same outputs, from Lp64, alpha64,
+// ils64 and Xraw.
+hipError_t launch_posterior_f64(const PosteriorArgs& a, hipStream_t st);
+// Blocks per objective of the fp64 fragments (lower 16x32 blocks).
+int64_t posterior_f64_blocks(int nb);
+// Pack W = L^{-1} ([m][nf][nf] fp64) as the fp64 kernel's A fragments.
+hipError_t launch_pack_f64(const double* W, int64_t n, int m, int nf, int nb, double* Lp64,
+                           hipStream_t st);
 // Packed L^{-1} blocks per objective (lower 16x32 blocks + the zero block).
 int64_t posterior_frag_blocks(int nb);
 // Floats per objective of the packed inverse factor: the fragment blocks
