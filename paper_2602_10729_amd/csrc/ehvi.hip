@@ -18,11 +18,15 @@
 //
 // Mapping: one lane per candidate batch; the S base samples and the boxes
 // are the same for every lane, so they sit in LDS and every read is a
-// broadcast. Samples are processed in chunks held in registers and each box
+// broadcast. For q > 1 a box that only one member reaches (on any lane and
+// sample of the chunk) adds that member's own extent product; the other
+// subset terms are exact zeros. Samples are processed in chunks held in registers and each box
 // is read once per chunk, which leaves a branch-free VALU loop of
 // 2m + (m-1) + 1 ops per (sample, box) for q = 1. No cross-lane reduction is
 // needed: a lane owns all S x boxes terms of its candidate.
 #include <hip/hip_runtime.h>
+
+#include <algorithm>
 
 #include "bo_internal.h"
 
@@ -99,7 +103,11 @@ __global__ __launch_bounds__(kThreads) void k_ehvi_q1(EhviArgs a) {
 
 // q-batch version: lane owns a batch of Q points; y_s[a][k] is sampled with
 // the lower factor of objective k, then the 2^Q - 1 member subsets are
-// expanded by inclusion-exclusion per box.
+// expanded by inclusion-exclusion per box. Batches are few (131,072 at the
+// q = 4 workload: two waves per SIMD at one lane each), so the four waves of
+// a workgroup share its 64 batches and split the samples; their partial sums
+// are added in LDS in wave order.
+constexpr int kQWaves = kThreads / 64;
 template <int MO, int Q, int SC, bool CONS>
 __global__ __launch_bounds__(kThreads) void k_ehvi_q(EhviArgs a) {
   extern __shared__ float sm[];
@@ -110,8 +118,13 @@ __global__ __launch_bounds__(kThreads) void k_ehvi_q(EhviArgs a) {
   for (int i = threadIdx.x; i < a.S * Q * MO; i += kThreads) zs[i] = a.Z[i];
   for (int i = threadIdx.x; i < a.nbox * 2 * MO; i += kThreads) bx[i] = a.boxes[i];
   __syncthreads();
-  const int64_t b = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int64_t b = (int64_t)blockIdx.x * 64 + lane;
   const bool valid = b < a.nbat;
+  // this wave's samples: a quarter of S, in whole chunks of SC
+  const int sw = (a.S + kQWaves * SC - 1) / (kQWaves * SC) * SC;
+  const int sbeg = wave * sw, send = min(a.S, sbeg + sw);
   float mu[Q][MO];
   float C[MO][T];
   bool nan_in = false;      // a NaN posterior gives a NaN acquisition
@@ -131,12 +144,12 @@ __global__ __launch_bounds__(kThreads) void k_ehvi_q(EhviArgs a) {
     }
 
   float acc_pos = 0.f, acc_neg = 0.f;
-  for (int s0 = 0; s0 < a.S; s0 += SC) {
+  for (int s0 = sbeg; s0 < send; s0 += SC) {
     float y[SC][Q][MO];
 #pragma unroll
     for (int j = 0; j < SC; ++j) {
       const int s = s0 + j;
-      const int sl = (s < a.S) ? s : (a.S - 1);
+      const int sl = (s < send) ? s : (send - 1);
 #pragma unroll
       for (int k = 0; k < MO; ++k)
 #pragma unroll
@@ -144,7 +157,7 @@ __global__ __launch_bounds__(kThreads) void k_ehvi_q(EhviArgs a) {
           float v = mu[i][k];
 #pragma unroll
           for (int t = 0; t <= i; ++t) v = fmaf(C[k][i * (i + 1) / 2 + t], zs[(sl * Q + t) * MO + k], v);
-          y[j][i][k] = (s < a.S) ? v : -__builtin_inff();
+          y[j][i][k] = (s < send) ? v : -__builtin_inff();
         }
       if constexpr (CONS) {
 #pragma unroll
@@ -179,6 +192,40 @@ __global__ __launch_bounds__(kThreads) void k_ehvi_q(EhviArgs a) {
         live = live || nz;
       }
       if (__ballot(live) == 0) continue;   // the whole wave would add zeros
+      // the members that reach the box (above its lower corner in every
+      // objective) on some lane and sample of the chunk; a member subset with
+      // any other member adds exactly zero. Mostly one member reaches a box:
+      // then only its own extent product is formed (the same sum, the other
+      // terms being zeros)
+      int rmask = 0;
+#pragma unroll
+      for (int i = 0; i < Q; ++i) {
+        bool r = false;
+#pragma unroll
+        for (int j = 0; j < SC; ++j) {
+          bool rj = true;
+#pragma unroll
+          for (int k = 0; k < MO; ++k) rj = rj && (y[j][i][k] > lo[k]);
+          r = r || rj;
+        }
+        if (__ballot(r) != 0) rmask |= 1 << i;
+      }
+      if (rmask == 0) continue;
+      if ((rmask & (rmask - 1)) == 0) {
+#pragma unroll
+        for (int i = 0; i < Q; ++i) {
+          if (rmask == (1 << i)) {
+#pragma unroll
+            for (int j = 0; j < SC; ++j) {
+              float t = clamp_ext(y[j][i][0], lo[0], w[0]);
+#pragma unroll
+              for (int k = 1; k < MO; ++k) t *= clamp_ext(y[j][i][k], lo[k], w[k]);
+              acc_pos += t;
+            }
+          }
+        }
+        continue;
+      }
 #pragma unroll
       for (int j = 0; j < SC; ++j) {
         float ext[NS][MO];
@@ -202,7 +249,17 @@ __global__ __launch_bounds__(kThreads) void k_ehvi_q(EhviArgs a) {
       }
     }
   }
-  if (valid) a.ehvi[b] = nan_in ? __builtin_nanf("") : (acc_pos - acc_neg) / static_cast<float>(a.S);
+  // the waves' partial sums, added in wave order (the samples' LDS is done)
+  __syncthreads();
+  float* part = sm;                                 // [kQWaves][64]
+  part[wave * 64 + lane] = acc_pos - acc_neg;
+  __syncthreads();
+  if (wave == 0) {
+    float tot = 0.f;
+#pragma unroll
+    for (int w = 0; w < kQWaves; ++w) tot += part[w * 64 + lane];
+    if (valid) a.ehvi[b] = nan_in ? __builtin_nanf("") : tot / static_cast<float>(a.S);
+  }
 }
 
 // Launch with the dynamic-LDS limit raised for that kernel (set on every
@@ -218,8 +275,12 @@ hipError_t launch_k(K kern, unsigned grid, size_t lds, hipStream_t st, const Ehv
 
 template <int MO, bool CONS>
 hipError_t launch_mo(const EhviArgs& a, hipStream_t st) {
-  const unsigned grid = static_cast<unsigned>((a.nbat + kThreads - 1) / kThreads);
-  const size_t lds = sizeof(float) * ((size_t)a.S * a.q * MO + (size_t)a.nbox * 2 * MO);
+  // q = 1: a lane per candidate; q > 1: a workgroup per 64 batches
+  const int per = (a.q == 1) ? kThreads : 64;
+  const unsigned grid = static_cast<unsigned>((a.nbat + per - 1) / per);
+  // (q > 1: at least the waves' partial sums, which reuse the space at the end)
+  const size_t lds = sizeof(float) * std::max<size_t>((size_t)a.S * a.q * MO + (size_t)a.nbox * 2 * MO,
+                                                      a.q > 1 ? kThreads : 0);
   switch (a.q) {
     case 1: return launch_k(&k_ehvi_q1<MO, 16, CONS>, grid, lds, st, a);
     case 2: return launch_k(&k_ehvi_q<MO, 2, 4, CONS>, grid, lds, st, a);

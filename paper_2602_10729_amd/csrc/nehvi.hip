@@ -24,6 +24,8 @@
 // sample's boxes).
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+
 #include <type_traits>
 
 #include "bo_internal.h"
@@ -507,7 +509,20 @@ __global__ __launch_bounds__(kET) void k_nehvi_ehvi(NehviEhviArgs a) {
     for (int i = threadIdx.x; i < a.total * BW; i += kET) bxl[i] = a.boxes[i];
   __syncthreads();
   const float* bx = LDSB ? bxl : a.boxes;
-  const int64_t b = (int64_t)blockIdx.x * kET + threadIdx.x;
+  // q > 1: batches are few (65,536 per chunk at q = 4), so the waves of a
+  // workgroup share 64 batches and split the draws; their partial sums are
+  // added in LDS in wave order. q = 1: a lane per batch over all draws.
+  constexpr bool SPLIT = Q > 1;
+  constexpr int kEW = kET / 64;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int64_t b = SPLIT ? (int64_t)blockIdx.x * 64 + lane : (int64_t)blockIdx.x * kET + threadIdx.x;
+  int sbeg = 0, send = a.S;
+  if constexpr (SPLIT) {
+    const int sw = (a.S + kEW * U - 1) / (kEW * U) * U;
+    sbeg = wave * sw;
+    send = min(a.S, sbeg + sw);
+  }
   const bool valid = b < a.nbat;
   const int64_t bb = valid ? b : a.nbat - 1;
   float mu[Q][MO];
@@ -530,11 +545,11 @@ __global__ __launch_bounds__(kET) void k_nehvi_ehvi(NehviEhviArgs a) {
   const float* dp = a.D + bb * Q;
   const int64_t kstride = (int64_t)a.S * a.ldd;
   float acc_pos = 0.f, acc_neg = 0.f;
-  for (int s0 = 0; s0 < a.S; s0 += U) {
+  for (int s0 = sbeg; s0 < send; s0 += U) {
     float dv[U][Q][MO];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int s = min(s0 + u, a.S - 1);
+      const int s = min(s0 + u, send - 1);
 #pragma unroll
       for (int k = 0; k < MO; ++k)
 #pragma unroll
@@ -543,7 +558,7 @@ __global__ __launch_bounds__(kET) void k_nehvi_ehvi(NehviEhviArgs a) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int s = s0 + u;
-      if (s >= a.S) continue;     // uniform: the tail of the last group
+      if (s >= send) continue;    // uniform: the tail of the last group
       float y[Q][MO];
 #pragma unroll
       for (int k = 0; k < MO; ++k)
@@ -583,6 +598,32 @@ __global__ __launch_bounds__(kET) void k_nehvi_ehvi(NehviEhviArgs a) {
           for (int k = 0; k < MO; ++k) nz = nz && (ymax[k] > lo[k]);
           if (__ballot(nz) == 0) continue;
         }
+        if constexpr (Q > 1) {
+          // the members that reach the box (above its lower corner in every
+          // objective) on some lane: when only one does, the box adds that
+          // member's own extent product (the other subset terms are zeros)
+          int rmask = 0;
+#pragma unroll
+          for (int i = 0; i < Q; ++i) {
+            bool r = true;
+#pragma unroll
+            for (int k = 0; k < MO; ++k) r = r && (y[i][k] > lo[k]);
+            if (__ballot(r) != 0) rmask |= 1 << i;
+          }
+          if (rmask == 0) continue;
+          if ((rmask & (rmask - 1)) == 0) {
+#pragma unroll
+            for (int i = 0; i < Q; ++i) {
+              if (rmask == (1 << i)) {
+                float t = __builtin_amdgcn_fmed3f(y[i][0] - lo[0], 0.f, w[0]);
+#pragma unroll
+                for (int k = 1; k < MO; ++k) t *= __builtin_amdgcn_fmed3f(y[i][k] - lo[k], 0.f, w[k]);
+                acc_pos += t;
+              }
+            }
+            continue;
+          }
+        }
         if constexpr (Q == 1) {
           float t = __builtin_amdgcn_fmed3f(y[0][0] - lo[0], 0.f, w[0]);
 #pragma unroll
@@ -612,7 +653,20 @@ __global__ __launch_bounds__(kET) void k_nehvi_ehvi(NehviEhviArgs a) {
       }
     }
   }
-  if (valid) a.ehvi[b] = nan_in ? __builtin_nanf("") : (acc_pos - acc_neg) / static_cast<float>(a.S);
+  if constexpr (SPLIT) {
+    __syncthreads();                    // the draws' LDS is done with
+    float* part = esm;                  // [kEW][64]
+    part[wave * 64 + lane] = acc_pos - acc_neg;
+    __syncthreads();
+    if (wave == 0) {
+      float tot = 0.f;
+#pragma unroll
+      for (int w = 0; w < kEW; ++w) tot += part[w * 64 + lane];
+      if (valid) a.ehvi[b] = nan_in ? __builtin_nanf("") : tot / static_cast<float>(a.S);
+    }
+  } else {
+    if (valid) a.ehvi[b] = nan_in ? __builtin_nanf("") : (acc_pos - acc_neg) / static_cast<float>(a.S);
+  }
 }
 
 template <int MO, int Q, bool CONS>
@@ -724,9 +778,13 @@ hipError_t launch_nehvi_means(const NehviMeansArgs& a, int m, hipStream_t st) {
 hipError_t launch_nehvi_ehvi(const NehviEhviArgs& a, hipStream_t st) {
   if (a.nbat <= 0) return hipSuccess;
   const bool ldsb = nehvi_ehvi_lds_bytes(a.S, a.q, a.m, a.total, true) <= 160 * 1024;
-  const size_t lds = nehvi_ehvi_lds_bytes(a.S, a.q, a.m, a.total, ldsb);
+  // (q > 1: at least the waves' partial sums, which reuse the space at the end)
+  const size_t lds = std::max<size_t>(nehvi_ehvi_lds_bytes(a.S, a.q, a.m, a.total, ldsb),
+                                      a.q > 1 ? sizeof(float) * kET : 0);
   if (lds > 160 * 1024) return hipErrorInvalidValue;
-  const unsigned grid = static_cast<unsigned>((a.nbat + kET - 1) / kET);
+  // q = 1: a lane per batch; q > 1: a workgroup per 64 batches
+  const int per = (a.q == 1) ? kET : 64;
+  const unsigned grid = static_cast<unsigned>((a.nbat + per - 1) / per);
   if (a.m == 2) return a.cons ? nz_ehvi_q<2, true>(a, ldsb, lds, grid, st)
                               : nz_ehvi_q<2, false>(a, ldsb, lds, grid, st);
   if (a.m == 3) return a.cons ? nz_ehvi_q<3, true>(a, ldsb, lds, grid, st)
