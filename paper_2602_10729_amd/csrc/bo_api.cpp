@@ -518,14 +518,21 @@ size_t score_workspace_floats(const Model& M, int64_t M_, int q, bool have_mu, b
 }
 
 // The kernels of one scoring call on stream st: the posterior of every
-// objective (into mu_buf, sd_buf and, for q > 1, chol_buf), then the EHVI
-// over `boxes` (device, [nbox][2m]). rec (optional) gets profile events.
+// objective (into mu_buf, sd_buf and, for q > 1, chol_buf [m][M_][T]), then
+// the EHVI over `boxes` (device, [nbox][2m]). mu_buf and sd_buf are the
+// caller's [npts][m] arrays when mu_user / sd_user, else planar [m][npts]
+// workspace, so that each objective's launch writes whole cache lines.
+// rec (optional) gets profile events.
 bo_status score_launches(const Model& M, const float* cand, int64_t M_, int q,
                          const float* feas_lower, const float* base_samples, int S,
-                         const float* boxes, int nbox, float* ehvi, float* mu_buf,
-                         float* sd_buf, float* chol_buf, hipStream_t st, Profile::Rec* rec) {
+                         const float* boxes, int nbox, float* ehvi, float* mu_buf, bool mu_user,
+                         float* sd_buf, bool sd_user, float* chol_buf, hipStream_t st,
+                         Profile::Rec* rec) {
   const int m = M.m;
   const int64_t npts = M_ * q;
+  const int T = q * (q + 1) / 2;
+  const int64_t mu_ps = mu_user ? m : 1, mu_ks = mu_user ? 1 : npts;
+  const int64_t sd_ps = sd_user ? m : 1, sd_ks = sd_user ? 1 : npts;
   bo_status s;
   if (rec) {
     rec->launches = m;
@@ -534,7 +541,9 @@ bo_status score_launches(const Model& M, const float* cand, int64_t M_, int q,
   }
   for (int k = 0; k < m; ++k) {
     PosteriorArgs pa = posterior_args(M, k, M.Lp, cand, npts, q);
-    pa.mu = mu_buf; pa.sd = sd_buf; pa.chol = chol_buf;
+    pa.mu = mu_buf + k * mu_ks; pa.mu_ps = mu_ps;
+    pa.sd = sd_buf + k * sd_ks; pa.sd_ps = sd_ps;
+    pa.chol = chol_buf ? chol_buf + (size_t)k * M_ * T : nullptr;
     const hipError_t e = M.f64 ? launch_posterior_f64(pa, st) : launch_posterior(pa, st);
     if ((s = after_launch(e, st, "posterior")) != BO_OK) return s;
   }
@@ -544,6 +553,7 @@ bo_status score_launches(const Model& M, const float* cand, int64_t M_, int q,
   }
   EhviArgs ea;
   ea.mu = mu_buf; ea.sd = sd_buf; ea.chol = chol_buf;
+  ea.mu_ps = mu_ps; ea.mu_ks = mu_ks; ea.sd_ps = sd_ps; ea.sd_ks = sd_ks;
   ea.Z = base_samples; ea.boxes = boxes;
   ea.nbat = M_; ea.q = q; ea.m = m; ea.S = S; ea.nbox = nbox;
   ea.constrained = feas_lower != nullptr;
@@ -1060,7 +1070,7 @@ bo_status bo_score_constrained(bo_model model, const float* cand, int64_t M_, in
     if (P.on && P.used < P.pool.size()) rec = &P.pool[P.used++];
   }
   if ((s = score_launches(M, cand, M_, q, feas_lower, base_samples, S, M.d_boxes, M.nbox, ehvi,
-                          mu_buf, sd_buf, chol_buf, st, rec)) != BO_OK)
+                          mu_buf, mu != nullptr, sd_buf, sigma != nullptr, chol_buf, st, rec)) != BO_OK)
     return s;
   return mark_call(M, st, "bo_score: stream ordering");
 }
@@ -1098,8 +1108,8 @@ bo_status bo_score_noalloc(bo_model model, const float* cand, int64_t M_, int32_
   float* mu_buf = scr + kNoallocBoxFloats;
   float* sd_buf = mu_buf + (size_t)npts * m;
   float* chol_buf = (q > 1) ? sd_buf + (size_t)npts * m : nullptr;
-  return score_launches(M, cand, M_, q, nullptr, base_samples, S, scr, nbox, ehvi, mu_buf,
-                        sd_buf, chol_buf, st, nullptr);
+  return score_launches(M, cand, M_, q, nullptr, base_samples, S, scr, nbox, ehvi, mu_buf, false,
+                        sd_buf, false, chol_buf, st, nullptr);
 }
 
 }  // extern "C"
@@ -1487,9 +1497,10 @@ bo_status score_nehvi_impl(bo_model model, const float* cand, int64_t M_, int32_
     if ((s = palloc(&z.ws, need, st, "noisy: scoring workspace")) != BO_OK) return s;
     z.ws_floats = need;
   }
-  float* mu_buf = z.ws;                                          // [C][m]
-  float* sd_buf = z.ws + (size_t)C * m;                          // [C][m] marginal tau
-  float* ch_buf = sd_buf + (size_t)C * m;                        // q > 1: [Cb][m][T] factors
+  // planar per objective: each posterior launch writes whole cache lines
+  float* mu_buf = z.ws;                                          // [m][C]
+  float* sd_buf = z.ws + (size_t)C * m;                          // [m][C] marginal tau
+  float* ch_buf = sd_buf + (size_t)C * m;                        // q > 1: [m][Cb][T] factors
   float* dbuf = ch_buf + (q > 1 ? (size_t)Cb * m * T : 0);       // [m][S][C]
   for (int64_t b0 = 0; b0 < M_; b0 += Cb) {
     const int64_t nb_ = std::min<int64_t>(Cb, M_ - b0);
@@ -1497,7 +1508,10 @@ bo_status score_nehvi_impl(bo_model model, const float* cand, int64_t M_, int32_
     const float* cc = cand + b0 * q * M.d;
     for (int k = 0; k < m; ++k) {
       PosteriorArgs pa = posterior_args(M, k, z.Lp0, cc, np_, q);
-      pa.mu = mu_buf; pa.sd = sd_buf; pa.chol = (q > 1) ? ch_buf : nullptr;
+      // chunk-sized planes: the EHVI kernel reads them at the chunk's nbat
+      pa.mu = mu_buf + (size_t)k * np_; pa.sd = sd_buf + (size_t)k * np_;
+      pa.mu_ps = pa.sd_ps = 1;
+      pa.chol = (q > 1) ? ch_buf + (size_t)k * nb_ * T : nullptr;
       if ((s = after_launch(launch_posterior(pa, st), st, "posterior")) != BO_OK) return s;
     }
     NehviMeansArgs ma;

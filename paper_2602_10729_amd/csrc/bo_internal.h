@@ -251,9 +251,9 @@ struct NehviMeansArgs {
 };
 hipError_t launch_nehvi_means(const NehviMeansArgs& a, int m, hipStream_t st);
 struct NehviEhviArgs {
-  const float* mu;         // [nbat * q][m] posterior mean
-  const float* sd;         // q = 1: [nbat][m] noise-free conditional std (tau)
-  const float* chol;       // q > 1: [nbat][m][q(q+1)/2] factor of the conditional batch covariance
+  const float* mu;         // [m][nbat * q] posterior mean (planar)
+  const float* sd;         // q = 1: [m][nbat] noise-free conditional std (tau)
+  const float* chol;       // q > 1: [m][nbat][q(q+1)/2] factor of the conditional batch covariance
   const float* D;          // [m][S][ldd] K* G (point index b * q + member)
   int64_t ldd;
   const float* Z;          // [S][q][m] candidate base samples
@@ -317,9 +317,13 @@ struct PosteriorArgs {
   const double* alpha64 = nullptr;
   const double* ils64 = nullptr;
   const float* Xraw = nullptr;
-  float* mu;           // [npts][m]   (mu of objective k at [p*m+k])
-  float* sd;           // [npts][m]   marginal posterior std
-  float* chol;         // q > 1: [npts/q][m][q(q+1)/2] lower factor, row-major
+  // outputs of this objective: mu and the marginal std of point p at
+  // mu[p * mu_ps] and sd[p * sd_ps] (1 for a planar workspace, m for the
+  // caller's [npts][m] arrays; the pointers are already at the objective)
+  float* mu;
+  float* sd;
+  int64_t mu_ps = 1, sd_ps = 1;
+  float* chol;         // q > 1: [npts/q][q(q+1)/2] lower factors of this objective, row-major
 };
 hipError_t launch_posterior(const PosteriorArgs& a, hipStream_t st);
 // The fp64 posterior (posterior_f64.hip): same outputs, from Lp64, alpha64,
@@ -341,9 +345,12 @@ inline size_t packed_factor_floats(int nb) {
 
 // Monte-Carlo EHVI over boxes for nbat batches.
 struct EhviArgs {
-  const float* mu;     // [nbat*q][m]
-  const float* sd;     // [nbat*q][m]  (q = 1)
-  const float* chol;   // [nbat][m][q(q+1)/2] (q > 1)
+  // mu and sd of objective k at point p: mu[p * mu_ps + k * mu_ks] (planar
+  // workspace: ps = 1, ks = nbat*q; the caller's [nbat*q][m]: ps = m, ks = 1)
+  const float* mu;
+  const float* sd;     // (q = 1)
+  int64_t mu_ps, mu_ks, sd_ps, sd_ks;
+  const float* chol;   // [m][nbat][q(q+1)/2] (q > 1)
   const float* Z;      // [S][q][m]
   const float* boxes;  // [nbox][2m] lo then width
   int64_t nbat;

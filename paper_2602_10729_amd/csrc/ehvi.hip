@@ -62,8 +62,8 @@ __global__ __launch_bounds__(kThreads) void k_ehvi_q1(EhviArgs a) {
   bool nan_in = false;      // a NaN posterior gives a NaN acquisition
 #pragma unroll
   for (int k = 0; k < MO; ++k) {
-    mu[k] = valid ? a.mu[b * MO + k] : 0.f;
-    sd[k] = valid ? a.sd[b * MO + k] : 0.f;
+    mu[k] = valid ? a.mu[b * a.mu_ps + k * a.mu_ks] : 0.f;
+    sd[k] = valid ? a.sd[b * a.sd_ps + k * a.sd_ks] : 0.f;
     nan_in = nan_in || (mu[k] != mu[k]) || (sd[k] != sd[k]);
   }
   float acc = 0.f;
@@ -132,14 +132,14 @@ __global__ __launch_bounds__(kThreads) void k_ehvi_q(EhviArgs a) {
   for (int i = 0; i < Q; ++i)
 #pragma unroll
     for (int k = 0; k < MO; ++k) {
-      mu[i][k] = valid ? a.mu[(b * Q + i) * MO + k] : 0.f;
+      mu[i][k] = valid ? a.mu[(b * Q + i) * a.mu_ps + k * a.mu_ks] : 0.f;
       nan_in = nan_in || (mu[i][k] != mu[i][k]);
     }
 #pragma unroll
   for (int k = 0; k < MO; ++k)
 #pragma unroll
     for (int e = 0; e < T; ++e) {
-      C[k][e] = valid ? a.chol[(b * MO + k) * T + e] : 0.f;
+      C[k][e] = valid ? a.chol[(k * a.nbat + b) * T + e] : 0.f;
       nan_in = nan_in || (C[k][e] != C[k][e]);
     }
 

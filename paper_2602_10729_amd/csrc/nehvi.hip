@@ -532,14 +532,14 @@ __global__ __launch_bounds__(kET) void k_nehvi_ehvi(NehviEhviArgs a) {
   for (int i = 0; i < Q; ++i)
 #pragma unroll
     for (int k = 0; k < MO; ++k) {
-      mu[i][k] = a.mu[(bb * Q + i) * MO + k];
+      mu[i][k] = a.mu[k * a.nbat * Q + bb * Q + i];
       nan_in = nan_in || (mu[i][k] != mu[i][k]);
     }
 #pragma unroll
   for (int k = 0; k < MO; ++k)
 #pragma unroll
     for (int e = 0; e < T; ++e) {
-      C[k][e] = (Q == 1) ? a.sd[bb * MO + k] : a.chol[(bb * MO + k) * T + e];
+      C[k][e] = (Q == 1) ? a.sd[k * a.nbat + bb] : a.chol[(k * a.nbat + bb) * T + e];
       nan_in = nan_in || (C[k][e] != C[k][e]);
     }
   const float* dp = a.D + bb * Q;

@@ -290,9 +290,9 @@ __global__ __launch_bounds__(kThreads) void k_posterior_f64(PosteriorArgs a) {
     }
     const double var = prior - tot[0];
     if (p < a.npts) {
-      a.mu[p * a.m + a.k] = static_cast<float>(mu);
+      a.mu[p * a.mu_ps] = static_cast<float>(mu);
       // clamp at zero; a NaN variance stays NaN
-      a.sd[p * a.m + a.k] = static_cast<float>(sqrt(var < 0.0 ? 0.0 : var));
+      a.sd[p * a.sd_ps] = static_cast<float>(sqrt(var < 0.0 ? 0.0 : var));
     }
     if (Q > 1) {
       kpp[tid][0] = var;
@@ -337,7 +337,7 @@ __global__ __launch_bounds__(kThreads) void k_posterior_f64(PosteriorArgs a) {
           }
         }
         constexpr int T = Q * (Q + 1) / 2;
-        float* dst = a.chol + (bat * a.m + a.k) * T;
+        float* dst = a.chol + bat * T;
 #pragma unroll
         for (int i = 0; i < Q; ++i)
 #pragma unroll

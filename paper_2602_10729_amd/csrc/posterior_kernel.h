@@ -774,9 +774,9 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
       var = (a.ss - tot[0] * ki) * ki;
     }
     if (valid) {
-      a.mu[p * a.m + a.k] = mu;
+      a.mu[p * a.mu_ps] = mu;
       // clamp at zero; a NaN variance stays NaN
-      a.sd[p * a.m + a.k] = __builtin_amdgcn_sqrtf(var < 0.f ? 0.f : var);
+      a.sd[p * a.sd_ps] = __builtin_amdgcn_sqrtf(var < 0.f ? 0.f : var);
     }
     if (Q > 1) {
       // covariance row of this point (diagonal, then partner p ^ x) for the
@@ -826,7 +826,7 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
           }
         }
         constexpr int T = Q * (Q + 1) / 2;
-        float* dst = a.chol + (bat * a.m + a.k) * T;
+        float* dst = a.chol + bat * T;
 #pragma unroll
         for (int i = 0; i < Q; ++i)
 #pragma unroll
