@@ -51,6 +51,17 @@ def test_config1_full_size_elementwise():
     _full_parity(wl, g, o)
 
 
+def test_config2_full_size_dense():
+    """Every one of config 2's 262,144 candidates element by element: the
+    oracle runs over the host's cores (spawned workers, one BLAS thread each)."""
+    import oracle_pool
+    _announce("config2 full dense", 0)
+    wl = bi.make_config(2, seed=0)
+    g = gpu_run(wl)
+    o = oracle_pool.score(oracle_fit(wl), wl.cand, wl.ref, wl.Z)
+    _full_parity(wl, g, o)
+
+
 def _sampled_full_size(cfg, nsample, seed=0):
     wl = bi.make_config(cfg, seed=seed)
     g = gpu_run(wl)

@@ -227,3 +227,17 @@ def test_score_pipeline_small_config_consistency():
     # same estimator recomputed from its parts with the generic box form
     ys = out["mu"][:, 0, None, :] + out["sigma"][:, 0, None, :] * wl.Z.astype(float)[None, :, 0, :]
     np.testing.assert_allclose(out["ehvi"], O.hvi(ys, out["lo"], out["hi"]).mean(axis=1), rtol=1e-12)
+
+
+def test_pooled_oracle_score_matches_one_process():
+    """The tile-parallel oracle used by the dense full-size parity check
+    returns the one-process score, in candidate order."""
+    import bo_inputs as bi
+    import oracle_pool
+    wl = bi.make_config(0, seed=1, M=700)
+    model = O.fit(wl.X, wl.Y, wl.lengthscale, wl.outputscale, wl.noise)
+    one = O.score(model, wl.cand.astype(np.float64), wl.ref, wl.Z.astype(np.float64))
+    many = oracle_pool.score(model, wl.cand, wl.ref, wl.Z, tile=128, workers=2)
+    for k in ("mu", "sigma", "ehvi"):
+        assert many[k].shape == one[k].shape
+        np.testing.assert_allclose(many[k], one[k], rtol=1e-12, atol=1e-14)
