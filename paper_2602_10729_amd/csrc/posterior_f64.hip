@@ -83,7 +83,9 @@ __global__ __launch_bounds__(kThreads) void k_posterior_f64(PosteriorArgs a) {
   constexpr int NX = (Q > 1) ? Q : 1;
   static_assert(PER >= 1 && kJ * NT == PER * kThreads, "whole blocks per step");
   __shared__ __align__(16) double kb[2][NT * kKs];      // produced blocks [col][pos(row)]
-  __shared__ double cs[NT][BO_MAX_D];                   // the tile's candidates (fp64 of fp32)
+  // the tile's candidates (fp64 of fp32), coordinate-major: the lanes of a
+  // wave read consecutive candidates of one coordinate (no bank conflicts)
+  __shared__ double cs[BO_MAX_D][NT];
   __shared__ double ils[BO_MAX_D];                      // 1 / lengthscale (fp64)
   __shared__ float xst[2][kJ][BO_MAX_D];                // staged training rows
   __shared__ double wst[2][kJ];                         // composite: their preference weights
@@ -104,13 +106,13 @@ __global__ __launch_bounds__(kThreads) void k_posterior_f64(PosteriorArgs a) {
   for (int e = tid; e < NT * d; e += kThreads) {
     const int c = e / d, t = e % d;
     const int64_t p = p0 + c;
-    cs[c][t] = (p < a.npts) ? static_cast<double>(a.cand[p * d + t]) : 0.0;
+    cs[t][c] = (p < a.npts) ? static_cast<double>(a.cand[p * d + t]) : 0.0;
   }
   for (int t = tid; t < d; t += kThreads) ils[t] = a.ils64[t];
   __syncthreads();
   if (COMP && tid < NT) {
     double e = 0.0;
-    for (int t = a.dr; t < d; ++t) e = fma(static_cast<double>(a.pref[t - a.dr]), cs[tid][t], e);
+    for (int t = a.dr; t < d; ++t) e = fma(static_cast<double>(a.pref[t - a.dr]), cs[t][tid], e);
     wsh[tid] = exp(e);
   }
 
@@ -143,7 +145,7 @@ __global__ __launch_bounds__(kThreads) void k_posterior_f64(PosteriorArgs a) {
       const int row = jb * kJ + r;
       double ra = 0.0, rc = 0.0;        // plain: all in ra; composite: routing / deployment
       for (int t = 0; t < d; ++t) {
-        const double df = (cs[col][t] - static_cast<double>(xst[jb & 1][r][t])) * ils[t];
+        const double df = (cs[t][col] - static_cast<double>(xst[jb & 1][r][t])) * ils[t];
         if (COMP && t >= a.dr) rc = fma(df, df, rc);
         else ra = fma(df, df, ra);
       }
@@ -169,7 +171,7 @@ __global__ __launch_bounds__(kThreads) void k_posterior_f64(PosteriorArgs a) {
       const int cm = c ^ x;
       double ra = 0.0, rc = 0.0;
       for (int t = 0; t < d; ++t) {
-        const double df = (cs[c][t] - cs[cm][t]) * ils[t];
+        const double df = (cs[t][c] - cs[t][cm]) * ils[t];
         if (COMP && t >= a.dr) rc = fma(df, df, rc);
         else ra = fma(df, df, ra);
       }
