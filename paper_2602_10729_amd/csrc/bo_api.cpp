@@ -17,7 +17,6 @@
 #include <cstring>
 #include <mutex>
 #include <string>
-#include <thread>
 #include <vector>
 
 #include "bo_internal.h"
@@ -85,11 +84,6 @@ bo_status after_launch(hipError_t e, hipStream_t st, const char* what) {
   return BO_OK;
 }
 
-bool all_finite_d(const std::vector<double>& v) {
-  for (double x : v)
-    if (!std::isfinite(x)) return false;
-  return true;
-}
 
 bool all_finite(const float* v, size_t n) {
   for (size_t i = 0; i < n; ++i)
@@ -1138,60 +1132,6 @@ struct NoisyScratch {
   }
 };
 
-// Per-draw fronts and boxes of three-objective in-sample draws on the host
-// (fp64, the same rules as the device kernel for two objectives): rows failing
-// a threshold are left out, the front keeps rows strictly above ref, boxes
-// are (lo, width) in fp32. Draws are split over host threads.
-void host_draw_boxes(const std::vector<double>& F, int S, int64_t n, int m, const float* ref,
-                     const float* lower, std::vector<int>& counts,
-                     std::vector<std::vector<float>>& boxes,
-                     std::vector<std::vector<int32_t>>& fronts) {
-  counts.assign(S, 0);
-  boxes.assign(S, {});
-  fronts.assign(S, {});
-  const double r[3] = {ref[0], ref[1], m > 2 ? static_cast<double>(ref[2]) : 0.0};
-  auto work = [&](int s0, int s1) {
-    std::vector<double> rows;
-    std::vector<int32_t> map, front;
-    std::vector<double> Ff, lo, hi;
-    for (int s = s0; s < s1; ++s) {
-      const double* Fs = F.data() + (size_t)s * n * m;
-      rows.clear();
-      map.clear();
-      for (int64_t i = 0; i < n; ++i) {
-        bool ok = true;
-        if (lower)
-          for (int k = 0; k < m; ++k) ok = ok && Fs[i * m + k] >= static_cast<double>(lower[k]);
-        if (!ok) continue;
-        rows.insert(rows.end(), Fs + i * m, Fs + (i + 1) * m);
-        map.push_back(static_cast<int32_t>(i));
-      }
-      host_front<double>(rows.data(), static_cast<int64_t>(map.size()), m, r, front);
-      Ff.clear();
-      for (int32_t j : front) {
-        Ff.insert(Ff.end(), rows.begin() + (size_t)j * m, rows.begin() + (size_t)(j + 1) * m);
-        fronts[s].push_back(map[j]);
-      }
-      host_boxes<double>(Ff.data(), static_cast<int>(front.size()), m, r, lo, hi);
-      const int nb = static_cast<int>(lo.size() / m);
-      std::vector<float>& out = boxes[s];
-      out.resize((size_t)nb * 2 * m);
-      for (int c = 0; c < nb; ++c)
-        for (int k = 0; k < m; ++k) {
-          const float l = static_cast<float>(lo[(size_t)c * m + k]);
-          out[(size_t)c * 2 * m + k] = l;
-          out[(size_t)c * 2 * m + m + k] = static_cast<float>(hi[(size_t)c * m + k]) - l;
-        }
-      counts[s] = nb;
-    }
-  };
-  const int nt = std::max(1, std::min<int>(16, static_cast<int>(std::thread::hardware_concurrency())));
-  const int per = (S + nt - 1) / nt;
-  std::vector<std::thread> th;
-  for (int t = 0; t < nt && t * per < S; ++t) th.emplace_back(work, t * per, std::min(S, (t + 1) * per));
-  for (auto& x : th) x.join();
-}
-
 bo_status nehvi_prepare_impl(bo_model model, const float* ZX, int32_t S, const float* ref,
                              const float* lower, void* stream) {
   const std::string W_("bo_nehvi_prepare");
@@ -1215,6 +1155,8 @@ bo_status nehvi_prepare_impl(bo_model model, const float* ZX, int32_t S, const f
   bo_status s;
   if ((s = check_dev(ZX, sizeof(float) * (size_t)S * n * m, "base_samples_X")) != BO_OK) return s;
   if (m == 2 && nehvi_front_lds_bytes(n) > 64 * 1024)
+    return fail(BO_ERR_CAPACITY, W_ + ": n beyond the front kernel's LDS");
+  if (m == 3 && nehvi_front3_lds_bytes(n) > kLdsLimit)
     return fail(BO_ERR_CAPACITY, W_ + ": n beyond the front kernel's LDS");
   hipStream_t st = static_cast<hipStream_t>(stream);
   const int nf = static_cast<int>((n + kFitBlk - 1) / kFitBlk) * kFitBlk;
@@ -1246,14 +1188,15 @@ bo_status nehvi_prepare_impl(bo_model model, const float* ZX, int32_t S, const f
   if ((s = palloc(&sc.G, vec, st, "noisy: G")) != BO_OK) return s;
   if ((s = palloc(&sc.Y, (size_t)n * m, st, "noisy: Y")) != BO_OK) return s;
   if ((s = palloc(&sc.alpha, (size_t)m * M.n_pad, st, "noisy: alpha (fp32)")) != BO_OK) return s;
-  if ((s = palloc(&sc.flag, 4, st, "noisy: flags")) != BO_OK) return s;
+  if ((s = palloc(&sc.flag, 8, st, "noisy: flags")) != BO_OK) return s;
   if ((s = palloc(&sc.stats, 2 * (size_t)m, st, "noisy: statistics")) != BO_OK) return s;
-  if ((s = palloc(&sc.counts, (size_t)S, st, "noisy: counts")) != BO_OK) return s;
+  if ((s = palloc(&sc.counts, 2 * (size_t)S, st, "noisy: counts")) != BO_OK) return s;
   if ((s = palloc(&sc.off, (size_t)S + 1, st, "noisy: offsets")) != BO_OK) return s;
   if (m == 2) {
     if ((s = palloc(&sc.btmp, (size_t)S * (n + 1) * 4, st, "noisy: boxes")) != BO_OK) return s;
   } else {
     if ((s = palloc(&sc.Fd, (size_t)S * n * m, st, "noisy: in-sample draws")) != BO_OK) return s;
+    if ((s = palloc(&sc.btmp, (size_t)S * (3 * n + 1) * 6, st, "noisy: boxes")) != BO_OK) return s;
   }
   if ((s = palloc(&z.Lp0, (size_t)m * M.lp_per_obj, st, "noisy: packed factor")) != BO_OK) return s;
   if ((s = palloc(&z.front, (size_t)S * n, st, "noisy: fronts")) != BO_OK) return s;
@@ -1275,10 +1218,10 @@ bo_status nehvi_prepare_impl(bo_model model, const float* ZX, int32_t S, const f
   if (!DS) return fail(BO_ERR_DEVICE, W_ + ": device index out of range");
   std::lock_guard<std::mutex> stage_lock(DS->fit_mu);
   const size_t off_flag = (sizeof(double) * nhyp + 15) / 16 * 16;
-  const size_t off_stats = off_flag + 16;
+  const size_t off_stats = off_flag + 32;
   const size_t off_y = off_stats + 16 * 3;
   const size_t off_cnt = (off_y + sizeof(float) * n * m + 15) / 16 * 16;
-  const size_t off_gmax = (off_cnt + sizeof(int) * S + 15) / 16 * 16;
+  const size_t off_gmax = (off_cnt + sizeof(int) * 2 * S + 15) / 16 * 16;
   const size_t off_off = off_gmax + sizeof(double) * m * kAbsmaxParts;
   const size_t need = off_off + sizeof(int) * ((size_t)S + 1);
   hipError_t e = hipSuccess;
@@ -1302,7 +1245,7 @@ bo_status nehvi_prepare_impl(bo_model model, const float* ZX, int32_t S, const f
   e = hipMemcpyAsync(sc.hyp, stage, sizeof(double) * nhyp, hipMemcpyHostToDevice, st);
   if (e == hipSuccess)
     e = hipMemcpyAsync(sc.Y, stage + off_y, sizeof(float) * n * m, hipMemcpyHostToDevice, st);
-  if (e == hipSuccess) e = hipMemsetAsync(sc.flag, 0, 4 * sizeof(int), st);
+  if (e == hipSuccess) e = hipMemsetAsync(sc.flag, 0, 8 * sizeof(int), st);
   if (e == hipSuccess) e = hipMemsetAsync(sc.stats, 0, sizeof(unsigned long long) * 2 * m, st);
   if (e != hipSuccess) return sync_fail(hip_fail(e, "bo_nehvi_prepare: upload"));
 
@@ -1336,7 +1279,6 @@ bo_status nehvi_prepare_impl(bo_model model, const float* ZX, int32_t S, const f
   if ((s = step(launch_trmm(false, sc.A, sc.Zk, sc.T1, nf, Sp, m, st), "trmm")) != BO_OK) return sync_fail(s);
   if ((s = step(launch_trmm(false, sc.W0, sc.T1, sc.Zk, nf, Sp, m, st), "trmm")) != BO_OK) return sync_fail(s);
   if ((s = step(launch_trmm(true, sc.W0, sc.Zk, sc.G, nf, Sp, m, st), "trmm")) != BO_OK) return sync_fail(s);
-  std::vector<double> Fh;
   if (m == 2) {
     // fronts and boxes of every draw on the device
     NehviFrontArgs fa;
@@ -1351,13 +1293,22 @@ bo_status nehvi_prepare_impl(bo_model model, const float* ZX, int32_t S, const f
     e = hipMemcpyAsync(stage + off_cnt, sc.counts, sizeof(int) * S, hipMemcpyDeviceToHost, st);
     if (e != hipSuccess) return sync_fail(hip_fail(e, "bo_nehvi_prepare: counts"));
   } else {
+    // three objectives: the draws, then every draw's front and boxes on the device
     if ((s = step(launch_insample_values(sc.Y, sc.alpha64, gp.noise, sc.T1, n, m, nf, Sp, S, sc.Fd, st), "draws")) != BO_OK) return sync_fail(s);
-    Fh.resize((size_t)S * n * m);
-    e = hipMemcpyAsync(Fh.data(), sc.Fd, sizeof(double) * Fh.size(), hipMemcpyDeviceToHost, st);
-    if (e != hipSuccess) return sync_fail(hip_fail(e, "bo_nehvi_prepare: draws"));
+    NehviFront3Args fa;
+    fa.F = sc.Fd; fa.n = n; fa.S = S;
+    for (int k = 0; k < 3; ++k) {
+      fa.ref[k] = ref[k];
+      fa.low[k] = lower ? lower[k] : -INFINITY;
+    }
+    fa.cons = lower != nullptr;
+    fa.boxes = sc.btmp; fa.counts = sc.counts; fa.front = z.front; fa.bad = sc.flag + 4;
+    if ((s = step(launch_sample_fronts3(fa, st), "fronts")) != BO_OK) return sync_fail(s);
+    e = hipMemcpyAsync(stage + off_cnt, sc.counts, sizeof(int) * 2 * S, hipMemcpyDeviceToHost, st);
+    if (e != hipSuccess) return sync_fail(hip_fail(e, "bo_nehvi_prepare: counts"));
   }
   if ((s = step(launch_absmax(sc.G, (int64_t)nf * Sp, m, sc.gmax, st), "absmax")) != BO_OK) return sync_fail(s);
-  e = hipMemcpyAsync(stage + off_flag, sc.flag, 4 * sizeof(int), hipMemcpyDeviceToHost, st);
+  e = hipMemcpyAsync(stage + off_flag, sc.flag, 8 * sizeof(int), hipMemcpyDeviceToHost, st);
   if (e == hipSuccess)
     e = hipMemcpyAsync(stage + off_stats, sc.stats, sizeof(unsigned long long) * 2 * m,
                        hipMemcpyDeviceToHost, st);
@@ -1366,7 +1317,7 @@ bo_status nehvi_prepare_impl(bo_model model, const float* ZX, int32_t S, const f
                        hipMemcpyDeviceToHost, st);
   if (e == hipSuccess) e = hipStreamSynchronize(st);
   if (e != hipSuccess) return sync_fail(hip_fail(e, "bo_nehvi_prepare: sync"));
-  int flags[4];
+  int flags[8];
   std::memcpy(flags, stage + off_flag, sizeof(flags));
   if (flags[0]) return sync_fail(fail(BO_ERR_NOT_POSITIVE_DEFINITE, W_ + ": K not positive definite"));
   if (flags[1]) return sync_fail(fail(BO_ERR_NOT_POSITIVE_DEFINITE, W_ + ": in-sample posterior covariance not positive definite"));
@@ -1389,18 +1340,14 @@ bo_status nehvi_prepare_impl(bo_model model, const float* ZX, int32_t S, const f
       }
     }
   }
-  std::vector<std::vector<float>> hboxes;
-  std::vector<std::vector<int32_t>> hfronts;
+  const int* cnt_h = reinterpret_cast<const int*>(stage + off_cnt);
+  z.counts.assign(cnt_h, cnt_h + S);
+  z.fsize.resize(S);
   if (m == 2) {
-    z.counts.assign(reinterpret_cast<const int*>(stage + off_cnt),
-                    reinterpret_cast<const int*>(stage + off_cnt) + S);
-    z.fsize.resize(S);
     for (int i = 0; i < S; ++i) z.fsize[i] = z.counts[i] - 1;     // the staircase has P + 1 boxes
   } else {
-    if (!all_finite_d(Fh)) return sync_fail(fail(BO_ERR_NONFINITE_INPUT, W_ + ": non-finite in-sample draw"));
-    host_draw_boxes(Fh, S, n, m, ref, lower, z.counts, hboxes, hfronts);
-    z.fsize.resize(S);
-    for (int i = 0; i < S; ++i) z.fsize[i] = static_cast<int>(hfronts[i].size());
+    if (flags[4]) return sync_fail(fail(BO_ERR_NONFINITE_INPUT, W_ + ": non-finite in-sample draw"));
+    for (int i = 0; i < S; ++i) z.fsize[i] = cnt_h[S + i];
   }
   int* off = reinterpret_cast<int*>(stage + off_off);
   int64_t total = 0;
@@ -1437,17 +1384,7 @@ bo_status nehvi_prepare_impl(bo_model model, const float* ZX, int32_t S, const f
   if (m == 2) {
     if ((s = step(launch_compact_boxes(sc.btmp, (int64_t)(n + 1) * 4, z.off, S, z.boxes, st), "boxes")) != BO_OK) return sync_fail(s);
   } else {
-    // boxes and fronts built on the host: one pageable upload each
-    std::vector<float> flat((size_t)total * 2 * m);
-    std::vector<int32_t> fr((size_t)S * n, -1);
-    for (int i = 0; i < S; ++i) {
-      std::copy(hboxes[i].begin(), hboxes[i].end(), flat.begin() + (size_t)off[i] * 2 * m);
-      std::copy(hfronts[i].begin(), hfronts[i].end(), fr.begin() + (size_t)i * n);
-    }
-    e = hipMemcpy(z.boxes, flat.data(), sizeof(float) * flat.size(), hipMemcpyHostToDevice);
-    if (e == hipSuccess)
-      e = hipMemcpy(z.front, fr.data(), sizeof(int32_t) * fr.size(), hipMemcpyHostToDevice);
-    if (e != hipSuccess) return sync_fail(hip_fail(e, "bo_nehvi_prepare: boxes"));
+    if ((s = step(launch_compact_boxes3(sc.btmp, (int64_t)(3 * n + 1) * 6, z.off, S, z.boxes, st), "boxes")) != BO_OK) return sync_fail(s);
   }
   if ((s = step(launch_pack_g(sc.G, nf, Sp, n32, m, scale, z.Gp, st), "pack G")) != BO_OK) return sync_fail(s);
   e = hipStreamSynchronize(st);

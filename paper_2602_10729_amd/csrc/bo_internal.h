@@ -219,6 +219,23 @@ struct NehviFrontArgs {
   int32_t* front;          // [S][n]
 };
 hipError_t launch_sample_fronts(const NehviFrontArgs& a, hipStream_t st);
+// Per-sample fronts and boxes of three objectives (k_sample_front3).
+struct NehviFront3Args {
+  const double* F;         // [S][n][3] in-sample draws
+  int64_t n;
+  int S;
+  float ref[3];
+  bool cons;
+  float low[3];
+  float* boxes;            // [S][3n + 1][6]
+  int* counts;             // [2S]: boxes, then front size, per sample
+  int32_t* front;          // [S][n]
+  int* bad;                // set to 1 on a non-finite draw
+};
+hipError_t launch_sample_fronts3(const NehviFront3Args& a, hipStream_t st);
+size_t nehvi_front3_lds_bytes(int64_t n);
+hipError_t launch_compact_boxes3(const float* tmp, int64_t stride, const int* off, int S,
+                                 float* out, hipStream_t st);
 // F[s][i][k] = y_ik - eta_k alpha_k,i + T1[k][i][s] (fp64, the in-sample draws)
 hipError_t launch_insample_values(const float* Y, const double* alpha64, const double* noise,
                                   const double* T1, int64_t n, int m, int nf, int Sp, int S,

@@ -141,6 +141,199 @@ __global__ __launch_bounds__(256) void k_sample_front(NehviFrontArgs a) {
   if (tid == 0) a.counts[s] = P + 1;
 }
 
+// Three objectives, one workgroup per sample s, from the in-sample values
+// F[s][i][k] (fp64). The front is selected by the rule above (points
+// strictly above ref and meeting the thresholds; non-dominated, exact
+// duplicates keep the lowest index) and listed by objective 0 ascending
+// (ties by index). Its boxes come from a sweep over the front points by
+// objective 2 descending (ties in list order) that keeps the staircase of
+// the points swept so far in the (objective 0, objective 1) plane, sorted by
+// objective 0: step t covers objective 0 from the previous step's value (ref
+// for the first) to its own and objective 1 from its own value up, and
+// carries the objective-2 value where its current box began (its top). A
+// new point that lies under a step in both coordinates adds nothing; else it
+// removes the steps it covers (objective 0 and 1 both at most its own), each
+// removed step and the step to its right (or the tail box past the last
+// step) close a box from the new point's objective 2 up to their tops, and it
+// enters the staircase with its own value as top; the step to its right
+// restarts there too. After the sweep every step, and the tail box above
+// ref_1, closes down to ref_2. Boxes are (lo0, lo1, lo2, w0, w1, w2) with
+// widths in fp32 (inf for unbounded sides), at most 3P + 1 per sample:
+// boxes[s][3n + 1][6], counts[s] = their number, counts[S + s] = P; a
+// non-finite value sets *bad.
+__global__ __launch_bounds__(256) void k_sample_front3(NehviFront3Args a) {
+  extern __shared__ double fsh[];
+  __shared__ int tsum[256];
+  __shared__ int np;
+  const int n = static_cast<int>(a.n);
+  double* f0 = fsh;
+  double* f1 = f0 + n;
+  double* f2 = f1 + n;
+  double* sx = f2 + n;          // staircase: objective 0, 1, top
+  double* sy = sx + n;
+  double* sz = sy + n;
+  int* flag = reinterpret_cast<int*>(sz + n);
+  int* pidx = flag + n;
+  int* sorted = pidx + n;
+  const int s = blockIdx.x, tid = threadIdx.x;
+  const double r0 = a.ref[0], r1 = a.ref[1], r2 = a.ref[2];
+  bool bad = false;
+  for (int i = tid; i < n; i += 256) {
+    const double* v = a.F + ((int64_t)s * n + i) * 3;
+    const double v0 = v[0], v1 = v[1], v2 = v[2];
+    bad = bad || !(fabs(v0) < __builtin_inf() && fabs(v1) < __builtin_inf() &&
+                   fabs(v2) < __builtin_inf());
+    bool ok = v0 > r0 && v1 > r1 && v2 > r2;
+    if (a.cons)
+      ok = ok && v0 >= static_cast<double>(a.low[0]) && v1 >= static_cast<double>(a.low[1]) &&
+           v2 >= static_cast<double>(a.low[2]);
+    f0[i] = ok ? v0 : -__builtin_inf();
+    f1[i] = ok ? v1 : -__builtin_inf();
+    f2[i] = ok ? v2 : -__builtin_inf();
+    flag[i] = ok ? 1 : 0;
+  }
+  if (bad) atomicOr(a.bad, 1);
+  __syncthreads();
+  for (int i = tid; i < n; i += 256) {
+    if (!flag[i]) continue;
+    const double a0 = f0[i], a1 = f1[i], a2 = f2[i];
+    bool dom = false;
+    for (int j = 0; j < n; ++j) {
+      const double b0 = f0[j], b1 = f1[j], b2 = f2[j];
+      const bool ge = b0 >= a0 && b1 >= a1 && b2 >= a2;
+      dom = dom || (ge && (b0 > a0 || b1 > a1 || b2 > a2 || j < i));
+    }
+    pidx[i] = dom ? 0 : 1;
+  }
+  __syncthreads();
+  for (int i = tid; i < n; i += 256) flag[i] = flag[i] ? pidx[i] : 0;
+  __syncthreads();
+  // compaction in index order: thread t owns a contiguous chunk
+  const int per = (n + 255) / 256;
+  const int i0 = min(n, tid * per), i1 = min(n, i0 + per);
+  int cnt = 0;
+  for (int i = i0; i < i1; ++i) cnt += flag[i];
+  tsum[tid] = cnt;
+  __syncthreads();
+  if (tid == 0) {
+    int run = 0;
+    for (int t = 0; t < 256; ++t) {
+      const int c = tsum[t];
+      tsum[t] = run;
+      run += c;
+    }
+    np = run;
+  }
+  __syncthreads();
+  {
+    int p = tsum[tid];
+    for (int i = i0; i < i1; ++i)
+      if (flag[i]) pidx[p++] = i;
+  }
+  __syncthreads();
+  const int P = np;
+  // list order: objective 0 ascending, ties by index
+  for (int q = tid; q < P; q += 256) {
+    const double v = f0[pidx[q]];
+    int rank = 0;
+    for (int r = 0; r < P; ++r) {
+      const double w = f0[pidx[r]];
+      rank += (w < v || (w == v && r < q)) ? 1 : 0;
+    }
+    sorted[rank] = pidx[q];
+    a.front[(int64_t)s * n + rank] = pidx[q];
+  }
+  __syncthreads();
+  // sweep order: objective 2 descending, ties in list order (flag[] reused)
+  for (int q = tid; q < P; q += 256) {
+    const double v = f2[sorted[q]];
+    int rank = 0;
+    for (int r = 0; r < P; ++r) {
+      const double w = f2[sorted[r]];
+      rank += (w > v || (w == v && r < q)) ? 1 : 0;
+    }
+    flag[rank] = sorted[q];
+  }
+  __syncthreads();
+  if (tid != 0) return;
+  float* bx = a.boxes + (int64_t)s * (3 * n + 1) * 6;
+  int nb = 0;
+  auto close = [&](double xl, double xh, double yl, double zl, double zt) {
+    if (zt > zl) {
+      const float l0 = static_cast<float>(xl), l1 = static_cast<float>(yl),
+                  l2 = static_cast<float>(zl);
+      float* o = bx + 6 * nb;
+      o[0] = l0;
+      o[1] = l1;
+      o[2] = l2;
+      o[3] = static_cast<float>(xh) - l0;
+      o[4] = __builtin_inff();
+      o[5] = static_cast<float>(zt) - l2;
+      ++nb;
+    }
+  };
+  int cntst = 0;
+  double tail = __builtin_inf();
+  for (int t = 0; t < P; ++t) {
+    const int idx = flag[t];
+    const double px = f0[idx], py = f1[idx], zb = f2[idx];
+    int p = 0;                                   // first step with x >= px
+    while (p < cntst && sx[p] < px) ++p;
+    if (p < cntst && sy[p] >= py) continue;      // under a step in both coordinates
+    const int first_rm = (p < cntst && sx[p] == px) ? p + 1 : p;
+    int left = p;
+    while (left > 0 && sy[left - 1] <= py) --left;
+    double xl = (left == 0) ? r0 : sx[left - 1];
+    for (int r = left; r < first_rm; ++r) {
+      close(xl, sx[r], sy[r], zb, sz[r]);
+      xl = sx[r];
+    }
+    if (first_rm < cntst) {
+      close(xl, sx[first_rm], sy[first_rm], zb, sz[first_rm]);
+      sz[first_rm] = zb;
+    } else {
+      close(xl, __builtin_inf(), r1, zb, tail);
+      tail = zb;
+    }
+    // steps [left, first_rm) give way to the new one at left
+    const int removed = first_rm - left;
+    if (removed == 0) {
+      for (int r = cntst; r > left; --r) {
+        sx[r] = sx[r - 1];
+        sy[r] = sy[r - 1];
+        sz[r] = sz[r - 1];
+      }
+    } else {
+      for (int r = first_rm; r < cntst; ++r) {
+        sx[r - removed + 1] = sx[r];
+        sy[r - removed + 1] = sy[r];
+        sz[r - removed + 1] = sz[r];
+      }
+    }
+    cntst += 1 - removed;
+    sx[left] = px;
+    sy[left] = py;
+    sz[left] = zb;
+  }
+  double xl = r0;
+  for (int r = 0; r < cntst; ++r) {
+    close(xl, sx[r], sy[r], r2, sz[r]);
+    xl = sx[r];
+  }
+  close(xl, __builtin_inf(), r1, r2, tail);
+  a.counts[s] = nb;
+  a.counts[a.S + s] = P;
+}
+
+// Boxes of three objectives from [S][stride] to the compact layout at off[s].
+__global__ __launch_bounds__(64) void k_compact_boxes3(const float* __restrict__ tmp,
+                                                       int64_t stride, const int* __restrict__ off,
+                                                       float* __restrict__ out) {
+  const int s = blockIdx.x;
+  const int b0 = off[s], nb = off[s + 1] - b0;
+  for (int e = threadIdx.x; e < 6 * nb; e += 64) out[6 * (int64_t)b0 + e] = tmp[(int64_t)s * stride + e];
+}
+
 // part[k][b] = max |G[k][e]| over the entries e = b*256 + t (mod 256 x
 // gridDim.x) of workgroup b; the host takes the maximum of the parts.
 __global__ __launch_bounds__(256) void k_absmax(const double* __restrict__ G, int64_t count,
@@ -721,6 +914,27 @@ hipError_t launch_sample_fronts(const NehviFrontArgs& a, hipStream_t st) {
   // at most 28 n bytes (57 KiB at n = 2048): within the default limit
   const size_t lds = nehvi_front_lds_bytes(a.n);
   hipLaunchKernelGGL(k_sample_front, dim3(a.S), dim3(256), lds, st, a);
+  return hipGetLastError();
+}
+
+size_t nehvi_front3_lds_bytes(int64_t n) {
+  return sizeof(double) * 6 * n + sizeof(int) * 3 * n;
+}
+
+hipError_t launch_sample_fronts3(const NehviFront3Args& a, hipStream_t st) {
+  // 60 n bytes (120 KiB at n = 2048): beyond the default dynamic limit
+  const size_t lds = nehvi_front3_lds_bytes(a.n);
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_sample_front3),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize,
+                                     static_cast<int>(lds));
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_sample_front3, dim3(a.S), dim3(256), lds, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_compact_boxes3(const float* tmp, int64_t stride, const int* off, int S,
+                                 float* out, hipStream_t st) {
+  hipLaunchKernelGGL(k_compact_boxes3, dim3(S), dim3(64), 0, st, tmp, stride, off, out);
   return hipGetLastError();
 }
 

@@ -208,7 +208,8 @@ def test_noisy_batch_parity_two_objectives(cfg, M, q, seed):
 @pytest.mark.parametrize("q,M,S,seed", [(1, 400, 128, 0), (4, 48, 512, 0), (2, 96, 200, 1)])
 def test_noisy_three_objectives(q, M, S, seed):
     # config 4's observations (n = 2048, d = 24, three objectives): per-draw
-    # fronts and 3-D boxes built on the host, boxes read from global memory
+    # fronts and 3-D boxes built on the device, boxes read from global memory;
+    # every draw's front is checked
     _announce("nehvi three objectives", q, M, S, seed)
     wl = bi.make_config(4, seed=seed, M=M)
     ZX = bi.insample_base_samples(wl, S)
@@ -222,7 +223,7 @@ def test_noisy_three_objectives(q, M, S, seed):
     o = _oracle(wl, cand, ZX, Zs)
     assert_close(g["ehvi"], o["ehvi"], TOL_EHVI, "nehvi three objectives")
     check_argmax(g["idx"], o["ehvi"])
-    _check_fronts(g, o, wl.ref, None, range(0, S, max(1, S // 8)))
+    _check_fronts(g, o, wl.ref, None, range(S))
 
 
 def test_noisy_three_objectives_constrained():
