@@ -193,45 +193,78 @@ __global__ __launch_bounds__(256) void k_sample_front3(NehviFront3Args a) {
     flag[i] = ok ? 1 : 0;
   }
   if (bad) atomicOr(a.bad, 1);
-  __syncthreads();
-  for (int i = tid; i < n; i += 256) {
-    if (!flag[i]) continue;
-    const double a0 = f0[i], a1 = f1[i], a2 = f2[i];
-    bool dom = false;
-    for (int j = 0; j < n; ++j) {
-      const double b0 = f0[j], b1 = f1[j], b2 = f2[j];
-      const bool ge = b0 >= a0 && b1 >= a1 && b2 >= a2;
-      dom = dom || (ge && (b0 > a0 || b1 > a1 || b2 > a2 || j < i));
-    }
-    pidx[i] = dom ? 0 : 1;
-  }
-  __syncthreads();
-  for (int i = tid; i < n; i += 256) flag[i] = flag[i] ? pidx[i] : 0;
-  __syncthreads();
-  // compaction in index order: thread t owns a contiguous chunk
+  // j beats i: at least as large in every objective and larger in one, or an
+  // exact duplicate with a lower index (a strict order: the front is the set
+  // of points nothing beats)
+  auto beats = [&](int j, int i) {
+    const double a0 = f0[i], a1 = f1[i], a2 = f2[i], b0 = f0[j], b1 = f1[j], b2 = f2[j];
+    return b0 >= a0 && b1 >= a1 && b2 >= a2 && (b0 > a0 || b1 > a1 || b2 > a2 || j < i);
+  };
+  // compaction of the flagged points in index order into pidx (thread t owns
+  // a contiguous chunk); returns their number
   const int per = (n + 255) / 256;
   const int i0 = min(n, tid * per), i1 = min(n, i0 + per);
-  int cnt = 0;
-  for (int i = i0; i < i1; ++i) cnt += flag[i];
-  tsum[tid] = cnt;
-  __syncthreads();
-  if (tid == 0) {
-    int run = 0;
-    for (int t = 0; t < 256; ++t) {
-      const int c = tsum[t];
-      tsum[t] = run;
-      run += c;
+  auto compact = [&]() {
+    __syncthreads();
+    int cnt = 0;
+    for (int i = i0; i < i1; ++i) cnt += flag[i];
+    tsum[tid] = cnt;
+    __syncthreads();
+    if (tid == 0) {
+      int run = 0;
+      for (int t = 0; t < 256; ++t) {
+        const int c = tsum[t];
+        tsum[t] = run;
+        run += c;
+      }
+      np = run;
     }
-    np = run;
-  }
-  __syncthreads();
-  {
+    __syncthreads();
     int p = tsum[tid];
     for (int i = i0; i < i1; ++i)
       if (flag[i]) pidx[p++] = i;
+    __syncthreads();
+    return np;
+  };
+  // Screen: the largest-sum point of each thread's chunk forms a strong set;
+  // a point some member beats is not on the front. Then the survivors are
+  // checked against each other: a point off the front is beaten by a front
+  // point (the order is transitive), and front points survive the screen.
+  {
+    int best = -1;
+    double bs = -__builtin_inf();
+    for (int i = i0; i < i1; ++i) {
+      const double sm = f0[i] + f1[i] + f2[i];
+      if (flag[i] && sm > bs) {
+        bs = sm;
+        best = i;
+      }
+    }
+    __syncthreads();
+    tsum[tid] = best;
+    __syncthreads();
+    for (int i = tid; i < n; i += 256) {
+      if (!flag[i]) continue;
+      bool dom = false;
+      for (int t = 0; t < 256 && !dom; ++t) {
+        const int j = tsum[t];
+        dom = j >= 0 && beats(j, i);
+      }
+      pidx[i] = dom ? 0 : 1;
+    }
+    __syncthreads();
+    for (int i = tid; i < n; i += 256) flag[i] = flag[i] ? pidx[i] : 0;
   }
+  const int V = compact();                     // survivors in pidx[0, V)
+  for (int q = tid; q < V; q += 256) sorted[q] = pidx[q];
   __syncthreads();
-  const int P = np;
+  for (int q = tid; q < V; q += 256) {
+    const int i = sorted[q];
+    bool dom = false;
+    for (int r = 0; r < V && !dom; ++r) dom = beats(sorted[r], i);
+    flag[i] = dom ? 0 : 1;
+  }
+  const int P = compact();
   // list order: objective 0 ascending, ties by index
   for (int q = tid; q < P; q += 256) {
     const double v = f0[pidx[q]];
@@ -277,8 +310,12 @@ __global__ __launch_bounds__(256) void k_sample_front3(NehviFront3Args a) {
   for (int t = 0; t < P; ++t) {
     const int idx = flag[t];
     const double px = f0[idx], py = f1[idx], zb = f2[idx];
-    int p = 0;                                   // first step with x >= px
-    while (p < cntst && sx[p] < px) ++p;
+    int p = 0, hi = cntst;                       // first step with x >= px
+    while (p < hi) {
+      const int mid = (p + hi) >> 1;
+      if (sx[mid] < px) p = mid + 1;
+      else hi = mid;
+    }
     if (p < cntst && sy[p] >= py) continue;      // under a step in both coordinates
     const int first_rm = (p < cntst && sx[p] == px) ? p + 1 : p;
     int left = p;
