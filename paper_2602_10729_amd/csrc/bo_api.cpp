@@ -107,7 +107,23 @@ struct DeviceState {
   std::mutex fit_mu;
   unsigned char* fit_stage = nullptr;
   size_t fit_stage_bytes = 0;
+  // under fit_mu: a second stream (default priority) for independent work
+  // inside one call, joined back by the two events
+  hipStream_t side = nullptr;
+  hipEvent_t side_evt[2] = {nullptr, nullptr};
 };
+
+// The side stream and its events of device state DS (created once).
+bo_status side_stream(DeviceState* DS) {
+  if (DS->side) return BO_OK;
+  hipError_t e = hipStreamCreateWithFlags(&DS->side, hipStreamNonBlocking);
+  if (e != hipSuccess) { DS->side = nullptr; return hip_fail(e, "side stream"); }
+  for (int i = 0; i < 2; ++i) {
+    e = hipEventCreateWithFlags(&DS->side_evt[i], hipEventDisableTiming);
+    if (e != hipSuccess) return hip_fail(e, "side stream event");
+  }
+  return BO_OK;
+}
 constexpr int kMaxDevices = 64;
 
 DeviceState* device_state(int dev) {
@@ -1237,6 +1253,7 @@ bo_status nehvi_prepare_impl(bo_model model, const float* ZX, int32_t S, const f
   unsigned char* stage = DS->fit_stage;
   auto sync_fail = [&](bo_status st_) {
     (void)hipStreamSynchronize(st);   // copies from the staging buffer may be pending
+    if (DS->side) (void)hipStreamSynchronize(DS->side);   // and work on the side stream
     release_noisy(&M);
     return st_;
   };
@@ -1262,6 +1279,20 @@ bo_status nehvi_prepare_impl(bo_model model, const float* ZX, int32_t S, const f
   GramParams g0 = gp;
   g0.noise = gp.noise + m;                  // zeros: the noise-free K_XX
   auto step = [&](hipError_t err, const char* what) { return after_launch(err, st, what); };
+  // The noise-free K_XX (factor, inverse, packed for the conditional
+  // (co)variance) is independent of K's chain: it runs on the side stream,
+  // after the uploads above, and joins before its factor is used.
+  if ((s = side_stream(DS)) != BO_OK) return sync_fail(s);
+  hipStream_t side = DS->side;
+  auto sstep = [&](hipError_t err, const char* what) { return after_launch(err, side, what); };
+  e = hipEventRecord(DS->side_evt[0], st);
+  if (e == hipSuccess) e = hipStreamWaitEvent(side, DS->side_evt[0], 0);
+  if (e != hipSuccess) return sync_fail(hip_fail(e, "bo_nehvi_prepare: side stream"));
+  if ((s = sstep(launch_gram(M.Xd, n, d, m, nf, g0, sc.A0, side, sc.stats), "gram")) != BO_OK) return sync_fail(s);
+  if ((s = sstep(launch_cholesky(sc.A0, sc.W0, nf, m, sc.flag + 2, side), "cholesky")) != BO_OK) return sync_fail(s);
+  if ((s = sstep(launch_pack_factor(sc.W0, n, m, nf, M.nb, z.Lp0, sc.stats + m, sc.flag + 3, side), "pack")) != BO_OK) return sync_fail(s);
+  e = hipEventRecord(DS->side_evt[1], side);
+  if (e != hipSuccess) return sync_fail(hip_fail(e, "bo_nehvi_prepare: side stream"));
   // K = K_XX + eta I: factor, inverse, alpha (fp64), then K^{-1}
   if ((s = step(launch_gram(M.Xd, n, d, m, nf, gp, sc.A, st), "gram")) != BO_OK) return sync_fail(s);
   if ((s = step(launch_cholesky(sc.A, sc.W, nf, m, sc.flag, st), "cholesky")) != BO_OK) return sync_fail(s);
@@ -1270,10 +1301,9 @@ bo_status nehvi_prepare_impl(bo_model model, const float* ZX, int32_t S, const f
   // in-sample posterior covariance eta (I - eta K^{-1}) and its factor
   if ((s = step(launch_sigma_xx(sc.A, n, nf, m, gp.noise, st), "in-sample covariance")) != BO_OK) return sync_fail(s);
   if ((s = step(launch_cholesky(sc.A, sc.W, nf, m, sc.flag + 1, st), "cholesky")) != BO_OK) return sync_fail(s);
-  // noise-free K_XX: factor, inverse, packed for the conditional (co)variance
-  if ((s = step(launch_gram(M.Xd, n, d, m, nf, g0, sc.A0, st, sc.stats), "gram")) != BO_OK) return sync_fail(s);
-  if ((s = step(launch_cholesky(sc.A0, sc.W0, nf, m, sc.flag + 2, st), "cholesky")) != BO_OK) return sync_fail(s);
-  if ((s = step(launch_pack_factor(sc.W0, n, m, nf, M.nb, z.Lp0, sc.stats + m, sc.flag + 3, st), "pack")) != BO_OK) return sync_fail(s);
+  // the noise-free factor from the side stream
+  e = hipStreamWaitEvent(st, DS->side_evt[1], 0);
+  if (e != hipSuccess) return sync_fail(hip_fail(e, "bo_nehvi_prepare: side stream"));
   // T1 = L_XX Z_X, G = K_XX^{-1} T1 = W0^T (W0 T1)
   if ((s = step(launch_gather_z(ZX, n, m, S, nf, Sp, sc.Zk, st), "gather")) != BO_OK) return sync_fail(s);
   if ((s = step(launch_trmm(false, sc.A, sc.Zk, sc.T1, nf, Sp, m, st), "trmm")) != BO_OK) return sync_fail(s);
