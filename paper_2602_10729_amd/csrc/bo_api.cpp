@@ -1484,6 +1484,8 @@ bo_status score_nehvi_impl(bo_model model, const float* cand, int64_t M_, int32_
     NehviMeansArgs ma;
     ma.cand = cc; ma.npts = np_; ma.d = M.d; ma.dx = M.dx; ma.n32 = z.n32;
     ma.n_pad = M.n_pad; ma.S = S; ma.Xs = M.Xs; ma.invls = M.invls; ma.Gp = z.Gp;
+    ma.xf = M.xf; ma.xf_stride = (int64_t)M.nb * dist_frags(M.dx) * 512;
+    ma.x2 = M.x2; ma.ctr = M.ctr;
     for (int k = 0; k < 3; ++k) {
       ma.s[k] = k < m ? M.os[k] : 0.f;
       ma.kbound[k] = k < m ? M.kbound[k] : 1.f;

@@ -254,6 +254,10 @@ struct NehviMeansArgs {
   int d, dx, n32, n_pad, S;
   const float* Xs;         // [m][n_pad][dx] scaled training inputs
   const float* invls;      // [m][dx]
+  const uint16_t* xf;      // [m][xf_stride] centred-X distance fragments (fp16 bits)
+  int64_t xf_stride;
+  const float* x2;         // [m][2][n_pad] squared norms of the centred rows per group
+  const float* ctr;        // [m][dx] centre of the scaled coordinates
   const uint16_t* Gp;      // packed G^T fragments (fp16 bits)
   float s[3];              // output scales (composite: of the routing term)
   float kbound[3];         // composite: bound on every training point's prior variance

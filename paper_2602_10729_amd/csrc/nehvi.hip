@@ -483,47 +483,65 @@ constexpr int kRingSlot = 2 * kPlane;  // hi + lo planes of one 32-row block
 // D[k][s][c] = sum_i G[k][i][s] K*_k(c, i) for the candidates of one tile and
 // every sample: blockIdx.x = tile of 64 candidates, blockIdx.y = objective.
 // Each 32-row block J of K*^T (training rows x candidates) is evaluated two
-// steps ahead into a three-slot LDS ring as fp16 hi/lo planes (wave w makes
-// rows 4w .. 4w+3 for all 64 candidates, one candidate per lane, from
-// training rows staged in LDS three steps ahead), while the matrix cores add
-// G^T[slots of this wave][J] K*^T[J] into accumulators that stay in registers
-// for the whole tile: wave w owns the sample blocks w + 8r (r < CB), all four
-// candidate blocks. Three products per pair (hi hi, hi lo, lo hi), fp32
-// accumulate. Training rows past the matrix read as zero; their G rows are
-// zero, so they add nothing. COMP: the composite kernel
+// steps ahead into a three-slot LDS ring as fp16 hi/lo planes, while the
+// matrix cores add G^T[slots of this wave][J] K*^T[J] into accumulators that
+// stay in registers for the whole tile: wave w owns the sample blocks w + 8r
+// (r < CB), all four candidate blocks. Three products per pair (hi hi, hi lo,
+// lo hi), fp32 accumulate. Training rows past the matrix read as zero; their
+// G rows are zero, so they add nothing.
+// The kernel values are made as the posterior kernel makes them: wave w
+// forms the squared distances of rows 16(w/4) .. +15 and candidates
+// 16(w%4) .. +15 of a block with a few more MFMAs (|c|^2 + |x|^2 - 2 c.x over
+// centred coordinates, from the training rows' distance fragments the fit
+// stores and the candidates' made here), and recomputes a pair from exact
+// differences of the scaled coordinates where the expansion could cancel
+// (approximate r^2 below 1 + (|c|^2 + |x|^2)/256). COMP: the composite kernel
 //   s_route M52(r_route) + s_dep w(c) w(x) M32(r_dep) + s_int M52 M32,
-// the routing coordinates in the first 4 dr4 slots, the training rows'
-// weights staged beside them.
+// one expansion per coordinate group (routing slots first).
 template <int DX4, int CB, bool COMP>
 __global__ __launch_bounds__(kMW * 64) void k_nehvi_means(NehviMeansArgs a) {
   constexpr int RS = 4 * DX4;
-  __shared__ __align__(16) float xst[2][32 * RS];
-  __shared__ float wst[2][32];             // COMP: weights of the staged rows
+  constexpr int NS = COMP ? 2 : 1;
+  constexpr int F0 = dist_frags0(RS), NF = dist_frags(RS);
+  static_assert(F0 == 1 && NF <= 3, "at most 32 coordinate slots");
+  static_assert(2 * kMT * 96 <= 3 * kRingSlot, "candidate fragments fit the ring");
   __shared__ __align__(16) _Float16 ring[3 * kRingSlot];
+  __shared__ __align__(16) float ctile[kMT * RS];   // exact scaled candidates
   __shared__ float kish[kMT];              // 2^(E-14): undoes a candidate's split scale
   const int k = blockIdx.y;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   const int64_t c0 = (int64_t)blockIdx.x * kMT;
   const int nrb = 8 * CB;
-  const float* Xs = a.Xs + (int64_t)k * a.n_pad * a.dx;
   const float* il = a.invls + k * a.dx;
+  const float* ctr = a.ctr + k * a.dx;
   const float sk = a.s[k];
-  const __amdgpu_buffer_rsrc_t xs_rs = rsrc(Xs, a.n_pad * a.dx * 4);
+  const float sint = COMP ? a.s_int[k] : 0.f;
+  const __amdgpu_buffer_rsrc_t xs_rs = rsrc(a.Xs + (int64_t)k * a.n_pad * a.dx,
+                                            a.n_pad * a.dx * 4);
+  const __amdgpu_buffer_rsrc_t xf_rs = rsrc(a.xf + (int64_t)k * a.xf_stride,
+                                            (a.n_pad / 16) * NF * 1024);
+  const __amdgpu_buffer_rsrc_t x2_rs = rsrc(a.x2 + (int64_t)k * 2 * a.n_pad, 2 * a.n_pad * 4);
+  const __amdgpu_buffer_rsrc_t w_rs = rsrc(COMP ? a.wts + (int64_t)k * a.n_pad : a.Xs,
+                                           COMP ? a.n_pad * 4 : 0);
   const __amdgpu_buffer_rsrc_t g_rs = rsrc(a.Gp + (int64_t)k * a.n32 * nrb * 1024,
                                            a.n32 * nrb * 2048);
-  // this lane's candidate, scaled, in the slot layout (zero past npts and in
+  // this lane's place in a produced block: column (candidate) col, rows
+  // rq .. rq+3 (the MFMA result layout of its wave's 16x16 distance tile)
+  const int half = wave >> 2;
+  const int col = 16 * (wave & 3) + (lane & 15);
+  const int rq = 16 * half + 4 * (lane >> 4);
+  // the column's candidate, scaled, in the slot layout (zero past npts and in
   // padding slots); COMP: s_dep times its preference weight
-  float cx[RS];
+  float cc[RS];
   float wsd = 0.f, wstar = 0.f;
-  const float sint = COMP ? a.s_int[k] : 0.f;
   {
-    const int64_t c = c0 + lane;
+    const int64_t c = c0 + col;
     const bool ok = c < a.npts;
 #pragma unroll
     for (int t = 0; t < RS; ++t) {
       const int cd = slot_dim(t, a.d, a.dr, a.dr4);
-      cx[t] = (ok && cd >= 0) ? a.cand[c * a.d + cd] * il[t] : 0.f;
+      cc[t] = (ok && cd >= 0) ? a.cand[c * a.d + cd] * il[t] : 0.f;
     }
     if constexpr (COMP) {
       if (ok) {
@@ -535,74 +553,162 @@ __global__ __launch_bounds__(kMW * 64) void k_nehvi_means(NehviMeansArgs a) {
       }
     }
   }
-  // power of two for this candidate's kernel values before their split (the
-  // composite covariance is bounded by sqrt(prior(candidate) * kbound))
+  // power of two for this column's kernel values before their split (the
+  // composite covariance is bounded by sqrt(prior(candidate) * kbound)); the
+  // values are made scaled, the scale rides in the output scales
   const KvScale ks = kv_split_scale(
       COMP ? __builtin_amdgcn_sqrtf(fmaf(wsd, wstar, sk + sint) * a.kbound[k]) : sk);
-  if (wave == 0) kish[lane] = ks.kinv;
-  // the kernel values are made scaled: the scale rides in the output scales
   const float sks = sk * ks.ksc, sints = sint * ks.ksc;
   wsd *= ks.ksc;
-  const __amdgpu_buffer_rsrc_t w_rs = rsrc(COMP ? a.wts + (int64_t)k * a.n_pad : a.Xs,
-                                           COMP ? a.n_pad * 4 : 0);
-  const int wrow = threadIdx.x - 256;       // COMP: threads 256 .. 287 stage the weights
-  // staging: thread t < 32 * DX4 moves one float4 of row t / DX4
-  const bool stager = threadIdx.x < 32 * DX4;
-  const int srow = stager ? threadIdx.x / DX4 : 0, st4 = threadIdx.x % DX4;
-  auto stage_load = [&](int jb) {
-    float4 v = ld4(xs_rs, ((jb * 32 + srow) * a.dx + 4 * st4) * 4, 0);
-    if constexpr (COMP) {
-      // the weight rides in the thread's fourth float when it stages one
-      if (wrow >= 0 && wrow < 32)
-        v.w = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
-                                            w_rs, (jb * 32 + wrow) * 4, 0, 0));
+  // centred coordinates: squared norms per group, and the B fragments of the
+  // distance MFMAs, staged in the (not yet used) ring as 96 halves per group
+  // and column: [0, 32) stream 0 (hi, zero past RS), [32, 96) stream 1 (hi at
+  // p < RS, 2^11-scaled lo at RS <= p < 2RS, zero beyond)
+  float c2[NS];
+  halfx8 cb[NS][NF];
+  {
+    float ct[RS];
+#pragma unroll
+    for (int t = 0; t < RS; ++t) ct[t] = cc[t] - ctr[t];
+#pragma unroll
+    for (int g = 0; g < NS; ++g) {
+      float n2 = 0.f;
+#pragma unroll
+      for (int t = 0; t < RS; ++t) {
+        const bool in = !COMP || ((t < 4 * a.dr4) == (g == 0));
+        if (in) n2 = fmaf(ct[t], ct[t], n2);
+      }
+      c2[g] = n2;
     }
-    return v;
-  };
-  auto stage_store = [&](int jb, float4 v) {
-    if (stager) *reinterpret_cast<float4*>(&xst[jb & 1][srow * RS + 4 * st4]) = v;
-    if constexpr (COMP) {
-      if (wrow >= 0 && wrow < 32) wst[jb & 1][wrow] = v.w;
+    if (half == 0 && (lane >> 4) == 0) {
+#pragma unroll
+      for (int g = 0; g < NS; ++g) {
+        _Float16* h = ring + (g * kMT + col) * 96;
+        halfx8 v[12];
+#pragma unroll
+        for (int i = 0; i < 12; ++i) v[i] = halfx8{};
+#pragma unroll
+        for (int t = 0; t < RS; ++t) {
+          const bool in = !COMP || ((t < 4 * a.dr4) == (g == 0));
+          const _Float16 hi = static_cast<_Float16>(in ? ct[t] : 0.f);
+          const _Float16 lo = static_cast<_Float16>(
+              in ? (ct[t] - static_cast<float>(static_cast<_Float16>(ct[t]))) * kDistLoScale : 0.f);
+          v[t / 8][t % 8] = hi;
+          v[(32 + t) / 8][(32 + t) % 8] = hi;
+          v[(32 + RS + t) / 8][(32 + RS + t) % 8] = lo;
+        }
+#pragma unroll
+        for (int i = 0; i < 12; ++i) *reinterpret_cast<halfx8*>(h + 8 * i) = v[i];
+      }
+#pragma unroll
+      for (int t4 = 0; t4 < DX4; ++t4)
+        *reinterpret_cast<float4*>(ctile + col * RS + 4 * t4) =
+            float4{cc[4 * t4], cc[4 * t4 + 1], cc[4 * t4 + 2], cc[4 * t4 + 3]};
+      kish[col] = ks.kinv;
     }
+    __syncthreads();
+#pragma unroll
+    for (int g = 0; g < NS; ++g)
+#pragma unroll
+      for (int f = 0; f < NF; ++f)
+        cb[g][f] = *reinterpret_cast<const halfx8*>(ring + (g * kMT + col) * 96 + 32 * f +
+                                                    8 * (lane >> 4));
+    __syncthreads();   // the ring is written from here on
+  }
+
+  // operands of the block made next, loaded a step ahead
+  halfx8 xa[NF];
+  floatx4 x2v[NS], wtv;
+  auto prod_load = [&](int jb) {
+    const int vo = (2 * jb + half) * (NF * 1024) + lane * 16;
+#pragma unroll
+    for (int f = 0; f < NF; ++f) xa[f] = __builtin_bit_cast(halfx8, ld4(xf_rs, vo + f * 1024, 0));
+    const int row = jb * 32 + rq;
+#pragma unroll
+    for (int g = 0; g < NS; ++g)
+      x2v[g] = __builtin_bit_cast(floatx4, ld4(x2_rs, ((COMP ? g : 1) * a.n_pad + row) * 4, 0));
+    if constexpr (COMP) wtv = __builtin_bit_cast(floatx4, ld4(w_rs, row * 4, 0));
   };
   auto produce = [&](int jb) {
-    const float* xr = &xst[jb & 1][4 * wave * RS];
-    halfx4 hi, lo;
+    floatx4 d0[NS], d1[NS];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      float r2 = 0.f, r2r = 0.f;    // r2r: composite, the routing part
+    for (int g = 0; g < NS; ++g) {
+      d0[g] = floatx4{0.f, 0.f, 0.f, 0.f};
+      d1[g] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int t4 = 0; t4 < DX4; ++t4) {
-        if constexpr (COMP) {
-          if (t4 == a.dr4) {         // routing slots come first
-            r2r = r2;
-            r2 = 0.f;
+      for (int f = 0; f < F0; ++f)
+        d0[g] = __builtin_amdgcn_mfma_f32_16x16x32_f16(xa[f], cb[g][f], d0[g], 0, 0, 0);
+#pragma unroll
+      for (int f = F0; f < NF; ++f)
+        d1[g] = __builtin_amdgcn_mfma_f32_16x16x32_f16(xa[f], cb[g][f], d1[g], 0, 0, 0);
+    }
+    float r2[NS][4];
+    bool ex[4];
+    bool any = false;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      float rt = 0.f, nt = 0.f;
+#pragma unroll
+      for (int g = 0; g < NS; ++g) {
+        const float nrm = c2[g] + x2v[g][e];
+        const float dot = fmaf(d1[g][e], 1.0f / kDistLoScale, d0[g][e]);
+        r2[g][e] = fmaxf(fmaf(-2.0f, dot, nrm), 0.f);
+        rt += r2[g][e];
+        nt += nrm;
+      }
+      ex[e] = rt < fmaf(nt, 1.0f / 256.0f, 1.0f);
+      any = any || ex[e];
+    }
+    if (__builtin_amdgcn_ballot_w64(any) != 0) {
+      // exact differences for the pairs that need them (rows past n_pad read
+      // zero coordinates); rare, kept off the common path
+      asm volatile("" ::: "memory");
+      const float* cx = ctile + col * RS;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int row = jb * 32 + rq + e;
+        float s0 = 0.f, s1 = 0.f;   // routing / deployment (plain: s1 only)
+#pragma unroll
+        for (int t4 = 0; t4 < DX4; ++t4) {
+          const float4 x = ld4(xs_rs, (row * a.dx + 4 * t4) * 4, 0);
+          const float4 cv = *reinterpret_cast<const float4*>(cx + 4 * t4);
+          const float e0 = cv.x - x.x, e1 = cv.y - x.y, e2 = cv.z - x.z, e3 = cv.w - x.w;
+          float t = fmaf(e0, e0, 0.f);
+          t = fmaf(e1, e1, t);
+          t = fmaf(e2, e2, t);
+          t = fmaf(e3, e3, t);
+          if (COMP && t4 < a.dr4) s0 += t;
+          else s1 += t;
+        }
+        if (ex[e]) {
+          if constexpr (COMP) {
+            r2[0][e] = s0;
+            r2[1][e] = s1;
+          } else {
+            r2[0][e] = s1;
           }
         }
-        const float4 x = *reinterpret_cast<const float4*>(xr + u * RS + 4 * t4);
-        const float d0 = cx[4 * t4 + 0] - x.x, d1 = cx[4 * t4 + 1] - x.y;
-        const float d2 = cx[4 * t4 + 2] - x.z, d3 = cx[4 * t4 + 3] - x.w;
-        r2 = fmaf(d0, d0, r2);
-        r2 = fmaf(d1, d1, r2);
-        r2 = fmaf(d2, d2, r2);
-        r2 = fmaf(d3, d3, r2);
       }
+    }
+    halfx4 hi, lo;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
       float kv;
       if constexpr (COMP) {
-        const float k5 = m52(r2r, 1.0f);
-        const float k3 = m32(r2);
-        kv = fmaf(wsd * wst[jb & 1][4 * wave + u], k3, k5 * fmaf(sints, k3, sks));
+        const float k5 = m52(r2[0][e], 1.0f);
+        const float k3 = m32(r2[1][e]);
+        kv = fmaf(wsd * wtv[e], k3, k5 * fmaf(sints, k3, sks));
       } else {
-        kv = m52(r2, sks);
+        kv = m52(r2[0][e], sks);
       }
       // one fp32 value for both halves (the compiler may otherwise fuse the
       // last product into the fp16 conversions and derive the high half twice)
       asm volatile("" : "+v"(kv));
       const _Float16 h = static_cast<_Float16>(kv);
-      hi[u] = h;
-      lo[u] = static_cast<_Float16>(kv - static_cast<float>(h));
+      hi[e] = h;
+      lo[e] = static_cast<_Float16>(kv - static_cast<float>(h));
     }
-    _Float16* dst = ring + (jb % 3) * kRingSlot + lane * kKS + 4 * wave;
+    _Float16* dst = ring + (jb % 3) * kRingSlot + col * kKS + rq;
     *reinterpret_cast<halfx4*>(dst) = hi;
     *reinterpret_cast<halfx4*>(dst + kPlane) = lo;
   };
@@ -619,32 +725,32 @@ __global__ __launch_bounds__(kMW * 64) void k_nehvi_means(NehviMeansArgs a) {
 #pragma unroll
   for (int r = 0; r < CB; ++r)
 #pragma unroll
-    for (int cb = 0; cb < 4; ++cb) acc[r][cb] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int cb4 = 0; cb4 < 4; ++cb4) acc[r][cb4] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  // prologue: rows of blocks 0, 1 staged; blocks 0, 1 produced; rows of 2 staged
-  stage_store(0, stage_load(0));
-  stage_store(1, stage_load(1));
-  __syncthreads();
+  // prologue: blocks 0 and 1 produced, block 2's operands loaded
+  prod_load(0);
   produce(0);
-  if (a.n32 > 1) produce(1);
-  __syncthreads();
-  stage_store(2, stage_load(2));
+  if (a.n32 > 1) {
+    prod_load(1);
+    produce(1);
+  }
+  prod_load(2);
   halfx8 ah[CB], al[CB];
   load_a(0, ah, al);
-  __syncthreads();
+  lds_sync();
 
   // One step: the MFMAs of block J (each product pass over all accumulators
   // before the next, so no MFMA waits on the one before it) and, when PROD,
-  // the evaluation of block J + 2, interleaved by the scheduler pattern below.
+  // the evaluation of block J + 2, interleaved by the scheduler pattern below;
+  // then the operands of block J + 3.
   auto step = [&](int J, auto prod) {
     constexpr bool PROD = decltype(prod)::value;
-    const float4 nx = stage_load(J + 3);
     halfx8 bh[4], bl[4];
     const _Float16* kb = ring + (J % 3) * kRingSlot + (lane % 16) * kKS + 8 * (lane / 16);
 #pragma unroll
-    for (int cb = 0; cb < 4; ++cb) {
-      bh[cb] = *reinterpret_cast<const halfx8*>(kb + 16 * cb * kKS);
-      bl[cb] = *reinterpret_cast<const halfx8*>(kb + 16 * cb * kKS + kPlane);
+    for (int cb4 = 0; cb4 < 4; ++cb4) {
+      bh[cb4] = *reinterpret_cast<const halfx8*>(kb + 16 * cb4 * kKS);
+      bl[cb4] = *reinterpret_cast<const halfx8*>(kb + 16 * cb4 * kKS + kPlane);
     }
     halfx8 nh[CB], nl[CB];
     load_a(min(J + 1, a.n32 - 1), nh, nl);
@@ -652,22 +758,22 @@ __global__ __launch_bounds__(kMW * 64) void k_nehvi_means(NehviMeansArgs a) {
 #pragma unroll
     for (int r = 0; r < CB; ++r)
 #pragma unroll
-      for (int cb = 0; cb < 4; ++cb)
-        acc[r][cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah[r], bh[cb], acc[r][cb], 0, 0, 0);
+      for (int cb4 = 0; cb4 < 4; ++cb4)
+        acc[r][cb4] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah[r], bh[cb4], acc[r][cb4], 0, 0, 0);
 #pragma unroll
     for (int r = 0; r < CB; ++r)
 #pragma unroll
-      for (int cb = 0; cb < 4; ++cb)
-        acc[r][cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah[r], bl[cb], acc[r][cb], 0, 0, 0);
+      for (int cb4 = 0; cb4 < 4; ++cb4)
+        acc[r][cb4] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah[r], bl[cb4], acc[r][cb4], 0, 0, 0);
 #pragma unroll
     for (int r = 0; r < CB; ++r)
 #pragma unroll
-      for (int cb = 0; cb < 4; ++cb)
-        acc[r][cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(al[r], bh[cb], acc[r][cb], 0, 0, 0);
+      for (int cb4 = 0; cb4 < 4; ++cb4)
+        acc[r][cb4] = __builtin_amdgcn_mfma_f32_16x16x32_f16(al[r], bh[cb4], acc[r][cb4], 0, 0, 0);
     if constexpr (PROD) {
       // interleave the kernel-value VALU work with the MFMAs
       constexpr int nM = 12 * CB;
-      constexpr int nV = 4 * (8 * DX4 + 14);
+      constexpr int nV = 4 * (COMP ? 34 : 20);
 #pragma unroll
       for (int i = 0; i < nM; ++i) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                  // MFMA
@@ -680,7 +786,7 @@ __global__ __launch_bounds__(kMW * 64) void k_nehvi_means(NehviMeansArgs a) {
       ah[r] = nh[r];
       al[r] = nl[r];
     }
-    stage_store(J + 3, nx);
+    if constexpr (PROD) prod_load(J + 3);
     lds_sync();
   };
   int J = 0;
