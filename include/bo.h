@@ -350,11 +350,11 @@ bo_status bo_score_noalloc(bo_model model, const float* cand, int64_t M, int32_t
  *   base_samples_X device [S][n][m] iid N(0,1), row-major (draw, observed
  *                  point, objective); 1 <= S <= 512
  *   ref_point      host [m];  feas_lower host [m] or NULL
- *   Builds, in fp64, the in-sample posterior and its factor, the S in-sample
- *   draws, each draw's front and box decomposition (on the device for two
- *   objectives, on the host's threads for three), the factor of K_XX and
- *   G = K_XX^{-1} L_XX Z_X; keeps them in the model (replacing an earlier
- *   preparation). Synchronous.
+ *   Builds, in fp64 on the device, the in-sample posterior and its factor,
+ *   the S in-sample draws, each draw's front and box decomposition, the
+ *   factor of K_XX (on a library-owned second stream of the model's device,
+ *   joined back to `stream`) and G = K_XX^{-1} L_XX Z_X; keeps them in the
+ *   model (replacing an earlier preparation). Synchronous.
  *   Errors: INVALID_ARGUMENT (m not 2 or 3, bad S or pointer), CAPACITY (S > 512, too many boxes), NOT_POSITIVE_DEFINITE (K,
  *   the in-sample covariance or K_XX), NONFINITE_INPUT, OUT_OF_MEMORY,
  *   DEVICE.
