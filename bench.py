@@ -421,9 +421,14 @@ def main(argv=None):
         ZX = torch.from_numpy(bi.insample_base_samples(wl)).to(dev)
         mn = bo.fit(X, Y, wl.lengthscale, wl.outputscale, wl.noise, stream=stream)
         torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        bo.nehvi_prepare(mn, ZX, wl.ref, stream=stream)
-        prep_ms = (time.perf_counter() - t0) * 1e3
+        # the first call also allocates its scratch in the pool and creates
+        # the side stream; the figure is the median of the three calls after it
+        prep = []
+        for _ in range(4):
+            t0 = time.perf_counter()
+            bo.nehvi_prepare(mn, ZX, wl.ref, stream=stream)
+            prep.append((time.perf_counter() - t0) * 1e3)
+        prep_first_ms, prep_ms = prep[0], float(np.median(prep[1:]))
         bo.score_nehvi(mn, cand, Z, ehvi=ehvi, stream=stream)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
@@ -438,7 +443,7 @@ def main(argv=None):
         rec["noisy_acquisition"] = {
             "kernels": "k_posterior (noise-free factor) per objective, k_nehvi_means, "
                        "k_nehvi_ehvi per 262144-point chunk",
-            "prepare_ms": prep_ms, "score_ms": nz_ms,
+            "prepare_ms": prep_ms, "prepare_first_call_ms": prep_first_ms, "score_ms": nz_ms,
             "batches_per_s": wl.M / (nz_ms / 1e3),
             "mean_front_size": float(np.mean(fronts)),
             "means_f16_mfma_flops_per_call": 2.0 * 3 * wl.M * wl.q * rows * sp * wl.m,
