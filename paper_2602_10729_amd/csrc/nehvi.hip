@@ -16,8 +16,9 @@
 // mu* the ordinary posterior mean.
 //
 // bo_nehvi_prepare (fp64, once per set of in-sample base samples) builds
-// f_X^s, every sample's front and staircase boxes (k_sample_front), G and
-// its fp16 hi/lo fragments (k_pack_g), and the packed inverse factor of K_XX.
+// f_X^s, every sample's front and staircase boxes (k_sample_front for two
+// objectives; k_insample_values and k_sample_front3 for three), G and its
+// fp16 hi/lo fragments (k_pack_g), and the packed inverse factor of K_XX.
 // Scoring runs per chunk of candidates: the posterior kernel on the
 // noise-free factor (mu*, tau), k_nehvi_means (K* G on the matrix cores, K*
 // evaluated on the fly), then k_nehvi_ehvi (per-sample HVI against that
@@ -25,7 +26,6 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
-
 #include <type_traits>
 
 #include "bo_internal.h"
