@@ -415,6 +415,32 @@ bo_status bo_model_front_indices(bo_model model, int32_t* idx_host, int32_t cap)
 bo_status bo_cholesky_test(const float* A, int64_t n, float* L, void* stream);
 
 /*
+ * bo_draw_fronts3_test — the per-draw fronts and box decompositions that
+ * bo_nehvi_prepare builds for three objectives, exposed so their rules can be
+ * tested on chosen values (ties, duplicates, thresholds).
+ * Paper: "Constrained qNEHVI" paragraph (each sample's improvement is
+ * measured against the Pareto front of that sample's in-sample values).
+ * F      device [S][n][3] fp64 values (draw, point, objective)
+ * ref    host [3]; feas_lower host [3] or NULL (rows failing any threshold
+ *        take no part)
+ * front  device [S][n] int32 out: per draw, its first P entries are the
+ *        front's indices (non-dominated among the points strictly above ref,
+ *        exact duplicates keep the lowest index), objective 0 ascending then
+ *        index; the rest is unspecified
+ * boxes  device [S][3n + 1][6] fp32 out: per draw, its first counts[s] boxes
+ *        (lo0, lo1, lo2, w0, w1, w2), disjoint, covering the part of the
+ *        region above ref that the front does not dominate (inf widths for
+ *        unbounded sides)
+ * counts device [2S] int32 out: the number of boxes per draw, then P
+ * 1 <= n <= BO_MAX_N, S >= 1. Synchronous.
+ * Errors: INVALID_ARGUMENT, CAPACITY, NONFINITE_INPUT (ref, a NaN threshold,
+ * or a non-finite value of F), OUT_OF_MEMORY, DEVICE.
+ */
+bo_status bo_draw_fronts3_test(const double* F, int64_t n, int32_t S, const float* ref,
+                               const float* feas_lower, int32_t* front, float* boxes,
+                               int32_t* counts, void* stream);
+
+/*
  * Host-only geometry (no device work; callable without a GPU).
  *
  * bo_pareto_front: non-dominated rows of Y (maximise; duplicates keep the

@@ -22,7 +22,7 @@ from typing import Optional
 import numpy as np
 
 __all__ = ["BoError", "Model", "lib", "lib_path", "fit", "fit_composite", "mll", "score", "score_noalloc", "nehvi_prepare", "score_nehvi", "argmax",
-           "cholesky_test", "profile_enable", "profile_read", "measure_peak", "pareto_front", "box_decomposition", "STATUS",
+           "cholesky_test", "draw_fronts3_test", "profile_enable", "profile_read", "measure_peak", "pareto_front", "box_decomposition", "STATUS",
            "MAX_N", "MAX_D", "MAX_S", "MAX_BOXES"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -89,6 +89,8 @@ def lib() -> ctypes.CDLL:
     L.bo_model_front_indices.restype = ctypes.c_int
     L.bo_cholesky_test.argtypes = [vp, i64, vp, vp]
     L.bo_cholesky_test.restype = ctypes.c_int
+    L.bo_draw_fronts3_test.argtypes = [vp, i64, i32, vp, vp, vp, vp, vp, vp]
+    L.bo_draw_fronts3_test.restype = ctypes.c_int
     L.bo_pareto_front.argtypes = [vp, i64, i32, vp, vp, i32, ctypes.POINTER(i32)]
     L.bo_pareto_front.restype = ctypes.c_int
     L.bo_box_decomposition.argtypes = [vp, i32, i32, vp, vp, vp, i32, ctypes.POINTER(i32)]
@@ -371,6 +373,31 @@ def cholesky_test(A, L=None, stream=None):
                                 _stream(stream))
     _check(st, "bo_cholesky_test")
     return L
+
+
+def draw_fronts3_test(F, ref, lower=None, stream=None):
+    """bo_draw_fronts3_test: per-draw fronts and boxes of three-objective
+    values F (fp64 GPU tensor [S][n][3]). Returns (fronts, boxes): per draw the
+    front's indices (objective 0 ascending) and its boxes [nb][6]
+    (lo0, lo1, lo2, w0, w1, w2)."""
+    import torch
+    S, n, m = F.shape
+    if m != 3:
+        raise ValueError("F must be [S][n][3]")
+    front = torch.empty((S, n), dtype=torch.int32, device=F.device)
+    boxes = torch.empty((S, 3 * n + 1, 6), dtype=torch.float32, device=F.device)
+    counts = torch.empty(2 * S, dtype=torch.int32, device=F.device)
+    r = np.ascontiguousarray(np.asarray(ref, dtype=np.float32))
+    lo = None if lower is None else np.ascontiguousarray(np.asarray(lower, dtype=np.float32))
+    st = lib().bo_draw_fronts3_test(
+        _dev(F, "F", torch.float64), n, S, r.ctypes.data_as(ctypes.c_void_p),
+        None if lo is None else lo.ctypes.data_as(ctypes.c_void_p),
+        _dev(front, "front"), _dev(boxes, "boxes"), _dev(counts, "counts"), _stream(stream))
+    _check(st, "bo_draw_fronts3_test")
+    c = counts.cpu().numpy()
+    fr, bx = front.cpu().numpy(), boxes.cpu().numpy()
+    return ([fr[s, :c[S + s]].copy() for s in range(S)],
+            [bx[s, :c[s]].copy() for s in range(S)])
 
 
 def pareto_front(Y, ref: Optional[np.ndarray] = None) -> np.ndarray:

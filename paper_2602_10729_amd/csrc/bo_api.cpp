@@ -1603,6 +1603,45 @@ bo_status bo_measure_peak(int32_t what, int64_t iters, double* rate, void* strea
   return BO_OK;
 }
 
+bo_status bo_draw_fronts3_test(const double* F, int64_t n, int32_t S, const float* ref,
+                               const float* feas_lower, int32_t* front, float* boxes,
+                               int32_t* counts, void* stream) {
+  const std::string W("bo_draw_fronts3_test");
+  if (n < 1 || S < 1) return fail(BO_ERR_INVALID_ARGUMENT, W + ": n < 1 or S < 1");
+  if (n > BO_MAX_N) return fail(BO_ERR_CAPACITY, W + ": n beyond limit");
+  if (!ref) return fail(BO_ERR_INVALID_ARGUMENT, W + ": ref is NULL");
+  if (!all_finite(ref, 3)) return fail(BO_ERR_NONFINITE_INPUT, W + ": ref not finite");
+  if (feas_lower)
+    for (int k = 0; k < 3; ++k)
+      if (std::isnan(feas_lower[k])) return fail(BO_ERR_NONFINITE_INPUT, W + ": threshold is NaN");
+  if (nehvi_front3_lds_bytes(n) > kLdsLimit) return fail(BO_ERR_CAPACITY, W + ": n beyond LDS");
+  bo_status s;
+  if ((s = check_dev(F, sizeof(double) * (size_t)S * n * 3, "F")) != BO_OK) return s;
+  if ((s = check_dev(front, sizeof(int32_t) * (size_t)S * n, "front")) != BO_OK) return s;
+  if ((s = check_dev(boxes, sizeof(float) * (size_t)S * (3 * n + 1) * 6, "boxes")) != BO_OK) return s;
+  if ((s = check_dev(counts, sizeof(int32_t) * 2 * (size_t)S, "counts")) != BO_OK) return s;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  int* bad = nullptr;
+  if ((s = palloc(&bad, 1, st, "flag")) != BO_OK) return s;
+  hipError_t e = hipMemsetAsync(bad, 0, sizeof(int), st);
+  NehviFront3Args fa;
+  fa.F = F; fa.n = n; fa.S = S;
+  for (int k = 0; k < 3; ++k) {
+    fa.ref[k] = ref[k];
+    fa.low[k] = feas_lower ? feas_lower[k] : -INFINITY;
+  }
+  fa.cons = feas_lower != nullptr;
+  fa.boxes = boxes; fa.counts = counts; fa.front = front; fa.bad = bad;
+  if (e == hipSuccess) e = launch_sample_fronts3(fa, st);
+  int flag = 0;
+  if (e == hipSuccess) e = hipMemcpyAsync(&flag, bad, sizeof(int), hipMemcpyDeviceToHost, st);
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  pfree(bad, st);
+  if (e != hipSuccess) return hip_fail(e, "bo_draw_fronts3_test: launch");
+  if (flag) return fail(BO_ERR_NONFINITE_INPUT, W + ": non-finite value");
+  return BO_OK;
+}
+
 bo_status bo_cholesky_test(const float* A, int64_t n, float* L, void* stream) {
   if (n < 1) return fail(BO_ERR_INVALID_ARGUMENT, "bo_cholesky_test: n < 1");
   if (n > BO_MAX_N) return fail(BO_ERR_CAPACITY, "bo_cholesky_test: n beyond limit");

@@ -102,6 +102,13 @@ def test_score_and_argmax_validation(bo):
     assert L.bo_argmax(fake, 1 << 31, fake, fake, None) == 1
     assert L.bo_cholesky_test(fake, 0, fake, None) == 1
     assert L.bo_cholesky_test(fake, 4096, fake, None) == 3
+    r3 = np.zeros(3, dtype=np.float32)
+    assert L.bo_draw_fronts3_test(fake, 0, 4, p(r3), None, fake, fake, fake, None) == 1
+    assert L.bo_draw_fronts3_test(fake, 8, 0, p(r3), None, fake, fake, fake, None) == 1
+    assert L.bo_draw_fronts3_test(fake, 4096, 4, p(r3), None, fake, fake, fake, None) == 3
+    assert L.bo_draw_fronts3_test(fake, 8, 4, None, None, fake, fake, fake, None) == 1
+    bad = np.array([0, np.nan, 0], dtype=np.float32)
+    assert L.bo_draw_fronts3_test(fake, 8, 4, p(bad), None, fake, fake, fake, None) == 6
     assert L.bo_model_front_size(None) == -1
 
 
