@@ -442,7 +442,7 @@ def main(argv=None):
         rows = (wl.n + 31) // 32 * 32
         rec["noisy_acquisition"] = {
             "kernels": "k_posterior (noise-free factor) per objective, k_nehvi_means, "
-                       "k_nehvi_ehvi per 262144-point chunk",
+                       "k_nehvi_ehvi per 1048576-point chunk",
             "prepare_ms": prep_ms, "prepare_first_call_ms": prep_first_ms, "score_ms": nz_ms,
             "batches_per_s": wl.M / (nz_ms / 1e3),
             "mean_front_size": float(np.mean(fronts)),

@@ -362,7 +362,7 @@ bo_status bo_score_noalloc(bo_model model, const float* cand, int64_t M, int32_t
  * bo_score_nehvi(model, cand, M, q, base_samples, S, ehvi, stream):
  *   cand device [M][q][d] (q in {1, 2, 4}); base_samples device [S][q][m]
  *   (z*, shared by all batches); S must equal the prepared S; ehvi device [M]
- *   out. Asynchronous; batches are processed in chunks of 262144 points,
+ *   out. Asynchronous; batches are processed in chunks of 1048576 points,
  *   whose per-draw conditional means (m x S x chunk floats) live in a
  *   model-owned workspace that grows on first use.
  *   Errors: INVALID_ARGUMENT (not prepared, S mismatch, bad q, pointers),

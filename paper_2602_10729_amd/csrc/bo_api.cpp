@@ -1127,9 +1127,9 @@ bo_status bo_score_noalloc(bo_model model, const float* cand, int64_t M_, int32_
 namespace {
 
 // Candidates per scoring chunk of the noisy acquisition: the conditional
-// means of a chunk, m x S x chunk floats (1 GiB at S = 512), stay in HBM
+// means of a chunk, m x S x chunk floats (4 GiB at m = 2, S = 512), stay in HBM
 // between the matrix-core kernel and the HVI kernel.
-constexpr int64_t kNehviChunk = 262144;
+constexpr int64_t kNehviChunk = 1048576;
 constexpr int kNehviMaxS = 512;
 
 struct NoisyScratch {
