@@ -111,6 +111,12 @@ struct DeviceState {
   // inside one call, joined back by the two events
   hipStream_t side = nullptr;
   hipEvent_t side_evt[2] = {nullptr, nullptr};
+  // under fit_mu: the fp64 scratch of bo_fit and bo_mll, kept and grown on
+  // demand (both synchronise their stream before releasing fit_mu, so none
+  // of it is in use between calls): A, W [mat], hyperparameters [nhyp],
+  // vector [vec], then 64 bytes of flag (int) and statistics (at byte 16)
+  double* fw = nullptr;
+  size_t fw_mat = 0, fw_hyp = 0, fw_vec = 0;
 };
 
 // The side stream and its events of device state DS (created once).
@@ -193,8 +199,11 @@ struct DeviceGuard {
 
 // Temporary device buffers of the fit, returned to the pool on every exit
 // path (ordered after the fit's work on its stream).
+// fp64 fit scratch: the device's kept workspace (fit_work), or buffers of
+// its own (own = true, freed on destruction).
 struct FitScratch {
   hipStream_t st = nullptr;
+  bool own = false;
   double* A = nullptr;
   double* W = nullptr;
   double* hyp = nullptr;
@@ -202,6 +211,7 @@ struct FitScratch {
   int* flag = nullptr;
   unsigned long long* stats = nullptr;   // [2m]: max K_ii, then max |L^{-1}| (double bits)
   ~FitScratch() {
+    if (!own) return;
     pfree(A, st); pfree(W, st); pfree(hyp, st); pfree(tmp, st); pfree(flag, st);
     pfree(stats, st);
   }
@@ -227,25 +237,57 @@ void release_noisy(Model* M) {
 
 void release_buffers(Model* M) {
   release_noisy(M);
-  if (M->Xs || M->invls || M->alpha || M->Lp || M->ws || M->d_boxes || M->wts ||
-      M->pref || M->Xd || M->xf || M->x2 || M->ctr || M->Lp64)
-    (void)hipDeviceSynchronize();
-  pfree(M->Lp64, nullptr);
-  pfree(M->alpha64, nullptr);
-  pfree(M->ils64, nullptr);
-  pfree(M->xf, nullptr);
-  pfree(M->x2, nullptr);
-  pfree(M->ctr, nullptr);
-  pfree(M->Xd, nullptr);
-  pfree(M->Xs, nullptr);
-  pfree(M->invls, nullptr);
-  pfree(M->alpha, nullptr);
-  pfree(M->Lp, nullptr);
+  if (M->arena || M->ws || M->d_boxes) (void)hipDeviceSynchronize();
+  pfree(M->arena, nullptr);
+  M->Lp64 = nullptr; M->alpha64 = nullptr; M->ils64 = nullptr;
+  M->xf = nullptr; M->x2 = nullptr; M->ctr = nullptr; M->Xd = nullptr;
+  M->Xs = nullptr; M->invls = nullptr; M->alpha = nullptr; M->Lp = nullptr;
+  M->wts = nullptr; M->pref = nullptr;
   pfree(M->ws, nullptr);
   pfree(M->d_boxes, nullptr);
-  pfree(M->wts, nullptr);
-  pfree(M->pref, nullptr);
 }
+
+// The device's kept fit scratch, grown to at least the given sizes (the
+// caller holds DS->fit_mu). Growing waits for the device, then replaces the
+// buffer.
+bo_status fit_work(DeviceState* DS, size_t mat, size_t nhyp, size_t vec, FitScratch* fs) {
+  if (!DS->fw || mat > DS->fw_mat || nhyp > DS->fw_hyp || vec > DS->fw_vec) {
+    const size_t m2 = std::max(mat, DS->fw_mat), h2 = std::max(nhyp, DS->fw_hyp),
+                 v2 = std::max(vec, DS->fw_vec);
+    if (DS->fw) {
+      (void)hipDeviceSynchronize();
+      (void)hipFree(DS->fw);
+      DS->fw = nullptr;
+      DS->fw_mat = DS->fw_hyp = DS->fw_vec = 0;
+    }
+    void* q = nullptr;
+    hipError_t e = hipMalloc(&q, sizeof(double) * (2 * m2 + h2 + v2) + 64);
+    if (e != hipSuccess) {
+      (void)hipGetLastError();
+      return fail(BO_ERR_OUT_OF_MEMORY, "device allocation failed for the fit scratch");
+    }
+    DS->fw = static_cast<double*>(q);
+    DS->fw_mat = m2; DS->fw_hyp = h2; DS->fw_vec = v2;
+  }
+  fs->own = false;
+  fs->A = DS->fw;
+  fs->W = fs->A + DS->fw_mat;
+  fs->hyp = fs->W + DS->fw_mat;
+  fs->tmp = fs->hyp + DS->fw_hyp;
+  fs->flag = reinterpret_cast<int*>(fs->tmp + DS->fw_vec);
+  fs->stats = reinterpret_cast<unsigned long long*>(fs->tmp + DS->fw_vec + 2);
+  return BO_OK;
+}
+
+// Byte offsets of a model's buffers inside its arena (256-byte aligned).
+struct ArenaLayout {
+  size_t total = 0;
+  size_t add(size_t bytes) {
+    const size_t o = total;
+    total += (bytes + 255) / 256 * 256;
+    return o;
+  }
+};
 
 // Phase timing (bo_profile_enable / bo_profile_read).
 struct Profile {
@@ -663,34 +705,50 @@ bo_status fit_impl(const char* who, const float* X, const float* Y, int64_t n, i
   const int nf = static_cast<int>((n + kFitBlk - 1) / kFitBlk) * kFitBlk;
   const int dc = d - dr;
   M->lp_per_obj = packed_factor_floats(M->nb);
-  FitScratch fs;
-  fs.st = st;
   // fp64 hyperparameters: [1/ls m*d][os m][noise m] (+ [s_dep m][s_int m][pref m*dc])
   const size_t nhyp = (size_t)m * d + 2 * m + (comp ? 2 * m + (size_t)m * dc : 0);
-  if ((s = palloc(&fs.A, (size_t)m * nf * nf, st, "fit matrix")) != BO_OK) return bail(s);
-  if ((s = palloc(&fs.W, (size_t)m * nf * nf, st, "fit inverse")) != BO_OK) return bail(s);
-  if ((s = palloc(&fs.hyp, nhyp, st, "hyperparameters")) != BO_OK) return bail(s);
-  if ((s = palloc(&fs.tmp, (size_t)m * nf, st, "fit vector")) != BO_OK) return bail(s);
-  if ((s = palloc(&fs.flag, 1, st, "flag")) != BO_OK) return bail(s);
-  if ((s = palloc(&fs.stats, 2 * (size_t)m, st, "fit statistics")) != BO_OK) return bail(s);
-  if ((s = palloc(&M->Xs, (size_t)m * M->n_pad * M->dx, st, "scaled X")) != BO_OK) return bail(s);
-  if ((s = palloc(&M->invls, (size_t)m * M->dx, st, "inverse lengthscales")) != BO_OK) return bail(s);
-  if ((s = palloc(&M->alpha, (size_t)m * M->n_pad, st, "alpha")) != BO_OK) return bail(s);
-  if ((s = palloc(&M->Lp, (size_t)m * M->lp_per_obj, st, "packed inverse")) != BO_OK) return bail(s);
-  if ((s = palloc(&M->Xd, (size_t)n * d, st, "training inputs")) != BO_OK) return bail(s);
-  if ((s = palloc(&M->xf, (size_t)m * M->nb * dist_frags(M->dx) * 512, st, "distance fragments")) != BO_OK) return bail(s);
-  if ((s = palloc(&M->x2, (size_t)m * 2 * M->n_pad, st, "row norms")) != BO_OK) return bail(s);
-  if ((s = palloc(&M->ctr, (size_t)m * M->dx, st, "coordinate centre")) != BO_OK) return bail(s);
-  M->n_fit = nf;
+  // every model buffer in one allocation
+  ArenaLayout lay;
+  const size_t o_xs = lay.add(sizeof(float) * m * M->n_pad * M->dx);
+  const size_t o_il = lay.add(sizeof(float) * m * M->dx);
+  const size_t o_al = lay.add(sizeof(float) * m * M->n_pad);
+  const size_t o_lp = lay.add(sizeof(float) * m * M->lp_per_obj);
+  const size_t o_xd = lay.add(sizeof(float) * n * d);
+  const size_t o_xf = lay.add(sizeof(uint16_t) * m * M->nb * dist_frags(M->dx) * 512);
+  const size_t o_x2 = lay.add(sizeof(float) * m * 2 * M->n_pad);
+  const size_t o_ct = lay.add(sizeof(float) * m * M->dx);
+  size_t o_l64 = 0, o_a64 = 0, o_i64 = 0, o_wt = 0, o_pf = 0;
   if (f64) {
-    if ((s = palloc(&M->Lp64, (size_t)m * posterior_f64_blocks(M->nb) * 512, st, "fp64 fragments")) != BO_OK) return bail(s);
-    if ((s = palloc(&M->alpha64, (size_t)m * nf, st, "fp64 alpha")) != BO_OK) return bail(s);
-    if ((s = palloc(&M->ils64, (size_t)m * d, st, "fp64 inverse lengthscales")) != BO_OK) return bail(s);
+    o_l64 = lay.add(sizeof(double) * m * posterior_f64_blocks(M->nb) * 512);
+    o_a64 = lay.add(sizeof(double) * m * nf);
+    o_i64 = lay.add(sizeof(double) * m * d);
   }
   if (comp) {
-    if ((s = palloc(&M->wts, (size_t)m * M->n_pad, st, "preference weights")) != BO_OK) return bail(s);
-    if ((s = palloc(&M->pref, (size_t)m * dc, st, "preference slopes")) != BO_OK) return bail(s);
+    o_wt = lay.add(sizeof(float) * m * M->n_pad);
+    o_pf = lay.add(sizeof(float) * m * dc);
   }
+  if ((s = palloc(&M->arena, lay.total, st, "model buffers")) != BO_OK) return bail(s);
+  {
+    unsigned char* b = M->arena;
+    M->Xs = reinterpret_cast<float*>(b + o_xs);
+    M->invls = reinterpret_cast<float*>(b + o_il);
+    M->alpha = reinterpret_cast<float*>(b + o_al);
+    M->Lp = reinterpret_cast<float*>(b + o_lp);
+    M->Xd = reinterpret_cast<float*>(b + o_xd);
+    M->xf = reinterpret_cast<uint16_t*>(b + o_xf);
+    M->x2 = reinterpret_cast<float*>(b + o_x2);
+    M->ctr = reinterpret_cast<float*>(b + o_ct);
+    if (f64) {
+      M->Lp64 = reinterpret_cast<double*>(b + o_l64);
+      M->alpha64 = reinterpret_cast<double*>(b + o_a64);
+      M->ils64 = reinterpret_cast<double*>(b + o_i64);
+    }
+    if (comp) {
+      M->wts = reinterpret_cast<float*>(b + o_wt);
+      M->pref = reinterpret_cast<float*>(b + o_pf);
+    }
+  }
+  M->n_fit = nf;
 
   std::vector<double> hyp(nhyp);
   for (int i = 0; i < m * d; ++i) hyp[i] = 1.0 / static_cast<double>(lengthscale[i]);
@@ -704,24 +762,17 @@ bo_status fit_impl(const char* who, const float* X, const float* Y, int64_t n, i
   }
   if (comp)
     for (size_t i = 0; i < (size_t)m * dc; ++i) hyp[(size_t)m * d + 4 * m + i] = comp->pref[i];
-  // per-slot inverse lengthscales (zero for padding slots)
-  std::vector<float> invls((size_t)m * M->dx, 0.f);
-  for (int k = 0; k < m; ++k)
-    for (int t = 0; t < M->dx; ++t) {
-      const int c = slot_dim(t, d, dr, dr4);
-      if (c >= 0) invls[(size_t)k * M->dx + t] = 1.0f / lengthscale[k * d + c];
-    }
 
-  // pinned staging: [hyperparameters (fp64)][1/lengthscale (fp32)][pref (fp32)][flag][Y]
+  // pinned staging: [hyperparameters (fp64)][flag, statistics (64 bytes)][Y]
   DeviceState* DS = device_state(M->device);
   if (!DS) return bail(fail(BO_ERR_DEVICE, W + ": device index out of range"));
   std::lock_guard<std::mutex> stage_lock(DS->fit_mu);
-  const size_t off_inv = sizeof(double) * hyp.size();
-  const size_t off_pref = off_inv + sizeof(float) * invls.size();
-  const size_t npref = comp ? (size_t)m * dc : 0;
-  const size_t off_flag = (off_pref + sizeof(float) * npref + 15) / 16 * 16;
+  FitScratch fs;
+  fs.st = st;
+  if ((s = fit_work(DS, (size_t)m * nf * nf, nhyp, (size_t)m * nf, &fs)) != BO_OK) return bail(s);
+  const size_t off_flag = (sizeof(double) * hyp.size() + 15) / 16 * 16;
   const size_t off_stats = off_flag + 16;
-  const size_t off_y = off_stats + 16 * 3;
+  const size_t off_y = off_flag + 64;
   const size_t need = off_y + sizeof(float) * n * m;
   hipError_t e = hipSuccess;
   if (need > DS->fit_stage_bytes) {
@@ -734,20 +785,11 @@ bo_status fit_impl(const char* who, const float* X, const float* Y, int64_t n, i
     DS->fit_stage_bytes = cap;
   }
   unsigned char* stage = DS->fit_stage;
-  std::memcpy(stage, hyp.data(), off_inv);
-  std::memcpy(stage + off_inv, invls.data(), sizeof(float) * invls.size());
-  if (comp) std::memcpy(stage + off_pref, comp->pref, sizeof(float) * npref);
-  e = hipMemcpyAsync(fs.hyp, stage, off_inv, hipMemcpyHostToDevice, st);
-  if (e == hipSuccess)
-    e = hipMemcpyAsync(M->invls, stage + off_inv, sizeof(float) * invls.size(),
-                       hipMemcpyHostToDevice, st);
-  if (e == hipSuccess && comp)
-    e = hipMemcpyAsync(M->pref, stage + off_pref, sizeof(float) * npref, hipMemcpyHostToDevice,
-                       st);
-  if (e == hipSuccess) e = hipMemsetAsync(fs.flag, 0, sizeof(int), st);
-  if (e == hipSuccess) e = hipMemsetAsync(fs.stats, 0, sizeof(unsigned long long) * 2 * m, st);
-  if (e == hipSuccess)
-    e = hipMemcpyAsync(M->Xd, X, sizeof(float) * n * d, hipMemcpyDeviceToDevice, st);
+  std::memcpy(stage, hyp.data(), sizeof(double) * hyp.size());
+  // the fp32 inverse lengthscales and preference slopes, and the copy of X,
+  // are written on the device from these (k_scale_x)
+  e = hipMemcpyAsync(fs.hyp, stage, sizeof(double) * hyp.size(), hipMemcpyHostToDevice, st);
+  if (e == hipSuccess) e = hipMemsetAsync(fs.flag, 0, 64, st);   // flag and statistics
   if (e != hipSuccess) return bail(hip_fail(e, "bo_fit: upload"));
 
   GramParams gp;
@@ -764,21 +806,15 @@ bo_status fit_impl(const char* who, const float* X, const float* Y, int64_t n, i
   if (comp && (s = after_launch(launch_weights(X, n, d, m, M->n_pad, gp, M->wts, st), st, "weights")) != BO_OK) return bail(s);
   if ((s = after_launch(launch_cholesky(fs.A, fs.W, nf, m, fs.flag, st), st, "cholesky")) != BO_OK) return bail(s);
   if ((s = after_launch(launch_alpha(fs.W, Y, n, m, nf, M->n_pad, fs.tmp, M->alpha, st, M->alpha64), st, "alpha")) != BO_OK) return bail(s);
-  if (f64) {
-    if ((s = after_launch(launch_pack_f64(fs.W, n, m, nf, M->nb, M->Lp64, st), st, "pack fp64")) != BO_OK) return bail(s);
-    // 1 / lengthscale in fp64: the first m d hyperparameters
-    e = hipMemcpyAsync(M->ils64, fs.hyp, sizeof(double) * m * d, hipMemcpyDeviceToDevice, st);
-    if (e != hipSuccess) return bail(hip_fail(e, "bo_fit: fp64 lengthscales"));
-  }
-  if ((s = after_launch(launch_pack(fs.W, n, m, nf, M->nb, M->Lp, fs.stats + m, fs.flag, X, d, M->dx, dr, dr4, M->invls, M->Xs, st), st, "pack")) != BO_OK) return bail(s);
+  if (f64 && (s = after_launch(launch_pack_f64(fs.W, n, m, nf, M->nb, M->Lp64, st), st, "pack fp64")) != BO_OK) return bail(s);
+  if ((s = after_launch(launch_pack(fs.W, n, m, nf, M->nb, M->Lp, fs.stats + m, fs.flag, X, d,
+                                    M->dx, dr, dr4, gp.ils, M->invls, comp ? gp.pref : nullptr,
+                                    M->pref, M->Xd, M->ils64, M->Xs, st), st, "pack")) != BO_OK) return bail(s);
   if ((s = after_launch(launch_pack_x(M->Xs, n, m, M->nb, M->dx, dr4, M->ctr, M->xf, M->x2, st), st, "pack X")) != BO_OK) return bail(s);
 
   // one synchronisation: the positive-definiteness flag and Y (for the front
   // and its finiteness check) come back together
-  e = hipMemcpyAsync(stage + off_flag, fs.flag, sizeof(int), hipMemcpyDeviceToHost, st);
-  if (e == hipSuccess)
-    e = hipMemcpyAsync(stage + off_stats, fs.stats, sizeof(unsigned long long) * 2 * m,
-                       hipMemcpyDeviceToHost, st);
+  e = hipMemcpyAsync(stage + off_flag, fs.flag, 64, hipMemcpyDeviceToHost, st);
   if (e == hipSuccess)
     e = hipMemcpyAsync(stage + off_y, Y, sizeof(float) * n * m, hipMemcpyDeviceToHost, st);
   if (e == hipSuccess) e = hipStreamSynchronize(st);
@@ -849,8 +885,6 @@ bo_status mll_impl(const float* X, const float* Y, int64_t n, int32_t d, int32_t
   const int nf = static_cast<int>((n + kFitBlk - 1) / kFitBlk) * kFitBlk;
   const int n_pad = static_cast<int>((n + kBlk - 1) / kBlk) * kBlk;
   const int64_t tiles = mll_tiles(nf);
-  FitScratch fs;
-  fs.st = st;
   struct Extra {
     hipStream_t st = nullptr;
     float* alpha = nullptr;
@@ -861,11 +895,6 @@ bo_status mll_impl(const float* X, const float* Y, int64_t n, int32_t d, int32_t
   } ex;
   ex.st = st;
   const size_t nhyp = (size_t)m * d + 2 * m;
-  if ((s = palloc(&fs.A, (size_t)m * nf * nf, st, "fit matrix")) != BO_OK) return s;
-  if ((s = palloc(&fs.W, (size_t)m * nf * nf, st, "fit inverse")) != BO_OK) return s;
-  if ((s = palloc(&fs.hyp, nhyp, st, "hyperparameters")) != BO_OK) return s;
-  if ((s = palloc(&fs.tmp, (size_t)m * nf, st, "fit vector")) != BO_OK) return s;
-  if ((s = palloc(&fs.flag, 1, st, "flag")) != BO_OK) return s;
   if ((s = palloc(&ex.alpha, (size_t)m * n_pad, st, "alpha")) != BO_OK) return s;
   if ((s = palloc(&ex.alpha64, (size_t)m * nf, st, "alpha (fp64)")) != BO_OK) return s;
   if ((s = palloc(&ex.partials, (size_t)m * tiles * (d + 2), st, "gradient partials")) != BO_OK) return s;
@@ -881,6 +910,9 @@ bo_status mll_impl(const float* X, const float* Y, int64_t n, int32_t d, int32_t
   DeviceState* DS = device_state(dev);
   if (!DS) return fail(BO_ERR_DEVICE, "bo_mll: device index out of range");
   std::lock_guard<std::mutex> stage_lock(DS->fit_mu);
+  FitScratch fs;
+  fs.st = st;
+  if ((s = fit_work(DS, (size_t)m * nf * nf, nhyp, (size_t)m * nf, &fs)) != BO_OK) return s;
   const size_t off_flag = (sizeof(double) * nhyp + 15) / 16 * 16;
   const size_t off_out = off_flag + 16;
   const size_t need = off_out + sizeof(double) * m * (d + 3);
@@ -1233,6 +1265,9 @@ bo_status nehvi_prepare_impl(bo_model model, const float* ZX, int32_t S, const f
   DeviceState* DS = device_state(M.device);
   if (!DS) return fail(BO_ERR_DEVICE, W_ + ": device index out of range");
   std::lock_guard<std::mutex> stage_lock(DS->fit_mu);
+  FitScratch fs;
+  fs.st = st;
+  if ((s = fit_work(DS, (size_t)m * nf * nf, nhyp, (size_t)m * nf, &fs)) != BO_OK) return s;
   const size_t off_flag = (sizeof(double) * nhyp + 15) / 16 * 16;
   const size_t off_stats = off_flag + 32;
   const size_t off_y = off_stats + 16 * 3;
@@ -1652,6 +1687,7 @@ bo_status bo_cholesky_test(const float* A, int64_t n, float* L, void* stream) {
   const int nf = static_cast<int>((n + kFitBlk - 1) / kFitBlk) * kFitBlk;
   FitScratch fs;
   fs.st = st;
+  fs.own = true;
   if ((s = palloc(&fs.A, (size_t)nf * nf, st, "matrix")) != BO_OK) return s;
   if ((s = palloc(&fs.W, (size_t)nf * nf, st, "inverse")) != BO_OK) return s;
   if ((s = palloc(&fs.flag, 1, st, "flag")) != BO_OK) return s;

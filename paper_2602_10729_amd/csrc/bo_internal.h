@@ -56,6 +56,9 @@ struct Model {
   std::vector<float> Yh;         // host copy of Y [n][m]
   std::vector<int32_t> nd;       // non-dominated rows (no reference filter)
 
+  // one device allocation holds every buffer the fit writes (Xs .. ils64,
+  // wts, pref below are views into it)
+  unsigned char* arena = nullptr;
   float* Xs = nullptr;           // [m][n_pad][dx] X / lengthscale (fp32)
   float* invls = nullptr;        // [m][dx] 1 / lengthscale (fp32, 0-padded)
   float* alpha = nullptr;        // [m][n_pad]
@@ -138,7 +141,8 @@ hipError_t launch_gram(const float* X, int64_t n, int d, int m, int n_fit,
 hipError_t launch_weights(const float* X, int64_t n, int d, int m, int n_pad,
                           const GramParams& g, float* wts, hipStream_t st);
 // Blocked right-looking Cholesky of m matrices [m][nf][nf] (lower, in place);
-// also leaves W = L^{-1} (lower, [m][nf][nf]).
+// also leaves W = L^{-1} in W's lower 64-blocks ([m][nf][nf]; W needs no
+// initial contents, its blocks above the diagonal are left as they were).
 // *flag is set non-zero on a non-positive or non-finite pivot.
 hipError_t launch_cholesky(double* A, double* W, int nf, int m, int* flag,
                            hipStream_t st);
@@ -163,11 +167,16 @@ hipError_t launch_mll(const float* X, int64_t n, int d, int m, int nf, const Gra
 // by the nb inverse scales (packed_factor_floats(nb) floats per objective;
 // wmax [m] = largest |W| per objective as a non-negative double's bit
 // pattern, zeroed by the caller; *flag set on a non-finite entry), and write
-// the lengthscale-scaled X in the slot layout (invls is per slot, [m][dx]).
+// the lengthscale-scaled X in the slot layout from the fp64 inverse
+// lengthscales ils [m][d], with the fp32 per-slot values invls [m][dx], the
+// copy Xd [n][d] of X, (composite, pref non-NULL) the fp32 preference slopes
+// pref [m][d - dr] from their fp64 copies pref_d, and (ils64 non-NULL) a copy
+// of ils.
 hipError_t launch_pack(const double* W, int64_t n, int m, int nf, int nb,
                        float* Lp, unsigned long long* wmax, int* flag,
                        const float* X, int d, int dx, int dr, int dr4,
-                       const float* invls, float* Xs, hipStream_t st);
+                       const double* ils, float* invls, const double* pref_d,
+                       float* pref, float* Xd, double* ils64, float* Xs, hipStream_t st);
 
 // Squared distances in the posterior kernel come from the expansion
 // |c|^2 + |x|^2 - 2 c.x of centred scaled coordinates, with c.x on the fp16

@@ -311,9 +311,14 @@ __device__ inline void gemm_nt_64(const double (*P)[LDP], const double (*Q)[LDP]
   }
 }
 
-// Panel of step kb, with D = L_kk^{-1} (held in W's diagonal block kb):
+// Panel of step kb, with D = L_kk^{-1} (held in W's diagonal block kb), in
+// quarters (u = blockIdx.x % 4) so that its T + kb tiles fill four times as
+// many workgroups:
 // tiles t < T: A[kb+1+t][kb] <- A[kb+1+t][kb] D^T (rows below the diagonal);
-// tiles T <= t < T + kb: W[kb][jb] <- D R[kb][jb] for jb = t - T (< kb).
+//   quarter u takes rows 16u .. 16u+15 of the tile, the only rows it reads;
+// tiles T <= t < T + kb: W[kb][jb] <- D R[kb][jb] for jb = t - T (< kb);
+//   quarter u takes columns 16u .. 16u+15 of R, the only columns it reads.
+// Each output is the same ascending sum over s as a whole-tile product.
 __global__ __launch_bounds__(256) void k_panel(double* __restrict__ A, double* __restrict__ W,
                                                int nf, int kb) {
   __shared__ double p[B][LDP];
@@ -321,35 +326,67 @@ __global__ __launch_bounds__(256) void k_panel(double* __restrict__ A, double* _
   const int k = blockIdx.y;
   const int nbk = nf / B;
   const int T = nbk - kb - 1;
-  const int t = blockIdx.x;
+  const int t = blockIdx.x >> 2, u = blockIdx.x & 3;
   const int tid = threadIdx.x, tx = tid % 16, ty = tid / 16;
   double* Ak = A + (int64_t)k * nf * nf;
   double* Wk = W + (int64_t)k * nf * nf;
   const int o = kb * B;
   const double* D = Wk + (int64_t)o * nf + o;
-  double* dst;
+  double v0[4], v1[16];
   if (t < T) {
-    const int ib = kb + 1 + t;
-    dst = Ak + (int64_t)ib * B * nf + o;
-    // P = A[ib][kb]; Q[c][s] = D[c][s]  ->  P D^T
-    load_blocks<false, false>(p, dst, q, D, nf);
+    double* dst = Ak + (int64_t)(kb + 1 + t) * B * nf + o + (int64_t)16 * u * nf;
+    // p[i][s] = tile row 16u + i (i < 16), q[c][s] = D[c][s]
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int g = tid + 256 * e;
+      v0[e] = dst[(int64_t)(g >> 6) * nf + (g & 63)];
+    }
+    get_tile(v1, D, nf);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int g = tid + 256 * e;
+      p[g >> 6][g & 63] = v0[e];
+    }
+    put_tile<false>(q, v1);
+    __syncthreads();
+    double acc[4] = {};
+    for (int s2 = 0; s2 < B; ++s2) {
+      const double pv = p[ty][s2];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) acc[c] = fma(pv, q[tx * 4 + c][s2], acc[c]);
+    }
+#pragma unroll
+    for (int c = 0; c < 4; ++c) dst[(int64_t)ty * nf + tx * 4 + c] = acc[c];
   } else {
-    const int jb = t - T;
-    dst = Wk + (int64_t)o * nf + jb * B;
-    // P = D; Q = R^T  ->  D R
-    load_blocks<false, true>(p, D, q, dst, nf);
+    double* dst = Wk + (int64_t)o * nf + (t - T) * B + 16 * u;
+    // p = D; q[c][s] = R[s][16u + c] (c < 16)
+    get_tile(v1, D, nf);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int g = tid + 256 * e;
+      v0[e] = dst[(int64_t)(g >> 4) * nf + (g & 15)];
+    }
+    put_tile<false>(p, v1);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int g = tid + 256 * e;
+      q[g & 15][g >> 4] = v0[e];
+    }
+    __syncthreads();
+    double acc[4] = {};
+    for (int s2 = 0; s2 < B; ++s2) {
+      const double qv = q[tx][s2];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) acc[r] = fma(p[ty * 4 + r][s2], qv, acc[r]);
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) dst[(int64_t)(ty * 4 + r) * nf + tx] = acc[r];
   }
-  __syncthreads();
-  double acc[4][4] = {};
-  gemm_nt_64(p, q, acc, ty, tx);
-#pragma unroll
-  for (int r = 0; r < 4; ++r)
-#pragma unroll
-    for (int c = 0; c < 4; ++c) dst[(int64_t)(ty * 4 + r) * nf + tx * 4 + c] = acc[r][c];
 }
 
 // Update of step kb. Tile t < T(T+1)/2: trailing A tile; the rest: R tiles
-// of W. Tile 0 is the next diagonal block, factored and inverted right after
+// of W (the tiles of block column kb are written, not updated: nothing
+// before this step writes them). Tile 0 is the next diagonal block, factored and inverted right after
 // its update (L into A, L^{-1} into W's diagonal block kb+1).
 __global__ __launch_bounds__(256) void k_update(double* __restrict__ A, double* __restrict__ W,
                                                 int nf, int kb, int* __restrict__ flag) {
@@ -366,6 +403,7 @@ __global__ __launch_bounds__(256) void k_update(double* __restrict__ A, double* 
   double* Wk = W + (int64_t)k * nf * nf;
   const int o = kb * B;
   double* dst;
+  bool first_r = false;
   if (t < nsyrk) {
     // (ib, cb) with kb < cb <= ib: tile index t -> row r, column within row
     int r = static_cast<int>((sqrt(8.0 * t + 1.0) - 1.0) * 0.5);
@@ -381,6 +419,7 @@ __global__ __launch_bounds__(256) void k_update(double* __restrict__ A, double* 
     const int u = t - nsyrk;
     const int ib = kb + 1 + u / (kb + 1);
     const int jb = u % (kb + 1);
+    first_r = (jb == kb);
     load_blocks<false, true>(p, Ak + (int64_t)ib * B * nf + o,        // L[ib][kb]
                              q, Wk + (int64_t)o * nf + jb * B, nf);   // q = W[kb][jb]^T
     dst = Wk + (int64_t)ib * B * nf + jb * B;
@@ -388,12 +427,15 @@ __global__ __launch_bounds__(256) void k_update(double* __restrict__ A, double* 
   __syncthreads();
   double acc[4][4] = {};
   gemm_nt_64(p, q, acc, ty, tx);
+  // the first update of an R tile (jb = kb) starts from zero: W is not
+  // cleared beforehand (its blocks above the diagonal are never read)
+  const bool fresh = first_r;
 #pragma unroll
   for (int rr = 0; rr < 4; ++rr)
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
       double* d = dst + (int64_t)(ty * 4 + rr) * nf + tx * 4 + c;
-      acc[rr][c] = *d - acc[rr][c];
+      acc[rr][c] = (fresh ? 0.0 : *d) - acc[rr][c];
       *d = acc[rr][c];
     }
   if (t == 0) {
@@ -409,14 +451,6 @@ __global__ __launch_bounds__(256) void k_update(double* __restrict__ A, double* 
     store_block(dst, nf, p);
     store_block(Wk + (int64_t)o1 * nf + o1, nf, q);
   }
-}
-
-// W = identity (the starting R of the carried inverse)
-__global__ void k_identity(double* __restrict__ W, int nf) {
-  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const int k = blockIdx.y;
-  if (e >= (int64_t)nf * nf) return;
-  W[(int64_t)k * nf * nf + e] = ((e / nf) == (e % nf)) ? 1.0 : 0.0;
 }
 
 // tmp_k = W_k y_k  (one wave per row, lanes over columns)
@@ -567,10 +601,20 @@ __global__ __launch_bounds__(256) void k_pack(const double* __restrict__ W, int6
 }
 
 // Xs[k][i][t] = X[i][slot_dim(t)] * invls[k][t] (zero for padding slots and
-// rows beyond n)
+// rows beyond n), with invls[k][t] = fp32(ils[k][slot_dim(t)]) also written
+// out (the fp64 inverse lengthscale rounded to fp32 is the fp32 quotient
+// 1 / lengthscale: double rounding is exact for a quotient when the wider
+// format has at least 2p + 2 bits). Objective 0 also copies X into Xd;
+// (composite) fp32 preference slopes come from their fp64 copies, and (fp64
+// scoring) ils is copied into ils64.
 __global__ __launch_bounds__(256) void k_scale_x(const float* __restrict__ X, int64_t n,
                                                  int d, int dx, int dr, int dr4, int n_pad,
-                                                 const float* __restrict__ invls,
+                                                 const double* __restrict__ ils,
+                                                 float* __restrict__ invls,
+                                                 const double* __restrict__ pref_d,
+                                                 float* __restrict__ pref, int dc,
+                                                 float* __restrict__ Xd,
+                                                 double* __restrict__ ils64,
                                                  float* __restrict__ Xs) {
   const int k = blockIdx.y;
   const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
@@ -578,9 +622,14 @@ __global__ __launch_bounds__(256) void k_scale_x(const float* __restrict__ X, in
   const int64_t i = e / dx;
   const int t = static_cast<int>(e % dx);
   const int c = slot_dim(t, d, dr, dr4);
+  const float il = (c >= 0) ? static_cast<float>(ils[k * d + c]) : 0.f;
   float v = 0.f;
-  if (i < n && c >= 0) v = X[i * d + c] * invls[k * dx + t];
+  if (i < n && c >= 0) v = X[i * d + c] * il;
   Xs[(int64_t)k * n_pad * dx + e] = v;
+  if (i == 0) invls[k * dx + t] = il;
+  if (k == 0 && e < n * d) Xd[e] = X[e];
+  if (pref && e < dc) pref[k * dc + e] = static_cast<float>(pref_d[k * dc + e]);
+  if (ils64 && e < d) ils64[k * d + e] = ils[k * d + e];
 }
 
 // ctr[k][t] = mean over the n rows of Xs[k][i][t] (fp64 sum, fp32 result):
@@ -928,13 +977,11 @@ hipError_t launch_weights(const float* X, int64_t n, int d, int m, int n_pad,
 hipError_t launch_cholesky(double* A, double* W, int nf, int m, int* flag,
                            hipStream_t st) {
   const int nbk = nf / B;
-  const unsigned g = static_cast<unsigned>(((int64_t)nf * nf + 255) / 256);
-  hipLaunchKernelGGL(k_identity, dim3(g, m), dim3(256), 0, st, W, nf);
   hipLaunchKernelGGL(k_factor_first, dim3(m), dim3(256), 0, st, A, W, nf, flag);
   for (int kb = 0; kb < nbk; ++kb) {
     const int T = nbk - kb - 1;
     if (T + kb > 0)
-      hipLaunchKernelGGL(k_panel, dim3(T + kb, m), dim3(256), 0, st, A, W, nf, kb);
+      hipLaunchKernelGGL(k_panel, dim3(4 * (T + kb), m), dim3(256), 0, st, A, W, nf, kb);
     if (T > 0)
       hipLaunchKernelGGL(k_update, dim3(T * (T + 1) / 2 + T * (kb + 1), m), dim3(256), 0, st,
                          A, W, nf, kb, flag);
@@ -973,13 +1020,15 @@ hipError_t launch_mll(const float* X, int64_t n, int d, int m, int nf, const Gra
 
 hipError_t launch_pack(const double* W, int64_t n, int m, int nf, int nb, float* Lp,
                        unsigned long long* wmax, int* flag, const float* X, int d,
-                       int dx, int dr, int dr4, const float* invls, float* Xs, hipStream_t st) {
+                       int dx, int dr, int dr4, const double* ils, float* invls,
+                       const double* pref_d, float* pref, float* Xd, double* ils64,
+                       float* Xs, hipStream_t st) {
   hipError_t e = launch_pack_factor(W, n, m, nf, nb, Lp, wmax, flag, st);
   if (e != hipSuccess) return e;
   const int n_pad = nb * kBlk;
   const unsigned gx2 = static_cast<unsigned>(((int64_t)n_pad * dx + 255) / 256);
   hipLaunchKernelGGL(k_scale_x, dim3(gx2, m), dim3(256), 0, st, X, n, d, dx, dr, dr4, n_pad,
-                     invls, Xs);
+                     ils, invls, pref_d, pref, d - dr, Xd, ils64, Xs);
   return hipGetLastError();
 }
 
