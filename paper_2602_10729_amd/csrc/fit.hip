@@ -12,16 +12,18 @@
 // once, and its whole error budget goes to the scoring arithmetic.
 //
 // Blocked right-looking Cholesky with 64x64 blocks that carries the inverse
-// along. W starts as the identity; after step kb its block rows <= kb hold
-// L^{-1} and the rows below hold R_i = delta_i - sum_{k<=kb} L_ik W_k.
+// along. R starts as the identity; after step kb the block rows <= kb of W
+// hold L^{-1} and the rows below hold R_i = delta_i - sum_{k<=kb} L_ik W_k
+// (W itself is never cleared: each block is written before it is read).
 // Every diagonal block is factored and inverted in one workgroup
 // (D_kk = L_kk^{-1} lands in W's diagonal block). Step kb:
 //   panel:  L_ik = A_ik D_kk^T for the rows below, W_kj = D_kk R_kj for the
-//           columns left of the diagonal (64x64x64 tiles);
+//           columns left of the diagonal (quarter tiles);
 //   update: trailing A_ic -= L_ik L_ck^T (kb < c <= i) and R_ij -= L_ik W_kj
-//           (i > kb, j <= kb), 64x64x64 tiles; the workgroup that updates
-//           the next diagonal tile factors and inverts it at once, so no
-//           separate factor launch is needed after the first.
+//           (i > kb, j <= kb), 64x64x64 tiles on the fp64 matrix cores; the
+//           workgroup that updates the next diagonal tile factors and
+//           inverts it at once, so no separate factor launch is needed after
+//           the first.
 // Two launches per block column; the serial chain is one 64-step fused
 // factor and inverse of the diagonal block per block column.
 #include <hip/hip_runtime.h>
@@ -295,20 +297,35 @@ __global__ __launch_bounds__(256) void k_factor_first(double* __restrict__ A,
   store_block(Wk, nf, x);
 }
 
-// 64x64x64 product helper: acc[r][c] (4x4 per thread) += sum_t P[ty*4+r][t] * Q[tx*4+c][t].
-__device__ inline void gemm_nt_64(const double (*P)[LDP], const double (*Q)[LDP],
-                                  double acc[4][4], int ty, int tx) {
-  for (int t = 0; t < B; ++t) {
-    double pv[4], qv[4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) pv[r] = P[ty * 4 + r][t];
-#pragma unroll
-    for (int c = 0; c < 4; ++c) qv[c] = Q[tx * 4 + c][t];
-#pragma unroll
-    for (int r = 0; r < 4; ++r)
-#pragma unroll
-      for (int c = 0; c < 4; ++c) acc[r][c] = fma(pv[r], qv[c], acc[r][c]);
+typedef double doublex4 __attribute__((ext_vector_type(4)));
+
+// 64x64x64 product on the fp64 matrix cores (v_mfma_f64_16x16x4f64: A[i][k]
+// from lane i + 16k, B[k][j] from lane j + 16k, D[i][j] in lane
+// j + 16(i%4), element i/4): wave w adds sum_t P[i][t] Q[c][t] over its
+// 32x32 quadrant, rows 32(w/2).., columns 32(w%2).., as 2x2 tiles of 16x16;
+// acc[a][b][v] is element (32(w/2) + 16a + lane/16 + 4v,
+// 32(w%2) + 16b + lane%16) (tile_row / tile_col below).
+__device__ __forceinline__ void gemm_nt_64(const double (*P)[LDP], const double (*Q)[LDP],
+                                           doublex4 (&acc)[2][2]) {
+  const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int r0 = 32 * (w >> 1) + (l & 15), c0 = 32 * (w & 1) + (l & 15), kq = l >> 4;
+#pragma unroll 4
+  for (int t = 0; t < B; t += 4) {
+    const double a0 = P[r0][t + kq], a1 = P[r0 + 16][t + kq];
+    const double b0 = Q[c0][t + kq], b1 = Q[c0 + 16][t + kq];
+    acc[0][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b0, acc[0][0], 0, 0, 0);
+    acc[0][1] = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b1, acc[0][1], 0, 0, 0);
+    acc[1][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b0, acc[1][0], 0, 0, 0);
+    acc[1][1] = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b1, acc[1][1], 0, 0, 0);
   }
+}
+__device__ __forceinline__ int tile_row(int a, int v) {
+  const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
+  return 32 * (w >> 1) + 16 * a + (l >> 4) + 4 * v;
+}
+__device__ __forceinline__ int tile_col(int b) {
+  const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
+  return 32 * (w & 1) + 16 * b + (l & 15);
 }
 
 // Panel of step kb, with D = L_kk^{-1} (held in W's diagonal block kb), in
@@ -398,7 +415,6 @@ __global__ __launch_bounds__(256) void k_update(double* __restrict__ A, double* 
   const int T = nbk - kb - 1;
   const int nsyrk = T * (T + 1) / 2;
   const int t = blockIdx.x;
-  const int tid = threadIdx.x, tx = tid % 16, ty = tid / 16;
   double* Ak = A + (int64_t)k * nf * nf;
   double* Wk = W + (int64_t)k * nf * nf;
   const int o = kb * B;
@@ -425,26 +441,30 @@ __global__ __launch_bounds__(256) void k_update(double* __restrict__ A, double* 
     dst = Wk + (int64_t)ib * B * nf + jb * B;
   }
   __syncthreads();
-  double acc[4][4] = {};
-  gemm_nt_64(p, q, acc, ty, tx);
+  doublex4 acc[2][2] = {};
+  gemm_nt_64(p, q, acc);
   // the first update of an R tile (jb = kb) starts from zero: W is not
   // cleared beforehand (its blocks above the diagonal are never read)
   const bool fresh = first_r;
 #pragma unroll
-  for (int rr = 0; rr < 4; ++rr)
+  for (int a = 0; a < 2; ++a)
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      double* d = dst + (int64_t)(ty * 4 + rr) * nf + tx * 4 + c;
-      acc[rr][c] = (fresh ? 0.0 : *d) - acc[rr][c];
-      *d = acc[rr][c];
-    }
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        double* d = dst + (int64_t)tile_row(a, v) * nf + tile_col(b);
+        acc[a][b][v] = (fresh ? 0.0 : *d) - acc[a][b][v];
+        *d = acc[a][b][v];
+      }
   if (t == 0) {
     // next diagonal block: stage the updated tile, factor and invert it
     __syncthreads();
 #pragma unroll
-    for (int rr = 0; rr < 4; ++rr)
+    for (int a = 0; a < 2; ++a)
 #pragma unroll
-      for (int c = 0; c < 4; ++c) p[ty * 4 + rr][tx * 4 + c] = acc[rr][c];
+      for (int b = 0; b < 2; ++b)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) p[tile_row(a, v)][tile_col(b)] = acc[a][b][v];
     __syncthreads();
     chol_inv64(p, q, scr, flag);
     const int o1 = o + B;
@@ -765,20 +785,21 @@ __global__ __launch_bounds__(256) void k_kinv(double* __restrict__ A, const doub
   const int J = t - I * (I + 1) / 2;
   const int nbk = nf / B;
   const double* Wk = W + (int64_t)k * nf * nf;
-  const int tx = threadIdx.x % 16, ty = threadIdx.x / 16;
-  double acc[4][4] = {};
+  doublex4 acc[2][2] = {};
   for (int K = I; K < nbk; ++K) {
     __syncthreads();   // the previous step's tiles are no longer read
     load_blocks<true, true>(p, Wk + (int64_t)K * B * nf + I * B,
                             q, Wk + (int64_t)K * B * nf + J * B, nf);
     __syncthreads();
-    gemm_nt_64(p, q, acc, ty, tx);
+    gemm_nt_64(p, q, acc);
   }
   double* dst = A + (int64_t)k * nf * nf + (int64_t)I * B * nf + J * B;
 #pragma unroll
-  for (int r = 0; r < 4; ++r)
+  for (int a = 0; a < 2; ++a)
 #pragma unroll
-    for (int c = 0; c < 4; ++c) dst[(int64_t)(ty * 4 + r) * nf + tx * 4 + c] = acc[r][c];
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) dst[(int64_t)tile_row(a, v) * nf + tile_col(b)] = acc[a][b][v];
 }
 
 // Gradient partials of one 16x16 tile of observation pairs (i >= i') per
@@ -936,8 +957,7 @@ __global__ __launch_bounds__(256) void k_trmm(const double* __restrict__ T,
   const int nbk = nf / B;
   const double* Tk = T + (int64_t)k * nf * nf;
   const double* Bk = Bm + (int64_t)k * nf * ldb;
-  const int tx = threadIdx.x % 16, ty = threadIdx.x / 16;
-  double acc[4][4] = {};
+  doublex4 acc[2][2] = {};
   const int k0 = TRANS ? I : 0, k1 = TRANS ? nbk : I + 1;
   for (int K = k0; K < k1; ++K) {
     __syncthreads();   // the previous step's tiles are no longer read
@@ -948,13 +968,15 @@ __global__ __launch_bounds__(256) void k_trmm(const double* __restrict__ T,
     put_tile<TRANS>(p, v0);
     put_tile<true>(q, v1);
     __syncthreads();
-    gemm_nt_64(p, q, acc, ty, tx);
+    gemm_nt_64(p, q, acc);
   }
   double* dst = C + (int64_t)k * nf * ldb + (int64_t)I * B * ldb + Jc * B;
 #pragma unroll
-  for (int r = 0; r < 4; ++r)
+  for (int a = 0; a < 2; ++a)
 #pragma unroll
-    for (int c = 0; c < 4; ++c) dst[(int64_t)(ty * 4 + r) * ldb + tx * 4 + c] = acc[r][c];
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) dst[(int64_t)tile_row(a, v) * ldb + tile_col(b)] = acc[a][b][v];
 }
 
 }  // namespace

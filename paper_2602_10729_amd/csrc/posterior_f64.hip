@@ -23,7 +23,7 @@
 // is produced.
 //
 // Fragments of v_mfma_f64_16x16x4f64: A[i][k] from lane i + 16k, B[k][j] from
-// lane j + 16k, D[i][j] in lane j + 16(i/4), element i%4. Only the pairing of
+// lane j + 16k, D[i][j] in lane j + 16(i%4), element i/4. Only the pairing of
 // A's and B's k and D's columns (lane % 16) are used.
 #include <hip/hip_runtime.h>
 
