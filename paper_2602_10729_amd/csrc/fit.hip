@@ -335,7 +335,7 @@ __device__ __forceinline__ int tile_col(int b) {
 //   quarter u takes rows 16u .. 16u+15 of the tile, the only rows it reads;
 // tiles T <= t < T + kb: W[kb][jb] <- D R[kb][jb] for jb = t - T (< kb);
 //   quarter u takes columns 16u .. 16u+15 of R, the only columns it reads.
-// Each output is the same ascending sum over s as a whole-tile product.
+// The products run on the fp64 matrix cores, each wave one 16x16 tile.
 __global__ __launch_bounds__(256) void k_panel(double* __restrict__ A, double* __restrict__ W,
                                                int nf, int kb) {
   __shared__ double p[B][LDP];
@@ -344,7 +344,7 @@ __global__ __launch_bounds__(256) void k_panel(double* __restrict__ A, double* _
   const int nbk = nf / B;
   const int T = nbk - kb - 1;
   const int t = blockIdx.x >> 2, u = blockIdx.x & 3;
-  const int tid = threadIdx.x, tx = tid % 16, ty = tid / 16;
+  const int tid = threadIdx.x, l = tid & 63, w = tid >> 6;
   double* Ak = A + (int64_t)k * nf * nf;
   double* Wk = W + (int64_t)k * nf * nf;
   const int o = kb * B;
@@ -366,14 +366,16 @@ __global__ __launch_bounds__(256) void k_panel(double* __restrict__ A, double* _
     }
     put_tile<false>(q, v1);
     __syncthreads();
-    double acc[4] = {};
-    for (int s2 = 0; s2 < B; ++s2) {
-      const double pv = p[ty][s2];
+    // wave w: output columns 16w .. 16w+15 (one 16x16 tile on the matrix cores)
+    doublex4 acc = {};
+#pragma unroll 4
+    for (int s2 = 0; s2 < B; s2 += 4)
+      acc = __builtin_amdgcn_mfma_f64_16x16x4f64(p[l & 15][s2 + (l >> 4)],
+                                                 q[16 * w + (l & 15)][s2 + (l >> 4)], acc, 0, 0,
+                                                 0);
 #pragma unroll
-      for (int c = 0; c < 4; ++c) acc[c] = fma(pv, q[tx * 4 + c][s2], acc[c]);
-    }
-#pragma unroll
-    for (int c = 0; c < 4; ++c) dst[(int64_t)ty * nf + tx * 4 + c] = acc[c];
+    for (int v = 0; v < 4; ++v)
+      dst[(int64_t)((l >> 4) + 4 * v) * nf + 16 * w + (l & 15)] = acc[v];
   } else {
     double* dst = Wk + (int64_t)o * nf + (t - T) * B + 16 * u;
     // p = D; q[c][s] = R[s][16u + c] (c < 16)
@@ -390,21 +392,23 @@ __global__ __launch_bounds__(256) void k_panel(double* __restrict__ A, double* _
       q[g & 15][g >> 4] = v0[e];
     }
     __syncthreads();
-    double acc[4] = {};
-    for (int s2 = 0; s2 < B; ++s2) {
-      const double qv = q[tx][s2];
+    // wave w: output rows 16w .. 16w+15
+    doublex4 acc = {};
+#pragma unroll 4
+    for (int s2 = 0; s2 < B; s2 += 4)
+      acc = __builtin_amdgcn_mfma_f64_16x16x4f64(p[16 * w + (l & 15)][s2 + (l >> 4)],
+                                                 q[l & 15][s2 + (l >> 4)], acc, 0, 0, 0);
 #pragma unroll
-      for (int r = 0; r < 4; ++r) acc[r] = fma(p[ty * 4 + r][s2], qv, acc[r]);
-    }
-#pragma unroll
-    for (int r = 0; r < 4; ++r) dst[(int64_t)(ty * 4 + r) * nf + tx] = acc[r];
+    for (int v = 0; v < 4; ++v)
+      dst[(int64_t)(16 * w + (l >> 4) + 4 * v) * nf + (l & 15)] = acc[v];
   }
 }
 
 // Update of step kb. Tile t < T(T+1)/2: trailing A tile; the rest: R tiles
 // of W (the tiles of block column kb are written, not updated: nothing
-// before this step writes them). Tile 0 is the next diagonal block, factored and inverted right after
-// its update (L into A, L^{-1} into W's diagonal block kb+1).
+// before this step writes them). Tile 0 is the next diagonal block,
+// factored and inverted right after its update (L into A, L^{-1} into W's
+// diagonal block kb+1).
 __global__ __launch_bounds__(256) void k_update(double* __restrict__ A, double* __restrict__ W,
                                                 int nf, int kb, int* __restrict__ flag) {
   __shared__ double p[B][LDP];
