@@ -802,15 +802,34 @@ bo_status fit_impl(const char* who, const float* X, const float* Y, int64_t n, i
     gp.s_int = gp.s_dep + m;
     gp.pref = gp.s_int + m;
   }
+  // The scaled X, its distance fragments and (composite) the preference
+  // weights depend only on X and the hyperparameters: they run on the side
+  // stream beside the factorisation, then alpha beside the fp16 pack, and
+  // the side stream joins before the read-back. (An event's later record
+  // does not change a wait already enqueued on it.)
+  if ((s = side_stream(DS)) != BO_OK) return bail(s);
+  hipStream_t side = DS->side;
+  e = hipEventRecord(DS->side_evt[0], st);
+  if (e == hipSuccess) e = hipStreamWaitEvent(side, DS->side_evt[0], 0);
+  if (e != hipSuccess) return bail(hip_fail(e, "bo_fit: side stream"));
+  if ((s = after_launch(launch_scale_x(X, n, d, m, M->nb, M->dx, dr, dr4, gp.ils, M->invls,
+                                       comp ? gp.pref : nullptr, M->pref, M->Xd, M->ils64,
+                                       M->Xs, side), side, "scale X")) != BO_OK) return bail(s);
+  if ((s = after_launch(launch_pack_x(M->Xs, n, m, M->nb, M->dx, dr4, M->ctr, M->xf, M->x2, side), side, "pack X")) != BO_OK) return bail(s);
+  if (comp && (s = after_launch(launch_weights(X, n, d, m, M->n_pad, gp, M->wts, side), side, "weights")) != BO_OK) return bail(s);
   if ((s = after_launch(launch_gram(X, n, d, m, nf, gp, fs.A, st, fs.stats), st, "gram")) != BO_OK) return bail(s);
-  if (comp && (s = after_launch(launch_weights(X, n, d, m, M->n_pad, gp, M->wts, st), st, "weights")) != BO_OK) return bail(s);
   if ((s = after_launch(launch_cholesky(fs.A, fs.W, nf, m, fs.flag, st), st, "cholesky")) != BO_OK) return bail(s);
-  if ((s = after_launch(launch_alpha(fs.W, Y, n, m, nf, M->n_pad, fs.tmp, M->alpha, st, M->alpha64), st, "alpha")) != BO_OK) return bail(s);
-  if (f64 && (s = after_launch(launch_pack_f64(fs.W, n, m, nf, M->nb, M->Lp64, st), st, "pack fp64")) != BO_OK) return bail(s);
-  if ((s = after_launch(launch_pack(fs.W, n, m, nf, M->nb, M->Lp, fs.stats + m, fs.flag, X, d,
-                                    M->dx, dr, dr4, gp.ils, M->invls, comp ? gp.pref : nullptr,
-                                    M->pref, M->Xd, M->ils64, M->Xs, st), st, "pack")) != BO_OK) return bail(s);
-  if ((s = after_launch(launch_pack_x(M->Xs, n, m, M->nb, M->dx, dr4, M->ctr, M->xf, M->x2, st), st, "pack X")) != BO_OK) return bail(s);
+  // alpha (and the fp64 fragments) on the side stream, the fp16 pack here
+  e = hipEventRecord(DS->side_evt[0], st);
+  if (e == hipSuccess) e = hipStreamWaitEvent(side, DS->side_evt[0], 0);
+  if (e != hipSuccess) return bail(hip_fail(e, "bo_fit: side stream"));
+  if ((s = after_launch(launch_alpha(fs.W, Y, n, m, nf, M->n_pad, fs.tmp, M->alpha, side, M->alpha64), side, "alpha")) != BO_OK) return bail(s);
+  if (f64 && (s = after_launch(launch_pack_f64(fs.W, n, m, nf, M->nb, M->Lp64, side), side, "pack fp64")) != BO_OK) return bail(s);
+  e = hipEventRecord(DS->side_evt[1], side);
+  if (e != hipSuccess) return bail(hip_fail(e, "bo_fit: side stream"));
+  if ((s = after_launch(launch_pack_factor(fs.W, n, m, nf, M->nb, M->Lp, fs.stats + m, fs.flag, st), st, "pack")) != BO_OK) return bail(s);
+  e = hipStreamWaitEvent(st, DS->side_evt[1], 0);
+  if (e != hipSuccess) return bail(hip_fail(e, "bo_fit: side stream"));
 
   // one synchronisation: the positive-definiteness flag and Y (for the front
   // and its finiteness check) come back together

@@ -160,23 +160,14 @@ int64_t mll_tiles(int nf);
 hipError_t launch_mll(const float* X, int64_t n, int d, int m, int nf, const GramParams& g,
                       double* A, const double* W, const double* tmp, const double* alpha64,
                       double* partials, double* out, hipStream_t st);
-// Pack W into the posterior's A-fragment format (fp16 hi/lo planes of 16x32
-// lower blocks, zeros beyond n, then one all-zero block; 2 KiB per block,
-// posterior_frag_blocks(nb) blocks per objective), each 16-row block I scaled
-// by a power of two that brings its largest entry into [2^13, 2^14), followed
-// by the nb inverse scales (packed_factor_floats(nb) floats per objective;
-// wmax [m] = largest |W| per objective as a non-negative double's bit
-// pattern, zeroed by the caller; *flag set on a non-finite entry), and write
-// the lengthscale-scaled X in the slot layout from the fp64 inverse
+// The lengthscale-scaled X in the slot layout from the fp64 inverse
 // lengthscales ils [m][d], with the fp32 per-slot values invls [m][dx], the
 // copy Xd [n][d] of X, (composite, pref non-NULL) the fp32 preference slopes
 // pref [m][d - dr] from their fp64 copies pref_d, and (ils64 non-NULL) a copy
 // of ils.
-hipError_t launch_pack(const double* W, int64_t n, int m, int nf, int nb,
-                       float* Lp, unsigned long long* wmax, int* flag,
-                       const float* X, int d, int dx, int dr, int dr4,
-                       const double* ils, float* invls, const double* pref_d,
-                       float* pref, float* Xd, double* ils64, float* Xs, hipStream_t st);
+hipError_t launch_scale_x(const float* X, int64_t n, int d, int m, int nb, int dx, int dr,
+                          int dr4, const double* ils, float* invls, const double* pref_d,
+                          float* pref, float* Xd, double* ils64, float* Xs, hipStream_t st);
 
 // Squared distances in the posterior kernel come from the expansion
 // |c|^2 + |x|^2 - 2 c.x of centred scaled coordinates, with c.x on the fp16
@@ -208,7 +199,13 @@ hipError_t launch_gather_z(const float* ZX, int64_t n, int m, int S, int nf, int
 // C[k] = op(T[k]) Bm[k]: T lower [nf][nf], Bm and C [nf][ldb], op = T or T^T.
 hipError_t launch_trmm(bool trans, const double* T, const double* Bm, double* C, int nf,
                        int ldb, int m, hipStream_t st);
-// The posterior's A-fragment packing of W alone (no coordinate scaling).
+// Pack W into the posterior's A-fragment format (fp16 hi/lo planes of 16x32
+// lower blocks, zeros beyond n, then one all-zero block; 2 KiB per block,
+// posterior_frag_blocks(nb) blocks per objective), each 16-row block I scaled
+// by a power of two that brings its largest entry into [2^13, 2^14), followed
+// by the nb inverse scales (packed_factor_floats(nb) floats per objective;
+// wmax [m] = largest |W| per objective as a non-negative double's bit
+// pattern, zeroed by the caller; *flag set on a non-finite entry).
 hipError_t launch_pack_factor(const double* W, int64_t n, int m, int nf, int nb, float* Lp,
                               unsigned long long* wmax, int* flag, hipStream_t st);
 

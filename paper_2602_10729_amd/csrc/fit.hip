@@ -444,22 +444,31 @@ __global__ __launch_bounds__(256) void k_update(double* __restrict__ A, double* 
                              q, Wk + (int64_t)o * nf + jb * B, nf);   // q = W[kb][jb]^T
     dst = Wk + (int64_t)ib * B * nf + jb * B;
   }
-  __syncthreads();
-  doublex4 acc[2][2] = {};
-  gemm_nt_64(p, q, acc);
-  // the first update of an R tile (jb = kb) starts from zero: W is not
-  // cleared beforehand (its blocks above the diagonal are never read)
-  const bool fresh = first_r;
+  // the tile's current values, requested before the product: the first
+  // update of an R tile (jb = kb) starts from zero instead (W is not cleared
+  // beforehand; its blocks above the diagonal are never read)
+  doublex4 cur[2][2];
 #pragma unroll
   for (int a = 0; a < 2; ++a)
 #pragma unroll
     for (int b = 0; b < 2; ++b)
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        double* d = dst + (int64_t)tile_row(a, v) * nf + tile_col(b);
-        acc[a][b][v] = (fresh ? 0.0 : *d) - acc[a][b][v];
-        *d = acc[a][b][v];
-      }
+      for (int v = 0; v < 4; ++v)
+        cur[a][b][v] = first_r ? 0.0 : dst[(int64_t)tile_row(a, v) * nf + tile_col(b)];
+  __syncthreads();
+  doublex4 acc[2][2] = {};
+  gemm_nt_64(p, q, acc);
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      acc[a][b] = cur[a][b] - acc[a][b];
+      // the next diagonal tile (t = 0) is stored once, factored, below
+      if (t != 0)
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+          dst[(int64_t)tile_row(a, v) * nf + tile_col(b)] = acc[a][b][v];
+    }
   if (t == 0) {
     // next diagonal block: stage the updated tile, factor and invert it
     __syncthreads();
@@ -545,14 +554,23 @@ __global__ __launch_bounds__(256) void k_rowblock_scale(const double* __restrict
   __shared__ double part[256];
   const int I = blockIdx.x, k = blockIdx.y;
   const double* Wk = W + (int64_t)k * nf * nf;
-  const int64_t row = (int64_t)I * kBlk + (threadIdx.x & 15);
+  // the block's 16 rows, columns 0 .. 16I + 15: consecutive threads take
+  // consecutive columns (coalesced), the 16 rows in turn
+  const int64_t lim = (int64_t)I * kBlk + kBlk;
+  const int64_t ncol = (lim < n) ? lim : n;
   double mx = 0.0;
   bool bad = false;
-  if (row < n) {
-    for (int64_t col = threadIdx.x >> 4; col <= row; col += 16) {
-      const double w = Wk[row * nf + col];
-      bad = bad || !(fabs(w) < INFINITY);
-      mx = fmax(mx, fabs(w));
+  for (int64_t col = threadIdx.x; col < ncol; col += 256) {
+    double v[kBlk];
+#pragma unroll
+    for (int r = 0; r < kBlk; ++r) {
+      const int64_t row = (int64_t)I * kBlk + r;
+      v[r] = (row < n && col <= row) ? Wk[row * nf + col] : 0.0;
+    }
+#pragma unroll
+    for (int r = 0; r < kBlk; ++r) {
+      bad = bad || !(fabs(v[r]) < INFINITY);
+      mx = fmax(mx, fabs(v[r]));
     }
   }
   if (bad) *flag = 1;
@@ -1044,13 +1062,9 @@ hipError_t launch_mll(const float* X, int64_t n, int d, int m, int nf, const Gra
   return hipGetLastError();
 }
 
-hipError_t launch_pack(const double* W, int64_t n, int m, int nf, int nb, float* Lp,
-                       unsigned long long* wmax, int* flag, const float* X, int d,
-                       int dx, int dr, int dr4, const double* ils, float* invls,
-                       const double* pref_d, float* pref, float* Xd, double* ils64,
-                       float* Xs, hipStream_t st) {
-  hipError_t e = launch_pack_factor(W, n, m, nf, nb, Lp, wmax, flag, st);
-  if (e != hipSuccess) return e;
+hipError_t launch_scale_x(const float* X, int64_t n, int d, int m, int nb, int dx, int dr,
+                          int dr4, const double* ils, float* invls, const double* pref_d,
+                          float* pref, float* Xd, double* ils64, float* Xs, hipStream_t st) {
   const int n_pad = nb * kBlk;
   const unsigned gx2 = static_cast<unsigned>(((int64_t)n_pad * dx + 255) / 256);
   hipLaunchKernelGGL(k_scale_x, dim3(gx2, m), dim3(256), 0, st, X, n, d, dx, dr, dr4, n_pad,
