@@ -1284,9 +1284,6 @@ bo_status nehvi_prepare_impl(bo_model model, const float* ZX, int32_t S, const f
   DeviceState* DS = device_state(M.device);
   if (!DS) return fail(BO_ERR_DEVICE, W_ + ": device index out of range");
   std::lock_guard<std::mutex> stage_lock(DS->fit_mu);
-  FitScratch fs;
-  fs.st = st;
-  if ((s = fit_work(DS, (size_t)m * nf * nf, nhyp, (size_t)m * nf, &fs)) != BO_OK) return s;
   const size_t off_flag = (sizeof(double) * nhyp + 15) / 16 * 16;
   const size_t off_stats = off_flag + 32;
   const size_t off_y = off_stats + 16 * 3;
