@@ -117,6 +117,8 @@ struct DeviceState {
   // vector [vec], then 64 bytes of flag (int) and statistics (at byte 16)
   double* fw = nullptr;
   size_t fw_mat = 0, fw_hyp = 0, fw_vec = 0;
+  // under fit_mu: marks bo_fit's early read-back of Y
+  hipEvent_t fit_evt = nullptr;
 };
 
 // The side stream and its events of device state DS (created once).
@@ -790,6 +792,12 @@ bo_status fit_impl(const char* who, const float* X, const float* Y, int64_t n, i
   // are written on the device from these (k_scale_x)
   e = hipMemcpyAsync(fs.hyp, stage, sizeof(double) * hyp.size(), hipMemcpyHostToDevice, st);
   if (e == hipSuccess) e = hipMemsetAsync(fs.flag, 0, 64, st);   // flag and statistics
+  // Y comes back first, so that its finiteness check and the front run on
+  // the host while the device factors
+  if (e == hipSuccess && !DS->fit_evt) e = hipEventCreateWithFlags(&DS->fit_evt, hipEventDisableTiming);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(stage + off_y, Y, sizeof(float) * n * m, hipMemcpyDeviceToHost, st);
+  if (e == hipSuccess) e = hipEventRecord(DS->fit_evt, st);
   if (e != hipSuccess) return bail(hip_fail(e, "bo_fit: upload"));
 
   GramParams gp;
@@ -831,19 +839,20 @@ bo_status fit_impl(const char* who, const float* X, const float* Y, int64_t n, i
   e = hipStreamWaitEvent(st, DS->side_evt[1], 0);
   if (e != hipSuccess) return bail(hip_fail(e, "bo_fit: side stream"));
 
-  // one synchronisation: the positive-definiteness flag and Y (for the front
-  // and its finiteness check) come back together
+  // the flag and statistics follow the work; Y (copied back first) is
+  // checked and its front formed meanwhile, then one synchronisation
   e = hipMemcpyAsync(stage + off_flag, fs.flag, 64, hipMemcpyDeviceToHost, st);
-  if (e == hipSuccess)
-    e = hipMemcpyAsync(stage + off_y, Y, sizeof(float) * n * m, hipMemcpyDeviceToHost, st);
-  if (e == hipSuccess) e = hipStreamSynchronize(st);
-  if (e != hipSuccess) return bail(hip_fail(e, "bo_fit: sync"));
-  int flag = 0;
-  std::memcpy(&flag, stage + off_flag, sizeof(int));
+  if (e == hipSuccess) e = hipEventSynchronize(DS->fit_evt);
+  if (e != hipSuccess) return bail(hip_fail(e, "bo_fit: read-back"));
   const float* yst = reinterpret_cast<const float*>(stage + off_y);
   M->Yh.assign(yst, yst + (size_t)n * m);
   if (!all_finite(M->Yh.data(), M->Yh.size()))
     return bail(fail(BO_ERR_NONFINITE_INPUT, W + ": Y not finite"));
+  host_front<float>(M->Yh.data(), n, m, nullptr, M->nd);
+  e = hipStreamSynchronize(st);
+  if (e != hipSuccess) return bail(hip_fail(e, "bo_fit: sync"));
+  int flag = 0;
+  std::memcpy(&flag, stage + off_flag, sizeof(int));
   if (flag)
     return bail(fail(BO_ERR_NOT_POSITIVE_DEFINITE,
                      W + ": non-positive Cholesky pivot or non-finite inverse factor"));
@@ -866,7 +875,6 @@ bo_status fit_impl(const char* who, const float* X, const float* Y, int64_t n, i
       }
     }
   }
-  host_front<float>(M->Yh.data(), n, m, nullptr, M->nd);
 
   M->last_stream = st;
   *out = h;
