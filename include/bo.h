@@ -120,10 +120,19 @@ typedef enum {
  * Synchronous: enqueues all device work on the stream (behind earlier work,
  * without waiting for it), then waits once and returns after the positive
  * definiteness flag, the conditioning estimate and Y have been read back. Y
- * lives on the device, so its finiteness is checked at that point (its
- * kernels have already run); the host arguments are validated before
- * anything is enqueued. Concurrent fits on one device share a pinned staging
- * buffer and run one at a time.
+ * lives on the device, so its finiteness is checked once it is back (it is
+ * read back first, so the host checks it and forms its front while the
+ * device factors; the kernels run either way); the host arguments are
+ * validated before anything is enqueued. Part of the work (the scaled X and
+ * its distance fragments, alpha) runs on a second stream of the library's
+ * own, at default priority, ordered after the caller's earlier work and
+ * joined back into the caller's stream before return. Concurrent fits on one
+ * device share a pinned staging buffer and run one at a time.
+ * Memory: the model's device buffers are one allocation from a stream-ordered
+ * pool; the fp64 factorisation scratch (2 m n_f^2 doubles with n_f the
+ * multiple of 64 at or above n, plus a few KB) is kept per device after the
+ * first fit and reused, growing when a larger fit needs more (at most 201 MB,
+ * at n = 2048, m = 3), until the process ends.
  * Errors: INVALID_ARGUMENT (also hyperparameters outside the accepted
  * range), NONFINITE_INPUT (hyperparameters or Y not finite), CAPACITY,
  * NOT_POSITIVE_DEFINITE (a pivot <= 0 or a non-finite inverse factor),
@@ -222,8 +231,9 @@ bo_status bo_fit_composite_f64(const float* X, const float* Y, int64_t n, int32_
  *
  * X, Y, n, d, m, lengthscale, outputscale, noise: as bo_fit
  * value  host [m] out;  grad  host [m][d + 2] out (fp64)
- * Synchronous; no model is created. Errors: as bo_fit (NOT_POSITIVE_DEFINITE
- * when K is not positive definite).
+ * Synchronous; no model is created; uses the device's kept fp64 scratch as
+ * bo_fit does. Errors: as bo_fit (NOT_POSITIVE_DEFINITE when K is not
+ * positive definite).
  */
 bo_status bo_mll(const float* X, const float* Y, int64_t n, int32_t d, int32_t m,
                  const float* lengthscale, const float* outputscale, const float* noise,
