@@ -144,11 +144,13 @@ __device__ __forceinline__ double rsqrt_d(double d) {
 
 // Factor the symmetric 64x64 block held in LDS `a` (lower triangle read) and
 // invert the factor: on return a = L (zeros above the diagonal) and
-// x = L^{-1} (zeros above the diagonal). All four waves of the 256-thread
-// workgroup take part (every thread must call this): thread (w, c) =
-// (wave, lane) keeps, in registers indexed only by unrolled constants,
-//   row c of A, columns 16w .. 16w+15, and
-//   column c of X, rows 16w .. 16w+15.
+// x = L^{-1} (zeros above the diagonal). All eight waves of the 512-thread
+// workgroup take part (every thread must call this), two per SIMD so that
+// one wave's multiply-adds fill the other's wait on the pivot chain: thread
+// (w, c) = (wave, lane) keeps, in registers indexed only by unrolled
+// constants,
+//   row c of A, columns 8w .. 8w+7, and
+//   column c of X, rows 8w .. 8w+7.
 //
 // The factor (right-looking, unscaled) and the inverse (forward
 // substitution, one column of X per lane) advance together, one barrier per
@@ -158,8 +160,8 @@ __device__ __forceinline__ double rsqrt_d(double d) {
 //   whole wave), the pivot A_jj, and row j of X as it stands (X_jc L_jj);
 //   the buffers are double-buffered by step parity;
 //   after it, every thread takes 1 / L_jj = A_jj^{-1/2} and updates
-//     A_ic -= A_ij A_cj / A_jj   (its row i, its 16 columns c)
-//     X_ic -= A_ij (X_jc L_jj) / A_jj   (its column c, its 16 rows i);
+//     A_ic -= A_ij A_cj / A_jj   (its row i, its 8 columns c)
+//     X_ic -= A_ij (X_jc L_jj) / A_jj   (its column c, its 8 rows i);
 //   the zeros of the published column leave rows and columns <= j as they
 //   are (above the diagonal A is never read again; rows of X up to j are
 //   final).
@@ -168,29 +170,30 @@ __device__ __forceinline__ double rsqrt_d(double d) {
 // A non-positive or non-finite pivot sets *flag and is replaced by 1.
 // Scratch: scr holds 6 x 64 doubles, 16-byte aligned (two published columns
 // of A, two published rows of X, two pivots, the 64 values 1 / L_jj).
+constexpr int kFactorThreads = 512;
 __device__ __forceinline__ void chol_inv64(double (*a)[LDP], double (*x)[LDP], double* scr,
                                            int* flag) {
   const int c = threadIdx.x & 63;
-  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // column group 16w ..
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // column group 8w ..
   double* colbuf = scr;                      // [2][64] column j of A, rows > j
   double* rowbuf = scr + 2 * B;              // [2][64] row j of X
   double* pivbuf = scr + 4 * B;              // [2]     A_jj
   double* rdiag = scr + 5 * B;               // [64]    1 / L_jj
-  double r[16], xv[16];
+  double r[8], xv[8];
 #pragma unroll
-  for (int t = 0; t < 16; ++t) {
-    r[t] = a[c][16 * w + t];
-    xv[t] = (16 * w + t == c) ? 1.0 : 0.0;
+  for (int t = 0; t < 8; ++t) {
+    r[t] = a[c][8 * w + t];
+    xv[t] = (8 * w + t == c) ? 1.0 : 0.0;
   }
   bool bad_any = false;
-  // steps j = 16 jw + jt: the group of the pivot is a loop variable and the
+  // steps j = 8 jw + jt: the group of the pivot is a loop variable and the
   // position within it an unrolled constant (register indices stay constant
   // while the straight-line code stays one group long)
 #pragma unroll 1
-  for (int jw = 0; jw < 4; ++jw) {
+  for (int jw = 0; jw < 8; ++jw) {
 #pragma unroll
-  for (int jt = 0; jt < 16; ++jt) {
-    const int j = 16 * jw + jt;
+  for (int jt = 0; jt < 8; ++jt) {
+    const int j = 8 * jw + jt;
     double* col = colbuf + (jt & 1) * B;
     double* row = rowbuf + (jt & 1) * B;
     if (w == jw) {
@@ -203,9 +206,9 @@ __device__ __forceinline__ void chol_inv64(double (*a)[LDP], double (*x)[LDP], d
     const double a_jj = pivbuf[jt & 1];
     const double a_cj = col[c];
     const double x_jc = row[c];
-    double2 l[8];
+    double2 l[4];
 #pragma unroll
-    for (int t = 0; t < 8; ++t) l[t] = *reinterpret_cast<const double2*>(col + 16 * w + 2 * t);
+    for (int t = 0; t < 4; ++t) l[t] = *reinterpret_cast<const double2*>(col + 8 * w + 2 * t);
     __builtin_amdgcn_sched_barrier(0);
     const bool bad = !(a_jj > 0.0) || !isfinite(a_jj);
     const double d = bad ? 1.0 : a_jj;
@@ -215,7 +218,7 @@ __device__ __forceinline__ void chol_inv64(double (*a)[LDP], double (*x)[LDP], d
     const double mrow = a_cj * id;          // A_cj / A_jj for this lane's row c
     const double xs = x_jc * id;            // (X_jc / L_jj) / L_jj
 #pragma unroll
-    for (int t = 0; t < 16; t += 2) {
+    for (int t = 0; t < 8; t += 2) {
       r[t] = fma(-mrow, l[t / 2].x, r[t]);
       r[t + 1] = fma(-mrow, l[t / 2].y, r[t + 1]);
       xv[t] = fma(-l[t / 2].x, xs, xv[t]);
@@ -224,11 +227,11 @@ __device__ __forceinline__ void chol_inv64(double (*a)[LDP], double (*x)[LDP], d
     if (threadIdx.x == 0) rdiag[j] = isd;
   }
   }
-  if (bad_any && threadIdx.x == 0) atomicOr(flag, 1);
+  if (bad_any && threadIdx.x == 0) atomicOr(flag, 1);   // every thread saw every pivot
   __syncthreads();   // rdiag is complete; every published read is done
 #pragma unroll
-  for (int t = 0; t < 16; ++t) {
-    const int k = 16 * w + t;               // column of A / row of X
+  for (int t = 0; t < 8; ++t) {
+    const int k = 8 * w + t;                // column of A / row of X
     a[c][k] = (c >= k) ? r[t] * rdiag[k] : 0.0;
     x[k][c] = xv[t] * rdiag[k];
   }
@@ -236,7 +239,7 @@ __device__ __forceinline__ void chol_inv64(double (*a)[LDP], double (*x)[LDP], d
 }
 
 // Copies of 64x64 tiles between global memory (leading dimension ld) and
-// padded LDS tiles, by a 256-thread workgroup. Every load of a call is
+// padded LDS tiles, by the first 256 threads of a workgroup. Every load of a call is
 // issued before the first LDS store, so the latencies overlap; two tiles
 // can be fetched in one call. Transposed variants store dst[c][i] = src[i][c].
 template <bool T>
@@ -282,15 +285,16 @@ __device__ inline void store_block(double* dst, int ld, const double (*srcb)[LDP
 }
 
 // First diagonal block (kb = 0) of every objective: L into A, L^{-1} into W.
-__global__ __launch_bounds__(256) void k_factor_first(double* __restrict__ A,
-                                                      double* __restrict__ W, int nf,
-                                                      int* __restrict__ flag) {
+// Eight waves (the factor's layout); the first four load the tile.
+__global__ __launch_bounds__(kFactorThreads) void k_factor_first(double* __restrict__ A,
+                                                                 double* __restrict__ W, int nf,
+                                                                 int* __restrict__ flag) {
   __shared__ double a[B][LDP];
   __shared__ __align__(16) double x[B][LDP];
   __shared__ __align__(16) double scr[6 * B];
   double* Ak = A + (int64_t)blockIdx.x * nf * nf;
   double* Wk = W + (int64_t)blockIdx.x * nf * nf;
-  load_block(a, Ak, nf);
+  if (threadIdx.x < 256) load_block(a, Ak, nf);
   __syncthreads();
   chol_inv64(a, x, scr, flag);
   store_block(Ak, nf, a);
@@ -301,8 +305,9 @@ typedef double doublex4 __attribute__((ext_vector_type(4)));
 
 // 64x64x64 product on the fp64 matrix cores (v_mfma_f64_16x16x4f64: A[i][k]
 // from lane i + 16k, B[k][j] from lane j + 16k, D[i][j] in lane
-// j + 16(i%4), element i/4): wave w adds sum_t P[i][t] Q[c][t] over its
-// 32x32 quadrant, rows 32(w/2).., columns 32(w%2).., as 2x2 tiles of 16x16;
+// j + 16(i%4), element i/4): wave w (of the first four) adds
+// sum_t P[i][t] Q[c][t] over its 32x32 quadrant, rows 32(w/2).., columns
+// 32(w%2).., as 2x2 tiles of 16x16;
 // acc[a][b][v] is element (32(w/2) + 16a + lane/16 + 4v,
 // 32(w%2) + 16b + lane%16) (tile_row / tile_col below).
 __device__ __forceinline__ void gemm_nt_64(const double (*P)[LDP], const double (*Q)[LDP],
@@ -409,8 +414,9 @@ __global__ __launch_bounds__(256) void k_panel(double* __restrict__ A, double* _
 // before this step writes them). Tile 0 is the next diagonal block,
 // factored and inverted right after its update (L into A, L^{-1} into W's
 // diagonal block kb+1).
-__global__ __launch_bounds__(256) void k_update(double* __restrict__ A, double* __restrict__ W,
-                                                int nf, int kb, int* __restrict__ flag) {
+__global__ __launch_bounds__(kFactorThreads) void k_update(double* __restrict__ A,
+                                                           double* __restrict__ W, int nf,
+                                                           int kb, int* __restrict__ flag) {
   __shared__ double p[B][LDP];
   __shared__ __align__(16) double q[B][LDP];
   __shared__ __align__(16) double scr[6 * B];
@@ -422,6 +428,9 @@ __global__ __launch_bounds__(256) void k_update(double* __restrict__ A, double* 
   double* Ak = A + (int64_t)k * nf * nf;
   double* Wk = W + (int64_t)k * nf * nf;
   const int o = kb * B;
+  // eight waves (the diagonal factor's layout): the first four load and
+  // multiply the tile, all eight factor the next diagonal block
+  const bool prod = threadIdx.x < 256;
   double* dst;
   bool first_r = false;
   if (t < nsyrk) {
@@ -431,8 +440,9 @@ __global__ __launch_bounds__(256) void k_update(double* __restrict__ A, double* 
     while (r * (r + 1) / 2 > t) --r;
     const int ib = kb + 1 + r;
     const int cb = kb + 1 + (t - r * (r + 1) / 2);
-    load_blocks<false, false>(p, Ak + (int64_t)ib * B * nf + o,      // L[ib][kb]
-                              q, Ak + (int64_t)cb * B * nf + o, nf); // L[cb][kb]
+    if (prod)
+      load_blocks<false, false>(p, Ak + (int64_t)ib * B * nf + o,      // L[ib][kb]
+                                q, Ak + (int64_t)cb * B * nf + o, nf); // L[cb][kb]
     dst = Ak + (int64_t)ib * B * nf + cb * B;
   } else {
     // R tile (ib, jb): ib > kb, jb <= kb:  W[ib][jb] -= L[ib][kb] W[kb][jb]
@@ -440,44 +450,51 @@ __global__ __launch_bounds__(256) void k_update(double* __restrict__ A, double* 
     const int ib = kb + 1 + u / (kb + 1);
     const int jb = u % (kb + 1);
     first_r = (jb == kb);
-    load_blocks<false, true>(p, Ak + (int64_t)ib * B * nf + o,        // L[ib][kb]
-                             q, Wk + (int64_t)o * nf + jb * B, nf);   // q = W[kb][jb]^T
+    if (prod)
+      load_blocks<false, true>(p, Ak + (int64_t)ib * B * nf + o,        // L[ib][kb]
+                               q, Wk + (int64_t)o * nf + jb * B, nf);   // q = W[kb][jb]^T
     dst = Wk + (int64_t)ib * B * nf + jb * B;
   }
   // the tile's current values, requested before the product: the first
   // update of an R tile (jb = kb) starts from zero instead (W is not cleared
   // beforehand; its blocks above the diagonal are never read)
-  doublex4 cur[2][2];
-#pragma unroll
-  for (int a = 0; a < 2; ++a)
-#pragma unroll
-    for (int b = 0; b < 2; ++b)
-#pragma unroll
-      for (int v = 0; v < 4; ++v)
-        cur[a][b][v] = first_r ? 0.0 : dst[(int64_t)tile_row(a, v) * nf + tile_col(b)];
-  __syncthreads();
-  doublex4 acc[2][2] = {};
-  gemm_nt_64(p, q, acc);
-#pragma unroll
-  for (int a = 0; a < 2; ++a)
-#pragma unroll
-    for (int b = 0; b < 2; ++b) {
-      acc[a][b] = cur[a][b] - acc[a][b];
-      // the next diagonal tile (t = 0) is stored once, factored, below
-      if (t != 0)
-#pragma unroll
-        for (int v = 0; v < 4; ++v)
-          dst[(int64_t)tile_row(a, v) * nf + tile_col(b)] = acc[a][b][v];
-    }
-  if (t == 0) {
-    // next diagonal block: stage the updated tile, factor and invert it
-    __syncthreads();
+  doublex4 cur[2][2] = {};
+  if (prod) {
 #pragma unroll
     for (int a = 0; a < 2; ++a)
 #pragma unroll
       for (int b = 0; b < 2; ++b)
 #pragma unroll
-        for (int v = 0; v < 4; ++v) p[tile_row(a, v)][tile_col(b)] = acc[a][b][v];
+        for (int v = 0; v < 4; ++v)
+          cur[a][b][v] = first_r ? 0.0 : dst[(int64_t)tile_row(a, v) * nf + tile_col(b)];
+  }
+  __syncthreads();
+  doublex4 acc[2][2] = {};
+  if (prod) {
+    gemm_nt_64(p, q, acc);
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+      for (int b = 0; b < 2; ++b) {
+        acc[a][b] = cur[a][b] - acc[a][b];
+        // the next diagonal tile (t = 0) is stored once, factored, below
+        if (t != 0)
+#pragma unroll
+          for (int v = 0; v < 4; ++v)
+            dst[(int64_t)tile_row(a, v) * nf + tile_col(b)] = acc[a][b][v];
+      }
+  }
+  if (t == 0) {
+    // next diagonal block: stage the updated tile, factor and invert it
+    __syncthreads();
+    if (prod) {
+#pragma unroll
+      for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int b = 0; b < 2; ++b)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) p[tile_row(a, v)][tile_col(b)] = acc[a][b][v];
+    }
     __syncthreads();
     chol_inv64(p, q, scr, flag);
     const int o1 = o + B;
@@ -1021,14 +1038,14 @@ hipError_t launch_weights(const float* X, int64_t n, int d, int m, int n_pad,
 hipError_t launch_cholesky(double* A, double* W, int nf, int m, int* flag,
                            hipStream_t st) {
   const int nbk = nf / B;
-  hipLaunchKernelGGL(k_factor_first, dim3(m), dim3(256), 0, st, A, W, nf, flag);
+  hipLaunchKernelGGL(k_factor_first, dim3(m), dim3(kFactorThreads), 0, st, A, W, nf, flag);
   for (int kb = 0; kb < nbk; ++kb) {
     const int T = nbk - kb - 1;
     if (T + kb > 0)
       hipLaunchKernelGGL(k_panel, dim3(4 * (T + kb), m), dim3(256), 0, st, A, W, nf, kb);
     if (T > 0)
-      hipLaunchKernelGGL(k_update, dim3(T * (T + 1) / 2 + T * (kb + 1), m), dim3(256), 0, st,
-                         A, W, nf, kb, flag);
+      hipLaunchKernelGGL(k_update, dim3(T * (T + 1) / 2 + T * (kb + 1), m), dim3(kFactorThreads),
+                         0, st, A, W, nf, kb, flag);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
