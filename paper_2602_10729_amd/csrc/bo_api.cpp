@@ -110,7 +110,7 @@ struct DeviceState {
   // under fit_mu: a second stream (default priority) for independent work
   // inside one call, joined back by the two events
   hipStream_t side = nullptr;
-  hipEvent_t side_evt[2] = {nullptr, nullptr};
+  hipEvent_t side_evt[3] = {nullptr, nullptr, nullptr};
   // under fit_mu: the fp64 scratch of bo_fit and bo_mll, kept and grown on
   // demand (both synchronise their stream before releasing fit_mu, so none
   // of it is in use between calls): A, W [mat], hyperparameters [nhyp],
@@ -126,7 +126,7 @@ bo_status side_stream(DeviceState* DS) {
   if (DS->side) return BO_OK;
   hipError_t e = hipStreamCreateWithFlags(&DS->side, hipStreamNonBlocking);
   if (e != hipSuccess) { DS->side = nullptr; return hip_fail(e, "side stream"); }
-  for (int i = 0; i < 2; ++i) {
+  for (int i = 0; i < 3; ++i) {
     e = hipEventCreateWithFlags(&DS->side_evt[i], hipEventDisableTiming);
     if (e != hipSuccess) return hip_fail(e, "side stream event");
   }
@@ -810,23 +810,28 @@ bo_status fit_impl(const char* who, const float* X, const float* Y, int64_t n, i
     gp.s_int = gp.s_dep + m;
     gp.pref = gp.s_int + m;
   }
-  // The scaled X, its distance fragments and (composite) the preference
-  // weights depend only on X and the hyperparameters: they run on the side
-  // stream beside the factorisation, then alpha beside the fp16 pack, and
-  // the side stream joins before the read-back. (An event's later record
-  // does not change a wait already enqueued on it.)
+  // The Gram matrix past its first 64 columns, the scaled X, its distance
+  // fragments and (composite) the preference weights depend only on X and
+  // the hyperparameters: they run on the side stream beside the first
+  // diagonal block's factor and panel (the first trailing update waits for
+  // the Gram columns), then alpha beside the fp16 pack, and the side stream
+  // joins before the read-back. (An event's later record does not change a
+  // wait already enqueued on it.)
   if ((s = side_stream(DS)) != BO_OK) return bail(s);
   hipStream_t side = DS->side;
   e = hipEventRecord(DS->side_evt[0], st);
   if (e == hipSuccess) e = hipStreamWaitEvent(side, DS->side_evt[0], 0);
+  if (e != hipSuccess) return bail(hip_fail(e, "bo_fit: side stream"));
+  if ((s = after_launch(launch_gram(X, n, d, m, nf, gp, fs.A, side, fs.stats, kFitBlk, nf), side, "gram")) != BO_OK) return bail(s);
+  e = hipEventRecord(DS->side_evt[2], side);
   if (e != hipSuccess) return bail(hip_fail(e, "bo_fit: side stream"));
   if ((s = after_launch(launch_scale_x(X, n, d, m, M->nb, M->dx, dr, dr4, gp.ils, M->invls,
                                        comp ? gp.pref : nullptr, M->pref, M->Xd, M->ils64,
                                        M->Xs, side), side, "scale X")) != BO_OK) return bail(s);
   if ((s = after_launch(launch_pack_x(M->Xs, n, m, M->nb, M->dx, dr4, M->ctr, M->xf, M->x2, side), side, "pack X")) != BO_OK) return bail(s);
   if (comp && (s = after_launch(launch_weights(X, n, d, m, M->n_pad, gp, M->wts, side), side, "weights")) != BO_OK) return bail(s);
-  if ((s = after_launch(launch_gram(X, n, d, m, nf, gp, fs.A, st, fs.stats), st, "gram")) != BO_OK) return bail(s);
-  if ((s = after_launch(launch_cholesky(fs.A, fs.W, nf, m, fs.flag, st), st, "cholesky")) != BO_OK) return bail(s);
+  if ((s = after_launch(launch_gram(X, n, d, m, nf, gp, fs.A, st, fs.stats, 0, kFitBlk), st, "gram")) != BO_OK) return bail(s);
+  if ((s = after_launch(launch_cholesky(fs.A, fs.W, nf, m, fs.flag, st, DS->side_evt[2]), st, "cholesky")) != BO_OK) return bail(s);
   // alpha (and the fp64 fragments) on the side stream, the fp16 pack here
   e = hipEventRecord(DS->side_evt[0], st);
   if (e == hipSuccess) e = hipStreamWaitEvent(side, DS->side_evt[0], 0);

@@ -133,9 +133,11 @@ struct GramParams {
 // blocks) is written. A: [m][n_fit][n_fit].
 // kdiag (optional, [m], zeroed by the caller): the largest diagonal entry of
 // each objective's K, as the bit pattern of a non-negative double.
+// [col0, col1) (multiples of 16; col1 < 0: n_fit) limits the launch to those
+// columns, so the matrix can be written in parts.
 hipError_t launch_gram(const float* X, int64_t n, int d, int m, int n_fit,
                        const GramParams& g, double* A, hipStream_t st,
-                       unsigned long long* kdiag = nullptr);
+                       unsigned long long* kdiag = nullptr, int col0 = 0, int col1 = -1);
 // Composite: wts[k][i] = fp32(exp(sum_j pref[k][j] X[i][dr + j])), 0 for
 // n <= i < n_pad.
 hipError_t launch_weights(const float* X, int64_t n, int d, int m, int n_pad,
@@ -144,8 +146,12 @@ hipError_t launch_weights(const float* X, int64_t n, int d, int m, int n_pad,
 // also leaves W = L^{-1} in W's lower 64-blocks ([m][nf][nf]; W needs no
 // initial contents, its blocks above the diagonal are left as they were).
 // *flag is set non-zero on a non-positive or non-finite pivot.
+// before_update (optional): an event the stream waits for after the first
+// diagonal block and its panel and before the first trailing update (which
+// reads the columns past the first 64), so that those columns may still be
+// in production on another stream when this is called.
 hipError_t launch_cholesky(double* A, double* W, int nf, int m, int* flag,
-                           hipStream_t st);
+                           hipStream_t st, hipEvent_t before_update = nullptr);
 // alpha_k = W_k^T (W_k y_k), y from Y [n][m] (fp32), written fp32 [m][n_pad]
 // (and, when alpha64 is not NULL, fp64 [m][nf]). tmp [m][nf] keeps W_k y_k.
 hipError_t launch_alpha(const double* W, const float* Y, int64_t n, int m,

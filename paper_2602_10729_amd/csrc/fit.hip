@@ -60,12 +60,12 @@ __device__ inline double matern32_d(double r2) {
 //                  + s_int M52(r_route) M32(r_dep)
 __global__ __launch_bounds__(256) void k_gram(const float* __restrict__ X, int64_t n, int d,
                                               int nf, GramParams g, double* __restrict__ A,
-                                              unsigned long long* __restrict__ kdiag) {
+                                              unsigned long long* __restrict__ kdiag, int bj0) {
   __shared__ float xs[2][16][BO_MAX_D + 1];
   __shared__ double il[BO_MAX_D];
   __shared__ double wrow[2][16];
   const int k = blockIdx.z;
-  const int bi = blockIdx.y, bj = blockIdx.x;      // 16x16 tiles
+  const int bi = blockIdx.y, bj = bj0 + blockIdx.x;   // 16x16 tiles from tile column bj0
   if ((bj >> 2) > (bi >> 2)) return;                // strictly above the 64-block diagonal
   const int tid = threadIdx.y * 16 + threadIdx.x;
   // rows bi*16.. (s = 0) and bj*16.. (s = 1); rows past n read as 0
@@ -1022,9 +1022,12 @@ __global__ __launch_bounds__(256) void k_trmm(const double* __restrict__ T,
 
 hipError_t launch_gram(const float* X, int64_t n, int d, int m, int n_fit,
                        const GramParams& g, double* A, hipStream_t st,
-                       unsigned long long* kdiag) {
-  dim3 grid((n_fit + 15) / 16, (n_fit + 15) / 16, m), block(16, 16);
-  hipLaunchKernelGGL(k_gram, grid, block, 0, st, X, n, d, n_fit, g, A, kdiag);
+                       unsigned long long* kdiag, int col0, int col1) {
+  if (col1 < 0) col1 = n_fit;
+  if (col0 % 16 != 0 || col1 % 16 != 0 || col0 < 0 || col1 > n_fit) return hipErrorInvalidValue;
+  if (col1 <= col0) return hipSuccess;
+  dim3 grid((col1 - col0) / 16, (n_fit + 15) / 16, m), block(16, 16);
+  hipLaunchKernelGGL(k_gram, grid, block, 0, st, X, n, d, n_fit, g, A, kdiag, col0 / 16);
   return hipGetLastError();
 }
 
@@ -1036,13 +1039,17 @@ hipError_t launch_weights(const float* X, int64_t n, int d, int m, int n_pad,
 }
 
 hipError_t launch_cholesky(double* A, double* W, int nf, int m, int* flag,
-                           hipStream_t st) {
+                           hipStream_t st, hipEvent_t before_update) {
   const int nbk = nf / B;
   hipLaunchKernelGGL(k_factor_first, dim3(m), dim3(kFactorThreads), 0, st, A, W, nf, flag);
   for (int kb = 0; kb < nbk; ++kb) {
     const int T = nbk - kb - 1;
     if (T + kb > 0)
       hipLaunchKernelGGL(k_panel, dim3(4 * (T + kb), m), dim3(256), 0, st, A, W, nf, kb);
+    if (kb == 0 && before_update) {
+      hipError_t e = hipStreamWaitEvent(st, before_update, 0);
+      if (e != hipSuccess) return e;
+    }
     if (T > 0)
       hipLaunchKernelGGL(k_update, dim3(T * (T + 1) / 2 + T * (kb + 1), m), dim3(kFactorThreads),
                          0, st, A, W, nf, kb, flag);
