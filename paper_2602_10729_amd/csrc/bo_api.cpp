@@ -114,7 +114,8 @@ struct DeviceState {
   // under fit_mu: the fp64 scratch of bo_fit and bo_mll, kept and grown on
   // demand (both synchronise their stream before releasing fit_mu, so none
   // of it is in use between calls): A, W [mat], hyperparameters [nhyp],
-  // vector [vec], then 64 bytes of flag (int) and statistics (at byte 16)
+  // vector [vec], then 64 bytes of flag (int) and statistics (at byte 16),
+  // then the row-block maxima [3][BO_MAX_N / 16] (kFitSmall bytes in all)
   double* fw = nullptr;
   size_t fw_mat = 0, fw_hyp = 0, fw_vec = 0;
   // under fit_mu: marks bo_fit's early read-back of Y
@@ -212,6 +213,7 @@ struct FitScratch {
   double* tmp = nullptr;
   int* flag = nullptr;
   unsigned long long* stats = nullptr;   // [2m]: max K_ii, then max |L^{-1}| (double bits)
+  unsigned long long* bmax = nullptr;    // [m][nb]: row-block maxima of |L^{-1}| (kept scratch)
   ~FitScratch() {
     if (!own) return;
     pfree(A, st); pfree(W, st); pfree(hyp, st); pfree(tmp, st); pfree(flag, st);
@@ -249,6 +251,10 @@ void release_buffers(Model* M) {
   pfree(M->d_boxes, nullptr);
 }
 
+// Bytes after the fit scratch's vector: flag and statistics (64), then the
+// row-block maxima of |L^{-1}| for up to three objectives.
+constexpr size_t kFitSmall = 64 + sizeof(unsigned long long) * 3 * (BO_MAX_N / kBlk);
+
 // The device's kept fit scratch, grown to at least the given sizes (the
 // caller holds DS->fit_mu). Growing waits for the device, then replaces the
 // buffer.
@@ -263,7 +269,7 @@ bo_status fit_work(DeviceState* DS, size_t mat, size_t nhyp, size_t vec, FitScra
       DS->fw_mat = DS->fw_hyp = DS->fw_vec = 0;
     }
     void* q = nullptr;
-    hipError_t e = hipMalloc(&q, sizeof(double) * (2 * m2 + h2 + v2) + 64);
+    hipError_t e = hipMalloc(&q, sizeof(double) * (2 * m2 + h2 + v2) + kFitSmall);
     if (e != hipSuccess) {
       (void)hipGetLastError();
       return fail(BO_ERR_OUT_OF_MEMORY, "device allocation failed for the fit scratch");
@@ -278,6 +284,7 @@ bo_status fit_work(DeviceState* DS, size_t mat, size_t nhyp, size_t vec, FitScra
   fs->tmp = fs->hyp + DS->fw_hyp;
   fs->flag = reinterpret_cast<int*>(fs->tmp + DS->fw_vec);
   fs->stats = reinterpret_cast<unsigned long long*>(fs->tmp + DS->fw_vec + 2);
+  fs->bmax = reinterpret_cast<unsigned long long*>(fs->tmp + DS->fw_vec + 8);
   return BO_OK;
 }
 
@@ -791,7 +798,7 @@ bo_status fit_impl(const char* who, const float* X, const float* Y, int64_t n, i
   // the fp32 inverse lengthscales and preference slopes, and the copy of X,
   // are written on the device from these (k_scale_x)
   e = hipMemcpyAsync(fs.hyp, stage, sizeof(double) * hyp.size(), hipMemcpyHostToDevice, st);
-  if (e == hipSuccess) e = hipMemsetAsync(fs.flag, 0, 64, st);   // flag and statistics
+  if (e == hipSuccess) e = hipMemsetAsync(fs.flag, 0, kFitSmall, st);   // flag, statistics, maxima
   // Y comes back first, so that its finiteness check and the front run on
   // the host while the device factors
   if (e == hipSuccess && !DS->fit_evt) e = hipEventCreateWithFlags(&DS->fit_evt, hipEventDisableTiming);
@@ -840,7 +847,7 @@ bo_status fit_impl(const char* who, const float* X, const float* Y, int64_t n, i
   if (f64 && (s = after_launch(launch_pack_f64(fs.W, n, m, nf, M->nb, M->Lp64, side), side, "pack fp64")) != BO_OK) return bail(s);
   e = hipEventRecord(DS->side_evt[1], side);
   if (e != hipSuccess) return bail(hip_fail(e, "bo_fit: side stream"));
-  if ((s = after_launch(launch_pack_factor(fs.W, n, m, nf, M->nb, M->Lp, fs.stats + m, fs.flag, st), st, "pack")) != BO_OK) return bail(s);
+  if ((s = after_launch(launch_pack_factor(fs.W, n, m, nf, M->nb, M->Lp, fs.stats + m, fs.flag, st, fs.bmax), st, "pack")) != BO_OK) return bail(s);
   e = hipStreamWaitEvent(st, DS->side_evt[1], 0);
   if (e != hipSuccess) return bail(hip_fail(e, "bo_fit: side stream"));
 

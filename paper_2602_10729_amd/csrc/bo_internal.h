@@ -212,8 +212,12 @@ hipError_t launch_trmm(bool trans, const double* T, const double* Bm, double* C,
 // by the nb inverse scales (packed_factor_floats(nb) floats per objective;
 // wmax [m] = largest |W| per objective as a non-negative double's bit
 // pattern, zeroed by the caller; *flag set on a non-finite entry).
+// bmax (optional, [m][nb], zeroed by the caller): the row-block maxima are
+// gathered there by column chunks (more workgroups, for the fit's critical
+// path) and the pack derives the scales from them.
 hipError_t launch_pack_factor(const double* W, int64_t n, int m, int nf, int nb, float* Lp,
-                              unsigned long long* wmax, int* flag, hipStream_t st);
+                              unsigned long long* wmax, int* flag, hipStream_t st,
+                              unsigned long long* bmax = nullptr);
 
 // Noisy acquisition kernels (nehvi.hip).
 struct NehviFrontArgs {

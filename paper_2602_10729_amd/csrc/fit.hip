@@ -608,6 +608,47 @@ __global__ __launch_bounds__(256) void k_rowblock_scale(const double* __restrict
   }
 }
 
+// The same row-block maxima spread over column chunks: workgroup (I, c, k)
+// takes columns 256c .. 256c+255 of row block I's lower entries and merges
+// its largest |W| into bmax[k][I] (bit pattern of a non-negative double,
+// zeroed by the caller); a non-finite entry sets *flag.
+__global__ __launch_bounds__(256) void k_rowblock_max(const double* __restrict__ W, int64_t n,
+                                                      int nf, int nb,
+                                                      unsigned long long* __restrict__ bmax,
+                                                      int* __restrict__ flag) {
+  __shared__ double part[4];
+  const int I = blockIdx.x, k = blockIdx.z;
+  const int64_t lim = (int64_t)I * kBlk + kBlk;
+  const int64_t ncol = (lim < n) ? lim : n;
+  const int64_t col = (int64_t)blockIdx.y * 256 + threadIdx.x;
+  if ((int64_t)blockIdx.y * 256 >= ncol) return;          // the whole workgroup
+  const double* Wk = W + (int64_t)k * nf * nf;
+  double mx = 0.0;
+  bool bad = false;
+  if (col < ncol) {
+    double v[kBlk];
+#pragma unroll
+    for (int r = 0; r < kBlk; ++r) {
+      const int64_t row = (int64_t)I * kBlk + r;
+      v[r] = (row < n && col <= row) ? Wk[row * nf + col] : 0.0;
+    }
+#pragma unroll
+    for (int r = 0; r < kBlk; ++r) {
+      bad = bad || !(fabs(v[r]) < INFINITY);
+      mx = fmax(mx, fabs(v[r]));
+    }
+  }
+  if (bad) *flag = 1;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) mx = fmax(mx, __shfl_xor(mx, o));
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = mx;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const double m = fmax(fmax(part[0], part[1]), fmax(part[2], part[3]));
+    atomicMax(bmax + (int64_t)k * nb + I, static_cast<unsigned long long>(__double_as_longlong(m)));
+  }
+}
+
 // Pack the lower triangle of W = L^{-1} as fp16 hi/lo MFMA A fragments of
 // 16-row x 32-column blocks (the scoring path's operand format):
 // row block I holds the blocks J = 0 .. I/2, block (I, J) at index
@@ -619,8 +660,10 @@ __global__ __launch_bounds__(256) void k_rowblock_scale(const double* __restrict
 // hi = fp16(w), lo = fp16(w - hi).
 __global__ __launch_bounds__(256) void k_pack(const double* __restrict__ W, int64_t n,
                                               int nf, int64_t nblk, int nb,
-                                              const float* __restrict__ rsc, int64_t stride,
-                                              _Float16* __restrict__ Lp) {
+                                              float* __restrict__ rsc, int64_t stride,
+                                              _Float16* __restrict__ Lp,
+                                              const unsigned long long* __restrict__ bmax,
+                                              unsigned long long* __restrict__ wmax) {
   const int k = blockIdx.y;
   const int64_t g = (int64_t)blockIdx.x * 256 + threadIdx.x;   // (blk, lane)
   if (g >= nblk * 64) return;
@@ -640,8 +683,26 @@ __global__ __launch_bounds__(256) void k_pack(const double* __restrict__ W, int6
   }
   const int64_t row = (int64_t)I * kBlk + lane % 16;
   const double* Wk = W + (int64_t)k * nf * nf;
-  // the zero block (I = nb) has no scale
-  const double sc = (I < nb) ? 1.0 / static_cast<double>(rsc[(int64_t)k * stride + I]) : 1.0;
+  // the zero block (I = nb) has no scale; with bmax the scale of row block I
+  // is taken here from its maximum (the first block of the row stores it)
+  float rs = 1.0f;
+  if (I < nb) {
+    if (bmax) {
+      const double mI = __longlong_as_double(static_cast<long long>(bmax[(int64_t)k * nb + I]));
+      int E = 0;
+      if (mI > 0.0) (void)frexp(mI, &E);
+      rs = ldexpf(1.0f, E - 14);
+      if (J == 0 && lane == 0) {
+        rsc[(int64_t)k * stride + I] = rs;
+        atomicMax(wmax + k, static_cast<unsigned long long>(__double_as_longlong(mI)));
+      }
+    } else {
+      rs = rsc[(int64_t)k * stride + I];
+    }
+  } else if (bmax && lane == 0) {
+    rsc[(int64_t)k * stride + nb] = 0.f;      // entry nb: past the matrix
+  }
+  const double sc = (I < nb) ? 1.0 / static_cast<double>(rs) : 1.0;
   _Float16 hi[8], lo[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
@@ -1139,15 +1200,23 @@ hipError_t launch_trmm(bool trans, const double* T, const double* Bm, double* C,
 }
 
 hipError_t launch_pack_factor(const double* W, int64_t n, int m, int nf, int nb, float* Lp,
-                              unsigned long long* wmax, int* flag, hipStream_t st) {
+                              unsigned long long* wmax, int* flag, hipStream_t st,
+                              unsigned long long* bmax) {
   const int64_t nblk = posterior_frag_blocks(nb);   // with the zero block
   const int64_t stride = static_cast<int64_t>(packed_factor_floats(nb));
   float* rsc = Lp + nblk * 512;                     // objective k's scales at rsc + k * stride
-  hipLaunchKernelGGL(k_rowblock_scale, dim3(nb, m), dim3(256), 0, st, W, n, nf, rsc, stride, wmax,
-                     flag);
+  if (bmax) {
+    const unsigned nch = static_cast<unsigned>((n + 255) / 256);
+    hipLaunchKernelGGL(k_rowblock_max, dim3(nb, nch, m), dim3(256), 0, st, W, n, nf, nb, bmax,
+                       flag);
+  } else {
+    hipLaunchKernelGGL(k_rowblock_scale, dim3(nb, m), dim3(256), 0, st, W, n, nf, rsc, stride,
+                       wmax, flag);
+  }
   const unsigned gx = static_cast<unsigned>((nblk * 64 + 255) / 256);
   hipLaunchKernelGGL(k_pack, dim3(gx, m), dim3(256), 0, st, W, n, nf, nblk, nb, rsc, stride,
-                     reinterpret_cast<_Float16*>(Lp));
+                     reinterpret_cast<_Float16*>(Lp), static_cast<const unsigned long long*>(bmax),
+                     wmax);
   return hipGetLastError();
 }
 
