@@ -829,16 +829,19 @@ bo_status fit_impl(const char* who, const float* X, const float* Y, int64_t n, i
   e = hipEventRecord(DS->side_evt[0], st);
   if (e == hipSuccess) e = hipStreamWaitEvent(side, DS->side_evt[0], 0);
   if (e != hipSuccess) return bail(hip_fail(e, "bo_fit: side stream"));
+  // enqueued in the order the device should start them: the critical chain
+  // first (the first block column of the Gram matrix, then the factor,
+  // which waits for the rest of the Gram matrix before its first update)
+  if ((s = after_launch(launch_gram(X, n, d, m, nf, gp, fs.A, st, fs.stats, 0, kFitBlk), st, "gram")) != BO_OK) return bail(s);
   if ((s = after_launch(launch_gram(X, n, d, m, nf, gp, fs.A, side, fs.stats, kFitBlk, nf), side, "gram")) != BO_OK) return bail(s);
   e = hipEventRecord(DS->side_evt[2], side);
   if (e != hipSuccess) return bail(hip_fail(e, "bo_fit: side stream"));
+  if ((s = after_launch(launch_cholesky(fs.A, fs.W, nf, m, fs.flag, st, DS->side_evt[2]), st, "cholesky")) != BO_OK) return bail(s);
   if ((s = after_launch(launch_scale_x(X, n, d, m, M->nb, M->dx, dr, dr4, gp.ils, M->invls,
                                        comp ? gp.pref : nullptr, M->pref, M->Xd, M->ils64,
                                        M->Xs, side), side, "scale X")) != BO_OK) return bail(s);
   if ((s = after_launch(launch_pack_x(M->Xs, n, m, M->nb, M->dx, dr4, M->ctr, M->xf, M->x2, side), side, "pack X")) != BO_OK) return bail(s);
   if (comp && (s = after_launch(launch_weights(X, n, d, m, M->n_pad, gp, M->wts, side), side, "weights")) != BO_OK) return bail(s);
-  if ((s = after_launch(launch_gram(X, n, d, m, nf, gp, fs.A, st, fs.stats, 0, kFitBlk), st, "gram")) != BO_OK) return bail(s);
-  if ((s = after_launch(launch_cholesky(fs.A, fs.W, nf, m, fs.flag, st, DS->side_evt[2]), st, "cholesky")) != BO_OK) return bail(s);
   // alpha (and the fp64 fragments) on the side stream, the fp16 pack here
   e = hipEventRecord(DS->side_evt[0], st);
   if (e == hipSuccess) e = hipStreamWaitEvent(side, DS->side_evt[0], 0);
