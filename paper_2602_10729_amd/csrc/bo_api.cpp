@@ -114,8 +114,9 @@ struct DeviceState {
   // under fit_mu: the fp64 scratch of bo_fit and bo_mll, kept and grown on
   // demand (both synchronise their stream before releasing fit_mu, so none
   // of it is in use between calls): A, W [mat], hyperparameters [nhyp],
-  // vector [vec], then 64 bytes of flag (int) and statistics (at byte 16),
-  // then the row-block maxima [3][BO_MAX_N / 16] (kFitSmall bytes in all)
+  // vector [vec], hyperparameters [nhyp], then 64 bytes of flag (int) and
+  // statistics (at byte 16), then the row-block maxima [3][BO_MAX_N / 16]
+  // (kFitSmall bytes in all)
   double* fw = nullptr;
   size_t fw_mat = 0, fw_hyp = 0, fw_vec = 0;
   // under fit_mu: marks bo_fit's early read-back of Y
@@ -214,6 +215,7 @@ struct FitScratch {
   int* flag = nullptr;
   unsigned long long* stats = nullptr;   // [2m]: max K_ii, then max |L^{-1}| (double bits)
   unsigned long long* bmax = nullptr;    // [m][nb]: row-block maxima of |L^{-1}| (kept scratch)
+  size_t hyp_cap = 0;                    // kept scratch: doubles from hyp to flag
   ~FitScratch() {
     if (!own) return;
     pfree(A, st); pfree(W, st); pfree(hyp, st); pfree(tmp, st); pfree(flag, st);
@@ -241,7 +243,7 @@ void release_noisy(Model* M) {
 
 void release_buffers(Model* M) {
   release_noisy(M);
-  if (M->arena || M->ws || M->d_boxes) (void)hipDeviceSynchronize();
+  if ((M->arena && M->pending) || M->ws || M->d_boxes) (void)hipDeviceSynchronize();
   pfree(M->arena, nullptr);
   M->Lp64 = nullptr; M->alpha64 = nullptr; M->ils64 = nullptr;
   M->xf = nullptr; M->x2 = nullptr; M->ctr = nullptr; M->Xd = nullptr;
@@ -277,14 +279,17 @@ bo_status fit_work(DeviceState* DS, size_t mat, size_t nhyp, size_t vec, FitScra
     DS->fw = static_cast<double*>(q);
     DS->fw_mat = m2; DS->fw_hyp = h2; DS->fw_vec = v2;
   }
+  // [A][W][vector][hyperparameters][flag, statistics, maxima]: the last two
+  // are contiguous, so one upload sets both
   fs->own = false;
   fs->A = DS->fw;
   fs->W = fs->A + DS->fw_mat;
-  fs->hyp = fs->W + DS->fw_mat;
-  fs->tmp = fs->hyp + DS->fw_hyp;
-  fs->flag = reinterpret_cast<int*>(fs->tmp + DS->fw_vec);
-  fs->stats = reinterpret_cast<unsigned long long*>(fs->tmp + DS->fw_vec + 2);
-  fs->bmax = reinterpret_cast<unsigned long long*>(fs->tmp + DS->fw_vec + 8);
+  fs->tmp = fs->W + DS->fw_mat;
+  fs->hyp = fs->tmp + DS->fw_vec;
+  fs->hyp_cap = DS->fw_hyp;
+  fs->flag = reinterpret_cast<int*>(fs->hyp + DS->fw_hyp);
+  fs->stats = reinterpret_cast<unsigned long long*>(fs->hyp + DS->fw_hyp + 2);
+  fs->bmax = reinterpret_cast<unsigned long long*>(fs->hyp + DS->fw_hyp + 8);
   return BO_OK;
 }
 
@@ -436,6 +441,7 @@ double bits_to_double(unsigned long long b) {
 // another stream) and records an event at its end, so a call never rewrites
 // the boxes or the workspace while an earlier call may still read them.
 bo_status order_after_previous(Model& M, hipStream_t st, const char* who) {
+  M.pending = true;
   if (M.last_evt && M.last_stream != st) {
     hipError_t e = hipStreamWaitEvent(st, M.last_evt, 0);
     if (e != hipSuccess) return hip_fail(e, who);
@@ -443,6 +449,7 @@ bo_status order_after_previous(Model& M, hipStream_t st, const char* who) {
   return BO_OK;
 }
 bo_status mark_call(Model& M, hipStream_t st, const char* who) {
+  M.pending = true;
   if (!M.last_evt) {
     hipError_t e = hipEventCreateWithFlags(&M.last_evt, hipEventDisableTiming);
     if (e != hipSuccess) {
@@ -737,6 +744,7 @@ bo_status fit_impl(const char* who, const float* X, const float* Y, int64_t n, i
     o_pf = lay.add(sizeof(float) * m * dc);
   }
   if ((s = palloc(&M->arena, lay.total, st, "model buffers")) != BO_OK) return bail(s);
+  M->pending = true;   // until the fit's work is known to be complete
   {
     unsigned char* b = M->arena;
     M->Xs = reinterpret_cast<float*>(b + o_xs);
@@ -772,16 +780,19 @@ bo_status fit_impl(const char* who, const float* X, const float* Y, int64_t n, i
   if (comp)
     for (size_t i = 0; i < (size_t)m * dc; ++i) hyp[(size_t)m * d + 4 * m + i] = comp->pref[i];
 
-  // pinned staging: [hyperparameters (fp64)][flag, statistics (64 bytes)][Y]
+  // pinned staging mirrors the device scratch from the hyperparameters on:
+  // [hyperparameters, zero padding to hyp_cap][flag, statistics, maxima
+  // (zeros going up; flag and statistics come back here)][Y]
   DeviceState* DS = device_state(M->device);
   if (!DS) return bail(fail(BO_ERR_DEVICE, W + ": device index out of range"));
   std::lock_guard<std::mutex> stage_lock(DS->fit_mu);
   FitScratch fs;
   fs.st = st;
   if ((s = fit_work(DS, (size_t)m * nf * nf, nhyp, (size_t)m * nf, &fs)) != BO_OK) return bail(s);
-  const size_t off_flag = (sizeof(double) * hyp.size() + 15) / 16 * 16;
+  const size_t off_flag = sizeof(double) * fs.hyp_cap;
   const size_t off_stats = off_flag + 16;
-  const size_t off_y = off_flag + 64;
+  const size_t up_bytes = off_flag + kFitSmall;
+  const size_t off_y = (up_bytes + 15) / 16 * 16;
   const size_t need = off_y + sizeof(float) * n * m;
   hipError_t e = hipSuccess;
   if (need > DS->fit_stage_bytes) {
@@ -795,10 +806,11 @@ bo_status fit_impl(const char* who, const float* X, const float* Y, int64_t n, i
   }
   unsigned char* stage = DS->fit_stage;
   std::memcpy(stage, hyp.data(), sizeof(double) * hyp.size());
+  std::memset(stage + sizeof(double) * hyp.size(), 0, up_bytes - sizeof(double) * hyp.size());
   // the fp32 inverse lengthscales and preference slopes, and the copy of X,
-  // are written on the device from these (k_scale_x)
-  e = hipMemcpyAsync(fs.hyp, stage, sizeof(double) * hyp.size(), hipMemcpyHostToDevice, st);
-  if (e == hipSuccess) e = hipMemsetAsync(fs.flag, 0, kFitSmall, st);   // flag, statistics, maxima
+  // are written on the device from these (k_scale_x); the flag, statistics
+  // and maxima start at zero
+  e = hipMemcpyAsync(fs.hyp, stage, up_bytes, hipMemcpyHostToDevice, st);
   // Y comes back first, so that its finiteness check and the front run on
   // the host while the device factors
   if (e == hipSuccess && !DS->fit_evt) e = hipEventCreateWithFlags(&DS->fit_evt, hipEventDisableTiming);
@@ -866,6 +878,7 @@ bo_status fit_impl(const char* who, const float* X, const float* Y, int64_t n, i
   host_front<float>(M->Yh.data(), n, m, nullptr, M->nd);
   e = hipStreamSynchronize(st);
   if (e != hipSuccess) return bail(hip_fail(e, "bo_fit: sync"));
+  M->pending = false;   // every kernel of the fit has finished
   int flag = 0;
   std::memcpy(&flag, stage + off_flag, sizeof(int));
   if (flag)
@@ -1249,6 +1262,7 @@ bo_status nehvi_prepare_impl(bo_model model, const float* ZX, int32_t S, const f
   if (m == 3 && nehvi_front3_lds_bytes(n) > kLdsLimit)
     return fail(BO_ERR_CAPACITY, W_ + ": n beyond the front kernel's LDS");
   hipStream_t st = static_cast<hipStream_t>(stream);
+  M.pending = true;   // its launches read the model's buffers
   const int nf = static_cast<int>((n + kFitBlk - 1) / kFitBlk) * kFitBlk;
   const int Sp = nehvi_padded_samples(S);
   const int n32 = static_cast<int>((n + 31) / 32);

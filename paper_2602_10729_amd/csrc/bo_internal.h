@@ -59,6 +59,10 @@ struct Model {
   // one device allocation holds every buffer the fit writes (Xs .. ils64,
   // wts, pref below are views into it)
   unsigned char* arena = nullptr;
+  // device work that reads the model's buffers may be pending (set while the
+  // fit runs and by every call that uses the model; cleared when the fit has
+  // synchronised): releasing then waits for the device first
+  bool pending = false;
   float* Xs = nullptr;           // [m][n_pad][dx] X / lengthscale (fp32)
   float* invls = nullptr;        // [m][dx] 1 / lengthscale (fp32, 0-padded)
   float* alpha = nullptr;        // [m][n_pad]
