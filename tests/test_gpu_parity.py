@@ -142,6 +142,19 @@ def test_small_models_and_odd_shapes():
         assert_close(g["ehvi"], o["ehvi"], TOL_EHVI, f"ehvi n={n} d={d}")
 
 
+def test_ragged_three_objective_fit():
+    """n = 700 (11 fit blocks, a padded tail in the last one) with three
+    objectives and q = 4: the Gram matrix in two column parts, the padded
+    rows of the factor and of the row-block scales, element by element."""
+    for seed in (0, 1):
+        _announce("ragged m=3", seed)
+        wl = bi.make_config(4, seed=seed, M=37)
+        wl.X, wl.Y, wl.n = wl.X[:700].copy(), wl.Y[:700].copy(), 700
+        g = gpu_run(wl)
+        o = oracle_score(oracle_fit(wl), wl)
+        _full_parity(wl, g, o)
+
+
 def _m52_root(target):
     """Distance r with (1 + sqrt5 r + 5 r^2 / 3) exp(-sqrt5 r) = target (fp64
     bisection; the correlation falls monotonically in r)."""
