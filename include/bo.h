@@ -129,7 +129,9 @@ typedef enum {
  * joined back into the caller's stream before return. Concurrent fits on one
  * device share a pinned staging buffer and run one at a time.
  * Memory: the model's device buffers are one allocation from a stream-ordered
- * pool; the fp64 factorisation scratch (2 m n_f^2 doubles with n_f the
+ * pool (bo_free keeps the largest released one per device, once no work on it
+ * is pending, and the next fit reuses it when it is large enough); the fp64
+ * factorisation scratch (2 m n_f^2 doubles with n_f the
  * multiple of 64 at or above n, plus a few KB) is kept per device after the
  * first fit and reused, growing when a larger fit needs more (at most 201 MB,
  * at n = 2048, m = 3), until the process ends.

@@ -101,6 +101,10 @@ bool all_finite(const float* v, size_t n) {
 struct DeviceState {
   std::mutex mu;
   hipMemPool_t pool = nullptr;
+  // under mu: one released model allocation kept for the next fit (nothing
+  // pending on it), so a fit-score-release loop neither frees nor allocates
+  unsigned char* spare = nullptr;
+  size_t spare_bytes = 0;
   float* stage = nullptr;
   size_t stage_floats = 0;
   hipEvent_t stage_evt = nullptr;
@@ -244,7 +248,23 @@ void release_noisy(Model* M) {
 void release_buffers(Model* M) {
   release_noisy(M);
   if ((M->arena && M->pending) || M->ws || M->d_boxes) (void)hipDeviceSynchronize();
-  pfree(M->arena, nullptr);
+  if (M->arena) {
+    // nothing reads the allocation any more: keep the larger of it and the
+    // device's spare for the next fit, free the other
+    DeviceState* DS = device_state(M->device);
+    unsigned char* drop = M->arena;
+    if (DS) {
+      std::lock_guard<std::mutex> lk(DS->mu);
+      if (M->arena_bytes > DS->spare_bytes) {
+        drop = DS->spare;
+        DS->spare = M->arena;
+        DS->spare_bytes = M->arena_bytes;
+      }
+    }
+    pfree(drop, nullptr);
+    M->arena = nullptr;
+    M->arena_bytes = 0;
+  }
   M->Lp64 = nullptr; M->alpha64 = nullptr; M->ils64 = nullptr;
   M->xf = nullptr; M->x2 = nullptr; M->ctr = nullptr; M->Xd = nullptr;
   M->Xs = nullptr; M->invls = nullptr; M->alpha = nullptr; M->Lp = nullptr;
@@ -743,7 +763,22 @@ bo_status fit_impl(const char* who, const float* X, const float* Y, int64_t n, i
     o_wt = lay.add(sizeof(float) * m * M->n_pad);
     o_pf = lay.add(sizeof(float) * m * dc);
   }
-  if ((s = palloc(&M->arena, lay.total, st, "model buffers")) != BO_OK) return bail(s);
+  {
+    // the device's spare allocation when it is large enough, else a new one
+    DeviceState* DSa = device_state(M->device);
+    if (!DSa) return bail(fail(BO_ERR_DEVICE, W + ": device index out of range"));
+    std::lock_guard<std::mutex> lk(DSa->mu);
+    if (DSa->spare && DSa->spare_bytes >= lay.total) {
+      M->arena = DSa->spare;
+      M->arena_bytes = DSa->spare_bytes;
+      DSa->spare = nullptr;
+      DSa->spare_bytes = 0;
+    }
+  }
+  if (!M->arena) {
+    if ((s = palloc(&M->arena, lay.total, st, "model buffers")) != BO_OK) return bail(s);
+    M->arena_bytes = lay.total;
+  }
   M->pending = true;   // until the fit's work is known to be complete
   {
     unsigned char* b = M->arena;

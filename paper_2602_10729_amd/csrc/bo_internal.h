@@ -59,6 +59,7 @@ struct Model {
   // one device allocation holds every buffer the fit writes (Xs .. ils64,
   // wts, pref below are views into it)
   unsigned char* arena = nullptr;
+  size_t arena_bytes = 0;
   // device work that reads the model's buffers may be pending (set while the
   // fit runs and by every call that uses the model; cleared when the fit has
   // synchronised): releasing then waits for the device first
