@@ -196,12 +196,12 @@ __device__ __forceinline__ void prod_load(Producer<NT, DX4, COMP>& P, int n_pad,
   if constexpr (COMP) P.wt = __builtin_bit_cast(floatx4, load4(P.wt_rs, row * 4, 0));
 }
 
-// Evaluate this lane's four rows of block jb (operands loaded by prod_load)
-// into the ring as fp16 hi/lo planes. ctile: the tile's exact scaled
-// candidate coordinates [NT][D].
+// Squared scaled distances of this lane's four rows of block jb (operands
+// loaded by prod_load). ctile: the tile's exact scaled candidate coordinates
+// [NT][D]. Reads the operands' distance part only (xa, x2).
 template <int NT, int DX4, bool COMP>
-__device__ __forceinline__ void produce(Producer<NT, DX4, COMP>& P, const PosteriorArgs& a, int jb,
-                                        const float* ctile, _Float16* ring) {
+__device__ __forceinline__ void produce_dist(Producer<NT, DX4, COMP>& P, const PosteriorArgs& a, int jb,
+                                             const float* ctile, float (&r2)[Producer<NT, DX4, COMP>::NS][4]) {
   using Pr = Producer<NT, DX4, COMP>;
   constexpr int NS = Pr::NS, F0 = Pr::F0, NF = Pr::NF;
   floatx4 d0[NS], d1[NS];
@@ -216,7 +216,6 @@ __device__ __forceinline__ void produce(Producer<NT, DX4, COMP>& P, const Poster
     for (int f = F0; f < NF; ++f)
       d1[g] = __builtin_amdgcn_mfma_f32_16x16x32_f16(P.xa[f], P.cb[g][f], d1[g], 0, 0, 0);
   }
-  float r2[NS][4];
   bool ex[4];
   bool any = false;
 #pragma unroll
@@ -263,6 +262,15 @@ __device__ __forceinline__ void produce(Producer<NT, DX4, COMP>& P, const Poster
       }
     }
   }
+}
+
+// Kernel values of this lane's four rows of block jb from their squared
+// distances, alpha and (composite) weights, into the ring as fp16 hi/lo
+// planes; adds them into mu.
+template <int NT, int DX4, bool COMP>
+__device__ __forceinline__ void produce_kv(Producer<NT, DX4, COMP>& P, const PosteriorArgs& a, int jb,
+                                           const float (&r2)[Producer<NT, DX4, COMP>::NS][4],
+                                           const floatx4& al, const floatx4& wt, _Float16* ring) {
   halfx4 hi, lo;
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
@@ -275,7 +283,7 @@ __device__ __forceinline__ void produce(Producer<NT, DX4, COMP>& P, const Poster
       // s_route M52(r_route) + s_dep w* w_i M32(r_dep) + s_int M52 M32
       const float k5 = matern52_f(r2[0][e], 1.0f);
       const float k3 = matern32_f(r2[1][e]);
-      kv = fmaf(P.wsd * P.wt[e], k3, k5 * fmaf(P.sis, k3, P.ss));
+      kv = fmaf(P.wsd * wt[e], k3, k5 * fmaf(P.sis, k3, P.ss));
     } else {
       kv = matern52_f(r2[0][e], a.ss);
     }
@@ -283,9 +291,10 @@ __device__ __forceinline__ void produce(Producer<NT, DX4, COMP>& P, const Poster
     // last product into the fp16 conversions and derive the high half twice
     // (once exactly, once from the fp32 value); within an fp32 ulp of an
     // fp16 rounding midpoint the stored high and low halves then disagree by
-    // one fp16 ulp
-    asm volatile("" : "+v"(kv));
-    P.mu = fmaf(P.al[e], kv, P.mu);
+    // one fp16 ulp. (The asm has no side effects: a volatile one would also
+    // pin the loads and LDS accesses around it.)
+    asm("" : "+v"(kv));
+    P.mu = fmaf(al[e], kv, P.mu);
     const _Float16 h = static_cast<_Float16>(kv);
     hi[e] = h;
     lo[e] = static_cast<_Float16>(kv - static_cast<float>(h));
@@ -293,6 +302,15 @@ __device__ __forceinline__ void produce(Producer<NT, DX4, COMP>& P, const Poster
   _Float16* dst = ring + P.col * kCSH + (jb % kRing) * kJ + P.rq;
   *reinterpret_cast<halfx4*>(dst) = hi;
   *reinterpret_cast<halfx4*>(dst + NT * kCSH) = lo;
+}
+
+// Both parts at once (operands loaded by prod_load).
+template <int NT, int DX4, bool COMP>
+__device__ __forceinline__ void produce(Producer<NT, DX4, COMP>& P, const PosteriorArgs& a, int jb,
+                                        const float* ctile, _Float16* ring) {
+  float r2[Producer<NT, DX4, COMP>::NS][4];
+  produce_dist(P, a, jb, ctile, r2);
+  produce_kv(P, a, jb, r2, P.al, P.wt, ring);
 }
 
 // Row block of slot r in the pass starting at row block `base`.
@@ -393,7 +411,20 @@ __device__ __forceinline__ void step(const Ctx& C, const PosteriorArgs& a, Produ
   static_assert(NCB == 4, "two halves of two column blocks");
   BHalf B1;
   load_b<NT>(C, J, 1, B1);
-  if constexpr (PROD) produce(P, a, J + C.poff, C.ctile, ring);
+  // the distances consume the producer's operands, except alpha and the
+  // weights (copied), so the next block's are requested right after them, a
+  // whole step before they are needed (requested at the end of the step,
+  // they made the next step start by waiting for them)
+  using Pr = Producer<NT, DX4, COMP>;
+  float r2[Pr::NS][4];
+  floatx4 al, wt;
+  if constexpr (PROD) {
+    produce_dist(P, a, J + C.poff, C.ctile, r2);
+    al = P.al;
+    wt = P.wt;
+  }
+  prod_load(P, C.n_pad, J + 1 + C.poff, C.tid & 63);
+  if constexpr (PROD) produce_kv(P, a, J + C.poff, r2, al, wt, ring);
   // slot pairs in turn, each pair's fragments for J + 1 requested as soon as
   // its MFMAs are issued (about half a step before the next step needs them);
   // the next block's first B half is read once the last pair is done with it
@@ -411,7 +442,6 @@ __device__ __forceinline__ void step(const Ctx& C, const PosteriorArgs& a, Produ
     // interleave: the scheduler otherwise runs the producer's VALU work and
     // the MFMAs as two separate stretches, and the two waves of a SIMD
     // (kept in step by the barriers) then contend for the same unit
-    using Pr = Producer<NT, DX4, COMP>;
     constexpr int nM = 3 * NCB * (RB - LO) + Pr::NS * Pr::NF;
     constexpr int nV = 4 * (COMP ? 40 : 22);
     if constexpr (nM > 0) {
@@ -423,8 +453,6 @@ __device__ __forceinline__ void step(const Ctx& C, const PosteriorArgs& a, Produ
     }
   }
   __builtin_amdgcn_sched_barrier(0);
-  // operands of the next step's block
-  prod_load(P, C.n_pad, J + 1 + C.poff, C.tid & 63);
   lds_barrier();
 }
 
