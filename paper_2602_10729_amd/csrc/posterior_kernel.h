@@ -26,7 +26,8 @@
 // implementation's would. The scales are undone exactly: the row block's when
 // a block of V is squared, the column's in the epilogue. On gfx950 this is
 // the fast path: the dense fp16 MFMA runs at 16x the fp32 MFMA rate, and
-// (unlike fp32 MFMA) it executes alongside VALU work, which hides the kernel
+// (unlike fp32 MFMA) it overlaps VALU work in part (each 16x16x32 MFMA takes
+// about 8 cycles of its SIMD's VALU issue), which partly hides the kernel
 // evaluations below. L^{-1} is split and packed once by the fit; K*^T is
 // split as it is made.
 //
@@ -50,7 +51,8 @@
 // A pass that starts while the ring still holds blocks 0.. reuses them, so
 // for n <= 1024 every kernel value is evaluated once.
 // The kernel evaluations and the MFMAs of a step are independent and are
-// interleaved, so each SIMD's matrix core and vector ALU stay busy together.
+// interleaved, so each SIMD's matrix core and vector ALU work together as far
+// as their shared issue allows.
 // One barrier per step publishes the produced block.
 //
 // Each wave owns RB row-block slots, slot r holding row block
