@@ -703,7 +703,7 @@ __global__ __launch_bounds__(kMW * 64) void k_nehvi_means(NehviMeansArgs a) {
       }
       // one fp32 value for both halves (the compiler may otherwise fuse the
       // last product into the fp16 conversions and derive the high half twice)
-      asm("" : "+v"(kv));
+      asm volatile("" : "+v"(kv));
       const _Float16 h = static_cast<_Float16>(kv);
       hi[e] = h;
       lo[e] = static_cast<_Float16>(kv - static_cast<float>(h));
