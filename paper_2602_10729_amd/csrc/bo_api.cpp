@@ -868,9 +868,11 @@ bo_status fit_impl(const char* who, const float* X, const float* Y, int64_t n, i
   // fragments and (composite) the preference weights depend only on X and
   // the hyperparameters: they run on the side stream beside the first
   // diagonal block's factor and panel (the first trailing update waits for
-  // the Gram columns), then alpha beside the fp16 pack, and the side stream
-  // joins before the read-back. (An event's later record does not change a
-  // wait already enqueued on it.)
+  // the Gram columns), and the side stream joins once the factorisation is
+  // done; the fp16 pack and alpha then follow on this stream (alpha on the
+  // side stream, beside the pack, took longer: its wait for the factor cost
+  // more than the pack). (An event's later record does not change a wait
+  // already enqueued on it.)
   if ((s = side_stream(DS)) != BO_OK) return bail(s);
   hipStream_t side = DS->side;
   e = hipEventRecord(DS->side_evt[0], st);
@@ -889,17 +891,14 @@ bo_status fit_impl(const char* who, const float* X, const float* Y, int64_t n, i
                                        M->Xs, side), side, "scale X")) != BO_OK) return bail(s);
   if ((s = after_launch(launch_pack_x(M->Xs, n, m, M->nb, M->dx, dr4, M->ctr, M->xf, M->x2, side), side, "pack X")) != BO_OK) return bail(s);
   if (comp && (s = after_launch(launch_weights(X, n, d, m, M->n_pad, gp, M->wts, side), side, "weights")) != BO_OK) return bail(s);
-  // alpha (and the fp64 fragments) on the side stream, the fp16 pack here
-  e = hipEventRecord(DS->side_evt[0], st);
-  if (e == hipSuccess) e = hipStreamWaitEvent(side, DS->side_evt[0], 0);
-  if (e != hipSuccess) return bail(hip_fail(e, "bo_fit: side stream"));
-  if ((s = after_launch(launch_alpha(fs.W, Y, n, m, nf, M->n_pad, fs.tmp, M->alpha, side, M->alpha64), side, "alpha")) != BO_OK) return bail(s);
-  if (f64 && (s = after_launch(launch_pack_f64(fs.W, n, m, nf, M->nb, M->Lp64, side), side, "pack fp64")) != BO_OK) return bail(s);
+  // alpha (and the fp64 fragments) and the fp16 pack on this stream; the side
+  // stream's work joins first
   e = hipEventRecord(DS->side_evt[1], side);
+  if (e == hipSuccess) e = hipStreamWaitEvent(st, DS->side_evt[1], 0);
   if (e != hipSuccess) return bail(hip_fail(e, "bo_fit: side stream"));
   if ((s = after_launch(launch_pack_factor(fs.W, n, m, nf, M->nb, M->Lp, fs.stats + m, fs.flag, st, fs.bmax), st, "pack")) != BO_OK) return bail(s);
-  e = hipStreamWaitEvent(st, DS->side_evt[1], 0);
-  if (e != hipSuccess) return bail(hip_fail(e, "bo_fit: side stream"));
+  if ((s = after_launch(launch_alpha(fs.W, Y, n, m, nf, M->n_pad, fs.tmp, M->alpha, st, M->alpha64), st, "alpha")) != BO_OK) return bail(s);
+  if (f64 && (s = after_launch(launch_pack_f64(fs.W, n, m, nf, M->nb, M->Lp64, st), st, "pack fp64")) != BO_OK) return bail(s);
 
   // the flag and statistics follow the work; Y (copied back first) is
   // checked and its front formed meanwhile, then one synchronisation
