@@ -380,6 +380,7 @@ struct Ctx {
   __amdgpu_buffer_rsrc_t lp_rs;   // packed fragments of this objective
   int nb, nbj, zero_blk, n_pad, wave, tid;
   int poff;                 // the block produced at step J is J + poff (this pass)
+  int pw0, pw1;             // the pass's production window: blocks [pw0, pw1)
   int voff;                 // this lane's byte offset inside a fragment plane
   const _Float16* Kb;       // this lane's B-fragment base inside the ring
   const float* ctile;       // the tile's exact scaled candidate coordinates [NT][D]
@@ -425,7 +426,13 @@ __device__ __forceinline__ void step(const Ctx& C, const PosteriorArgs& a, Produ
     al = P.al;
     wt = P.wt;
   }
-  prod_load(P, C.n_pad, J + 1 + C.poff, C.tid & 63);
+  if constexpr (PROD) {
+    prod_load(P, C.n_pad, J + 1 + C.poff, C.tid & 63);
+  } else {
+    // only the step before the first producing one needs them
+    const int jn = J + 1 + C.poff;
+    if (jn >= C.pw0 && jn < C.pw1) prod_load(P, C.n_pad, jn, C.tid & 63);
+  }
   if constexpr (PROD) produce_kv(P, a, J + C.poff, r2, al, wt, ring);
   // slot pairs in turn, each pair's fragments for J + 1 requested as soon as
   // its MFMAs are issued (about half a step before the next step needs them);
@@ -723,6 +730,8 @@ __global__ __launch_bounds__(kThreads) void k_posterior(PosteriorArgs a) {
     C.poff = have0 ? have0 - 1 : 2;
     prod_load(P, n_pad, C.poff, lane);   // block poff: made at step 0 when new
     const int pw0 = have, pw1 = jpass;   // blocks this pass produces
+    C.pw0 = pw0;
+    C.pw1 = pw1;
     BHalf B0;
     load_b<NT>(C, 0, 0, B0);
     // blocks left of this pass's triangle: every slot is live
