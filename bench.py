@@ -209,7 +209,7 @@ def main(argv=None):
     a = ap.parse_args(argv)
 
     if a.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
+        print(json.dumps({"error": "the scoring path runs on one GPU; --gpus must be 1 (sharding by candidates across GPUs is not built)"}))
         return 2
 
     import bo_inputs as bi
