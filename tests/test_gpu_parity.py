@@ -51,18 +51,20 @@ def test_config1_full_size_elementwise():
     _full_parity(wl, g, o)
 
 
-def test_config2_full_size_dense():
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_config2_full_size_dense(seed):
     """Every one of config 2's 262,144 candidates element by element: the
     oracle runs over the host's cores (spawned workers, one BLAS thread each)."""
     import oracle_pool
-    _announce("config2 full dense", 0)
-    wl = bi.make_config(2, seed=0)
+    _announce("config2 full dense", seed)
+    wl = bi.make_config(2, seed=seed)
     g = gpu_run(wl)
     o = oracle_pool.score(oracle_fit(wl), wl.cand, wl.ref, wl.Z)
     _full_parity(wl, g, o)
 
 
-def test_config3_full_size_dense():
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_config3_full_size_dense(seed):
     """The headline workload, all 1,048,576 candidates element by element
     (mu, sigma, EHVI) and the argmax rule, the oracle over the host's cores
     as for config 2. The benchmark's call (no mu/sigma outputs: the same
@@ -70,8 +72,8 @@ def test_config3_full_size_dense():
     import torch
     import oracle_pool
     import paper_2602_10729_amd as bo
-    _announce("config3 full dense", 0)
-    wl = bi.make_config(3, seed=0)
+    _announce("config3 full dense", seed)
+    wl = bi.make_config(3, seed=seed)
     g = gpu_run(wl)
     e = bo.score(g["model"], to_dev(wl.cand), wl.ref, to_dev(wl.Z))
     torch.cuda.synchronize()
