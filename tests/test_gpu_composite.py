@@ -5,7 +5,7 @@ import pytest
 
 import bo_inputs as bi
 from gpu_util import (TOL_MU, TOL_SIGMA, TOL_EHVI, gpu_run, oracle_fit, oracle_score,
-                      assert_close, check_argmax, to_dev, near_var_tol)
+                      assert_close, check_argmax, to_dev, near_var_tol, log_ratio)
 
 pytestmark = pytest.mark.gpu
 
@@ -71,6 +71,41 @@ def test_composite_config3_full_size_sampled():
     op = oracle_score(model, wl, cand=wl.cand[pool])
     assert_close(e[pool], op["ehvi"], TOL_EHVI, "ehvi (top pool)")
     check_argmax(g["idx"], op["ehvi"], idx_pool=pool)
+
+
+def test_composite_config3_full_size_dense():
+    """The composite model on all 1,048,576 headline candidates, element by
+    element, the oracle over the host's cores. Its preference weights make
+    the mean cancel hard at some points (mu = sum_i k_i alpha_i with
+    sum_i |k_i alpha_i| up to thousands of times |mu|), where fp32 kernel
+    values bound the error absolutely: a mean outside the plain bar must lie
+    within the fp32 error model |mu_g - mu_o| <= 1e-4 |mu_o| + 1e-5 +
+    2^-18 sum_i |k_i alpha_i| (the learned-hyperparameter bound); how many
+    need it, and the worst plain-bar ratio, are logged."""
+    import oracle_pool
+    _announce("composite config3 full dense")
+    wl = bi.make_config(3, seed=0)
+    comp = bi.composite_hyperparameters(wl)
+    g = gpu_run(wl, comp=comp)
+    model = oracle_fit(wl, comp)
+    o = oracle_pool.score(model, wl.cand, wl.ref, wl.Z)
+    err = np.abs(g["mu"].astype(np.float64) - o["mu"])
+    plain = TOL_MU[0] * np.abs(o["mu"]) + TOL_MU[1]
+    log_ratio("composite mu, plain bar (informational)", float(np.max(err / plain)))
+    out = np.argwhere(err > plain)      # (candidate, member, objective)
+    print(f"[composite] {len(out)} of {err.size} means outside the plain bar", flush=True)
+    assert len(out) <= 0.001 * err.size, len(out)
+    for k in range(wl.m):
+        rows = out[out[:, 2] == k, 0]
+        if rows.size:
+            P = wl.cand[rows, 0, :].astype(np.float64)
+            sabs = np.abs(model.cov(k, P, model.X)) @ np.abs(model.alpha[k])
+            bound = plain[rows, 0, k] + 2.0 ** -18 * sabs
+            assert_close(g["mu"][rows, 0, k], o["mu"][rows, 0, k], (0.0, bound),
+                         f"composite mu k={k}, fp32 error model")
+    assert_close(g["sigma"], o["sigma"], TOL_SIGMA, "sigma")
+    assert_close(g["ehvi"], o["ehvi"], TOL_EHVI, "ehvi")
+    check_argmax(g["idx"], o["ehvi"])
 
 
 def test_composite_bad_arguments():
