@@ -136,6 +136,19 @@ def test_f64_composite_and_batches():
     _parity(wl, g, o, "q=2")
 
 
+def test_f64_composite_headline_dense():
+    """The composite model of the headline workload in fp64, all 1,048,576
+    candidates at the plain bars: the means that cancel too hard for the
+    fp32-class path (there held to the fp32 error model) meet them here."""
+    import oracle_pool
+    _announce("f64 composite config3 full dense")
+    wl = bi.make_config(3, seed=0)
+    comp = bi.composite_hyperparameters(wl)
+    g = gpu_run_f64(wl, comp=comp)
+    o = oracle_pool.score(oracle_fit(wl, comp), wl.cand, wl.ref, wl.Z)
+    _parity(wl, g, o, "composite dense")
+
+
 def test_f64_noalloc_and_noisy_refusal():
     import torch
     import paper_2602_10729_amd as bo
