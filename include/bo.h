@@ -123,10 +123,11 @@ typedef enum {
  * lives on the device, so its finiteness is checked once it is back (it is
  * read back first, so the host checks it and forms its front while the
  * device factors; the kernels run either way); the host arguments are
- * validated before anything is enqueued. Part of the work (the scaled X and
- * its distance fragments, alpha) runs on a second stream of the library's
- * own, at default priority, ordered after the caller's earlier work and
- * joined back into the caller's stream before return. Concurrent fits on one
+ * validated before anything is enqueued. Part of the work (the Gram matrix
+ * past its first 64 columns, the scaled X and its distance fragments) runs
+ * on a second stream of the library's own, at default priority, ordered
+ * after the caller's earlier work and joined back into the caller's stream
+ * once the factorisation is done (alpha and the packing follow there). Concurrent fits on one
  * device share a pinned staging buffer and run one at a time.
  * Memory: the model's device buffers are one allocation from a stream-ordered
  * pool (bo_free keeps the largest released one per device, once no work on it
